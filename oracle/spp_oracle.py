@@ -1,0 +1,550 @@
+"""Plain fp64 restatement of one offloaded-MoE decode step with SpecPrefetch.
+
+TEST INFRASTRUCTURE ONLY (see the package docstring): never imported by the
+product path.
+
+What is computed, and where the paper defines it:
+
+* native routing, T = Top_K(R(x)) -- Section "Problem Formulation"; the batch
+  demand is the union of the per-token sets (same section);
+* the adapter, z_hat = B A x, pi_hat = softmax(z_hat), s_e = sum over tokens of
+  pi_hat_e -- Section "Expert Prediction Adapter";
+* the candidate set C_M = Top_M(s) and the adapter parameter count
+  (L-1) r (D+n) -- same section;
+* the window-aware budget M_max and the prefetch set
+  P = Top_{M_max}{ s_e : e not available and not in flight }, issued in
+  descending priority, |P| <= M_max -- Section "Window-Aware Prefetch
+  Budgeting";
+* on-demand loading of every routed expert that is missing at execution, so
+  that outputs never depend on prediction -- same section, last paragraph;
+* ExpertRecall@M and ReadyRecall -- Section "Experimental Setup",
+  "Evaluation Metrics".
+
+Readings where the paper is silent (each listed with its reason in the design
+notes): the block prologue (RMS normalisation without a learned scale; an
+optional dense stand-in projection in place of attention), SwiGLU experts
+combined with gates renormalised over the selected K, the fp32 router-input
+and logit precision, the tie rule "lowest expert index wins", the budget
+formula M_max = clamp(floor(W / c), 0, n), and a deterministic
+least-recently-stamped slot replacement policy.
+"""
+from __future__ import annotations
+
+import math
+from dataclasses import dataclass, field
+from typing import Dict, List, Optional, Sequence, Tuple
+
+import numpy as np
+
+EMPTY = -1
+
+# --------------------------------------------------------------------------
+# storage <-> values (the oracle's own decoding; inputs arrive as bf16 bit
+# patterns or fp32 arrays)
+# --------------------------------------------------------------------------
+
+
+def decode(a: np.ndarray, dtype: str) -> np.ndarray:
+    """Stored values as fp64: bf16 bits are the high half of an fp32 pattern."""
+    if dtype == "bf16":
+        bits = np.asarray(a, dtype=np.uint16).astype(np.uint32) << np.uint32(16)
+        return bits.view(np.float32).astype(np.float64)
+    return np.asarray(a, dtype=np.float32).astype(np.float64)
+
+
+def encode(v: np.ndarray, dtype: str) -> np.ndarray:
+    """Round fp64 values once to the storage dtype (nearest, ties to even).
+
+    bf16 keeps 8 significant bits: v = m 2^e with 0.5 <= |m| < 1, so the
+    rounded value is rint(m 2^8) 2^(e-8) (numpy's rint rounds ties to even).
+    Values stay in the normal range here (|v| >= 2^-126 or v == 0).
+    """
+    v = np.asarray(v, dtype=np.float64)
+    if dtype == "bf16":
+        m, e = np.frexp(v)
+        r = np.ldexp(np.rint(m * 256.0), e - 8)
+        return (r.astype(np.float32).view(np.uint32) >> np.uint32(16)).astype(np.uint16)
+    return v.astype(np.float32)
+
+
+def f32(v) -> np.ndarray:
+    """Round to fp32 and return the rounded values as fp64."""
+    return np.asarray(v, dtype=np.float64).astype(np.float32).astype(np.float64)
+
+
+# --------------------------------------------------------------------------
+# elementary functions
+# --------------------------------------------------------------------------
+
+
+def rms_normalize(v: np.ndarray, eps: float) -> np.ndarray:
+    """v / sqrt(mean(v^2) + eps) along the last axis (no learned scale)."""
+    v = np.asarray(v, dtype=np.float64)
+    return v / np.sqrt(np.mean(v * v, axis=-1, keepdims=True) + eps)
+
+
+def softmax(v: np.ndarray) -> np.ndarray:
+    """softmax along the last axis in fp64."""
+    v = np.asarray(v, dtype=np.float64)
+    e = np.exp(v - np.max(v, axis=-1, keepdims=True))
+    return e / np.sum(e, axis=-1, keepdims=True)
+
+
+def silu(v: np.ndarray) -> np.ndarray:
+    return v / (1.0 + np.exp(-v))
+
+
+def top_k(values: np.ndarray, k: int) -> np.ndarray:
+    """Indices of the k largest values in descending order; the lower index wins a tie."""
+    values = np.asarray(values)
+    order = np.lexsort((np.arange(values.shape[0]), -values))
+    return order[:k].astype(np.int64)
+
+
+# --------------------------------------------------------------------------
+# Section "Problem Formulation": native routing
+# --------------------------------------------------------------------------
+
+
+def router_logits(Wr: np.ndarray, x: np.ndarray) -> np.ndarray:
+    """Router logits z = W_r x as fp64 dot products rounded once to fp32 ([B, n])."""
+    return f32(np.asarray(x, dtype=np.float64) @ np.asarray(Wr, dtype=np.float64).T)
+
+
+def route(Wr: np.ndarray, x: np.ndarray, K: int):
+    """Native Top-K routing of every token plus its combine weights.
+
+    Returns (T [B,K] int64, g [B,K] fp32 values as fp64, z [B,n] fp32 logits).
+    The combine weights are the softmax over all n logits renormalised over
+    the K selected experts.
+    """
+    z = router_logits(Wr, x)
+    B = z.shape[0]
+    T = np.stack([top_k(z[b], K) for b in range(B)])
+    p = softmax(z)
+    g = np.empty((B, K))
+    for b in range(B):
+        sel = p[b, T[b]]
+        g[b] = sel / np.sum(sel)
+    return T, f32(g), z
+
+
+def batch_demand(T: np.ndarray) -> List[int]:
+    """Union of the per-token native selections, ascending expert index."""
+    return sorted(set(int(e) for e in np.asarray(T).ravel()))
+
+
+# --------------------------------------------------------------------------
+# Section "Expert Prediction Adapter"
+# --------------------------------------------------------------------------
+
+
+def adapter_scores(A: np.ndarray, Bm: np.ndarray, x: np.ndarray):
+    """Predicted next-layer logits, token distributions and batch priorities.
+
+    z_hat = B (A x) (fp64 products, z_hat rounded to fp32); pi_hat = softmax(z_hat);
+    s_e = sum over tokens, in token order, of pi_hat_e, rounded to fp32.
+    Returns (z_hat [B,n], pi_hat [B,n], s [n]).
+    """
+    x = np.asarray(x, dtype=np.float64)
+    a = x @ np.asarray(A, dtype=np.float64).T                     # [B, r]
+    zhat = f32(a @ np.asarray(Bm, dtype=np.float64).T)            # [B, n]
+    pi = softmax(zhat)
+    s = np.zeros(zhat.shape[1])
+    for b in range(pi.shape[0]):
+        s = s + pi[b]
+    return zhat, pi, f32(s)
+
+
+def candidate_set(s: np.ndarray, M: int) -> np.ndarray:
+    """C_M = Top_M(s) (model-level candidate set)."""
+    return top_k(s, M)
+
+
+def adapter_param_count(L: int, r: int, D: int, n: int) -> int:
+    """Trainable adapter parameters over all adjacent layer pairs: (L-1) r (D+n)."""
+    return (L - 1) * r * (D + n)
+
+
+# --------------------------------------------------------------------------
+# Section "Window-Aware Prefetch Budgeting"
+# --------------------------------------------------------------------------
+
+
+class BudgetError(ValueError):
+    pass
+
+
+def prefetch_budget(window_us: float, per_expert_cost_us: float, n: int) -> int:
+    """Maximum prefetch budget: the number of whole expert transfers that fit in
+    the profiled overlap window, clamp(floor(W / c), 0, n).
+
+    A non-positive window gives 0; a non-positive or non-finite cost, or a
+    non-finite window, is an error.
+    """
+    if not (math.isfinite(window_us) and math.isfinite(per_expert_cost_us)) or per_expert_cost_us <= 0:
+        raise BudgetError("window and per-expert cost must be finite, cost > 0")
+    if n < 0:
+        raise BudgetError("n must be >= 0")
+    if window_us <= 0:
+        return 0
+    return int(min(n, math.floor(window_us / per_expert_cost_us)))
+
+
+def select_prefetch(s: np.ndarray, occupied: Sequence[bool], M_max: int) -> List[int]:
+    """P = Top_{M_max}{ s_e : e not available and not in flight }, descending priority."""
+    eligible = [e for e in range(len(s)) if not occupied[e]]
+    if M_max <= 0 or not eligible:
+        return []
+    vals = np.asarray([s[e] for e in eligible])
+    picked = top_k(vals, min(M_max, len(eligible)))
+    return [eligible[int(i)] for i in picked]
+
+
+# --------------------------------------------------------------------------
+# Available set of one layer: a logical slot table with deterministic
+# least-recently-stamped replacement (the paper leaves replacement open)
+# --------------------------------------------------------------------------
+
+
+class SlotCache:
+    """S accelerator slots of one layer; each holds one expert (or is EMPTY).
+
+    Every slot carries the stamp of the last decode step that used or filled
+    it.  Replacement rules:
+
+    * on-demand load of a missing expert: the lowest-index EMPTY slot, else the
+      slot with the smallest (stamp, slot index) whose expert is not needed by
+      the current batch;
+    * prefetch: the lowest-index EMPTY slot, else the smallest (stamp, slot
+      index) among slots stamped before the current step; prefetching stops
+      when no such slot is left;
+    * after the on-demand loads of a step, every slot holding a needed expert
+      takes the step's stamp; a prefetched slot takes the step's stamp.
+    """
+
+    def __init__(self, S: int, n: int, resident: Optional[Sequence[int]] = None):
+        if S <= 0:
+            raise ValueError("S must be positive")
+        self.S, self.n = S, n
+        self.expert = np.full(S, EMPTY, dtype=np.int64)
+        self.stamp = np.zeros(S, dtype=np.int64)
+        if resident is not None:
+            if len(resident) > S or len(set(resident)) != len(resident):
+                raise ValueError("bad resident list")
+            for j, e in enumerate(resident):
+                self.expert[j] = int(e)
+
+    def occupied(self) -> np.ndarray:
+        occ = np.zeros(self.n, dtype=bool)
+        for e in self.expert:
+            if e != EMPTY:
+                occ[e] = True
+        return occ
+
+    def slot_of(self, e: int) -> int:
+        hit = np.nonzero(self.expert == e)[0]
+        return int(hit[0]) if hit.size else EMPTY
+
+    def _victim(self, allowed) -> int:
+        empties = [j for j in range(self.S) if self.expert[j] == EMPTY]
+        if empties:
+            return empties[0]
+        cands = [(int(self.stamp[j]), j) for j in range(self.S) if allowed(j)]
+        return min(cands)[1] if cands else EMPTY
+
+    def on_demand(self, needed: Sequence[int], tau: int):
+        """Load every needed expert that is not present; returns [(expert, slot, evicted)]."""
+        need = set(int(e) for e in needed)
+        if len(need) > self.S:
+            raise ValueError("batch demand exceeds the slot count")
+        occ = self.occupied()
+        loads = []
+        for e in sorted(need):
+            if occ[e]:
+                continue
+            v = self._victim(lambda j: int(self.expert[j]) not in need)
+            assert v != EMPTY
+            loads.append((e, v, int(self.expert[v])))
+            self.expert[v] = e
+        for j in range(self.S):
+            if int(self.expert[j]) in need:
+                self.stamp[j] = tau
+        return loads
+
+    def prefetch(self, ordered: Sequence[int], tau: int):
+        """Place experts in the given order; returns [(expert, slot, evicted)]."""
+        placed = []
+        for e in ordered:
+            v = self._victim(lambda j: self.stamp[j] < tau)
+            if v == EMPTY:
+                break
+            placed.append((int(e), v, int(self.expert[v])))
+            self.expert[v] = int(e)
+            self.stamp[v] = tau
+        return placed
+
+
+# --------------------------------------------------------------------------
+# routed SwiGLU experts (the FFN the native router executes)
+# --------------------------------------------------------------------------
+
+
+def expert_ffn(Wg: np.ndarray, Wu: np.ndarray, Wd: np.ndarray, x: np.ndarray) -> np.ndarray:
+    """Wd (silu(Wg x) * (Wu x)) in fp64 for one token."""
+    x = np.asarray(x, dtype=np.float64)
+    return np.asarray(Wd, dtype=np.float64) @ (silu(np.asarray(Wg, dtype=np.float64) @ x)
+                                               * (np.asarray(Wu, dtype=np.float64) @ x))
+
+
+# --------------------------------------------------------------------------
+# weights as the oracle sees them
+# --------------------------------------------------------------------------
+
+
+class OracleWeights:
+    """Decoded (fp64-valued) weights of a workload, regenerated from its seeds.
+
+    Expert matrices are kept as decoded fp32 (exact for bf16 and fp32 storage)
+    in a bounded cache.  ``adapter_override(l) -> (A, B)`` replaces the seeded
+    adapters (values, not storage) for special-case tests.
+    """
+
+    def __init__(self, cfg, cache_experts: int = 48, adapter_override=None):
+        import workload.gen as gen  # seeded inputs only
+        self.cfg, self.gen = cfg, gen
+        self._cache: Dict[Tuple[int, int], tuple] = {}
+        self._order: List[Tuple[int, int]] = []
+        self._cap = cache_experts
+        self._router: Dict[int, np.ndarray] = {}
+        self._adapter: Dict[int, tuple] = {}
+        self._proj: Dict[int, np.ndarray] = {}
+        self._shared: Dict[Tuple[int, int], tuple] = {}
+        self.adapter_override = adapter_override
+
+    def _dec(self, a):
+        return decode(a, self.cfg.dtype).astype(np.float32)
+
+    def router(self, l: int) -> np.ndarray:
+        if l not in self._router:
+            self._router[l] = decode(self.gen.router_weight(self.cfg, l), self.cfg.dtype)
+        return self._router[l]
+
+    def adapter(self, l: int):
+        if self.adapter_override is not None:
+            return self.adapter_override(l)
+        if l not in self._adapter:
+            A, B = self.gen.adapter_weights(self.cfg, l)
+            self._adapter[l] = (decode(A, self.cfg.dtype), decode(B, self.cfg.dtype))
+        return self._adapter[l]
+
+    def proj(self, l: int) -> np.ndarray:
+        if l not in self._proj:
+            self._proj[l] = decode(self.gen.proj_weight(self.cfg, l), self.cfg.dtype)
+        return self._proj[l]
+
+    def expert(self, l: int, e: int):
+        key = (l, e)
+        if key in self._cache:
+            return self._cache[key]
+        w = tuple(self._dec(a) for a in self.gen.expert_weights(self.cfg, l, e))
+        self._cache[key] = w
+        self._order.append(key)
+        if len(self._order) > self._cap:
+            del self._cache[self._order.pop(0)]
+        return w
+
+    def shared(self, l: int, j: int):
+        key = (l, j)
+        if key not in self._shared:
+            self._shared[key] = tuple(self._dec(a) for a in self.gen.shared_expert_weights(self.cfg, l, j))
+        return self._shared[key]
+
+
+# --------------------------------------------------------------------------
+# one layer and the decode loop
+# --------------------------------------------------------------------------
+
+
+@dataclass
+class LayerStep:
+    t: int
+    l: int
+    tau: int
+    x: np.ndarray                 # router input [B, D] (fp64)
+    z: np.ndarray                 # router logits [B, n] (fp32 values)
+    T: np.ndarray                 # native selection [B, K]
+    g: np.ndarray                 # combine weights [B, K] (fp32 values)
+    ready: np.ndarray             # per token |T_b cap available| before on-demand loads
+    loads: list                   # on-demand loads [(expert, slot, evicted)]
+    table_after_demand: np.ndarray
+    s: Optional[np.ndarray] = None          # priorities for layer l+1 (fp32 values)
+    zhat: Optional[np.ndarray] = None
+    P: list = field(default_factory=list)   # prefetch placements for layer l+1 [(expert, slot, evicted)]
+    next_table_after_prefetch: Optional[np.ndarray] = None
+    next_stamps_after_prefetch: Optional[np.ndarray] = None
+    stamps_after_demand: Optional[np.ndarray] = None
+    h_out: Optional[np.ndarray] = None      # stored output [B, D] (storage dtype)
+    recall: Optional[Dict[int, np.ndarray]] = None   # M -> per token |T_b cap C_M| (prediction made at l-1)
+    demand: Optional[Dict[int, int]] = None          # M -> |Top_M(s) minus available(l+1)| at prediction time
+
+
+def layer_prologue(cfg, W: OracleWeights, l: int, h: np.ndarray):
+    """u = h + P_l rms(h) with the stand-in projection, else u = h; x = rms(u)."""
+    h = np.asarray(h, dtype=np.float64)
+    if cfg.has_proj:
+        u = h + rms_normalize(h, cfg.rms_eps) @ W.proj(l).T
+    else:
+        u = h
+    return u, rms_normalize(u, cfg.rms_eps)
+
+
+def moe_output(cfg, W: OracleWeights, l: int, cache: SlotCache, u, x, T, g):
+    """h' = u + sum_k g_k FFN_{T_k}(x) (+ shared experts with weight 1), weights
+    looked up through the slot table; every executed expert must be present."""
+    B = x.shape[0]
+    y = np.zeros((B, cfg.D))
+    for b in range(B):
+        for k in range(T.shape[1]):
+            slot = cache.slot_of(int(T[b, k]))
+            if slot == EMPTY:
+                raise AssertionError("executed expert is not available")
+            Wg, Wu, Wd = W.expert(l, int(cache.expert[slot]))
+            y[b] += g[b, k] * expert_ffn(Wg, Wu, Wd, x[b])
+        for j in range(cfg.n_shared):
+            y[b] += expert_ffn(*W.shared(l, j), x[b])
+    return u + y
+
+
+@dataclass
+class DecodeResult:
+    steps: List[LayerStep]
+    ready_recall: float            # mean over target layers 1..L-1 (next-layer coverage)
+    layer0_hit_rate: float
+    expert_recall: Dict[int, float]
+    loads: int
+    prefetched: int
+    prefetch_used: int
+    demand_exceeds: Dict[int, float]
+    outputs: List[np.ndarray]      # stored h after the last layer, per token
+
+
+def run_decode(cfg, W: OracleWeights, h0: np.ndarray, M_max: int, S: Optional[int] = None,
+               resident: Optional[Sequence[int]] = None, tokens: Optional[int] = None,
+               keep_x: bool = False) -> DecodeResult:
+    """Decode ``tokens`` steps through all L layers.
+
+    M_max < 0: no prediction at all (OFF); M_max == 0: prediction without
+    transfers (PRED0); M_max > 0: prediction and budgeted prefetch.
+    ``h0`` holds the stored layer-0 hidden states [tokens, B, D].
+    Decode step t, layer l has stamp tau = t L + l + 1.
+    """
+    L, n, K = cfg.L, cfg.n, cfg.K
+    S = cfg.S if S is None else S
+    resident = list(range(min(S, n))) if resident is None else list(resident)
+    caches = [SlotCache(S, n, resident) for _ in range(L)]
+    Ms = sorted(set(m for m in (max(1, K // 2), K, K + 2) if m <= n))
+    predicted: List[Optional[Dict[int, np.ndarray]]] = [None] * L
+    pending: List[set] = [set() for _ in range(L)]
+    steps: List[LayerStep] = []
+    outputs = []
+    tau = 0
+    nT = h0.shape[0] if tokens is None else tokens
+    ready_sum, ready_cnt, hit0_sum, hit0_cnt = 0.0, 0, 0.0, 0
+    recall_sum = {m: 0.0 for m in Ms}
+    recall_cnt = 0
+    n_loads = n_pref = n_used = 0
+    demand_events = {m: 0 for m in Ms}
+    n_events = 0
+    for t in range(nT):
+        h = decode(h0[t], cfg.dtype)
+        for l in range(L):
+            tau += 1
+            u, x = layer_prologue(cfg, W, l, h)
+            T, g, z = route(W.router(l), x, K)
+            need = batch_demand(T)
+            cache = caches[l]
+            occ = cache.occupied()
+            ready = np.array([sum(int(occ[e]) for e in T[b]) for b in range(T.shape[0])])
+            if l >= 1:
+                ready_sum += float(np.sum(ready)) / K
+                ready_cnt += T.shape[0]
+            else:
+                hit0_sum += float(np.sum(ready)) / K
+                hit0_cnt += T.shape[0]
+            recall = None
+            if predicted[l] is not None:
+                recall = {m: np.array([len(set(T[b].tolist()) & set(predicted[l][m].tolist()))
+                                       for b in range(T.shape[0])]) for m in Ms}
+                for m in Ms:
+                    recall_sum[m] += float(np.sum(recall[m])) / K
+                recall_cnt += T.shape[0]
+            n_used += len(pending[l] & set(need))
+            pending[l] = set()
+            loads = cache.on_demand(need, tau)
+            n_loads += len(loads)
+            step = LayerStep(t=t, l=l, tau=tau, x=x if keep_x else None, z=z, T=T, g=g, ready=ready,
+                             loads=loads, table_after_demand=cache.expert.copy(),
+                             stamps_after_demand=cache.stamp.copy(), recall=recall)
+            predicted[l] = None
+            if l < L - 1 and M_max >= 0:
+                A, Bm = W.adapter(l)
+                zhat, _, s = adapter_scores(A, Bm, x)
+                step.s, step.zhat = s, zhat
+                predicted[l + 1] = {m: candidate_set(s, m) for m in Ms}
+                nxt = caches[l + 1]
+                occ_next = nxt.occupied()
+                step.demand = {m: int(sum(1 for e in predicted[l + 1][m] if not occ_next[e])) for m in Ms}
+                for m in Ms:
+                    demand_events[m] += int(step.demand[m] > max(M_max, 0))
+                n_events += 1
+                if M_max > 0:
+                    P = select_prefetch(s, occ_next, M_max)
+                    step.P = nxt.prefetch(P, tau)
+                    n_pref += len(step.P)
+                    pending[l + 1] = set(e for e, _, _ in step.P)
+                step.next_table_after_prefetch = nxt.expert.copy()
+                step.next_stamps_after_prefetch = nxt.stamp.copy()
+            hout = moe_output(cfg, W, l, cache, u, x, T, g)
+            step.h_out = encode(hout, cfg.dtype)
+            h = decode(step.h_out, cfg.dtype)
+            steps.append(step)
+        outputs.append(step.h_out)
+    return DecodeResult(
+        steps=steps,
+        ready_recall=ready_sum / ready_cnt if ready_cnt else float("nan"),
+        layer0_hit_rate=hit0_sum / hit0_cnt if hit0_cnt else float("nan"),
+        expert_recall={m: (recall_sum[m] / recall_cnt if recall_cnt else float("nan")) for m in Ms},
+        loads=n_loads, prefetched=n_pref, prefetch_used=n_used,
+        demand_exceeds={m: (demand_events[m] / n_events if n_events else float("nan")) for m in Ms},
+        outputs=outputs)
+
+
+def layer_step(cfg, W: OracleWeights, l: int, h_stored: np.ndarray, cache: SlotCache,
+               next_cache: Optional[SlotCache], tau: int, M_max: int):
+    """One layer in isolation from given state (the lock-step parity unit).
+
+    Mutates ``cache`` / ``next_cache`` exactly as the decode loop does and
+    returns the LayerStep record (x kept).
+    """
+    K = cfg.K
+    u, x = layer_prologue(cfg, W, l, decode(h_stored, cfg.dtype))
+    T, g, z = route(W.router(l), x, K)
+    need = batch_demand(T)
+    occ = cache.occupied()
+    ready = np.array([sum(int(occ[e]) for e in T[b]) for b in range(T.shape[0])])
+    loads = cache.on_demand(need, tau)
+    step = LayerStep(t=-1, l=l, tau=tau, x=x, z=z, T=T, g=g, ready=ready, loads=loads,
+                     table_after_demand=cache.expert.copy(), stamps_after_demand=cache.stamp.copy())
+    if l < cfg.L - 1 and M_max >= 0:
+        A, Bm = W.adapter(l)
+        zhat, _, s = adapter_scores(A, Bm, x)
+        step.s, step.zhat = s, zhat
+        if M_max > 0 and next_cache is not None:
+            P = select_prefetch(s, next_cache.occupied(), M_max)
+            step.P = next_cache.prefetch(P, tau)
+        if next_cache is not None:
+            step.next_table_after_prefetch = next_cache.expert.copy()
+            step.next_stamps_after_prefetch = next_cache.stamp.copy()
+    step.h_out = encode(moe_output(cfg, W, l, cache, u, x, T, g), cfg.dtype)
+    return step

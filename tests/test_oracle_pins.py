@@ -1,0 +1,378 @@
+"""Pins of the CPU oracle to things other than itself (no GPU needed).
+
+Each test checks an oracle function against brute force, a closed form, an
+independent library routine (torch / scipy), an invariant the paper states, or
+a hand-worked trace, so that a plausible slip in the oracle (a dropped term, a
+wrong sign or index, a transposed operand, a wrong tie rule) fails here.
+"""
+import itertools
+import math
+
+import numpy as np
+import pytest
+import scipy.special
+import torch
+import torch.nn.functional as F
+
+import oracle as o
+import workload as w
+from workload import gen
+
+
+# ---------------------------------------------------------------- top-k ----
+
+def _brute_top_k(v, k):
+    """Definition by pairwise comparison: a beats b iff v[a] > v[b] or (equal and a < b)."""
+    n = len(v)
+    beats = lambda a, b: v[a] > v[b] or (v[a] == v[b] and a < b)
+    best = None
+    for combo in itertools.permutations(range(n), k):
+        ok = all(beats(combo[i], combo[i + 1]) for i in range(k - 1))
+        rest = [e for e in range(n) if e not in combo]
+        ok = ok and all(beats(combo[-1], e) for e in rest) if k else ok
+        if ok:
+            assert best is None
+            best = list(combo)
+    return best
+
+
+@pytest.mark.parametrize("seed", range(40))
+def test_top_k_matches_brute_force_with_ties(seed):
+    rng = np.random.default_rng(seed)
+    n = int(rng.integers(1, 7))
+    v = rng.integers(-2, 3, size=n).astype(np.float32)     # many ties
+    for k in range(0, n + 1):
+        assert o.top_k(v, k).tolist() == _brute_top_k(v, k)
+
+
+def test_top_k_lowest_index_wins_tie():
+    assert o.top_k(np.array([1.0, 3.0, 3.0, 2.0, 3.0]), 2).tolist() == [1, 2]
+
+
+# --------------------------------------------------- elementary functions --
+
+def test_softmax_against_scipy_and_shift_invariance():
+    rng = np.random.default_rng(1)
+    v = rng.normal(size=(4, 17)) * 3
+    np.testing.assert_allclose(o.softmax(v), scipy.special.softmax(v, axis=-1), rtol=1e-13, atol=0)
+    np.testing.assert_allclose(o.softmax(v + 123.0), o.softmax(v), rtol=1e-12, atol=0)
+    np.testing.assert_allclose(o.softmax(v).sum(-1), 1.0, rtol=1e-14)
+
+
+def test_silu_against_torch():
+    v = np.linspace(-20, 20, 401)
+    np.testing.assert_allclose(o.silu(v), F.silu(torch.tensor(v, dtype=torch.float64)).numpy(), rtol=1e-14, atol=1e-300)
+
+
+def test_rms_normalize_closed_form():
+    rng = np.random.default_rng(2)
+    u = rng.normal(size=(3, 64)) * 5
+    eps = 1e-6
+    x = o.rms_normalize(u, eps)
+    m = np.mean(u * u, axis=-1)
+    np.testing.assert_allclose(np.mean(x * x, axis=-1), m / (m + eps), rtol=1e-13)
+    np.testing.assert_allclose(x / u, (1 / np.sqrt(m + eps))[:, None] * np.ones_like(u), rtol=1e-13)
+
+
+def test_bf16_encode_hand_ties_and_torch():
+    # hand-worked ties: 1 + 2^-8 lies halfway between 1 and 1 + 2^-7 -> even (1.0);
+    # 1 + 3*2^-8 lies halfway between 1 + 2^-7 and 1 + 2^-6 -> even (1 + 2^-6).
+    vals = np.array([1 + 2 ** -8, 1 + 3 * 2 ** -8, -(1 + 2 ** -8), 0.0, 2.0 ** -20])
+    expect = [0x3F80, 0x3F82, 0xBF80, 0x0000, 0x3580]
+    assert o.encode(vals, "bf16").tolist() == expect
+    rng = np.random.default_rng(3)
+    v = rng.normal(size=5000).astype(np.float32).astype(np.float64)   # fp32-exact: no double rounding
+    ours = o.encode(v, "bf16")
+    ref = torch.tensor(v, dtype=torch.float32).to(torch.bfloat16).view(torch.int16).numpy().astype(np.uint16)
+    assert np.array_equal(ours, ref)
+    np.testing.assert_array_equal(o.decode(ours, "bf16"),
+                                  torch.tensor(v, dtype=torch.float32).to(torch.bfloat16).double().numpy())
+
+
+# ------------------------------------------------------ routing + adapter --
+
+def _torch_layer(u, Wr, K, experts, shared, eps, proj=None):
+    """Textbook MoE block built from torch library routines (no oracle code)."""
+    u = torch.tensor(u, dtype=torch.float64)
+    if proj is not None:
+        u = u + F.linear(u * torch.rsqrt(u.pow(2).mean(-1, keepdim=True) + eps), torch.tensor(proj))
+    x = u * torch.rsqrt(u.pow(2).mean(-1, keepdim=True) + eps)
+    logits = F.linear(x, torch.tensor(Wr)).float().double()
+    top = torch.topk(logits, K, dim=-1, sorted=True)
+    p = torch.softmax(logits, dim=-1)
+    gsel = torch.gather(p, 1, top.indices)
+    gsel = (gsel / gsel.sum(-1, keepdim=True)).float().double()
+    y = torch.zeros_like(u)
+    for b in range(u.shape[0]):
+        for k in range(K):
+            Wg, Wu, Wd = (torch.tensor(m, dtype=torch.float64) for m in experts[int(top.indices[b, k])])
+            y[b] += gsel[b, k] * F.linear(F.silu(F.linear(x[b], Wg)) * F.linear(x[b], Wu), Wd)
+        for (Wg, Wu, Wd) in shared:
+            Wg, Wu, Wd = (torch.tensor(m, dtype=torch.float64) for m in (Wg, Wu, Wd))
+            y[b] += F.linear(F.silu(F.linear(x[b], Wg)) * F.linear(x[b], Wu), Wd)
+    return top.indices.numpy(), gsel.numpy(), (u + y).numpy(), x.numpy()
+
+
+@pytest.mark.parametrize("has_proj,n_shared", [(False, 0), (True, 0), (False, 2)])
+def test_layer_against_torch_textbook_block(has_proj, n_shared):
+    cfg = w.MoEConfig(name="t", L=2, D=96, n=12, K=3, I=40, r=8, S=12, windows=(1,), tokens=3,
+                      batch=3, dtype="f32", has_proj=has_proj, n_shared=n_shared, seed=7)
+    W = o.OracleWeights(cfg)
+    h = o.decode(gen.hidden_states(cfg)[0], "f32") * 1.7
+    cache = o.SlotCache(cfg.S, cfg.n, list(range(cfg.n)))
+    u, x = o.layer_prologue(cfg, W, 0, h)
+    T, g, z = o.route(W.router(0), x, cfg.K)
+    out = o.moe_output(cfg, W, 0, cache, u, x, T, g)
+    experts = [W.expert(0, e) for e in range(cfg.n)]
+    shared = [W.shared(0, j) for j in range(cfg.n_shared)]
+    tT, tg, tout, tx = _torch_layer(h, W.router(0), cfg.K, experts, shared, cfg.rms_eps,
+                                    W.proj(0) if has_proj else None)
+    np.testing.assert_allclose(x, tx, rtol=1e-13, atol=1e-15)
+    assert np.array_equal(T, tT)
+    np.testing.assert_allclose(g, tg, rtol=1e-7)
+    np.testing.assert_allclose(out, tout, rtol=1e-11, atol=1e-12)
+
+
+def test_expert_ffn_against_torch():
+    rng = np.random.default_rng(4)
+    Wg, Wu = rng.normal(size=(30, 20)), rng.normal(size=(30, 20))
+    Wd = rng.normal(size=(20, 30))
+    x = rng.normal(size=20)
+    ref = F.linear(F.silu(F.linear(torch.tensor(x), torch.tensor(Wg))) * F.linear(torch.tensor(x), torch.tensor(Wu)),
+                   torch.tensor(Wd)).numpy()
+    np.testing.assert_allclose(o.expert_ffn(Wg, Wu, Wd, x), ref, rtol=1e-12)
+    # a gate row orthogonal to x switches its unit off exactly: silu(0) = 0
+    Wg2 = Wg.copy()
+    Wg2[5] -= (Wg2[5] @ x) / (x @ x) * x
+    Wd2 = np.zeros_like(Wd)
+    Wd2[:, 5] = 1.0
+    assert abs(o.expert_ffn(Wg2, Wu, Wd2, x)).max() < 1e-12
+
+
+def test_route_gates_and_adapter_scores_invariants():
+    rng = np.random.default_rng(5)
+    B, D, n, r, K = 5, 32, 10, 4, 3
+    Wr, A, Bm = rng.normal(size=(n, D)), rng.normal(size=(r, D)), rng.normal(size=(n, r))
+    x = rng.normal(size=(B, D))
+    T, g, z = o.route(Wr, x, K)
+    np.testing.assert_allclose(g.sum(-1), 1.0, rtol=1e-6)
+    assert np.all(np.diff(g, axis=1) <= 0)             # descending logits -> descending gates
+    assert np.array_equal(z, z.astype(np.float32).astype(np.float64))
+    zhat, pi, s = o.adapter_scores(A, Bm, x)
+    np.testing.assert_allclose(pi.sum(-1), 1.0, rtol=1e-14)
+    np.testing.assert_allclose(s.sum(), B, rtol=1e-6)     # sum_e s_e = |Omega|
+    ref = torch.softmax(torch.tensor(zhat), -1).sum(0).float().double().numpy()
+    np.testing.assert_allclose(s, ref, rtol=1e-7)
+    # z_hat = B (A x): against a single fused product (B A) x
+    np.testing.assert_allclose(zhat, x @ (Bm @ A).T, rtol=1e-6, atol=1e-6)
+
+
+def test_adapter_param_count_matches_generated_arrays():
+    for name in ("c0", "c1", "c3"):
+        cfg = w.get(name)
+        count = 0
+        for l in range(cfg.L - 1) if cfg.L <= 2 else range(1):
+            A, B = gen.adapter_weights(cfg, l)
+            count += A.size + B.size
+        per_pair = cfg.r * (cfg.D + cfg.n)
+        assert count == per_pair * (min(cfg.L - 1, 1) if cfg.L > 2 else cfg.L - 1)
+        assert o.adapter_param_count(cfg.L, cfg.r, cfg.D, cfg.n) == (cfg.L - 1) * per_pair
+    # 48-layer Qwen-shaped stack at r = 64: 47 * 64 * 2176
+    assert o.adapter_param_count(48, 64, 2048, 128) == 6_545_408
+
+
+# --------------------------------------------------------------- budget ----
+
+def test_prefetch_budget_rule():
+    assert o.prefetch_budget(300.0, 150.0, 128) == 2
+    assert o.prefetch_budget(299.9, 150.0, 128) == 1
+    assert o.prefetch_budget(0.0, 150.0, 128) == 0
+    assert o.prefetch_budget(-5.0, 150.0, 128) == 0
+    assert o.prefetch_budget(1e9, 1.0, 128) == 128
+    for bad in [(1.0, 0.0), (1.0, -1.0), (float("nan"), 1.0), (1.0, float("inf")), (float("inf"), 1.0)]:
+        with pytest.raises(o.BudgetError):
+            o.prefetch_budget(bad[0], bad[1], 8)
+    rng = np.random.default_rng(6)
+    for _ in range(200):
+        W_, c = rng.uniform(0, 1000), rng.uniform(1, 300)
+        m = o.prefetch_budget(W_, c, 64)
+        assert m * c <= W_ + 1e-9 and ((m + 1) * c > W_ or m == 64)
+        assert o.prefetch_budget(W_ + 50, c, 64) >= m          # monotone in the window
+        assert o.prefetch_budget(W_, c + 10, 64) <= m          # antitone in the cost
+
+
+@pytest.mark.parametrize("seed", range(30))
+def test_select_prefetch_brute_force(seed):
+    rng = np.random.default_rng(seed)
+    n = int(rng.integers(1, 8))
+    s = rng.integers(0, 4, size=n).astype(np.float64) / 4      # ties
+    occ = rng.random(n) < 0.4
+    for M in range(0, n + 2):
+        P = o.select_prefetch(s, occ, M)
+        elig = [e for e in range(n) if not occ[e]]
+        assert len(P) == min(max(M, 0), len(elig))
+        assert not any(occ[e] for e in P)
+        beats = lambda a, b: s[a] > s[b] or (s[a] == s[b] and a < b)
+        assert all(beats(P[i], P[i + 1]) for i in range(len(P) - 1))
+        assert all(beats(P[-1], e) for e in elig if e not in P) if P else True
+
+
+# ---------------------------------------------------------- slot cache -----
+
+def test_slot_cache_hand_worked_trace():
+    """Expected tables derived by hand from the replacement rules in SlotCache's docstring."""
+    c = o.SlotCache(3, 6, [0, 1, 2])                      # table [0,1,2], stamps [0,0,0]
+    # tau=1, need {1,4}: miss 4; victims exclude needed {1,4}: slots 0 (st 0), 2 (st 0) -> slot 0
+    assert c.on_demand([4, 1], 1) == [(4, 0, 0)]
+    assert c.expert.tolist() == [4, 1, 2] and c.stamp.tolist() == [1, 1, 0]
+    # tau=2, need {2,3,5}: miss 3 -> min(stamp,slot) over {slot0 (1), slot1 (1)} = slot 0;
+    # miss 5 -> only slot 1 holds an unneeded expert
+    assert c.on_demand([5, 3, 2], 2) == [(3, 0, 4), (5, 1, 1)]
+    assert c.expert.tolist() == [3, 5, 2] and c.stamp.tolist() == [2, 2, 2]
+    # prefetch at tau=2: every slot is stamped 2 (not before the step) -> nothing placed
+    assert c.prefetch([0, 1], 2) == []
+    # prefetch at tau=3 in order [0,4,1]: slots 0, 1, 2 in turn (all stamped 2, lowest slot first)
+    assert c.prefetch([0, 4, 1], 3) == [(0, 0, 3), (4, 1, 5), (1, 2, 2)]
+    assert c.expert.tolist() == [0, 4, 1] and c.stamp.tolist() == [3, 3, 3]
+    # tau=4, need {4,5}: miss 5; unneeded slots 0 (st 3) and 2 (st 3) -> slot 0
+    assert c.on_demand([4, 5], 4) == [(5, 0, 0)]
+    assert c.expert.tolist() == [5, 4, 1] and c.stamp.tolist() == [4, 4, 3]
+
+    e = o.SlotCache(3, 8, [7])                            # [7, EMPTY, EMPTY]
+    assert e.on_demand([2, 7], 1) == [(2, 1, o.EMPTY)]    # lowest EMPTY slot first
+    assert e.expert.tolist() == [7, 2, -1] and e.stamp.tolist() == [1, 1, 0]
+    # prefetch at tau=1: 5 takes the EMPTY slot 2; 6 finds no slot stamped before 1 -> stop
+    assert e.prefetch([5, 6], 1) == [(5, 2, -1)]
+    assert e.expert.tolist() == [7, 2, 5]
+    with pytest.raises(ValueError):
+        e.on_demand([0, 1, 3, 4], 2)                      # demand larger than S
+
+
+# ------------------------------------------------------- decode loop ------
+
+def _small_cfg(**kw):
+    base = dict(name="s", L=3, D=64, n=10, K=3, I=24, r=6, S=5, windows=(1,), tokens=12,
+                dtype="f32", seed=11)
+    base.update(kw)
+    return w.MoEConfig(**base)
+
+
+def _adapter_variants(cfg, W):
+    rng = np.random.default_rng(9)
+    def zero(l):
+        return np.zeros((cfg.r, cfg.D)), np.zeros((cfg.n, cfg.r))
+    def rand(l):
+        return rng.normal(size=(cfg.r, cfg.D)), rng.normal(size=(cfg.n, cfg.r))
+    def reverse(l):
+        A, B = W.adapter(l)
+        return A, -B
+    return {"svd": None, "zero": zero, "random": rand, "reversed": reverse}
+
+
+def test_router_preservation_outputs_independent_of_policy():
+    """Outputs never depend on M_max, the slot count or the adapter (paper: the
+    native router stays authoritative; missing experts are loaded on demand)."""
+    cfg = _small_cfg(batch=2, S=7)
+    h0 = gen.hidden_states(cfg)
+    W0 = o.OracleWeights(cfg)
+    ref = np.stack(o.run_decode(cfg, W0, h0, M_max=-1).outputs)
+    for name, ov in _adapter_variants(cfg, W0).items():
+        W = o.OracleWeights(cfg, adapter_override=ov)
+        for S in (cfg.K * 2, 7, cfg.n):
+            for M in (0, 1, 2, 4, cfg.n):
+                res = o.run_decode(cfg, W, h0, M_max=M, S=S)
+                assert np.array_equal(np.stack(res.outputs), ref), (name, S, M)
+                for st in res.steps:
+                    table = st.table_after_demand
+                    held = table[table != o.EMPTY]
+                    assert len(set(held.tolist())) == len(held)            # no duplicates
+                    assert set(np.asarray(st.T).ravel().tolist()) <= set(held.tolist())
+                    for e, slot, ev in st.loads:
+                        assert ev not in set(np.asarray(st.T).ravel().tolist())   # victim not needed
+                    assert len(st.P) <= max(M, 0)
+                    if st.P:
+                        placed = [e for e, _, _ in st.P]
+                        assert len(set(placed)) == len(placed)
+                assert 0.0 <= res.ready_recall <= 1.0
+
+
+def test_all_resident_and_no_prefetch_special_cases():
+    cfg = _small_cfg()
+    h0 = gen.hidden_states(cfg)
+    W = o.OracleWeights(cfg)
+    full = o.run_decode(cfg, W, h0, M_max=2, S=cfg.n)
+    assert full.ready_recall == 1.0 and full.loads == 0 and full.prefetched == 0
+    off = o.run_decode(cfg, W, h0, M_max=-1)
+    pred0 = o.run_decode(cfg, W, h0, M_max=0)
+    assert pred0.prefetched == 0
+    assert pred0.ready_recall == off.ready_recall and pred0.loads == off.loads
+
+
+def test_closed_form_exact_adapter_gives_perfect_recall():
+    """Noise 0, rank r >= rank(W^{l+1}), zero down projections, no stand-in:
+    h^{l+1} = h^l, so x^{l+1} = x^l and z_hat = W^{l+1} x^l = z^{l+1}; then
+    R@K = 1, R@K/2 = 1/2 (the paper's maximum for half the budget) and R@(K+2) = 1."""
+    cfg = w.get("c0")
+
+    class ZeroDown(o.OracleWeights):
+        def expert(self, l, e):
+            Wg, Wu, Wd = super().expert(l, e)
+            return Wg, Wu, np.zeros_like(Wd)
+
+    W = ZeroDown(cfg, adapter_override=lambda l: tuple(
+        o.decode(a, cfg.dtype) for a in gen.adapter_weights(cfg, l, noise=0.0)))
+    res = o.run_decode(cfg, W, gen.hidden_states(cfg), M_max=1)
+    K = cfg.K
+    assert res.expert_recall[K] == 1.0
+    assert res.expert_recall[K // 2] == 0.5
+    assert res.expert_recall[K + 2] == 1.0
+
+
+def test_metrics_recomputed_from_step_records():
+    cfg = _small_cfg(batch=2, L=3, S=7)
+    h0 = gen.hidden_states(cfg)
+    W = o.OracleWeights(cfg)
+    res = o.run_decode(cfg, W, h0, M_max=2)
+    K, Ms = cfg.K, sorted(res.expert_recall)
+    by_tl = {(s.t, s.l): s for s in res.steps}
+    num = {m: 0 for m in Ms}
+    ready, cnt = 0, 0
+    for (t, l), st in by_tl.items():
+        if l == 0:
+            continue
+        prev = by_tl[(t, l - 1)]
+        for b in range(cfg.batch):
+            Tb = set(int(e) for e in st.T[b])
+            for m in Ms:
+                order = sorted(range(cfg.n), key=lambda e: (-prev.s[e], e))[:m]
+                num[m] += len(Tb & set(order))
+            avail = set(int(e) for e in prev.next_table_after_prefetch if e != o.EMPTY)
+            ready += len(Tb & avail)
+            cnt += 1
+    for m in Ms:
+        assert res.expert_recall[m] == pytest.approx(num[m] / (cnt * K))
+    assert res.ready_recall == pytest.approx(ready / (cnt * K))
+    assert res.expert_recall[Ms[0]] <= res.expert_recall[Ms[1]] <= res.expert_recall[Ms[2]]
+    assert res.expert_recall[Ms[0]] <= 0.5 + 1e-12          # K/2 candidates cover at most half
+    # candidate set of all n experts covers everything
+    for st in res.steps:
+        if st.s is not None:
+            assert set(o.candidate_set(st.s, cfg.n).tolist()) == set(range(cfg.n))
+
+
+def test_layer_step_matches_decode_loop():
+    cfg = _small_cfg()
+    h0 = gen.hidden_states(cfg)
+    W = o.OracleWeights(cfg)
+    res = o.run_decode(cfg, W, h0, M_max=2, tokens=3)
+    caches = [o.SlotCache(cfg.S, cfg.n, list(range(cfg.S))) for _ in range(cfg.L)]
+    tau = 0
+    for t in range(3):
+        h = h0[t]
+        for l in range(cfg.L):
+            tau += 1
+            st = o.layer_step(cfg, W, l, h, caches[l], caches[l + 1] if l + 1 < cfg.L else None, tau, 2)
+            ref = res.steps[t * cfg.L + l]
+            assert np.array_equal(st.T, ref.T) and np.array_equal(st.h_out, ref.h_out)
+            assert st.P == ref.P and st.loads == ref.loads
+            h = st.h_out

@@ -1,0 +1,103 @@
+"""Workload configurations for the offloaded-MoE decode hot path.
+
+Each configuration fixes the shapes of a synthetic MoE decode stack and the
+recipe of its seeded inputs.  The shapes follow the two models the paper
+evaluates (Section "Experimental Setup": Qwen3-VL-30B-A3B with 128 routed
+experts and top-8, DeepSeek-VL2-Tiny with 64 routed experts, top-6 and shared
+experts); the values are synthetic (no checkpoint or dataset is used).
+
+This module holds no arithmetic of the method: it only names sizes, seeds and
+distributions.  Both the CPU oracle and the device path read it.
+"""
+from __future__ import annotations
+
+import dataclasses
+from dataclasses import dataclass, field
+from typing import Tuple
+
+
+@dataclass(frozen=True)
+class MoEConfig:
+    """Shapes, storage precision and input recipe of one synthetic decode stack.
+
+    Notation follows the paper's problem formulation: ``L`` MoE layers, ``n``
+    routed experts per layer, top-``K`` routing, hidden size ``D``; the adapter
+    rank ``r`` (Section "Expert Prediction Adapter").  ``I`` is the SwiGLU
+    intermediate size of one routed expert, ``S`` the number of accelerator
+    expert slots per layer (the capacity of the available set), ``windows``
+    the prefetch window capacities (in whole expert transfers) the budget is
+    evaluated at.
+    """
+
+    name: str
+    L: int
+    D: int
+    n: int
+    K: int
+    I: int
+    r: int
+    S: int
+    windows: Tuple[int, ...]
+    tokens: int
+    batch: int = 1
+    n_shared: int = 0
+    has_proj: bool = False
+    dtype: str = "bf16"          # storage dtype of weights and hidden states: "bf16" | "f32"
+    seed: int = 0
+    rho: float = 0.8             # AR(1) coefficient of the layer-0 hidden states
+    sigma: float = 0.6           # AR(1) innovation scale
+    w_std: float = 0.02          # std of router, expert, shared-expert and projection weights
+    adapter_noise: float = 0.005  # std of the noise added to the SVD-built adapters
+    rms_eps: float = 1e-6
+
+    @property
+    def elem_bytes(self) -> int:
+        return 2 if self.dtype == "bf16" else 4
+
+    @property
+    def blob_elems(self) -> int:
+        """Elements of one expert: gate [I,D] + up [I,D] + down [D,I]."""
+        return 3 * self.I * self.D
+
+    @property
+    def blob_bytes(self) -> int:
+        return self.blob_elems * self.elem_bytes
+
+    @property
+    def window(self) -> int:
+        """Default window capacity (first entry of ``windows``)."""
+        return self.windows[0]
+
+    def with_(self, **kw) -> "MoEConfig":
+        return dataclasses.replace(self, **kw)
+
+
+# Tiny fp32 parity case: 2 layers, 8 experts, top-2.
+C0 = MoEConfig(name="tiny_f32_L2_D256_n8_k2", L=2, D=256, n=8, K=2, I=512, r=16,
+               S=4, windows=(1,), tokens=64, dtype="f32", seed=0)
+
+# Qwen3-VL-30B-A3B-shaped MoE layer pair in bf16 (layer 0 is the predictor's
+# source, layer 1 the prefetch target): 128 experts, top-8, 9.44 MB per expert.
+C1 = MoEConfig(name="qwen3vl30b_a3b_layer_bf16", L=2, D=2048, n=128, K=8, I=768, r=64,
+               S=32, windows=(2,), tokens=256, seed=0)
+
+# Full 48-layer Qwen3-VL-30B-A3B-shaped stack with a dense 2048x2048 stand-in
+# projection per layer in place of attention; 25% of experts resident.
+C2 = MoEConfig(name="qwen3vl30b_a3b_stack48_bf16", L=48, D=2048, n=128, K=8, I=768, r=64,
+               S=32, windows=(1, 2, 4), tokens=512, has_proj=True, seed=0)
+
+# DeepSeek-VL2-Tiny-shaped stack: 12 layers, 64 routed experts, top-6, two
+# always-resident shared experts; 30% of routed experts resident (floor).
+C3 = MoEConfig(name="deepseekvl2_tiny_stack12_bf16", L=12, D=1280, n=64, K=6, I=896, r=32,
+               S=19, windows=(2,), tokens=512, n_shared=2, seed=0)
+
+# Batched Qwen3-VL-30B-A3B-shaped stack at 64 concurrent decode sequences.
+C4 = MoEConfig(name="qwen3vl30b_a3b_stack48_b64_bf16", L=48, D=2048, n=128, K=8, I=768, r=64,
+               S=32, windows=(4,), tokens=256, batch=64, has_proj=True, seed=0)
+
+CONFIGS = {"c0": C0, "c1": C1, "c2": C2, "c3": C3, "c4": C4}
+
+
+def get(name: str, **overrides) -> MoEConfig:
+    cfg = CONFIGS[name]
+    return cfg.with_(**overrides) if overrides else cfg
