@@ -1,0 +1,234 @@
+/*
+ * spp.h -- C ABI of the MI355X (gfx950) SpecPrefetch offloaded-MoE decode hot path.
+ *
+ * One decode step of an offloaded MoE layer, as the paper's problem statement
+ * and method sections describe it:
+ *   native router (softmax, top-K) -> layer-specific low-rank adapter scoring
+ *   the next layer's expert priorities -> window-aware prefetch budget ->
+ *   routed-expert SwiGLU FFN over an HBM expert-slot cache, while budgeted
+ *   host-to-device copies of the next layer's experts overlap with it.
+ *
+ * Conventions for every call:
+ *  - Plain pointers only.  "dev" pointers are device (HBM) addresses on the
+ *    device that was current at spp_create; "host" pointers are ordinary host
+ *    memory unless stated.  The caller owns every pointer it passes and keeps
+ *    it valid for as long as the context may use it (weights and host stores:
+ *    until spp_destroy).  The library owns its slot pools, events, copy stream
+ *    and scratch.
+ *  - Every call returns an spp_status and never throws.  On SPP_EINVAL no
+ *    state has changed.  HIP runtime failures return SPP_EHIP.  The message of
+ *    the last non-OK status of the calling thread is spp_last_error().
+ *  - Device work is enqueued on the compute stream given to spp_create; the
+ *    library's copy stream runs host-to-device expert copies beside it.  Calls
+ *    with host outputs return once those outputs are valid.
+ *  - Layouts are row-major.  dtype SPP_DTYPE_F32 stores weights and hidden
+ *    states as fp32, SPP_DTYPE_BF16 as bf16 (bit patterns, 2 bytes); router
+ *    logits, gates, priorities and the router input are always fp32.
+ *
+ * Expert blob layout (one routed or shared expert, "blob"): I units of 3*D
+ * elements, unit i = [gate row i (D), up row i (D), down column i (D)], i.e.
+ *   blob[(3i+0)D + d] = W_gate[i][d],  blob[(3i+1)D + d] = W_up[i][d],
+ *   blob[(3i+2)D + d] = W_down[d][i].
+ * Blobs are placed at a stride of spp_blob_stride(desc) bytes (3*I*D*elem
+ * rounded up to 4096).
+ */
+#ifndef SPP_H
+#define SPP_H
+
+#include <stddef.h>
+#include <stdint.h>
+
+#ifdef __cplusplus
+extern "C" {
+#endif
+
+typedef struct spp_ctx spp_ctx;
+typedef struct spp_slot_policy spp_slot_policy;
+
+typedef enum {
+  SPP_OK = 0,
+  SPP_EINVAL = -1,  /* bad argument; nothing changed */
+  SPP_ENOMEM = -2,  /* device or pinned allocation failed */
+  SPP_EHIP = -3,    /* a HIP runtime call failed; see spp_last_error() */
+  SPP_ESTATE = -4   /* call not valid in the current state (e.g. layer not bound) */
+} spp_status;
+
+enum { SPP_DTYPE_F32 = 0, SPP_DTYPE_BF16 = 1 };
+
+/* Model shape.  Notation of the paper's problem formulation: L MoE layers,
+ * n routed experts per layer, top-K routing, router input size D, adapter
+ * rank r.  I: SwiGLU intermediate size of an expert; n_shared: always-resident
+ * shared experts per layer (weight 1); S: HBM expert slots per layer;
+ * max_batch: largest batch B passed to any call; has_proj: 1 if each layer
+ * starts with the dense D x D stand-in projection u = h + P rms(h). */
+typedef struct {
+  int32_t L, D, n, K, I, r, n_shared, S, max_batch, dtype, has_proj;
+  float rms_eps;
+} spp_model_desc;
+
+/* Counters of one moe_layer_forward call. */
+typedef struct {
+  int32_t hits;           /* routed experts of the batch demand already available (resident or in flight) */
+  int32_t misses;         /* on-demand loads issued for this layer */
+  int32_t prefetched;     /* prefetch copies issued for layer l+1 */
+  int32_t prefetch_used;  /* experts prefetched for this layer that its native router selected */
+  int32_t ready_on_time;  /* needed experts whose copy had completed when the FFN was enqueued */
+} spp_layer_stats;
+
+/* Accumulated since the last spp_reset_run_stats.  Times come from HIP events
+ * on the compute stream (only when timing is enabled). */
+typedef struct {
+  int64_t layer_calls, hits, misses, prefetched, prefetch_used, ready_on_time, copies;
+  int64_t copy_bytes, ffn_launches, window_samples;
+  double router_us;   /* router+adapter kernel and result read-back */
+  double exposed_us;  /* compute stream waiting on expert copies before the FFN */
+  double ffn_us;      /* routed-expert FFN main kernel */
+  double tail_us;     /* FFN combine/residual kernel */
+  double span_us;     /* first layer start to last layer end */
+  double window_us;   /* sum of prediction-available -> next-layer FFN start */
+} spp_run_stats;
+
+/* ---------------------------------------------------------------- lifecycle */
+
+/* Bytes between consecutive expert blobs in a host store or slot pool. */
+size_t spp_blob_stride(const spp_model_desc* desc);
+
+/* Create a context on the current device.  hip_stream: the compute stream
+ * (hipStream_t, may be NULL for the null stream).  Allocates S slots per layer
+ * plus scratch; every slot starts EMPTY.  Errors: EINVAL for inconsistent
+ * shapes (S < K*max_batch when the batch demand could exceed S is allowed but
+ * such a call later fails), ENOMEM, EHIP. */
+spp_status spp_create(const spp_model_desc* desc, void* hip_stream, spp_ctx** out);
+spp_status spp_destroy(spp_ctx* ctx);
+
+/* Bind layer l's weights.  router_w: dev [n,D]; adapter_a: dev [r,D] and
+ * adapter_b: dev [n,r] (both NULL for the last layer, which has no adapter);
+ * proj_w: dev [D,D] or NULL (required iff has_proj); shared_blobs: dev
+ * n_shared blobs at blob stride (NULL iff n_shared == 0); host_store: the
+ * offload tier, n blobs at blob stride in pinned host memory (hipHostMalloc
+ * or a pinned torch tensor), expert e at host_store + e*stride. */
+spp_status spp_bind_layer(spp_ctx* ctx, int32_t l, const void* router_w, const void* adapter_a,
+                          const void* adapter_b, const void* proj_w, const void* shared_blobs,
+                          const void* host_store);
+
+/* Fill slots 0..count-1 of layer l with the listed experts (synchronous
+ * copies), stamp 0; the other slots become EMPTY.  count <= S, no duplicates. */
+spp_status spp_set_resident(spp_ctx* ctx, int32_t l, const int32_t* experts, int32_t count);
+
+/* ------------------------------------------------------- the four calls */
+
+/* Section "Expert Prediction Adapter": s^{l+1}_e = sum over the B tokens of
+ * softmax(B^l A^l x_b)_e.  x_dev: dev fp32 [B,D], the router inputs of layer
+ * l; s_out: host fp32 [n].  Synchronous.  ESTATE if layer l has no adapter. */
+spp_status adapter_predict(spp_ctx* ctx, int32_t l, const float* x_dev, int32_t B, float* s_out);
+
+/* Section "Window-Aware Prefetch Budgeting": the maximum prefetch budget is the
+ * number of whole expert transfers that fit in the profiled overlap window W,
+ * M_max = clamp(floor(window_us / per_expert_cost_us), 0, n_experts).
+ * window_us <= 0 gives 0.  EINVAL for a non-finite input, a cost <= 0 or
+ * n_experts < 0.  Pure host arithmetic; needs no device. */
+spp_status select_prefetch_budget(double window_us, double per_expert_cost_us, int32_t n_experts,
+                                  int32_t* M_max_out);
+
+/* Same section: P^{l+1} = Top_{M_max}{ s_e : e neither available nor in
+ * flight in target_layer }, lowest expert index first on equal priority,
+ * issued as asynchronous host-to-device copies in descending priority, each
+ * into a replacement slot (lowest EMPTY slot, else the least recently stamped
+ * slot not filled in this step; stops early when none is left).  s_host: host
+ * fp32 [n].  issued_out: host int32 [M_max] receives P in issue order; m_out:
+ * |P| <= M_max.  Advances the step clock by one.  Returns without waiting for
+ * the copies. */
+spp_status expert_cache_issue_prefetch(spp_ctx* ctx, int32_t target_layer, const float* s_host,
+                                       int32_t M_max, int32_t* issued_out, int32_t* m_out);
+
+/* One MoE layer of one decode step (sections "Problem Formulation" through
+ * "Window-Aware Prefetch Budgeting"):
+ *   u = h (+ P rms(h) if has_proj); x = rms(u) (fp32, no learned scale);
+ *   z = W_r x (fp32); T_b = Top_K(z_b), lowest index first on ties;
+ *   g_b = softmax(z_b) renormalised over T_b;
+ *   if l < L-1 and M_max >= 0: s = sum_b softmax(B A x_b);
+ *   on-demand copies of every expert of the batch demand not available
+ *   (replacement: lowest EMPTY slot, else the least recently stamped slot
+ *   whose expert the batch does not need); every slot holding a needed
+ *   expert takes the step stamp;
+ *   if M_max > 0: the expert_cache_issue_prefetch selection for layer l+1
+ *   with this s, in the same step;
+ *   FFN: h_out_b = round(u_b + sum_k g_bk W_down(silu(W_gate x_b) * (W_up x_b))
+ *   [+ shared experts, weight 1]), reading each expert from its HBM slot
+ *   after its copy completed.
+ * h_in_dev / h_out_dev: dev [B,D] in dtype (may not alias).  M_max: -1 = no
+ * prediction (OFF), 0 = prediction without transfers, > 0 = budget.
+ * topk_out: host int32 [B,K] or NULL; gate_out: host fp32 [B,K] or NULL;
+ * stats: host or NULL.  Outputs never depend on M_max, S or the adapter.
+ * Advances the step clock by one.  Returns once topk/gates are on the host;
+ * h_out is complete when the compute stream reaches that point. */
+spp_status moe_layer_forward(spp_ctx* ctx, int32_t l, const void* h_in_dev, void* h_out_dev, int32_t B,
+                             int32_t M_max, int32_t* topk_out, float* gate_out, spp_layer_stats* stats);
+
+/* Message of the calling thread's last non-OK status ("" if none). */
+const char* spp_last_error(void);
+
+/* ------------------------------------------------------ inspection / runs */
+
+/* Slot table of layer l: experts_out host int32 [S] (-1 = EMPTY), stamps_out
+ * host int64 [S] (either may be NULL). */
+spp_status spp_get_slot_table(spp_ctx* ctx, int32_t l, int32_t* experts_out, int64_t* stamps_out);
+
+/* Replace layer l's slot table (copies the listed experts in, synchronously).
+ * Used to re-synchronise with a reference state. */
+spp_status spp_set_slot_table(spp_ctx* ctx, int32_t l, const int32_t* experts, const int64_t* stamps);
+
+/* The step clock: the stamp of the last step taken (0 after spp_create). */
+spp_status spp_get_clock(spp_ctx* ctx, int64_t* tau_out);
+spp_status spp_set_clock(spp_ctx* ctx, int64_t tau);
+
+/* Transfers of the last moe_layer_forward: loads_out / pref_out host int32
+ * [3*cap] as (expert, slot, evicted expert or -1) triples in issue order;
+ * n_loads / n_pref receive the counts (may exceed cap: then truncated). */
+spp_status spp_get_last_transfers(spp_ctx* ctx, int32_t* loads_out, int32_t* n_loads, int32_t* pref_out,
+                                   int32_t* n_pref, int32_t cap);
+
+/* Priorities s (host fp32 [n]) and router inputs x (host fp32 [B,D]) of the
+ * last moe_layer_forward (s is undefined when no adapter ran). */
+spp_status spp_get_last_priorities(spp_ctx* ctx, float* s_out);
+spp_status spp_get_last_router_input(spp_ctx* ctx, float* x_out, int32_t B);
+
+/* Event timing of layer calls (adds ~6 event records per call). */
+spp_status spp_set_timing(spp_ctx* ctx, int32_t enabled);
+/* Waits for all enqueued work, folds finished event timings into the totals. */
+spp_status spp_get_run_stats(spp_ctx* ctx, spp_run_stats* out);
+spp_status spp_reset_run_stats(spp_ctx* ctx);
+
+/* Measured host-to-device cost of one expert blob on the copy stream
+ * (average over reps copies from layer l's host store into scratch), in us. */
+spp_status spp_profile_expert_copy(spp_ctx* ctx, int32_t l, int32_t reps, double* per_expert_us);
+
+/* Launch shape of the routed-expert FFN: about `wgs` workgroups share the
+ * (expert, unit) work list of one token (default 256; 1..4096).  Applies to
+ * every context in the process. */
+spp_status spp_set_ffn_workgroups(spp_ctx* ctx, int32_t wgs);
+
+/* ------------------------------------- host replacement policy (no device) */
+
+/* The slot-replacement and prefetch-selection policy the context runs for
+ * each layer, as a host-only object (no HIP calls), so that it can be driven
+ * without a GPU.  Semantics are exactly those of the calls above. */
+spp_status spp_policy_create(int32_t S, int32_t n, const int32_t* resident, int32_t count,
+                             spp_slot_policy** out);
+spp_status spp_policy_destroy(spp_slot_policy* p);
+/* needed: the batch demand (any order, duplicates allowed); loads_out host
+ * int32 [3*S] receives (expert, slot, evicted) triples; EINVAL if the demand
+ * has more distinct experts than S. */
+spp_status spp_policy_on_demand(spp_slot_policy* p, const int32_t* needed, int32_t count, int64_t tau,
+                                int32_t* loads_out, int32_t* n_loads);
+/* Prefetch selection + placement with priorities s (host fp32 [n]);
+ * placed_out host int32 [3*max(M_max,0)]. */
+spp_status spp_policy_prefetch(spp_slot_policy* p, const float* s, int32_t M_max, int64_t tau,
+                               int32_t* placed_out, int32_t* n_placed);
+spp_status spp_policy_get(spp_slot_policy* p, int32_t* experts_out, int64_t* stamps_out);
+
+#ifdef __cplusplus
+}
+#endif
+
+#endif /* SPP_H */

@@ -1,0 +1,69 @@
+// Internal interface between the runtime (spp_runtime.cpp) and the gfx950
+// kernels (spp_kernels.hip).  Not part of the public ABI.
+#pragma once
+
+#include <hip/hip_runtime_api.h>
+
+#include <cstdint>
+
+namespace spp {
+
+constexpr int kMaxWork = 32;       // expert blobs one FFN launch can combine
+constexpr int kMaxExpertsTopK = 1024;
+
+// Router + adapter (one launch).  Rows [0, n) are router logits (if
+// router_on), rows [n, n+r) adapter hidden units (if A != nullptr).
+struct RouterArgs {
+  const void* h;        // [B, D] storage dtype; layer input when u == nullptr
+  const float* u;       // [B, D] fp32 input (prologue output, or x itself when x_given)
+  const void* Wr;       // [n, D]
+  const void* A;        // [r, D] or nullptr
+  const void* Bm;       // [n, r]
+  float* x_out;         // [B, D] router input written by block 0 (nullptr: skip)
+  float* zbuf;          // [B, n + r] logits then adapter hidden units
+  int32_t* topk;        // [B, K]
+  float* gates;         // [B, K]
+  float* s;             // [n]
+  unsigned* counter;    // zero between launches
+  int B, D, n, K, r;
+  float eps;
+  int x_given;          // u holds x (no normalisation)
+  int router_on;
+};
+
+struct FfnArgs {
+  const void* blob[kMaxWork];  // expert blobs (slot or shared expert)
+  int32_t gate_idx[kMaxWork];  // index into gates, or -1 for weight 1
+  int nW;
+  int I, D;
+  int upw;                     // units per workgroup
+  const float* x;              // [D] router input of the token
+  const float* gates;
+  float* partial;              // [gridDim.x, D]
+};
+
+struct CombineArgs {
+  const float* partial;  // [nparts, D]
+  int nparts, D;
+  const void* res_h;     // residual in storage dtype (used when res_u == nullptr)
+  const float* res_u;    // fp32 residual (prologue output)
+  void* out;             // [D] storage dtype
+};
+
+struct ProjArgs {
+  const void* h;   // [B, D]
+  const void* P;   // [D, D]
+  float* u;        // [B, D]
+  int B, D;
+  float eps;
+};
+
+hipError_t launch_router(const RouterArgs& a, int dtype, hipStream_t st);
+hipError_t launch_ffn(const FfnArgs& a, int grid, int dtype, hipStream_t st);
+hipError_t launch_combine(const CombineArgs& a, int dtype, hipStream_t st);
+hipError_t launch_proj(const ProjArgs& a, int dtype, hipStream_t st);
+int ffn_grid_for(int nunits, int* upw);
+size_t ffn_max_grid();
+void set_ffn_target_wgs(int wgs);
+
+}  // namespace spp

@@ -1,0 +1,748 @@
+// Host runtime of the offloaded-MoE decode hot path: context, per-layer HBM
+// slot pools, copy engine (pinned host -> device on a side stream, fenced by
+// events), the layer orchestrator, event timing, and the C ABI of spp.h.
+#include <hip/hip_runtime_api.h>
+
+#include <algorithm>
+#include <cmath>
+#include <cstring>
+#include <memory>
+#include <new>
+#include <string>
+#include <vector>
+
+#include "spp.h"
+#include "spp_internal.h"
+#include "spp_policy.h"
+
+namespace {
+
+thread_local std::string g_err;
+
+spp_status fail(spp_status s, const std::string& m) {
+  g_err = m;
+  return s;
+}
+
+#define SPP_HIP(expr)                                                                              \
+  do {                                                                                             \
+    hipError_t e_ = (expr);                                                                        \
+    if (e_ != hipSuccess) return fail(SPP_EHIP, std::string(#expr) + ": " + hipGetErrorString(e_)); \
+  } while (0)
+
+constexpr int kEvStart = 0, kEvRouted = 1, kEvWaitA = 2, kEvFfnStart = 3, kEvFfnDone = 4, kEvEnd = 5;
+constexpr int kNumEv = 6;
+
+struct TimingSet {
+  hipEvent_t ev[kNumEv] = {};
+  int32_t l = -1;
+  bool predicted = false;
+};
+
+struct LayerState {
+  bool bound = false;
+  const void* router_w = nullptr;
+  const void* A = nullptr;
+  const void* Bm = nullptr;
+  const void* proj = nullptr;
+  const void* shared = nullptr;
+  const uint8_t* host_store = nullptr;
+  uint8_t* slots = nullptr;
+  std::unique_ptr<spp::SlotPolicy> policy;
+  std::vector<hipEvent_t> slot_ready;  // recorded on the copy stream after the last copy into the slot
+  std::vector<char> slot_pending;      // slot_ready holds a copy that may not have been waited on
+  hipEvent_t last_read = nullptr;      // recorded on the compute stream after the layer's FFN
+  bool last_read_valid = false;
+  std::vector<int32_t> pending_prefetch;  // prefetched for this layer, not yet executed
+};
+
+size_t round_up(size_t v, size_t a) { return (v + a - 1) / a * a; }
+
+}  // namespace
+
+struct spp_ctx {
+  spp_model_desc d{};
+  int device = 0;
+  hipStream_t compute = nullptr;
+  hipStream_t copy = nullptr;
+  size_t elem = 0, blob_bytes = 0, stride = 0;
+  std::vector<LayerState> layers;
+  float* u_dev = nullptr;      // [maxB, D] prologue output
+  float* x_dev = nullptr;      // [maxB, D] router input
+  float* zbuf = nullptr;       // [maxB, n + r]
+  uint8_t* res_dev = nullptr;  // topk [maxB*K] i32 | gates [maxB*K] f32 | s [n] f32
+  uint8_t* res_host = nullptr; // pinned mirror
+  size_t res_bytes = 0, off_gates = 0, off_s = 0;
+  unsigned* counter = nullptr;
+  float* partial = nullptr;    // [ffn_max_grid, D]
+  uint8_t* probe_dev = nullptr;  // one blob, for copy profiling
+  hipEvent_t ev_res = nullptr;
+  int64_t clock = 0;
+  int ffn_wgs = 256;
+  // last call record
+  std::vector<spp::Transfer> last_loads, last_pref;
+  std::vector<float> last_s;
+  int32_t last_B = 0;
+  bool last_s_valid = false;
+  // timing
+  bool timing = false;
+  std::vector<TimingSet> pending_sets, free_sets;
+  bool have_prev = false;
+  TimingSet prev{};
+  spp_run_stats stats{};
+};
+
+namespace {
+
+bool desc_ok(const spp_model_desc* d, std::string* why) {
+  if (!d) return *why = "desc is NULL", false;
+  if (d->dtype != SPP_DTYPE_F32 && d->dtype != SPP_DTYPE_BF16) return *why = "dtype must be 0 (f32) or 1 (bf16)", false;
+  const int elem = d->dtype == SPP_DTYPE_BF16 ? 2 : 4;
+  if (d->L < 1 || d->D < 1 || d->n < 1 || d->K < 1 || d->I < 1 || d->S < 1 || d->max_batch < 1)
+    return *why = "L, D, n, K, I, S, max_batch must be >= 1", false;
+  if ((static_cast<int64_t>(d->D) * elem) % 16 != 0) return *why = "D * element size must be a multiple of 16 bytes", false;
+  const int nch = (d->D * elem / 16 + 63) / 64;
+  if (nch > 8) return *why = "D too large (at most 4096 bf16 / 2048 fp32)", false;
+  if (d->n > spp::kMaxExpertsTopK) return *why = "n must be <= 1024", false;
+  if (d->K > d->n || d->K > 32) return *why = "K must be <= min(n, 32)", false;
+  if (d->r < 0 || d->r > 256) return *why = "r must be in [0, 256]", false;
+  if (d->n_shared < 0 || d->K + d->n_shared > spp::kMaxWork) return *why = "K + n_shared must be <= 32", false;
+  if (d->has_proj != 0 && d->has_proj != 1) return *why = "has_proj must be 0 or 1", false;
+  if (!(d->rms_eps >= 0.f) || !std::isfinite(d->rms_eps)) return *why = "rms_eps must be finite and >= 0", false;
+  return true;
+}
+
+spp_status check_ctx(spp_ctx* c) {
+  if (!c) return fail(SPP_EINVAL, "ctx is NULL");
+  return SPP_OK;
+}
+
+spp_status check_layer(spp_ctx* c, int32_t l, bool need_bound) {
+  if (!c) return fail(SPP_EINVAL, "ctx is NULL");
+  if (l < 0 || l >= c->d.L) return fail(SPP_EINVAL, "layer index out of range");
+  if (need_bound && !c->layers[l].bound) return fail(SPP_ESTATE, "layer not bound");
+  return SPP_OK;
+}
+
+spp_status take_set(spp_ctx* c, TimingSet* out) {
+  if (!c->free_sets.empty()) {
+    *out = c->free_sets.back();
+    c->free_sets.pop_back();
+    return SPP_OK;
+  }
+  TimingSet s;
+  for (int i = 0; i < kNumEv; ++i) SPP_HIP(hipEventCreate(&s.ev[i]));
+  *out = s;
+  return SPP_OK;
+}
+
+float elapsed(hipEvent_t a, hipEvent_t b) {
+  float ms = 0.f;
+  if (hipEventElapsedTime(&ms, a, b) != hipSuccess) return 0.f;
+  return ms;
+}
+
+// Fold the first `count` pending sets (all complete) into the totals.
+void harvest(spp_ctx* c, size_t count) {
+  for (size_t i = 0; i < count; ++i) {
+    TimingSet& s = c->pending_sets[i];
+    spp_run_stats& st = c->stats;
+    st.router_us += 1e3 * elapsed(s.ev[kEvStart], s.ev[kEvRouted]);
+    st.exposed_us += 1e3 * elapsed(s.ev[kEvWaitA], s.ev[kEvFfnStart]);
+    st.ffn_us += 1e3 * elapsed(s.ev[kEvFfnStart], s.ev[kEvFfnDone]);
+    st.tail_us += 1e3 * elapsed(s.ev[kEvFfnDone], s.ev[kEvEnd]);
+    if (c->have_prev) {
+      st.span_us += 1e3 * elapsed(c->prev.ev[kEvStart], s.ev[kEvStart]);
+      if (c->prev.predicted && s.l == c->prev.l + 1) {
+        st.window_us += 1e3 * elapsed(c->prev.ev[kEvRouted], s.ev[kEvFfnStart]);
+        st.window_samples += 1;
+      }
+      c->free_sets.push_back(c->prev);
+    }
+    c->prev = s;
+    c->have_prev = true;
+  }
+  c->pending_sets.erase(c->pending_sets.begin(), c->pending_sets.begin() + count);
+}
+
+// Issue host->device copies for transfers into layer `ls`.
+spp_status issue_copies(spp_ctx* c, LayerState& ls, const std::vector<spp::Transfer>& xs) {
+  if (xs.empty()) return SPP_OK;
+  if (ls.last_read_valid) SPP_HIP(hipStreamWaitEvent(c->copy, ls.last_read, 0));  // WAR on slot reuse
+  for (const spp::Transfer& t : xs) {
+    SPP_HIP(hipMemcpyAsync(ls.slots + static_cast<size_t>(t.slot) * c->stride,
+                           ls.host_store + static_cast<size_t>(t.expert) * c->stride, c->blob_bytes,
+                           hipMemcpyHostToDevice, c->copy));
+    SPP_HIP(hipEventRecord(ls.slot_ready[t.slot], c->copy));
+    ls.slot_pending[t.slot] = 1;
+    c->stats.copies += 1;
+    c->stats.copy_bytes += static_cast<int64_t>(c->blob_bytes);
+  }
+  return SPP_OK;
+}
+
+spp_status sync_all(spp_ctx* c) {
+  SPP_HIP(hipStreamSynchronize(c->copy));
+  SPP_HIP(hipStreamSynchronize(c->compute));
+  return SPP_OK;
+}
+
+// Synchronous fill of slots from the host store according to the policy table.
+spp_status fill_slots(spp_ctx* c, LayerState& ls, const std::vector<int32_t>& before) {
+  const auto& table = ls.policy->slot_experts();
+  for (int32_t j = 0; j < c->d.S; ++j) {
+    ls.slot_pending[j] = 0;
+    if (table[j] == spp::kEmpty || table[j] == before[j]) continue;
+    SPP_HIP(hipMemcpy(ls.slots + static_cast<size_t>(j) * c->stride,
+                      ls.host_store + static_cast<size_t>(table[j]) * c->stride, c->blob_bytes,
+                      hipMemcpyHostToDevice));
+  }
+  return SPP_OK;
+}
+
+void free_ctx(spp_ctx* c) {
+  if (!c) return;
+  if (c->copy) (void)hipStreamSynchronize(c->copy);
+  (void)hipStreamSynchronize(c->compute);
+  for (LayerState& ls : c->layers) {
+    if (ls.slots) (void)hipFree(ls.slots);
+    for (hipEvent_t e : ls.slot_ready)
+      if (e) (void)hipEventDestroy(e);
+    if (ls.last_read) (void)hipEventDestroy(ls.last_read);
+  }
+  for (auto* v : {&c->pending_sets, &c->free_sets})
+    for (TimingSet& s : *v)
+      for (hipEvent_t e : s.ev)
+        if (e) (void)hipEventDestroy(e);
+  if (c->have_prev)
+    for (hipEvent_t e : c->prev.ev)
+      if (e) (void)hipEventDestroy(e);
+  for (void* p : {static_cast<void*>(c->u_dev), static_cast<void*>(c->x_dev), static_cast<void*>(c->zbuf),
+                  static_cast<void*>(c->res_dev), static_cast<void*>(c->counter), static_cast<void*>(c->partial),
+                  static_cast<void*>(c->probe_dev)})
+    if (p) (void)hipFree(p);
+  if (c->res_host) (void)hipHostFree(c->res_host);
+  if (c->ev_res) (void)hipEventDestroy(c->ev_res);
+  if (c->copy) (void)hipStreamDestroy(c->copy);
+  delete c;
+}
+
+spp_status create_impl(const spp_model_desc* desc, void* stream, spp_ctx** out) {
+  std::string why;
+  if (!out) return fail(SPP_EINVAL, "out is NULL");
+  *out = nullptr;
+  if (!desc_ok(desc, &why)) return fail(SPP_EINVAL, why);
+  std::unique_ptr<spp_ctx, void (*)(spp_ctx*)> c(new (std::nothrow) spp_ctx(), free_ctx);
+  if (!c) return fail(SPP_ENOMEM, "host allocation failed");
+  c->d = *desc;
+  SPP_HIP(hipGetDevice(&c->device));
+  c->compute = static_cast<hipStream_t>(stream);
+  c->elem = desc->dtype == SPP_DTYPE_BF16 ? 2 : 4;
+  c->blob_bytes = static_cast<size_t>(3) * desc->I * desc->D * c->elem;
+  c->stride = round_up(c->blob_bytes, 4096);
+  SPP_HIP(hipStreamCreateWithFlags(&c->copy, hipStreamNonBlocking));
+  const spp_model_desc& d = c->d;
+  c->layers.resize(d.L);
+  for (LayerState& ls : c->layers) {
+    ls.policy.reset(new spp::SlotPolicy(d.S, d.n));
+    if (hipMalloc(&ls.slots, c->stride * d.S) != hipSuccess) return fail(SPP_ENOMEM, "slot pool allocation failed");
+    ls.slot_ready.assign(d.S, nullptr);
+    ls.slot_pending.assign(d.S, 0);
+    for (hipEvent_t& e : ls.slot_ready) SPP_HIP(hipEventCreateWithFlags(&e, hipEventDisableTiming));
+    SPP_HIP(hipEventCreateWithFlags(&ls.last_read, hipEventDisableTiming));
+  }
+  const size_t BD = static_cast<size_t>(d.max_batch) * d.D;
+  if (hipMalloc(&c->u_dev, BD * sizeof(float)) != hipSuccess ||
+      hipMalloc(&c->x_dev, BD * sizeof(float)) != hipSuccess ||
+      hipMalloc(&c->zbuf, static_cast<size_t>(d.max_batch) * (d.n + d.r) * sizeof(float)) != hipSuccess ||
+      hipMalloc(&c->partial, spp::ffn_max_grid() * d.D * sizeof(float)) != hipSuccess ||
+      hipMalloc(&c->counter, 256) != hipSuccess)
+    return fail(SPP_ENOMEM, "scratch allocation failed");
+  const size_t bk = static_cast<size_t>(d.max_batch) * d.K;
+  c->off_gates = round_up(bk * sizeof(int32_t), 64);
+  c->off_s = c->off_gates + round_up(bk * sizeof(float), 64);
+  c->res_bytes = c->off_s + round_up(static_cast<size_t>(d.n) * sizeof(float), 64);
+  if (hipMalloc(&c->res_dev, c->res_bytes) != hipSuccess) return fail(SPP_ENOMEM, "result buffer allocation failed");
+  if (hipHostMalloc(&c->res_host, c->res_bytes, hipHostMallocDefault) != hipSuccess)
+    return fail(SPP_ENOMEM, "pinned result buffer allocation failed");
+  SPP_HIP(hipMemset(c->counter, 0, 256));
+  SPP_HIP(hipMemset(c->res_dev, 0, c->res_bytes));
+  SPP_HIP(hipEventCreateWithFlags(&c->ev_res, hipEventDisableTiming));
+  c->last_s.assign(d.n, 0.f);
+  SPP_HIP(hipDeviceSynchronize());
+  *out = c.release();
+  return SPP_OK;
+}
+
+spp_status layer_forward_impl(spp_ctx* c, int32_t l, const void* h_in, void* h_out, int32_t B, int32_t M_max,
+                              int32_t* topk_out, float* gate_out, spp_layer_stats* st_out) {
+  if (spp_status s = check_layer(c, l, true)) return s;
+  const spp_model_desc& d = c->d;
+  if (!h_in || !h_out) return fail(SPP_EINVAL, "h_in / h_out is NULL");
+  if (h_in == h_out) return fail(SPP_EINVAL, "h_in and h_out may not alias");
+  if (B < 1 || B > d.max_batch) return fail(SPP_EINVAL, "B must be in [1, max_batch]");
+  if (M_max < -1) return fail(SPP_EINVAL, "M_max must be >= -1");
+  LayerState& ls = c->layers[l];
+  const bool predict = l < d.L - 1 && M_max >= 0 && ls.A != nullptr && d.r > 0;
+  if (predict && M_max > 0 && !c->layers[l + 1].bound) return fail(SPP_ESTATE, "next layer not bound");
+  const int64_t tau = ++c->clock;
+  const int dt = d.dtype;
+  const size_t row_bytes = static_cast<size_t>(d.D) * c->elem;
+
+  TimingSet ts;
+  if (c->timing) {
+    if (spp_status s = take_set(c, &ts)) return s;
+    ts.l = l;
+    ts.predicted = predict;
+    SPP_HIP(hipEventRecord(ts.ev[kEvStart], c->compute));
+  }
+  if (d.has_proj) {
+    spp::ProjArgs pa{h_in, ls.proj, c->u_dev, B, d.D, d.rms_eps};
+    SPP_HIP(spp::launch_proj(pa, dt, c->compute));
+  }
+  int32_t* topk_dev = reinterpret_cast<int32_t*>(c->res_dev);
+  float* gates_dev = reinterpret_cast<float*>(c->res_dev + c->off_gates);
+  float* s_dev = reinterpret_cast<float*>(c->res_dev + c->off_s);
+  spp::RouterArgs ra{};
+  ra.h = h_in;
+  ra.u = d.has_proj ? c->u_dev : nullptr;
+  ra.Wr = ls.router_w;
+  ra.A = predict ? ls.A : nullptr;
+  ra.Bm = ls.Bm;
+  ra.x_out = c->x_dev;
+  ra.zbuf = c->zbuf;
+  ra.topk = topk_dev;
+  ra.gates = gates_dev;
+  ra.s = s_dev;
+  ra.counter = c->counter;
+  ra.B = B;
+  ra.D = d.D;
+  ra.n = d.n;
+  ra.K = d.K;
+  ra.r = d.r;
+  ra.eps = d.rms_eps;
+  ra.x_given = 0;
+  ra.router_on = 1;
+  SPP_HIP(spp::launch_router(ra, dt, c->compute));
+  const size_t fetch = predict ? c->res_bytes : c->off_s;
+  SPP_HIP(hipMemcpyAsync(c->res_host, c->res_dev, fetch, hipMemcpyDeviceToHost, c->compute));
+  if (c->timing) SPP_HIP(hipEventRecord(ts.ev[kEvRouted], c->compute));
+  SPP_HIP(hipEventRecord(c->ev_res, c->compute));
+  SPP_HIP(hipEventSynchronize(c->ev_res));
+  if (c->timing && c->pending_sets.size() >= 64) harvest(c, c->pending_sets.size());
+
+  const int32_t* T = reinterpret_cast<const int32_t*>(c->res_host);
+  const float* g = reinterpret_cast<const float*>(c->res_host + c->off_gates);
+  const float* s = reinterpret_cast<const float*>(c->res_host + c->off_s);
+  const int32_t BK = B * d.K;
+
+  spp_layer_stats st{};
+  {
+    std::vector<char> seen(d.n, 0);
+    for (int32_t i = 0; i < BK; ++i) {
+      const int32_t e = T[i];
+      if (e < 0 || e >= d.n) return fail(SPP_EHIP, "router produced an out-of-range expert id");
+      if (seen[e]) continue;
+      seen[e] = 1;
+      if (ls.policy->available(e)) st.hits += 1;
+    }
+    for (int32_t e : ls.pending_prefetch) st.prefetch_used += seen[e] ? 1 : 0;
+  }
+  ls.pending_prefetch.clear();
+  std::string why;
+  if (!ls.policy->on_demand(T, BK, tau, &c->last_loads, &why)) return fail(SPP_ESTATE, why);
+  st.misses = static_cast<int32_t>(c->last_loads.size());
+  if (spp_status e = issue_copies(c, ls, c->last_loads)) return e;
+
+  c->last_pref.clear();
+  c->last_s_valid = predict;
+  c->last_B = B;
+  if (predict) {
+    std::memcpy(c->last_s.data(), s, sizeof(float) * d.n);
+    if (M_max > 0) {
+      LayerState& nx = c->layers[l + 1];
+      nx.policy->prefetch(s, M_max, tau, &c->last_pref);
+      if (spp_status e = issue_copies(c, nx, c->last_pref)) return e;
+      nx.pending_prefetch.clear();
+      for (const spp::Transfer& t : c->last_pref) nx.pending_prefetch.push_back(t.expert);
+      st.prefetched = static_cast<int32_t>(c->last_pref.size());
+    }
+  }
+
+  // RAW: the FFN reads each needed slot only after its copy completed
+  if (c->timing) SPP_HIP(hipEventRecord(ts.ev[kEvWaitA], c->compute));
+  {
+    std::vector<char> waited(d.S, 0);
+    for (int32_t i = 0; i < BK; ++i) {
+      const int32_t slot = ls.policy->slot_of(T[i]);
+      if (waited[slot]) continue;
+      waited[slot] = 1;
+      if (!ls.slot_pending[slot]) {
+        st.ready_on_time += 1;
+        continue;
+      }
+      if (hipEventQuery(ls.slot_ready[slot]) == hipSuccess) {
+        st.ready_on_time += 1;
+        ls.slot_pending[slot] = 0;
+        continue;
+      }
+      SPP_HIP(hipStreamWaitEvent(c->compute, ls.slot_ready[slot], 0));
+    }
+  }
+  if (c->timing) SPP_HIP(hipEventRecord(ts.ev[kEvFfnStart], c->compute));
+  for (int32_t b = 0; b < B; ++b) {
+    spp::FfnArgs fa{};
+    int nW = 0;
+    for (int32_t k = 0; k < d.K; ++k) {
+      fa.blob[nW] = ls.slots + static_cast<size_t>(ls.policy->slot_of(T[b * d.K + k])) * c->stride;
+      fa.gate_idx[nW] = b * d.K + k;
+      ++nW;
+    }
+    for (int32_t j = 0; j < d.n_shared; ++j) {
+      fa.blob[nW] = static_cast<const uint8_t*>(ls.shared) + static_cast<size_t>(j) * c->stride;
+      fa.gate_idx[nW] = -1;
+      ++nW;
+    }
+    fa.nW = nW;
+    fa.I = d.I;
+    fa.D = d.D;
+    fa.x = c->x_dev + static_cast<size_t>(b) * d.D;
+    fa.gates = gates_dev;
+    fa.partial = c->partial;
+    const int grid = spp::ffn_grid_for(nW * d.I, &fa.upw);
+    SPP_HIP(spp::launch_ffn(fa, grid, dt, c->compute));
+    if (c->timing && b == B - 1) SPP_HIP(hipEventRecord(ts.ev[kEvFfnDone], c->compute));
+    spp::CombineArgs ca{};
+    ca.partial = c->partial;
+    ca.nparts = grid;
+    ca.D = d.D;
+    ca.res_h = static_cast<const uint8_t*>(h_in) + b * row_bytes;
+    ca.res_u = d.has_proj ? c->u_dev + static_cast<size_t>(b) * d.D : nullptr;
+    ca.out = static_cast<uint8_t*>(h_out) + b * row_bytes;
+    SPP_HIP(spp::launch_combine(ca, dt, c->compute));
+    c->stats.ffn_launches += 1;
+  }
+  SPP_HIP(hipEventRecord(ls.last_read, c->compute));
+  ls.last_read_valid = true;
+  if (c->timing) {
+    SPP_HIP(hipEventRecord(ts.ev[kEvEnd], c->compute));
+    c->pending_sets.push_back(ts);
+  }
+
+  if (topk_out) std::memcpy(topk_out, T, sizeof(int32_t) * BK);
+  if (gate_out) std::memcpy(gate_out, g, sizeof(float) * BK);
+  c->stats.layer_calls += 1;
+  c->stats.hits += st.hits;
+  c->stats.misses += st.misses;
+  c->stats.prefetched += st.prefetched;
+  c->stats.prefetch_used += st.prefetch_used;
+  c->stats.ready_on_time += st.ready_on_time;
+  if (st_out) *st_out = st;
+  return SPP_OK;
+}
+
+}  // namespace
+
+extern "C" {
+
+size_t spp_blob_stride(const spp_model_desc* d) {
+  if (!d) return 0;
+  const size_t elem = d->dtype == SPP_DTYPE_BF16 ? 2 : 4;
+  return round_up(static_cast<size_t>(3) * d->I * d->D * elem, 4096);
+}
+
+spp_status spp_create(const spp_model_desc* desc, void* hip_stream, spp_ctx** out) {
+  return create_impl(desc, hip_stream, out);
+}
+
+spp_status spp_destroy(spp_ctx* ctx) {
+  if (!ctx) return fail(SPP_EINVAL, "ctx is NULL");
+  free_ctx(ctx);
+  return SPP_OK;
+}
+
+spp_status spp_bind_layer(spp_ctx* c, int32_t l, const void* router_w, const void* adapter_a, const void* adapter_b,
+                          const void* proj_w, const void* shared_blobs, const void* host_store) {
+  if (spp_status s = check_layer(c, l, false)) return s;
+  const spp_model_desc& d = c->d;
+  if (!router_w || !host_store) return fail(SPP_EINVAL, "router_w and host_store are required");
+  if ((adapter_a == nullptr) != (adapter_b == nullptr)) return fail(SPP_EINVAL, "adapter_a and adapter_b go together");
+  if (adapter_a && (l == d.L - 1 || d.r == 0)) return fail(SPP_EINVAL, "the last layer (or r == 0) has no adapter");
+  if ((proj_w != nullptr) != (d.has_proj == 1)) return fail(SPP_EINVAL, "proj_w must be given iff has_proj");
+  if ((shared_blobs != nullptr) != (d.n_shared > 0)) return fail(SPP_EINVAL, "shared_blobs must be given iff n_shared > 0");
+  LayerState& ls = c->layers[l];
+  ls.router_w = router_w;
+  ls.A = adapter_a;
+  ls.Bm = adapter_b;
+  ls.proj = proj_w;
+  ls.shared = shared_blobs;
+  ls.host_store = static_cast<const uint8_t*>(host_store);
+  ls.bound = true;
+  return SPP_OK;
+}
+
+spp_status spp_set_resident(spp_ctx* c, int32_t l, const int32_t* experts, int32_t count) {
+  if (spp_status s = check_layer(c, l, true)) return s;
+  LayerState& ls = c->layers[l];
+  spp::SlotPolicy trial(c->d.S, c->d.n);
+  std::string why;
+  if (!trial.set_resident(experts, count, &why)) return fail(SPP_EINVAL, why);
+  if (spp_status s = sync_all(c)) return s;
+  const std::vector<int32_t> before(c->d.S, spp::kEmpty);
+  ls.policy->set_resident(experts, count, &why);
+  ls.pending_prefetch.clear();
+  return fill_slots(c, ls, before);
+}
+
+spp_status spp_set_slot_table(spp_ctx* c, int32_t l, const int32_t* experts, const int64_t* stamps) {
+  if (spp_status s = check_layer(c, l, true)) return s;
+  if (!experts) return fail(SPP_EINVAL, "experts is NULL");
+  LayerState& ls = c->layers[l];
+  spp::SlotPolicy trial(c->d.S, c->d.n);
+  std::string why;
+  if (!trial.set_table(experts, stamps, &why)) return fail(SPP_EINVAL, why);
+  if (spp_status s = sync_all(c)) return s;
+  const std::vector<int32_t> before = ls.policy->slot_experts();
+  ls.policy->set_table(experts, stamps, &why);
+  ls.pending_prefetch.clear();
+  return fill_slots(c, ls, before);
+}
+
+spp_status spp_get_slot_table(spp_ctx* c, int32_t l, int32_t* experts_out, int64_t* stamps_out) {
+  if (spp_status s = check_layer(c, l, false)) return s;
+  const LayerState& ls = c->layers[l];
+  if (experts_out) std::memcpy(experts_out, ls.policy->slot_experts().data(), sizeof(int32_t) * c->d.S);
+  if (stamps_out) std::memcpy(stamps_out, ls.policy->slot_stamps().data(), sizeof(int64_t) * c->d.S);
+  return SPP_OK;
+}
+
+spp_status spp_get_clock(spp_ctx* c, int64_t* tau_out) {
+  if (spp_status s = check_ctx(c)) return s;
+  if (!tau_out) return fail(SPP_EINVAL, "tau_out is NULL");
+  *tau_out = c->clock;
+  return SPP_OK;
+}
+
+spp_status spp_set_clock(spp_ctx* c, int64_t tau) {
+  if (spp_status s = check_ctx(c)) return s;
+  if (tau < 0) return fail(SPP_EINVAL, "tau must be >= 0");
+  c->clock = tau;
+  return SPP_OK;
+}
+
+spp_status adapter_predict(spp_ctx* c, int32_t l, const float* x_dev, int32_t B, float* s_out) {
+  if (spp_status s = check_layer(c, l, true)) return s;
+  const spp_model_desc& d = c->d;
+  LayerState& ls = c->layers[l];
+  if (!x_dev || !s_out) return fail(SPP_EINVAL, "x_dev / s_out is NULL");
+  if (B < 1 || B > d.max_batch) return fail(SPP_EINVAL, "B must be in [1, max_batch]");
+  if (!ls.A || d.r == 0) return fail(SPP_ESTATE, "layer has no adapter");
+  spp::RouterArgs ra{};
+  ra.u = x_dev;
+  ra.A = ls.A;
+  ra.Bm = ls.Bm;
+  ra.zbuf = c->zbuf;
+  ra.s = reinterpret_cast<float*>(c->res_dev + c->off_s);
+  ra.counter = c->counter;
+  ra.B = B;
+  ra.D = d.D;
+  ra.n = d.n;
+  ra.K = d.K;
+  ra.r = d.r;
+  ra.eps = d.rms_eps;
+  ra.x_given = 1;
+  ra.router_on = 0;
+  SPP_HIP(spp::launch_router(ra, d.dtype, c->compute));
+  SPP_HIP(hipMemcpyAsync(c->res_host + c->off_s, c->res_dev + c->off_s, sizeof(float) * d.n,
+                         hipMemcpyDeviceToHost, c->compute));
+  SPP_HIP(hipEventRecord(c->ev_res, c->compute));
+  SPP_HIP(hipEventSynchronize(c->ev_res));
+  std::memcpy(s_out, c->res_host + c->off_s, sizeof(float) * d.n);
+  return SPP_OK;
+}
+
+spp_status select_prefetch_budget(double window_us, double per_expert_cost_us, int32_t n_experts, int32_t* M_max_out) {
+  if (!M_max_out) return fail(SPP_EINVAL, "M_max_out is NULL");
+  if (!spp::prefetch_budget(window_us, per_expert_cost_us, n_experts, M_max_out))
+    return fail(SPP_EINVAL, "window and cost must be finite, cost > 0, n >= 0");
+  return SPP_OK;
+}
+
+spp_status expert_cache_issue_prefetch(spp_ctx* c, int32_t target_layer, const float* s_host, int32_t M_max,
+                                       int32_t* issued_out, int32_t* m_out) {
+  if (spp_status s = check_layer(c, target_layer, true)) return s;
+  if (!s_host || !m_out || (M_max > 0 && !issued_out)) return fail(SPP_EINVAL, "s_host / issued_out / m_out is NULL");
+  if (M_max < 0) return fail(SPP_EINVAL, "M_max must be >= 0");
+  LayerState& ls = c->layers[target_layer];
+  const int64_t tau = ++c->clock;
+  std::vector<spp::Transfer> placed;
+  ls.policy->prefetch(s_host, M_max, tau, &placed);
+  if (spp_status e = issue_copies(c, ls, placed)) return e;
+  ls.pending_prefetch.clear();
+  for (size_t i = 0; i < placed.size(); ++i) {
+    issued_out[i] = placed[i].expert;
+    ls.pending_prefetch.push_back(placed[i].expert);
+  }
+  *m_out = static_cast<int32_t>(placed.size());
+  c->stats.prefetched += *m_out;
+  return SPP_OK;
+}
+
+spp_status moe_layer_forward(spp_ctx* c, int32_t l, const void* h_in_dev, void* h_out_dev, int32_t B, int32_t M_max,
+                             int32_t* topk_out, float* gate_out, spp_layer_stats* stats) {
+  return layer_forward_impl(c, l, h_in_dev, h_out_dev, B, M_max, topk_out, gate_out, stats);
+}
+
+const char* spp_last_error(void) { return g_err.c_str(); }
+
+spp_status spp_get_last_transfers(spp_ctx* c, int32_t* loads_out, int32_t* n_loads, int32_t* pref_out,
+                                  int32_t* n_pref, int32_t cap) {
+  if (spp_status s = check_ctx(c)) return s;
+  if (cap < 0) return fail(SPP_EINVAL, "cap must be >= 0");
+  auto put = [cap](const std::vector<spp::Transfer>& xs, int32_t* out, int32_t* n) {
+    if (n) *n = static_cast<int32_t>(xs.size());
+    if (!out) return;
+    for (size_t i = 0; i < xs.size() && static_cast<int32_t>(i) < cap; ++i) {
+      out[3 * i] = xs[i].expert;
+      out[3 * i + 1] = xs[i].slot;
+      out[3 * i + 2] = xs[i].evicted;
+    }
+  };
+  put(c->last_loads, loads_out, n_loads);
+  put(c->last_pref, pref_out, n_pref);
+  return SPP_OK;
+}
+
+spp_status spp_get_last_priorities(spp_ctx* c, float* s_out) {
+  if (spp_status s = check_ctx(c)) return s;
+  if (!s_out) return fail(SPP_EINVAL, "s_out is NULL");
+  if (!c->last_s_valid) return fail(SPP_ESTATE, "no adapter ran in the last layer call");
+  std::memcpy(s_out, c->last_s.data(), sizeof(float) * c->d.n);
+  return SPP_OK;
+}
+
+spp_status spp_get_last_router_input(spp_ctx* c, float* x_out, int32_t B) {
+  if (spp_status s = check_ctx(c)) return s;
+  if (!x_out || B < 1 || B > c->d.max_batch) return fail(SPP_EINVAL, "bad x_out / B");
+  SPP_HIP(hipStreamSynchronize(c->compute));
+  SPP_HIP(hipMemcpy(x_out, c->x_dev, sizeof(float) * B * c->d.D, hipMemcpyDeviceToHost));
+  return SPP_OK;
+}
+
+spp_status spp_set_timing(spp_ctx* c, int32_t enabled) {
+  if (spp_status s = check_ctx(c)) return s;
+  c->timing = enabled != 0;
+  return SPP_OK;
+}
+
+spp_status spp_get_run_stats(spp_ctx* c, spp_run_stats* out) {
+  if (spp_status s = check_ctx(c)) return s;
+  if (!out) return fail(SPP_EINVAL, "out is NULL");
+  if (spp_status s = sync_all(c)) return s;
+  harvest(c, c->pending_sets.size());
+  *out = c->stats;
+  if (c->have_prev) out->span_us += 1e3 * elapsed(c->prev.ev[kEvStart], c->prev.ev[kEvEnd]);
+  return SPP_OK;
+}
+
+spp_status spp_reset_run_stats(spp_ctx* c) {
+  if (spp_status s = check_ctx(c)) return s;
+  if (spp_status s = sync_all(c)) return s;
+  harvest(c, c->pending_sets.size());
+  if (c->have_prev) {
+    c->free_sets.push_back(c->prev);
+    c->have_prev = false;
+  }
+  c->stats = spp_run_stats{};
+  return SPP_OK;
+}
+
+spp_status spp_profile_expert_copy(spp_ctx* c, int32_t l, int32_t reps, double* per_expert_us) {
+  if (spp_status s = check_layer(c, l, true)) return s;
+  if (reps < 1 || !per_expert_us) return fail(SPP_EINVAL, "reps must be >= 1, per_expert_us non-NULL");
+  if (!c->probe_dev && hipMalloc(&c->probe_dev, c->stride) != hipSuccess) return fail(SPP_ENOMEM, "probe buffer");
+  LayerState& ls = c->layers[l];
+  hipEvent_t e0, e1;
+  SPP_HIP(hipEventCreate(&e0));
+  SPP_HIP(hipEventCreate(&e1));
+  SPP_HIP(hipMemcpyAsync(c->probe_dev, ls.host_store, c->blob_bytes, hipMemcpyHostToDevice, c->copy));
+  SPP_HIP(hipEventRecord(e0, c->copy));
+  for (int32_t i = 0; i < reps; ++i)
+    SPP_HIP(hipMemcpyAsync(c->probe_dev, ls.host_store + static_cast<size_t>(i % c->d.n) * c->stride,
+                           c->blob_bytes, hipMemcpyHostToDevice, c->copy));
+  SPP_HIP(hipEventRecord(e1, c->copy));
+  SPP_HIP(hipEventSynchronize(e1));
+  *per_expert_us = 1e3 * elapsed(e0, e1) / reps;
+  (void)hipEventDestroy(e0);
+  (void)hipEventDestroy(e1);
+  return SPP_OK;
+}
+
+spp_status spp_set_ffn_workgroups(spp_ctx* c, int32_t wgs) {
+  if (spp_status s = check_ctx(c)) return s;
+  if (wgs < 1 || static_cast<size_t>(wgs) > spp::ffn_max_grid()) return fail(SPP_EINVAL, "wgs out of range");
+  spp::set_ffn_target_wgs(wgs);
+  c->ffn_wgs = wgs;
+  return SPP_OK;
+}
+
+// ------------------------------------------------------------ host policy
+
+struct spp_slot_policy {
+  spp::SlotPolicy p;
+  spp_slot_policy(int32_t S, int32_t n) : p(S, n) {}
+};
+
+spp_status spp_policy_create(int32_t S, int32_t n, const int32_t* resident, int32_t count, spp_slot_policy** out) {
+  if (!out || S < 1 || n < 1) return fail(SPP_EINVAL, "S, n must be >= 1 and out non-NULL");
+  std::unique_ptr<spp_slot_policy> p(new (std::nothrow) spp_slot_policy(S, n));
+  if (!p) return fail(SPP_ENOMEM, "host allocation failed");
+  std::string why;
+  if (!p->p.set_resident(resident, count, &why)) return fail(SPP_EINVAL, why);
+  *out = p.release();
+  return SPP_OK;
+}
+
+spp_status spp_policy_destroy(spp_slot_policy* p) {
+  if (!p) return fail(SPP_EINVAL, "policy is NULL");
+  delete p;
+  return SPP_OK;
+}
+
+spp_status spp_policy_on_demand(spp_slot_policy* p, const int32_t* needed, int32_t count, int64_t tau,
+                                int32_t* loads_out, int32_t* n_loads) {
+  if (!p || (count > 0 && !needed) || count < 0 || !n_loads) return fail(SPP_EINVAL, "bad arguments");
+  std::vector<spp::Transfer> loads;
+  std::string why;
+  if (!p->p.on_demand(needed, count, tau, &loads, &why)) return fail(SPP_EINVAL, why);
+  *n_loads = static_cast<int32_t>(loads.size());
+  for (size_t i = 0; i < loads.size() && loads_out; ++i) {
+    loads_out[3 * i] = loads[i].expert;
+    loads_out[3 * i + 1] = loads[i].slot;
+    loads_out[3 * i + 2] = loads[i].evicted;
+  }
+  return SPP_OK;
+}
+
+spp_status spp_policy_prefetch(spp_slot_policy* p, const float* s, int32_t M_max, int64_t tau, int32_t* placed_out,
+                               int32_t* n_placed) {
+  if (!p || !s || !n_placed || M_max < 0) return fail(SPP_EINVAL, "bad arguments");
+  std::vector<spp::Transfer> placed;
+  p->p.prefetch(s, M_max, tau, &placed);
+  *n_placed = static_cast<int32_t>(placed.size());
+  for (size_t i = 0; i < placed.size() && placed_out; ++i) {
+    placed_out[3 * i] = placed[i].expert;
+    placed_out[3 * i + 1] = placed[i].slot;
+    placed_out[3 * i + 2] = placed[i].evicted;
+  }
+  return SPP_OK;
+}
+
+spp_status spp_policy_get(spp_slot_policy* p, int32_t* experts_out, int64_t* stamps_out) {
+  if (!p) return fail(SPP_EINVAL, "policy is NULL");
+  if (experts_out) std::memcpy(experts_out, p->p.slot_experts().data(), sizeof(int32_t) * p->p.S());
+  if (stamps_out) std::memcpy(stamps_out, p->p.slot_stamps().data(), sizeof(int64_t) * p->p.S());
+  return SPP_OK;
+}
+
+}  // extern "C"

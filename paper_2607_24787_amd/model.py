@@ -1,0 +1,166 @@
+"""Assemble a synthetic offloaded-MoE decode stack on the device and drive it.
+
+PyTorch is used for device memory, pinned host memory and the compute stream
+only; every step of the hot path runs in libspp (see ``spp.py``).  Expert
+weights are packed into the library's blob layout (unit i = [gate row i | up
+row i | down column i]) inside one pinned host store per layer: the offload
+tier.  Router, adapter, stand-in projection and shared-expert weights are
+resident in HBM.
+"""
+from __future__ import annotations
+
+import os
+from concurrent.futures import ThreadPoolExecutor
+from typing import Optional, Sequence
+
+import numpy as np
+
+from . import spp
+
+
+def pack_blob(Wg: np.ndarray, Wu: np.ndarray, Wd: np.ndarray) -> np.ndarray:
+    """[I, 3, D] interleave of gate rows, up rows and down columns (storage dtype kept)."""
+    I, D = Wg.shape
+    out = np.empty((I, 3, D), dtype=Wg.dtype)
+    out[:, 0, :] = Wg
+    out[:, 1, :] = Wu
+    out[:, 2, :] = Wd.T
+    return out
+
+
+def _torch_from_storage(a: np.ndarray, device):
+    import torch
+    if a.dtype == np.uint16:
+        return torch.from_numpy(np.ascontiguousarray(a).view(np.int16)).to(device)
+    return torch.from_numpy(np.ascontiguousarray(a, dtype=np.float32)).to(device)
+
+
+class OffloadedMoEStack:
+    """One spp context over a whole synthetic stack (all L layers).
+
+    ``adapter_values(l) -> (A, B)`` optionally replaces the seeded adapters
+    (values, rounded to the storage dtype here) for router-preservation tests.
+    """
+
+    def __init__(self, cfg, device: str = "cuda:0", S: Optional[int] = None,
+                 resident: Optional[Sequence[int]] = None, adapter_values=None,
+                 threads: Optional[int] = None, host_layers: Optional[int] = None):
+        import torch
+        from workload import gen
+
+        self.cfg = cfg
+        self.torch = torch
+        self.device = torch.device(device)
+        torch.cuda.set_device(self.device)
+        self.stream = torch.cuda.current_stream(self.device)
+        self.S = cfg.S if S is None else S
+        self.dtype_code = spp.DTYPE_BF16 if cfg.dtype == "bf16" else spp.DTYPE_F32
+        self.desc = spp.make_desc(cfg.L, cfg.D, cfg.n, cfg.K, cfg.I, cfg.r, self.S, max_batch=cfg.batch,
+                                  n_shared=cfg.n_shared, dtype=self.dtype_code, has_proj=cfg.has_proj,
+                                  rms_eps=cfg.rms_eps)
+        self.stride = spp.spp_blob_stride(self.desc)
+        self.elem = cfg.elem_bytes
+        # host_layers < L reuses host stores cyclically (tied offload tier) to bound pinned memory
+        self.host_layers = cfg.L if host_layers is None else max(1, min(host_layers, cfg.L))
+        threads = threads or min(16, os.cpu_count() or 1)
+
+        self.router, self.adapter, self.proj, self.shared, self.host = [], [], [], [], []
+        for l in range(cfg.L):
+            self.router.append(_torch_from_storage(gen.router_weight(cfg, l), self.device))
+            if l < cfg.L - 1 and cfg.r > 0:
+                if adapter_values is not None:
+                    A, B = adapter_values(l)
+                    A, B = self._to_storage(A), self._to_storage(B)
+                else:
+                    A, B = gen.adapter_weights(cfg, l)
+                self.adapter.append((_torch_from_storage(A, self.device), _torch_from_storage(B, self.device)))
+            else:
+                self.adapter.append(None)
+            self.proj.append(_torch_from_storage(gen.proj_weight(cfg, l), self.device) if cfg.has_proj else None)
+            if cfg.n_shared:
+                buf = np.zeros(cfg.n_shared * self.stride, dtype=np.uint8)
+                for j in range(cfg.n_shared):
+                    blob = pack_blob(*gen.shared_expert_weights(cfg, l, j))
+                    buf[j * self.stride: j * self.stride + blob.nbytes] = blob.reshape(-1).view(np.uint8)
+                self.shared.append(torch.from_numpy(buf).to(self.device))
+            else:
+                self.shared.append(None)
+
+        # offload tier: pinned host stores, blobs packed in parallel
+        for hl in range(self.host_layers):
+            self.host.append(torch.empty(cfg.n * self.stride, dtype=torch.uint8, pin_memory=True))
+        views = [h.numpy() for h in self.host]
+
+        def fill(job):
+            hl, e = job
+            blob = pack_blob(*gen.expert_weights(cfg, hl, e)).reshape(-1).view(np.uint8)
+            views[hl][e * self.stride: e * self.stride + blob.nbytes] = blob
+
+        jobs = [(hl, e) for hl in range(self.host_layers) for e in range(cfg.n)]
+        with ThreadPoolExecutor(max_workers=threads) as ex:
+            list(ex.map(fill, jobs))
+
+        self.ctx = spp.spp_create(self.desc, self.stream.cuda_stream)
+        for l in range(cfg.L):
+            ad = self.adapter[l]
+            spp.spp_bind_layer(self.ctx, l, self.router[l].data_ptr(),
+                               ad[0].data_ptr() if ad else 0, ad[1].data_ptr() if ad else 0,
+                               self.proj[l].data_ptr() if self.proj[l] is not None else 0,
+                               self.shared[l].data_ptr() if self.shared[l] is not None else 0,
+                               self.host[l % self.host_layers].data_ptr())
+        res = list(range(min(self.S, cfg.n))) if resident is None else list(resident)
+        for l in range(cfg.L):
+            spp.spp_set_resident(self.ctx, l, res)
+        # ping-pong hidden-state buffers [B, D] in the storage dtype
+        nbytes = cfg.batch * cfg.D * self.elem
+        self.hbuf = [torch.empty(nbytes, dtype=torch.uint8, device=self.device) for _ in range(2)]
+
+    def _to_storage(self, v):
+        from workload.gen import f32_to_bf16_bits
+        v = np.asarray(v, dtype=np.float32)
+        return f32_to_bf16_bits(v) if self.cfg.dtype == "bf16" else v
+
+    # ---------------------------------------------------------------- data
+
+    def upload_hidden(self, h_storage: np.ndarray, buf: int = 0):
+        """Copy stored hidden states [B, D] into ping-pong buffer ``buf``."""
+        a = np.ascontiguousarray(h_storage).reshape(-1).view(np.uint8)
+        self.hbuf[buf].copy_(self.torch.from_numpy(a.copy()))
+        return self.hbuf[buf]
+
+    def download(self, t, B: Optional[int] = None) -> np.ndarray:
+        B = self.cfg.batch if B is None else B
+        self.torch.cuda.synchronize(self.device)
+        raw = t[: B * self.cfg.D * self.elem].cpu().numpy()
+        dt = np.uint16 if self.cfg.dtype == "bf16" else np.float32
+        return raw.view(dt).reshape(B, self.cfg.D).copy()
+
+    # ------------------------------------------------------------- compute
+
+    def layer(self, l: int, src: int, dst: int, M_max: int, B: Optional[int] = None):
+        B = self.cfg.batch if B is None else B
+        return spp.moe_layer_forward(self.ctx, l, self.hbuf[src].data_ptr(), self.hbuf[dst].data_ptr(), B,
+                                     self.cfg.K, M_max)
+
+    def step(self, h_storage: Optional[np.ndarray], M_max: int, B: Optional[int] = None):
+        """One decode step through all layers; returns the per-layer (topk, gates, stats)."""
+        if h_storage is not None:
+            self.upload_hidden(h_storage, 0)
+        out = []
+        src = 0
+        for l in range(self.cfg.L):
+            out.append(self.layer(l, src, 1 - src, M_max, B))
+            src = 1 - src
+        self.last_buf = src
+        return out
+
+    def close(self):
+        if getattr(self, "ctx", None):
+            spp.spp_destroy(self.ctx)
+            self.ctx = None
+
+    def __del__(self):
+        try:
+            self.close()
+        except Exception:
+            pass

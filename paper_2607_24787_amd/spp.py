@@ -1,0 +1,306 @@
+"""ctypes binding of libspp.so (the C ABI declared in include/spp.h).
+
+Argument marshalling only: every step of the hot path runs in the HIP library.
+Pointers are passed as Python ints (device or pinned-host addresses); numpy
+arrays carry small host inputs and outputs.  The library must have been built
+(``python -m paper_2607_24787_amd.build``); loading fails loudly otherwise.
+"""
+from __future__ import annotations
+
+import ctypes
+import os
+from ctypes import POINTER, byref, c_char_p, c_double, c_float, c_int32, c_int64, c_size_t, c_void_p
+
+import numpy as np
+
+LIB_PATH = os.path.join(os.path.dirname(os.path.abspath(__file__)), "libspp.so")
+
+SPP_OK, SPP_EINVAL, SPP_ENOMEM, SPP_EHIP, SPP_ESTATE = 0, -1, -2, -3, -4
+DTYPE_F32, DTYPE_BF16 = 0, 1
+
+
+class SppError(RuntimeError):
+    def __init__(self, status: int, msg: str):
+        super().__init__(f"spp status {status}: {msg}")
+        self.status = status
+
+
+class ModelDesc(ctypes.Structure):
+    _fields_ = [(f, c_int32) for f in ("L", "D", "n", "K", "I", "r", "n_shared", "S", "max_batch", "dtype",
+                                       "has_proj")] + [("rms_eps", c_float)]
+
+
+class LayerStats(ctypes.Structure):
+    _fields_ = [(f, c_int32) for f in ("hits", "misses", "prefetched", "prefetch_used", "ready_on_time")]
+
+
+class RunStats(ctypes.Structure):
+    _fields_ = ([(f, c_int64) for f in ("layer_calls", "hits", "misses", "prefetched", "prefetch_used",
+                                         "ready_on_time", "copies", "copy_bytes", "ffn_launches",
+                                         "window_samples")]
+                + [(f, c_double) for f in ("router_us", "exposed_us", "ffn_us", "tail_us", "span_us",
+                                           "window_us")])
+
+    def as_dict(self):
+        return {f: getattr(self, f) for f, _ in self._fields_}
+
+
+_SIGS = {
+    "spp_blob_stride": (c_size_t, [POINTER(ModelDesc)]),
+    "spp_create": (c_int32, [POINTER(ModelDesc), c_void_p, POINTER(c_void_p)]),
+    "spp_destroy": (c_int32, [c_void_p]),
+    "spp_bind_layer": (c_int32, [c_void_p, c_int32, c_void_p, c_void_p, c_void_p, c_void_p, c_void_p, c_void_p]),
+    "spp_set_resident": (c_int32, [c_void_p, c_int32, POINTER(c_int32), c_int32]),
+    "adapter_predict": (c_int32, [c_void_p, c_int32, c_void_p, c_int32, POINTER(c_float)]),
+    "select_prefetch_budget": (c_int32, [c_double, c_double, c_int32, POINTER(c_int32)]),
+    "expert_cache_issue_prefetch": (c_int32, [c_void_p, c_int32, POINTER(c_float), c_int32, POINTER(c_int32),
+                                              POINTER(c_int32)]),
+    "moe_layer_forward": (c_int32, [c_void_p, c_int32, c_void_p, c_void_p, c_int32, c_int32, POINTER(c_int32),
+                                    POINTER(c_float), POINTER(LayerStats)]),
+    "spp_last_error": (c_char_p, []),
+    "spp_get_slot_table": (c_int32, [c_void_p, c_int32, POINTER(c_int32), POINTER(c_int64)]),
+    "spp_set_slot_table": (c_int32, [c_void_p, c_int32, POINTER(c_int32), POINTER(c_int64)]),
+    "spp_get_clock": (c_int32, [c_void_p, POINTER(c_int64)]),
+    "spp_set_clock": (c_int32, [c_void_p, c_int64]),
+    "spp_get_last_transfers": (c_int32, [c_void_p, POINTER(c_int32), POINTER(c_int32), POINTER(c_int32),
+                                         POINTER(c_int32), c_int32]),
+    "spp_get_last_priorities": (c_int32, [c_void_p, POINTER(c_float)]),
+    "spp_get_last_router_input": (c_int32, [c_void_p, POINTER(c_float), c_int32]),
+    "spp_set_timing": (c_int32, [c_void_p, c_int32]),
+    "spp_get_run_stats": (c_int32, [c_void_p, POINTER(RunStats)]),
+    "spp_reset_run_stats": (c_int32, [c_void_p]),
+    "spp_profile_expert_copy": (c_int32, [c_void_p, c_int32, c_int32, POINTER(c_double)]),
+    "spp_set_ffn_workgroups": (c_int32, [c_void_p, c_int32]),
+    "spp_policy_create": (c_int32, [c_int32, c_int32, POINTER(c_int32), c_int32, POINTER(c_void_p)]),
+    "spp_policy_destroy": (c_int32, [c_void_p]),
+    "spp_policy_on_demand": (c_int32, [c_void_p, POINTER(c_int32), c_int32, c_int64, POINTER(c_int32),
+                                       POINTER(c_int32)]),
+    "spp_policy_prefetch": (c_int32, [c_void_p, POINTER(c_float), c_int32, c_int64, POINTER(c_int32),
+                                      POINTER(c_int32)]),
+    "spp_policy_get": (c_int32, [c_void_p, POINTER(c_int32), POINTER(c_int64)]),
+}
+
+_lib = None
+
+
+def lib() -> ctypes.CDLL:
+    """The loaded library; raises if it has not been built."""
+    global _lib
+    if _lib is None:
+        if not os.path.exists(LIB_PATH):
+            raise RuntimeError(f"{LIB_PATH} is missing: build it with `python -m paper_2607_24787_amd.build`")
+        L = ctypes.CDLL(LIB_PATH)
+        for name, (res, args) in _SIGS.items():
+            fn = getattr(L, name)
+            fn.restype, fn.argtypes = res, args
+        _lib = L
+    return _lib
+
+
+def exported_symbols():
+    return list(_SIGS)
+
+
+def _check(status: int):
+    if status != SPP_OK:
+        raise SppError(status, lib().spp_last_error().decode())
+
+
+def _i32(a):
+    a = np.ascontiguousarray(a, dtype=np.int32)
+    return a, a.ctypes.data_as(POINTER(c_int32))
+
+
+def _f32(a):
+    a = np.ascontiguousarray(a, dtype=np.float32)
+    return a, a.ctypes.data_as(POINTER(c_float))
+
+
+def _i64(a):
+    a = np.ascontiguousarray(a, dtype=np.int64)
+    return a, a.ctypes.data_as(POINTER(c_int64))
+
+
+# ------------------------------------------------------------------ lifecycle
+
+def make_desc(L, D, n, K, I, r, S, max_batch=1, n_shared=0, dtype=DTYPE_BF16, has_proj=0, rms_eps=1e-6):
+    return ModelDesc(L, D, n, K, I, r, n_shared, S, max_batch, dtype, int(has_proj), rms_eps)
+
+
+def spp_blob_stride(desc: ModelDesc) -> int:
+    return int(lib().spp_blob_stride(byref(desc)))
+
+
+def spp_create(desc: ModelDesc, stream: int = 0) -> int:
+    out = c_void_p()
+    _check(lib().spp_create(byref(desc), c_void_p(stream), byref(out)))
+    return out.value
+
+
+def spp_destroy(ctx: int):
+    _check(lib().spp_destroy(c_void_p(ctx)))
+
+
+def spp_bind_layer(ctx, l, router_w, adapter_a, adapter_b, proj_w, shared_blobs, host_store):
+    _check(lib().spp_bind_layer(c_void_p(ctx), l, c_void_p(router_w or None), c_void_p(adapter_a or None),
+                                c_void_p(adapter_b or None), c_void_p(proj_w or None),
+                                c_void_p(shared_blobs or None), c_void_p(host_store or None)))
+
+
+def spp_set_resident(ctx, l, experts):
+    a, p = _i32(experts)
+    _check(lib().spp_set_resident(c_void_p(ctx), l, p, len(a)))
+
+
+# --------------------------------------------------------------- the four calls
+
+def adapter_predict(ctx, l, x_dev: int, B: int, n: int) -> np.ndarray:
+    s = np.zeros(n, dtype=np.float32)
+    _check(lib().adapter_predict(c_void_p(ctx), l, c_void_p(x_dev), B, s.ctypes.data_as(POINTER(c_float))))
+    return s
+
+
+def select_prefetch_budget(window_us: float, per_expert_cost_us: float, n_experts: int) -> int:
+    m = c_int32()
+    _check(lib().select_prefetch_budget(window_us, per_expert_cost_us, n_experts, byref(m)))
+    return m.value
+
+
+def expert_cache_issue_prefetch(ctx, target_layer, s, M_max):
+    s, ps = _f32(s)
+    issued = np.zeros(max(M_max, 1), dtype=np.int32)
+    m = c_int32()
+    _check(lib().expert_cache_issue_prefetch(c_void_p(ctx), target_layer, ps, M_max,
+                                             issued.ctypes.data_as(POINTER(c_int32)), byref(m)))
+    return issued[:m.value].tolist()
+
+
+def moe_layer_forward(ctx, l, h_in_dev: int, h_out_dev: int, B: int, K: int, M_max: int):
+    """Returns (topk int32 [B,K], gates fp32 [B,K], LayerStats)."""
+    topk = np.zeros((B, K), dtype=np.int32)
+    gates = np.zeros((B, K), dtype=np.float32)
+    st = LayerStats()
+    _check(lib().moe_layer_forward(c_void_p(ctx), l, c_void_p(h_in_dev), c_void_p(h_out_dev), B, M_max,
+                                   topk.ctypes.data_as(POINTER(c_int32)), gates.ctypes.data_as(POINTER(c_float)),
+                                   byref(st)))
+    return topk, gates, st
+
+
+def spp_last_error() -> str:
+    return lib().spp_last_error().decode()
+
+
+# ----------------------------------------------------------------- inspection
+
+def spp_get_slot_table(ctx, l, S):
+    e = np.zeros(S, dtype=np.int32)
+    t = np.zeros(S, dtype=np.int64)
+    _check(lib().spp_get_slot_table(c_void_p(ctx), l, e.ctypes.data_as(POINTER(c_int32)),
+                                    t.ctypes.data_as(POINTER(c_int64))))
+    return e, t
+
+
+def spp_set_slot_table(ctx, l, experts, stamps):
+    e, pe = _i32(experts)
+    t, pt = _i64(stamps)
+    _check(lib().spp_set_slot_table(c_void_p(ctx), l, pe, pt))
+
+
+def spp_get_clock(ctx) -> int:
+    t = c_int64()
+    _check(lib().spp_get_clock(c_void_p(ctx), byref(t)))
+    return t.value
+
+
+def spp_set_clock(ctx, tau: int):
+    _check(lib().spp_set_clock(c_void_p(ctx), tau))
+
+
+def spp_get_last_transfers(ctx, cap: int = 1024):
+    loads = np.zeros(3 * cap, dtype=np.int32)
+    pref = np.zeros(3 * cap, dtype=np.int32)
+    nl, npf = c_int32(), c_int32()
+    _check(lib().spp_get_last_transfers(c_void_p(ctx), loads.ctypes.data_as(POINTER(c_int32)), byref(nl),
+                                        pref.ctypes.data_as(POINTER(c_int32)), byref(npf), cap))
+    tri = lambda a, k: [tuple(int(v) for v in a[3 * i:3 * i + 3]) for i in range(min(k, cap))]
+    return tri(loads, nl.value), tri(pref, npf.value)
+
+
+def spp_get_last_priorities(ctx, n):
+    s = np.zeros(n, dtype=np.float32)
+    _check(lib().spp_get_last_priorities(c_void_p(ctx), s.ctypes.data_as(POINTER(c_float))))
+    return s
+
+
+def spp_get_last_router_input(ctx, B, D):
+    x = np.zeros((B, D), dtype=np.float32)
+    _check(lib().spp_get_last_router_input(c_void_p(ctx), x.ctypes.data_as(POINTER(c_float)), B))
+    return x
+
+
+def spp_set_timing(ctx, enabled: bool):
+    _check(lib().spp_set_timing(c_void_p(ctx), int(bool(enabled))))
+
+
+def spp_get_run_stats(ctx) -> RunStats:
+    st = RunStats()
+    _check(lib().spp_get_run_stats(c_void_p(ctx), byref(st)))
+    return st
+
+
+def spp_reset_run_stats(ctx):
+    _check(lib().spp_reset_run_stats(c_void_p(ctx)))
+
+
+def spp_profile_expert_copy(ctx, l, reps) -> float:
+    us = c_double()
+    _check(lib().spp_profile_expert_copy(c_void_p(ctx), l, reps, byref(us)))
+    return us.value
+
+
+def spp_set_ffn_workgroups(ctx, wgs: int):
+    _check(lib().spp_set_ffn_workgroups(c_void_p(ctx), wgs))
+
+
+# ------------------------------------------------------- host policy (no GPU)
+
+class SlotPolicy:
+    """Host-only replacement / prefetch-selection policy (same code the context runs)."""
+
+    def __init__(self, S, n, resident=()):
+        self._h = None
+        self.S, self.n = S, n
+        a, p = _i32(list(resident))
+        out = c_void_p()
+        _check(lib().spp_policy_create(S, n, p, len(a), byref(out)))
+        self._h = out.value
+
+    def close(self):
+        if getattr(self, "_h", None):
+            _check(lib().spp_policy_destroy(c_void_p(self._h)))
+            self._h = None
+
+    __del__ = close
+
+    def on_demand(self, needed, tau):
+        a, p = _i32(list(needed))
+        out = np.zeros(3 * self.S, dtype=np.int32)
+        k = c_int32()
+        _check(lib().spp_policy_on_demand(c_void_p(self._h), p, len(a), tau, out.ctypes.data_as(POINTER(c_int32)),
+                                          byref(k)))
+        return [tuple(int(v) for v in out[3 * i:3 * i + 3]) for i in range(k.value)]
+
+    def prefetch(self, s, M_max, tau):
+        s, ps = _f32(s)
+        out = np.zeros(3 * max(M_max, 1), dtype=np.int32)
+        k = c_int32()
+        _check(lib().spp_policy_prefetch(c_void_p(self._h), ps, M_max, tau, out.ctypes.data_as(POINTER(c_int32)),
+                                         byref(k)))
+        return [tuple(int(v) for v in out[3 * i:3 * i + 3]) for i in range(k.value)]
+
+    def table(self):
+        e = np.zeros(self.S, dtype=np.int32)
+        t = np.zeros(self.S, dtype=np.int64)
+        _check(lib().spp_policy_get(c_void_p(self._h), e.ctypes.data_as(POINTER(c_int32)),
+                                    t.ctypes.data_as(POINTER(c_int64))))
+        return e, t

@@ -1,0 +1,192 @@
+"""Device parity: libspp (HIP on gfx950) against the CPU oracle, through the C ABI.
+
+Lock-step (see lockstep.py): bit-exact selected experts, on-demand loads,
+prefetch sets, slot tables and stamps; layer outputs within 2e-2 (bf16) /
+1e-4 (fp32) max relative error, and elementwise within one storage ulp plus
+1e-6 of the output's largest magnitude.
+"""
+import sys
+
+import numpy as np
+import pytest
+
+import oracle as o
+import workload as w
+from workload import gen
+
+pytestmark = pytest.mark.gpu
+
+
+def _log(msg):
+    print(msg, flush=True)
+    sys.stdout.flush()
+
+
+@pytest.fixture(scope="module")
+def torch_cuda():
+    import torch
+    if not torch.cuda.is_available():
+        pytest.skip("no GPU")
+    return torch
+
+
+def _stack(cfg, **kw):
+    from paper_2607_24787_amd.model import OffloadedMoEStack
+    return OffloadedMoEStack(cfg, **kw)
+
+
+RAGGED = w.MoEConfig(name="ragged_bf16_D640_n40_k5", L=3, D=640, n=40, K=5, I=100, r=12, S=11, windows=(2,),
+                     tokens=16, seed=3)
+PROJ = w.MoEConfig(name="proj_bf16_D512_n16_k4", L=3, D=512, n=16, K=4, I=128, r=8, S=8, windows=(2,),
+                   tokens=10, has_proj=True, seed=5)
+BATCH = w.MoEConfig(name="batch3_f32_D128_n12_k3", L=2, D=128, n=12, K=3, I=64, r=8, S=12, windows=(2,),
+                    tokens=8, batch=3, dtype="f32", seed=9)
+C3_SHORT = w.get("c3").with_(L=3, tokens=6)
+
+
+def _assert_report(rep, cfg, name):
+    from lockstep import LockstepReport  # noqa: F401
+    _log(f"[{name}] layers={rep.layers} exempt={len(rep.exempt)} max_rel_h={rep.max_rel_h:.3g} "
+         f"max_ulp_h={rep.max_ulp_h:.3g} g={rep.max_err_g:.3g} s={rep.max_err_s:.3g} x={rep.max_err_x:.3g}")
+    # one storage ulp plus fp32 accumulation slack (1e-6 of the output scale) per element
+    assert rep.max_ulp_h <= 1.0 + 1e-9, "an output element differs by more than one storage ulp"
+    assert rep.max_err_g <= 1e-5
+    assert len(rep.exempt) <= max(1, rep.layers // 100)
+
+
+@pytest.mark.parametrize("cfg,M_max,tokens", [
+    (w.get("c0"), 1, 64),
+    (w.get("c0"), 3, 16),
+    (RAGGED, 2, 16),
+    (PROJ, 2, 10),
+    (BATCH, 2, 8),
+    (C3_SHORT, 2, 6),
+], ids=["c0_M1", "c0_M3", "ragged", "proj", "batch3", "c3_short"])
+def test_lockstep_parity(torch_cuda, cfg, M_max, tokens):
+    from lockstep import run_lockstep
+    _log(f"[lockstep] {cfg.name} M_max={M_max} tokens={tokens}")
+    st = _stack(cfg)
+    try:
+        rep = run_lockstep(st, cfg, tokens, M_max)
+    finally:
+        st.close()
+    _assert_report(rep, cfg, cfg.name)
+
+
+def test_lockstep_parity_qwen_layer_full_size(torch_cuda):
+    """The 128-expert, top-8, D=2048 bf16 layer pair at full size, in the launch
+    configuration the benchmark times (default FFN workgroups)."""
+    from lockstep import run_lockstep
+    cfg = w.get("c1")
+    _log(f"[lockstep] {cfg.name} full size, 10 tokens")
+    st = _stack(cfg)
+    try:
+        rep = run_lockstep(st, cfg, 10, cfg.window)
+    finally:
+        st.close()
+    _assert_report(rep, cfg, cfg.name)
+
+
+@pytest.mark.parametrize("cfg", [w.get("c0"), RAGGED], ids=["c0", "ragged"])
+def test_router_preservation_on_device(torch_cuda, cfg):
+    """Free-running decode: outputs bitwise identical for every budget, slot count and adapter."""
+    _log(f"[preservation] {cfg.name}")
+    h0 = gen.hidden_states(cfg, tokens=12)
+    rng = np.random.default_rng(0)
+
+    def run(S, M, adapter_values=None):
+        st = _stack(cfg, S=S, adapter_values=adapter_values)
+        try:
+            outs = []
+            for t in range(h0.shape[0]):
+                st.step(h0[t], M)
+                outs.append(st.download(st.hbuf[st.last_buf]))
+            return np.stack(outs)
+        finally:
+            st.close()
+
+    ref = run(cfg.S, -1)
+    W = o.OracleWeights(cfg)
+    variants = [(cfg.S, 0, None), (cfg.S, 1, None), (cfg.S, 2, None), (cfg.S, cfg.n, None),
+                (cfg.n, 2, None), (max(cfg.K, 2), 1, None),
+                (cfg.S, 2, lambda l: (np.zeros((cfg.r, cfg.D)), np.zeros((cfg.n, cfg.r)))),
+                (cfg.S, 2, lambda l: (W.adapter(l)[0], -W.adapter(l)[1])),
+                (cfg.S, 3, lambda l: (rng.normal(size=(cfg.r, cfg.D)), rng.normal(size=(cfg.n, cfg.r))))]
+    for S, M, ad in variants:
+        out = run(S, M, ad)
+        assert np.array_equal(out, ref), (S, M)
+
+
+def test_adapter_predict_against_oracle(torch_cuda):
+    import torch
+    from paper_2607_24787_amd import spp
+    cfg = BATCH.with_(dtype="bf16", D=256, batch=4)
+    st = _stack(cfg)
+    try:
+        rng = np.random.default_rng(1)
+        for B in (1, 3, 4):
+            x = rng.normal(size=(B, cfg.D)).astype(np.float32)
+            xd = torch.from_numpy(x).to(st.device)
+            s = spp.adapter_predict(st.ctx, 0, xd.data_ptr(), B, cfg.n)
+            A, Bm = o.OracleWeights(cfg).adapter(0)
+            _, _, s_ref = o.adapter_scores(A, Bm, x.astype(np.float64))
+            np.testing.assert_allclose(s, s_ref, rtol=1e-5, atol=2e-6)
+            assert abs(float(s.sum()) - B) < 1e-4
+        with pytest.raises(spp.SppError) as e:
+            spp.adapter_predict(st.ctx, cfg.L - 1, xd.data_ptr(), 1, cfg.n)    # last layer: no adapter
+        assert e.value.status == spp.SPP_ESTATE
+    finally:
+        st.close()
+
+
+def test_issue_prefetch_against_oracle(torch_cuda):
+    from paper_2607_24787_amd import spp
+    cfg = RAGGED
+    st = _stack(cfg)
+    try:
+        ora = o.SlotCache(cfg.S, cfg.n, list(range(cfg.S)))
+        rng = np.random.default_rng(2)
+        tau = spp.spp_get_clock(st.ctx)
+        for it in range(12):
+            s = (rng.integers(0, 8, size=cfg.n) / 7).astype(np.float32)
+            M = int(rng.integers(0, 6))
+            tau += 1
+            got = spp.expert_cache_issue_prefetch(st.ctx, 1, s, M)
+            want = ora.prefetch(o.select_prefetch(s.astype(np.float64), ora.occupied(), M), tau)
+            assert got == [e for e, _, _ in want]
+            e, t = spp.spp_get_slot_table(st.ctx, 1, cfg.S)
+            assert e.tolist() == ora.expert.tolist() and t.tolist() == ora.stamp.tolist()
+    finally:
+        st.close()
+
+
+def test_error_paths_on_device(torch_cuda):
+    from paper_2607_24787_amd import spp
+    cfg = RAGGED
+    st = _stack(cfg)
+    try:
+        h0 = gen.hidden_states(cfg, tokens=1)
+        st.upload_hidden(h0[0], 0)
+        with pytest.raises(spp.SppError) as e:
+            spp.moe_layer_forward(st.ctx, 0, st.hbuf[0].data_ptr(), st.hbuf[0].data_ptr(), 1, cfg.K, 1)
+        assert e.value.status == spp.SPP_EINVAL          # aliasing in/out
+        with pytest.raises(spp.SppError):
+            spp.moe_layer_forward(st.ctx, cfg.L, st.hbuf[0].data_ptr(), st.hbuf[1].data_ptr(), 1, cfg.K, 1)
+        with pytest.raises(spp.SppError):
+            spp.moe_layer_forward(st.ctx, 0, st.hbuf[0].data_ptr(), st.hbuf[1].data_ptr(), 2, cfg.K, 1)
+        with pytest.raises(spp.SppError):
+            spp.spp_set_resident(st.ctx, 0, [0, 0])
+        # a slot count below the batch demand is refused at the first layer call
+        small = _stack(cfg, S=cfg.K - 1, resident=[])
+        try:
+            small.upload_hidden(h0[0], 0)
+            with pytest.raises(spp.SppError) as e:
+                small.layer(0, 0, 1, 1)
+            assert e.value.status == spp.SPP_ESTATE
+        finally:
+            small.close()
+        # the context still works after refused calls
+        topk, _, _ = st.layer(0, 0, 1, 1)
+        assert topk.shape == (1, cfg.K)
+    finally:
+        st.close()

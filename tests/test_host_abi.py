@@ -1,0 +1,115 @@
+"""Host-side checks of libspp without a GPU: exports, budget rule, replacement policy.
+
+The native slot policy (the same object every device context runs per layer)
+is compared bit-exactly with the oracle's logical slot cache on random traces.
+"""
+import ctypes
+import math
+import os
+import re
+
+import numpy as np
+import pytest
+
+import oracle as o
+from paper_2607_24787_amd import spp
+
+ROOT = os.path.dirname(os.path.dirname(os.path.abspath(__file__)))
+
+
+def _declared_functions():
+    text = open(os.path.join(ROOT, "include", "spp.h")).read()
+    text = re.sub(r"/\*.*?\*/", "", text, flags=re.S)
+    names = re.findall(r"^\s*(?:const\s+)?[a-z_0-9]+\s*\*?\s*([a-z_0-9]+)\s*\(", text, flags=re.M)
+    return sorted(set(names))
+
+
+def test_library_exports_every_declared_symbol():
+    L = spp.lib()
+    declared = _declared_functions()
+    assert len(declared) >= 25
+    for name in declared:
+        assert hasattr(L, name), name
+    assert set(declared) == set(spp.exported_symbols())
+
+
+def test_select_prefetch_budget_matches_oracle_rule():
+    rng = np.random.default_rng(0)
+    cases = [(300.0, 150.0, 128), (299.9, 150.0, 128), (0.0, 1.0, 8), (-3.0, 1.0, 8), (1e9, 1.0, 64)]
+    cases += [(float(rng.uniform(-50, 2000)), float(rng.uniform(0.5, 400)), int(rng.integers(0, 200)))
+              for _ in range(300)]
+    for W, c, n in cases:
+        assert spp.select_prefetch_budget(W, c, n) == o.prefetch_budget(W, c, n)
+    for W, c, n in [(1.0, 0.0, 8), (1.0, -2.0, 8), (math.nan, 1.0, 8), (1.0, math.inf, 8), (math.inf, 1.0, 8),
+                    (1.0, 1.0, -1)]:
+        with pytest.raises(spp.SppError) as e:
+            spp.select_prefetch_budget(W, c, n)
+        assert e.value.status == spp.SPP_EINVAL
+        assert "finite" in spp.spp_last_error()
+
+
+@pytest.mark.parametrize("seed", range(25))
+def test_native_policy_matches_oracle_slot_cache(seed):
+    rng = np.random.default_rng(seed)
+    n = int(rng.integers(4, 40))
+    S = int(rng.integers(1, n + 1))
+    resident = list(rng.permutation(n)[: int(rng.integers(0, S + 1))])
+    nat = spp.SlotPolicy(S, n, resident)
+    ora = o.SlotCache(S, n, resident)
+    tau = 0
+    for step in range(60):
+        tau += 1
+        k = int(rng.integers(1, S + 1))
+        need = list(rng.integers(0, n, size=k))          # duplicates allowed
+        if len(set(need)) > S:
+            with pytest.raises(spp.SppError):
+                nat.on_demand(need, tau)
+            continue
+        assert nat.on_demand(need, tau) == ora.on_demand(need, tau)
+        e, t = nat.table()
+        assert e.tolist() == ora.expert.tolist() and t.tolist() == ora.stamp.tolist()
+        s = (rng.integers(0, 6, size=n) / 5).astype(np.float32)      # ties on purpose
+        M = int(rng.integers(0, 6))
+        if rng.random() < 0.5:
+            tau += 1
+        got = nat.prefetch(s, M, tau)
+        want = ora.prefetch(o.select_prefetch(s.astype(np.float64), ora.occupied(), M), tau)
+        assert got == want
+        e, t = nat.table()
+        assert e.tolist() == ora.expert.tolist() and t.tolist() == ora.stamp.tolist()
+
+
+def test_native_policy_rejects_bad_input():
+    with pytest.raises(spp.SppError):
+        spp.SlotPolicy(2, 4, [0, 0])
+    with pytest.raises(spp.SppError):
+        spp.SlotPolicy(2, 4, [0, 1, 2])
+    p = spp.SlotPolicy(2, 4, [0])
+    with pytest.raises(spp.SppError):
+        p.on_demand([5], 1)
+    with pytest.raises(spp.SppError):
+        p.on_demand([0, 1, 2], 1)
+    e, t = p.table()
+    assert e.tolist() == [0, -1]                         # failed calls change nothing
+
+
+def test_create_rejects_bad_shapes_without_touching_a_device():
+    bad = [
+        spp.make_desc(L=0, D=256, n=8, K=2, I=64, r=4, S=4),
+        spp.make_desc(L=2, D=250, n=8, K=2, I=64, r=4, S=4),            # D*2 not a multiple of 16
+        spp.make_desc(L=2, D=256, n=8, K=9, I=64, r=4, S=4),            # K > n
+        spp.make_desc(L=2, D=256, n=8, K=2, I=64, r=300, S=4),          # r too large
+        spp.make_desc(L=2, D=8192, n=8, K=2, I=64, r=4, S=4),           # D too large
+        spp.make_desc(L=2, D=256, n=8, K=2, I=64, r=4, S=4, dtype=7),
+    ]
+    for d in bad:
+        with pytest.raises(spp.SppError) as e:
+            spp.spp_create(d, 0)
+        assert e.value.status == spp.SPP_EINVAL
+
+
+def test_blob_stride():
+    d = spp.make_desc(L=2, D=2048, n=128, K=8, I=768, r=64, S=32)
+    assert spp.spp_blob_stride(d) == 9_437_184                 # 3*768*2048*2, already 4 KiB aligned
+    d = spp.make_desc(L=2, D=96, n=12, K=3, I=40, r=8, S=12, dtype=spp.DTYPE_F32)
+    assert spp.spp_blob_stride(d) == 49152                     # 46080 rounded up to 4 KiB
