@@ -82,10 +82,11 @@ typedef struct {
   int64_t copy_bytes, ffn_launches, window_samples;
   double router_us;   /* router+adapter kernel and result read-back */
   double exposed_us;  /* compute stream waiting on expert copies before the FFN */
-  double ffn_us;      /* routed-expert FFN main kernel */
+  double ffn_us;      /* routed-expert FFN main kernel (kernel begin/end stamps) */
   double tail_us;     /* FFN combine/residual kernel */
   double span_us;     /* first layer start to last layer end */
-  double window_us;   /* sum of prediction-available -> next-layer FFN start */
+  double window_us;   /* sum over layer pairs of W_l = t_exec(l+1) - t_pred(l) */
+  double compute_window_us;  /* the same minus the copy stalls of both layers inside it */
 } spp_run_stats;
 
 /* ---------------------------------------------------------------- lifecycle */

@@ -24,6 +24,9 @@ struct RouterArgs {
   int32_t* topk;        // [B, K]
   float* gates;         // [B, K]
   float* s;             // [n]
+  int32_t* topk_host;   // [B, K] host-mapped mirror (device-visible address) or nullptr
+  float* gates_host;    // [B, K] host-mapped mirror or nullptr
+  float* s_host;        // [n] host-mapped mirror or nullptr
   unsigned* counter;    // zero between launches
   int B, D, n, K, r;
   float eps;
@@ -59,7 +62,8 @@ struct ProjArgs {
 };
 
 hipError_t launch_router(const RouterArgs& a, int dtype, hipStream_t st);
-hipError_t launch_ffn(const FfnArgs& a, int grid, int dtype, hipStream_t st);
+// start/stop (nullable) are stamped with the kernel's own begin/end times.
+hipError_t launch_ffn(const FfnArgs& a, int grid, int dtype, hipStream_t st, hipEvent_t start, hipEvent_t stop);
 hipError_t launch_combine(const CombineArgs& a, int dtype, hipStream_t st);
 hipError_t launch_proj(const ProjArgs& a, int dtype, hipStream_t st);
 int ffn_grid_for(int nunits, int* upw);

@@ -3,9 +3,11 @@
 // Lane layout shared by every row-dot kernel: a row of D elements is read as
 // 16-byte chunks (8 bf16 or 4 fp32); lane l of a 64-wide wave owns chunks
 // l, l+64, l+128, ... so one wave-wide load instruction moves 1 KiB of
-// contiguous memory.  A row's dot product is the sum of per-lane partial sums
-// followed by a butterfly reduction across the wave (every lane ends with the
-// same bits, since fp32 addition is commutative).
+// contiguous memory.  Loads are issued into raw registers first and unpacked
+// only after every load of the step is in flight.  A row's dot product is the
+// sum of per-lane partial sums followed by a DPP reduction across the wave
+// whose result is bit-identical in every lane.
+#include <hip/hip_ext.h>
 #include <hip/hip_runtime.h>
 
 #include <climits>
@@ -19,6 +21,7 @@ namespace {
 
 constexpr int kWaves = 4;
 constexpr int kThreads = 64 * kWaves;
+constexpr int kBStage = 8192;  // adapter B elements staged in LDS (n * r)
 
 template <typename T>
 struct Vec;
@@ -31,7 +34,16 @@ struct Vec<uint16_t> {
   static constexpr int N = 8;
 };
 
-__device__ __forceinline__ uint4 ld16(const void* p) { return *reinterpret_cast<const uint4*>(p); }
+// Loads through global-address-space pointers: a generic pointer (e.g. one read
+// back from LDS) would otherwise become a flat load, which also counts against
+// the LDS counter and serialises unrelated waits.
+#if defined(__HIP_DEVICE_COMPILE__)
+#define SPP_GLOBAL(T, p) ((const __attribute__((address_space(1))) T*)(p))
+#else
+#define SPP_GLOBAL(T, p) (reinterpret_cast<const T*>(p))
+#endif
+
+__device__ __forceinline__ uint4 ld16(const void* p) { return *SPP_GLOBAL(uint4, p); }
 
 template <typename T>
 __device__ __forceinline__ void unpack(const uint4 r, float* f);
@@ -85,10 +97,34 @@ __device__ __forceinline__ void store_elem<uint16_t>(void* p, size_t i, float v)
   reinterpret_cast<uint16_t*>(p)[i] = o;
 }
 
+// DPP move of a float across lanes (row/bank masks all on).
+template <int CTRL>
+__device__ __forceinline__ float dpp(float v) {
+  return __int_as_float(__builtin_amdgcn_update_dpp(0, __float_as_int(v), CTRL, 0xF, 0xF, false));
+}
+
+__device__ __forceinline__ float lane_value(float v, int lane) {
+  return __int_as_float(__builtin_amdgcn_readlane(__float_as_int(v), lane));
+}
+
+// Sum over the 64 lanes.  Within each 16-lane row: xor-1 and xor-2 quad
+// permutes, then half-row and row mirrors (each step adds a commutative pair,
+// so every lane of a row holds identical bits); then the four row sums are
+// added in row order.  Every lane returns the same value.
 __device__ __forceinline__ float wave_sum(float v) {
-#pragma unroll
-  for (int o = 32; o > 0; o >>= 1) v += __shfl_xor(v, o, 64);
-  return v;
+  v += dpp<0xB1>(v);   // quad_perm [1,0,3,2]
+  v += dpp<0x4E>(v);   // quad_perm [2,3,0,1]
+  v += dpp<0x141>(v);  // row_half_mirror
+  v += dpp<0x140>(v);  // row_mirror
+  return ((lane_value(v, 0) + lane_value(v, 16)) + lane_value(v, 32)) + lane_value(v, 48);
+}
+
+__device__ __forceinline__ float wave_max(float v) {
+  v = fmaxf(v, dpp<0xB1>(v));
+  v = fmaxf(v, dpp<0x4E>(v));
+  v = fmaxf(v, dpp<0x141>(v));
+  v = fmaxf(v, dpp<0x140>(v));
+  return fmaxf(fmaxf(lane_value(v, 0), lane_value(v, 16)), fmaxf(lane_value(v, 32), lane_value(v, 48)));
 }
 
 __device__ __forceinline__ void st_agent(float* p, float v) {
@@ -98,35 +134,58 @@ __device__ __forceinline__ float ld_agent(const float* p) {
   return __hip_atomic_load(p, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
 }
 
-// Row of D input values of token b in lane layout, as fp32.
-template <typename T, int NCH>
-__device__ __forceinline__ void load_row_f32(const float* src, int lane, int nch, float (&xv)[NCH][Vec<T>::N]) {
-  constexpr int V = Vec<T>::N;
+typedef unsigned int u32x4 __attribute__((ext_vector_type(4)));
+
+// One 16-byte load; NT marks it non-temporal (streamed once, kept out of the caches' reuse set).
+template <bool NT>
+__device__ __forceinline__ uint4 ld_chunk(const void* row, int c) {
+  if (NT) {
+    const u32x4 t = __builtin_nontemporal_load(SPP_GLOBAL(u32x4, row) + c);
+    return make_uint4(t.x, t.y, t.z, t.w);
+  }
+  return SPP_GLOBAL(uint4, row)[c];
+}
+
+// Raw 16-byte chunks of a row in lane layout (zero past the row end).  FULL:
+// the row is exactly 64*NCH chunks, so no lane needs a bounds check.
+template <int NCH, bool FULL = false, bool NT = false>
+__device__ __forceinline__ void load_chunks(const void* row, int lane, int nch, uint4 (&r)[NCH]) {
 #pragma unroll
   for (int j = 0; j < NCH; ++j) {
     const int c = lane + 64 * j;
-#pragma unroll
-    for (int v = 0; v < V; ++v) xv[j][v] = 0.f;
-    if (c < nch) {
-#pragma unroll
-      for (int v = 0; v < V; v += 4) {
-        const uint4 r = ld16(src + c * V + v);
-        unpack<float>(r, &xv[j][v]);
-      }
+    if (FULL) {
+      r[j] = ld_chunk<NT>(row, c);
+    } else {
+      r[j] = make_uint4(0, 0, 0, 0);
+      if (c < nch) r[j] = ld_chunk<NT>(row, c);
     }
   }
 }
 
+// fp32 row (V values per chunk of the storage type T) in lane layout.
 template <typename T, int NCH>
-__device__ __forceinline__ void load_row_storage(const T* src, int lane, int nch, float (&xv)[NCH][Vec<T>::N]) {
+__device__ __forceinline__ void load_row_f32(const float* src, int lane, int nch, float (&xv)[NCH][Vec<T>::N]) {
   constexpr int V = Vec<T>::N;
+  constexpr int Q = V / 4;  // 16-byte fp32 pieces per storage chunk
+  uint4 r[NCH][Q];
 #pragma unroll
   for (int j = 0; j < NCH; ++j) {
     const int c = lane + 64 * j;
 #pragma unroll
-    for (int v = 0; v < V; ++v) xv[j][v] = 0.f;
-    if (c < nch) unpack<T>(ld16(src + c * V), xv[j]);
+    for (int q = 0; q < Q; ++q) r[j][q] = c < nch ? ld16(src + c * V + 4 * q) : make_uint4(0, 0, 0, 0);
   }
+#pragma unroll
+  for (int j = 0; j < NCH; ++j)
+#pragma unroll
+    for (int q = 0; q < Q; ++q) unpack<float>(r[j][q], &xv[j][4 * q]);
+}
+
+template <typename T, int NCH>
+__device__ __forceinline__ void load_row_storage(const T* src, int lane, int nch, float (&xv)[NCH][Vec<T>::N]) {
+  uint4 r[NCH];
+  load_chunks<NCH>(src, lane, nch, r);
+#pragma unroll
+  for (int j = 0; j < NCH; ++j) unpack<T>(r[j], xv[j]);
 }
 
 template <typename T, int NCH>
@@ -147,17 +206,19 @@ __device__ __forceinline__ float rms_scale(float (&xv)[NCH][Vec<T>::N], int D, f
 template <typename T, int NCH>
 __global__ __launch_bounds__(kThreads) void router_adapter_kernel(RouterArgs a) {
   constexpr int V = Vec<T>::N;
-  const int lane = threadIdx.x & 63, wave = threadIdx.x >> 6;
+  const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
   const int D = a.D, nch = D / V, n = a.n, r = a.r, ldz = a.n + a.r;
   const int nr = a.router_on ? n : 0;
   const int na = a.A ? r : 0;
   const int row = blockIdx.x * kWaves + wave;
 
   __shared__ int s_last;
-  __shared__ float s_zsel[kWaves][32];
-  __shared__ int s_isel[kWaves][32];
+  __shared__ float s_z[kMaxExpertsTopK];
+  __shared__ float s_zsel[32];
+  __shared__ int s_isel[32];
   __shared__ float s_red[kWaves];
   __shared__ float s_a[256];
+  __shared__ float s_B[kBStage];  // adapter B transposed ([r][n]) when n*r fits
 
   const T* wrow = nullptr;
   int zcol = 0;
@@ -169,13 +230,7 @@ __global__ __launch_bounds__(kThreads) void router_adapter_kernel(RouterArgs a) 
     zcol = n + (row - nr);
   }
   uint4 w[NCH];
-  if (wrow) {
-#pragma unroll
-    for (int j = 0; j < NCH; ++j) {
-      const int c = lane + 64 * j;
-      w[j] = c < nch ? ld16(wrow + c * V) : make_uint4(0, 0, 0, 0);
-    }
-  }
+  load_chunks<NCH>(wrow ? wrow : reinterpret_cast<const T*>(a.Wr), lane, wrow ? nch : 0, w);
 
   for (int b = 0; b < a.B; ++b) {
     float xv[NCH][V];
@@ -217,68 +272,80 @@ __global__ __launch_bounds__(kThreads) void router_adapter_kernel(RouterArgs a) 
   }
 
   // single-pass handoff: the last workgroup to finish does the selection
-  __threadfence();
+  __builtin_amdgcn_fence(__ATOMIC_RELEASE, "agent");  // release this workgroup's results
   __syncthreads();
-  if (threadIdx.x == 0) {
-    const unsigned prev = __hip_atomic_fetch_add(a.counter, 1u, __ATOMIC_ACQ_REL, __HIP_MEMORY_SCOPE_AGENT);
+  if (tid == 0) {
+    const unsigned prev = __hip_atomic_fetch_add(a.counter, 1u, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
     s_last = (prev == gridDim.x - 1);
   }
   __syncthreads();
   if (!s_last) return;
-  __threadfence();
+  __builtin_amdgcn_fence(__ATOMIC_ACQUIRE, "agent");
+
+  // adapter B staging is independent of the other workgroups: issue it first
+  const bool staged = na && n * r <= kBStage;
+  if (staged) {
+    constexpr int VB = Vec<T>::N;
+    const int nchunk = (n * r) / VB;       // n*r*sizeof(T) is a multiple of 16 (checked at launch)
+    for (int c0 = tid; c0 < nchunk; c0 += kThreads * 4) {
+      uint4 rb[4];
+#pragma unroll
+      for (int q = 0; q < 4; ++q) {
+        const int c = c0 + q * kThreads;
+        rb[q] = c < nchunk ? ld16(reinterpret_cast<const T*>(a.Bm) + static_cast<size_t>(c) * VB)
+                           : make_uint4(0, 0, 0, 0);
+      }
+#pragma unroll
+      for (int q = 0; q < 4; ++q) {
+        const int c = c0 + q * kThreads;
+        if (c < nchunk) {
+          float f[VB];
+          unpack<T>(rb[q], f);
+#pragma unroll
+          for (int v = 0; v < VB; ++v) {
+            const int idx = c * VB + v;
+            const int e = idx / r, j = idx - e * r;
+            s_B[j * n + e] = f[v];
+          }
+        }
+      }
+    }
+  }
 
   if (a.router_on) {
-    constexpr int QMAX = kMaxExpertsTopK / 64;
-    const int nq = (n + 63) / 64;
-    for (int b = wave; b < a.B; b += kWaves) {
+    // Top-K by rank counting: expert e takes position rank(e) = #{e' beating e},
+    // where e' beats e iff z_e' > z_e, or z_e' == z_e and e' < e.
+    for (int b = 0; b < a.B; ++b) {
       const float* zb = a.zbuf + static_cast<size_t>(b) * ldz;
-      float v[QMAX];
-      uint32_t used = 0;
-#pragma unroll
-      for (int q = 0; q < QMAX; ++q) {
-        const int e = lane + 64 * q;
-        v[q] = (q < nq && e < n) ? ld_agent(zb + e) : -INFINITY;
-      }
-      for (int k = 0; k < a.K; ++k) {
-        float bv = -INFINITY;
-        int bi = INT_MAX;
-#pragma unroll
-        for (int q = 0; q < QMAX; ++q) {
-          const int e = lane + 64 * q;
-          if (q < nq && e < n && !((used >> q) & 1u)) {
-            if (v[q] > bv || (v[q] == bv && e < bi)) {
-              bv = v[q];
-              bi = e;
-            }
-          }
+      __syncthreads();
+      for (int e = tid; e < n; e += kThreads) s_z[e] = ld_agent(zb + e);
+      __syncthreads();
+      for (int e = tid; e < n; e += kThreads) {
+        const float v = s_z[e];
+        int rank = 0;
+#pragma unroll 8
+        for (int j = 0; j < n; ++j) {
+          const float u = s_z[j];
+          rank += (u > v || (u == v && j < e)) ? 1 : 0;
         }
-#pragma unroll
-        for (int o = 32; o > 0; o >>= 1) {
-          const float ov = __shfl_xor(bv, o, 64);
-          const int oi = __shfl_xor(bi, o, 64);
-          if (ov > bv || (ov == bv && oi < bi)) {
-            bv = ov;
-            bi = oi;
-          }
-        }
-        if (bi != INT_MAX && (bi & 63) == lane) used |= 1u << (bi >> 6);
-        if (lane == 0) {
-          s_zsel[wave][k] = bv;
-          s_isel[wave][k] = bi;
+        if (rank < a.K) {
+          s_isel[rank] = e;
+          s_zsel[rank] = v;
         }
       }
-      if (lane == 0) {
+      __syncthreads();
+      if (tid < a.K) {
         // softmax over all n renormalised over the K selected = softmax over the selected
-        const float m = s_zsel[wave][0];
+        const float m = s_zsel[0];
         float sum = 0.f;
-        for (int k = 0; k < a.K; ++k) {
-          const float e = expf(s_zsel[wave][k] - m);
-          s_zsel[wave][k] = e;
-          sum += e;
-        }
-        for (int k = 0; k < a.K; ++k) {
-          a.topk[b * a.K + k] = s_isel[wave][k];
-          a.gates[b * a.K + k] = s_zsel[wave][k] / sum;
+        for (int k = 0; k < a.K; ++k) sum += expf(s_zsel[k] - m);
+        const int idx = b * a.K + tid;
+        const float gk = expf(s_zsel[tid] - m) / sum;
+        a.topk[idx] = s_isel[tid];
+        a.gates[idx] = gk;
+        if (a.topk_host) {
+          a.topk_host[idx] = s_isel[tid];
+          a.gates_host[idx] = gk;
         }
       }
     }
@@ -292,23 +359,27 @@ __global__ __launch_bounds__(kThreads) void router_adapter_kernel(RouterArgs a) 
     for (int q = 0; q < EQ; ++q) sacc[q] = 0.f;
     for (int b = 0; b < a.B; ++b) {
       __syncthreads();
-      for (int j = threadIdx.x; j < r; j += kThreads) s_a[j] = ld_agent(a.zbuf + static_cast<size_t>(b) * ldz + n + j);
+      for (int j = tid; j < r; j += kThreads) s_a[j] = ld_agent(a.zbuf + static_cast<size_t>(b) * ldz + n + j);
       __syncthreads();
       float zh[EQ];
       float mx = -INFINITY;
 #pragma unroll
       for (int q = 0; q < EQ; ++q) {
-        const int e = threadIdx.x + kThreads * q;
+        const int e = tid + kThreads * q;
         zh[q] = -INFINITY;
         if (e < n) {
           float acc = 0.f;
-          for (int j = 0; j < r; ++j) acc += load_elem<T>(a.Bm, static_cast<size_t>(e) * r + j) * s_a[j];
+          if (staged) {
+#pragma unroll 8
+            for (int j = 0; j < r; ++j) acc += s_B[j * n + e] * s_a[j];
+          } else {
+            for (int j = 0; j < r; ++j) acc += load_elem<T>(a.Bm, static_cast<size_t>(e) * r + j) * s_a[j];
+          }
           zh[q] = acc;
           mx = fmaxf(mx, acc);
         }
       }
-#pragma unroll
-      for (int o = 32; o > 0; o >>= 1) mx = fmaxf(mx, __shfl_xor(mx, o, 64));
+      mx = wave_max(mx);
       if (lane == 0) s_red[wave] = mx;
       __syncthreads();
       mx = s_red[0];
@@ -318,7 +389,7 @@ __global__ __launch_bounds__(kThreads) void router_adapter_kernel(RouterArgs a) 
       float part = 0.f;
 #pragma unroll
       for (int q = 0; q < EQ; ++q) {
-        const int e = threadIdx.x + kThreads * q;
+        const int e = tid + kThreads * q;
         ex[q] = e < n ? expf(zh[q] - mx) : 0.f;
         part += ex[q];
       }
@@ -332,11 +403,14 @@ __global__ __launch_bounds__(kThreads) void router_adapter_kernel(RouterArgs a) 
     }
 #pragma unroll
     for (int q = 0; q < EQ; ++q) {
-      const int e = threadIdx.x + kThreads * q;
-      if (e < n) a.s[e] = sacc[q];
+      const int e = tid + kThreads * q;
+      if (e < n) {
+        a.s[e] = sacc[q];
+        if (a.s_host) a.s_host[e] = sacc[q];
+      }
     }
   }
-  if (threadIdx.x == 0) __hip_atomic_store(a.counter, 0u, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
+  if (tid == 0) __hip_atomic_store(a.counter, 0u, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
 }
 
 // ---------------------------------------------------------------------------
@@ -345,17 +419,36 @@ __global__ __launch_bounds__(kThreads) void router_adapter_kernel(RouterArgs a) 
 // [gate row i | up row i | down column i].  A wave computes
 //   h_i = silu(gate_i . x) * (up_i . x) * g_k
 // and accumulates h_i * down_i into its lane-owned slice of y; the workgroup
-// then sums its waves and writes one partial y.
+// then sums its waves and writes one partial y.  Expert addresses and gates
+// sit in LDS, so each wave issues the loads of UPP units (3*UPP*NCH 16-byte
+// loads per lane) before waiting on any of them.
 // ---------------------------------------------------------------------------
-template <typename T, int NCH>
-__global__ __launch_bounds__(kThreads) void ffn_units_kernel(FfnArgs a) {
+constexpr int kFfnWaves = 8;
+constexpr int kFfnThreads = 64 * kFfnWaves;
+
+template <int NCH>
+constexpr int ffn_upp() {
+  return NCH <= 3 ? 4 : (NCH == 4 ? 3 : (NCH == 5 ? 2 : 1));
+}
+
+template <typename T, int NCH, bool FULL>
+__global__ __launch_bounds__(kFfnThreads) void ffn_units_kernel(FfnArgs a) {
   constexpr int V = Vec<T>::N;
-  extern __shared__ float s_red[];  // [kWaves][D]
-  const int lane = threadIdx.x & 63, wave = threadIdx.x >> 6;
+  constexpr int UPP = ffn_upp<NCH>();
+  extern __shared__ float s_red[];  // [kFfnWaves / 2][D]
+  __shared__ const T* s_blob[kMaxWork];
+  __shared__ float s_gate[kMaxWork];
+  const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
   const int D = a.D, nch = D / V, I = a.I;
 
+  if (tid < a.nW) {
+    s_blob[tid] = reinterpret_cast<const T*>(a.blob[tid]);
+    s_gate[tid] = a.gate_idx[tid] >= 0 ? a.gates[a.gate_idx[tid]] : 1.f;
+  }
   float xv[NCH][V];
   load_row_f32<T, NCH>(a.x, lane, nch, xv);
+  __syncthreads();
+
   float acc[NCH][V];
 #pragma unroll
   for (int j = 0; j < NCH; ++j)
@@ -367,32 +460,31 @@ __global__ __launch_bounds__(kThreads) void ffn_units_kernel(FfnArgs a) {
   const int u1 = min(u0 + a.upw, total);
   const size_t unit_elems = static_cast<size_t>(3) * D;
 
-  int uidx = u0 + wave;
-  // two units per iteration keep 6*NCH 16-byte loads in flight per lane
-  for (; uidx + kWaves < u1; uidx += 2 * kWaves) {
-    uint4 rg[2][NCH], ru[2][NCH], rd[2][NCH];
-    float gate[2];
+  for (int ub = u0 + wave; ub < u1; ub += kFfnWaves * UPP) {
+    uint4 rg[UPP][NCH], ru[UPP][NCH], rd[UPP][NCH];
+    float gate[UPP];
 #pragma unroll
-    for (int p = 0; p < 2; ++p) {
-      const int uu = uidx + p * kWaves;
-      const int d = uu / I, i = uu - d * I;
-      const T* base = reinterpret_cast<const T*>(a.blob[d]) + static_cast<size_t>(i) * unit_elems;
-      gate[p] = a.gate_idx[d] >= 0 ? a.gates[a.gate_idx[d]] : 1.f;
+    for (int p = 0; p < UPP; ++p) {
+      const int uu = ub + p * kFfnWaves;
+      gate[p] = 0.f;
+      if (uu < u1) {  // wave-uniform
+        const int d = uu / I;
+        const int i = uu - d * I;
+        const T* base = s_blob[d] + static_cast<size_t>(i) * unit_elems;
+        gate[p] = s_gate[d];
+        load_chunks<NCH, FULL, true>(base, lane, nch, rg[p]);
+        load_chunks<NCH, FULL, true>(base + D, lane, nch, ru[p]);
+        load_chunks<NCH, FULL, true>(base + 2 * D, lane, nch, rd[p]);
+      } else {
 #pragma unroll
-      for (int j = 0; j < NCH; ++j) {
-        const int c = lane + 64 * j;
-        if (c < nch) {
-          rg[p][j] = ld16(base + c * V);
-          ru[p][j] = ld16(base + D + c * V);
-          rd[p][j] = ld16(base + 2 * D + c * V);
-        } else {
-          rg[p][j] = ru[p][j] = rd[p][j] = make_uint4(0, 0, 0, 0);
-        }
+        for (int j = 0; j < NCH; ++j) rg[p][j] = ru[p][j] = rd[p][j] = make_uint4(0, 0, 0, 0);
       }
     }
-    float gs[2] = {0.f, 0.f}, us[2] = {0.f, 0.f};
+    float gs[UPP], us[UPP];
 #pragma unroll
-    for (int p = 0; p < 2; ++p)
+    for (int p = 0; p < UPP; ++p) {
+      gs[p] = 0.f;
+      us[p] = 0.f;
 #pragma unroll
       for (int j = 0; j < NCH; ++j) {
         float fg[V], fu[V];
@@ -404,16 +496,12 @@ __global__ __launch_bounds__(kThreads) void ffn_units_kernel(FfnArgs a) {
           us[p] += fu[v] * xv[j][v];
         }
       }
-#pragma unroll
-    for (int o = 32; o > 0; o >>= 1) {
-      gs[0] += __shfl_xor(gs[0], o, 64);
-      us[0] += __shfl_xor(us[0], o, 64);
-      gs[1] += __shfl_xor(gs[1], o, 64);
-      us[1] += __shfl_xor(us[1], o, 64);
     }
 #pragma unroll
-    for (int p = 0; p < 2; ++p) {
-      const float hval = gs[p] / (1.f + expf(-gs[p])) * us[p] * gate[p];
+    for (int p = 0; p < UPP; ++p) {
+      const float g = wave_sum(gs[p]);
+      const float u = wave_sum(us[p]);
+      const float hval = g / (1.f + expf(-g)) * u * gate[p];
 #pragma unroll
       for (int j = 0; j < NCH; ++j) {
         float fd[V];
@@ -423,79 +511,72 @@ __global__ __launch_bounds__(kThreads) void ffn_units_kernel(FfnArgs a) {
       }
     }
   }
-  for (; uidx < u1; uidx += kWaves) {
-    const int d = uidx / I, i = uidx - d * I;
-    const T* base = reinterpret_cast<const T*>(a.blob[d]) + static_cast<size_t>(i) * unit_elems;
-    const float gate = a.gate_idx[d] >= 0 ? a.gates[a.gate_idx[d]] : 1.f;
-    uint4 rg[NCH], ru[NCH], rd[NCH];
+
+  // sum the waves of this workgroup in a fixed order: (w + w+4) for w < 4, then slots 0..3
+  constexpr int H = kFfnWaves / 2;
+  if (wave >= H) {
 #pragma unroll
     for (int j = 0; j < NCH; ++j) {
       const int c = lane + 64 * j;
       if (c < nch) {
-        rg[j] = ld16(base + c * V);
-        ru[j] = ld16(base + D + c * V);
-        rd[j] = ld16(base + 2 * D + c * V);
-      } else {
-        rg[j] = ru[j] = rd[j] = make_uint4(0, 0, 0, 0);
+#pragma unroll
+        for (int v = 0; v < V; ++v) s_red[(wave - H) * D + c * V + v] = acc[j][v];
       }
-    }
-    float gs = 0.f, us = 0.f;
-#pragma unroll
-    for (int j = 0; j < NCH; ++j) {
-      float fg[V], fu[V];
-      unpack<T>(rg[j], fg);
-      unpack<T>(ru[j], fu);
-#pragma unroll
-      for (int v = 0; v < V; ++v) {
-        gs += fg[v] * xv[j][v];
-        us += fu[v] * xv[j][v];
-      }
-    }
-    gs = wave_sum(gs);
-    us = wave_sum(us);
-    const float hval = gs / (1.f + expf(-gs)) * us * gate;
-#pragma unroll
-    for (int j = 0; j < NCH; ++j) {
-      float fd[V];
-      unpack<T>(rd[j], fd);
-#pragma unroll
-      for (int v = 0; v < V; ++v) acc[j][v] += hval * fd[v];
     }
   }
-
-  // sum the waves of this workgroup, wave order fixed
+  __syncthreads();
+  if (wave < H) {
 #pragma unroll
-  for (int j = 0; j < NCH; ++j) {
-    const int c = lane + 64 * j;
-    if (c < nch) {
+    for (int j = 0; j < NCH; ++j) {
+      const int c = lane + 64 * j;
+      if (c < nch) {
 #pragma unroll
-      for (int v = 0; v < V; ++v) s_red[wave * D + c * V + v] = acc[j][v];
+        for (int v = 0; v < V; ++v) {
+          float* slot = &s_red[wave * D + c * V + v];
+          *slot = acc[j][v] + *slot;
+        }
+      }
     }
   }
   __syncthreads();
   float* out = a.partial + static_cast<size_t>(blockIdx.x) * D;
-  for (int d = threadIdx.x; d < D; d += kThreads) {
-    float s = s_red[d];
+  for (int d = tid; d < D; d += kFfnThreads) {
+    float v = s_red[d];
 #pragma unroll
-    for (int wv = 1; wv < kWaves; ++wv) s += s_red[wv * D + d];
-    out[d] = s;
+    for (int wv = 1; wv < H; ++wv) v += s_red[wv * D + d];
+    out[d] = v;
   }
 }
 
 // y = sum of the workgroup partials (fixed order), h_out = round(residual + y).
-// 256 threads cover 64 outputs: four groups split the partials, then combine.
+// 1024 threads cover 64 outputs: 16 groups split the partials (8 loads in
+// flight per thread), then the groups are added in order.
+constexpr int kCombGroups = 16;
+
 template <typename T>
-__global__ __launch_bounds__(kThreads) void ffn_combine_kernel(CombineArgs a) {
-  __shared__ float s_part[kWaves][64];
+__global__ __launch_bounds__(64 * kCombGroups) void ffn_combine_kernel(CombineArgs a) {
+  __shared__ float s_part[kCombGroups][64];
   const int lane = threadIdx.x & 63, grp = threadIdx.x >> 6;
   const int col = blockIdx.x * 64 + lane;
   float s = 0.f;
-  if (col < a.D)
-    for (int w = grp; w < a.nparts; w += kWaves) s += a.partial[static_cast<size_t>(w) * a.D + col];
+  if (col < a.D) {
+    for (int w0 = grp; w0 < a.nparts; w0 += kCombGroups * 8) {
+      float v[8];
+#pragma unroll
+      for (int k = 0; k < 8; ++k) {
+        const int w = w0 + kCombGroups * k;
+        v[k] = w < a.nparts ? a.partial[static_cast<size_t>(w) * a.D + col] : 0.f;
+      }
+#pragma unroll
+      for (int k = 0; k < 8; ++k) s += v[k];
+    }
+  }
   s_part[grp][lane] = s;
   __syncthreads();
   if (grp == 0 && col < a.D) {
-    const float y = ((s_part[0][lane] + s_part[1][lane]) + s_part[2][lane]) + s_part[3][lane];
+    float y = s_part[0][lane];
+#pragma unroll
+    for (int g = 1; g < kCombGroups; ++g) y += s_part[g][lane];
     const float res = a.res_u ? a.res_u[col] : load_elem<T>(a.res_h, col);
     store_elem<T>(a.out, col, res + y);
   }
@@ -511,11 +592,7 @@ __global__ __launch_bounds__(kThreads) void proj_kernel(ProjArgs a) {
   if (row >= D) return;
   const T* prow = reinterpret_cast<const T*>(a.P) + static_cast<size_t>(row) * D;
   uint4 w[NCH];
-#pragma unroll
-  for (int j = 0; j < NCH; ++j) {
-    const int c = lane + 64 * j;
-    w[j] = c < nch ? ld16(prow + c * V) : make_uint4(0, 0, 0, 0);
-  }
+  load_chunks<NCH>(prow, lane, nch, w);
   for (int b = 0; b < a.B; ++b) {
     const T* hb = reinterpret_cast<const T*>(a.h) + static_cast<size_t>(b) * D;
     float xv[NCH][V];
@@ -557,18 +634,31 @@ template <typename T>
 hipError_t router_t(const RouterArgs& a, hipStream_t st) {
   const int rows = (a.router_on ? a.n : 0) + (a.A ? a.r : 0);
   if (rows <= 0) return hipErrorInvalidValue;
+  // the staged adapter path reads B in 16-byte chunks
+  if (a.A && (static_cast<size_t>(a.n) * a.r * sizeof(T)) % 16 != 0) return hipErrorInvalidValue;
   const int grid = (rows + kWaves - 1) / kWaves;
   SPP_DISPATCH_NCH(nch_for<T>(a.D),
                    hipLaunchKernelGGL((router_adapter_kernel<T, NCH>), dim3(grid), dim3(kThreads), 0, st, a));
   return hipGetLastError();
 }
 
-template <typename T>
-hipError_t ffn_t(const FfnArgs& a, int grid, hipStream_t st) {
-  const size_t lds = sizeof(float) * kWaves * a.D;
-  SPP_DISPATCH_NCH(nch_for<T>(a.D),
-                   hipLaunchKernelGGL((ffn_units_kernel<T, NCH>), dim3(grid), dim3(kThreads), lds, st, a));
+template <typename T, bool FULL>
+hipError_t ffn_tf(const FfnArgs& a, int grid, hipStream_t st, hipEvent_t start, hipEvent_t stop) {
+  const uint32_t lds = sizeof(float) * (kFfnWaves / 2) * a.D;
+  if (start || stop) {
+    SPP_DISPATCH_NCH(nch_for<T>(a.D), hipExtLaunchKernelGGL((ffn_units_kernel<T, NCH, FULL>), dim3(grid),
+                                                            dim3(kFfnThreads), lds, st, start, stop, 0u, a));
+  } else {
+    SPP_DISPATCH_NCH(nch_for<T>(a.D), hipLaunchKernelGGL((ffn_units_kernel<T, NCH, FULL>), dim3(grid),
+                                                         dim3(kFfnThreads), lds, st, a));
+  }
   return hipGetLastError();
+}
+
+template <typename T>
+hipError_t ffn_t(const FfnArgs& a, int grid, hipStream_t st, hipEvent_t start, hipEvent_t stop) {
+  const int nch = a.D / Vec<T>::N;
+  return nch % 64 == 0 ? ffn_tf<T, true>(a, grid, st, start, stop) : ffn_tf<T, false>(a, grid, st, start, stop);
 }
 
 template <typename T>
@@ -588,17 +678,17 @@ hipError_t launch_router(const RouterArgs& a, int dtype, hipStream_t st) {
   return dtype == 1 ? router_t<uint16_t>(a, st) : router_t<float>(a, st);
 }
 
-hipError_t launch_ffn(const FfnArgs& a, int grid, int dtype, hipStream_t st) {
-  if (a.nW <= 0 || a.nW > kMaxWork || grid <= 0) return hipErrorInvalidValue;
-  return dtype == 1 ? ffn_t<uint16_t>(a, grid, st) : ffn_t<float>(a, grid, st);
+hipError_t launch_ffn(const FfnArgs& a, int grid, int dtype, hipStream_t st, hipEvent_t start, hipEvent_t stop) {
+  if (a.nW <= 0 || a.nW > kMaxWork || grid <= 0 || a.D > 4096) return hipErrorInvalidValue;
+  return dtype == 1 ? ffn_t<uint16_t>(a, grid, st, start, stop) : ffn_t<float>(a, grid, st, start, stop);
 }
 
 hipError_t launch_combine(const CombineArgs& a, int dtype, hipStream_t st) {
   const int grid = (a.D + 63) / 64;
   if (dtype == 1)
-    hipLaunchKernelGGL((ffn_combine_kernel<uint16_t>), dim3(grid), dim3(kThreads), 0, st, a);
+    hipLaunchKernelGGL((ffn_combine_kernel<uint16_t>), dim3(grid), dim3(64 * kCombGroups), 0, st, a);
   else
-    hipLaunchKernelGGL((ffn_combine_kernel<float>), dim3(grid), dim3(kThreads), 0, st, a);
+    hipLaunchKernelGGL((ffn_combine_kernel<float>), dim3(grid), dim3(64 * kCombGroups), 0, st, a);
   return hipGetLastError();
 }
 
@@ -610,7 +700,7 @@ void set_ffn_target_wgs(int wgs) { g_ffn_target_wgs = wgs > 0 ? wgs : 256; }
 
 // Units per workgroup so that about g_ffn_target_wgs workgroups share the work.
 int ffn_grid_for(int nunits, int* upw) {
-  int grid = (nunits + kWaves - 1) / kWaves;
+  int grid = (nunits + kFfnWaves - 1) / kFfnWaves;
   if (grid > g_ffn_target_wgs) grid = g_ffn_target_wgs;
   if (grid < 1) grid = 1;
   *upw = (nunits + grid - 1) / grid;
@@ -618,6 +708,5 @@ int ffn_grid_for(int nunits, int* upw) {
 }
 
 size_t ffn_max_grid() { return 4096; }
-
 
 }  // namespace spp

@@ -30,8 +30,10 @@ spp_status fail(spp_status s, const std::string& m) {
     if (e_ != hipSuccess) return fail(SPP_EHIP, std::string(#expr) + ": " + hipGetErrorString(e_)); \
   } while (0)
 
-constexpr int kEvStart = 0, kEvRouted = 1, kEvWaitA = 2, kEvFfnStart = 3, kEvFfnDone = 4, kEvEnd = 5;
-constexpr int kNumEv = 6;
+// Per layer call: start, routing result on the host, before/after the copy
+// waits, FFN kernel begin/end (stamped by the kernel dispatch), end.
+constexpr int kEvStart = 0, kEvRouted = 1, kEvWaitA = 2, kEvWaitB = 3, kEvFfnBegin = 4, kEvFfnEnd = 5, kEvEnd = 6;
+constexpr int kNumEv = 7;
 
 struct TimingSet {
   hipEvent_t ev[kNumEv] = {};
@@ -71,7 +73,8 @@ struct spp_ctx {
   float* x_dev = nullptr;      // [maxB, D] router input
   float* zbuf = nullptr;       // [maxB, n + r]
   uint8_t* res_dev = nullptr;  // topk [maxB*K] i32 | gates [maxB*K] f32 | s [n] f32
-  uint8_t* res_host = nullptr; // pinned mirror
+  uint8_t* res_host = nullptr; // pinned, host-mapped mirror written by the router kernel
+  uint8_t* res_host_dev = nullptr;  // device-visible address of res_host
   size_t res_bytes = 0, off_gates = 0, off_s = 0;
   unsigned* counter = nullptr;
   float* partial = nullptr;    // [ffn_max_grid, D]
@@ -106,6 +109,7 @@ bool desc_ok(const spp_model_desc* d, std::string* why) {
   if (d->n > spp::kMaxExpertsTopK) return *why = "n must be <= 1024", false;
   if (d->K > d->n || d->K > 32) return *why = "K must be <= min(n, 32)", false;
   if (d->r < 0 || d->r > 256) return *why = "r must be in [0, 256]", false;
+  if ((static_cast<int64_t>(d->n) * d->r * elem) % 16 != 0) return *why = "n * r * element size must be a multiple of 16 bytes", false;
   if (d->n_shared < 0 || d->K + d->n_shared > spp::kMaxWork) return *why = "K + n_shared must be <= 32", false;
   if (d->has_proj != 0 && d->has_proj != 1) return *why = "has_proj must be 0 or 1", false;
   if (!(d->rms_eps >= 0.f) || !std::isfinite(d->rms_eps)) return *why = "rms_eps must be finite and >= 0", false;
@@ -148,13 +152,18 @@ void harvest(spp_ctx* c, size_t count) {
     TimingSet& s = c->pending_sets[i];
     spp_run_stats& st = c->stats;
     st.router_us += 1e3 * elapsed(s.ev[kEvStart], s.ev[kEvRouted]);
-    st.exposed_us += 1e3 * elapsed(s.ev[kEvWaitA], s.ev[kEvFfnStart]);
-    st.ffn_us += 1e3 * elapsed(s.ev[kEvFfnStart], s.ev[kEvFfnDone]);
-    st.tail_us += 1e3 * elapsed(s.ev[kEvFfnDone], s.ev[kEvEnd]);
+    const double exposed = 1e3 * elapsed(s.ev[kEvWaitA], s.ev[kEvWaitB]);
+    st.exposed_us += exposed;
+    st.ffn_us += 1e3 * elapsed(s.ev[kEvFfnBegin], s.ev[kEvFfnEnd]);
+    st.tail_us += 1e3 * elapsed(s.ev[kEvFfnEnd], s.ev[kEvEnd]);
     if (c->have_prev) {
       st.span_us += 1e3 * elapsed(c->prev.ev[kEvStart], s.ev[kEvStart]);
       if (c->prev.predicted && s.l == c->prev.l + 1) {
-        st.window_us += 1e3 * elapsed(c->prev.ev[kEvRouted], s.ev[kEvFfnStart]);
+        // W_l = t_exec(l+1) - t_pred(l); the compute window excludes the copy stalls inside it
+        const double w = 1e3 * elapsed(c->prev.ev[kEvRouted], s.ev[kEvFfnBegin]);
+        const double prev_exposed = 1e3 * elapsed(c->prev.ev[kEvWaitA], c->prev.ev[kEvWaitB]);
+        st.window_us += w;
+        st.compute_window_us += w - prev_exposed - exposed;
         st.window_samples += 1;
       }
       c->free_sets.push_back(c->prev);
@@ -263,8 +272,10 @@ spp_status create_impl(const spp_model_desc* desc, void* stream, spp_ctx** out) 
   c->off_s = c->off_gates + round_up(bk * sizeof(float), 64);
   c->res_bytes = c->off_s + round_up(static_cast<size_t>(d.n) * sizeof(float), 64);
   if (hipMalloc(&c->res_dev, c->res_bytes) != hipSuccess) return fail(SPP_ENOMEM, "result buffer allocation failed");
-  if (hipHostMalloc(&c->res_host, c->res_bytes, hipHostMallocDefault) != hipSuccess)
+  if (hipHostMalloc(&c->res_host, c->res_bytes, hipHostMallocMapped | hipHostMallocCoherent) != hipSuccess)
     return fail(SPP_ENOMEM, "pinned result buffer allocation failed");
+  SPP_HIP(hipHostGetDevicePointer(reinterpret_cast<void**>(&c->res_host_dev), c->res_host, 0));
+  std::memset(c->res_host, 0, c->res_bytes);
   SPP_HIP(hipMemset(c->counter, 0, 256));
   SPP_HIP(hipMemset(c->res_dev, 0, c->res_bytes));
   SPP_HIP(hipEventCreateWithFlags(&c->ev_res, hipEventDisableTiming));
@@ -314,6 +325,9 @@ spp_status layer_forward_impl(spp_ctx* c, int32_t l, const void* h_in, void* h_o
   ra.topk = topk_dev;
   ra.gates = gates_dev;
   ra.s = s_dev;
+  ra.topk_host = reinterpret_cast<int32_t*>(c->res_host_dev);
+  ra.gates_host = reinterpret_cast<float*>(c->res_host_dev + c->off_gates);
+  ra.s_host = predict ? reinterpret_cast<float*>(c->res_host_dev + c->off_s) : nullptr;
   ra.counter = c->counter;
   ra.B = B;
   ra.D = d.D;
@@ -324,8 +338,6 @@ spp_status layer_forward_impl(spp_ctx* c, int32_t l, const void* h_in, void* h_o
   ra.x_given = 0;
   ra.router_on = 1;
   SPP_HIP(spp::launch_router(ra, dt, c->compute));
-  const size_t fetch = predict ? c->res_bytes : c->off_s;
-  SPP_HIP(hipMemcpyAsync(c->res_host, c->res_dev, fetch, hipMemcpyDeviceToHost, c->compute));
   if (c->timing) SPP_HIP(hipEventRecord(ts.ev[kEvRouted], c->compute));
   SPP_HIP(hipEventRecord(c->ev_res, c->compute));
   SPP_HIP(hipEventSynchronize(c->ev_res));
@@ -389,7 +401,7 @@ spp_status layer_forward_impl(spp_ctx* c, int32_t l, const void* h_in, void* h_o
       SPP_HIP(hipStreamWaitEvent(c->compute, ls.slot_ready[slot], 0));
     }
   }
-  if (c->timing) SPP_HIP(hipEventRecord(ts.ev[kEvFfnStart], c->compute));
+  if (c->timing) SPP_HIP(hipEventRecord(ts.ev[kEvWaitB], c->compute));
   for (int32_t b = 0; b < B; ++b) {
     spp::FfnArgs fa{};
     int nW = 0;
@@ -410,8 +422,9 @@ spp_status layer_forward_impl(spp_ctx* c, int32_t l, const void* h_in, void* h_o
     fa.gates = gates_dev;
     fa.partial = c->partial;
     const int grid = spp::ffn_grid_for(nW * d.I, &fa.upw);
-    SPP_HIP(spp::launch_ffn(fa, grid, dt, c->compute));
-    if (c->timing && b == B - 1) SPP_HIP(hipEventRecord(ts.ev[kEvFfnDone], c->compute));
+    const bool stamp = c->timing && b == B - 1;
+    SPP_HIP(spp::launch_ffn(fa, grid, dt, c->compute, stamp ? ts.ev[kEvFfnBegin] : nullptr,
+                            stamp ? ts.ev[kEvFfnEnd] : nullptr));
     spp::CombineArgs ca{};
     ca.partial = c->partial;
     ca.nparts = grid;
@@ -539,6 +552,7 @@ spp_status adapter_predict(spp_ctx* c, int32_t l, const float* x_dev, int32_t B,
   if (!ls.A || d.r == 0) return fail(SPP_ESTATE, "layer has no adapter");
   spp::RouterArgs ra{};
   ra.u = x_dev;
+  ra.s_host = reinterpret_cast<float*>(c->res_host_dev + c->off_s);
   ra.A = ls.A;
   ra.Bm = ls.Bm;
   ra.zbuf = c->zbuf;
@@ -553,8 +567,6 @@ spp_status adapter_predict(spp_ctx* c, int32_t l, const float* x_dev, int32_t B,
   ra.x_given = 1;
   ra.router_on = 0;
   SPP_HIP(spp::launch_router(ra, d.dtype, c->compute));
-  SPP_HIP(hipMemcpyAsync(c->res_host + c->off_s, c->res_dev + c->off_s, sizeof(float) * d.n,
-                         hipMemcpyDeviceToHost, c->compute));
   SPP_HIP(hipEventRecord(c->ev_res, c->compute));
   SPP_HIP(hipEventSynchronize(c->ev_res));
   std::memcpy(s_out, c->res_host + c->off_s, sizeof(float) * d.n);

@@ -108,12 +108,17 @@ class OffloadedMoEStack:
                                self.proj[l].data_ptr() if self.proj[l] is not None else 0,
                                self.shared[l].data_ptr() if self.shared[l] is not None else 0,
                                self.host[l % self.host_layers].data_ptr())
-        res = list(range(min(self.S, cfg.n))) if resident is None else list(resident)
-        for l in range(cfg.L):
-            spp.spp_set_resident(self.ctx, l, res)
+        self.resident = list(range(min(self.S, cfg.n))) if resident is None else list(resident)
+        self.reset()
         # ping-pong hidden-state buffers [B, D] in the storage dtype
         nbytes = cfg.batch * cfg.D * self.elem
         self.hbuf = [torch.empty(nbytes, dtype=torch.uint8, device=self.device) for _ in range(2)]
+
+    def reset(self):
+        """Initial slot tables (the resident set in slots 0.., stamp 0) and step clock 0."""
+        for l in range(self.cfg.L):
+            spp.spp_set_resident(self.ctx, l, self.resident)
+        spp.spp_set_clock(self.ctx, 0)
 
     def _to_storage(self, v):
         from workload.gen import f32_to_bf16_bits
@@ -152,6 +157,19 @@ class OffloadedMoEStack:
             out.append(self.layer(l, src, 1 - src, M_max, B))
             src = 1 - src
         self.last_buf = src
+        return out
+
+    def step_from(self, h_in_ptr: int, M_max: int, B: Optional[int] = None):
+        """One decode step whose layer-0 input is read from device address ``h_in_ptr``."""
+        B = self.cfg.batch if B is None else B
+        out = []
+        src_ptr = h_in_ptr
+        dst = 0
+        for l in range(self.cfg.L):
+            out.append(spp.moe_layer_forward(self.ctx, l, src_ptr, self.hbuf[dst].data_ptr(), B, self.cfg.K, M_max))
+            src_ptr = self.hbuf[dst].data_ptr()
+            dst = 1 - dst
+        self.last_buf = 1 - dst
         return out
 
     def close(self):

@@ -39,7 +39,7 @@ class RunStats(ctypes.Structure):
                                          "ready_on_time", "copies", "copy_bytes", "ffn_launches",
                                          "window_samples")]
                 + [(f, c_double) for f in ("router_us", "exposed_us", "ffn_us", "tail_us", "span_us",
-                                           "window_us")])
+                                           "window_us", "compute_window_us")])
 
     def as_dict(self):
         return {f: getattr(self, f) for f, _ in self._fields_}
