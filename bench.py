@@ -31,6 +31,20 @@ def _log(msg):
     print(msg, file=sys.stderr, flush=True)
 
 
+def measured_traffic(profile: str, kernel_source: str):
+    """HBM bytes per launch from the committed counter summary, or None when the
+    kernel source changed since the counters were taken."""
+    import hashlib
+    try:
+        fields = dict(line.split(": ", 1) for line in open(profile).read().splitlines() if ": " in line)
+        digest = hashlib.sha256(open(kernel_source, "rb").read()).hexdigest()[:16]
+        if fields.get("kernel_source_sha256_16", "").strip() != digest:
+            return None
+        return int(fields["traffic_bytes_per_launch"])
+    except (OSError, KeyError, ValueError):
+        return None
+
+
 def _ffn_stats(rs):
     n = max(rs.ffn_launches, 1)
     return rs.ffn_us / n
@@ -183,6 +197,10 @@ def main():
                       if window_us is not None else None)
     ffn_bytes = cfg.K * cfg.blob_bytes + cfg.n_shared * cfg.blob_bytes   # algorithmic bytes per FFN launch
     achieved = ffn_bytes / (on["ffn_kernel_us"] * 1e3)                   # GB/s
+    traffic = None
+    if cfg.name == "qwen3vl30b_a3b_layer_bf16":
+        traffic = measured_traffic(os.path.join(ROOT, "profiles", f"ffn_units_kernel__{cfg.name}.md"),
+                                   os.path.join(ROOT, "paper_2607_24787_amd", "csrc", "spp_kernels.hip"))
     line = {
         "metric": METRIC,
         "value": on["tokens_per_s"],
@@ -204,7 +222,7 @@ def main():
         "exposed_transfer_pct": on["exposed_transfer_pct"],
         "roofline": {"kernel": "ffn_units_kernel (routed-expert SwiGLU FFN)", "bound": "hbm",
                      "achieved": achieved, "peak": HBM_PEAK_GBS, "unit": "GB/s", "frac": achieved / HBM_PEAK_GBS,
-                     "traffic": None, "bytes_per_launch": ffn_bytes, "avg_launch_us": on["ffn_kernel_us"]},
+                     "traffic": traffic, "bytes_per_launch": ffn_bytes, "avg_launch_us": on["ffn_kernel_us"]},
         "link": {"bound": "host link (pinned H2D)", "per_expert_us": per_expert_us, "peak_gbs_measured": link_gbs,
                  "achieved_gbs_during_run": on["h2d_gbs_during_run"],
                  "frac": (on["h2d_gbs_during_run"] / link_gbs) if on["h2d_gbs_during_run"] else None},

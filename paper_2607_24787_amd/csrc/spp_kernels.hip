@@ -22,6 +22,7 @@ namespace {
 constexpr int kWaves = 4;
 constexpr int kThreads = 64 * kWaves;
 constexpr int kBStage = 8192;  // adapter B elements staged in LDS (n * r)
+constexpr int kZStage = 2048;  // logits + adapter hidden units staged per token chunk
 
 template <typename T>
 struct Vec;
@@ -213,12 +214,12 @@ __global__ __launch_bounds__(kThreads) void router_adapter_kernel(RouterArgs a) 
   const int row = blockIdx.x * kWaves + wave;
 
   __shared__ int s_last;
-  __shared__ float s_z[kMaxExpertsTopK];
   __shared__ float s_zsel[32];
   __shared__ int s_isel[32];
   __shared__ float s_red[kWaves];
   __shared__ float s_a[256];
   __shared__ float s_B[kBStage];  // adapter B transposed ([r][n]) when n*r fits
+  __shared__ float s_zall[kZStage];  // logits | adapter hidden units of a chunk of tokens
 
   const T* wrow = nullptr;
   int zcol = 0;
@@ -282,23 +283,41 @@ __global__ __launch_bounds__(kThreads) void router_adapter_kernel(RouterArgs a) 
   if (!s_last) return;
   __builtin_amdgcn_fence(__ATOMIC_ACQUIRE, "agent");
 
-  // adapter B staging is independent of the other workgroups: issue it first
+  // Every load of the tail is issued before the first barrier: adapter B (staged
+  // transposed in LDS when it fits) and the logits / adapter hidden units of a
+  // chunk of tokens.
   const bool staged = na && n * r <= kBStage;
-  if (staged) {
-    constexpr int VB = Vec<T>::N;
-    const int nchunk = (n * r) / VB;       // n*r*sizeof(T) is a multiple of 16 (checked at launch)
-    for (int c0 = tid; c0 < nchunk; c0 += kThreads * 4) {
-      uint4 rb[4];
+  constexpr int VB = Vec<T>::N;
+  constexpr int kBLoads = kBStage / VB / kThreads;  // 16-byte B chunks per thread
+  uint4 rb[kBLoads];
+  const int nbchunk = staged ? (n * r) / VB : 0;    // n*r*sizeof(T) is a multiple of 16 (checked at launch)
 #pragma unroll
-      for (int q = 0; q < 4; ++q) {
-        const int c = c0 + q * kThreads;
-        rb[q] = c < nchunk ? ld16(reinterpret_cast<const T*>(a.Bm) + static_cast<size_t>(c) * VB)
-                           : make_uint4(0, 0, 0, 0);
-      }
+  for (int q = 0; q < kBLoads; ++q) {
+    const int c = tid + q * kThreads;
+    rb[q] = c < nbchunk ? ld16(reinterpret_cast<const T*>(a.Bm) + static_cast<size_t>(c) * VB)
+                        : make_uint4(0, 0, 0, 0);
+  }
+  constexpr int EQ = kMaxExpertsTopK / kThreads;
+  float sacc[EQ];
 #pragma unroll
-      for (int q = 0; q < 4; ++q) {
-        const int c = c0 + q * kThreads;
-        if (c < nchunk) {
+  for (int q = 0; q < EQ; ++q) sacc[q] = 0.f;
+  static_assert(kZStage >= kMaxExpertsTopK + 256, "one token's logits and hidden units fit the stage");
+  const int bchunk = kZStage / ldz;
+  for (int b0 = 0; b0 < a.B; b0 += bchunk) {
+    const int nb = min(bchunk, a.B - b0);
+    const int cnt = nb * ldz;
+    float zr[kZStage / kThreads];
+#pragma unroll
+    for (int q = 0; q < kZStage / kThreads; ++q) {
+      const int idx = tid + q * kThreads;
+      zr[q] = idx < cnt ? ld_agent(a.zbuf + static_cast<size_t>(b0) * ldz + idx) : 0.f;
+    }
+    __syncthreads();  // previous chunk is done with s_zall
+    if (b0 == 0) {
+#pragma unroll
+      for (int q = 0; q < kBLoads; ++q) {
+        const int c = tid + q * kThreads;
+        if (c < nbchunk) {
           float f[VB];
           unpack<T>(rb[q], f);
 #pragma unroll
@@ -310,97 +329,94 @@ __global__ __launch_bounds__(kThreads) void router_adapter_kernel(RouterArgs a) 
         }
       }
     }
-  }
-
-  if (a.router_on) {
-    // Top-K by rank counting: expert e takes position rank(e) = #{e' beating e},
-    // where e' beats e iff z_e' > z_e, or z_e' == z_e and e' < e.
-    for (int b = 0; b < a.B; ++b) {
-      const float* zb = a.zbuf + static_cast<size_t>(b) * ldz;
-      __syncthreads();
-      for (int e = tid; e < n; e += kThreads) s_z[e] = ld_agent(zb + e);
-      __syncthreads();
-      for (int e = tid; e < n; e += kThreads) {
-        const float v = s_z[e];
-        int rank = 0;
-#pragma unroll 8
-        for (int j = 0; j < n; ++j) {
-          const float u = s_z[j];
-          rank += (u > v || (u == v && j < e)) ? 1 : 0;
-        }
-        if (rank < a.K) {
-          s_isel[rank] = e;
-          s_zsel[rank] = v;
-        }
-      }
-      __syncthreads();
-      if (tid < a.K) {
-        // softmax over all n renormalised over the K selected = softmax over the selected
-        const float m = s_zsel[0];
-        float sum = 0.f;
-        for (int k = 0; k < a.K; ++k) sum += expf(s_zsel[k] - m);
-        const int idx = b * a.K + tid;
-        const float gk = expf(s_zsel[tid] - m) / sum;
-        a.topk[idx] = s_isel[tid];
-        a.gates[idx] = gk;
-        if (a.topk_host) {
-          a.topk_host[idx] = s_isel[tid];
-          a.gates_host[idx] = gk;
-        }
-      }
+#pragma unroll
+    for (int q = 0; q < kZStage / kThreads; ++q) {
+      const int idx = tid + q * kThreads;
+      if (idx < cnt) s_zall[idx] = zr[q];
     }
-  }
-
-  if (na) {
-    // z_hat = B a per token, softmax over the n experts, summed over tokens in order
-    constexpr int EQ = kMaxExpertsTopK / kThreads;
-    float sacc[EQ];
-#pragma unroll
-    for (int q = 0; q < EQ; ++q) sacc[q] = 0.f;
-    for (int b = 0; b < a.B; ++b) {
-      __syncthreads();
-      for (int j = tid; j < r; j += kThreads) s_a[j] = ld_agent(a.zbuf + static_cast<size_t>(b) * ldz + n + j);
-      __syncthreads();
-      float zh[EQ];
-      float mx = -INFINITY;
-#pragma unroll
-      for (int q = 0; q < EQ; ++q) {
-        const int e = tid + kThreads * q;
-        zh[q] = -INFINITY;
-        if (e < n) {
-          float acc = 0.f;
-          if (staged) {
+    __syncthreads();
+    for (int bb = 0; bb < nb; ++bb) {
+      const int b = b0 + bb;
+      const float* zb = s_zall + bb * ldz;
+      if (a.router_on) {
+        // Top-K by rank counting: expert e takes position rank(e) = #{e' beating e},
+        // where e' beats e iff z_e' > z_e, or z_e' == z_e and e' < e.
+        for (int e = tid; e < n; e += kThreads) {
+          const float v = zb[e];
+          int rank = 0;
 #pragma unroll 8
-            for (int j = 0; j < r; ++j) acc += s_B[j * n + e] * s_a[j];
-          } else {
-            for (int j = 0; j < r; ++j) acc += load_elem<T>(a.Bm, static_cast<size_t>(e) * r + j) * s_a[j];
+          for (int j = 0; j < n; ++j) {
+            const float u = zb[j];
+            rank += (u > v || (u == v && j < e)) ? 1 : 0;
           }
-          zh[q] = acc;
-          mx = fmaxf(mx, acc);
+          if (rank < a.K) {
+            s_isel[rank] = e;
+            s_zsel[rank] = v;
+          }
+        }
+        __syncthreads();
+        if (tid < a.K) {
+          // softmax over all n renormalised over the K selected = softmax over the selected
+          const float m = s_zsel[0];
+          float sum = 0.f;
+          for (int k = 0; k < a.K; ++k) sum += expf(s_zsel[k] - m);
+          const int idx = b * a.K + tid;
+          const float gk = expf(s_zsel[tid] - m) / sum;
+          a.topk[idx] = s_isel[tid];
+          a.gates[idx] = gk;
+          if (a.topk_host) {
+            a.topk_host[idx] = s_isel[tid];
+            a.gates_host[idx] = gk;
+          }
         }
       }
-      mx = wave_max(mx);
-      if (lane == 0) s_red[wave] = mx;
-      __syncthreads();
-      mx = s_red[0];
-      for (int wv = 1; wv < kWaves; ++wv) mx = fmaxf(mx, s_red[wv]);
-      __syncthreads();
-      float ex[EQ];
-      float part = 0.f;
+      if (na) {
+        // z_hat = B a, softmax over the n experts, accumulated over tokens in order
+        const float* sa = zb + n;
+        float zh[EQ];
+        float mx = -INFINITY;
 #pragma unroll
-      for (int q = 0; q < EQ; ++q) {
-        const int e = tid + kThreads * q;
-        ex[q] = e < n ? expf(zh[q] - mx) : 0.f;
-        part += ex[q];
+        for (int q = 0; q < EQ; ++q) {
+          const int e = tid + kThreads * q;
+          zh[q] = -INFINITY;
+          if (e < n) {
+            float acc = 0.f;
+            if (staged) {
+#pragma unroll 8
+              for (int j = 0; j < r; ++j) acc += s_B[j * n + e] * sa[j];
+            } else {
+              for (int j = 0; j < r; ++j) acc += load_elem<T>(a.Bm, static_cast<size_t>(e) * r + j) * sa[j];
+            }
+            zh[q] = acc;
+            mx = fmaxf(mx, acc);
+          }
+        }
+        mx = wave_max(mx);
+        if (lane == 0) s_red[wave] = mx;
+        __syncthreads();
+        mx = s_red[0];
+        for (int wv = 1; wv < kWaves; ++wv) mx = fmaxf(mx, s_red[wv]);
+        __syncthreads();
+        float ex[EQ];
+        float part = 0.f;
+#pragma unroll
+        for (int q = 0; q < EQ; ++q) {
+          const int e = tid + kThreads * q;
+          ex[q] = e < n ? expf(zh[q] - mx) : 0.f;
+          part += ex[q];
+        }
+        part = wave_sum(part);
+        if (lane == 0) s_red[wave] = part;
+        __syncthreads();
+        float sum = 0.f;
+        for (int wv = 0; wv < kWaves; ++wv) sum += s_red[wv];
+#pragma unroll
+        for (int q = 0; q < EQ; ++q) sacc[q] += ex[q] / sum;
       }
-      part = wave_sum(part);
-      if (lane == 0) s_red[wave] = part;
-      __syncthreads();
-      float sum = 0.f;
-      for (int wv = 0; wv < kWaves; ++wv) sum += s_red[wv];
-#pragma unroll
-      for (int q = 0; q < EQ; ++q) sacc[q] += ex[q] / sum;
+      __syncthreads();  // s_isel / s_red are reused by the next token
     }
+  }
+  if (na) {
 #pragma unroll
     for (int q = 0; q < EQ; ++q) {
       const int e = tid + kThreads * q;
@@ -435,25 +451,18 @@ template <typename T, int NCH, bool FULL>
 __global__ __launch_bounds__(kFfnThreads) void ffn_units_kernel(FfnArgs a) {
   constexpr int V = Vec<T>::N;
   constexpr int UPP = ffn_upp<NCH>();
-  extern __shared__ float s_red[];  // [kFfnWaves / 2][D]
-  __shared__ const T* s_blob[kMaxWork];
-  __shared__ float s_gate[kMaxWork];
-  const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
+  extern __shared__ float s_red[];  // [kFfnWaves / 2][D] wave partials
+  const int tid = threadIdx.x, lane = tid & 63;
+  const int wave = __builtin_amdgcn_readfirstlane(tid >> 6);
   const int D = a.D, nch = D / V, I = a.I;
-
-  if (tid < a.nW) {
-    s_blob[tid] = reinterpret_cast<const T*>(a.blob[tid]);
-    s_gate[tid] = a.gate_idx[tid] >= 0 ? a.gates[a.gate_idx[tid]] : 1.f;
-  }
-  float xv[NCH][V];
-  load_row_f32<T, NCH>(a.x, lane, nch, xv);
-  __syncthreads();
 
   float acc[NCH][V];
 #pragma unroll
   for (int j = 0; j < NCH; ++j)
 #pragma unroll
     for (int v = 0; v < V; ++v) acc[j][v] = 0.f;
+  float xv[NCH][V];
+  bool have_x = false;
 
   const int total = a.nW * I;
   const int u0 = blockIdx.x * a.upw;
@@ -461,6 +470,7 @@ __global__ __launch_bounds__(kFfnThreads) void ffn_units_kernel(FfnArgs a) {
   const size_t unit_elems = static_cast<size_t>(3) * D;
 
   for (int ub = u0 + wave; ub < u1; ub += kFfnWaves * UPP) {
+    // the weight loads of this pass go out first; x follows them on the first pass
     uint4 rg[UPP][NCH], ru[UPP][NCH], rd[UPP][NCH];
     float gate[UPP];
 #pragma unroll
@@ -470,15 +480,20 @@ __global__ __launch_bounds__(kFfnThreads) void ffn_units_kernel(FfnArgs a) {
       if (uu < u1) {  // wave-uniform
         const int d = uu / I;
         const int i = uu - d * I;
-        const T* base = s_blob[d] + static_cast<size_t>(i) * unit_elems;
-        gate[p] = s_gate[d];
+        const T* base = reinterpret_cast<const T*>(a.blob[d]) + static_cast<size_t>(i) * unit_elems;
         load_chunks<NCH, FULL, true>(base, lane, nch, rg[p]);
         load_chunks<NCH, FULL, true>(base + D, lane, nch, ru[p]);
         load_chunks<NCH, FULL, true>(base + 2 * D, lane, nch, rd[p]);
+        const int gi = a.gate_idx[d];
+        gate[p] = gi >= 0 ? a.gates[gi] : 1.f;
       } else {
 #pragma unroll
         for (int j = 0; j < NCH; ++j) rg[p][j] = ru[p][j] = rd[p][j] = make_uint4(0, 0, 0, 0);
       }
+    }
+    if (!have_x) {
+      load_row_f32<T, NCH>(a.x, lane, nch, xv);
+      have_x = true;
     }
     float gs[UPP], us[UPP];
 #pragma unroll
