@@ -209,6 +209,16 @@ spp_status spp_profile_expert_copy(spp_ctx* ctx, int32_t l, int32_t reps, double
  * every context in the process. */
 spp_status spp_set_ffn_workgroups(spp_ctx* ctx, int32_t wgs);
 
+/* Test hooks for the copy/compute fences (for tests, not for production runs).
+ * Poison: before every expert copy the target slot is filled with 0xFF bytes
+ * (NaN in bf16 and fp32) on the copy stream, so a kernel that read a slot
+ * before its copy completed would produce NaN.  Copy delay: a bounded busy
+ * kernel of about delay_us (0..100000) runs on the copy stream before every
+ * copy, so copies are still in flight when the FFN is enqueued and the
+ * compute stream must wait on their events.  Outputs are unchanged by both. */
+spp_status spp_debug_set_poison(spp_ctx* ctx, int32_t enabled);
+spp_status spp_debug_set_copy_delay(spp_ctx* ctx, int32_t delay_us);
+
 /* ------------------------------------- host replacement policy (no device) */
 
 /* The slot-replacement and prefetch-selection policy the context runs for

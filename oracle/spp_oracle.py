@@ -344,7 +344,7 @@ class OracleWeights:
         return self._proj[l]
 
     def expert(self, l: int, e: int):
-        key = (l, e)
+        key = (self.cfg.expert_layer(l), e)   # tied layers share their expert weights
         if key in self._cache:
             return self._cache[key]
         w = tuple(self._dec(a) for a in self.gen.expert_weights(self.cfg, l, e))
@@ -353,6 +353,14 @@ class OracleWeights:
         if len(self._order) > self._cap:
             del self._cache[self._order.pop(0)]
         return w
+
+    def warm(self, threads: int = 16):
+        """Decode every expert of the offload tier ahead of time (in threads)."""
+        from concurrent.futures import ThreadPoolExecutor
+        self._cap = max(self._cap, self.cfg.host_layers * self.cfg.n + 8)
+        with ThreadPoolExecutor(max_workers=threads) as ex:
+            list(ex.map(lambda le: self.expert(*le),
+                        [(l, e) for l in range(self.cfg.host_layers) for e in range(self.cfg.n)]))
 
     def shared(self, l: int, j: int):
         key = (l, j)

@@ -66,6 +66,7 @@ hipError_t launch_router(const RouterArgs& a, int dtype, hipStream_t st);
 hipError_t launch_ffn(const FfnArgs& a, int grid, int dtype, hipStream_t st, hipEvent_t start, hipEvent_t stop);
 hipError_t launch_combine(const CombineArgs& a, int dtype, hipStream_t st);
 hipError_t launch_proj(const ProjArgs& a, int dtype, hipStream_t st);
+hipError_t launch_spin(uint64_t ticks, uint32_t max_iter, hipStream_t st);
 int ffn_grid_for(int nunits, int* upw);
 size_t ffn_max_grid();
 void set_ffn_target_wgs(int wgs);

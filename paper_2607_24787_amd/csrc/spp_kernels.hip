@@ -626,6 +626,17 @@ __global__ __launch_bounds__(kThreads) void proj_kernel(ProjArgs a) {
   }
 }
 
+// Bounded busy wait used only by the copy-delay test hook: returns after
+// `ticks` of the constant-rate wall clock or after `max_iter` sleeps, whichever
+// comes first.
+__global__ void spin_kernel(uint64_t ticks, uint32_t max_iter) {
+  const uint64_t t0 = wall_clock64();
+  for (uint32_t it = 0; it < max_iter; ++it) {
+    if (wall_clock64() - t0 >= ticks) break;
+    __builtin_amdgcn_s_sleep(8);
+  }
+}
+
 template <typename T>
 int nch_for(int D) {
   const int nch = D / Vec<T>::N;
@@ -709,6 +720,11 @@ hipError_t launch_combine(const CombineArgs& a, int dtype, hipStream_t st) {
 
 hipError_t launch_proj(const ProjArgs& a, int dtype, hipStream_t st) {
   return dtype == 1 ? proj_t<uint16_t>(a, st) : proj_t<float>(a, st);
+}
+
+hipError_t launch_spin(uint64_t ticks, uint32_t max_iter, hipStream_t st) {
+  hipLaunchKernelGGL(spin_kernel, dim3(1), dim3(64), 0, st, ticks, max_iter);
+  return hipGetLastError();
 }
 
 void set_ffn_target_wgs(int wgs) { g_ffn_target_wgs = wgs > 0 ? wgs : 256; }

@@ -82,6 +82,10 @@ struct spp_ctx {
   hipEvent_t ev_res = nullptr;
   int64_t clock = 0;
   int ffn_wgs = 256;
+  // test hooks
+  bool poison = false;
+  int32_t copy_delay_us = 0;
+  uint64_t wall_khz = 0;
   // last call record
   std::vector<spp::Transfer> last_loads, last_pref;
   std::vector<float> last_s;
@@ -179,6 +183,11 @@ spp_status issue_copies(spp_ctx* c, LayerState& ls, const std::vector<spp::Trans
   if (xs.empty()) return SPP_OK;
   if (ls.last_read_valid) SPP_HIP(hipStreamWaitEvent(c->copy, ls.last_read, 0));  // WAR on slot reuse
   for (const spp::Transfer& t : xs) {
+    if (c->copy_delay_us > 0) {
+      const uint64_t ticks = c->wall_khz * static_cast<uint64_t>(c->copy_delay_us) / 1000;
+      SPP_HIP(spp::launch_spin(ticks, static_cast<uint32_t>(c->copy_delay_us) * 64u + 1024u, c->copy));
+    }
+    if (c->poison) SPP_HIP(hipMemsetAsync(ls.slots + static_cast<size_t>(t.slot) * c->stride, 0xFF, c->blob_bytes, c->copy));
     SPP_HIP(hipMemcpyAsync(ls.slots + static_cast<size_t>(t.slot) * c->stride,
                            ls.host_store + static_cast<size_t>(t.expert) * c->stride, c->blob_bytes,
                            hipMemcpyHostToDevice, c->copy));
@@ -687,6 +696,25 @@ spp_status spp_profile_expert_copy(spp_ctx* c, int32_t l, int32_t reps, double* 
   *per_expert_us = 1e3 * elapsed(e0, e1) / reps;
   (void)hipEventDestroy(e0);
   (void)hipEventDestroy(e1);
+  return SPP_OK;
+}
+
+spp_status spp_debug_set_poison(spp_ctx* c, int32_t enabled) {
+  if (spp_status s = check_ctx(c)) return s;
+  c->poison = enabled != 0;
+  return SPP_OK;
+}
+
+spp_status spp_debug_set_copy_delay(spp_ctx* c, int32_t delay_us) {
+  if (spp_status s = check_ctx(c)) return s;
+  if (delay_us < 0 || delay_us > 100000) return fail(SPP_EINVAL, "delay_us must be in [0, 100000]");
+  if (delay_us > 0 && c->wall_khz == 0) {
+    int khz = 0;
+    SPP_HIP(hipDeviceGetAttribute(&khz, hipDeviceAttributeWallClockRate, c->device));
+    if (khz <= 0) return fail(SPP_EHIP, "wall clock rate unavailable");
+    c->wall_khz = static_cast<uint64_t>(khz);
+  }
+  c->copy_delay_us = delay_us;
   return SPP_OK;
 }
 

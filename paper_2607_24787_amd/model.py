@@ -44,7 +44,7 @@ class OffloadedMoEStack:
 
     def __init__(self, cfg, device: str = "cuda:0", S: Optional[int] = None,
                  resident: Optional[Sequence[int]] = None, adapter_values=None,
-                 threads: Optional[int] = None, host_layers: Optional[int] = None):
+                 threads: Optional[int] = None):
         import torch
         from workload import gen
 
@@ -60,8 +60,8 @@ class OffloadedMoEStack:
                                   rms_eps=cfg.rms_eps)
         self.stride = spp.spp_blob_stride(self.desc)
         self.elem = cfg.elem_bytes
-        # host_layers < L reuses host stores cyclically (tied offload tier) to bound pinned memory
-        self.host_layers = cfg.L if host_layers is None else max(1, min(host_layers, cfg.L))
+        # a tied offload tier (cfg.expert_layers) shares one host store between the layers it ties
+        self.host_layers = cfg.host_layers
         threads = threads or min(16, os.cpu_count() or 1)
 
         self.router, self.adapter, self.proj, self.shared, self.host = [], [], [], [], []

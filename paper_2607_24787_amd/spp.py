@@ -71,6 +71,8 @@ _SIGS = {
     "spp_reset_run_stats": (c_int32, [c_void_p]),
     "spp_profile_expert_copy": (c_int32, [c_void_p, c_int32, c_int32, POINTER(c_double)]),
     "spp_set_ffn_workgroups": (c_int32, [c_void_p, c_int32]),
+    "spp_debug_set_poison": (c_int32, [c_void_p, c_int32]),
+    "spp_debug_set_copy_delay": (c_int32, [c_void_p, c_int32]),
     "spp_policy_create": (c_int32, [c_int32, c_int32, POINTER(c_int32), c_int32, POINTER(c_void_p)]),
     "spp_policy_destroy": (c_int32, [c_void_p]),
     "spp_policy_on_demand": (c_int32, [c_void_p, POINTER(c_int32), c_int32, c_int64, POINTER(c_int32),
@@ -260,6 +262,14 @@ def spp_profile_expert_copy(ctx, l, reps) -> float:
 
 def spp_set_ffn_workgroups(ctx, wgs: int):
     _check(lib().spp_set_ffn_workgroups(c_void_p(ctx), wgs))
+
+
+def spp_debug_set_poison(ctx, enabled: bool):
+    _check(lib().spp_debug_set_poison(c_void_p(ctx), int(bool(enabled))))
+
+
+def spp_debug_set_copy_delay(ctx, delay_us: int):
+    _check(lib().spp_debug_set_copy_delay(c_void_p(ctx), delay_us))
 
 
 # ------------------------------------------------------- host policy (no GPU)

@@ -58,7 +58,8 @@ def _prefetch_gap(s: np.ndarray, occupied: np.ndarray, M: int) -> float:
 def run_lockstep(stack, cfg, tokens: int, M_max: int, check_x: bool = True) -> LockstepReport:
     from paper_2607_24787_amd import spp
 
-    W = o.OracleWeights(cfg, cache_experts=4 * cfg.n)
+    W = o.OracleWeights(cfg, cache_experts=cfg.host_layers * cfg.n + 8)
+    W.warm()
     h0 = gen.hidden_states(cfg, tokens=tokens)
     S = stack.S
     res = list(range(min(S, cfg.n)))

@@ -1,0 +1,81 @@
+"""Copy/compute fence tests on the device.
+
+The FFN may read a slot only after the copy into it completed (RAW), and a
+copy may overwrite a slot only after the last kernel that read it (WAR).  With
+every copied slot poisoned with NaN bytes just before its copy, and every copy
+held back by a bounded busy kernel on the copy stream, outputs must stay
+bitwise identical to an unpoisoned, undelayed run, and contain no NaN.
+"""
+import sys
+
+import numpy as np
+import pytest
+
+import oracle as o
+import workload as w
+from workload import gen
+
+pytestmark = pytest.mark.gpu
+
+RAGGED = w.MoEConfig(name="ragged_bf16_D640_n40_k5", L=3, D=640, n=40, K=5, I=100, r=12, S=11, windows=(2,),
+                     tokens=16, seed=3)
+
+
+def _log(msg):
+    print(msg, flush=True)
+    sys.stdout.flush()
+
+
+@pytest.fixture(scope="module")
+def torch_cuda():
+    import torch
+    if not torch.cuda.is_available():
+        pytest.skip("no GPU")
+    return torch
+
+
+def _run(cfg, M_max, tokens, poison=False, delay_us=0):
+    from paper_2607_24787_amd import spp
+    from paper_2607_24787_amd.model import OffloadedMoEStack
+    h0 = gen.hidden_states(cfg, tokens=tokens)
+    st = OffloadedMoEStack(cfg)
+    try:
+        spp.spp_debug_set_poison(st.ctx, poison)
+        spp.spp_debug_set_copy_delay(st.ctx, delay_us)
+        outs, on_time, needed, misses = [], 0, 0, 0
+        for t in range(tokens):
+            res = st.step(h0[t], M_max)
+            for topk, _, stats in res:
+                on_time += stats.ready_on_time
+                needed += len(set(topk.ravel().tolist()))
+                misses += stats.misses
+            outs.append(st.download(st.hbuf[st.last_buf]))
+        return np.stack(outs), on_time, needed, misses
+    finally:
+        st.close()
+
+
+@pytest.mark.parametrize("cfg,M_max,tokens", [(RAGGED, 2, 12), (w.get("c0"), 1, 16)], ids=["ragged", "c0"])
+def test_poisoned_delayed_copies_leave_outputs_unchanged(torch_cuda, cfg, M_max, tokens):
+    _log(f"[fences] {cfg.name} M_max={M_max}")
+    ref, ref_on_time, needed, misses = _run(cfg, M_max, tokens)
+    assert misses > 0, "the case must exercise on-demand loads"
+    assert not np.isnan(o.decode(ref, cfg.dtype)).any()
+    for poison, delay in [(True, 0), (True, 300), (False, 300)]:
+        out, on_time, needed2, _ = _run(cfg, M_max, tokens, poison, delay)
+        assert needed2 == needed
+        dec = o.decode(out, cfg.dtype)
+        assert not np.isnan(dec).any(), (poison, delay)
+        assert np.array_equal(out, ref), (poison, delay)
+        if delay:
+            # held-back copies were still in flight when the FFN was enqueued:
+            # the compute stream had to wait on their events
+            assert on_time < needed, (on_time, needed)
+        _log(f"[fences] poison={poison} delay={delay}us ready_on_time={on_time}/{needed}")
+
+
+def test_repeat_runs_are_bitwise_identical(torch_cuda):
+    cfg = w.get("c1")
+    a, _, _, _ = _run(cfg, cfg.window, 6)
+    b, _, _, _ = _run(cfg, cfg.window, 6, poison=True)
+    assert np.array_equal(a, b)

@@ -42,6 +42,10 @@ PROJ = w.MoEConfig(name="proj_bf16_D512_n16_k4", L=3, D=512, n=16, K=4, I=128, r
 BATCH = w.MoEConfig(name="batch3_f32_D128_n12_k3", L=2, D=128, n=12, K=3, I=64, r=8, S=12, windows=(2,),
                     tokens=8, batch=3, dtype="f32", seed=9)
 C3_SHORT = w.get("c3").with_(L=3, tokens=6)
+# the full 12-layer DeepSeek-shaped stack and the 48-layer Qwen-shaped stack
+# with its stand-in projection (offload tier tied over 2 expert-weight layers)
+C3_FULL = w.get("c3").with_(tokens=4)
+C2_TIED = w.get("c2").with_(tokens=2, expert_layers=2)
 
 
 def _assert_report(rep, cfg, name):
@@ -68,6 +72,18 @@ def test_lockstep_parity(torch_cuda, cfg, M_max, tokens):
     st = _stack(cfg)
     try:
         rep = run_lockstep(st, cfg, tokens, M_max)
+    finally:
+        st.close()
+    _assert_report(rep, cfg, cfg.name)
+
+
+@pytest.mark.parametrize("cfg,tokens", [(C3_FULL, 4), (C2_TIED, 2)], ids=["c3_stack12", "c2_stack48_tied"])
+def test_lockstep_parity_full_stacks(torch_cuda, cfg, tokens):
+    from lockstep import run_lockstep
+    _log(f"[lockstep] {cfg.name} L={cfg.L} tokens={tokens}")
+    st = _stack(cfg)
+    try:
+        rep = run_lockstep(st, cfg, tokens, cfg.window)
     finally:
         st.close()
     _assert_report(rep, cfg, cfg.name)

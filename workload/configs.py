@@ -49,6 +49,10 @@ class MoEConfig:
     w_std: float = 0.02          # std of router, expert, shared-expert and projection weights
     adapter_noise: float = 0.005  # std of the noise added to the SVD-built adapters
     rms_eps: float = 1e-6
+    # 0: every layer has its own experts.  E > 0: layer l's expert weights are
+    # those of layer l mod E (a tied offload tier that bounds pinned host
+    # memory; routers, adapters and slot pools stay per layer).
+    expert_layers: int = 0
 
     @property
     def elem_bytes(self) -> int:
@@ -62,6 +66,15 @@ class MoEConfig:
     @property
     def blob_bytes(self) -> int:
         return self.blob_elems * self.elem_bytes
+
+    def expert_layer(self, layer: int) -> int:
+        """The layer whose seeded expert weights layer `layer` uses."""
+        return layer % self.expert_layers if self.expert_layers > 0 else layer
+
+    @property
+    def host_layers(self) -> int:
+        """Distinct expert-weight layers in the offload tier."""
+        return min(self.expert_layers, self.L) if self.expert_layers > 0 else self.L
 
     @property
     def window(self) -> int:

@@ -68,9 +68,10 @@ def router_weight(cfg: MoEConfig, layer: int) -> np.ndarray:
 
 def expert_weights(cfg: MoEConfig, layer: int, expert: int):
     """Routed expert ``expert`` of ``layer``: (gate [I,D], up [I,D], down [D,I])."""
-    return (_normal_weights(cfg, KIND_GATE, layer, expert, (cfg.I, cfg.D)),
-            _normal_weights(cfg, KIND_UP, layer, expert, (cfg.I, cfg.D)),
-            _normal_weights(cfg, KIND_DOWN, layer, expert, (cfg.D, cfg.I)))
+    src = cfg.expert_layer(layer)
+    return (_normal_weights(cfg, KIND_GATE, src, expert, (cfg.I, cfg.D)),
+            _normal_weights(cfg, KIND_UP, src, expert, (cfg.I, cfg.D)),
+            _normal_weights(cfg, KIND_DOWN, src, expert, (cfg.D, cfg.I)))
 
 
 def shared_expert_weights(cfg: MoEConfig, layer: int, j: int):
