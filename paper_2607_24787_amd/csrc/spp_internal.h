@@ -45,6 +45,33 @@ struct FfnArgs {
   float* partial;              // [gridDim.x, D]
 };
 
+// Batched decode: one group = up to kGroupTokens tokens that share one expert.
+constexpr int kGroupTokens = 16;
+struct GroupDesc {
+  const void* blob;                // expert blob (slot or shared expert)
+  int32_t m;                       // tokens in the group, 1..kGroupTokens
+  int32_t tok[kGroupTokens];       // token index b of each row
+  int32_t pair[kGroupTokens];      // output pair: b*K + k (routed) or B*K + b*n_shared + j (shared)
+  int32_t pad;
+};
+
+struct GroupArgs {
+  const GroupDesc* groups;  // [ngroups] (device)
+  int ngroups, nsplit, upw; // each group's I units are split into nsplit ranges of upw units
+  int I, D;
+  const float* x;           // [B, D] router inputs
+  float* ypart;             // [npairs * nsplit, D] partial expert outputs
+};
+
+struct CombineBArgs {
+  const float* ypart;       // [npairs * nsplit, D]
+  const float* gates;       // [B, K]
+  int B, K, n_shared, nsplit, D;
+  const void* res_h;        // [B, D] residual in storage dtype (used when res_u == nullptr)
+  const float* res_u;       // [B, D] fp32 residual (prologue output)
+  void* out;                // [B, D] storage dtype
+};
+
 struct CombineArgs {
   const float* partial;  // [nparts, D]
   int nparts, D;
@@ -66,6 +93,9 @@ hipError_t launch_router(const RouterArgs& a, int dtype, hipStream_t st);
 hipError_t launch_ffn(const FfnArgs& a, int grid, int dtype, hipStream_t st, hipEvent_t start, hipEvent_t stop);
 hipError_t launch_combine(const CombineArgs& a, int dtype, hipStream_t st);
 hipError_t launch_proj(const ProjArgs& a, int dtype, hipStream_t st);
+// Grouped (batched) routed-expert FFN, bf16 only; D % 256 == 0.
+hipError_t launch_ffn_grouped(const GroupArgs& a, hipStream_t st, hipEvent_t start, hipEvent_t stop);
+hipError_t launch_combine_batched(const CombineBArgs& a, int dtype, hipStream_t st);
 hipError_t launch_spin(uint64_t ticks, uint32_t max_iter, hipStream_t st);
 int ffn_grid_for(int nunits, int* upw);
 size_t ffn_max_grid();

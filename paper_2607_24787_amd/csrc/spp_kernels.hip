@@ -597,6 +597,184 @@ __global__ __launch_bounds__(64 * kCombGroups) void ffn_combine_kernel(CombineAr
   }
 }
 
+// ---------------------------------------------------------------------------
+// Batched decode: each workgroup takes one group (up to 16 tokens routed to
+// the same expert) and one range of upw units of that expert.
+//   phase A: G = X W_gate^T and U = X W_up^T on MFMA (v_mfma_f32_16x16x32_bf16,
+//            tokens padded to the 16 rows of the tile, units as the 16
+//            columns, D as the contraction).  x is staged in LDS per
+//            512-wide chunk as a bf16 pair x = hi + lo (hi = bf16(x),
+//            lo = bf16(x - hi)), and both halves are multiplied, so the
+//            contraction keeps x to ~2^-17 relative (the weights are bf16
+//            already); H = silu(G) * U into LDS (fp32).
+//   phase B: each wave streams the down columns of the range over its
+//            256-wide slices of D and accumulates H[t][i] * down_i for every
+//            token of the group; one partial output row per (token, range).
+// ---------------------------------------------------------------------------
+constexpr int kGrpWaves = 8;
+constexpr int kGrpThreads = 64 * kGrpWaves;
+constexpr int kGrpKC = 512;     // x columns staged per chunk
+constexpr int kGrpMaxUpw = 256; // units per range
+
+typedef __bf16 bf16x8 __attribute__((ext_vector_type(8)));
+typedef float f32x4 __attribute__((ext_vector_type(4)));
+
+__device__ __forceinline__ uint16_t f32_to_bf16_rne(float v) {
+  uint32_t b = __float_as_uint(v);
+  if ((b & 0x7fffffffu) > 0x7f800000u) return 0x7fc0;
+  b += 0x7fffu + ((b >> 16) & 1u);
+  return static_cast<uint16_t>(b >> 16);
+}
+
+__global__ __launch_bounds__(kGrpThreads) void ffn_grouped_kernel(GroupArgs a) {
+  __shared__ uint16_t s_xh[kGroupTokens * kGrpKC];  // 16 KiB, bf16(x)
+  __shared__ uint16_t s_xl[kGroupTokens * kGrpKC];  // 16 KiB, bf16(x - bf16(x))
+  __shared__ float s_h[kGroupTokens * kGrpMaxUpw];  // 16 KiB
+  const int tid = threadIdx.x, lane = tid & 63;
+  const int wave = __builtin_amdgcn_readfirstlane(tid >> 6);
+  const int D = a.D;
+  const int g = blockIdx.x / a.nsplit, split = blockIdx.x - g * a.nsplit;
+  const GroupDesc* G = a.groups + g;
+  const int m = G->m;
+  const int i0 = split * a.upw;
+  const int nu = min(a.upw, a.I - i0);
+  const uint16_t* blob = reinterpret_cast<const uint16_t*>(G->blob);
+  const size_t unit_elems = static_cast<size_t>(3) * D;
+
+  // ---- phase A: gate / up tiles of 16 units on MFMA
+  const int ntiles = (nu + 15) >> 4;
+  constexpr int kMaxTilesPerWave = kGrpMaxUpw / 16 / kGrpWaves;  // 2
+  f32x4 accg[kMaxTilesPerWave], accu[kMaxTilesPerWave];
+#pragma unroll
+  for (int q = 0; q < kMaxTilesPerWave; ++q) accg[q] = accu[q] = f32x4{0.f, 0.f, 0.f, 0.f};
+  const int krow = lane & 15;         // A row (token) and B column (unit) of this lane
+  const int koff = 8 * (lane >> 4);   // this lane's 8-wide k slice inside a 32-wide step
+  for (int kc = 0; kc < D; kc += kGrpKC) {
+    const int kw = min(kGrpKC, D - kc);
+    __syncthreads();  // previous chunk consumed
+    for (int idx = tid; idx < kGroupTokens * (kw / 4); idx += kGrpThreads) {
+      const int t = idx / (kw / 4), c4 = idx - t * (kw / 4);
+      float4 v = make_float4(0.f, 0.f, 0.f, 0.f);
+      if (t < m) v = *SPP_GLOBAL(float4, a.x + static_cast<size_t>(G->tok[t]) * D + kc + 4 * c4);
+      const float vv[4] = {v.x, v.y, v.z, v.w};
+      uint16_t* dh = s_xh + t * kGrpKC + 4 * c4;
+      uint16_t* dl = s_xl + t * kGrpKC + 4 * c4;
+#pragma unroll
+      for (int q = 0; q < 4; ++q) {
+        const uint16_t hi = f32_to_bf16_rne(vv[q]);
+        dh[q] = hi;
+        dl[q] = f32_to_bf16_rne(vv[q] - __uint_as_float(static_cast<uint32_t>(hi) << 16));
+      }
+    }
+    __syncthreads();
+#pragma unroll
+    for (int q = 0; q < kMaxTilesPerWave; ++q) {
+      const int tile = wave + q * kGrpWaves;
+      if (tile >= ntiles) break;  // wave-uniform
+      const int ul = tile * 16 + krow;
+      const bool uok = ul < nu;
+      const uint16_t* grow = blob + static_cast<size_t>(i0 + (uok ? ul : 0)) * unit_elems + kc;
+      const uint16_t* urow = grow + D;
+#pragma unroll 4
+      for (int ks = 0; ks < kw; ks += 32) {
+        const u32x4 ah = *reinterpret_cast<const u32x4*>(s_xh + krow * kGrpKC + ks + koff);
+        const u32x4 al = *reinterpret_cast<const u32x4*>(s_xl + krow * kGrpKC + ks + koff);
+        u32x4 bg = u32x4{0u, 0u, 0u, 0u}, bu = u32x4{0u, 0u, 0u, 0u};
+        if (uok) {
+          bg = __builtin_nontemporal_load(SPP_GLOBAL(u32x4, grow + ks + koff));
+          bu = __builtin_nontemporal_load(SPP_GLOBAL(u32x4, urow + ks + koff));
+        }
+        const bf16x8 wg = __builtin_bit_cast(bf16x8, bg), wu = __builtin_bit_cast(bf16x8, bu);
+        accg[q] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(__builtin_bit_cast(bf16x8, ah), wg, accg[q], 0, 0, 0);
+        accg[q] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(__builtin_bit_cast(bf16x8, al), wg, accg[q], 0, 0, 0);
+        accu[q] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(__builtin_bit_cast(bf16x8, ah), wu, accu[q], 0, 0, 0);
+        accu[q] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(__builtin_bit_cast(bf16x8, al), wu, accu[q], 0, 0, 0);
+      }
+    }
+  }
+  // this lane holds rows (tokens) 4*(lane/16)+j of column (unit) lane%16
+#pragma unroll
+  for (int q = 0; q < kMaxTilesPerWave; ++q) {
+    const int tile = wave + q * kGrpWaves;
+    if (tile >= ntiles) break;
+    const int ul = tile * 16 + krow;
+    if (ul < nu) {
+#pragma unroll
+      for (int j = 0; j < 4; ++j) {
+        const int t = 4 * (lane >> 4) + j;
+        const float gv = accg[q][j];
+        s_h[t * kGrpMaxUpw + ul] = gv / (1.f + expf(-gv)) * accu[q][j];
+      }
+    }
+  }
+  __syncthreads();
+
+  // ---- phase B: down columns over 256-wide slices of D, all tokens of the group
+  for (int dc = wave; dc * 256 < D; dc += kGrpWaves) {
+    const int d0 = dc * 256 + lane * 4;
+    float acc[kGroupTokens][4];
+#pragma unroll
+    for (int t = 0; t < kGroupTokens; ++t)
+#pragma unroll
+      for (int v = 0; v < 4; ++v) acc[t][v] = 0.f;
+    const uint16_t* dcol = blob + static_cast<size_t>(i0) * unit_elems + 2 * D + d0;
+    for (int u = 0; u < nu; u += 8) {
+      uint2 raw[8];
+#pragma unroll
+      for (int uu = 0; uu < 8; ++uu) {
+        raw[uu] = make_uint2(0u, 0u);
+        if (u + uu < nu) raw[uu] = *SPP_GLOBAL(uint2, dcol + static_cast<size_t>(u + uu) * unit_elems);
+      }
+#pragma unroll
+      for (int uu = 0; uu < 8; ++uu) {
+        if (u + uu >= nu) break;
+        const float dv[4] = {__uint_as_float(raw[uu].x << 16), __uint_as_float(raw[uu].x & 0xffff0000u),
+                             __uint_as_float(raw[uu].y << 16), __uint_as_float(raw[uu].y & 0xffff0000u)};
+#pragma unroll
+        for (int t = 0; t < kGroupTokens; ++t) {
+          if (t < m) {
+            const float h = s_h[t * kGrpMaxUpw + u + uu];
+#pragma unroll
+            for (int v = 0; v < 4; ++v) acc[t][v] += h * dv[v];
+          }
+        }
+      }
+    }
+#pragma unroll
+    for (int t = 0; t < kGroupTokens; ++t) {
+      if (t < m) {
+        float* dst = a.ypart + (static_cast<size_t>(G->pair[t]) * a.nsplit + split) * D + d0;
+        *reinterpret_cast<float4*>(dst) = make_float4(acc[t][0], acc[t][1], acc[t][2], acc[t][3]);
+      }
+    }
+  }
+}
+
+// Batched combine: h_out[b] = round(residual[b] + sum_k g_bk sum_r ypart[(b,k), r]
+//                                   + sum_j sum_r ypart[(b, shared j), r]), fixed order.
+template <typename T>
+__global__ __launch_bounds__(256) void ffn_combine_batched_kernel(CombineBArgs a) {
+  const int b = blockIdx.y;
+  const int d = blockIdx.x * 256 + threadIdx.x;
+  if (d >= a.D) return;
+  float y = 0.f;
+  for (int k = 0; k < a.K; ++k) {
+    const size_t row = static_cast<size_t>(b * a.K + k) * a.nsplit;
+    float v = 0.f;
+    for (int r = 0; r < a.nsplit; ++r) v += a.ypart[(row + r) * a.D + d];
+    y += a.gates[b * a.K + k] * v;
+  }
+  for (int j = 0; j < a.n_shared; ++j) {
+    const size_t row = static_cast<size_t>(a.B * a.K + b * a.n_shared + j) * a.nsplit;
+    float v = 0.f;
+    for (int r = 0; r < a.nsplit; ++r) v += a.ypart[(row + r) * a.D + d];
+    y += v;
+  }
+  const size_t o = static_cast<size_t>(b) * a.D + d;
+  const float res = a.res_u ? a.res_u[o] : load_elem<T>(a.res_h, o);
+  store_elem<T>(a.out, o, res + y);
+}
+
 // Stand-in projection prologue: u = h + P rms(h) (fp32 result).  One wave per row of P.
 template <typename T, int NCH>
 __global__ __launch_bounds__(kThreads) void proj_kernel(ProjArgs a) {
@@ -720,6 +898,27 @@ hipError_t launch_combine(const CombineArgs& a, int dtype, hipStream_t st) {
 
 hipError_t launch_proj(const ProjArgs& a, int dtype, hipStream_t st) {
   return dtype == 1 ? proj_t<uint16_t>(a, st) : proj_t<float>(a, st);
+}
+
+hipError_t launch_ffn_grouped(const GroupArgs& a, hipStream_t st, hipEvent_t start, hipEvent_t stop) {
+  if (a.ngroups <= 0 || a.nsplit <= 0 || a.upw <= 0 || a.upw > kGrpMaxUpw || a.D % 256 != 0 ||
+      a.nsplit * a.upw < a.I)
+    return hipErrorInvalidValue;
+  const dim3 grid(static_cast<unsigned>(a.ngroups * a.nsplit));
+  if (start || stop)
+    hipExtLaunchKernelGGL(ffn_grouped_kernel, grid, dim3(kGrpThreads), 0, st, start, stop, 0u, a);
+  else
+    hipLaunchKernelGGL(ffn_grouped_kernel, grid, dim3(kGrpThreads), 0, st, a);
+  return hipGetLastError();
+}
+
+hipError_t launch_combine_batched(const CombineBArgs& a, int dtype, hipStream_t st) {
+  const dim3 grid((a.D + 255) / 256, a.B);
+  if (dtype == 1)
+    hipLaunchKernelGGL((ffn_combine_batched_kernel<uint16_t>), grid, dim3(256), 0, st, a);
+  else
+    hipLaunchKernelGGL((ffn_combine_batched_kernel<float>), grid, dim3(256), 0, st, a);
+  return hipGetLastError();
 }
 
 hipError_t launch_spin(uint64_t ticks, uint32_t max_iter, hipStream_t st) {

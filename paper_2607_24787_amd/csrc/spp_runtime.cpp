@@ -79,6 +79,12 @@ struct spp_ctx {
   unsigned* counter = nullptr;
   float* partial = nullptr;    // [ffn_max_grid, D]
   uint8_t* probe_dev = nullptr;  // one blob, for copy profiling
+  // batched decode (B > 1, bf16): expert groups and partial outputs
+  bool grouped = false;
+  int max_groups = 0, max_nsplit = 0;
+  spp::GroupDesc* groups_dev = nullptr;
+  spp::GroupDesc* groups_host = nullptr;  // pinned staging for the per-layer group list
+  float* ypart = nullptr;
   hipEvent_t ev_res = nullptr;
   int64_t clock = 0;
   int ffn_wgs = 256;
@@ -240,6 +246,9 @@ void free_ctx(spp_ctx* c) {
                   static_cast<void*>(c->probe_dev)})
     if (p) (void)hipFree(p);
   if (c->res_host) (void)hipHostFree(c->res_host);
+  if (c->groups_host) (void)hipHostFree(c->groups_host);
+  if (c->groups_dev) (void)hipFree(c->groups_dev);
+  if (c->ypart) (void)hipFree(c->ypart);
   if (c->ev_res) (void)hipEventDestroy(c->ev_res);
   if (c->copy) (void)hipStreamDestroy(c->copy);
   delete c;
@@ -285,12 +294,89 @@ spp_status create_impl(const spp_model_desc* desc, void* stream, spp_ctx** out) 
     return fail(SPP_ENOMEM, "pinned result buffer allocation failed");
   SPP_HIP(hipHostGetDevicePointer(reinterpret_cast<void**>(&c->res_host_dev), c->res_host, 0));
   std::memset(c->res_host, 0, c->res_bytes);
+  // batched decode runs the routed experts as grouped MFMA contractions
+  c->grouped = d.max_batch > 1 && d.dtype == SPP_DTYPE_BF16 && d.D % 256 == 0;
+  if (c->grouped) {
+    c->max_groups = d.max_batch * d.K + d.n_shared * ((d.max_batch + spp::kGroupTokens - 1) / spp::kGroupTokens);
+    c->max_nsplit = (d.I + 127) / 128;
+    const size_t npairs = static_cast<size_t>(d.max_batch) * (d.K + d.n_shared);
+    if (hipMalloc(&c->groups_dev, sizeof(spp::GroupDesc) * c->max_groups) != hipSuccess ||
+        hipHostMalloc(&c->groups_host, sizeof(spp::GroupDesc) * c->max_groups, hipHostMallocDefault) != hipSuccess ||
+        hipMalloc(&c->ypart, npairs * c->max_nsplit * d.D * sizeof(float)) != hipSuccess)
+      return fail(SPP_ENOMEM, "batched-decode buffers allocation failed");
+  }
   SPP_HIP(hipMemset(c->counter, 0, 256));
   SPP_HIP(hipMemset(c->res_dev, 0, c->res_bytes));
   SPP_HIP(hipEventCreateWithFlags(&c->ev_res, hipEventDisableTiming));
   c->last_s.assign(d.n, 0.f);
   SPP_HIP(hipDeviceSynchronize());
   *out = c.release();
+  return SPP_OK;
+}
+
+// Batched decode: group the (token, k) pairs by expert (ascending expert,
+// ascending token, at most kGroupTokens per group), then the shared experts
+// over all tokens; upload the list; one grouped FFN launch and one combine.
+spp_status grouped_ffn(spp_ctx* c, LayerState& ls, const int32_t* T, int32_t B, const void* h_in, void* h_out,
+                       TimingSet& ts) {
+  const spp_model_desc& d = c->d;
+  std::vector<std::vector<std::pair<int32_t, int32_t>>> by_expert(d.n);  // (token, pair)
+  for (int32_t b = 0; b < B; ++b)
+    for (int32_t k = 0; k < d.K; ++k) by_expert[T[b * d.K + k]].push_back({b, b * d.K + k});
+  int ng = 0;
+  auto add = [&](const void* blob, const std::vector<std::pair<int32_t, int32_t>>& rows) {
+    for (size_t r0 = 0; r0 < rows.size(); r0 += spp::kGroupTokens) {
+      spp::GroupDesc& g = c->groups_host[ng++];
+      std::memset(&g, 0, sizeof(g));
+      g.blob = blob;
+      g.m = static_cast<int32_t>(std::min<size_t>(spp::kGroupTokens, rows.size() - r0));
+      for (int32_t t = 0; t < g.m; ++t) {
+        g.tok[t] = rows[r0 + t].first;
+        g.pair[t] = rows[r0 + t].second;
+      }
+    }
+  };
+  for (int32_t e = 0; e < d.n; ++e)
+    if (!by_expert[e].empty())
+      add(ls.slots + static_cast<size_t>(ls.policy->slot_of(e)) * c->stride, by_expert[e]);
+  for (int32_t j = 0; j < d.n_shared; ++j) {
+    std::vector<std::pair<int32_t, int32_t>> rows;
+    for (int32_t b = 0; b < B; ++b) rows.push_back({b, B * d.K + b * d.n_shared + j});
+    add(static_cast<const uint8_t*>(ls.shared) + static_cast<size_t>(j) * c->stride, rows);
+  }
+  if (ng > c->max_groups) return fail(SPP_ESTATE, "group list overflow");
+  SPP_HIP(hipMemcpyAsync(c->groups_dev, c->groups_host, sizeof(spp::GroupDesc) * ng, hipMemcpyHostToDevice,
+                         c->compute));
+  // unit ranges of 128 or 256 units, about 512 workgroups in total
+  const int target = std::max(1, (512 + ng - 1) / ng);
+  int upw = 128 * std::max(1, static_cast<int>(std::lround(static_cast<double>(d.I) / (128.0 * target))));
+  upw = std::min(upw, 256);
+  const int nsplit = (d.I + upw - 1) / upw;
+  if (nsplit > c->max_nsplit) return fail(SPP_ESTATE, "unit split exceeds the partial buffer");
+  spp::GroupArgs ga{};
+  ga.groups = c->groups_dev;
+  ga.ngroups = ng;
+  ga.nsplit = nsplit;
+  ga.upw = upw;
+  ga.I = d.I;
+  ga.D = d.D;
+  ga.x = c->x_dev;
+  ga.ypart = c->ypart;
+  SPP_HIP(spp::launch_ffn_grouped(ga, c->compute, c->timing ? ts.ev[kEvFfnBegin] : nullptr,
+                                  c->timing ? ts.ev[kEvFfnEnd] : nullptr));
+  spp::CombineBArgs cb{};
+  cb.ypart = c->ypart;
+  cb.gates = reinterpret_cast<const float*>(c->res_dev + c->off_gates);
+  cb.B = B;
+  cb.K = d.K;
+  cb.n_shared = d.n_shared;
+  cb.nsplit = nsplit;
+  cb.D = d.D;
+  cb.res_h = h_in;
+  cb.res_u = d.has_proj ? c->u_dev : nullptr;
+  cb.out = h_out;
+  SPP_HIP(spp::launch_combine_batched(cb, d.dtype, c->compute));
+  c->stats.ffn_launches += 1;
   return SPP_OK;
 }
 
@@ -411,7 +497,10 @@ spp_status layer_forward_impl(spp_ctx* c, int32_t l, const void* h_in, void* h_o
     }
   }
   if (c->timing) SPP_HIP(hipEventRecord(ts.ev[kEvWaitB], c->compute));
-  for (int32_t b = 0; b < B; ++b) {
+  if (c->grouped && B > 1) {
+    if (spp_status e = grouped_ffn(c, ls, T, B, h_in, h_out, ts)) return e;
+  }
+  for (int32_t b = 0; b < B && !(c->grouped && B > 1); ++b) {
     spp::FfnArgs fa{};
     int nW = 0;
     for (int32_t k = 0; k < d.K; ++k) {

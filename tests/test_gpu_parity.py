@@ -45,6 +45,12 @@ C3_SHORT = w.get("c3").with_(L=3, tokens=6)
 # the full 12-layer DeepSeek-shaped stack and the 48-layer Qwen-shaped stack
 # with its stand-in projection (offload tier tied over 2 expert-weight layers)
 C3_FULL = w.get("c3").with_(tokens=4)
+# batched decode (grouped MFMA path): ragged unit ranges; the Qwen shape at 16
+# sequences with the stand-in projection; the DeepSeek shape with shared experts
+BATCH_BF16 = w.MoEConfig(name="batch5_bf16_D512_n24_k4_I160", L=2, D=512, n=24, K=4, I=160, r=8, S=24,
+                         windows=(2,), tokens=6, batch=5, seed=13)
+QWEN_B16 = w.get("c4").with_(L=2, batch=16, S=128, tokens=3)
+DSV2_B4 = w.get("c3").with_(L=2, batch=4, S=64, tokens=3)
 C2_TIED = w.get("c2").with_(tokens=2, expert_layers=2)
 
 
@@ -69,6 +75,19 @@ def _assert_report(rep, cfg, name):
 def test_lockstep_parity(torch_cuda, cfg, M_max, tokens):
     from lockstep import run_lockstep
     _log(f"[lockstep] {cfg.name} M_max={M_max} tokens={tokens}")
+    st = _stack(cfg)
+    try:
+        rep = run_lockstep(st, cfg, tokens, M_max)
+    finally:
+        st.close()
+    _assert_report(rep, cfg, cfg.name)
+
+
+@pytest.mark.parametrize("cfg,M_max,tokens", [(BATCH_BF16, 2, 6), (QWEN_B16, 4, 3), (DSV2_B4, 2, 3)],
+                         ids=["batch5_bf16", "qwen_b16", "dsv2_b4"])
+def test_lockstep_parity_batched_grouped(torch_cuda, cfg, M_max, tokens):
+    from lockstep import run_lockstep
+    _log(f"[lockstep] {cfg.name} B={cfg.batch} M_max={M_max} tokens={tokens}")
     st = _stack(cfg)
     try:
         rep = run_lockstep(st, cfg, tokens, M_max)
