@@ -65,12 +65,15 @@ def run_mode(stack, dev_h, row_bytes, warmup, steps, M_max):
     spp.spp_set_timing(stack.ctx, 1)
     hits_target = 0
     hits_first = 0
+    distinct = 0
     t0 = time.perf_counter()
     for t in range(warmup, warmup + steps):
         out = stack.step_from(base + t * row_bytes, M_max)
-        hits_first += out[0][2].hits
+        hits_first += out[0][2].token_hits
         for l in range(1, cfg.L):
-            hits_target += out[l][2].hits
+            hits_target += out[l][2].token_hits
+        for l in range(cfg.L):
+            distinct += out[l][2].hits + out[l][2].misses
     torch.cuda.synchronize()
     wall = time.perf_counter() - t0
     rs = spp.spp_get_run_stats(stack.ctx)
@@ -95,6 +98,7 @@ def run_mode(stack, dev_h, row_bytes, warmup, steps, M_max):
         "ready_on_time_frac": rs.ready_on_time / max(rs.hits + rs.misses, 1),
         "copy_bytes": rs.copy_bytes,
         "h2d_gbs_during_run": rs.copy_bytes / (rs.span_us * 1e3) if rs.span_us > 0 else None,
+        "distinct_experts_per_layer": distinct / (steps * cfg.L),
         "window_us": rs.window_us / rs.window_samples if rs.window_samples else None,
         "compute_window_us": rs.compute_window_us / rs.window_samples if rs.window_samples else None,
         "combine_us_per_layer": rs.tail_us / max(rs.layer_calls, 1),
@@ -139,6 +143,9 @@ def main():
     ap.add_argument("--cpu-tokens", type=int, default=96, help="oracle sample size (0 disables)")
     ap.add_argument("--ablation", type=int, default=1, help="also time OFF and PRED0 modes")
     ap.add_argument("--ffn-wgs", type=int, default=0, help="FFN workgroups (0: library default)")
+    ap.add_argument("--batch", type=int, default=0, help="override the workload's batch (0: keep)")
+    ap.add_argument("--slots", type=int, default=0, help="override HBM slots per layer (0: keep)")
+    ap.add_argument("--layers", type=int, default=0, help="override the layer count (0: keep)")
     ap.add_argument("--copy-probe", action="store_true",
                     help="only run a 256 MiB device-to-device copy three times (counter calibration)")
     args = ap.parse_args()
@@ -167,6 +174,9 @@ def main():
     from workload import gen
 
     cfg = workload.get(args.workload)
+    over = {k: v for k, v in (("batch", args.batch), ("S", args.slots), ("L", args.layers)) if v > 0}
+    if over:
+        cfg = cfg.with_(**over)
     total = args.warmup + args.steps
     t_setup = time.perf_counter()
     h_all = gen.hidden_states(cfg, tokens=total)                      # [T, B, D] storage
@@ -195,7 +205,9 @@ def main():
     window_us = on["compute_window_us"]
     implied_budget = (spp.select_prefetch_budget(window_us, per_expert_us, cfg.n)
                       if window_us is not None else None)
-    ffn_bytes = cfg.K * cfg.blob_bytes + cfg.n_shared * cfg.blob_bytes   # algorithmic bytes per FFN launch
+    # algorithmic bytes per FFN launch: every distinct expert the batch routes to, streamed once
+    distinct = on["distinct_experts_per_layer"] if cfg.batch > 1 else cfg.K
+    ffn_bytes = int(round((distinct + cfg.n_shared) * cfg.blob_bytes))
     achieved = ffn_bytes / (on["ffn_kernel_us"] * 1e3)                   # GB/s
     traffic = None
     if cfg.name == "qwen3vl30b_a3b_layer_bf16":
@@ -214,7 +226,8 @@ def main():
         "vs_baseline": None,
         "dtype": cfg.dtype,
         "data": "synthetic (seeded AR(1) hidden states, N(0,0.02) weights, SVD-built adapters)",
-        "config": {"workload": cfg.name, "layers": cfg.L, "hidden": cfg.D, "experts": cfg.n, "top_k": cfg.K,
+        "config": {"workload": cfg.name + ("" if not over else "+" + ",".join(f"{k}={v}" for k, v in over.items())),
+                   "layers": cfg.L, "hidden": cfg.D, "experts": cfg.n, "top_k": cfg.K,
                    "intermediate": cfg.I, "adapter_rank": cfg.r, "hbm_slots_per_layer": cfg.S,
                    "window_experts": cfg.window, "batch": cfg.batch, "shared_experts": cfg.n_shared,
                    "offload_tier": "pinned host DRAM", "expert_bytes": cfg.blob_bytes},

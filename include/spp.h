@@ -73,6 +73,7 @@ typedef struct {
   int32_t prefetched;     /* prefetch copies issued for layer l+1 */
   int32_t prefetch_used;  /* experts prefetched for this layer that its native router selected */
   int32_t ready_on_time;  /* needed experts whose copy had completed when the FFN was enqueued */
+  int32_t token_hits;     /* sum over tokens b of |T_b cap available| before the on-demand loads */
 } spp_layer_stats;
 
 /* Accumulated since the last spp_reset_run_stats.  Times come from HIP events
@@ -151,7 +152,10 @@ spp_status expert_cache_issue_prefetch(spp_ctx* ctx, int32_t target_layer, const
  *   on-demand copies of every expert of the batch demand not available
  *   (replacement: lowest EMPTY slot, else the least recently stamped slot
  *   whose expert the batch does not need); every slot holding a needed
- *   expert takes the step stamp;
+ *   expert takes the step stamp.  When the batch needs more distinct experts
+ *   than S (B > 1, bf16 only), the step runs in rounds: load while a victim
+ *   exists (third victim class: the lowest-index slot whose expert already
+ *   ran this step), run every resident needed expert not yet run, repeat;
  *   if M_max > 0: the expert_cache_issue_prefetch selection for layer l+1
  *   with this s, in the same step;
  *   FFN: h_out_b = round(u_b + sum_k g_bk W_down(silu(W_gate x_b) * (W_up x_b))
@@ -228,8 +232,9 @@ spp_status spp_policy_create(int32_t S, int32_t n, const int32_t* resident, int3
                              spp_slot_policy** out);
 spp_status spp_policy_destroy(spp_slot_policy* p);
 /* needed: the batch demand (any order, duplicates allowed); loads_out host
- * int32 [3*S] receives (expert, slot, evicted) triples; EINVAL if the demand
- * has more distinct experts than S. */
+ * int32 [3*n] receives (expert, slot, evicted) triples in load order.  A
+ * demand of more distinct experts than S is served in rounds (see
+ * moe_layer_forward).  EINVAL for an out-of-range id. */
 spp_status spp_policy_on_demand(spp_slot_policy* p, const int32_t* needed, int32_t count, int64_t tau,
                                 int32_t* loads_out, int32_t* n_loads);
 /* Prefetch selection + placement with priorities s (host fp32 [n]);

@@ -215,7 +215,12 @@ class SlotCache:
 
     * on-demand load of a missing expert: the lowest-index EMPTY slot, else the
       slot with the smallest (stamp, slot index) whose expert is not needed by
-      the current batch;
+      the current batch, else (when the batch needs more distinct experts than
+      there are slots) the lowest-index slot whose expert already ran in an
+      earlier round of this step.  A step runs in rounds: load missing experts
+      in ascending order while a victim exists, then run every needed expert
+      that is resident and has not run yet; repeat until all have run.  With
+      at most S distinct needed experts there is a single round;
     * prefetch: the lowest-index EMPTY slot, else the smallest (stamp, slot
       index) among slots stamped before the current step; prefetching stops
       when no such slot is left;
@@ -253,20 +258,40 @@ class SlotCache:
         cands = [(int(self.stamp[j]), j) for j in range(self.S) if allowed(j)]
         return min(cands)[1] if cands else EMPTY
 
+    def _round_victim(self, need, ran) -> int:
+        v = self._victim(lambda j: int(self.expert[j]) not in need)
+        if v != EMPTY:
+            return v
+        done = [j for j in range(self.S) if int(self.expert[j]) in ran]
+        return done[0] if done else EMPTY
+
     def on_demand(self, needed: Sequence[int], tau: int):
-        """Load every needed expert that is not present; returns [(expert, slot, evicted)]."""
+        """Load every needed expert that is not present, in rounds; returns
+        [(expert, slot, evicted)].  self.rounds lists the experts run in each
+        round and self.run_slot maps each needed expert to the slot it ran from."""
         need = set(int(e) for e in needed)
-        if len(need) > self.S:
-            raise ValueError("batch demand exceeds the slot count")
         occ = self.occupied()
-        loads = []
-        for e in sorted(need):
-            if occ[e]:
-                continue
-            v = self._victim(lambda j: int(self.expert[j]) not in need)
-            assert v != EMPTY
-            loads.append((e, v, int(self.expert[v])))
-            self.expert[v] = e
+        pending = [e for e in sorted(need) if not occ[e]]
+        loads, ran = [], set()
+        self.rounds, self.run_slot = [], {}
+        while True:
+            while pending:
+                v = self._round_victim(need, ran)
+                if v == EMPTY:
+                    break
+                e = pending.pop(0)
+                loads.append((e, v, int(self.expert[v])))
+                self.expert[v] = e
+            run = sorted(int(self.expert[j]) for j in range(self.S)
+                         if int(self.expert[j]) in need and int(self.expert[j]) not in ran)
+            if not run and pending:
+                raise AssertionError("no progress: no victim and nothing to run")
+            for e in run:
+                self.run_slot[e] = self.slot_of(e)
+            ran |= set(run)
+            self.rounds.append(run)
+            if not pending:
+                break
         for j in range(self.S):
             if int(self.expert[j]) in need:
                 self.stamp[j] = tau
@@ -409,15 +434,17 @@ def layer_prologue(cfg, W: OracleWeights, l: int, h: np.ndarray):
 
 def moe_output(cfg, W: OracleWeights, l: int, cache: SlotCache, u, x, T, g):
     """h' = u + sum_k g_k FFN_{T_k}(x) (+ shared experts with weight 1), weights
-    looked up through the slot table; every executed expert must be present."""
+    looked up through the slot each expert ran from (the round structure of the
+    on-demand step decides which slot held it at its turn)."""
     B = x.shape[0]
     y = np.zeros((B, cfg.D))
     for b in range(B):
         for k in range(T.shape[1]):
-            slot = cache.slot_of(int(T[b, k]))
+            e = int(T[b, k])
+            slot = cache.run_slot.get(e, EMPTY)
             if slot == EMPTY:
-                raise AssertionError("executed expert is not available")
-            Wg, Wu, Wd = W.expert(l, int(cache.expert[slot]))
+                raise AssertionError("executed expert was never resident")
+            Wg, Wu, Wd = W.expert(l, e)
             y[b] += g[b, k] * expert_ffn(Wg, Wu, Wd, x[b])
         for j in range(cfg.n_shared):
             y[b] += expert_ffn(*W.shared(l, j), x[b])

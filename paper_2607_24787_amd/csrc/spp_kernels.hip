@@ -200,6 +200,127 @@ __device__ __forceinline__ float rms_scale(float (&xv)[NCH][Vec<T>::N], int D, f
   return 1.0f / sqrtf(ss / static_cast<float>(D) + eps);
 }
 
+constexpr int kEQ = kMaxExpertsTopK / kThreads;  // experts per thread in the tails
+
+// Top-K of one token's logits zb (LDS, n values) by rank counting -- expert e
+// takes position rank(e) = #{e' beating e}, where e' beats e iff z_e' > z_e, or
+// z_e' == z_e and e' < e -- then its combine weights (softmax over all n
+// renormalised over the K selected = softmax over the selected).  Writes token
+// b's outputs.  Every thread of the workgroup calls it.
+__device__ __forceinline__ void select_token(const RouterArgs& a, const float* zb, int b, int tid, float* s_zsel,
+                                             int* s_isel) {
+  const int n = a.n;
+  for (int e = tid; e < n; e += kThreads) {
+    const float v = zb[e];
+    int rank = 0;
+#pragma unroll 8
+    for (int j = 0; j < n; ++j) {
+      const float u = zb[j];
+      rank += (u > v || (u == v && j < e)) ? 1 : 0;
+    }
+    if (rank < a.K) {
+      s_isel[rank] = e;
+      s_zsel[rank] = v;
+    }
+  }
+  __syncthreads();
+  if (tid < a.K) {
+    const float m = s_zsel[0];
+    float sum = 0.f;
+    for (int k = 0; k < a.K; ++k) sum += expf(s_zsel[k] - m);
+    const int idx = b * a.K + tid;
+    const float gk = expf(s_zsel[tid] - m) / sum;
+    a.topk[idx] = s_isel[tid];
+    a.gates[idx] = gk;
+    if (a.topk_host) {
+      a.topk_host[idx] = s_isel[tid];
+      a.gates_host[idx] = gk;
+    }
+  }
+}
+
+// One token's predicted distribution pi_hat = softmax(B a) over the n experts
+// (sa: the token's r adapter hidden units in LDS; B transposed in LDS when
+// staged).  Thread tid gets experts tid + kThreads*q in pi[q].
+template <typename T>
+__device__ __forceinline__ void adapter_token(const RouterArgs& a, const float* sa, bool staged, const float* s_B,
+                                              int tid, int lane, int wave, float* s_red, float (&pi)[kEQ]) {
+  const int n = a.n, r = a.r;
+  float zh[kEQ];
+  float mx = -INFINITY;
+#pragma unroll
+  for (int q = 0; q < kEQ; ++q) {
+    const int e = tid + kThreads * q;
+    zh[q] = -INFINITY;
+    if (e < n) {
+      float acc = 0.f;
+      if (staged) {
+#pragma unroll 8
+        for (int j = 0; j < r; ++j) acc += s_B[j * n + e] * sa[j];
+      } else {
+        for (int j = 0; j < r; ++j) acc += load_elem<T>(a.Bm, static_cast<size_t>(e) * r + j) * sa[j];
+      }
+      zh[q] = acc;
+      mx = fmaxf(mx, acc);
+    }
+  }
+  mx = wave_max(mx);
+  if (lane == 0) s_red[wave] = mx;
+  __syncthreads();
+  mx = s_red[0];
+  for (int wv = 1; wv < kWaves; ++wv) mx = fmaxf(mx, s_red[wv]);
+  __syncthreads();
+  float part = 0.f;
+#pragma unroll
+  for (int q = 0; q < kEQ; ++q) {
+    const int e = tid + kThreads * q;
+    pi[q] = e < n ? expf(zh[q] - mx) : 0.f;
+    part += pi[q];
+  }
+  part = wave_sum(part);
+  if (lane == 0) s_red[wave] = part;
+  __syncthreads();
+  float sum = 0.f;
+  for (int wv = 0; wv < kWaves; ++wv) sum += s_red[wv];
+#pragma unroll
+  for (int q = 0; q < kEQ; ++q) pi[q] /= sum;
+}
+
+// Adapter B, transposed into LDS ([r][n]); the loads are issued by the caller
+// (load_B_chunks) before its first barrier.
+template <typename T>
+struct BStage {
+  static constexpr int VB = Vec<T>::N;
+  static constexpr int kLoads = kBStage / VB / kThreads;  // 16-byte chunks per thread
+  uint4 rb[kLoads];
+  int nchunk = 0;
+  __device__ __forceinline__ void load(const RouterArgs& a, int tid, bool staged) {
+    nchunk = staged ? (a.n * a.r) / VB : 0;  // n*r*sizeof(T) is a multiple of 16 (checked at launch)
+#pragma unroll
+    for (int q = 0; q < kLoads; ++q) {
+      const int c = tid + q * kThreads;
+      rb[q] = c < nchunk ? ld16(reinterpret_cast<const T*>(a.Bm) + static_cast<size_t>(c) * VB)
+                         : make_uint4(0, 0, 0, 0);
+    }
+  }
+  __device__ __forceinline__ void store(const RouterArgs& a, int tid, float* s_B) const {
+#pragma unroll
+    for (int q = 0; q < kLoads; ++q) {
+      const int c = tid + q * kThreads;
+      if (c < nchunk) {
+        float f[VB];
+        unpack<T>(rb[q], f);
+#pragma unroll
+        for (int v = 0; v < VB; ++v) {
+          const int idx = c * VB + v;
+          const int e = idx / a.r, j = idx - e * a.r;
+          s_B[j * a.n + e] = f[v];
+        }
+      }
+    }
+  }
+};
+
 // ---------------------------------------------------------------------------
 // Router logits, adapter hidden units, then (last workgroup) Top-K, gates and
 // adapter priorities.  One wave per weight row.
@@ -287,20 +408,11 @@ __global__ __launch_bounds__(kThreads) void router_adapter_kernel(RouterArgs a) 
   // transposed in LDS when it fits) and the logits / adapter hidden units of a
   // chunk of tokens.
   const bool staged = na && n * r <= kBStage;
-  constexpr int VB = Vec<T>::N;
-  constexpr int kBLoads = kBStage / VB / kThreads;  // 16-byte B chunks per thread
-  uint4 rb[kBLoads];
-  const int nbchunk = staged ? (n * r) / VB : 0;    // n*r*sizeof(T) is a multiple of 16 (checked at launch)
+  BStage<T> bst;
+  bst.load(a, tid, staged);
+  float sacc[kEQ];
 #pragma unroll
-  for (int q = 0; q < kBLoads; ++q) {
-    const int c = tid + q * kThreads;
-    rb[q] = c < nbchunk ? ld16(reinterpret_cast<const T*>(a.Bm) + static_cast<size_t>(c) * VB)
-                        : make_uint4(0, 0, 0, 0);
-  }
-  constexpr int EQ = kMaxExpertsTopK / kThreads;
-  float sacc[EQ];
-#pragma unroll
-  for (int q = 0; q < EQ; ++q) sacc[q] = 0.f;
+  for (int q = 0; q < kEQ; ++q) sacc[q] = 0.f;
   static_assert(kZStage >= kMaxExpertsTopK + 256, "one token's logits and hidden units fit the stage");
   const int bchunk = kZStage / ldz;
   for (int b0 = 0; b0 < a.B; b0 += bchunk) {
@@ -313,22 +425,7 @@ __global__ __launch_bounds__(kThreads) void router_adapter_kernel(RouterArgs a) 
       zr[q] = idx < cnt ? ld_agent(a.zbuf + static_cast<size_t>(b0) * ldz + idx) : 0.f;
     }
     __syncthreads();  // previous chunk is done with s_zall
-    if (b0 == 0) {
-#pragma unroll
-      for (int q = 0; q < kBLoads; ++q) {
-        const int c = tid + q * kThreads;
-        if (c < nbchunk) {
-          float f[VB];
-          unpack<T>(rb[q], f);
-#pragma unroll
-          for (int v = 0; v < VB; ++v) {
-            const int idx = c * VB + v;
-            const int e = idx / r, j = idx - e * r;
-            s_B[j * n + e] = f[v];
-          }
-        }
-      }
-    }
+    if (b0 == 0) bst.store(a, tid, s_B);
 #pragma unroll
     for (int q = 0; q < kZStage / kThreads; ++q) {
       const int idx = tid + q * kThreads;
@@ -336,95 +433,144 @@ __global__ __launch_bounds__(kThreads) void router_adapter_kernel(RouterArgs a) 
     }
     __syncthreads();
     for (int bb = 0; bb < nb; ++bb) {
-      const int b = b0 + bb;
       const float* zb = s_zall + bb * ldz;
-      if (a.router_on) {
-        // Top-K by rank counting: expert e takes position rank(e) = #{e' beating e},
-        // where e' beats e iff z_e' > z_e, or z_e' == z_e and e' < e.
-        for (int e = tid; e < n; e += kThreads) {
-          const float v = zb[e];
-          int rank = 0;
-#pragma unroll 8
-          for (int j = 0; j < n; ++j) {
-            const float u = zb[j];
-            rank += (u > v || (u == v && j < e)) ? 1 : 0;
-          }
-          if (rank < a.K) {
-            s_isel[rank] = e;
-            s_zsel[rank] = v;
-          }
-        }
-        __syncthreads();
-        if (tid < a.K) {
-          // softmax over all n renormalised over the K selected = softmax over the selected
-          const float m = s_zsel[0];
-          float sum = 0.f;
-          for (int k = 0; k < a.K; ++k) sum += expf(s_zsel[k] - m);
-          const int idx = b * a.K + tid;
-          const float gk = expf(s_zsel[tid] - m) / sum;
-          a.topk[idx] = s_isel[tid];
-          a.gates[idx] = gk;
-          if (a.topk_host) {
-            a.topk_host[idx] = s_isel[tid];
-            a.gates_host[idx] = gk;
-          }
-        }
-      }
+      if (a.router_on) select_token(a, zb, b0 + bb, tid, s_zsel, s_isel);
       if (na) {
-        // z_hat = B a, softmax over the n experts, accumulated over tokens in order
-        const float* sa = zb + n;
-        float zh[EQ];
-        float mx = -INFINITY;
+        float pi[kEQ];
+        adapter_token<T>(a, zb + n, staged, s_B, tid, lane, wave, s_red, pi);
 #pragma unroll
-        for (int q = 0; q < EQ; ++q) {
-          const int e = tid + kThreads * q;
-          zh[q] = -INFINITY;
-          if (e < n) {
-            float acc = 0.f;
-            if (staged) {
-#pragma unroll 8
-              for (int j = 0; j < r; ++j) acc += s_B[j * n + e] * sa[j];
-            } else {
-              for (int j = 0; j < r; ++j) acc += load_elem<T>(a.Bm, static_cast<size_t>(e) * r + j) * sa[j];
-            }
-            zh[q] = acc;
-            mx = fmaxf(mx, acc);
-          }
-        }
-        mx = wave_max(mx);
-        if (lane == 0) s_red[wave] = mx;
-        __syncthreads();
-        mx = s_red[0];
-        for (int wv = 1; wv < kWaves; ++wv) mx = fmaxf(mx, s_red[wv]);
-        __syncthreads();
-        float ex[EQ];
-        float part = 0.f;
-#pragma unroll
-        for (int q = 0; q < EQ; ++q) {
-          const int e = tid + kThreads * q;
-          ex[q] = e < n ? expf(zh[q] - mx) : 0.f;
-          part += ex[q];
-        }
-        part = wave_sum(part);
-        if (lane == 0) s_red[wave] = part;
-        __syncthreads();
-        float sum = 0.f;
-        for (int wv = 0; wv < kWaves; ++wv) sum += s_red[wv];
-#pragma unroll
-        for (int q = 0; q < EQ; ++q) sacc[q] += ex[q] / sum;
+        for (int q = 0; q < kEQ; ++q) sacc[q] += pi[q];
       }
       __syncthreads();  // s_isel / s_red are reused by the next token
     }
   }
   if (na) {
 #pragma unroll
-    for (int q = 0; q < EQ; ++q) {
+    for (int q = 0; q < kEQ; ++q) {
       const int e = tid + kThreads * q;
       if (e < n) {
         a.s[e] = sacc[q];
         if (a.s_host) a.s_host[e] = sacc[q];
       }
     }
+  }
+  if (tid == 0) __hip_atomic_store(a.counter, 0u, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
+}
+
+// ---------------------------------------------------------------------------
+// Router for B > 1 tokens, in two launches.
+//   rows:   one wave per router / adapter-A row over a block of kRowTok tokens
+//           (the row stays in registers, the tokens' rows are read in turn);
+//   select: one workgroup per token -- Top-K, gates and the adapter
+//           distribution; the last workgroup to finish sums the distributions
+//           over the tokens, in token order, into s.
+// ---------------------------------------------------------------------------
+constexpr int kRowTok = 8;
+
+template <typename T, int NCH>
+__global__ __launch_bounds__(kThreads) void router_rows_kernel(RouterArgs a) {
+  constexpr int V = Vec<T>::N;
+  const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
+  const int D = a.D, nch = D / V, n = a.n, ldz = a.n + a.r;
+  const int nr = a.router_on ? n : 0;
+  const int na = a.A ? a.r : 0;
+  const int row = blockIdx.x * kWaves + wave;
+  const T* wrow = nullptr;
+  int zcol = 0;
+  if (row < nr) {
+    wrow = reinterpret_cast<const T*>(a.Wr) + static_cast<size_t>(row) * D;
+    zcol = row;
+  } else if (row < nr + na) {
+    wrow = reinterpret_cast<const T*>(a.A) + static_cast<size_t>(row - nr) * D;
+    zcol = n + (row - nr);
+  }
+  uint4 w[NCH];
+  load_chunks<NCH>(wrow ? wrow : reinterpret_cast<const T*>(a.Wr), lane, wrow ? nch : 0, w);
+  const int b1 = min(a.B, static_cast<int>(blockIdx.y + 1) * kRowTok);
+  for (int b = blockIdx.y * kRowTok; b < b1; ++b) {
+    float xv[NCH][V];
+    if (a.u) {
+      load_row_f32<T, NCH>(a.u + static_cast<size_t>(b) * D, lane, nch, xv);
+    } else {
+      load_row_storage<T, NCH>(reinterpret_cast<const T*>(a.h) + static_cast<size_t>(b) * D, lane, nch, xv);
+    }
+    if (!a.x_given) {
+      const float inv = rms_scale<T, NCH>(xv, D, a.eps);
+#pragma unroll
+      for (int j = 0; j < NCH; ++j)
+#pragma unroll
+        for (int v = 0; v < V; ++v) xv[j][v] *= inv;
+    }
+    if (blockIdx.x == 0 && wave == 0 && a.x_out) {
+#pragma unroll
+      for (int j = 0; j < NCH; ++j) {
+        const int c = lane + 64 * j;
+        if (c < nch) {
+          float* dst = a.x_out + static_cast<size_t>(b) * D + c * V;
+#pragma unroll
+          for (int v = 0; v < V; ++v) dst[v] = xv[j][v];
+        }
+      }
+    }
+    if (wrow) {
+      float acc = 0.f;
+#pragma unroll
+      for (int j = 0; j < NCH; ++j) {
+        float wf[V];
+        unpack<T>(w[j], wf);
+#pragma unroll
+        for (int v = 0; v < V; ++v) acc += wf[v] * xv[j][v];
+      }
+      acc = wave_sum(acc);
+      if (lane == 0) a.zbuf[static_cast<size_t>(b) * ldz + zcol] = acc;
+    }
+  }
+}
+
+template <typename T>
+__global__ __launch_bounds__(kThreads) void router_select_kernel(RouterArgs a) {
+  const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
+  const int n = a.n, r = a.r, ldz = a.n + a.r;
+  const int na = a.A ? r : 0;
+  const int b = blockIdx.x;
+  __shared__ int s_last;
+  __shared__ float s_row[kMaxExpertsTopK + 256];
+  __shared__ float s_zsel[32];
+  __shared__ int s_isel[32];
+  __shared__ float s_red[kWaves];
+  __shared__ float s_B[kBStage];
+
+  const bool staged = na && n * r <= kBStage;
+  BStage<T> bst;
+  bst.load(a, tid, staged);
+  float* zrow = a.zbuf + static_cast<size_t>(b) * ldz;
+  for (int e = tid; e < ldz; e += kThreads) s_row[e] = zrow[e];   // written by the rows launch
+  bst.store(a, tid, s_B);
+  __syncthreads();
+  if (a.router_on) select_token(a, s_row, b, tid, s_zsel, s_isel);
+  if (!na) return;
+  float pi[kEQ];
+  adapter_token<T>(a, s_row + n, staged, s_B, tid, lane, wave, s_red, pi);
+  // this token's distribution replaces its logits in zbuf (only this workgroup touches row b)
+#pragma unroll
+  for (int q = 0; q < kEQ; ++q) {
+    const int e = tid + kThreads * q;
+    if (e < n) st_agent(zrow + e, pi[q]);
+  }
+  __builtin_amdgcn_fence(__ATOMIC_RELEASE, "agent");
+  __syncthreads();
+  if (tid == 0) {
+    const unsigned prev = __hip_atomic_fetch_add(a.counter, 1u, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
+    s_last = (prev == gridDim.x - 1);
+  }
+  __syncthreads();
+  if (!s_last) return;
+  __builtin_amdgcn_fence(__ATOMIC_ACQUIRE, "agent");
+  for (int e = tid; e < n; e += kThreads) {
+    float acc = 0.f;
+    for (int bb = 0; bb < a.B; ++bb) acc += ld_agent(a.zbuf + static_cast<size_t>(bb) * ldz + e);
+    a.s[e] = acc;
+    if (a.s_host) a.s_host[e] = acc;
   }
   if (tid == 0) __hip_atomic_store(a.counter, 0u, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
 }
@@ -670,7 +816,7 @@ __global__ __launch_bounds__(kGrpThreads) void ffn_grouped_kernel(GroupArgs a) {
 #pragma unroll
     for (int q = 0; q < kMaxTilesPerWave; ++q) {
       const int tile = wave + q * kGrpWaves;
-      if (tile >= ntiles) break;  // wave-uniform
+      if (tile >= ntiles) continue;  // wave-uniform
       const int ul = tile * 16 + krow;
       const bool uok = ul < nu;
       const uint16_t* grow = blob + static_cast<size_t>(i0 + (uok ? ul : 0)) * unit_elems + kc;
@@ -696,7 +842,7 @@ __global__ __launch_bounds__(kGrpThreads) void ffn_grouped_kernel(GroupArgs a) {
 #pragma unroll
   for (int q = 0; q < kMaxTilesPerWave; ++q) {
     const int tile = wave + q * kGrpWaves;
-    if (tile >= ntiles) break;
+    if (tile >= ntiles) continue;
     const int ul = tile * 16 + krow;
     if (ul < nu) {
 #pragma unroll
@@ -718,22 +864,24 @@ __global__ __launch_bounds__(kGrpThreads) void ffn_grouped_kernel(GroupArgs a) {
 #pragma unroll
       for (int v = 0; v < 4; ++v) acc[t][v] = 0.f;
     const uint16_t* dcol = blob + static_cast<size_t>(i0) * unit_elems + 2 * D + d0;
-    for (int u = 0; u < nu; u += 8) {
-      uint2 raw[8];
+    constexpr int kUB = 8;  // down-column loads in flight per lane
+    for (int u = 0; u < nu; u += kUB) {
+      uint2 raw[kUB];
 #pragma unroll
-      for (int uu = 0; uu < 8; ++uu) {
+      for (int uu = 0; uu < kUB; ++uu) {
         raw[uu] = make_uint2(0u, 0u);
         if (u + uu < nu) raw[uu] = *SPP_GLOBAL(uint2, dcol + static_cast<size_t>(u + uu) * unit_elems);
       }
 #pragma unroll
-      for (int uu = 0; uu < 8; ++uu) {
-        if (u + uu >= nu) break;
+      for (int uu = 0; uu < kUB; ++uu) {
+        // units past the range loaded zeros; their s_h index is clamped in range
+        const int ui = min(u + uu, nu - 1);
         const float dv[4] = {__uint_as_float(raw[uu].x << 16), __uint_as_float(raw[uu].x & 0xffff0000u),
                              __uint_as_float(raw[uu].y << 16), __uint_as_float(raw[uu].y & 0xffff0000u)};
 #pragma unroll
         for (int t = 0; t < kGroupTokens; ++t) {
           if (t < m) {
-            const float h = s_h[t * kGrpMaxUpw + u + uu];
+            const float h = s_h[t * kGrpMaxUpw + ui];
 #pragma unroll
             for (int v = 0; v < 4; ++v) acc[t][v] += h * dv[v];
           }
@@ -841,8 +989,16 @@ hipError_t router_t(const RouterArgs& a, hipStream_t st) {
   // the staged adapter path reads B in 16-byte chunks
   if (a.A && (static_cast<size_t>(a.n) * a.r * sizeof(T)) % 16 != 0) return hipErrorInvalidValue;
   const int grid = (rows + kWaves - 1) / kWaves;
-  SPP_DISPATCH_NCH(nch_for<T>(a.D),
-                   hipLaunchKernelGGL((router_adapter_kernel<T, NCH>), dim3(grid), dim3(kThreads), 0, st, a));
+  if (a.B == 1) {
+    SPP_DISPATCH_NCH(nch_for<T>(a.D),
+                     hipLaunchKernelGGL((router_adapter_kernel<T, NCH>), dim3(grid), dim3(kThreads), 0, st, a));
+    return hipGetLastError();
+  }
+  const dim3 g2(grid, (a.B + kRowTok - 1) / kRowTok);
+  SPP_DISPATCH_NCH(nch_for<T>(a.D), hipLaunchKernelGGL((router_rows_kernel<T, NCH>), g2, dim3(kThreads), 0, st, a));
+  hipError_t e = hipGetLastError();
+  if (e != hipSuccess) return e;
+  hipLaunchKernelGGL((router_select_kernel<T>), dim3(a.B), dim3(kThreads), 0, st, a);
   return hipGetLastError();
 }
 

@@ -54,36 +54,68 @@ bool SlotPolicy::set_table(const int32_t* experts, const int64_t* stamps, std::s
   return true;
 }
 
+int32_t SlotPolicy::distinct(const int32_t* needed, int32_t count) const {
+  std::vector<char> seen(n_, 0);
+  int32_t k = 0;
+  for (int32_t i = 0; i < count; ++i) {
+    const int32_t e = needed[i];
+    if (e >= 0 && e < n_ && !seen[e]) {
+      seen[e] = 1;
+      ++k;
+    }
+  }
+  return k;
+}
+
 bool SlotPolicy::on_demand(const int32_t* needed, int32_t count, int64_t tau, std::vector<Transfer>* loads,
-                           std::string* err) {
+                           std::vector<Round>* rounds, std::string* err) {
   std::vector<char> need(n_, 0);
-  int32_t distinct = 0;
   for (int32_t i = 0; i < count; ++i) {
     const int32_t e = needed[i];
     if (e < 0 || e >= n_) {
       *err = "needed expert id out of range";
       return false;
     }
-    if (!need[e]) ++distinct;
     need[e] = 1;
   }
-  if (distinct > S_) {
-    *err = "batch demand has more distinct experts than slots";
-    return false;
-  }
   loads->clear();
-  for (int32_t e = 0; e < n_; ++e) {
-    if (!need[e] || available(e)) continue;
-    int32_t v = lowest_empty();
-    if (v == kEmpty) {
-      for (int32_t j = 0; j < S_; ++j) {
-        if (need[slot_expert_[j]]) continue;
-        if (v == kEmpty || slot_stamp_[j] < slot_stamp_[v]) v = j;  // ties keep the lower slot
+  rounds->clear();
+  std::vector<int32_t> pending;
+  for (int32_t e = 0; e < n_; ++e)
+    if (need[e] && !available(e)) pending.push_back(e);
+  std::vector<char> ran(n_, 0);
+  size_t next = 0;
+  for (int32_t round = 0;; ++round) {
+    while (next < pending.size()) {
+      int32_t v = lowest_empty();
+      if (v == kEmpty) {
+        for (int32_t j = 0; j < S_; ++j) {
+          if (need[slot_expert_[j]]) continue;
+          if (v == kEmpty || slot_stamp_[j] < slot_stamp_[v]) v = j;  // ties keep the lower slot
+        }
       }
+      if (v == kEmpty) {
+        for (int32_t j = 0; j < S_; ++j)
+          if (ran[slot_expert_[j]]) {
+            v = j;
+            break;
+          }
+      }
+      if (v == kEmpty) break;
+      const int32_t e = pending[next++];
+      loads->push_back({e, v, slot_expert_[v], round});
+      put(v, e);
     }
-    // distinct <= S guarantees a victim exists
-    loads->push_back({e, v, slot_expert_[v]});
-    put(v, e);
+    Round run;
+    for (int32_t e = 0; e < n_; ++e)
+      if (need[e] && !ran[e] && available(e)) run.push_back({e, expert_slot_[e]});
+    if (run.empty() && next < pending.size()) {
+      *err = "on-demand rounds made no progress";  // cannot happen with S >= 1
+      return false;
+    }
+    for (const auto& es : run) ran[es.first] = 1;
+    rounds->push_back(std::move(run));
+    if (next == pending.size()) break;
   }
   for (int32_t j = 0; j < S_; ++j)
     if (slot_expert_[j] != kEmpty && need[slot_expert_[j]]) slot_stamp_[j] = tau;

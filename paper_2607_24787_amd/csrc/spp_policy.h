@@ -6,6 +6,7 @@
 
 #include <cstdint>
 #include <string>
+#include <utility>
 #include <vector>
 
 namespace spp {
@@ -16,7 +17,11 @@ struct Transfer {
   int32_t expert;
   int32_t slot;
   int32_t evicted;  // expert previously in the slot, or kEmpty
+  int32_t round = 0;  // on-demand round the load belongs to
 };
+
+// (expert, slot) pairs that run in one round of an on-demand step.
+using Round = std::vector<std::pair<int32_t, int32_t>>;
 
 class SlotPolicy {
  public:
@@ -35,12 +40,17 @@ class SlotPolicy {
   bool set_table(const int32_t* experts, const int64_t* stamps, std::string* err);
 
   // Load every distinct needed expert that is not available, in ascending
-  // expert order; victim = lowest EMPTY slot, else the smallest
-  // (stamp, slot index) among slots whose expert is not needed.  Then every
-  // slot holding a needed expert takes stamp tau.  Fails (no change) if the
-  // demand has more distinct experts than S or an id is out of range.
+  // expert order, in rounds.  Victim = the lowest EMPTY slot, else the smallest
+  // (stamp, slot index) among slots whose expert is not needed, else the
+  // lowest-index slot whose expert already ran in an earlier round.  A round
+  // loads while a victim exists, then runs every needed resident expert that
+  // has not run yet (ascending expert); with at most S distinct needed experts
+  // there is one round.  Then every slot holding a needed expert takes stamp
+  // tau.  Fails (no change) if an id is out of range.
   bool on_demand(const int32_t* needed, int32_t count, int64_t tau, std::vector<Transfer>* loads,
-                 std::string* err);
+                 std::vector<Round>* rounds, std::string* err);
+  // Distinct experts among needed[0..count).
+  int32_t distinct(const int32_t* needed, int32_t count) const;
 
   // P = the first M_max experts, not available, in order (s desc, index asc);
   // each placed in turn into the lowest EMPTY slot, else the smallest

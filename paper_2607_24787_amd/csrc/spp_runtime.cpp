@@ -39,6 +39,10 @@ struct TimingSet {
   hipEvent_t ev[kNumEv] = {};
   int32_t l = -1;
   bool predicted = false;
+  // batched steps with several on-demand rounds: (before, after) the copy
+  // waits of rounds 1.. (inside the FFN span)
+  std::vector<hipEvent_t> extra;
+  int32_t extra_used = 0;
 };
 
 struct LayerState {
@@ -85,6 +89,7 @@ struct spp_ctx {
   spp::GroupDesc* groups_dev = nullptr;
   spp::GroupDesc* groups_host = nullptr;  // pinned staging for the per-layer group list
   float* ypart = nullptr;
+  std::vector<hipEvent_t> round_done;  // per on-demand round: its FFN launch finished
   hipEvent_t ev_res = nullptr;
   int64_t clock = 0;
   int ffn_wgs = 256;
@@ -142,6 +147,7 @@ spp_status take_set(spp_ctx* c, TimingSet* out) {
   if (!c->free_sets.empty()) {
     *out = c->free_sets.back();
     c->free_sets.pop_back();
+    out->extra_used = 0;
     return SPP_OK;
   }
   TimingSet s;
@@ -163,8 +169,10 @@ void harvest(spp_ctx* c, size_t count) {
     spp_run_stats& st = c->stats;
     st.router_us += 1e3 * elapsed(s.ev[kEvStart], s.ev[kEvRouted]);
     const double exposed = 1e3 * elapsed(s.ev[kEvWaitA], s.ev[kEvWaitB]);
-    st.exposed_us += exposed;
-    st.ffn_us += 1e3 * elapsed(s.ev[kEvFfnBegin], s.ev[kEvFfnEnd]);
+    double extra = 0.0;
+    for (int32_t q = 0; q + 1 < s.extra_used; q += 2) extra += 1e3 * elapsed(s.extra[q], s.extra[q + 1]);
+    st.exposed_us += exposed + extra;
+    st.ffn_us += 1e3 * elapsed(s.ev[kEvFfnBegin], s.ev[kEvFfnEnd]) - extra;
     st.tail_us += 1e3 * elapsed(s.ev[kEvFfnEnd], s.ev[kEvEnd]);
     if (c->have_prev) {
       st.span_us += 1e3 * elapsed(c->prev.ev[kEvStart], s.ev[kEvStart]);
@@ -184,10 +192,11 @@ void harvest(spp_ctx* c, size_t count) {
   c->pending_sets.erase(c->pending_sets.begin(), c->pending_sets.begin() + count);
 }
 
-// Issue host->device copies for transfers into layer `ls`.
-spp_status issue_copies(spp_ctx* c, LayerState& ls, const std::vector<spp::Transfer>& xs) {
+// Issue host->device copies for transfers into layer `ls`; the copy stream
+// first waits on `war` (the last kernel that read slots being overwritten).
+spp_status issue_copies(spp_ctx* c, LayerState& ls, const std::vector<spp::Transfer>& xs, hipEvent_t war) {
   if (xs.empty()) return SPP_OK;
-  if (ls.last_read_valid) SPP_HIP(hipStreamWaitEvent(c->copy, ls.last_read, 0));  // WAR on slot reuse
+  if (war) SPP_HIP(hipStreamWaitEvent(c->copy, war, 0));  // WAR on slot reuse
   for (const spp::Transfer& t : xs) {
     if (c->copy_delay_us > 0) {
       const uint64_t ticks = c->wall_khz * static_cast<uint64_t>(c->copy_delay_us) / 1000;
@@ -234,13 +243,17 @@ void free_ctx(spp_ctx* c) {
       if (e) (void)hipEventDestroy(e);
     if (ls.last_read) (void)hipEventDestroy(ls.last_read);
   }
-  for (auto* v : {&c->pending_sets, &c->free_sets})
-    for (TimingSet& s : *v)
-      for (hipEvent_t e : s.ev)
-        if (e) (void)hipEventDestroy(e);
-  if (c->have_prev)
-    for (hipEvent_t e : c->prev.ev)
+  auto destroy_set = [](TimingSet& s) {
+    for (hipEvent_t e : s.ev)
       if (e) (void)hipEventDestroy(e);
+    for (hipEvent_t e : s.extra)
+      if (e) (void)hipEventDestroy(e);
+  };
+  for (auto* v : {&c->pending_sets, &c->free_sets})
+    for (TimingSet& s : *v) destroy_set(s);
+  if (c->have_prev) destroy_set(c->prev);
+  for (hipEvent_t e : c->round_done)
+    if (e) (void)hipEventDestroy(e);
   for (void* p : {static_cast<void*>(c->u_dev), static_cast<void*>(c->x_dev), static_cast<void*>(c->zbuf),
                   static_cast<void*>(c->res_dev), static_cast<void*>(c->counter), static_cast<void*>(c->partial),
                   static_cast<void*>(c->probe_dev)})
@@ -298,7 +311,7 @@ spp_status create_impl(const spp_model_desc* desc, void* stream, spp_ctx** out) 
   c->grouped = d.max_batch > 1 && d.dtype == SPP_DTYPE_BF16 && d.D % 256 == 0;
   if (c->grouped) {
     c->max_groups = d.max_batch * d.K + d.n_shared * ((d.max_batch + spp::kGroupTokens - 1) / spp::kGroupTokens);
-    c->max_nsplit = (d.I + 127) / 128;
+    c->max_nsplit = (d.I + 63) / 64;
     const size_t npairs = static_cast<size_t>(d.max_batch) * (d.K + d.n_shared);
     if (hipMalloc(&c->groups_dev, sizeof(spp::GroupDesc) * c->max_groups) != hipSuccess ||
         hipHostMalloc(&c->groups_host, sizeof(spp::GroupDesc) * c->max_groups, hipHostMallocDefault) != hipSuccess ||
@@ -314,18 +327,61 @@ spp_status create_impl(const spp_model_desc* desc, void* stream, spp_ctx** out) 
   return SPP_OK;
 }
 
+// RAW: the compute stream waits for the copies into the slots a round reads.
+spp_status wait_round(spp_ctx* c, LayerState& ls, const spp::Round& round, spp_layer_stats* st) {
+  for (const auto& es : round) {
+    const int32_t slot = es.second;
+    if (!ls.slot_pending[slot]) {
+      st->ready_on_time += 1;
+      continue;
+    }
+    if (hipEventQuery(ls.slot_ready[slot]) == hipSuccess) {
+      st->ready_on_time += 1;
+      ls.slot_pending[slot] = 0;
+      continue;
+    }
+    SPP_HIP(hipStreamWaitEvent(c->compute, ls.slot_ready[slot], 0));
+  }
+  return SPP_OK;
+}
+
+spp_status record_extra(spp_ctx* c, TimingSet& ts) {
+  if (ts.extra_used >= static_cast<int32_t>(ts.extra.size())) {
+    hipEvent_t e;
+    SPP_HIP(hipEventCreate(&e));
+    ts.extra.push_back(e);
+  }
+  SPP_HIP(hipEventRecord(ts.extra[ts.extra_used++], c->compute));
+  return SPP_OK;
+}
+
+spp_status round_event(spp_ctx* c, size_t r, hipEvent_t* out) {
+  while (c->round_done.size() <= r) {
+    hipEvent_t e;
+    SPP_HIP(hipEventCreateWithFlags(&e, hipEventDisableTiming));
+    c->round_done.push_back(e);
+  }
+  *out = c->round_done[r];
+  return SPP_OK;
+}
+
 // Batched decode: group the (token, k) pairs by expert (ascending expert,
-// ascending token, at most kGroupTokens per group), then the shared experts
-// over all tokens; upload the list; one grouped FFN launch and one combine.
-spp_status grouped_ffn(spp_ctx* c, LayerState& ls, const int32_t* T, int32_t B, const void* h_in, void* h_out,
-                       TimingSet& ts) {
+// ascending token, at most kGroupTokens per group) round by round, with the
+// shared experts in round 0; upload the list once; per round: the round's
+// copies (waiting for the previous round's FFN, whose slots they reuse), the
+// compute stream's waits for them, one grouped FFN launch; then the next
+// layer's prefetch copies; one combine.
+spp_status grouped_ffn(spp_ctx* c, LayerState& ls, LayerState* next, const int32_t* T, int32_t B,
+                       const void* h_in, void* h_out, const std::vector<spp::Round>& rounds,
+                       const std::vector<spp::Transfer>& loads, spp_layer_stats* st, TimingSet& ts) {
   const spp_model_desc& d = c->d;
   std::vector<std::vector<std::pair<int32_t, int32_t>>> by_expert(d.n);  // (token, pair)
   for (int32_t b = 0; b < B; ++b)
     for (int32_t k = 0; k < d.K; ++k) by_expert[T[b * d.K + k]].push_back({b, b * d.K + k});
   int ng = 0;
-  auto add = [&](const void* blob, const std::vector<std::pair<int32_t, int32_t>>& rows) {
+  auto add = [&](const void* blob, const std::vector<std::pair<int32_t, int32_t>>& rows) -> bool {
     for (size_t r0 = 0; r0 < rows.size(); r0 += spp::kGroupTokens) {
+      if (ng >= c->max_groups) return false;
       spp::GroupDesc& g = c->groups_host[ng++];
       std::memset(&g, 0, sizeof(g));
       g.blob = blob;
@@ -335,35 +391,66 @@ spp_status grouped_ffn(spp_ctx* c, LayerState& ls, const int32_t* T, int32_t B, 
         g.pair[t] = rows[r0 + t].second;
       }
     }
+    return true;
   };
-  for (int32_t e = 0; e < d.n; ++e)
-    if (!by_expert[e].empty())
-      add(ls.slots + static_cast<size_t>(ls.policy->slot_of(e)) * c->stride, by_expert[e]);
-  for (int32_t j = 0; j < d.n_shared; ++j) {
-    std::vector<std::pair<int32_t, int32_t>> rows;
-    for (int32_t b = 0; b < B; ++b) rows.push_back({b, B * d.K + b * d.n_shared + j});
-    add(static_cast<const uint8_t*>(ls.shared) + static_cast<size_t>(j) * c->stride, rows);
+  std::vector<int> rstart(rounds.size()), rcount(rounds.size());
+  int maxg = 0;
+  for (size_t r = 0; r < rounds.size(); ++r) {
+    rstart[r] = ng;
+    for (const auto& es : rounds[r])
+      if (!add(ls.slots + static_cast<size_t>(es.second) * c->stride, by_expert[es.first]))
+        return fail(SPP_ESTATE, "group list overflow");
+    if (r == 0)
+      for (int32_t j = 0; j < d.n_shared; ++j) {
+        std::vector<std::pair<int32_t, int32_t>> rows;
+        for (int32_t b = 0; b < B; ++b) rows.push_back({b, B * d.K + b * d.n_shared + j});
+        if (!add(static_cast<const uint8_t*>(ls.shared) + static_cast<size_t>(j) * c->stride, rows))
+          return fail(SPP_ESTATE, "group list overflow");
+      }
+    rcount[r] = ng - rstart[r];
+    maxg = std::max(maxg, rcount[r]);
   }
-  if (ng > c->max_groups) return fail(SPP_ESTATE, "group list overflow");
   SPP_HIP(hipMemcpyAsync(c->groups_dev, c->groups_host, sizeof(spp::GroupDesc) * ng, hipMemcpyHostToDevice,
                          c->compute));
-  // unit ranges of 128 or 256 units, about 512 workgroups in total
-  const int target = std::max(1, (512 + ng - 1) / ng);
-  int upw = 128 * std::max(1, static_cast<int>(std::lround(static_cast<double>(d.I) / (128.0 * target))));
+  // unit ranges in multiples of 64 units (at most 256), about 512 workgroups
+  // per launch: one full round at two workgroups per compute unit
+  const int target = std::max(1, 512 / std::max(1, maxg));
+  int upw = 64 * std::max(1, static_cast<int>(std::lround(static_cast<double>(d.I) / (64.0 * target))));
   upw = std::min(upw, 256);
   const int nsplit = (d.I + upw - 1) / upw;
   if (nsplit > c->max_nsplit) return fail(SPP_ESTATE, "unit split exceeds the partial buffer");
-  spp::GroupArgs ga{};
-  ga.groups = c->groups_dev;
-  ga.ngroups = ng;
-  ga.nsplit = nsplit;
-  ga.upw = upw;
-  ga.I = d.I;
-  ga.D = d.D;
-  ga.x = c->x_dev;
-  ga.ypart = c->ypart;
-  SPP_HIP(spp::launch_ffn_grouped(ga, c->compute, c->timing ? ts.ev[kEvFfnBegin] : nullptr,
-                                  c->timing ? ts.ev[kEvFfnEnd] : nullptr));
+  for (size_t r = 0; r < rounds.size(); ++r) {
+    if (r > 0) {
+      hipEvent_t done;
+      if (spp_status e = round_event(c, r - 1, &done)) return e;
+      SPP_HIP(hipEventRecord(done, c->compute));
+      std::vector<spp::Transfer> xs;
+      for (const spp::Transfer& t : loads)
+        if (t.round == static_cast<int32_t>(r)) xs.push_back(t);
+      if (spp_status e = issue_copies(c, ls, xs, done)) return e;
+      if (c->timing)
+        if (spp_status e = record_extra(c, ts)) return e;
+      if (spp_status e = wait_round(c, ls, rounds[r], st)) return e;
+      if (c->timing)
+        if (spp_status e = record_extra(c, ts)) return e;
+    }
+    if (rcount[r] == 0) continue;
+    spp::GroupArgs ga{};
+    ga.groups = c->groups_dev + rstart[r];
+    ga.ngroups = rcount[r];
+    ga.nsplit = nsplit;
+    ga.upw = upw;
+    ga.I = d.I;
+    ga.D = d.D;
+    ga.x = c->x_dev;
+    ga.ypart = c->ypart;
+    const bool first = r == 0, last = r + 1 == rounds.size();
+    SPP_HIP(spp::launch_ffn_grouped(ga, c->compute, c->timing && first ? ts.ev[kEvFfnBegin] : nullptr,
+                                    c->timing && last ? ts.ev[kEvFfnEnd] : nullptr));
+  }
+  if (rounds.size() > 1 && next && !c->last_pref.empty())
+    if (spp_status e = issue_copies(c, *next, c->last_pref, next->last_read_valid ? next->last_read : nullptr))
+      return e;
   spp::CombineBArgs cb{};
   cb.ypart = c->ypart;
   cb.gates = reinterpret_cast<const float*>(c->res_dev + c->off_gates);
@@ -454,53 +541,49 @@ spp_status layer_forward_impl(spp_ctx* c, int32_t l, const void* h_in, void* h_o
       if (ls.policy->available(e)) st.hits += 1;
     }
     for (int32_t e : ls.pending_prefetch) st.prefetch_used += seen[e] ? 1 : 0;
+    for (int32_t i = 0; i < BK; ++i) st.token_hits += ls.policy->available(T[i]) ? 1 : 0;
   }
   ls.pending_prefetch.clear();
   std::string why;
-  if (!ls.policy->on_demand(T, BK, tau, &c->last_loads, &why)) return fail(SPP_ESTATE, why);
+  const bool batched = c->grouped && B > 1;
+  if (!batched && ls.policy->distinct(T, BK) > d.S)
+    return fail(SPP_ESTATE, "batch demand exceeds the slot count; more than S distinct experts per step "
+                            "needs the batched bf16 path");
+  std::vector<spp::Round> rounds;
+  if (!ls.policy->on_demand(T, BK, tau, &c->last_loads, &rounds, &why)) return fail(SPP_ESTATE, why);
   st.misses = static_cast<int32_t>(c->last_loads.size());
-  if (spp_status e = issue_copies(c, ls, c->last_loads)) return e;
 
+  // prefetch selection for layer l+1 (the copies are enqueued after this layer's loads)
+  LayerState* nx = predict && M_max > 0 ? &c->layers[l + 1] : nullptr;
   c->last_pref.clear();
   c->last_s_valid = predict;
   c->last_B = B;
   if (predict) {
     std::memcpy(c->last_s.data(), s, sizeof(float) * d.n);
-    if (M_max > 0) {
-      LayerState& nx = c->layers[l + 1];
-      nx.policy->prefetch(s, M_max, tau, &c->last_pref);
-      if (spp_status e = issue_copies(c, nx, c->last_pref)) return e;
-      nx.pending_prefetch.clear();
-      for (const spp::Transfer& t : c->last_pref) nx.pending_prefetch.push_back(t.expert);
+    if (nx) {
+      nx->policy->prefetch(s, M_max, tau, &c->last_pref);
+      nx->pending_prefetch.clear();
+      for (const spp::Transfer& t : c->last_pref) nx->pending_prefetch.push_back(t.expert);
       st.prefetched = static_cast<int32_t>(c->last_pref.size());
     }
   }
+  {
+    std::vector<spp::Transfer> first;
+    for (const spp::Transfer& t : c->last_loads)
+      if (t.round == 0) first.push_back(t);
+    if (spp_status e = issue_copies(c, ls, first, ls.last_read_valid ? ls.last_read : nullptr)) return e;
+  }
+  if (rounds.size() == 1 && nx)
+    if (spp_status e = issue_copies(c, *nx, c->last_pref, nx->last_read_valid ? nx->last_read : nullptr)) return e;
 
   // RAW: the FFN reads each needed slot only after its copy completed
   if (c->timing) SPP_HIP(hipEventRecord(ts.ev[kEvWaitA], c->compute));
-  {
-    std::vector<char> waited(d.S, 0);
-    for (int32_t i = 0; i < BK; ++i) {
-      const int32_t slot = ls.policy->slot_of(T[i]);
-      if (waited[slot]) continue;
-      waited[slot] = 1;
-      if (!ls.slot_pending[slot]) {
-        st.ready_on_time += 1;
-        continue;
-      }
-      if (hipEventQuery(ls.slot_ready[slot]) == hipSuccess) {
-        st.ready_on_time += 1;
-        ls.slot_pending[slot] = 0;
-        continue;
-      }
-      SPP_HIP(hipStreamWaitEvent(c->compute, ls.slot_ready[slot], 0));
-    }
-  }
+  if (spp_status e = wait_round(c, ls, rounds[0], &st)) return e;
   if (c->timing) SPP_HIP(hipEventRecord(ts.ev[kEvWaitB], c->compute));
-  if (c->grouped && B > 1) {
-    if (spp_status e = grouped_ffn(c, ls, T, B, h_in, h_out, ts)) return e;
+  if (batched) {
+    if (spp_status e = grouped_ffn(c, ls, nx, T, B, h_in, h_out, rounds, c->last_loads, &st, ts)) return e;
   }
-  for (int32_t b = 0; b < B && !(c->grouped && B > 1); ++b) {
+  for (int32_t b = 0; b < B && !batched; ++b) {
     spp::FfnArgs fa{};
     int nW = 0;
     for (int32_t k = 0; k < d.K; ++k) {
@@ -687,7 +770,7 @@ spp_status expert_cache_issue_prefetch(spp_ctx* c, int32_t target_layer, const f
   const int64_t tau = ++c->clock;
   std::vector<spp::Transfer> placed;
   ls.policy->prefetch(s_host, M_max, tau, &placed);
-  if (spp_status e = issue_copies(c, ls, placed)) return e;
+  if (spp_status e = issue_copies(c, ls, placed, ls.last_read_valid ? ls.last_read : nullptr)) return e;
   ls.pending_prefetch.clear();
   for (size_t i = 0; i < placed.size(); ++i) {
     issued_out[i] = placed[i].expert;
@@ -842,8 +925,9 @@ spp_status spp_policy_on_demand(spp_slot_policy* p, const int32_t* needed, int32
                                 int32_t* loads_out, int32_t* n_loads) {
   if (!p || (count > 0 && !needed) || count < 0 || !n_loads) return fail(SPP_EINVAL, "bad arguments");
   std::vector<spp::Transfer> loads;
+  std::vector<spp::Round> rounds;
   std::string why;
-  if (!p->p.on_demand(needed, count, tau, &loads, &why)) return fail(SPP_EINVAL, why);
+  if (!p->p.on_demand(needed, count, tau, &loads, &rounds, &why)) return fail(SPP_EINVAL, why);
   *n_loads = static_cast<int32_t>(loads.size());
   for (size_t i = 0; i < loads.size() && loads_out; ++i) {
     loads_out[3 * i] = loads[i].expert;

@@ -31,7 +31,8 @@ class ModelDesc(ctypes.Structure):
 
 
 class LayerStats(ctypes.Structure):
-    _fields_ = [(f, c_int32) for f in ("hits", "misses", "prefetched", "prefetch_used", "ready_on_time")]
+    _fields_ = [(f, c_int32) for f in ("hits", "misses", "prefetched", "prefetch_used", "ready_on_time",
+                                       "token_hits")]
 
 
 class RunStats(ctypes.Structure):
@@ -294,7 +295,7 @@ class SlotPolicy:
 
     def on_demand(self, needed, tau):
         a, p = _i32(list(needed))
-        out = np.zeros(3 * self.S, dtype=np.int32)
+        out = np.zeros(3 * self.n, dtype=np.int32)
         k = c_int32()
         _check(lib().spp_policy_on_demand(c_void_p(self._h), p, len(a), tau, out.ctypes.data_as(POINTER(c_int32)),
                                           byref(k)))

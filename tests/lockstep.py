@@ -91,6 +91,7 @@ def run_lockstep(stack, cfg, tokens: int, M_max: int, check_x: bool = True) -> L
                     rep.max_err_g = max(rep.max_err_g, float(np.max(np.abs(gates[b] - ref.g[b]))))
             if not resync:
                 assert loads == ref.loads, f"{tag}: loads {loads} != {ref.loads}"
+                assert stats.misses == len(ref.loads) and stats.token_hits == int(np.sum(ref.ready)), tag
                 e, st = spp.spp_get_slot_table(stack.ctx, l, S)
                 assert e.tolist() == ref.table_after_demand.tolist(), tag
                 assert st.tolist() == ref.stamps_after_demand.tolist(), tag
@@ -104,6 +105,7 @@ def run_lockstep(stack, cfg, tokens: int, M_max: int, check_x: bool = True) -> L
                     rep.exempt.append(f"{tag} prefetch gap {gap:.3g}")
                     resync = True
                 if not resync and nxt is not None:
+                    assert stats.prefetched == len(ref.P), tag
                     e2, st2 = spp.spp_get_slot_table(stack.ctx, l + 1, S)
                     assert e2.tolist() == ref.next_table_after_prefetch.tolist(), tag
                     assert st2.tolist() == ref.next_stamps_after_prefetch.tolist(), tag

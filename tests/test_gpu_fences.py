@@ -55,7 +55,14 @@ def _run(cfg, M_max, tokens, poison=False, delay_us=0):
         st.close()
 
 
-@pytest.mark.parametrize("cfg,M_max,tokens", [(RAGGED, 2, 12), (w.get("c0"), 1, 16)], ids=["ragged", "c0"])
+# batched, 6 slots for a demand of ~14 experts: the on-demand step runs in
+# rounds and later rounds overwrite slots an earlier round's FFN read (WAR)
+BATCH_ROUNDS = w.MoEConfig(name="batch5_bf16_D512_n24_k4_I160", L=2, D=512, n=24, K=4, I=160, r=8, S=6,
+                           windows=(2,), tokens=6, batch=5, seed=13)
+
+
+@pytest.mark.parametrize("cfg,M_max,tokens", [(RAGGED, 2, 12), (w.get("c0"), 1, 16), (BATCH_ROUNDS, 2, 6)],
+                         ids=["ragged", "c0", "batched_rounds"])
 def test_poisoned_delayed_copies_leave_outputs_unchanged(torch_cuda, cfg, M_max, tokens):
     _log(f"[fences] {cfg.name} M_max={M_max}")
     ref, ref_on_time, needed, misses = _run(cfg, M_max, tokens)

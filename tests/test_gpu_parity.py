@@ -51,6 +51,11 @@ BATCH_BF16 = w.MoEConfig(name="batch5_bf16_D512_n24_k4_I160", L=2, D=512, n=24, 
                          windows=(2,), tokens=6, batch=5, seed=13)
 QWEN_B16 = w.get("c4").with_(L=2, batch=16, S=128, tokens=3)
 DSV2_B4 = w.get("c3").with_(L=2, batch=4, S=64, tokens=3)
+# batch demand above the slot count: on-demand rounds (the 64-sequence, 32-slot
+# configuration as specified, two layers)
+BATCH_BF16_ROUNDS = BATCH_BF16.with_(S=6)
+QWEN_B16_S32 = w.get("c4").with_(L=2, batch=16, S=32, tokens=2)
+QWEN_B64_S32 = w.get("c4").with_(L=2, tokens=2)
 C2_TIED = w.get("c2").with_(tokens=2, expert_layers=2)
 
 
@@ -83,8 +88,11 @@ def test_lockstep_parity(torch_cuda, cfg, M_max, tokens):
     _assert_report(rep, cfg, cfg.name)
 
 
-@pytest.mark.parametrize("cfg,M_max,tokens", [(BATCH_BF16, 2, 6), (QWEN_B16, 4, 3), (DSV2_B4, 2, 3)],
-                         ids=["batch5_bf16", "qwen_b16", "dsv2_b4"])
+@pytest.mark.parametrize("cfg,M_max,tokens", [(BATCH_BF16, 2, 6), (QWEN_B16, 4, 3), (DSV2_B4, 2, 3),
+                                              (BATCH_BF16_ROUNDS, 2, 6), (QWEN_B16_S32, 4, 2),
+                                              (QWEN_B64_S32, 4, 2)],
+                         ids=["batch5_bf16", "qwen_b16", "dsv2_b4", "batch5_rounds", "qwen_b16_s32_rounds",
+                              "qwen_b64_s32_rounds"])
 def test_lockstep_parity_batched_grouped(torch_cuda, cfg, M_max, tokens):
     from lockstep import run_lockstep
     _log(f"[lockstep] {cfg.name} B={cfg.batch} M_max={M_max} tokens={tokens}")
