@@ -25,12 +25,22 @@
  *    states as fp32, SPP_DTYPE_BF16 as bf16 (bit patterns, 2 bytes); router
  *    logits, gates, priorities and the router input are always fp32.
  *
- * Expert blob layout (one routed or shared expert, "blob"): I units of 3*D
- * elements, unit i = [gate row i (D), up row i (D), down column i (D)], i.e.
- *   blob[(3i+0)D + d] = W_gate[i][d],  blob[(3i+1)D + d] = W_up[i][d],
- *   blob[(3i+2)D + d] = W_down[d][i].
+ * Expert blob ("blob": one routed or shared expert, W_gate and W_up [I][D],
+ * W_down [D][I], 3*I*D elements) in one of two layouts, fixed by the model
+ * shape (spp_blob_layout); spp_pack_expert writes either on the host.
+ *  SPP_LAYOUT_UNITS (batch-1 contexts): I units of 3*D elements, unit i =
+ *    [gate row i, up row i, down column i]:
+ *      blob[(3i+0)D + d] = W_gate[i][d],  blob[(3i+1)D + d] = W_up[i][d],
+ *      blob[(3i+2)D + d] = W_down[d][i].
+ *  SPP_LAYOUT_TILED (bf16 contexts with max_batch > 1, D % 256 == 0 and
+ *    I % 16 == 0): with nb = D/256, first the gate/up part in pieces of 8
+ *    elements, piece (((t*nb + b)*2 + w)*8 + j)*64 + l (w = 0 gate, 1 up;
+ *    t < I/16, b < nb, j < 8, l < 64) holding
+ *      W_w[16t + l%16][256b + 32j + 8(l/16) + e], e = 0..7,
+ *    then, from element 2*I*D, the down part in runs of 256 elements, run
+ *    (s*I + i) (s < nb, i < I) holding W_down[256s + c][i], c = 0..255.
  * Blobs are placed at a stride of spp_blob_stride(desc) bytes (3*I*D*elem
- * rounded up to 4096).
+ * rounded up to 4096); the padding is zero.
  */
 #ifndef SPP_H
 #define SPP_H
@@ -54,6 +64,7 @@ typedef enum {
 } spp_status;
 
 enum { SPP_DTYPE_F32 = 0, SPP_DTYPE_BF16 = 1 };
+enum { SPP_LAYOUT_UNITS = 0, SPP_LAYOUT_TILED = 1 };
 
 /* Model shape.  Notation of the paper's problem formulation: L MoE layers,
  * n routed experts per layer, top-K routing, router input size D, adapter
@@ -94,6 +105,18 @@ typedef struct {
 
 /* Bytes between consecutive expert blobs in a host store or slot pool. */
 size_t spp_blob_stride(const spp_model_desc* desc);
+
+/* Blob layout of contexts with this shape: SPP_LAYOUT_UNITS or
+ * SPP_LAYOUT_TILED (see the top of this header); -1 if desc is NULL. */
+int32_t spp_blob_layout(const spp_model_desc* desc);
+
+/* Pack one expert into its blob on the host, in the layout of
+ * spp_blob_layout(desc).  gate, up: host [I][D]; down: host [D][I]; all in
+ * the storage dtype; blob: host, spp_blob_stride(desc) bytes (the padding is
+ * zeroed).  Host stores and shared-expert blobs must hold blobs in this
+ * layout.  Errors: EINVAL for a bad desc or a NULL pointer. */
+spp_status spp_pack_expert(const spp_model_desc* desc, const void* gate, const void* up, const void* down,
+                           void* blob);
 
 /* Create a context on the current device.  hip_stream: the compute stream
  * (hipStream_t, may be NULL for the null stream).  Allocates S slots per layer
@@ -153,7 +176,7 @@ spp_status expert_cache_issue_prefetch(spp_ctx* ctx, int32_t target_layer, const
  *   (replacement: lowest EMPTY slot, else the least recently stamped slot
  *   whose expert the batch does not need); every slot holding a needed
  *   expert takes the step stamp.  When the batch needs more distinct experts
- *   than S (B > 1, bf16 only), the step runs in rounds: load while a victim
+ *   than S (tiled-layout contexts only), the step runs in rounds: load while a victim
  *   exists (third victim class: the lowest-index slot whose expert already
  *   ran this step), run every resident needed expert not yet run, repeat;
  *   if M_max > 0: the expert_cache_issue_prefetch selection for layer l+1

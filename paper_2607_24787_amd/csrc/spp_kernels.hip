@@ -744,23 +744,34 @@ __global__ __launch_bounds__(64 * kCombGroups) void ffn_combine_kernel(CombineAr
 }
 
 // ---------------------------------------------------------------------------
-// Batched decode: each workgroup takes one group (up to 16 tokens routed to
-// the same expert) and one range of upw units of that expert.
+// Batched decode over the tiled expert layout (nb = D/256 column blocks,
+// I/16 tiles of 16 units):
+//   gate/up part, 16-byte pieces in MFMA operand order: piece
+//     (((tile*nb + blk)*2 + w)*8 + j)*64 + l  holds  W_w[16 tile + l%16][256 blk + 32 j + 8 (l/16) + e],
+//     e < 8, w = 0 gate / 1 up -- one wave load of step j is 1 KiB contiguous;
+//   down part, after the 2*I*D gate/up elements: run (s*I + i) holds
+//     W_down[256 s + c][i], c < 256 -- consecutive units of a slice are contiguous.
+// Each workgroup takes one group (up to 16 tokens routed to the same expert)
+// and one range of upw units of that expert (upw = 64, 128 or 256).
 //   phase A: G = X W_gate^T and U = X W_up^T on MFMA (v_mfma_f32_16x16x32_bf16,
 //            tokens padded to the 16 rows of the tile, units as the 16
-//            columns, D as the contraction).  x is staged in LDS per
-//            512-wide chunk as a bf16 pair x = hi + lo (hi = bf16(x),
-//            lo = bf16(x - hi)), and both halves are multiplied, so the
-//            contraction keeps x to ~2^-17 relative (the weights are bf16
-//            already); H = silu(G) * U into LDS (fp32).
-//   phase B: each wave streams the down columns of the range over its
-//            256-wide slices of D and accumulates H[t][i] * down_i for every
-//            token of the group; one partial output row per (token, range).
+//            columns, D as the contraction); wave w owns tiles w, w+8.  x is
+//            staged in LDS per 512-wide chunk as a bf16 pair x = hi + lo
+//            (hi = bf16(x), lo = bf16(x - hi)), and both halves are
+//            multiplied, so the contraction keeps x to ~2^-17 relative (the
+//            weights are bf16 already).  The 16 loads of one 256-column block
+//            (16 KiB contiguous per wave) are all issued before its MFMAs.
+//            H = silu(G) * U into LDS (fp32).
+//   phase B: each wave streams the down runs of the range over its 256-wide
+//            slices of D (kUB units in flight, 4 KiB contiguous) and
+//            accumulates H[t][i] * down_i for every token of the group; one
+//            partial output row per (token, range).
 // ---------------------------------------------------------------------------
 constexpr int kGrpWaves = 8;
 constexpr int kGrpThreads = 64 * kGrpWaves;
-constexpr int kGrpKC = 512;     // x columns staged per chunk
-constexpr int kGrpMaxUpw = 256; // units per range
+constexpr int kGrpKC = 512;      // x columns staged per chunk (two blocks)
+constexpr int kGrpBlk = 256;     // columns per block: 8 k-steps of 32
+constexpr int kGrpMaxUpw = 256;  // units per range
 
 typedef __bf16 bf16x8 __attribute__((ext_vector_type(8)));
 typedef float f32x4 __attribute__((ext_vector_type(4)));
@@ -772,44 +783,62 @@ __device__ __forceinline__ uint16_t f32_to_bf16_rne(float v) {
   return static_cast<uint16_t>(b >> 16);
 }
 
+__device__ __forceinline__ uint32_t pack2(uint16_t lo, uint16_t hi) {
+  return lo | (static_cast<uint32_t>(hi) << 16);
+}
+
 __global__ __launch_bounds__(kGrpThreads) void ffn_grouped_kernel(GroupArgs a) {
-  __shared__ uint16_t s_xh[kGroupTokens * kGrpKC];  // 16 KiB, bf16(x)
-  __shared__ uint16_t s_xl[kGroupTokens * kGrpKC];  // 16 KiB, bf16(x - bf16(x))
-  __shared__ float s_h[kGroupTokens * kGrpMaxUpw];  // 16 KiB
+  __shared__ __attribute__((aligned(16))) uint16_t s_xh[kGroupTokens * kGrpKC];  // 16 KiB, bf16(x)
+  __shared__ __attribute__((aligned(16))) uint16_t s_xl[kGroupTokens * kGrpKC];  // 16 KiB, bf16(x - hi)
+  __shared__ __attribute__((aligned(16))) float s_h[kGroupTokens * kGrpMaxUpw];  // 16 KiB
+  __shared__ int s_pair[kGroupTokens];
   const int tid = threadIdx.x, lane = tid & 63;
   const int wave = __builtin_amdgcn_readfirstlane(tid >> 6);
-  const int D = a.D;
+  const int D = a.D, I = a.I, nb = D / kGrpBlk;
   const int g = blockIdx.x / a.nsplit, split = blockIdx.x - g * a.nsplit;
   const GroupDesc* G = a.groups + g;
   const int m = G->m;
   const int i0 = split * a.upw;
-  const int nu = min(a.upw, a.I - i0);
+  const int nu = min(a.upw, I - i0);  // a multiple of 16
   const uint16_t* blob = reinterpret_cast<const uint16_t*>(G->blob);
-  const size_t unit_elems = static_cast<size_t>(3) * D;
+  if (tid < kGroupTokens) s_pair[tid] = tid < m ? G->pair[tid] : 0;  // read after the first barrier
 
   // ---- phase A: gate / up tiles of 16 units on MFMA
-  const int ntiles = (nu + 15) >> 4;
+  const int ntiles = nu >> 4;
   constexpr int kMaxTilesPerWave = kGrpMaxUpw / 16 / kGrpWaves;  // 2
   f32x4 accg[kMaxTilesPerWave], accu[kMaxTilesPerWave];
 #pragma unroll
   for (int q = 0; q < kMaxTilesPerWave; ++q) accg[q] = accu[q] = f32x4{0.f, 0.f, 0.f, 0.f};
-  const int krow = lane & 15;         // A row (token) and B column (unit) of this lane
-  const int koff = 8 * (lane >> 4);   // this lane's 8-wide k slice inside a 32-wide step
-  for (int kc = 0; kc < D; kc += kGrpKC) {
-    const int kw = min(kGrpKC, D - kc);
-    __syncthreads();  // previous chunk consumed
-    for (int idx = tid; idx < kGroupTokens * (kw / 4); idx += kGrpThreads) {
-      const int t = idx / (kw / 4), c4 = idx - t * (kw / 4);
-      float4 v = make_float4(0.f, 0.f, 0.f, 0.f);
-      if (t < m) v = *SPP_GLOBAL(float4, a.x + static_cast<size_t>(G->tok[t]) * D + kc + 4 * c4);
-      const float vv[4] = {v.x, v.y, v.z, v.w};
-      uint16_t* dh = s_xh + t * kGrpKC + 4 * c4;
-      uint16_t* dl = s_xl + t * kGrpKC + 4 * c4;
+  const int krow = lane & 15;        // A row (token) of this lane
+  const int koff = 8 * (lane >> 4);  // this lane's 8-wide k slice inside a 32-wide step
+  // x staging: thread tid covers float4 column c4 = tid % 128 of tokens tid / 128 + 4 q
+  const int sc4 = tid & 127, st0 = tid >> 7;
+  const float* xrow[kGroupTokens / 4];
 #pragma unroll
-      for (int q = 0; q < 4; ++q) {
-        const uint16_t hi = f32_to_bf16_rne(vv[q]);
-        dh[q] = hi;
-        dl[q] = f32_to_bf16_rne(vv[q] - __uint_as_float(static_cast<uint32_t>(hi) << 16));
+  for (int q = 0; q < kGroupTokens / 4; ++q) {
+    const int t = st0 + 4 * q;
+    xrow[q] = a.x + static_cast<size_t>(G->tok[t < m ? t : 0]) * D;
+  }
+  for (int kc = 0; kc < D; kc += kGrpKC) {
+    const int kw = min(kGrpKC, D - kc);  // 512 or 256
+    __syncthreads();                     // previous chunk consumed
+    if (4 * sc4 < kw) {
+      float4 v[kGroupTokens / 4];
+#pragma unroll
+      for (int q = 0; q < kGroupTokens / 4; ++q) v[q] = *SPP_GLOBAL(float4, xrow[q] + kc + 4 * sc4);
+#pragma unroll
+      for (int q = 0; q < kGroupTokens / 4; ++q) {
+        const int t = st0 + 4 * q;
+        const float vv[4] = {v[q].x, v[q].y, v[q].z, v[q].w};
+        uint16_t hi[4], lo[4];
+#pragma unroll
+        for (int c = 0; c < 4; ++c) {
+          hi[c] = t < m ? f32_to_bf16_rne(vv[c]) : 0;
+          lo[c] = t < m ? f32_to_bf16_rne(vv[c] - __uint_as_float(static_cast<uint32_t>(hi[c]) << 16)) : 0;
+        }
+        const int o = t * kGrpKC + 4 * sc4;
+        *reinterpret_cast<uint2*>(s_xh + o) = make_uint2(pack2(hi[0], hi[1]), pack2(hi[2], hi[3]));
+        *reinterpret_cast<uint2*>(s_xl + o) = make_uint2(pack2(lo[0], lo[1]), pack2(lo[2], lo[3]));
       }
     }
     __syncthreads();
@@ -817,24 +846,28 @@ __global__ __launch_bounds__(kGrpThreads) void ffn_grouped_kernel(GroupArgs a) {
     for (int q = 0; q < kMaxTilesPerWave; ++q) {
       const int tile = wave + q * kGrpWaves;
       if (tile >= ntiles) continue;  // wave-uniform
-      const int ul = tile * 16 + krow;
-      const bool uok = ul < nu;
-      const uint16_t* grow = blob + static_cast<size_t>(i0 + (uok ? ul : 0)) * unit_elems + kc;
-      const uint16_t* urow = grow + D;
-#pragma unroll 4
-      for (int ks = 0; ks < kw; ks += 32) {
-        const u32x4 ah = *reinterpret_cast<const u32x4*>(s_xh + krow * kGrpKC + ks + koff);
-        const u32x4 al = *reinterpret_cast<const u32x4*>(s_xl + krow * kGrpKC + ks + koff);
-        u32x4 bg = u32x4{0u, 0u, 0u, 0u}, bu = u32x4{0u, 0u, 0u, 0u};
-        if (uok) {
-          bg = __builtin_nontemporal_load(SPP_GLOBAL(u32x4, grow + ks + koff));
-          bu = __builtin_nontemporal_load(SPP_GLOBAL(u32x4, urow + ks + koff));
+      const int gt = (i0 >> 4) + tile;
+      for (int bo = 0; bo < kw; bo += kGrpBlk) {
+        const int blk = (kc + bo) / kGrpBlk;
+        const u32x4* pg = reinterpret_cast<const u32x4*>(blob) + static_cast<size_t>(gt * nb + blk) * 2 * 8 * 64 + lane;
+        u32x4 bg[kGrpBlk / 32], bu[kGrpBlk / 32];
+#pragma unroll
+        for (int j = 0; j < kGrpBlk / 32; ++j) {
+          bg[j] = __builtin_nontemporal_load(SPP_GLOBAL(u32x4, pg + j * 64));
+          bu[j] = __builtin_nontemporal_load(SPP_GLOBAL(u32x4, pg + (8 + j) * 64));
         }
-        const bf16x8 wg = __builtin_bit_cast(bf16x8, bg), wu = __builtin_bit_cast(bf16x8, bu);
-        accg[q] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(__builtin_bit_cast(bf16x8, ah), wg, accg[q], 0, 0, 0);
-        accg[q] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(__builtin_bit_cast(bf16x8, al), wg, accg[q], 0, 0, 0);
-        accu[q] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(__builtin_bit_cast(bf16x8, ah), wu, accu[q], 0, 0, 0);
-        accu[q] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(__builtin_bit_cast(bf16x8, al), wu, accu[q], 0, 0, 0);
+        __builtin_amdgcn_sched_barrier(0);  // keep the whole block of loads ahead of the MFMAs
+#pragma unroll
+        for (int j = 0; j < kGrpBlk / 32; ++j) {
+          const int ko = krow * kGrpKC + bo + 32 * j + koff;
+          const bf16x8 ah = __builtin_bit_cast(bf16x8, *reinterpret_cast<const u32x4*>(s_xh + ko));
+          const bf16x8 al = __builtin_bit_cast(bf16x8, *reinterpret_cast<const u32x4*>(s_xl + ko));
+          const bf16x8 wg = __builtin_bit_cast(bf16x8, bg[j]), wu = __builtin_bit_cast(bf16x8, bu[j]);
+          accg[q] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(ah, wg, accg[q], 0, 0, 0);
+          accg[q] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(al, wg, accg[q], 0, 0, 0);
+          accu[q] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(ah, wu, accu[q], 0, 0, 0);
+          accu[q] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(al, wu, accu[q], 0, 0, 0);
+        }
       }
     }
   }
@@ -844,46 +877,46 @@ __global__ __launch_bounds__(kGrpThreads) void ffn_grouped_kernel(GroupArgs a) {
     const int tile = wave + q * kGrpWaves;
     if (tile >= ntiles) continue;
     const int ul = tile * 16 + krow;
-    if (ul < nu) {
 #pragma unroll
-      for (int j = 0; j < 4; ++j) {
-        const int t = 4 * (lane >> 4) + j;
-        const float gv = accg[q][j];
-        s_h[t * kGrpMaxUpw + ul] = gv / (1.f + expf(-gv)) * accu[q][j];
-      }
+    for (int j = 0; j < 4; ++j) {
+      const int t = 4 * (lane >> 4) + j;
+      const float gv = accg[q][j];
+      s_h[t * kGrpMaxUpw + ul] = gv / (1.f + expf(-gv)) * accu[q][j];
     }
   }
   __syncthreads();
 
-  // ---- phase B: down columns over 256-wide slices of D, all tokens of the group
-  for (int dc = wave; dc * 256 < D; dc += kGrpWaves) {
-    const int d0 = dc * 256 + lane * 4;
+  // ---- phase B: down runs over 256-wide slices of D, all tokens of the group
+  constexpr int kUB = 8;  // down-run loads in flight per lane (nu is a multiple of 16)
+  const uint16_t* down = blob + static_cast<size_t>(2) * I * D;
+  for (int dc = wave; dc < nb; dc += kGrpWaves) {
+    const int d0 = dc * kGrpBlk + lane * 4;
     float acc[kGroupTokens][4];
 #pragma unroll
     for (int t = 0; t < kGroupTokens; ++t)
 #pragma unroll
       for (int v = 0; v < 4; ++v) acc[t][v] = 0.f;
-    const uint16_t* dcol = blob + static_cast<size_t>(i0) * unit_elems + 2 * D + d0;
-    constexpr int kUB = 8;  // down-column loads in flight per lane
+    const uint16_t* drun = down + (static_cast<size_t>(dc) * I + i0) * kGrpBlk + lane * 4;
     for (int u = 0; u < nu; u += kUB) {
       uint2 raw[kUB];
 #pragma unroll
-      for (int uu = 0; uu < kUB; ++uu) {
-        raw[uu] = make_uint2(0u, 0u);
-        if (u + uu < nu) raw[uu] = *SPP_GLOBAL(uint2, dcol + static_cast<size_t>(u + uu) * unit_elems);
-      }
+      for (int uu = 0; uu < kUB; ++uu) raw[uu] = *SPP_GLOBAL(uint2, drun + static_cast<size_t>(u + uu) * kGrpBlk);
 #pragma unroll
-      for (int uu = 0; uu < kUB; ++uu) {
-        // units past the range loaded zeros; their s_h index is clamped in range
-        const int ui = min(u + uu, nu - 1);
-        const float dv[4] = {__uint_as_float(raw[uu].x << 16), __uint_as_float(raw[uu].x & 0xffff0000u),
-                             __uint_as_float(raw[uu].y << 16), __uint_as_float(raw[uu].y & 0xffff0000u)};
+      for (int t = 0; t < kGroupTokens; ++t) {
+        if (t < m) {  // wave-uniform
+          const float4* hp = reinterpret_cast<const float4*>(s_h + t * kGrpMaxUpw + u);
 #pragma unroll
-        for (int t = 0; t < kGroupTokens; ++t) {
-          if (t < m) {
-            const float h = s_h[t * kGrpMaxUpw + ui];
+          for (int p = 0; p < kUB / 4; ++p) {
+            const float4 h4 = hp[p];
+            const float hv[4] = {h4.x, h4.y, h4.z, h4.w};
 #pragma unroll
-            for (int v = 0; v < 4; ++v) acc[t][v] += h * dv[v];
+            for (int c = 0; c < 4; ++c) {
+              const uint2 r = raw[4 * p + c];
+              acc[t][0] += hv[c] * __uint_as_float(r.x << 16);
+              acc[t][1] += hv[c] * __uint_as_float(r.x & 0xffff0000u);
+              acc[t][2] += hv[c] * __uint_as_float(r.y << 16);
+              acc[t][3] += hv[c] * __uint_as_float(r.y & 0xffff0000u);
+            }
           }
         }
       }
@@ -891,7 +924,7 @@ __global__ __launch_bounds__(kGrpThreads) void ffn_grouped_kernel(GroupArgs a) {
 #pragma unroll
     for (int t = 0; t < kGroupTokens; ++t) {
       if (t < m) {
-        float* dst = a.ypart + (static_cast<size_t>(G->pair[t]) * a.nsplit + split) * D + d0;
+        float* dst = a.ypart + (static_cast<size_t>(s_pair[t]) * a.nsplit + split) * D + d0;
         *reinterpret_cast<float4*>(dst) = make_float4(acc[t][0], acc[t][1], acc[t][2], acc[t][3]);
       }
     }
@@ -900,27 +933,62 @@ __global__ __launch_bounds__(kGrpThreads) void ffn_grouped_kernel(GroupArgs a) {
 
 // Batched combine: h_out[b] = round(residual[b] + sum_k g_bk sum_r ypart[(b,k), r]
 //                                   + sum_j sum_r ypart[(b, shared j), r]), fixed order.
+// One thread per 4 consecutive columns; the partials of one pair are loaded
+// four ranges at a time.
+__device__ __forceinline__ float4 sum_ranges(const float* p, int nsplit, int D) {
+  float4 v = make_float4(0.f, 0.f, 0.f, 0.f);
+  int r = 0;
+  for (; r + 4 <= nsplit; r += 4) {
+    float4 w[4];
+#pragma unroll
+    for (int q = 0; q < 4; ++q) w[q] = *SPP_GLOBAL(float4, p + static_cast<size_t>(r + q) * D);
+#pragma unroll
+    for (int q = 0; q < 4; ++q) {
+      v.x += w[q].x;
+      v.y += w[q].y;
+      v.z += w[q].z;
+      v.w += w[q].w;
+    }
+  }
+  for (; r < nsplit; ++r) {
+    const float4 w = *SPP_GLOBAL(float4, p + static_cast<size_t>(r) * D);
+    v.x += w.x;
+    v.y += w.y;
+    v.z += w.z;
+    v.w += w.w;
+  }
+  return v;
+}
+
 template <typename T>
 __global__ __launch_bounds__(256) void ffn_combine_batched_kernel(CombineBArgs a) {
   const int b = blockIdx.y;
-  const int d = blockIdx.x * 256 + threadIdx.x;
+  const int d = 4 * (blockIdx.x * 256 + threadIdx.x);
   if (d >= a.D) return;
-  float y = 0.f;
+  float y[4] = {0.f, 0.f, 0.f, 0.f};
   for (int k = 0; k < a.K; ++k) {
     const size_t row = static_cast<size_t>(b * a.K + k) * a.nsplit;
-    float v = 0.f;
-    for (int r = 0; r < a.nsplit; ++r) v += a.ypart[(row + r) * a.D + d];
-    y += a.gates[b * a.K + k] * v;
+    const float4 v = sum_ranges(a.ypart + row * a.D + d, a.nsplit, a.D);
+    const float gk = a.gates[b * a.K + k];
+    y[0] += gk * v.x;
+    y[1] += gk * v.y;
+    y[2] += gk * v.z;
+    y[3] += gk * v.w;
   }
   for (int j = 0; j < a.n_shared; ++j) {
     const size_t row = static_cast<size_t>(a.B * a.K + b * a.n_shared + j) * a.nsplit;
-    float v = 0.f;
-    for (int r = 0; r < a.nsplit; ++r) v += a.ypart[(row + r) * a.D + d];
-    y += v;
+    const float4 v = sum_ranges(a.ypart + row * a.D + d, a.nsplit, a.D);
+    y[0] += v.x;
+    y[1] += v.y;
+    y[2] += v.z;
+    y[3] += v.w;
   }
   const size_t o = static_cast<size_t>(b) * a.D + d;
-  const float res = a.res_u ? a.res_u[o] : load_elem<T>(a.res_h, o);
-  store_elem<T>(a.out, o, res + y);
+#pragma unroll
+  for (int c = 0; c < 4; ++c) {
+    const float res = a.res_u ? a.res_u[o + c] : load_elem<T>(a.res_h, o + c);
+    store_elem<T>(a.out, o + c, res + y[c]);
+  }
 }
 
 // Stand-in projection prologue: u = h + P rms(h) (fp32 result).  One wave per row of P.
@@ -1057,8 +1125,8 @@ hipError_t launch_proj(const ProjArgs& a, int dtype, hipStream_t st) {
 }
 
 hipError_t launch_ffn_grouped(const GroupArgs& a, hipStream_t st, hipEvent_t start, hipEvent_t stop) {
-  if (a.ngroups <= 0 || a.nsplit <= 0 || a.upw <= 0 || a.upw > kGrpMaxUpw || a.D % 256 != 0 ||
-      a.nsplit * a.upw < a.I)
+  if (a.ngroups <= 0 || a.nsplit <= 0 || (a.upw != 64 && a.upw != 128 && a.upw != 256) || a.D % kGrpBlk != 0 ||
+      a.I % 16 != 0 || a.nsplit * a.upw < a.I)
     return hipErrorInvalidValue;
   const dim3 grid(static_cast<unsigned>(a.ngroups * a.nsplit));
   if (start || stop)
@@ -1069,7 +1137,8 @@ hipError_t launch_ffn_grouped(const GroupArgs& a, hipStream_t st, hipEvent_t sta
 }
 
 hipError_t launch_combine_batched(const CombineBArgs& a, int dtype, hipStream_t st) {
-  const dim3 grid((a.D + 255) / 256, a.B);
+  if (a.D % 4 != 0) return hipErrorInvalidValue;
+  const dim3 grid((a.D / 4 + 255) / 256, a.B);
   if (dtype == 1)
     hipLaunchKernelGGL((ffn_combine_batched_kernel<uint16_t>), grid, dim3(256), 0, st, a);
   else

@@ -69,6 +69,7 @@ size_t round_up(size_t v, size_t a) { return (v + a - 1) / a * a; }
 struct spp_ctx {
   spp_model_desc d{};
   int device = 0;
+  int num_cu = 256;  // compute units of the device
   hipStream_t compute = nullptr;
   hipStream_t copy = nullptr;
   size_t elem = 0, blob_bytes = 0, stride = 0;
@@ -111,6 +112,12 @@ struct spp_ctx {
 };
 
 namespace {
+
+// Batched contexts (bf16, max_batch > 1, D % 256 == 0, I % 16 == 0) store
+// experts in the tiled layout the grouped MFMA kernel streams linearly.
+bool tiled_layout(const spp_model_desc& d) {
+  return d.max_batch > 1 && d.dtype == SPP_DTYPE_BF16 && d.D % 256 == 0 && d.I % 16 == 0;
+}
 
 bool desc_ok(const spp_model_desc* d, std::string* why) {
   if (!d) return *why = "desc is NULL", false;
@@ -276,6 +283,7 @@ spp_status create_impl(const spp_model_desc* desc, void* stream, spp_ctx** out) 
   if (!c) return fail(SPP_ENOMEM, "host allocation failed");
   c->d = *desc;
   SPP_HIP(hipGetDevice(&c->device));
+  SPP_HIP(hipDeviceGetAttribute(&c->num_cu, hipDeviceAttributeMultiprocessorCount, c->device));
   c->compute = static_cast<hipStream_t>(stream);
   c->elem = desc->dtype == SPP_DTYPE_BF16 ? 2 : 4;
   c->blob_bytes = static_cast<size_t>(3) * desc->I * desc->D * c->elem;
@@ -308,7 +316,7 @@ spp_status create_impl(const spp_model_desc* desc, void* stream, spp_ctx** out) 
   SPP_HIP(hipHostGetDevicePointer(reinterpret_cast<void**>(&c->res_host_dev), c->res_host, 0));
   std::memset(c->res_host, 0, c->res_bytes);
   // batched decode runs the routed experts as grouped MFMA contractions
-  c->grouped = d.max_batch > 1 && d.dtype == SPP_DTYPE_BF16 && d.D % 256 == 0;
+  c->grouped = tiled_layout(d);
   if (c->grouped) {
     c->max_groups = d.max_batch * d.K + d.n_shared * ((d.max_batch + spp::kGroupTokens - 1) / spp::kGroupTokens);
     c->max_nsplit = (d.I + 63) / 64;
@@ -412,11 +420,9 @@ spp_status grouped_ffn(spp_ctx* c, LayerState& ls, LayerState* next, const int32
   }
   SPP_HIP(hipMemcpyAsync(c->groups_dev, c->groups_host, sizeof(spp::GroupDesc) * ng, hipMemcpyHostToDevice,
                          c->compute));
-  // unit ranges in multiples of 64 units (at most 256), about 512 workgroups
-  // per launch: one full round at two workgroups per compute unit
-  const int target = std::max(1, 512 / std::max(1, maxg));
-  int upw = 64 * std::max(1, static_cast<int>(std::lround(static_cast<double>(d.I) / (64.0 * target))));
-  upw = std::min(upw, 256);
+  // ranges of 128 units (one 16-unit tile per wave); 64 when the largest
+  // round would not give two workgroups per compute unit
+  const int upw = static_cast<long>(maxg) * ((d.I + 127) / 128) >= 2L * c->num_cu ? 128 : 64;
   const int nsplit = (d.I + upw - 1) / upw;
   if (nsplit > c->max_nsplit) return fail(SPP_ESTATE, "unit split exceeds the partial buffer");
   for (size_t r = 0; r < rounds.size(); ++r) {
@@ -545,7 +551,7 @@ spp_status layer_forward_impl(spp_ctx* c, int32_t l, const void* h_in, void* h_o
   }
   ls.pending_prefetch.clear();
   std::string why;
-  const bool batched = c->grouped && B > 1;
+  const bool batched = c->grouped;  // the tiled layout is read by the grouped kernel only
   if (!batched && ls.policy->distinct(T, BK) > d.S)
     return fail(SPP_ESTATE, "batch demand exceeds the slot count; more than S distinct experts per step "
                             "needs the batched bf16 path");
@@ -643,6 +649,51 @@ size_t spp_blob_stride(const spp_model_desc* d) {
   if (!d) return 0;
   const size_t elem = d->dtype == SPP_DTYPE_BF16 ? 2 : 4;
   return round_up(static_cast<size_t>(3) * d->I * d->D * elem, 4096);
+}
+
+int32_t spp_blob_layout(const spp_model_desc* d) {
+  if (!d) return -1;
+  return tiled_layout(*d) ? SPP_LAYOUT_TILED : SPP_LAYOUT_UNITS;
+}
+
+spp_status spp_pack_expert(const spp_model_desc* d, const void* gate, const void* up, const void* down,
+                           void* blob) {
+  std::string why;
+  if (!desc_ok(d, &why)) return fail(SPP_EINVAL, why);
+  if (!gate || !up || !down || !blob) return fail(SPP_EINVAL, "gate, up, down and blob must not be NULL");
+  const size_t D = d->D, I = d->I, es = d->dtype == SPP_DTYPE_BF16 ? 2 : 4;
+  const uint8_t* g = static_cast<const uint8_t*>(gate);
+  const uint8_t* u = static_cast<const uint8_t*>(up);
+  const uint8_t* w = static_cast<const uint8_t*>(down);
+  uint8_t* o = static_cast<uint8_t*>(blob);
+  if (!tiled_layout(*d)) {
+    for (size_t i = 0; i < I; ++i) {
+      std::memcpy(o + (3 * i + 0) * D * es, g + i * D * es, D * es);
+      std::memcpy(o + (3 * i + 1) * D * es, u + i * D * es, D * es);
+      uint8_t* col = o + (3 * i + 2) * D * es;
+      for (size_t r = 0; r < D; ++r) std::memcpy(col + r * es, w + (r * I + i) * es, es);
+    }
+  } else {
+    const size_t nb = D / 256, nt = I / 16;
+    const uint8_t* src[2] = {g, u};
+    for (size_t t = 0; t < nt; ++t)
+      for (size_t b = 0; b < nb; ++b)
+        for (size_t m = 0; m < 2; ++m)
+          for (size_t j = 0; j < 8; ++j)
+            for (size_t l = 0; l < 64; ++l) {
+              const size_t piece = (((t * nb + b) * 2 + m) * 8 + j) * 64 + l;
+              const size_t row = 16 * t + (l & 15), col = 256 * b + 32 * j + 8 * (l >> 4);
+              std::memcpy(o + piece * 8 * es, src[m] + (row * D + col) * es, 8 * es);
+            }
+    uint8_t* dn = o + 2 * I * D * es;
+    for (size_t sl = 0; sl < nb; ++sl)
+      for (size_t i = 0; i < I; ++i)
+        for (size_t c = 0; c < 256; ++c)
+          std::memcpy(dn + ((sl * I + i) * 256 + c) * es, w + ((256 * sl + c) * I + i) * es, es);
+  }
+  const size_t bytes = 3 * I * D * es, stride = round_up(bytes, 4096);
+  std::memset(o + bytes, 0, stride - bytes);
+  return SPP_OK;
 }
 
 spp_status spp_create(const spp_model_desc* desc, void* hip_stream, spp_ctx** out) {

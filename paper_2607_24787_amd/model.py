@@ -18,16 +18,6 @@ import numpy as np
 from . import spp
 
 
-def pack_blob(Wg: np.ndarray, Wu: np.ndarray, Wd: np.ndarray) -> np.ndarray:
-    """[I, 3, D] interleave of gate rows, up rows and down columns (storage dtype kept)."""
-    I, D = Wg.shape
-    out = np.empty((I, 3, D), dtype=Wg.dtype)
-    out[:, 0, :] = Wg
-    out[:, 1, :] = Wu
-    out[:, 2, :] = Wd.T
-    return out
-
-
 def _torch_from_storage(a: np.ndarray, device):
     import torch
     if a.dtype == np.uint16:
@@ -80,8 +70,8 @@ class OffloadedMoEStack:
             if cfg.n_shared:
                 buf = np.zeros(cfg.n_shared * self.stride, dtype=np.uint8)
                 for j in range(cfg.n_shared):
-                    blob = pack_blob(*gen.shared_expert_weights(cfg, l, j))
-                    buf[j * self.stride: j * self.stride + blob.nbytes] = blob.reshape(-1).view(np.uint8)
+                    spp.spp_pack_expert(self.desc, *gen.shared_expert_weights(cfg, l, j),
+                                        out=buf[j * self.stride:(j + 1) * self.stride])
                 self.shared.append(torch.from_numpy(buf).to(self.device))
             else:
                 self.shared.append(None)
@@ -93,8 +83,8 @@ class OffloadedMoEStack:
 
         def fill(job):
             hl, e = job
-            blob = pack_blob(*gen.expert_weights(cfg, hl, e)).reshape(-1).view(np.uint8)
-            views[hl][e * self.stride: e * self.stride + blob.nbytes] = blob
+            spp.spp_pack_expert(self.desc, *gen.expert_weights(cfg, hl, e),
+                                out=views[hl][e * self.stride:(e + 1) * self.stride])
 
         jobs = [(hl, e) for hl in range(self.host_layers) for e in range(cfg.n)]
         with ThreadPoolExecutor(max_workers=threads) as ex:

@@ -17,6 +17,7 @@ LIB_PATH = os.path.join(os.path.dirname(os.path.abspath(__file__)), "libspp.so")
 
 SPP_OK, SPP_EINVAL, SPP_ENOMEM, SPP_EHIP, SPP_ESTATE = 0, -1, -2, -3, -4
 DTYPE_F32, DTYPE_BF16 = 0, 1
+LAYOUT_UNITS, LAYOUT_TILED = 0, 1
 
 
 class SppError(RuntimeError):
@@ -48,6 +49,8 @@ class RunStats(ctypes.Structure):
 
 _SIGS = {
     "spp_blob_stride": (c_size_t, [POINTER(ModelDesc)]),
+    "spp_blob_layout": (c_int32, [POINTER(ModelDesc)]),
+    "spp_pack_expert": (c_int32, [POINTER(ModelDesc), c_void_p, c_void_p, c_void_p, c_void_p]),
     "spp_create": (c_int32, [POINTER(ModelDesc), c_void_p, POINTER(c_void_p)]),
     "spp_destroy": (c_int32, [c_void_p]),
     "spp_bind_layer": (c_int32, [c_void_p, c_int32, c_void_p, c_void_p, c_void_p, c_void_p, c_void_p, c_void_p]),
@@ -132,6 +135,28 @@ def make_desc(L, D, n, K, I, r, S, max_batch=1, n_shared=0, dtype=DTYPE_BF16, ha
 
 def spp_blob_stride(desc: ModelDesc) -> int:
     return int(lib().spp_blob_stride(byref(desc)))
+
+
+def spp_blob_layout(desc: ModelDesc) -> int:
+    return int(lib().spp_blob_layout(byref(desc)))
+
+
+def spp_pack_expert(desc: ModelDesc, gate, up, down, out=None):
+    """Pack one expert (storage-dtype arrays gate/up [I, D], down [D, I]) into
+    `out` (writable uint8, at least spp_blob_stride bytes) or a new array."""
+    import numpy as np
+    want = np.uint16 if desc.dtype == DTYPE_BF16 else np.float32
+    mats = [np.ascontiguousarray(m, dtype=want) for m in (gate, up, down)]
+    if mats[0].shape != (desc.I, desc.D) or mats[1].shape != (desc.I, desc.D) or mats[2].shape != (desc.D, desc.I):
+        raise ValueError("gate/up must be [I, D] and down [D, I]")
+    stride = spp_blob_stride(desc)
+    if out is None:
+        out = np.empty(stride, dtype=np.uint8)
+    if out.dtype != np.uint8 or out.nbytes < stride or not out.flags.c_contiguous or not out.flags.writeable:
+        raise ValueError("out must be a writable contiguous uint8 array of at least the blob stride")
+    _check(lib().spp_pack_expert(byref(desc), mats[0].ctypes.data, mats[1].ctypes.data, mats[2].ctypes.data,
+                                 out.ctypes.data))
+    return out
 
 
 def spp_create(desc: ModelDesc, stream: int = 0) -> int:

@@ -111,3 +111,58 @@ def test_blob_stride():
     assert spp.spp_blob_stride(d) == 9_437_184                 # 3*768*2048*2, already 4 KiB aligned
     d = spp.make_desc(L=2, D=96, n=12, K=3, I=40, r=8, S=12, dtype=spp.DTYPE_F32)
     assert spp.spp_blob_stride(d) == 49152                     # 46080 rounded up to 4 KiB
+
+
+def _expected_blob(layout, G, U, Wd):
+    """The blob the header's layout formulas describe, element by element."""
+    I, D = G.shape
+    out = np.zeros(3 * I * D, dtype=G.dtype)
+    if layout == spp.LAYOUT_UNITS:
+        for i in range(I):
+            for d in range(D):
+                out[(3 * i + 0) * D + d] = G[i, d]
+                out[(3 * i + 1) * D + d] = U[i, d]
+                out[(3 * i + 2) * D + d] = Wd[d, i]
+        return out
+    nb = D // 256
+    for t in range(I // 16):
+        for b in range(nb):
+            for w, W in enumerate((G, U)):
+                for j in range(8):
+                    for l in range(64):
+                        piece = (((t * nb + b) * 2 + w) * 8 + j) * 64 + l
+                        row, col = 16 * t + l % 16, 256 * b + 32 * j + 8 * (l // 16)
+                        out[piece * 8: piece * 8 + 8] = W[row, col: col + 8]
+    for s in range(nb):
+        for i in range(I):
+            run = s * I + i
+            out[2 * I * D + run * 256: 2 * I * D + run * 256 + 256] = Wd[256 * s: 256 * s + 256, i]
+    return out
+
+
+@pytest.mark.parametrize("case", ["units_f32", "units_bf16_batch1", "tiled_bf16"])
+def test_pack_expert_places_every_element_where_the_header_says(case):
+    if case == "units_f32":
+        d, dt = spp.make_desc(L=2, D=96, n=12, K=3, I=40, r=8, S=12, dtype=spp.DTYPE_F32), np.float32
+    elif case == "units_bf16_batch1":
+        d, dt = spp.make_desc(L=2, D=512, n=12, K=3, I=32, r=8, S=12), np.uint16
+    else:
+        d, dt = spp.make_desc(L=2, D=512, n=12, K=3, I=32, r=8, S=12, max_batch=4), np.uint16
+    want_layout = spp.LAYOUT_TILED if case == "tiled_bf16" else spp.LAYOUT_UNITS
+    assert spp.spp_blob_layout(d) == want_layout
+    I, D = d.I, d.D
+    vals = np.arange(3 * I * D).astype(dt)                     # every element distinct
+    G, U, Wd = vals[:I * D].reshape(I, D), vals[I * D:2 * I * D].reshape(I, D), vals[2 * I * D:].reshape(D, I)
+    stride = spp.spp_blob_stride(d)
+    out = np.full(stride, 0xAB, dtype=np.uint8)
+    spp.spp_pack_expert(d, G, U, Wd, out=out)
+    got = out[:3 * I * D * np.dtype(dt).itemsize].view(dt)
+    assert np.array_equal(got, _expected_blob(want_layout, G, U, Wd))
+    assert not out[3 * I * D * np.dtype(dt).itemsize:].any()   # padding zeroed
+    # the tiled layout needs D % 256 == 0 and I % 16 == 0; other batched shapes keep the unit layout
+    assert spp.spp_blob_layout(spp.make_desc(L=2, D=640, n=12, K=3, I=32, r=8, S=12, max_batch=4)) == spp.LAYOUT_UNITS
+    assert spp.spp_blob_layout(spp.make_desc(L=2, D=512, n=12, K=3, I=40, r=8, S=12, max_batch=4)) == spp.LAYOUT_UNITS
+    assert spp.lib().spp_pack_expert(None, None, None, None, None) == spp.SPP_EINVAL
+    assert spp.lib().spp_pack_expert(ctypes.byref(d), None, None, None, out.ctypes.data) == spp.SPP_EINVAL
+    with pytest.raises(ValueError):
+        spp.spp_pack_expert(d, G.T, U, Wd)
