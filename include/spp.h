@@ -232,7 +232,7 @@ spp_status spp_reset_run_stats(spp_ctx* ctx);
 spp_status spp_profile_expert_copy(spp_ctx* ctx, int32_t l, int32_t reps, double* per_expert_us);
 
 /* Launch shape of the routed-expert FFN: about `wgs` workgroups share the
- * (expert, unit) work list of one token (default 256; 1..4096).  Applies to
+ * (expert, unit) work list of one token (default 512; 1..4096).  Applies to
  * every context in the process. */
 spp_status spp_set_ffn_workgroups(spp_ctx* ctx, int32_t wgs);
 

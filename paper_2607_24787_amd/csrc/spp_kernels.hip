@@ -585,7 +585,7 @@ __global__ __launch_bounds__(kThreads) void router_select_kernel(RouterArgs a) {
 // sit in LDS, so each wave issues the loads of UPP units (3*UPP*NCH 16-byte
 // loads per lane) before waiting on any of them.
 // ---------------------------------------------------------------------------
-constexpr int kFfnWaves = 8;
+constexpr int kFfnWaves = 4;
 constexpr int kFfnThreads = 64 * kFfnWaves;
 
 template <int NCH>
@@ -607,8 +607,12 @@ __global__ __launch_bounds__(kFfnThreads) void ffn_units_kernel(FfnArgs a) {
   for (int j = 0; j < NCH; ++j)
 #pragma unroll
     for (int v = 0; v < V; ++v) acc[j][v] = 0.f;
+  // x goes out first: each unit's dot products then wait only for that
+  // unit's loads, and the math of the first units overlaps the arrival of
+  // the later ones
   float xv[NCH][V];
-  bool have_x = false;
+  load_row_f32<T, NCH>(a.x, lane, nch, xv);
+  __builtin_amdgcn_sched_barrier(0);
 
   const int total = a.nW * I;
   const int u0 = blockIdx.x * a.upw;
@@ -616,7 +620,6 @@ __global__ __launch_bounds__(kFfnThreads) void ffn_units_kernel(FfnArgs a) {
   const size_t unit_elems = static_cast<size_t>(3) * D;
 
   for (int ub = u0 + wave; ub < u1; ub += kFfnWaves * UPP) {
-    // the weight loads of this pass go out first; x follows them on the first pass
     uint4 rg[UPP][NCH], ru[UPP][NCH], rd[UPP][NCH];
     float gate[UPP];
 #pragma unroll
@@ -637,15 +640,9 @@ __global__ __launch_bounds__(kFfnThreads) void ffn_units_kernel(FfnArgs a) {
         for (int j = 0; j < NCH; ++j) rg[p][j] = ru[p][j] = rd[p][j] = make_uint4(0, 0, 0, 0);
       }
     }
-    if (!have_x) {
-      load_row_f32<T, NCH>(a.x, lane, nch, xv);
-      have_x = true;
-    }
-    float gs[UPP], us[UPP];
 #pragma unroll
     for (int p = 0; p < UPP; ++p) {
-      gs[p] = 0.f;
-      us[p] = 0.f;
+      float gs = 0.f, us = 0.f;
 #pragma unroll
       for (int j = 0; j < NCH; ++j) {
         float fg[V], fu[V];
@@ -653,15 +650,12 @@ __global__ __launch_bounds__(kFfnThreads) void ffn_units_kernel(FfnArgs a) {
         unpack<T>(ru[p][j], fu);
 #pragma unroll
         for (int v = 0; v < V; ++v) {
-          gs[p] += fg[v] * xv[j][v];
-          us[p] += fu[v] * xv[j][v];
+          gs += fg[v] * xv[j][v];
+          us += fu[v] * xv[j][v];
         }
       }
-    }
-#pragma unroll
-    for (int p = 0; p < UPP; ++p) {
-      const float g = wave_sum(gs[p]);
-      const float u = wave_sum(us[p]);
+      const float g = wave_sum(gs);
+      const float u = wave_sum(us);
       const float hval = g / (1.f + expf(-g)) * u * gate[p];
 #pragma unroll
       for (int j = 0; j < NCH; ++j) {
@@ -673,7 +667,7 @@ __global__ __launch_bounds__(kFfnThreads) void ffn_units_kernel(FfnArgs a) {
     }
   }
 
-  // sum the waves of this workgroup in a fixed order: (w + w+4) for w < 4, then slots 0..3
+  // sum the waves of this workgroup in a fixed order: (w + w+H) for w < H, then slots 0..H-1
   constexpr int H = kFfnWaves / 2;
   if (wave >= H) {
 #pragma unroll
@@ -1097,7 +1091,7 @@ hipError_t proj_t(const ProjArgs& a, hipStream_t st) {
   return hipGetLastError();
 }
 
-int g_ffn_target_wgs = 256;
+int g_ffn_target_wgs = 512;
 
 }  // namespace
 
@@ -1151,7 +1145,7 @@ hipError_t launch_spin(uint64_t ticks, uint32_t max_iter, hipStream_t st) {
   return hipGetLastError();
 }
 
-void set_ffn_target_wgs(int wgs) { g_ffn_target_wgs = wgs > 0 ? wgs : 256; }
+void set_ffn_target_wgs(int wgs) { g_ffn_target_wgs = wgs > 0 ? wgs : 512; }
 
 // Units per workgroup so that about g_ffn_target_wgs workgroups share the work.
 int ffn_grid_for(int nunits, int* upw) {
