@@ -28,6 +28,8 @@ struct RouterArgs {
   float* gates_host;    // [B, K] host-mapped mirror or nullptr
   float* s_host;        // [n] host-mapped mirror or nullptr
   unsigned* counter;    // zero between launches
+  unsigned* done_host;  // host-mapped completion flag (device-visible address) or nullptr
+  unsigned seq;         // value written to *done_host once every host mirror is written
   int B, D, n, K, r;
   float eps;
   int x_given;          // u holds x (no normalisation)

@@ -202,6 +202,16 @@ __device__ __forceinline__ float rms_scale(float (&xv)[NCH][Vec<T>::N], int D, f
 
 constexpr int kEQ = kMaxExpertsTopK / kThreads;  // experts per thread in the tails
 
+// Completion signal for the host: every thread's host-mirror writes are made
+// visible system-wide, then one thread stores the launch's sequence number
+// into the host-mapped flag.  Called by every thread of the last workgroup.
+__device__ __forceinline__ void signal_done(const RouterArgs& a, int tid) {
+  if (!a.done_host) return;
+  __builtin_amdgcn_fence(__ATOMIC_RELEASE, "");
+  __syncthreads();
+  if (tid == 0) __hip_atomic_store(a.done_host, a.seq, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_SYSTEM);
+}
+
 // Top-K of one token's logits zb (LDS, n values) by rank counting -- expert e
 // takes position rank(e) = #{e' beating e}, where e' beats e iff z_e' > z_e, or
 // z_e' == z_e and e' < e -- then its combine weights (softmax over all n
@@ -455,6 +465,7 @@ __global__ __launch_bounds__(kThreads) void router_adapter_kernel(RouterArgs a) 
     }
   }
   if (tid == 0) __hip_atomic_store(a.counter, 0u, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
+  signal_done(a, tid);
 }
 
 // ---------------------------------------------------------------------------
@@ -548,16 +559,22 @@ __global__ __launch_bounds__(kThreads) void router_select_kernel(RouterArgs a) {
   bst.store(a, tid, s_B);
   __syncthreads();
   if (a.router_on) select_token(a, s_row, b, tid, s_zsel, s_isel);
-  if (!na) return;
-  float pi[kEQ];
-  adapter_token<T>(a, s_row + n, staged, s_B, tid, lane, wave, s_red, pi);
-  // this token's distribution replaces its logits in zbuf (only this workgroup touches row b)
+  if (!na && !a.done_host) return;
+  if (na) {
+    float pi[kEQ];
+    adapter_token<T>(a, s_row + n, staged, s_B, tid, lane, wave, s_red, pi);
+    // this token's distribution replaces its logits in zbuf (only this workgroup touches row b)
 #pragma unroll
-  for (int q = 0; q < kEQ; ++q) {
-    const int e = tid + kThreads * q;
-    if (e < n) st_agent(zrow + e, pi[q]);
+    for (int q = 0; q < kEQ; ++q) {
+      const int e = tid + kThreads * q;
+      if (e < n) st_agent(zrow + e, pi[q]);
+    }
   }
-  __builtin_amdgcn_fence(__ATOMIC_RELEASE, "agent");
+  // release this token's results; system scope when the host reads the mirrors
+  if (a.done_host)
+    __builtin_amdgcn_fence(__ATOMIC_RELEASE, "");
+  else
+    __builtin_amdgcn_fence(__ATOMIC_RELEASE, "agent");
   __syncthreads();
   if (tid == 0) {
     const unsigned prev = __hip_atomic_fetch_add(a.counter, 1u, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
@@ -566,13 +583,16 @@ __global__ __launch_bounds__(kThreads) void router_select_kernel(RouterArgs a) {
   __syncthreads();
   if (!s_last) return;
   __builtin_amdgcn_fence(__ATOMIC_ACQUIRE, "agent");
-  for (int e = tid; e < n; e += kThreads) {
-    float acc = 0.f;
-    for (int bb = 0; bb < a.B; ++bb) acc += ld_agent(a.zbuf + static_cast<size_t>(bb) * ldz + e);
-    a.s[e] = acc;
-    if (a.s_host) a.s_host[e] = acc;
+  if (na) {
+    for (int e = tid; e < n; e += kThreads) {
+      float acc = 0.f;
+      for (int bb = 0; bb < a.B; ++bb) acc += ld_agent(a.zbuf + static_cast<size_t>(bb) * ldz + e);
+      a.s[e] = acc;
+      if (a.s_host) a.s_host[e] = acc;
+    }
   }
   if (tid == 0) __hip_atomic_store(a.counter, 0u, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
+  signal_done(a, tid);
 }
 
 // ---------------------------------------------------------------------------
@@ -1014,6 +1034,61 @@ __global__ __launch_bounds__(kThreads) void proj_kernel(ProjArgs a) {
   }
 }
 
+// Stand-in projection for a batch (bf16, B > 1): one wave per 16 output rows
+// x 16 tokens on MFMA.  h and P are bf16, so their products are exact on the
+// bf16 MFMA; the normalisation moves to the epilogue,
+//   u[b][o] = h[b][o] + (sum_i P[o][i] h[b][i]) / sqrt(mean_i h[b][i]^2 + eps),
+// with sum_i h[b][i]^2 accumulated from the same loads.  Token rows past B
+// read the last token and are not stored.
+__global__ __launch_bounds__(64) void proj_mfma_kernel(ProjArgs a) {
+  const int lane = threadIdx.x;
+  const int o0 = blockIdx.x * 16, b0 = blockIdx.y * 16;
+  const int D = a.D;
+  const int krow = lane & 15, koff = 8 * (lane >> 4);
+  const int tok = min(b0 + krow, a.B - 1);
+  const uint16_t* hrow = reinterpret_cast<const uint16_t*>(a.h) + static_cast<size_t>(tok) * D + koff;
+  const uint16_t* prow = reinterpret_cast<const uint16_t*>(a.P) + static_cast<size_t>(o0 + krow) * D + koff;
+  f32x4 acc = f32x4{0.f, 0.f, 0.f, 0.f};
+  float ss = 0.f;
+  for (int k0 = 0; k0 < D; k0 += 256) {
+    u32x4 ha[8], pb[8];
+#pragma unroll
+    for (int j = 0; j < 8; ++j) {
+      ha[j] = *SPP_GLOBAL(u32x4, hrow + k0 + 32 * j);
+      pb[j] = __builtin_nontemporal_load(SPP_GLOBAL(u32x4, prow + k0 + 32 * j));
+    }
+    __builtin_amdgcn_sched_barrier(0);
+#pragma unroll
+    for (int j = 0; j < 8; ++j) {
+      acc = __builtin_amdgcn_mfma_f32_16x16x32_bf16(__builtin_bit_cast(bf16x8, ha[j]),
+                                                    __builtin_bit_cast(bf16x8, pb[j]), acc, 0, 0, 0);
+      const uint32_t w[4] = {ha[j].x, ha[j].y, ha[j].z, ha[j].w};
+#pragma unroll
+      for (int q = 0; q < 4; ++q) {
+        const float lo = __uint_as_float(w[q] << 16), hi = __uint_as_float(w[q] & 0xffff0000u);
+        ss += lo * lo + hi * hi;
+      }
+    }
+  }
+  // lanes l, l+16, l+32, l+48 hold the k-slices of token b0 + l%16
+  ss += __shfl_xor(ss, 16);
+  ss += __shfl_xor(ss, 32);
+  // this lane holds tokens 4*(lane/16)+j of output row o0 + lane%16
+#pragma unroll
+  for (int j = 0; j < 4; ++j) {
+    const int t = 4 * (lane >> 4) + j;
+    const float sst = __shfl(ss, t);
+    const int b = b0 + t;
+    if (b < a.B) {
+      const int o = o0 + krow;
+      const float inv = 1.0f / sqrtf(sst / static_cast<float>(D) + a.eps);
+      const size_t idx = static_cast<size_t>(b) * D + o;
+      a.u[idx] = __uint_as_float(static_cast<uint32_t>(reinterpret_cast<const uint16_t*>(a.h)[idx]) << 16) +
+                 inv * acc[j];
+    }
+  }
+}
+
 // Bounded busy wait used only by the copy-delay test hook: returns after
 // `ticks` of the constant-rate wall clock or after `max_iter` sleeps, whichever
 // comes first.
@@ -1115,6 +1190,10 @@ hipError_t launch_combine(const CombineArgs& a, int dtype, hipStream_t st) {
 }
 
 hipError_t launch_proj(const ProjArgs& a, int dtype, hipStream_t st) {
+  if (dtype == 1 && a.B > 1 && a.D % 256 == 0) {
+    hipLaunchKernelGGL(proj_mfma_kernel, dim3(a.D / 16, (a.B + 15) / 16), dim3(64), 0, st, a);
+    return hipGetLastError();
+  }
   return dtype == 1 ? proj_t<uint16_t>(a, st) : proj_t<float>(a, st);
 }
 

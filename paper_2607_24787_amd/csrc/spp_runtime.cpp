@@ -4,6 +4,8 @@
 #include <hip/hip_runtime_api.h>
 
 #include <algorithm>
+#include <chrono>
+#include <immintrin.h>
 #include <cmath>
 #include <cstring>
 #include <memory>
@@ -80,7 +82,8 @@ struct spp_ctx {
   uint8_t* res_dev = nullptr;  // topk [maxB*K] i32 | gates [maxB*K] f32 | s [n] f32
   uint8_t* res_host = nullptr; // pinned, host-mapped mirror written by the router kernel
   uint8_t* res_host_dev = nullptr;  // device-visible address of res_host
-  size_t res_bytes = 0, off_gates = 0, off_s = 0;
+  size_t res_bytes = 0, off_gates = 0, off_s = 0, off_flag = 0;
+  uint32_t router_seq = 0;  // last sequence number handed to a router launch
   unsigned* counter = nullptr;
   float* partial = nullptr;    // [ffn_max_grid, D]
   uint8_t* probe_dev = nullptr;  // one blob, for copy profiling
@@ -91,7 +94,6 @@ struct spp_ctx {
   spp::GroupDesc* groups_host = nullptr;  // pinned staging for the per-layer group list
   float* ypart = nullptr;
   std::vector<hipEvent_t> round_done;  // per on-demand round: its FFN launch finished
-  hipEvent_t ev_res = nullptr;
   int64_t clock = 0;
   int ffn_wgs = 256;
   // test hooks
@@ -269,7 +271,6 @@ void free_ctx(spp_ctx* c) {
   if (c->groups_host) (void)hipHostFree(c->groups_host);
   if (c->groups_dev) (void)hipFree(c->groups_dev);
   if (c->ypart) (void)hipFree(c->ypart);
-  if (c->ev_res) (void)hipEventDestroy(c->ev_res);
   if (c->copy) (void)hipStreamDestroy(c->copy);
   delete c;
 }
@@ -309,7 +310,8 @@ spp_status create_impl(const spp_model_desc* desc, void* stream, spp_ctx** out) 
   const size_t bk = static_cast<size_t>(d.max_batch) * d.K;
   c->off_gates = round_up(bk * sizeof(int32_t), 64);
   c->off_s = c->off_gates + round_up(bk * sizeof(float), 64);
-  c->res_bytes = c->off_s + round_up(static_cast<size_t>(d.n) * sizeof(float), 64);
+  c->off_flag = c->off_s + round_up(static_cast<size_t>(d.n) * sizeof(float), 64);
+  c->res_bytes = c->off_flag + 64;
   if (hipMalloc(&c->res_dev, c->res_bytes) != hipSuccess) return fail(SPP_ENOMEM, "result buffer allocation failed");
   if (hipHostMalloc(&c->res_host, c->res_bytes, hipHostMallocMapped | hipHostMallocCoherent) != hipSuccess)
     return fail(SPP_ENOMEM, "pinned result buffer allocation failed");
@@ -328,11 +330,33 @@ spp_status create_impl(const spp_model_desc* desc, void* stream, spp_ctx** out) 
   }
   SPP_HIP(hipMemset(c->counter, 0, 256));
   SPP_HIP(hipMemset(c->res_dev, 0, c->res_bytes));
-  SPP_HIP(hipEventCreateWithFlags(&c->ev_res, hipEventDisableTiming));
   c->last_s.assign(d.n, 0.f);
   SPP_HIP(hipDeviceSynchronize());
   *out = c.release();
   return SPP_OK;
+}
+
+// Hand the next sequence number to a router launch (never 0, the initial flag).
+uint32_t next_router_seq(spp_ctx* c) {
+  if (++c->router_seq == 0) c->router_seq = 1;
+  return c->router_seq;
+}
+
+// Wait until the router launch tagged `seq` has written its host mirrors: spin
+// on the host-mapped flag its last workgroup stores after a system-scope
+// release.  After about 20 ms of spinning (queued work ahead of the router)
+// the wait blocks on the stream instead; a flag still not set then is an error.
+spp_status wait_router(spp_ctx* c, uint32_t seq) {
+  const uint32_t* flag = reinterpret_cast<const uint32_t*>(c->res_host + c->off_flag);
+  const auto t0 = std::chrono::steady_clock::now();
+  for (uint32_t it = 1;; ++it) {
+    if (__atomic_load_n(flag, __ATOMIC_ACQUIRE) == seq) return SPP_OK;
+    if ((it & 1023u) == 0 && std::chrono::steady_clock::now() - t0 > std::chrono::milliseconds(20)) break;
+    _mm_pause();
+  }
+  SPP_HIP(hipStreamSynchronize(c->compute));
+  if (__atomic_load_n(flag, __ATOMIC_ACQUIRE) == seq) return SPP_OK;
+  return fail(SPP_EHIP, "router results were not signalled by the router launch");
 }
 
 // RAW: the compute stream waits for the copies into the slots a round reads.
@@ -525,10 +549,11 @@ spp_status layer_forward_impl(spp_ctx* c, int32_t l, const void* h_in, void* h_o
   ra.eps = d.rms_eps;
   ra.x_given = 0;
   ra.router_on = 1;
+  ra.done_host = reinterpret_cast<unsigned*>(c->res_host_dev + c->off_flag);
+  ra.seq = next_router_seq(c);
   SPP_HIP(spp::launch_router(ra, dt, c->compute));
   if (c->timing) SPP_HIP(hipEventRecord(ts.ev[kEvRouted], c->compute));
-  SPP_HIP(hipEventRecord(c->ev_res, c->compute));
-  SPP_HIP(hipEventSynchronize(c->ev_res));
+  if (spp_status e = wait_router(c, ra.seq)) return e;
   if (c->timing && c->pending_sets.size() >= 64) harvest(c, c->pending_sets.size());
 
   const int32_t* T = reinterpret_cast<const int32_t*>(c->res_host);
@@ -798,9 +823,10 @@ spp_status adapter_predict(spp_ctx* c, int32_t l, const float* x_dev, int32_t B,
   ra.eps = d.rms_eps;
   ra.x_given = 1;
   ra.router_on = 0;
+  ra.done_host = reinterpret_cast<unsigned*>(c->res_host_dev + c->off_flag);
+  ra.seq = next_router_seq(c);
   SPP_HIP(spp::launch_router(ra, d.dtype, c->compute));
-  SPP_HIP(hipEventRecord(c->ev_res, c->compute));
-  SPP_HIP(hipEventSynchronize(c->ev_res));
+  if (spp_status e = wait_router(c, ra.seq)) return e;
   std::memcpy(s_out, c->res_host + c->off_s, sizeof(float) * d.n);
   return SPP_OK;
 }
