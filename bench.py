@@ -209,10 +209,13 @@ def main():
     distinct = on["distinct_experts_per_layer"] if cfg.batch > 1 else cfg.K
     ffn_bytes = int(round((distinct + cfg.n_shared) * cfg.blob_bytes))
     achieved = ffn_bytes / (on["ffn_kernel_us"] * 1e3)                   # GB/s
-    traffic = None
-    if cfg.name == "qwen3vl30b_a3b_layer_bf16":
-        traffic = measured_traffic(os.path.join(ROOT, "profiles", f"ffn_units_kernel__{cfg.name}.md"),
-                                   os.path.join(ROOT, "paper_2607_24787_amd", "csrc", "spp_kernels.hip"))
+    # the FFN kernel this context runs: grouped MFMA over the tiled layout, or the unit-stream kernel
+    tiled = spp.spp_blob_layout(stack.desc) == spp.LAYOUT_TILED
+    kernel = "ffn_grouped_kernel" if tiled else "ffn_units_kernel"
+    workload = cfg.name + ("" if not over else "+" + ",".join(f"{k}={v}" for k, v in over.items()))
+    slug = workload.replace("+", "__").replace("=", "").replace(",", "_")
+    traffic = measured_traffic(os.path.join(ROOT, "profiles", f"{kernel}__{slug}.md"),
+                               os.path.join(ROOT, "paper_2607_24787_amd", "csrc", "spp_kernels.hip"))
     line = {
         "metric": METRIC,
         "value": on["tokens_per_s"],
@@ -226,14 +229,14 @@ def main():
         "vs_baseline": None,
         "dtype": cfg.dtype,
         "data": "synthetic (seeded AR(1) hidden states, N(0,0.02) weights, SVD-built adapters)",
-        "config": {"workload": cfg.name + ("" if not over else "+" + ",".join(f"{k}={v}" for k, v in over.items())),
+        "config": {"workload": workload,
                    "layers": cfg.L, "hidden": cfg.D, "experts": cfg.n, "top_k": cfg.K,
                    "intermediate": cfg.I, "adapter_rank": cfg.r, "hbm_slots_per_layer": cfg.S,
                    "window_experts": cfg.window, "batch": cfg.batch, "shared_experts": cfg.n_shared,
                    "offload_tier": "pinned host DRAM", "expert_bytes": cfg.blob_bytes},
         "next_layer_coverage": on["next_layer_coverage"],
         "exposed_transfer_pct": on["exposed_transfer_pct"],
-        "roofline": {"kernel": "ffn_units_kernel (routed-expert SwiGLU FFN)", "bound": "hbm",
+        "roofline": {"kernel": kernel + " (routed-expert SwiGLU FFN)", "bound": "hbm",
                      "achieved": achieved, "peak": HBM_PEAK_GBS, "unit": "GB/s", "frac": achieved / HBM_PEAK_GBS,
                      "traffic": traffic, "bytes_per_launch": ffn_bytes, "avg_launch_us": on["ffn_kernel_us"]},
         "link": {"bound": "host link (pinned H2D)", "per_expert_us": per_expert_us, "peak_gbs_measured": link_gbs,
