@@ -50,12 +50,14 @@ def _ffn_stats(rs):
     return rs.ffn_us / n
 
 
-def run_mode(stack, dev_h, row_bytes, warmup, steps, M_max):
+def run_mode(stack, dev_h, row_bytes, warmup, steps, M_max, naive=False):
+    """One timed run; naive: Naive Prefetch (the preceding step's experts) instead of the adapter."""
     import torch
     from paper_2607_24787_amd import spp
 
     cfg = stack.cfg
     base = dev_h.data_ptr()
+    spp.spp_set_prefetch_source(stack.ctx, spp.PREFETCH_PREV_TOKEN if naive else spp.PREFETCH_ADAPTER)
     stack.reset()
     spp.spp_set_timing(stack.ctx, 0)
     for t in range(warmup):
@@ -78,9 +80,11 @@ def run_mode(stack, dev_h, row_bytes, warmup, steps, M_max):
     wall = time.perf_counter() - t0
     rs = spp.spp_get_run_stats(stack.ctx)
     spp.spp_set_timing(stack.ctx, 0)
+    spp.spp_set_prefetch_source(stack.ctx, spp.PREFETCH_ADAPTER)
     demand = cfg.K * cfg.batch * steps
     return {
         "M_max": M_max,
+        "policy": "naive" if naive else ("off" if M_max < 0 else "adapter"),
         "tokens_per_s": cfg.batch * steps / wall,
         "ms_per_step": 1e3 * wall / steps,
         "wall_s": wall,
@@ -141,11 +145,15 @@ def main():
     ap.add_argument("--warmup", type=int, default=16)
     ap.add_argument("--workload", default="c1", help="configuration key in workload.configs")
     ap.add_argument("--cpu-tokens", type=int, default=96, help="oracle sample size (0 disables)")
-    ap.add_argument("--ablation", type=int, default=1, help="also time OFF and PRED0 modes")
+    ap.add_argument("--ablation", type=int, default=1, help="also time OFF, PRED0 and Naive Prefetch modes")
     ap.add_argument("--ffn-wgs", type=int, default=0, help="FFN workgroups (0: library default)")
     ap.add_argument("--batch", type=int, default=0, help="override the workload's batch (0: keep)")
     ap.add_argument("--slots", type=int, default=0, help="override HBM slots per layer (0: keep)")
     ap.add_argument("--layers", type=int, default=0, help="override the layer count (0: keep)")
+    ap.add_argument("--tie-layers", type=int, default=0,
+                    help="offload tier of k distinct expert layers shared round-robin (0: one per layer)")
+    ap.add_argument("--sweep", type=lambda v: [int(x) for x in v.split(",") if x != ""], default=[],
+                    help="extra modes at these M_max values, e.g. 0,1,2,4,8,16")
     ap.add_argument("--copy-probe", action="store_true",
                     help="only run a 256 MiB device-to-device copy three times (counter calibration)")
     args = ap.parse_args()
@@ -174,7 +182,8 @@ def main():
     from workload import gen
 
     cfg = workload.get(args.workload)
-    over = {k: v for k, v in (("batch", args.batch), ("S", args.slots), ("L", args.layers)) if v > 0}
+    over = {k: v for k, v in (("batch", args.batch), ("S", args.slots), ("L", args.layers),
+                              ("expert_layers", args.tie_layers)) if v > 0}
     if over:
         cfg = cfg.with_(**over)
     total = args.warmup + args.steps
@@ -197,10 +206,15 @@ def main():
          f"exposed={on['exposed_transfer_pct']:.1f}% ffn={on['ffn_kernel_us']:.2f}us")
     modes = {"on": on}
     if args.ablation:
-        for name, M in (("pred0", 0), ("off", -1)):
-            modes[name] = run_mode(stack, dev_h, row_bytes, args.warmup, args.steps, M)
+        for name, M, naive in (("pred0", 0, False), ("off", -1, False), ("naive", cfg.window, True)):
+            modes[name] = run_mode(stack, dev_h, row_bytes, args.warmup, args.steps, M, naive)
             _log(f"[bench] {name} {modes[name]['tokens_per_s']:.1f} tok/s "
                  f"coverage={modes[name]['next_layer_coverage']:.3f}")
+    for M in args.sweep:
+        modes[f"M{M}"] = run_mode(stack, dev_h, row_bytes, args.warmup, args.steps, M)
+        _log(f"[bench] sweep M_max={M} {modes[f'M{M}']['tokens_per_s']:.1f} tok/s "
+             f"coverage={modes[f'M{M}']['next_layer_coverage']:.3f} "
+             f"exposed={modes[f'M{M}']['exposed_transfer_pct']:.1f}%")
 
     window_us = on["compute_window_us"]
     implied_budget = (spp.select_prefetch_budget(window_us, per_expert_us, cfg.n)

@@ -65,6 +65,7 @@ typedef enum {
 
 enum { SPP_DTYPE_F32 = 0, SPP_DTYPE_BF16 = 1 };
 enum { SPP_LAYOUT_UNITS = 0, SPP_LAYOUT_TILED = 1 };
+enum { SPP_PREFETCH_ADAPTER = 0, SPP_PREFETCH_PREV_TOKEN = 1 };
 
 /* Model shape.  Notation of the paper's problem formulation: L MoE layers,
  * n routed experts per layer, top-K routing, router input size D, adapter
@@ -156,7 +157,8 @@ spp_status select_prefetch_budget(double window_us, double per_expert_cost_us, i
                                   int32_t* M_max_out);
 
 /* Same section: P^{l+1} = Top_{M_max}{ s_e : e neither available nor in
- * flight in target_layer }, lowest expert index first on equal priority,
+ * flight in target_layer }, lowest expert index first on equal priority
+ * (an expert with priority -inf is never a candidate),
  * issued as asynchronous host-to-device copies in descending priority, each
  * into a replacement slot (lowest EMPTY slot, else the least recently stamped
  * slot not filled in this step; stops early when none is left).  s_host: host
@@ -180,7 +182,9 @@ spp_status expert_cache_issue_prefetch(spp_ctx* ctx, int32_t target_layer, const
  *   exists (third victim class: the lowest-index slot whose expert already
  *   ran this step), run every resident needed expert not yet run, repeat;
  *   if M_max > 0: the expert_cache_issue_prefetch selection for layer l+1
- *   with this s, in the same step;
+ *   with this s, in the same step (with SPP_PREFETCH_PREV_TOKEN, see
+ *   spp_set_prefetch_source, s comes from the preceding step instead and no
+ *   adapter runs);
  *   FFN: h_out_b = round(u_b + sum_k g_bk W_down(silu(W_gate x_b) * (W_up x_b))
  *   [+ shared experts, weight 1]), reading each expert from its HBM slot
  *   after its copy completed.
@@ -230,6 +234,15 @@ spp_status spp_reset_run_stats(spp_ctx* ctx);
 /* Measured host-to-device cost of one expert blob on the copy stream
  * (average over reps copies from layer l's host store into scratch), in us. */
 spp_status spp_profile_expert_copy(spp_ctx* ctx, int32_t l, int32_t reps, double* per_expert_us);
+
+/* Where moe_layer_forward takes the priorities for the next layer's prefetch
+ * (Table 5).  SPP_PREFETCH_ADAPTER (default): the layer's adapter, as above.
+ * SPP_PREFETCH_PREV_TOKEN (Naive Prefetch): the experts layer l+1 activated
+ * at its preceding call, each scored by its gate mass summed over that
+ * call's tokens (fp64 in token order, then fp32), every other expert -inf;
+ * no adapter runs.  spp_set_resident starts a new sequence (no preceding
+ * call: nothing is prefetched).  EINVAL for an unknown source. */
+spp_status spp_set_prefetch_source(spp_ctx* ctx, int32_t source);
 
 /* Launch shape of the routed-expert FFN: about `wgs` workgroups share the
  * (expert, unit) work list of one token (default 512; 1..4096).  Applies to

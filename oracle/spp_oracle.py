@@ -192,13 +192,31 @@ def prefetch_budget(window_us: float, per_expert_cost_us: float, n: int) -> int:
 
 
 def select_prefetch(s: np.ndarray, occupied: Sequence[bool], M_max: int) -> List[int]:
-    """P = Top_{M_max}{ s_e : e not available and not in flight }, descending priority."""
-    eligible = [e for e in range(len(s)) if not occupied[e]]
+    """P = Top_{M_max}{ s_e : e not available and not in flight }, descending priority.
+
+    An expert whose priority is -inf is not a candidate (the adapter's
+    priorities are sums of probabilities and never are; the Naive Prefetch
+    scores mark the experts the preceding token did not use that way)."""
+    eligible = [e for e in range(len(s)) if not occupied[e] and not (np.isinf(s[e]) and s[e] < 0)]
     if M_max <= 0 or not eligible:
         return []
     vals = np.asarray([s[e] for e in eligible])
     picked = top_k(vals, min(M_max, len(eligible)))
     return [eligible[int(i)] for i in picked]
+
+
+def naive_scores(prev_T: Optional[np.ndarray], prev_g: Optional[np.ndarray], n: int) -> np.ndarray:
+    """Naive Prefetch priorities for a target layer (Table 5): the experts the
+    preceding decode step activated there, ranked by their gate mass summed
+    over the batch (fp64 in token order, then fp32); -inf for every other
+    expert, so only those experts are candidates."""
+    acc = np.full(n, -np.inf)
+    if prev_T is not None:
+        for b in range(prev_T.shape[0]):
+            for k in range(prev_T.shape[1]):
+                e = int(prev_T[b, k])
+                acc[e] = (0.0 if np.isinf(acc[e]) else acc[e]) + float(prev_g[b, k])
+    return acc.astype(np.float32)
 
 
 # --------------------------------------------------------------------------
@@ -466,11 +484,14 @@ class DecodeResult:
 
 def run_decode(cfg, W: OracleWeights, h0: np.ndarray, M_max: int, S: Optional[int] = None,
                resident: Optional[Sequence[int]] = None, tokens: Optional[int] = None,
-               keep_x: bool = False) -> DecodeResult:
+               keep_x: bool = False, policy: str = "adapter") -> DecodeResult:
     """Decode ``tokens`` steps through all L layers.
 
     M_max < 0: no prediction at all (OFF); M_max == 0: prediction without
     transfers (PRED0); M_max > 0: prediction and budgeted prefetch.
+    policy "adapter": priorities from the layer's adapter (SpecPrefetch);
+    "naive": the preceding step's experts of the target layer (Naive
+    Prefetch, Table 5; no adapter runs and no ExpertRecall is scored).
     ``h0`` holds the stored layer-0 hidden states [tokens, B, D].
     Decode step t, layer l has stamp tau = t L + l + 1.
     """
@@ -491,6 +512,7 @@ def run_decode(cfg, W: OracleWeights, h0: np.ndarray, M_max: int, S: Optional[in
     n_loads = n_pref = n_used = 0
     demand_events = {m: 0 for m in Ms}
     n_events = 0
+    prev_route: List[Optional[tuple]] = [None] * L   # (T, g) of each layer at its last step
     for t in range(nT):
         h = decode(h0[t], cfg.dtype)
         for l in range(L):
@@ -523,16 +545,21 @@ def run_decode(cfg, W: OracleWeights, h0: np.ndarray, M_max: int, S: Optional[in
                              stamps_after_demand=cache.stamp.copy(), recall=recall)
             predicted[l] = None
             if l < L - 1 and M_max >= 0:
-                A, Bm = W.adapter(l)
-                zhat, _, s = adapter_scores(A, Bm, x)
-                step.s, step.zhat = s, zhat
-                predicted[l + 1] = {m: candidate_set(s, m) for m in Ms}
                 nxt = caches[l + 1]
                 occ_next = nxt.occupied()
-                step.demand = {m: int(sum(1 for e in predicted[l + 1][m] if not occ_next[e])) for m in Ms}
-                for m in Ms:
-                    demand_events[m] += int(step.demand[m] > max(M_max, 0))
-                n_events += 1
+                if policy == "naive":
+                    prev = prev_route[l + 1]
+                    s = naive_scores(prev[0] if prev else None, prev[1] if prev else None, n)
+                    step.s = s
+                else:
+                    A, Bm = W.adapter(l)
+                    zhat, _, s = adapter_scores(A, Bm, x)
+                    step.s, step.zhat = s, zhat
+                    predicted[l + 1] = {m: candidate_set(s, m) for m in Ms}
+                    step.demand = {m: int(sum(1 for e in predicted[l + 1][m] if not occ_next[e])) for m in Ms}
+                    for m in Ms:
+                        demand_events[m] += int(step.demand[m] > max(M_max, 0))
+                    n_events += 1
                 if M_max > 0:
                     P = select_prefetch(s, occ_next, M_max)
                     step.P = nxt.prefetch(P, tau)
@@ -543,6 +570,7 @@ def run_decode(cfg, W: OracleWeights, h0: np.ndarray, M_max: int, S: Optional[in
             hout = moe_output(cfg, W, l, cache, u, x, T, g)
             step.h_out = encode(hout, cfg.dtype)
             h = decode(step.h_out, cfg.dtype)
+            prev_route[l] = (T, g)
             steps.append(step)
         outputs.append(step.h_out)
     return DecodeResult(
@@ -556,11 +584,13 @@ def run_decode(cfg, W: OracleWeights, h0: np.ndarray, M_max: int, S: Optional[in
 
 
 def layer_step(cfg, W: OracleWeights, l: int, h_stored: np.ndarray, cache: SlotCache,
-               next_cache: Optional[SlotCache], tau: int, M_max: int):
+               next_cache: Optional[SlotCache], tau: int, M_max: int, policy: str = "adapter",
+               next_prev: Optional[tuple] = None):
     """One layer in isolation from given state (the lock-step parity unit).
 
     Mutates ``cache`` / ``next_cache`` exactly as the decode loop does and
-    returns the LayerStep record (x kept).
+    returns the LayerStep record (x kept).  ``next_prev``: (T, g) of layer
+    l+1 at the preceding step, for the "naive" policy.
     """
     K = cfg.K
     u, x = layer_prologue(cfg, W, l, decode(h_stored, cfg.dtype))
@@ -572,9 +602,13 @@ def layer_step(cfg, W: OracleWeights, l: int, h_stored: np.ndarray, cache: SlotC
     step = LayerStep(t=-1, l=l, tau=tau, x=x, z=z, T=T, g=g, ready=ready, loads=loads,
                      table_after_demand=cache.expert.copy(), stamps_after_demand=cache.stamp.copy())
     if l < cfg.L - 1 and M_max >= 0:
-        A, Bm = W.adapter(l)
-        zhat, _, s = adapter_scores(A, Bm, x)
-        step.s, step.zhat = s, zhat
+        if policy == "naive":
+            s = naive_scores(next_prev[0] if next_prev else None, next_prev[1] if next_prev else None, cfg.n)
+            step.s = s
+        else:
+            A, Bm = W.adapter(l)
+            zhat, _, s = adapter_scores(A, Bm, x)
+            step.s, step.zhat = s, zhat
         if M_max > 0 and next_cache is not None:
             P = select_prefetch(s, next_cache.occupied(), M_max)
             step.P = next_cache.prefetch(P, tau)

@@ -128,7 +128,7 @@ void SlotPolicy::prefetch(const float* s, int32_t M_max, int64_t tau, std::vecto
   std::vector<int32_t> elig;
   elig.reserve(n_);
   for (int32_t e = 0; e < n_; ++e)
-    if (!available(e)) elig.push_back(e);
+    if (!available(e) && !(std::isinf(s[e]) && s[e] < 0.f)) elig.push_back(e);
   // priority order: larger s first, lower index on equal s; NaN ranks last
   auto key_less = [s](int32_t a, int32_t b) {
     const float sa = s[a], sb = s[b];

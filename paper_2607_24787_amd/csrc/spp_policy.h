@@ -52,7 +52,8 @@ class SlotPolicy {
   // Distinct experts among needed[0..count).
   int32_t distinct(const int32_t* needed, int32_t count) const;
 
-  // P = the first M_max experts, not available, in order (s desc, index asc);
+  // P = the first M_max experts, not available and with s > -inf, in order
+  // (s desc, index asc);
   // each placed in turn into the lowest EMPTY slot, else the smallest
   // (stamp, slot index) among slots stamped before tau; stops when no slot is
   // left.  Placed slots take stamp tau.

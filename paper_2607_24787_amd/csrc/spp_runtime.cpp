@@ -62,6 +62,8 @@ struct LayerState {
   hipEvent_t last_read = nullptr;      // recorded on the compute stream after the layer's FFN
   bool last_read_valid = false;
   std::vector<int32_t> pending_prefetch;  // prefetched for this layer, not yet executed
+  std::vector<int32_t> prev_T;            // routing of this layer at its last call [B*K]
+  std::vector<float> prev_g;              // and its gates
 };
 
 size_t round_up(size_t v, size_t a) { return (v + a - 1) / a * a; }
@@ -84,6 +86,7 @@ struct spp_ctx {
   uint8_t* res_host_dev = nullptr;  // device-visible address of res_host
   size_t res_bytes = 0, off_gates = 0, off_s = 0, off_flag = 0;
   uint32_t router_seq = 0;  // last sequence number handed to a router launch
+  int32_t prefetch_source = SPP_PREFETCH_ADAPTER;
   unsigned* counter = nullptr;
   float* partial = nullptr;    // [ffn_max_grid, D]
   uint8_t* probe_dev = nullptr;  // one blob, for copy profiling
@@ -506,7 +509,11 @@ spp_status layer_forward_impl(spp_ctx* c, int32_t l, const void* h_in, void* h_o
   if (B < 1 || B > d.max_batch) return fail(SPP_EINVAL, "B must be in [1, max_batch]");
   if (M_max < -1) return fail(SPP_EINVAL, "M_max must be >= -1");
   LayerState& ls = c->layers[l];
-  const bool predict = l < d.L - 1 && M_max >= 0 && ls.A != nullptr && d.r > 0;
+  // a prediction for layer l+1: the adapter's priorities, or (Naive Prefetch)
+  // the preceding step's experts of layer l+1; the adapter runs only for the first
+  const bool naive = c->prefetch_source == SPP_PREFETCH_PREV_TOKEN;
+  const bool adapter_on = l < d.L - 1 && M_max >= 0 && !naive && ls.A != nullptr && d.r > 0;
+  const bool predict = adapter_on || (naive && l < d.L - 1 && M_max >= 0);
   if (predict && M_max > 0 && !c->layers[l + 1].bound) return fail(SPP_ESTATE, "next layer not bound");
   const int64_t tau = ++c->clock;
   const int dt = d.dtype;
@@ -530,7 +537,7 @@ spp_status layer_forward_impl(spp_ctx* c, int32_t l, const void* h_in, void* h_o
   ra.h = h_in;
   ra.u = d.has_proj ? c->u_dev : nullptr;
   ra.Wr = ls.router_w;
-  ra.A = predict ? ls.A : nullptr;
+  ra.A = adapter_on ? ls.A : nullptr;
   ra.Bm = ls.Bm;
   ra.x_out = c->x_dev;
   ra.zbuf = c->zbuf;
@@ -539,7 +546,7 @@ spp_status layer_forward_impl(spp_ctx* c, int32_t l, const void* h_in, void* h_o
   ra.s = s_dev;
   ra.topk_host = reinterpret_cast<int32_t*>(c->res_host_dev);
   ra.gates_host = reinterpret_cast<float*>(c->res_host_dev + c->off_gates);
-  ra.s_host = predict ? reinterpret_cast<float*>(c->res_host_dev + c->off_s) : nullptr;
+  ra.s_host = adapter_on ? reinterpret_cast<float*>(c->res_host_dev + c->off_s) : nullptr;
   ra.counter = c->counter;
   ra.B = B;
   ra.D = d.D;
@@ -560,6 +567,20 @@ spp_status layer_forward_impl(spp_ctx* c, int32_t l, const void* h_in, void* h_o
   const float* g = reinterpret_cast<const float*>(c->res_host + c->off_gates);
   const float* s = reinterpret_cast<const float*>(c->res_host + c->off_s);
   const int32_t BK = B * d.K;
+  std::vector<float> s_naive;
+  if (naive && predict) {
+    // gate mass of each expert of layer l+1 at its preceding step (fp64 in
+    // token order, then fp32); -inf marks the experts it did not use
+    const LayerState& nl = c->layers[l + 1];
+    std::vector<double> acc(d.n, -INFINITY);
+    for (size_t i = 0; i < nl.prev_T.size(); ++i) {
+      double& a = acc[nl.prev_T[i]];
+      a = (std::isinf(a) ? 0.0 : a) + static_cast<double>(nl.prev_g[i]);
+    }
+    s_naive.resize(d.n);
+    for (int32_t e = 0; e < d.n; ++e) s_naive[e] = static_cast<float>(acc[e]);
+    s = s_naive.data();
+  }
 
   spp_layer_stats st{};
   {
@@ -656,6 +677,8 @@ spp_status layer_forward_impl(spp_ctx* c, int32_t l, const void* h_in, void* h_o
 
   if (topk_out) std::memcpy(topk_out, T, sizeof(int32_t) * BK);
   if (gate_out) std::memcpy(gate_out, g, sizeof(float) * BK);
+  ls.prev_T.assign(T, T + BK);
+  ls.prev_g.assign(g, g + BK);
   c->stats.layer_calls += 1;
   c->stats.hits += st.hits;
   c->stats.misses += st.misses;
@@ -761,7 +784,17 @@ spp_status spp_set_resident(spp_ctx* c, int32_t l, const int32_t* experts, int32
   const std::vector<int32_t> before(c->d.S, spp::kEmpty);
   ls.policy->set_resident(experts, count, &why);
   ls.pending_prefetch.clear();
+  ls.prev_T.clear();  // a new decode sequence: no preceding step
+  ls.prev_g.clear();
   return fill_slots(c, ls, before);
+}
+
+spp_status spp_set_prefetch_source(spp_ctx* c, int32_t source) {
+  if (!c) return fail(SPP_EINVAL, "ctx is NULL");
+  if (source != SPP_PREFETCH_ADAPTER && source != SPP_PREFETCH_PREV_TOKEN)
+    return fail(SPP_EINVAL, "source must be SPP_PREFETCH_ADAPTER or SPP_PREFETCH_PREV_TOKEN");
+  c->prefetch_source = source;
+  return SPP_OK;
 }
 
 spp_status spp_set_slot_table(spp_ctx* c, int32_t l, const int32_t* experts, const int64_t* stamps) {

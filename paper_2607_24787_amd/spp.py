@@ -18,6 +18,7 @@ LIB_PATH = os.path.join(os.path.dirname(os.path.abspath(__file__)), "libspp.so")
 SPP_OK, SPP_EINVAL, SPP_ENOMEM, SPP_EHIP, SPP_ESTATE = 0, -1, -2, -3, -4
 DTYPE_F32, DTYPE_BF16 = 0, 1
 LAYOUT_UNITS, LAYOUT_TILED = 0, 1
+PREFETCH_ADAPTER, PREFETCH_PREV_TOKEN = 0, 1
 
 
 class SppError(RuntimeError):
@@ -74,6 +75,7 @@ _SIGS = {
     "spp_get_run_stats": (c_int32, [c_void_p, POINTER(RunStats)]),
     "spp_reset_run_stats": (c_int32, [c_void_p]),
     "spp_profile_expert_copy": (c_int32, [c_void_p, c_int32, c_int32, POINTER(c_double)]),
+    "spp_set_prefetch_source": (c_int32, [c_void_p, c_int32]),
     "spp_set_ffn_workgroups": (c_int32, [c_void_p, c_int32]),
     "spp_debug_set_poison": (c_int32, [c_void_p, c_int32]),
     "spp_debug_set_copy_delay": (c_int32, [c_void_p, c_int32]),
@@ -284,6 +286,10 @@ def spp_profile_expert_copy(ctx, l, reps) -> float:
     us = c_double()
     _check(lib().spp_profile_expert_copy(c_void_p(ctx), l, reps, byref(us)))
     return us.value
+
+
+def spp_set_prefetch_source(ctx, source: int):
+    _check(lib().spp_set_prefetch_source(c_void_p(ctx), source))
 
 
 def spp_set_ffn_workgroups(ctx, wgs: int):

@@ -31,6 +31,7 @@ class LockstepReport:
     max_err_g: float = 0.0
     max_err_s: float = 0.0
     max_err_x: float = 0.0
+    prefetched: int = 0           # prefetch placements (oracle side) over the run
 
 
 def _spacing(v: np.ndarray, dtype: str) -> np.ndarray:
@@ -48,14 +49,18 @@ def _topk_gap(z_row: np.ndarray, K: int) -> float:
 
 
 def _prefetch_gap(s: np.ndarray, occupied: np.ndarray, M: int) -> float:
-    elig = [e for e in range(len(s)) if not occupied[e]]
+    elig = [e for e in range(len(s)) if not occupied[e] and np.isfinite(s[e])]
     vals = sorted((float(s[e]) for e in elig), reverse=True)[: M + 1]
     if len(vals) < 2:
         return np.inf
     return float(np.min(-np.diff(vals)))
 
 
-def run_lockstep(stack, cfg, tokens: int, M_max: int, check_x: bool = True) -> LockstepReport:
+def run_lockstep(stack, cfg, tokens: int, M_max: int, check_x: bool = True,
+                 policy: str = "adapter") -> LockstepReport:
+    """policy "naive": Naive Prefetch on both sides (the device via
+    spp_set_prefetch_source); the oracle gets each layer's routing of the
+    preceding step."""
     from paper_2607_24787_amd import spp
 
     W = o.OracleWeights(cfg, cache_experts=cfg.host_layers * cfg.n + 8)
@@ -66,6 +71,8 @@ def run_lockstep(stack, cfg, tokens: int, M_max: int, check_x: bool = True) -> L
     caches = [o.SlotCache(S, cfg.n, res) for _ in range(cfg.L)]
     tol = 2e-2 if cfg.dtype == "bf16" else 1e-4
     rep = LockstepReport()
+    spp.spp_set_prefetch_source(stack.ctx, spp.PREFETCH_PREV_TOKEN if policy == "naive" else spp.PREFETCH_ADAPTER)
+    prev = [None] * cfg.L          # (T, g) of each layer at the preceding step (oracle side)
     tau = 0
     for t in range(tokens):
         h = h0[t]
@@ -73,7 +80,10 @@ def run_lockstep(stack, cfg, tokens: int, M_max: int, check_x: bool = True) -> L
             tau += 1
             nxt = caches[l + 1] if l + 1 < cfg.L else None
             occ_next_before = nxt.occupied() if nxt is not None else None
-            ref = o.layer_step(cfg, W, l, h, caches[l], nxt, tau, M_max)
+            ref = o.layer_step(cfg, W, l, h, caches[l], nxt, tau, M_max, policy=policy,
+                               next_prev=prev[l + 1] if l + 1 < cfg.L else None)
+            prev[l] = (ref.T, ref.g)
+            rep.prefetched += len(ref.P)
             stack.upload_hidden(h, 0)
             spp.spp_set_clock(stack.ctx, tau - 1)
             topk, gates, stats = stack.layer(l, 0, 1, M_max)
@@ -97,8 +107,11 @@ def run_lockstep(stack, cfg, tokens: int, M_max: int, check_x: bool = True) -> L
                 assert st.tolist() == ref.stamps_after_demand.tolist(), tag
             if ref.s is not None:
                 s_gpu = spp.spp_get_last_priorities(stack.ctx, cfg.n)
-                rep.max_err_s = max(rep.max_err_s, float(np.max(np.abs(s_gpu - ref.s))))
-                assert np.allclose(s_gpu, ref.s, rtol=1e-5, atol=2e-6), f"{tag}: priorities differ"
+                fin = np.isfinite(ref.s)
+                assert np.array_equal(fin, np.isfinite(s_gpu)), f"{tag}: candidate sets differ"
+                if fin.any():
+                    rep.max_err_s = max(rep.max_err_s, float(np.max(np.abs(s_gpu[fin] - ref.s[fin]))))
+                assert np.allclose(s_gpu[fin], ref.s[fin], rtol=1e-5, atol=2e-6), f"{tag}: priorities differ"
                 if not resync and pref != ref.P:
                     gap = _prefetch_gap(ref.s, occ_next_before, max(M_max, 0))
                     assert gap < GAP_EXEMPT, f"{tag}: prefetch {pref} != {ref.P} (oracle gap {gap:.3g})"

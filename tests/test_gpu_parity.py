@@ -104,6 +104,24 @@ def test_lockstep_parity_batched_grouped(torch_cuda, cfg, M_max, tokens):
     _assert_report(rep, cfg, cfg.name)
 
 
+@pytest.mark.parametrize("cfg,M_max,tokens,must_issue", [(BATCH_BF16_ROUNDS, 3, 6, True),
+                                                         (w.get("c0"), 2, 12, False)],
+                         ids=["batch5_rounds", "c0"])
+def test_lockstep_parity_naive_prefetch(torch_cuda, cfg, M_max, tokens, must_issue):
+    """Naive Prefetch (the preceding step's experts of the next layer, Table 5):
+    candidate sets, prefetch sets and slot tables bit-exact with the oracle."""
+    from lockstep import run_lockstep
+    _log(f"[lockstep naive] {cfg.name} B={cfg.batch} M_max={M_max} tokens={tokens}")
+    st = _stack(cfg)
+    try:
+        rep = run_lockstep(st, cfg, tokens, M_max, policy="naive")
+    finally:
+        st.close()
+    _assert_report(rep, cfg, cfg.name + " naive")
+    if must_issue:
+        assert rep.prefetched > 0, "the case must exercise naive prefetches"
+
+
 @pytest.mark.parametrize("cfg,tokens", [(C3_FULL, 4), (C2_TIED, 2)], ids=["c3_stack12", "c2_stack48_tied"])
 def test_lockstep_parity_full_stacks(torch_cuda, cfg, tokens):
     from lockstep import run_lockstep

@@ -166,3 +166,22 @@ def test_pack_expert_places_every_element_where_the_header_says(case):
     assert spp.lib().spp_pack_expert(ctypes.byref(d), None, None, None, out.ctypes.data) == spp.SPP_EINVAL
     with pytest.raises(ValueError):
         spp.spp_pack_expert(d, G.T, U, Wd)
+
+
+@pytest.mark.parametrize("seed", range(10))
+def test_native_prefetch_skips_minus_inf_like_the_oracle(seed):
+    rng = np.random.default_rng(300 + seed)
+    n = int(rng.integers(4, 30))
+    S = int(rng.integers(1, n + 1))
+    nat, ora = spp.SlotPolicy(S, n, []), o.SlotCache(S, n, [])
+    tau = 0
+    for step in range(30):
+        tau += 1
+        need = list(rng.integers(0, n, size=int(rng.integers(1, S + 1))))
+        assert nat.on_demand(need, tau) == ora.on_demand(need, tau)
+        s = (rng.integers(0, 5, size=n) / 4).astype(np.float32)
+        s[rng.random(n) < 0.6] = -np.inf
+        M = int(rng.integers(0, 6))
+        got = nat.prefetch(s, M, tau)
+        assert got == ora.prefetch(o.select_prefetch(s.astype(np.float64), ora.occupied(), M), tau)
+        assert all(np.isfinite(s[e]) for e, _, _ in got)

@@ -388,3 +388,66 @@ def test_layer_step_matches_decode_loop():
             assert np.array_equal(st.T, ref.T) and np.array_equal(st.h_out, ref.h_out)
             assert st.P == ref.P and st.loads == ref.loads
             h = st.h_out
+
+
+# ------------------------------------------------ Naive Prefetch (Table 5) --
+
+@pytest.mark.parametrize("seed", range(20))
+def test_naive_scores_brute_force(seed):
+    """Gate mass per expert of the preceding step, accumulated independently."""
+    rng = np.random.default_rng(100 + seed)
+    n, B, K = int(rng.integers(4, 12)), int(rng.integers(1, 4)), 3
+    K = min(K, n)
+    T = np.stack([rng.choice(n, size=K, replace=False) for _ in range(B)])
+    g = rng.random((B, K)).astype(np.float32)
+    s = o.naive_scores(T, g, n)
+    mass = {}
+    for b in range(B):
+        for k in range(K):
+            mass[int(T[b, k])] = mass.get(int(T[b, k]), 0.0) + float(g[b, k])
+    for e in range(n):
+        if e in mass:
+            assert s[e] == np.float32(mass[e])
+        else:
+            assert np.isneginf(s[e])
+    assert np.isneginf(o.naive_scores(None, None, n)).all()        # no preceding step: no candidates
+
+
+@pytest.mark.parametrize("seed", range(20))
+def test_select_prefetch_never_picks_minus_inf(seed):
+    rng = np.random.default_rng(200 + seed)
+    n = int(rng.integers(2, 10))
+    s = (rng.integers(0, 4, size=n) / 4).astype(np.float64)
+    s[rng.random(n) < 0.5] = -np.inf
+    occ = rng.random(n) < 0.3
+    for M in range(0, n + 2):
+        P = o.select_prefetch(s, occ, M)
+        cand = [e for e in range(n) if not occ[e] and np.isfinite(s[e])]
+        assert len(P) == min(M, len(cand)) and set(P) <= set(cand)
+        want = sorted(cand, key=lambda e: (-s[e], e))[:M]
+        assert P == want
+
+
+def test_naive_prefetch_takes_only_the_preceding_steps_experts():
+    """Naive Prefetch: every prefetched expert of target layer l+1 was routed
+    there at the preceding step, never more than M_max; outputs equal the
+    adapter policy's (router preservation holds across policies)."""
+    cfg = _small_cfg(batch=2, S=4)
+    h0 = gen.hidden_states(cfg)
+    W = o.OracleWeights(cfg)
+    ref = o.run_decode(cfg, W, h0, M_max=2)
+    for M in (1, 2, 5):
+        res = o.run_decode(cfg, W, h0, M_max=M, policy="naive")
+        assert np.array_equal(np.stack(res.outputs), np.stack(ref.outputs))
+        by = {(st.t, st.l): st for st in res.steps}
+        issued = 0
+        for st in res.steps:
+            assert len(st.P) <= M
+            issued += len(st.P)
+            if st.P:
+                prev = by[(st.t - 1, st.l + 1)]
+                assert {e for e, _, _ in st.P} <= set(np.asarray(prev.T).ravel().tolist())
+            if st.t == 0:
+                assert not st.P                                   # nothing preceded the first step
+        assert issued > 0
+        assert all(np.isnan(v) for v in res.expert_recall.values())  # no adapter, no ExpertRecall
