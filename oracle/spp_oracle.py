@@ -345,6 +345,16 @@ def expert_ffn(Wg: np.ndarray, Wu: np.ndarray, Wd: np.ndarray, x: np.ndarray) ->
 # --------------------------------------------------------------------------
 
 
+def q4_decode_expert(gq, gs, uq, us, dq, ds):
+    """Values of a 4-bit expert: w = scale * (q - 8), one scale per 32
+    consecutive elements along D (gate and up rows, and each down column).
+    Returns (gate [I,D], up [I,D], down [D,I]) in fp64."""
+    def rows(q, sc):
+        return np.repeat(sc.astype(np.float64), 32, axis=1) * (q.astype(np.float64) - 8.0)
+    Wd = np.repeat(ds.astype(np.float64), 32, axis=1).T * (dq.astype(np.float64) - 8.0)
+    return rows(gq, gs), rows(uq, us), Wd
+
+
 class OracleWeights:
     """Decoded (fp64-valued) weights of a workload, regenerated from its seeds.
 
@@ -390,7 +400,10 @@ class OracleWeights:
         key = (self.cfg.expert_layer(l), e)   # tied layers share their expert weights
         if key in self._cache:
             return self._cache[key]
-        w = tuple(self._dec(a) for a in self.gen.expert_weights(self.cfg, l, e))
+        if self.cfg.codec == "q4":
+            w = tuple(a.astype(np.float32) for a in q4_decode_expert(*self.gen.expert_weights_q4(self.cfg, l, e)))
+        else:
+            w = tuple(self._dec(a) for a in self.gen.expert_weights(self.cfg, l, e))
         self._cache[key] = w
         self._order.append(key)
         if len(self._order) > self._cap:
@@ -408,7 +421,11 @@ class OracleWeights:
     def shared(self, l: int, j: int):
         key = (l, j)
         if key not in self._shared:
-            self._shared[key] = tuple(self._dec(a) for a in self.gen.shared_expert_weights(self.cfg, l, j))
+            if self.cfg.codec == "q4":
+                self._shared[key] = tuple(a.astype(np.float32) for a in
+                                          q4_decode_expert(*self.gen.shared_expert_weights_q4(self.cfg, l, j)))
+            else:
+                self._shared[key] = tuple(self._dec(a) for a in self.gen.shared_expert_weights(self.cfg, l, j))
         return self._shared[key]
 
 

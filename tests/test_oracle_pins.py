@@ -451,3 +451,47 @@ def test_naive_prefetch_takes_only_the_preceding_steps_experts():
                 assert not st.P                                   # nothing preceded the first step
         assert issued > 0
         assert all(np.isnan(v) for v in res.expert_recall.values())  # no adapter, no ExpertRecall
+
+
+# ------------------------------------------------------ 4-bit expert codec --
+
+def test_q4_decode_elementwise():
+    """w = scale * (q - 8), one scale per 32 elements along D; checked element by element."""
+    cfg = w.MoEConfig(name="q", L=2, D=64, n=4, K=2, I=5, r=4, S=4, windows=(1,), tokens=1, codec="q4", seed=3)
+    gq, gs, uq, us, dq, ds = gen.expert_weights_q4(cfg, 0, 1)
+    assert gq.dtype == np.uint8 and gq.max() <= 15 and gs.dtype == np.float16 and (gs > 0).all()
+    Wg, Wu, Wd = o.q4_decode_expert(gq, gs, uq, us, dq, ds)
+    for i in range(cfg.I):
+        for d in range(cfg.D):
+            assert Wg[i, d] == float(gs[i, d // 32]) * (int(gq[i, d]) - 8)
+            assert Wu[i, d] == float(us[i, d // 32]) * (int(uq[i, d]) - 8)
+            assert Wd[d, i] == float(ds[i, d // 32]) * (int(dq[d, i]) - 8)
+
+
+def test_q4_expert_size_matches_the_papers_on_device_figure():
+    """4-bit DeepSeek-VL2-Tiny experts occupy 1.94 MB (on-device evaluation)."""
+    assert w.get("c3q4").blob_bytes == 1_935_360
+    assert round(w.get("c3q4").blob_bytes / 1e6, 2) == 1.94
+
+
+def test_q4_layer_against_torch_textbook_block():
+    import torch
+    cfg = w.MoEConfig(name="tq", L=2, D=64, n=6, K=2, I=32, r=4, S=6, windows=(1,), tokens=2, batch=2,
+                      n_shared=1, codec="q4", seed=5)
+    W = o.OracleWeights(cfg)
+    h = o.decode(gen.hidden_states(cfg)[0], "bf16")
+    cache = o.SlotCache(cfg.S, cfg.n, list(range(cfg.n)))
+    u, x = o.layer_prologue(cfg, W, 0, h)
+    T, g, z = o.route(W.router(0), x, cfg.K)
+    assert cache.on_demand(o.batch_demand(T), 1) == []
+    out = o.moe_output(cfg, W, 0, cache, u, x, T, g)
+
+    def deq(parts):
+        gq, gs, uq, us, dq, ds = (torch.tensor(np.asarray(p, dtype=np.float64)) for p in parts)
+        rep = lambda sc: torch.repeat_interleave(sc, 32, dim=1)
+        return (rep(gs) * (gq - 8), rep(us) * (uq - 8), rep(ds).T * (dq - 8))
+    experts = [tuple(m.numpy() for m in deq(gen.expert_weights_q4(cfg, 0, e))) for e in range(cfg.n)]
+    shared = [tuple(m.numpy() for m in deq(gen.shared_expert_weights_q4(cfg, 0, j))) for j in range(cfg.n_shared)]
+    tT, tg, tout, tx = _torch_layer(h, W.router(0), cfg.K, experts, shared, cfg.rms_eps, None)
+    assert np.array_equal(T, tT)
+    np.testing.assert_allclose(out, tout, rtol=1e-11, atol=1e-12)

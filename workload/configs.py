@@ -16,6 +16,9 @@ from dataclasses import dataclass, field
 from typing import Tuple
 
 
+Q4_BLOCK = 32  # elements per scale in the "q4" expert codec
+
+
 @dataclass(frozen=True)
 class MoEConfig:
     """Shapes, storage precision and input recipe of one synthetic decode stack.
@@ -53,6 +56,10 @@ class MoEConfig:
     # those of layer l mod E (a tied offload tier that bounds pinned host
     # memory; routers, adapters and slot pools stay per layer).
     expert_layers: int = 0
+    # expert weight codec: "plain" (the storage dtype) or "q4": 4-bit codes q in
+    # 0..15 in blocks of 32 with one fp16 scale per block, w = scale * (q - 8);
+    # blocks run along D for gate rows, up rows and down columns alike
+    codec: str = "plain"
 
     @property
     def elem_bytes(self) -> int:
@@ -65,6 +72,10 @@ class MoEConfig:
 
     @property
     def blob_bytes(self) -> int:
+        """Bytes of one expert: 3 I D elements, or for "q4" 3 I D half-bytes plus
+        one 2-byte scale per 32 elements."""
+        if self.codec == "q4":
+            return self.I * (3 * self.D // 2 + 3 * (self.D // Q4_BLOCK) * 2)
         return self.blob_elems * self.elem_bytes
 
     def expert_layer(self, layer: int) -> int:
@@ -108,7 +119,12 @@ C3 = MoEConfig(name="deepseekvl2_tiny_stack12_bf16", L=12, D=1280, n=64, K=6, I=
 C4 = MoEConfig(name="qwen3vl30b_a3b_stack48_b64_bf16", L=48, D=2048, n=128, K=8, I=768, r=64,
                S=32, windows=(4,), tokens=256, batch=64, has_proj=True, seed=0)
 
-CONFIGS = {"c0": C0, "c1": C1, "c2": C2, "c3": C3, "c4": C4}
+# The same shapes with 4-bit experts (the paper's on-device setting runs a 4-bit
+# DeepSeek-VL2-Tiny, 1.94 MB per expert; the "q4" codec gives exactly that size).
+C1Q4 = C1.with_(name="qwen3vl30b_a3b_layer_q4", codec="q4")
+C3Q4 = C3.with_(name="deepseekvl2_tiny_stack12_q4", codec="q4")
+
+CONFIGS = {"c0": C0, "c1": C1, "c2": C2, "c3": C3, "c4": C4, "c1q4": C1Q4, "c3q4": C3Q4}
 
 
 def get(name: str, **overrides) -> MoEConfig:

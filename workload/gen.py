@@ -18,6 +18,9 @@ checkpoints; neither is available, so synthetic stand-ins take their place):
   A = diag(sqrt(sig_1..r)) V_r^T and B = U_r diag(sqrt(sig_1..r)) (zero rows /
   columns where r exceeds the rank), plus i.i.d. N(0, adapter_noise^2) on every
   entry; built once in fp64 and stored in the config dtype;
+* 4-bit experts (codec "q4"): codes q = clip(round(N(0, 2.5^2)), -8, 7) + 8
+  and per-block fp16 scales w_std/2.5 * U(0.75, 1.25), drawn directly (the
+  codec is the workload's weight format; nothing is quantised here);
 * layer-0 hidden states: an AR(1) sequence per batch element,
   h_0 = e_0, h_t = rho h_{t-1} + sigma e_t with e_t ~ N(0, I), built in fp64 and
   stored in the config dtype.
@@ -26,7 +29,7 @@ from __future__ import annotations
 
 import numpy as np
 
-from .configs import MoEConfig
+from .configs import Q4_BLOCK, MoEConfig
 
 KIND_ROUTER = 1
 KIND_ADAPTER_A = 2
@@ -39,6 +42,10 @@ KIND_SHARED_GATE = 8
 KIND_SHARED_UP = 9
 KIND_SHARED_DOWN = 10
 KIND_HIDDEN = 11
+KIND_Q4_CODES = 12
+KIND_Q4_SCALES = 13
+KIND_SHARED_Q4_CODES = 14
+KIND_SHARED_Q4_SCALES = 15
 
 
 def _rng(cfg: MoEConfig, kind: int, layer: int, index: int = 0) -> np.random.Generator:
@@ -72,6 +79,29 @@ def expert_weights(cfg: MoEConfig, layer: int, expert: int):
     return (_normal_weights(cfg, KIND_GATE, src, expert, (cfg.I, cfg.D)),
             _normal_weights(cfg, KIND_UP, src, expert, (cfg.I, cfg.D)),
             _normal_weights(cfg, KIND_DOWN, src, expert, (cfg.D, cfg.I)))
+
+
+def _q4_expert(cfg: MoEConfig, kind_codes: int, kind_scales: int, layer: int, index: int):
+    nb = cfg.D // Q4_BLOCK
+    g = _rng(cfg, kind_codes, layer, index)
+    codes = np.clip(np.rint(g.standard_normal((3, cfg.I, cfg.D)) * 2.5), -8, 7).astype(np.int16) + 8
+    gs = _rng(cfg, kind_scales, layer, index)
+    scales = (cfg.w_std / 2.5 * gs.uniform(0.75, 1.25, size=(3, cfg.I, nb))).astype(np.float16)
+    # gate [I,D], its scales [I,D/32]; up alike; down [D,I] with scales [I,D/32] (blocks along D of column i)
+    return (codes[0].astype(np.uint8), scales[0], codes[1].astype(np.uint8), scales[1],
+            np.ascontiguousarray(codes[2].T.astype(np.uint8)), scales[2])
+
+
+def expert_weights_q4(cfg: MoEConfig, layer: int, expert: int):
+    """4-bit routed expert: (gate codes [I,D], gate scales [I,D/32], up codes,
+    up scales, down codes [D,I], down scales [I,D/32]); codes uint8 in 0..15,
+    scales float16."""
+    return _q4_expert(cfg, KIND_Q4_CODES, KIND_Q4_SCALES, cfg.expert_layer(layer), expert)
+
+
+def shared_expert_weights_q4(cfg: MoEConfig, layer: int, j: int):
+    """4-bit always-resident shared expert ``j`` of ``layer`` (layout as expert_weights_q4)."""
+    return _q4_expert(cfg, KIND_SHARED_Q4_CODES, KIND_SHARED_Q4_SCALES, layer, j)
 
 
 def shared_expert_weights(cfg: MoEConfig, layer: int, j: int):
