@@ -39,7 +39,16 @@
  *      W_w[16t + l%16][256b + 32j + 8(l/16) + e], e = 0..7,
  *    then, from element 2*I*D, the down part in runs of 256 elements, run
  *    (s*I + i) (s < nb, i < I) holding W_down[256s + c][i], c = 0..255.
- * Blobs are placed at a stride of spp_blob_stride(desc) bytes (3*I*D*elem
+ *  SPP_LAYOUT_Q4_UNITS (expert_codec SPP_CODEC_Q4: dtype bf16, max_batch 1,
+ *    D % 256 == 0): 4-bit codes q (0..15) in blocks of 32 elements along D,
+ *    one fp16 scale per block, value scale * (q - 8).  I units of
+ *    3*D/2 + 3*(D/32)*2 bytes, unit i =
+ *      [gate codes | up codes | down codes | gate scales | up scales | down scales],
+ *    each code run D/2 bytes (byte j: element 2j in the low nibble, 2j+1 in
+ *    the high nibble; the down run holds column i of W_down, element d =
+ *    W_down[d][i]), each scale run D/32 fp16 values (scale b covers elements
+ *    32b..32b+31 of the run).
+ * Blobs are placed at a stride of spp_blob_stride(desc) bytes (the blob size
  * rounded up to 4096); the padding is zero.
  */
 #ifndef SPP_H
@@ -64,7 +73,8 @@ typedef enum {
 } spp_status;
 
 enum { SPP_DTYPE_F32 = 0, SPP_DTYPE_BF16 = 1 };
-enum { SPP_LAYOUT_UNITS = 0, SPP_LAYOUT_TILED = 1 };
+enum { SPP_LAYOUT_UNITS = 0, SPP_LAYOUT_TILED = 1, SPP_LAYOUT_Q4_UNITS = 2 };
+enum { SPP_CODEC_PLAIN = 0, SPP_CODEC_Q4 = 1 };
 enum { SPP_PREFETCH_ADAPTER = 0, SPP_PREFETCH_PREV_TOKEN = 1 };
 
 /* Model shape.  Notation of the paper's problem formulation: L MoE layers,
@@ -76,6 +86,7 @@ enum { SPP_PREFETCH_ADAPTER = 0, SPP_PREFETCH_PREV_TOKEN = 1 };
 typedef struct {
   int32_t L, D, n, K, I, r, n_shared, S, max_batch, dtype, has_proj;
   float rms_eps;
+  int32_t expert_codec;  /* SPP_CODEC_PLAIN: experts in dtype; SPP_CODEC_Q4: 4-bit (see the blob layouts) */
 } spp_model_desc;
 
 /* Counters of one moe_layer_forward call. */
@@ -115,9 +126,20 @@ int32_t spp_blob_layout(const spp_model_desc* desc);
  * spp_blob_layout(desc).  gate, up: host [I][D]; down: host [D][I]; all in
  * the storage dtype; blob: host, spp_blob_stride(desc) bytes (the padding is
  * zeroed).  Host stores and shared-expert blobs must hold blobs in this
- * layout.  Errors: EINVAL for a bad desc or a NULL pointer. */
+ * layout.  Errors: EINVAL for a bad desc (or one with the 4-bit codec: use
+ * spp_pack_expert_q4) or a NULL pointer. */
 spp_status spp_pack_expert(const spp_model_desc* desc, const void* gate, const void* up, const void* down,
                            void* blob);
+
+/* Pack one 4-bit expert (expert_codec SPP_CODEC_Q4) into its blob on the host.
+ * gate_q, up_q: host uint8 [I][D] codes 0..15; down_q: host uint8 [D][I];
+ * gate_s, up_s, down_s: host fp16 bit patterns [I][D/32] (down_s[i][b] scales
+ * elements 32b..32b+31 of column i).  blob: spp_blob_stride(desc) bytes.
+ * Errors: EINVAL for a desc without the 4-bit codec, a code above 15 or a NULL
+ * pointer (nothing written). */
+spp_status spp_pack_expert_q4(const spp_model_desc* desc, const uint8_t* gate_q, const uint16_t* gate_s,
+                              const uint8_t* up_q, const uint16_t* up_s, const uint8_t* down_q,
+                              const uint16_t* down_s, void* blob);
 
 /* Create a context on the current device.  hip_stream: the compute stream
  * (hipStream_t, may be NULL for the null stream).  Allocates S slots per layer

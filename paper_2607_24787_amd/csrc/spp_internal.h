@@ -42,6 +42,7 @@ struct FfnArgs {
   int nW;
   int I, D;
   int upw;                     // units per workgroup
+  int codec;                   // 0: experts in dtype; 1: 4-bit blocks (dtype bf16)
   const float* x;              // [D] router input of the token
   const float* gates;
   float* partial;              // [gridDim.x, D]
@@ -100,6 +101,8 @@ hipError_t launch_ffn_grouped(const GroupArgs& a, hipStream_t st, hipEvent_t sta
 hipError_t launch_combine_batched(const CombineBArgs& a, int dtype, hipStream_t st);
 hipError_t launch_spin(uint64_t ticks, uint32_t max_iter, hipStream_t st);
 int ffn_grid_for(int nunits, int* upw);
+// 4-bit experts: one pass per wave, kFfnWaves * 3 units per workgroup.
+int ffn_grid_q4(int nunits, int* upw);
 size_t ffn_max_grid();
 void set_ffn_target_wgs(int wgs);
 

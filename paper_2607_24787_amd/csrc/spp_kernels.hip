@@ -148,7 +148,9 @@ __device__ __forceinline__ uint4 ld_chunk(const void* row, int c) {
 }
 
 // Raw 16-byte chunks of a row in lane layout (zero past the row end).  FULL:
-// the row is exactly 64*NCH chunks, so no lane needs a bounds check.
+// the row is exactly 64*NCH chunks, so no lane needs a bounds check.  Past
+// the end a lane re-reads chunk 0 and keeps zero: the loads carry no branch,
+// so all of them are in flight before the first wait.
 template <int NCH, bool FULL = false, bool NT = false>
 __device__ __forceinline__ void load_chunks(const void* row, int lane, int nch, uint4 (&r)[NCH]) {
 #pragma unroll
@@ -157,8 +159,9 @@ __device__ __forceinline__ void load_chunks(const void* row, int lane, int nch, 
     if (FULL) {
       r[j] = ld_chunk<NT>(row, c);
     } else {
-      r[j] = make_uint4(0, 0, 0, 0);
-      if (c < nch) r[j] = ld_chunk<NT>(row, c);
+      const bool ok = c < nch;
+      const uint4 v = ld_chunk<NT>(row, ok ? c : 0);
+      r[j] = ok ? v : make_uint4(0, 0, 0, 0);
     }
   }
 }
@@ -172,8 +175,12 @@ __device__ __forceinline__ void load_row_f32(const float* src, int lane, int nch
 #pragma unroll
   for (int j = 0; j < NCH; ++j) {
     const int c = lane + 64 * j;
+    const bool ok = c < nch;
 #pragma unroll
-    for (int q = 0; q < Q; ++q) r[j][q] = c < nch ? ld16(src + c * V + 4 * q) : make_uint4(0, 0, 0, 0);
+    for (int q = 0; q < Q; ++q) {
+      const uint4 v = ld16(src + (ok ? c : 0) * V + 4 * q);  // no branch: all loads go out together
+      r[j][q] = ok ? v : make_uint4(0, 0, 0, 0);
+    }
   }
 #pragma unroll
   for (int j = 0; j < NCH; ++j)
@@ -723,6 +730,195 @@ __global__ __launch_bounds__(kFfnThreads) void ffn_units_kernel(FfnArgs a) {
   }
 }
 
+// ---------------------------------------------------------------------------
+// Routed-expert SwiGLU FFN over 4-bit experts (batch 1).  Unit i of an expert
+// is one contiguous run: [gate codes | up codes | down codes] (D/2 bytes each,
+// two codes per byte, low nibble first) then [gate | up | down scales] (D/32
+// fp16 each); value = scale * (q - 8) per block of 32 elements along D.
+// Lane l owns blocks l and l + 64 (NQ of them): 32 consecutive elements of x,
+// one 16-byte code load and one 2-byte scale load per row and block.  The -8
+// offset is folded out: a gate/up dot product is scale * (sum q x - 8 sum x)
+// with the block sums of x taken once, and the down accumulation adds
+// (h scale) q per element and subtracts 8 * sum(h scale) per block at the end.
+// Work list, wave order and the workgroup partials as in ffn_units_kernel.
+// ---------------------------------------------------------------------------
+constexpr int kQ4Upp = 3;  // units per wave and pass; the launch gives each workgroup kFfnWaves * kQ4Upp units
+
+__device__ __forceinline__ float q4_scale(uint16_t bits) {
+  return static_cast<float>(__builtin_bit_cast(_Float16, bits));
+}
+
+// Nibble mask the optimiser cannot see through: with the mask visible it
+// turns the four byte converts below into per-nibble extracts (two ops each)
+// instead of v_cvt_f32_ubyte0..3 (one op each).
+__device__ __forceinline__ uint32_t low_nibbles(uint32_t w) {
+  uint32_t r;
+  asm("v_and_b32 %0, 0x0f0f0f0f, %1" : "=v"(r) : "v"(w));
+  return r;
+}
+
+// The 32 codes of one block (16 bytes) as floats q_0..q_31, in element order.
+__device__ __forceinline__ void q4_codes(const uint4& c, float (&q)[32]) {
+  const uint32_t w[4] = {c.x, c.y, c.z, c.w};
+#pragma unroll
+  for (int m = 0; m < 4; ++m) {
+    const uint32_t lo = low_nibbles(w[m]), hi = low_nibbles(w[m] >> 4);
+#pragma unroll
+    for (int b = 0; b < 4; ++b) {
+      q[8 * m + 2 * b] = static_cast<float>((lo >> (8 * b)) & 0xFFu);
+      q[8 * m + 2 * b + 1] = static_cast<float>((hi >> (8 * b)) & 0xFFu);
+    }
+  }
+}
+
+template <int NQ, bool FULLQ>
+__global__ __launch_bounds__(kFfnThreads) void ffn_q4_kernel(FfnArgs a) {
+  extern __shared__ float s_red[];  // [kFfnWaves / 2][D] wave partials
+  const int tid = threadIdx.x, lane = tid & 63;
+  const int wave = __builtin_amdgcn_readfirstlane(tid >> 6);
+  const int D = a.D, I = a.I, nblk = D / 32;
+  const size_t cb = static_cast<size_t>(D) / 2, sb = static_cast<size_t>(nblk) * 2;
+  const size_t unit_bytes = 3 * cb + 3 * sb;
+
+  // lanes past the row's blocks read block 0 and keep zeros: no branch in front of the loads
+  float xv[NQ][32], xs[NQ];
+#pragma unroll
+  for (int q = 0; q < NQ; ++q) {
+    const int blk = lane + 64 * q;
+    const bool ok = FULLQ || blk < nblk;
+    float4 v[8];
+#pragma unroll
+    for (int j = 0; j < 8; ++j) {
+      const float4 t = *SPP_GLOBAL(float4, a.x + 32 * (ok ? blk : 0) + 4 * j);
+      v[j] = ok ? t : make_float4(0.f, 0.f, 0.f, 0.f);
+    }
+    xs[q] = 0.f;
+#pragma unroll
+    for (int j = 0; j < 8; ++j) {
+      xv[q][4 * j] = v[j].x;
+      xv[q][4 * j + 1] = v[j].y;
+      xv[q][4 * j + 2] = v[j].z;
+      xv[q][4 * j + 3] = v[j].w;
+      xs[q] += (v[j].x + v[j].y) + (v[j].z + v[j].w);
+    }
+  }
+  __builtin_amdgcn_sched_barrier(0);
+  float acc[NQ][32], corr[NQ];
+#pragma unroll
+  for (int q = 0; q < NQ; ++q) {
+    corr[q] = 0.f;
+#pragma unroll
+    for (int j = 0; j < 32; ++j) acc[q][j] = 0.f;
+  }
+
+  const int total = a.nW * I;
+  const int u0 = blockIdx.x * a.upw;
+  const int u1 = min(u0 + a.upw, total);
+  for (int ub = u0 + wave; ub < u1; ub += kFfnWaves * kQ4Upp) {
+    uint4 cg[kQ4Upp][NQ], cu[kQ4Upp][NQ], cd[kQ4Upp][NQ];
+    uint16_t sg[kQ4Upp][NQ], su[kQ4Upp][NQ], sd[kQ4Upp][NQ];
+    float gate[kQ4Upp];
+    // no branch in front of the loads: a unit past the range re-reads the
+    // range's last unit, a lane past the row's blocks reads block 0 (its x is
+    // zero and its outputs are not stored)
+#pragma unroll
+    for (int p = 0; p < kQ4Upp; ++p) {
+      const int uu = ub + p * kFfnWaves;
+      const int uc = uu < u1 ? uu : u1 - 1;  // wave-uniform
+      const int d = uc / I;
+      const int i = uc - d * I;
+      const uint8_t* base = reinterpret_cast<const uint8_t*>(a.blob[d]) + static_cast<size_t>(i) * unit_bytes;
+#pragma unroll
+      for (int q = 0; q < NQ; ++q) {
+        const int blk = (FULLQ || lane + 64 * q < nblk) ? lane + 64 * q : 0;
+        const u32x4 g4 = __builtin_nontemporal_load(SPP_GLOBAL(u32x4, base + 16 * blk));
+        const u32x4 u4 = __builtin_nontemporal_load(SPP_GLOBAL(u32x4, base + cb + 16 * blk));
+        const u32x4 d4 = __builtin_nontemporal_load(SPP_GLOBAL(u32x4, base + 2 * cb + 16 * blk));
+        cg[p][q] = make_uint4(g4.x, g4.y, g4.z, g4.w);
+        cu[p][q] = make_uint4(u4.x, u4.y, u4.z, u4.w);
+        cd[p][q] = make_uint4(d4.x, d4.y, d4.z, d4.w);
+        sg[p][q] = *SPP_GLOBAL(uint16_t, base + 3 * cb + 2 * blk);
+        su[p][q] = *SPP_GLOBAL(uint16_t, base + 3 * cb + sb + 2 * blk);
+        sd[p][q] = *SPP_GLOBAL(uint16_t, base + 3 * cb + 2 * sb + 2 * blk);
+      }
+      const int gi = a.gate_idx[d];
+      gate[p] = gi >= 0 ? a.gates[gi] : 1.f;
+    }
+    __builtin_amdgcn_sched_barrier(0);
+#pragma unroll
+    for (int p = 0; p < kQ4Upp; ++p) {
+      if (ub + p * kFfnWaves >= u1) continue;  // wave-uniform: no work past the range (its loads are harmless)
+      float gs = 0.f, us = 0.f;
+#pragma unroll
+      for (int q = 0; q < NQ; ++q) {
+        float qg[32], qu[32];
+        q4_codes(cg[p][q], qg);
+        q4_codes(cu[p][q], qu);
+        // four independent partial sums per row: short dependence chains
+        float dg[4] = {0.f, 0.f, 0.f, 0.f}, du[4] = {0.f, 0.f, 0.f, 0.f};
+#pragma unroll
+        for (int j = 0; j < 32; ++j) {
+          dg[j & 3] += qg[j] * xv[q][j];
+          du[j & 3] += qu[j] * xv[q][j];
+        }
+        gs += q4_scale(sg[p][q]) * (((dg[0] + dg[1]) + (dg[2] + dg[3])) - 8.f * xs[q]);
+        us += q4_scale(su[p][q]) * (((du[0] + du[1]) + (du[2] + du[3])) - 8.f * xs[q]);
+      }
+      const float g = wave_sum(gs);
+      const float u = wave_sum(us);
+      const float hval = g / (1.f + expf(-g)) * u * gate[p];
+#pragma unroll
+      for (int q = 0; q < NQ; ++q) {
+        const float hs = hval * q4_scale(sd[p][q]);
+        float qd[32];
+        q4_codes(cd[p][q], qd);
+        corr[q] += hs;
+#pragma unroll
+        for (int j = 0; j < 32; ++j) acc[q][j] += hs * qd[j];
+      }
+    }
+  }
+#pragma unroll
+  for (int q = 0; q < NQ; ++q)
+#pragma unroll
+    for (int j = 0; j < 32; ++j) acc[q][j] -= 8.f * corr[q];
+
+  // sum the waves of this workgroup in a fixed order: (w + w+H) for w < H, then slots 0..H-1
+  constexpr int H = kFfnWaves / 2;
+  if (wave >= H) {
+#pragma unroll
+    for (int q = 0; q < NQ; ++q) {
+      const int blk = lane + 64 * q;
+      if (FULLQ || blk < nblk) {
+#pragma unroll
+        for (int j = 0; j < 32; ++j) s_red[(wave - H) * D + 32 * blk + j] = acc[q][j];
+      }
+    }
+  }
+  __syncthreads();
+  if (wave < H) {
+#pragma unroll
+    for (int q = 0; q < NQ; ++q) {
+      const int blk = lane + 64 * q;
+      if (FULLQ || blk < nblk) {
+#pragma unroll
+        for (int j = 0; j < 32; ++j) {
+          float* slot = &s_red[wave * D + 32 * blk + j];
+          *slot = acc[q][j] + *slot;
+        }
+      }
+    }
+  }
+  __syncthreads();
+  float* out = a.partial + static_cast<size_t>(blockIdx.x) * D;
+  for (int d = tid; d < D; d += kFfnThreads) {
+    float v = s_red[d];
+#pragma unroll
+    for (int wv = 1; wv < H; ++wv) v += s_red[wv * D + d];
+    out[d] = v;
+  }
+}
+
 // y = sum of the workgroup partials (fixed order), h_out = round(residual + y).
 // 1024 threads cover 64 outputs: 16 groups split the partials (8 loads in
 // flight per thread), then the groups are added in order.
@@ -1175,8 +1371,27 @@ hipError_t launch_router(const RouterArgs& a, int dtype, hipStream_t st) {
   return dtype == 1 ? router_t<uint16_t>(a, st) : router_t<float>(a, st);
 }
 
+template <int NQ, bool FULLQ>
+hipError_t ffn_q4_t(const FfnArgs& a, int grid, hipStream_t st, hipEvent_t start, hipEvent_t stop) {
+  const uint32_t lds = sizeof(float) * (kFfnWaves / 2) * a.D;
+  if (start || stop)
+    hipExtLaunchKernelGGL((ffn_q4_kernel<NQ, FULLQ>), dim3(grid), dim3(kFfnThreads), lds, st, start, stop, 0u, a);
+  else
+    hipLaunchKernelGGL((ffn_q4_kernel<NQ, FULLQ>), dim3(grid), dim3(kFfnThreads), lds, st, a);
+  return hipGetLastError();
+}
+
 hipError_t launch_ffn(const FfnArgs& a, int grid, int dtype, hipStream_t st, hipEvent_t start, hipEvent_t stop) {
   if (a.nW <= 0 || a.nW > kMaxWork || grid <= 0 || a.D > 4096) return hipErrorInvalidValue;
+  if (a.codec == 1) {
+    // 4-bit experts: 32 elements per lane and block, 64 blocks per 2048-element chunk
+    if (dtype != 1 || a.D % 256 != 0) return hipErrorInvalidValue;
+    const int nblk = a.D / 32;
+    if (nblk == 64) return ffn_q4_t<1, true>(a, grid, st, start, stop);
+    if (nblk < 64) return ffn_q4_t<1, false>(a, grid, st, start, stop);
+    if (nblk == 128) return ffn_q4_t<2, true>(a, grid, st, start, stop);
+    return ffn_q4_t<2, false>(a, grid, st, start, stop);
+  }
   return dtype == 1 ? ffn_t<uint16_t>(a, grid, st, start, stop) : ffn_t<float>(a, grid, st, start, stop);
 }
 
@@ -1227,6 +1442,15 @@ hipError_t launch_spin(uint64_t ticks, uint32_t max_iter, hipStream_t st) {
 void set_ffn_target_wgs(int wgs) { g_ffn_target_wgs = wgs > 0 ? wgs : 512; }
 
 // Units per workgroup so that about g_ffn_target_wgs workgroups share the work.
+int ffn_grid_q4(int nunits, int* upw) {
+  // whole passes of kQ4Upp units per wave; more passes once the grid would
+  // exceed the partial buffer (ffn_max_grid rows)
+  const int pass = kFfnWaves * kQ4Upp;
+  const int passes = (nunits + pass * 4096 - 1) / (pass * 4096);
+  *upw = pass * (passes > 0 ? passes : 1);
+  return (nunits + *upw - 1) / *upw;
+}
+
 int ffn_grid_for(int nunits, int* upw) {
   int grid = (nunits + kFfnWaves - 1) / kFfnWaves;
   if (grid > g_ffn_target_wgs) grid = g_ffn_target_wgs;

@@ -121,7 +121,15 @@ namespace {
 // Batched contexts (bf16, max_batch > 1, D % 256 == 0, I % 16 == 0) store
 // experts in the tiled layout the grouped MFMA kernel streams linearly.
 bool tiled_layout(const spp_model_desc& d) {
-  return d.max_batch > 1 && d.dtype == SPP_DTYPE_BF16 && d.D % 256 == 0 && d.I % 16 == 0;
+  return d.expert_codec == SPP_CODEC_PLAIN && d.max_batch > 1 && d.dtype == SPP_DTYPE_BF16 && d.D % 256 == 0 &&
+         d.I % 16 == 0;
+}
+
+// Bytes of one expert blob (before the 4 KiB stride rounding).
+size_t expert_bytes(const spp_model_desc& d) {
+  if (d.expert_codec == SPP_CODEC_Q4)
+    return static_cast<size_t>(d.I) * (3 * static_cast<size_t>(d.D) / 2 + 3 * static_cast<size_t>(d.D / 32) * 2);
+  return static_cast<size_t>(3) * d.I * d.D * (d.dtype == SPP_DTYPE_BF16 ? 2 : 4);
 }
 
 bool desc_ok(const spp_model_desc* d, std::string* why) {
@@ -140,6 +148,10 @@ bool desc_ok(const spp_model_desc* d, std::string* why) {
   if (d->n_shared < 0 || d->K + d->n_shared > spp::kMaxWork) return *why = "K + n_shared must be <= 32", false;
   if (d->has_proj != 0 && d->has_proj != 1) return *why = "has_proj must be 0 or 1", false;
   if (!(d->rms_eps >= 0.f) || !std::isfinite(d->rms_eps)) return *why = "rms_eps must be finite and >= 0", false;
+  if (d->expert_codec != SPP_CODEC_PLAIN && d->expert_codec != SPP_CODEC_Q4)
+    return *why = "expert_codec must be SPP_CODEC_PLAIN or SPP_CODEC_Q4", false;
+  if (d->expert_codec == SPP_CODEC_Q4 && (d->dtype != SPP_DTYPE_BF16 || d->max_batch != 1 || d->D % 256 != 0))
+    return *why = "4-bit experts need dtype bf16, max_batch 1 and D a multiple of 256", false;
   return true;
 }
 
@@ -290,7 +302,7 @@ spp_status create_impl(const spp_model_desc* desc, void* stream, spp_ctx** out) 
   SPP_HIP(hipDeviceGetAttribute(&c->num_cu, hipDeviceAttributeMultiprocessorCount, c->device));
   c->compute = static_cast<hipStream_t>(stream);
   c->elem = desc->dtype == SPP_DTYPE_BF16 ? 2 : 4;
-  c->blob_bytes = static_cast<size_t>(3) * desc->I * desc->D * c->elem;
+  c->blob_bytes = expert_bytes(*desc);
   c->stride = round_up(c->blob_bytes, 4096);
   SPP_HIP(hipStreamCreateWithFlags(&c->copy, hipStreamNonBlocking));
   const spp_model_desc& d = c->d;
@@ -651,10 +663,12 @@ spp_status layer_forward_impl(spp_ctx* c, int32_t l, const void* h_in, void* h_o
     fa.nW = nW;
     fa.I = d.I;
     fa.D = d.D;
+    fa.codec = d.expert_codec;
     fa.x = c->x_dev + static_cast<size_t>(b) * d.D;
     fa.gates = gates_dev;
     fa.partial = c->partial;
-    const int grid = spp::ffn_grid_for(nW * d.I, &fa.upw);
+    const int grid = d.expert_codec == SPP_CODEC_Q4 ? spp::ffn_grid_q4(nW * d.I, &fa.upw)
+                                                    : spp::ffn_grid_for(nW * d.I, &fa.upw);
     const bool stamp = c->timing && b == B - 1;
     SPP_HIP(spp::launch_ffn(fa, grid, dt, c->compute, stamp ? ts.ev[kEvFfnBegin] : nullptr,
                             stamp ? ts.ev[kEvFfnEnd] : nullptr));
@@ -695,19 +709,47 @@ extern "C" {
 
 size_t spp_blob_stride(const spp_model_desc* d) {
   if (!d) return 0;
-  const size_t elem = d->dtype == SPP_DTYPE_BF16 ? 2 : 4;
-  return round_up(static_cast<size_t>(3) * d->I * d->D * elem, 4096);
+  return round_up(expert_bytes(*d), 4096);
 }
 
 int32_t spp_blob_layout(const spp_model_desc* d) {
   if (!d) return -1;
+  if (d->expert_codec == SPP_CODEC_Q4) return SPP_LAYOUT_Q4_UNITS;
   return tiled_layout(*d) ? SPP_LAYOUT_TILED : SPP_LAYOUT_UNITS;
+}
+
+spp_status spp_pack_expert_q4(const spp_model_desc* d, const uint8_t* gq, const uint16_t* gs, const uint8_t* uq,
+                              const uint16_t* us, const uint8_t* dq, const uint16_t* ds, void* blob) {
+  std::string why;
+  if (!desc_ok(d, &why)) return fail(SPP_EINVAL, why);
+  if (d->expert_codec != SPP_CODEC_Q4) return fail(SPP_EINVAL, "desc does not use the 4-bit expert codec");
+  if (!gq || !gs || !uq || !us || !dq || !ds || !blob) return fail(SPP_EINVAL, "a NULL pointer was passed");
+  const size_t D = d->D, I = d->I, nb = D / 32, cb = D / 2, sb = nb * 2;
+  const size_t unit = 3 * cb + 3 * sb;
+  for (size_t k = 0; k < I * D; ++k)
+    if (gq[k] > 15 || uq[k] > 15 || dq[k] > 15) return fail(SPP_EINVAL, "4-bit codes must be in 0..15");
+  uint8_t* o = static_cast<uint8_t*>(blob);
+  for (size_t i = 0; i < I; ++i) {
+    uint8_t* u = o + i * unit;
+    for (size_t j = 0; j < cb; ++j) {
+      u[j] = static_cast<uint8_t>(gq[i * D + 2 * j] | (gq[i * D + 2 * j + 1] << 4));
+      u[cb + j] = static_cast<uint8_t>(uq[i * D + 2 * j] | (uq[i * D + 2 * j + 1] << 4));
+      u[2 * cb + j] = static_cast<uint8_t>(dq[(2 * j) * I + i] | (dq[(2 * j + 1) * I + i] << 4));
+    }
+    std::memcpy(u + 3 * cb, gs + i * nb, sb);
+    std::memcpy(u + 3 * cb + sb, us + i * nb, sb);
+    std::memcpy(u + 3 * cb + 2 * sb, ds + i * nb, sb);
+  }
+  const size_t bytes = expert_bytes(*d);
+  std::memset(o + bytes, 0, round_up(bytes, 4096) - bytes);
+  return SPP_OK;
 }
 
 spp_status spp_pack_expert(const spp_model_desc* d, const void* gate, const void* up, const void* down,
                            void* blob) {
   std::string why;
   if (!desc_ok(d, &why)) return fail(SPP_EINVAL, why);
+  if (d->expert_codec != SPP_CODEC_PLAIN) return fail(SPP_EINVAL, "4-bit experts are packed by spp_pack_expert_q4");
   if (!gate || !up || !down || !blob) return fail(SPP_EINVAL, "gate, up, down and blob must not be NULL");
   const size_t D = d->D, I = d->I, es = d->dtype == SPP_DTYPE_BF16 ? 2 : 4;
   const uint8_t* g = static_cast<const uint8_t*>(gate);

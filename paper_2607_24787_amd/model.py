@@ -47,7 +47,9 @@ class OffloadedMoEStack:
         self.dtype_code = spp.DTYPE_BF16 if cfg.dtype == "bf16" else spp.DTYPE_F32
         self.desc = spp.make_desc(cfg.L, cfg.D, cfg.n, cfg.K, cfg.I, cfg.r, self.S, max_batch=cfg.batch,
                                   n_shared=cfg.n_shared, dtype=self.dtype_code, has_proj=cfg.has_proj,
-                                  rms_eps=cfg.rms_eps)
+                                  rms_eps=cfg.rms_eps,
+                                  expert_codec=spp.CODEC_Q4 if cfg.codec == "q4" else spp.CODEC_PLAIN)
+        q4 = cfg.codec == "q4"
         self.stride = spp.spp_blob_stride(self.desc)
         self.elem = cfg.elem_bytes
         # a tied offload tier (cfg.expert_layers) shares one host store between the layers it ties
@@ -70,8 +72,11 @@ class OffloadedMoEStack:
             if cfg.n_shared:
                 buf = np.zeros(cfg.n_shared * self.stride, dtype=np.uint8)
                 for j in range(cfg.n_shared):
-                    spp.spp_pack_expert(self.desc, *gen.shared_expert_weights(cfg, l, j),
-                                        out=buf[j * self.stride:(j + 1) * self.stride])
+                    dst = buf[j * self.stride:(j + 1) * self.stride]
+                    if q4:
+                        spp.spp_pack_expert_q4(self.desc, *gen.shared_expert_weights_q4(cfg, l, j), out=dst)
+                    else:
+                        spp.spp_pack_expert(self.desc, *gen.shared_expert_weights(cfg, l, j), out=dst)
                 self.shared.append(torch.from_numpy(buf).to(self.device))
             else:
                 self.shared.append(None)
@@ -83,8 +88,11 @@ class OffloadedMoEStack:
 
         def fill(job):
             hl, e = job
-            spp.spp_pack_expert(self.desc, *gen.expert_weights(cfg, hl, e),
-                                out=views[hl][e * self.stride:(e + 1) * self.stride])
+            dst = views[hl][e * self.stride:(e + 1) * self.stride]
+            if q4:
+                spp.spp_pack_expert_q4(self.desc, *gen.expert_weights_q4(cfg, hl, e), out=dst)
+            else:
+                spp.spp_pack_expert(self.desc, *gen.expert_weights(cfg, hl, e), out=dst)
 
         jobs = [(hl, e) for hl in range(self.host_layers) for e in range(cfg.n)]
         with ThreadPoolExecutor(max_workers=threads) as ex:

@@ -17,7 +17,8 @@ LIB_PATH = os.path.join(os.path.dirname(os.path.abspath(__file__)), "libspp.so")
 
 SPP_OK, SPP_EINVAL, SPP_ENOMEM, SPP_EHIP, SPP_ESTATE = 0, -1, -2, -3, -4
 DTYPE_F32, DTYPE_BF16 = 0, 1
-LAYOUT_UNITS, LAYOUT_TILED = 0, 1
+LAYOUT_UNITS, LAYOUT_TILED, LAYOUT_Q4_UNITS = 0, 1, 2
+CODEC_PLAIN, CODEC_Q4 = 0, 1
 PREFETCH_ADAPTER, PREFETCH_PREV_TOKEN = 0, 1
 
 
@@ -29,7 +30,7 @@ class SppError(RuntimeError):
 
 class ModelDesc(ctypes.Structure):
     _fields_ = [(f, c_int32) for f in ("L", "D", "n", "K", "I", "r", "n_shared", "S", "max_batch", "dtype",
-                                       "has_proj")] + [("rms_eps", c_float)]
+                                       "has_proj")] + [("rms_eps", c_float), ("expert_codec", c_int32)]
 
 
 class LayerStats(ctypes.Structure):
@@ -52,6 +53,8 @@ _SIGS = {
     "spp_blob_stride": (c_size_t, [POINTER(ModelDesc)]),
     "spp_blob_layout": (c_int32, [POINTER(ModelDesc)]),
     "spp_pack_expert": (c_int32, [POINTER(ModelDesc), c_void_p, c_void_p, c_void_p, c_void_p]),
+    "spp_pack_expert_q4": (c_int32, [POINTER(ModelDesc), c_void_p, c_void_p, c_void_p, c_void_p, c_void_p,
+                                     c_void_p, c_void_p]),
     "spp_create": (c_int32, [POINTER(ModelDesc), c_void_p, POINTER(c_void_p)]),
     "spp_destroy": (c_int32, [c_void_p]),
     "spp_bind_layer": (c_int32, [c_void_p, c_int32, c_void_p, c_void_p, c_void_p, c_void_p, c_void_p, c_void_p]),
@@ -131,8 +134,9 @@ def _i64(a):
 
 # ------------------------------------------------------------------ lifecycle
 
-def make_desc(L, D, n, K, I, r, S, max_batch=1, n_shared=0, dtype=DTYPE_BF16, has_proj=0, rms_eps=1e-6):
-    return ModelDesc(L, D, n, K, I, r, n_shared, S, max_batch, dtype, int(has_proj), rms_eps)
+def make_desc(L, D, n, K, I, r, S, max_batch=1, n_shared=0, dtype=DTYPE_BF16, has_proj=0, rms_eps=1e-6,
+              expert_codec=0):
+    return ModelDesc(L, D, n, K, I, r, n_shared, S, max_batch, dtype, int(has_proj), rms_eps, expert_codec)
 
 
 def spp_blob_stride(desc: ModelDesc) -> int:
@@ -158,6 +162,27 @@ def spp_pack_expert(desc: ModelDesc, gate, up, down, out=None):
         raise ValueError("out must be a writable contiguous uint8 array of at least the blob stride")
     _check(lib().spp_pack_expert(byref(desc), mats[0].ctypes.data, mats[1].ctypes.data, mats[2].ctypes.data,
                                  out.ctypes.data))
+    return out
+
+
+def spp_pack_expert_q4(desc: ModelDesc, gq, gs, uq, us, dq, ds, out=None):
+    """Pack one 4-bit expert: codes uint8 gate/up [I, D], down [D, I]; scales
+    float16 [I, D/32] each; into `out` (writable uint8, >= blob stride) or a new array."""
+    import numpy as np
+    nb = desc.D // 32
+    codes = [np.ascontiguousarray(q, dtype=np.uint8) for q in (gq, uq, dq)]
+    scales = [np.ascontiguousarray(np.asarray(sc, dtype=np.float16)).view(np.uint16) for sc in (gs, us, ds)]
+    if (codes[0].shape != (desc.I, desc.D) or codes[1].shape != (desc.I, desc.D)
+            or codes[2].shape != (desc.D, desc.I) or any(sc.shape != (desc.I, nb) for sc in scales)):
+        raise ValueError("codes gate/up [I, D], down [D, I]; scales [I, D/32]")
+    stride = spp_blob_stride(desc)
+    if out is None:
+        out = np.empty(stride, dtype=np.uint8)
+    if out.dtype != np.uint8 or out.nbytes < stride or not out.flags.c_contiguous or not out.flags.writeable:
+        raise ValueError("out must be a writable contiguous uint8 array of at least the blob stride")
+    _check(lib().spp_pack_expert_q4(byref(desc), codes[0].ctypes.data, scales[0].ctypes.data, codes[1].ctypes.data,
+                                    scales[1].ctypes.data, codes[2].ctypes.data, scales[2].ctypes.data,
+                                    out.ctypes.data))
     return out
 
 

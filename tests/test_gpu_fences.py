@@ -61,8 +61,14 @@ BATCH_ROUNDS = w.MoEConfig(name="batch5_bf16_D512_n24_k4_I160", L=2, D=512, n=24
                            windows=(2,), tokens=6, batch=5, seed=13)
 
 
-@pytest.mark.parametrize("cfg,M_max,tokens", [(RAGGED, 2, 12), (w.get("c0"), 1, 16), (BATCH_ROUNDS, 2, 6)],
-                         ids=["ragged", "c0", "batched_rounds"])
+# 4-bit experts: a poisoned slot holds 0xFF bytes, i.e. NaN scales
+Q4_FENCE = w.MoEConfig(name="q4_D256_n12_k3_I96", L=3, D=256, n=12, K=3, I=96, r=8, S=5, windows=(2,), tokens=12,
+                       codec="q4", seed=21)
+
+
+@pytest.mark.parametrize("cfg,M_max,tokens", [(RAGGED, 2, 12), (w.get("c0"), 1, 16), (BATCH_ROUNDS, 2, 6),
+                                              (Q4_FENCE, 2, 12)],
+                         ids=["ragged", "c0", "batched_rounds", "q4"])
 def test_poisoned_delayed_copies_leave_outputs_unchanged(torch_cuda, cfg, M_max, tokens):
     _log(f"[fences] {cfg.name} M_max={M_max}")
     ref, ref_on_time, needed, misses = _run(cfg, M_max, tokens)

@@ -104,6 +104,29 @@ def test_lockstep_parity_batched_grouped(torch_cuda, cfg, M_max, tokens):
     _assert_report(rep, cfg, cfg.name)
 
 
+# 4-bit experts: 8 blocks per row (partial lanes), 40 blocks with shared
+# experts (DeepSeek shape), 64 blocks (Qwen shape, full size), 128 blocks (two per lane)
+Q4_SMALL = w.MoEConfig(name="q4_D256_n12_k3_I96", L=3, D=256, n=12, K=3, I=96, r=8, S=5, windows=(2,), tokens=10,
+                       codec="q4", seed=21)
+Q4_WIDE = w.MoEConfig(name="q4_D4096_n8_k2_I64", L=2, D=4096, n=8, K=2, I=64, r=8, S=3, windows=(1,), tokens=6,
+                      codec="q4", seed=22)
+C3Q4_SHORT = w.get("c3q4").with_(L=3, tokens=4)
+C1Q4 = w.get("c1q4")
+
+
+@pytest.mark.parametrize("cfg,M_max,tokens", [(Q4_SMALL, 2, 10), (Q4_WIDE, 1, 6), (C3Q4_SHORT, 2, 4), (C1Q4, 2, 4)],
+                         ids=["q4_small", "q4_wide", "dsv2_q4", "qwen_q4_full"])
+def test_lockstep_parity_q4_experts(torch_cuda, cfg, M_max, tokens):
+    from lockstep import run_lockstep
+    _log(f"[lockstep q4] {cfg.name} M_max={M_max} tokens={tokens}")
+    st = _stack(cfg)
+    try:
+        rep = run_lockstep(st, cfg, tokens, M_max)
+    finally:
+        st.close()
+    _assert_report(rep, cfg, cfg.name)
+
+
 @pytest.mark.parametrize("cfg,M_max,tokens,must_issue", [(BATCH_BF16_ROUNDS, 3, 6, True),
                                                          (w.get("c0"), 2, 12, False)],
                          ids=["batch5_rounds", "c0"])

@@ -185,3 +185,37 @@ def test_native_prefetch_skips_minus_inf_like_the_oracle(seed):
         got = nat.prefetch(s, M, tau)
         assert got == ora.prefetch(o.select_prefetch(s.astype(np.float64), ora.occupied(), M), tau)
         assert all(np.isfinite(s[e]) for e, _, _ in got)
+
+
+def test_pack_expert_q4_places_codes_and_scales_where_the_header_says():
+    d = spp.make_desc(L=2, D=256, n=6, K=2, I=5, r=4, S=6, expert_codec=spp.CODEC_Q4)
+    assert spp.spp_blob_layout(d) == spp.LAYOUT_Q4_UNITS
+    I, D, nb = d.I, d.D, d.D // 32
+    unit = 3 * D // 2 + 3 * nb * 2
+    assert spp.spp_blob_stride(d) == -(-I * unit // 4096) * 4096
+    rng = np.random.default_rng(7)
+    gq, uq = rng.integers(0, 16, size=(I, D)).astype(np.uint8), rng.integers(0, 16, size=(I, D)).astype(np.uint8)
+    dq = rng.integers(0, 16, size=(D, I)).astype(np.uint8)
+    gs, us, ds = (rng.uniform(0.001, 0.01, size=(I, nb)).astype(np.float16) for _ in range(3))
+    blob = spp.spp_pack_expert_q4(d, gq, gs, uq, us, dq, ds)
+    for i in range(I):
+        u = blob[i * unit:(i + 1) * unit]
+        for run, codes in enumerate((gq[i], uq[i], dq[:, i])):
+            for e in range(D):
+                byte = int(u[run * D // 2 + e // 2])
+                assert (byte >> (4 * (e % 2))) & 0xF == codes[e]
+        for run, sc in enumerate((gs[i], us[i], ds[i])):
+            got = u[3 * D // 2 + run * nb * 2: 3 * D // 2 + (run + 1) * nb * 2].view(np.float16)
+            assert np.array_equal(got, sc)
+    assert not blob[I * unit:].any()
+    bad = gq.copy()
+    bad[0, 0] = 16
+    with pytest.raises(spp.SppError):
+        spp.spp_pack_expert_q4(d, bad, gs, uq, us, dq, ds)
+    with pytest.raises(spp.SppError):                                  # plain packer refuses a 4-bit desc
+        spp.spp_pack_expert(d, np.zeros((I, D), np.uint16), np.zeros((I, D), np.uint16), np.zeros((D, I), np.uint16))
+    for kw in (dict(max_batch=2), dict(dtype=spp.DTYPE_F32), dict(D=320)):  # 4-bit needs bf16, batch 1, D % 256
+        args = dict(L=2, D=256, n=6, K=2, I=5, r=4, S=6, expert_codec=spp.CODEC_Q4)
+        args.update(kw)
+        with pytest.raises(spp.SppError):
+            spp.spp_create(spp.make_desc(**args), 0)
