@@ -224,8 +224,9 @@ def main():
     ffn_bytes = int(round((distinct + cfg.n_shared) * cfg.blob_bytes))
     achieved = ffn_bytes / (on["ffn_kernel_us"] * 1e3)                   # GB/s
     # the FFN kernel this context runs: grouped MFMA over the tiled layout, or the unit-stream kernel
-    tiled = spp.spp_blob_layout(stack.desc) == spp.LAYOUT_TILED
-    kernel = "ffn_grouped_kernel" if tiled else "ffn_units_kernel"
+    layout = spp.spp_blob_layout(stack.desc)
+    kernel = {spp.LAYOUT_TILED: "ffn_grouped_kernel", spp.LAYOUT_Q4_UNITS: "ffn_q4_kernel"}.get(layout,
+                                                                                             "ffn_units_kernel")
     workload = cfg.name + ("" if not over else "+" + ",".join(f"{k}={v}" for k, v in over.items()))
     slug = workload.replace("+", "__").replace("=", "").replace(",", "_")
     traffic = measured_traffic(os.path.join(ROOT, "profiles", f"{kernel}__{slug}.md"),
