@@ -219,6 +219,17 @@ spp_status expert_cache_issue_prefetch(spp_ctx* ctx, int32_t target_layer, const
 spp_status moe_layer_forward(spp_ctx* ctx, int32_t l, const void* h_in_dev, void* h_out_dev, int32_t B,
                              int32_t M_max, int32_t* topk_out, float* gate_out, spp_layer_stats* stats);
 
+/* One whole decode step: moe_layer_forward for layers 0..L-1 in order, each
+ * layer reading the previous one's output.  The last layer writes h_out_dev;
+ * earlier layers alternate between h_out_dev and h_scratch_dev (layer l
+ * writes h_out_dev when L-1-l is even).  h_in_dev, h_out_dev, h_scratch_dev:
+ * dev [B,D] in dtype, pairwise distinct.  topk_out / gate_out: host [L,B,K]
+ * or NULL; stats: host [L] or NULL.  Saves one host round trip per layer
+ * against L separate calls.  Errors: those of moe_layer_forward; on an error
+ * in layer l, layers before l have run. */
+spp_status spp_decode_step(spp_ctx* ctx, const void* h_in_dev, void* h_out_dev, void* h_scratch_dev, int32_t B,
+                           int32_t M_max, int32_t* topk_out, float* gate_out, spp_layer_stats* stats);
+
 /* Message of the calling thread's last non-OK status ("" if none). */
 const char* spp_last_error(void);
 

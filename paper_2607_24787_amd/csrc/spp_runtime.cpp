@@ -938,6 +938,27 @@ spp_status moe_layer_forward(spp_ctx* c, int32_t l, const void* h_in_dev, void* 
   return layer_forward_impl(c, l, h_in_dev, h_out_dev, B, M_max, topk_out, gate_out, stats);
 }
 
+spp_status spp_decode_step(spp_ctx* c, const void* h_in_dev, void* h_out_dev, void* h_scratch_dev, int32_t B,
+                           int32_t M_max, int32_t* topk_out, float* gate_out, spp_layer_stats* stats) {
+  if (spp_status s = check_ctx(c)) return s;
+  if (!h_in_dev || !h_out_dev || !h_scratch_dev) return fail(SPP_EINVAL, "h_in / h_out / h_scratch is NULL");
+  if (h_in_dev == h_out_dev || h_in_dev == h_scratch_dev || h_out_dev == h_scratch_dev)
+    return fail(SPP_EINVAL, "h_in, h_out and h_scratch must be distinct");
+  const int32_t L = c->d.L, BK = B * c->d.K;
+  for (int32_t l = 0; l < L; ++l)
+    if (!c->layers[l].bound) return fail(SPP_ESTATE, "every layer must be bound");
+  // the last layer writes h_out; earlier layers alternate between the two buffers
+  const void* src = h_in_dev;
+  for (int32_t l = 0; l < L; ++l) {
+    void* dst = ((L - 1 - l) % 2 == 0) ? h_out_dev : h_scratch_dev;
+    if (spp_status s = layer_forward_impl(c, l, src, dst, B, M_max, topk_out ? topk_out + l * BK : nullptr,
+                                          gate_out ? gate_out + l * BK : nullptr, stats ? stats + l : nullptr))
+      return s;
+    src = dst;
+  }
+  return SPP_OK;
+}
+
 const char* spp_last_error(void) { return g_err.c_str(); }
 
 spp_status spp_get_last_transfers(spp_ctx* c, int32_t* loads_out, int32_t* n_loads, int32_t* pref_out,

@@ -170,6 +170,16 @@ class OffloadedMoEStack:
         self.last_buf = 1 - dst
         return out
 
+    def decode_step_from(self, h_in_ptr: int, M_max: int, B: Optional[int] = None):
+        """One decode step through all layers in a single library call
+        (spp_decode_step); the output lands in hbuf[0].  Returns the per-layer
+        (topk, gates, stats) like step_from."""
+        B = self.cfg.batch if B is None else B
+        topk, gates, stats = spp.spp_decode_step(self.ctx, self.cfg.L, h_in_ptr, self.hbuf[0].data_ptr(),
+                                                 self.hbuf[1].data_ptr(), B, self.cfg.K, M_max)
+        self.last_buf = 0
+        return [(topk[l], gates[l], stats[l]) for l in range(self.cfg.L)]
+
     def close(self):
         if getattr(self, "ctx", None):
             spp.spp_destroy(self.ctx)

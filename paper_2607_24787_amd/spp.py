@@ -63,6 +63,8 @@ _SIGS = {
     "select_prefetch_budget": (c_int32, [c_double, c_double, c_int32, POINTER(c_int32)]),
     "expert_cache_issue_prefetch": (c_int32, [c_void_p, c_int32, POINTER(c_float), c_int32, POINTER(c_int32),
                                               POINTER(c_int32)]),
+    "spp_decode_step": (c_int32, [c_void_p, c_void_p, c_void_p, c_void_p, c_int32, c_int32, POINTER(c_int32),
+                                  POINTER(c_float), c_void_p]),
     "moe_layer_forward": (c_int32, [c_void_p, c_int32, c_void_p, c_void_p, c_int32, c_int32, POINTER(c_int32),
                                     POINTER(c_float), POINTER(LayerStats)]),
     "spp_last_error": (c_char_p, []),
@@ -239,6 +241,17 @@ def moe_layer_forward(ctx, l, h_in_dev: int, h_out_dev: int, B: int, K: int, M_m
                                    topk.ctypes.data_as(POINTER(c_int32)), gates.ctypes.data_as(POINTER(c_float)),
                                    byref(st)))
     return topk, gates, st
+
+
+def spp_decode_step(ctx, L: int, h_in_dev: int, h_out_dev: int, h_scratch_dev: int, B: int, K: int, M_max: int):
+    """All L layers of one decode step; returns (topk [L,B,K], gates [L,B,K], [LayerStats] * L)."""
+    topk = np.zeros((L, B, K), dtype=np.int32)
+    gates = np.zeros((L, B, K), dtype=np.float32)
+    st = (LayerStats * L)()
+    _check(lib().spp_decode_step(c_void_p(ctx), c_void_p(h_in_dev), c_void_p(h_out_dev), c_void_p(h_scratch_dev),
+                                 B, M_max, topk.ctypes.data_as(POINTER(c_int32)),
+                                 gates.ctypes.data_as(POINTER(c_float)), st))
+    return topk, gates, list(st)
 
 
 def spp_last_error() -> str:

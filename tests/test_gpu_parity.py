@@ -274,3 +274,32 @@ def test_error_paths_on_device(torch_cuda):
         assert topk.shape == (1, cfg.K)
     finally:
         st.close()
+
+
+def test_decode_step_matches_per_layer_calls(torch_cuda):
+    """spp_decode_step (all layers in one call) gives the same outputs, routing,
+    loads and slot tables as L calls of moe_layer_forward from the same state."""
+    from paper_2607_24787_amd import spp
+    cfg = w.get("c3").with_(L=4, tokens=5)
+    h0 = gen.hidden_states(cfg)
+    a, b = _stack(cfg), _stack(cfg)
+    try:
+        for t in range(cfg.tokens):
+            a.upload_hidden(h0[t], 0)
+            b.upload_hidden(h0[t], 0)
+            ra = a.step(None, 2)
+            # the whole-step call reads its input from a buffer it does not write
+            src = b.torch.empty_like(b.hbuf[0])
+            src.copy_(b.hbuf[0])
+            rb = b.decode_step_from(src.data_ptr(), 2)
+            for l in range(cfg.L):
+                assert np.array_equal(ra[l][0], rb[l][0]) and np.array_equal(ra[l][1], rb[l][1])
+                assert (ra[l][2].misses, ra[l][2].prefetched, ra[l][2].token_hits) == \
+                       (rb[l][2].misses, rb[l][2].prefetched, rb[l][2].token_hits)
+                ea, sa = spp.spp_get_slot_table(a.ctx, l, a.S)
+                eb, sb = spp.spp_get_slot_table(b.ctx, l, b.S)
+                assert ea.tolist() == eb.tolist() and sa.tolist() == sb.tolist()
+            assert np.array_equal(a.download(a.hbuf[a.last_buf]), b.download(b.hbuf[b.last_buf]))
+    finally:
+        a.close()
+        b.close()
