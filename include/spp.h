@@ -13,13 +13,15 @@
  *    device that was current at spp_create; "host" pointers are ordinary host
  *    memory unless stated.  The caller owns every pointer it passes and keeps
  *    it valid for as long as the context may use it (weights and host stores:
- *    until spp_destroy).  The library owns its slot pools, events, copy stream
+ *    until spp_destroy).  The library owns its slot pools, events, copy streams
  *    and scratch.
  *  - Every call returns an spp_status and never throws.  On SPP_EINVAL no
  *    state has changed.  HIP runtime failures return SPP_EHIP.  The message of
  *    the last non-OK status of the calling thread is spp_last_error().
  *  - Device work is enqueued on the compute stream given to spp_create; the
- *    library's copy stream runs host-to-device expert copies beside it.  Calls
+ *    library's two copy streams run host-to-device expert copies beside it
+ *    (each blob in two halves, one per stream, so that one stream's per-copy
+ *    start-up overlaps the other's transfer).  Calls
  *    with host outputs return once those outputs are valid.
  *  - Layouts are row-major.  dtype SPP_DTYPE_F32 stores weights and hidden
  *    states as fp32, SPP_DTYPE_BF16 as bf16 (bit patterns, 2 bytes); router
@@ -284,9 +286,9 @@ spp_status spp_set_ffn_workgroups(spp_ctx* ctx, int32_t wgs);
 
 /* Test hooks for the copy/compute fences (for tests, not for production runs).
  * Poison: before every expert copy the target slot is filled with 0xFF bytes
- * (NaN in bf16 and fp32) on the copy stream, so a kernel that read a slot
+ * (NaN in bf16 and fp32) on the copy streams, so a kernel that read a slot
  * before its copy completed would produce NaN.  Copy delay: a bounded busy
- * kernel of about delay_us (0..100000) runs on the copy stream before every
+ * kernel of about delay_us (0..100000) runs on each copy stream before every
  * copy, so copies are still in flight when the FFN is enqueued and the
  * compute stream must wait on their events.  Outputs are unchanged by both. */
 spp_status spp_debug_set_poison(spp_ctx* ctx, int32_t enabled);

@@ -57,8 +57,10 @@ struct LayerState {
   const uint8_t* host_store = nullptr;
   uint8_t* slots = nullptr;
   std::unique_ptr<spp::SlotPolicy> policy;
-  std::vector<hipEvent_t> slot_ready;  // recorded on the copy stream after the last copy into the slot
-  std::vector<char> slot_pending;      // slot_ready holds a copy that may not have been waited on
+  std::vector<hipEvent_t> slot_ready;  // recorded on the copy stream after a copy into the slot
+  std::vector<hipEvent_t> slot_ready2; // the same on the second copy stream
+  std::vector<int32_t> slot_event;     // the slot whose slot_ready covers this slot's last copy
+  std::vector<char> slot_pending;      // that event may not have been waited on
   hipEvent_t last_read = nullptr;      // recorded on the compute stream after the layer's FFN
   bool last_read_valid = false;
   std::vector<int32_t> pending_prefetch;  // prefetched for this layer, not yet executed
@@ -75,7 +77,8 @@ struct spp_ctx {
   int device = 0;
   int num_cu = 256;  // compute units of the device
   hipStream_t compute = nullptr;
-  hipStream_t copy = nullptr;
+  hipStream_t copy = nullptr;   // expert copies: first half of every blob
+  hipStream_t copy2 = nullptr;  // and second half, so that one stream's per-copy gap overlaps the other's transfer
   size_t elem = 0, blob_bytes = 0, stride = 0;
   std::vector<LayerState> layers;
   float* u_dev = nullptr;      // [maxB, D] prologue output
@@ -218,19 +221,41 @@ void harvest(spp_ctx* c, size_t count) {
 
 // Issue host->device copies for transfers into layer `ls`; the copy stream
 // first waits on `war` (the last kernel that read slots being overwritten).
-spp_status issue_copies(spp_ctx* c, LayerState& ls, const std::vector<spp::Transfer>& xs, hipEvent_t war) {
+// Enqueue host-to-device copies on the copy stream.  grouped: the copies are
+// consumed together (one on-demand round), so one event after the last copy
+// covers all of them (the copy stream is in order); otherwise every copy gets
+// its own event (prefetches are consumed one by one).
+spp_status issue_copies(spp_ctx* c, LayerState& ls, const std::vector<spp::Transfer>& xs, hipEvent_t war,
+                        bool grouped) {
   if (xs.empty()) return SPP_OK;
-  if (war) SPP_HIP(hipStreamWaitEvent(c->copy, war, 0));  // WAR on slot reuse
+  // WAR on slot reuse, unless the last kernel that read this layer already finished
+  if (war && hipEventQuery(war) != hipSuccess) {
+    SPP_HIP(hipStreamWaitEvent(c->copy, war, 0));
+    SPP_HIP(hipStreamWaitEvent(c->copy2, war, 0));
+  }
+  const int32_t last = xs.back().slot;
+  // each blob in two halves, one per copy stream (the split is 4 KiB aligned)
+  const size_t half = (c->blob_bytes / 2 + 4095) / 4096 * 4096;
+  const size_t part[2] = {std::min(half, c->blob_bytes), c->blob_bytes - std::min(half, c->blob_bytes)};
+  hipStream_t streams[2] = {c->copy, c->copy2};
   for (const spp::Transfer& t : xs) {
-    if (c->copy_delay_us > 0) {
-      const uint64_t ticks = c->wall_khz * static_cast<uint64_t>(c->copy_delay_us) / 1000;
-      SPP_HIP(spp::launch_spin(ticks, static_cast<uint32_t>(c->copy_delay_us) * 64u + 1024u, c->copy));
+    uint8_t* dst = ls.slots + static_cast<size_t>(t.slot) * c->stride;
+    const uint8_t* src = ls.host_store + static_cast<size_t>(t.expert) * c->stride;
+    for (int h = 0; h < 2; ++h) {
+      if (part[h] == 0) continue;
+      if (c->copy_delay_us > 0) {
+        const uint64_t ticks = c->wall_khz * static_cast<uint64_t>(c->copy_delay_us) / 1000;
+        SPP_HIP(spp::launch_spin(ticks, static_cast<uint32_t>(c->copy_delay_us) * 64u + 1024u, streams[h]));
+      }
+      const size_t off = h == 0 ? 0 : part[0];
+      if (c->poison) SPP_HIP(hipMemsetAsync(dst + off, 0xFF, part[h], streams[h]));
+      SPP_HIP(hipMemcpyAsync(dst + off, src + off, part[h], hipMemcpyHostToDevice, streams[h]));
     }
-    if (c->poison) SPP_HIP(hipMemsetAsync(ls.slots + static_cast<size_t>(t.slot) * c->stride, 0xFF, c->blob_bytes, c->copy));
-    SPP_HIP(hipMemcpyAsync(ls.slots + static_cast<size_t>(t.slot) * c->stride,
-                           ls.host_store + static_cast<size_t>(t.expert) * c->stride, c->blob_bytes,
-                           hipMemcpyHostToDevice, c->copy));
-    SPP_HIP(hipEventRecord(ls.slot_ready[t.slot], c->copy));
+    if (!grouped || t.slot == last) {
+      SPP_HIP(hipEventRecord(ls.slot_ready[t.slot], c->copy));
+      SPP_HIP(hipEventRecord(ls.slot_ready2[t.slot], c->copy2));
+    }
+    ls.slot_event[t.slot] = grouped ? last : t.slot;
     ls.slot_pending[t.slot] = 1;
     c->stats.copies += 1;
     c->stats.copy_bytes += static_cast<int64_t>(c->blob_bytes);
@@ -240,6 +265,7 @@ spp_status issue_copies(spp_ctx* c, LayerState& ls, const std::vector<spp::Trans
 
 spp_status sync_all(spp_ctx* c) {
   SPP_HIP(hipStreamSynchronize(c->copy));
+  SPP_HIP(hipStreamSynchronize(c->copy2));
   SPP_HIP(hipStreamSynchronize(c->compute));
   return SPP_OK;
 }
@@ -260,10 +286,13 @@ spp_status fill_slots(spp_ctx* c, LayerState& ls, const std::vector<int32_t>& be
 void free_ctx(spp_ctx* c) {
   if (!c) return;
   if (c->copy) (void)hipStreamSynchronize(c->copy);
+  if (c->copy2) (void)hipStreamSynchronize(c->copy2);
   (void)hipStreamSynchronize(c->compute);
   for (LayerState& ls : c->layers) {
     if (ls.slots) (void)hipFree(ls.slots);
     for (hipEvent_t e : ls.slot_ready)
+      if (e) (void)hipEventDestroy(e);
+    for (hipEvent_t e : ls.slot_ready2)
       if (e) (void)hipEventDestroy(e);
     if (ls.last_read) (void)hipEventDestroy(ls.last_read);
   }
@@ -287,6 +316,7 @@ void free_ctx(spp_ctx* c) {
   if (c->groups_dev) (void)hipFree(c->groups_dev);
   if (c->ypart) (void)hipFree(c->ypart);
   if (c->copy) (void)hipStreamDestroy(c->copy);
+  if (c->copy2) (void)hipStreamDestroy(c->copy2);
   delete c;
 }
 
@@ -305,14 +335,19 @@ spp_status create_impl(const spp_model_desc* desc, void* stream, spp_ctx** out) 
   c->blob_bytes = expert_bytes(*desc);
   c->stride = round_up(c->blob_bytes, 4096);
   SPP_HIP(hipStreamCreateWithFlags(&c->copy, hipStreamNonBlocking));
+  SPP_HIP(hipStreamCreateWithFlags(&c->copy2, hipStreamNonBlocking));
   const spp_model_desc& d = c->d;
   c->layers.resize(d.L);
   for (LayerState& ls : c->layers) {
     ls.policy.reset(new spp::SlotPolicy(d.S, d.n));
     if (hipMalloc(&ls.slots, c->stride * d.S) != hipSuccess) return fail(SPP_ENOMEM, "slot pool allocation failed");
     ls.slot_ready.assign(d.S, nullptr);
+    ls.slot_ready2.assign(d.S, nullptr);
     ls.slot_pending.assign(d.S, 0);
+    ls.slot_event.resize(d.S);
+    for (int32_t j = 0; j < d.S; ++j) ls.slot_event[j] = j;
     for (hipEvent_t& e : ls.slot_ready) SPP_HIP(hipEventCreateWithFlags(&e, hipEventDisableTiming));
+    for (hipEvent_t& e : ls.slot_ready2) SPP_HIP(hipEventCreateWithFlags(&e, hipEventDisableTiming));
     SPP_HIP(hipEventCreateWithFlags(&ls.last_read, hipEventDisableTiming));
   }
   const size_t BD = static_cast<size_t>(d.max_batch) * d.D;
@@ -376,18 +411,24 @@ spp_status wait_router(spp_ctx* c, uint32_t seq) {
 
 // RAW: the compute stream waits for the copies into the slots a round reads.
 spp_status wait_round(spp_ctx* c, LayerState& ls, const spp::Round& round, spp_layer_stats* st) {
+  std::vector<int32_t> waited;  // each covering event is waited on once
   for (const auto& es : round) {
     const int32_t slot = es.second;
     if (!ls.slot_pending[slot]) {
       st->ready_on_time += 1;
       continue;
     }
-    if (hipEventQuery(ls.slot_ready[slot]) == hipSuccess) {
+    const int32_t ev = ls.slot_event[slot];
+    if (hipEventQuery(ls.slot_ready[ev]) == hipSuccess && hipEventQuery(ls.slot_ready2[ev]) == hipSuccess) {
       st->ready_on_time += 1;
       ls.slot_pending[slot] = 0;
       continue;
     }
-    SPP_HIP(hipStreamWaitEvent(c->compute, ls.slot_ready[slot], 0));
+    if (std::find(waited.begin(), waited.end(), ev) == waited.end()) {
+      SPP_HIP(hipStreamWaitEvent(c->compute, ls.slot_ready[ev], 0));
+      SPP_HIP(hipStreamWaitEvent(c->compute, ls.slot_ready2[ev], 0));
+      waited.push_back(ev);
+    }
   }
   return SPP_OK;
 }
@@ -472,7 +513,7 @@ spp_status grouped_ffn(spp_ctx* c, LayerState& ls, LayerState* next, const int32
       std::vector<spp::Transfer> xs;
       for (const spp::Transfer& t : loads)
         if (t.round == static_cast<int32_t>(r)) xs.push_back(t);
-      if (spp_status e = issue_copies(c, ls, xs, done)) return e;
+      if (spp_status e = issue_copies(c, ls, xs, done, true)) return e;
       if (c->timing)
         if (spp_status e = record_extra(c, ts)) return e;
       if (spp_status e = wait_round(c, ls, rounds[r], st)) return e;
@@ -494,7 +535,8 @@ spp_status grouped_ffn(spp_ctx* c, LayerState& ls, LayerState* next, const int32
                                     c->timing && last ? ts.ev[kEvFfnEnd] : nullptr));
   }
   if (rounds.size() > 1 && next && !c->last_pref.empty())
-    if (spp_status e = issue_copies(c, *next, c->last_pref, next->last_read_valid ? next->last_read : nullptr))
+    if (spp_status e = issue_copies(c, *next, c->last_pref, next->last_read_valid ? next->last_read : nullptr,
+                                    false))
       return e;
   spp::CombineBArgs cb{};
   cb.ypart = c->ypart;
@@ -635,10 +677,11 @@ spp_status layer_forward_impl(spp_ctx* c, int32_t l, const void* h_in, void* h_o
     std::vector<spp::Transfer> first;
     for (const spp::Transfer& t : c->last_loads)
       if (t.round == 0) first.push_back(t);
-    if (spp_status e = issue_copies(c, ls, first, ls.last_read_valid ? ls.last_read : nullptr)) return e;
+    if (spp_status e = issue_copies(c, ls, first, ls.last_read_valid ? ls.last_read : nullptr, true)) return e;
   }
   if (rounds.size() == 1 && nx)
-    if (spp_status e = issue_copies(c, *nx, c->last_pref, nx->last_read_valid ? nx->last_read : nullptr)) return e;
+    if (spp_status e = issue_copies(c, *nx, c->last_pref, nx->last_read_valid ? nx->last_read : nullptr, false))
+      return e;
 
   // RAW: the FFN reads each needed slot only after its copy completed
   if (c->timing) SPP_HIP(hipEventRecord(ts.ev[kEvWaitA], c->compute));
@@ -922,7 +965,7 @@ spp_status expert_cache_issue_prefetch(spp_ctx* c, int32_t target_layer, const f
   const int64_t tau = ++c->clock;
   std::vector<spp::Transfer> placed;
   ls.policy->prefetch(s_host, M_max, tau, &placed);
-  if (spp_status e = issue_copies(c, ls, placed, ls.last_read_valid ? ls.last_read : nullptr)) return e;
+  if (spp_status e = issue_copies(c, ls, placed, ls.last_read_valid ? ls.last_read : nullptr, false)) return e;
   ls.pending_prefetch.clear();
   for (size_t i = 0; i < placed.size(); ++i) {
     issued_out[i] = placed[i].expert;
