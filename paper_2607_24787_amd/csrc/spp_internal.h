@@ -59,7 +59,7 @@ struct GroupDesc {
 };
 
 struct GroupArgs {
-  const GroupDesc* groups;  // [ngroups] (device)
+  const GroupDesc* groups;  // [ngroups] (device-visible; host-mapped pinned memory)
   int ngroups, nsplit, upw; // each group's I units are split into nsplit ranges of upw units
   int I, D;
   const float* x;           // [B, D] router inputs

@@ -96,8 +96,10 @@ struct spp_ctx {
   // batched decode (B > 1, bf16): expert groups and partial outputs
   bool grouped = false;
   int max_groups = 0, max_nsplit = 0;
-  spp::GroupDesc* groups_dev = nullptr;
-  spp::GroupDesc* groups_host = nullptr;  // pinned staging for the per-layer group list
+  spp::GroupDesc* groups_dev = nullptr;   // device address of groups_host (host-mapped)
+  spp::GroupDesc* groups_host = nullptr;  // per-layer group list, pinned and device-mapped: the grouped
+                                          // kernel reads it in place (rewritten only after the next
+                                          // router, i.e. after the previous FFN, has finished)
   float* ypart = nullptr;
   std::vector<hipEvent_t> round_done;  // per on-demand round: its FFN launch finished
   int64_t clock = 0;
@@ -313,7 +315,6 @@ void free_ctx(spp_ctx* c) {
     if (p) (void)hipFree(p);
   if (c->res_host) (void)hipHostFree(c->res_host);
   if (c->groups_host) (void)hipHostFree(c->groups_host);
-  if (c->groups_dev) (void)hipFree(c->groups_dev);
   if (c->ypart) (void)hipFree(c->ypart);
   if (c->copy) (void)hipStreamDestroy(c->copy);
   if (c->copy2) (void)hipStreamDestroy(c->copy2);
@@ -373,10 +374,11 @@ spp_status create_impl(const spp_model_desc* desc, void* stream, spp_ctx** out) 
     c->max_groups = d.max_batch * d.K + d.n_shared * ((d.max_batch + spp::kGroupTokens - 1) / spp::kGroupTokens);
     c->max_nsplit = (d.I + 63) / 64;
     const size_t npairs = static_cast<size_t>(d.max_batch) * (d.K + d.n_shared);
-    if (hipMalloc(&c->groups_dev, sizeof(spp::GroupDesc) * c->max_groups) != hipSuccess ||
-        hipHostMalloc(&c->groups_host, sizeof(spp::GroupDesc) * c->max_groups, hipHostMallocDefault) != hipSuccess ||
+    if (hipHostMalloc(&c->groups_host, sizeof(spp::GroupDesc) * c->max_groups,
+                      hipHostMallocMapped | hipHostMallocCoherent) != hipSuccess ||
         hipMalloc(&c->ypart, npairs * c->max_nsplit * d.D * sizeof(float)) != hipSuccess)
       return fail(SPP_ENOMEM, "batched-decode buffers allocation failed");
+    SPP_HIP(hipHostGetDevicePointer(reinterpret_cast<void**>(&c->groups_dev), c->groups_host, 0));
   }
   SPP_HIP(hipMemset(c->counter, 0, 256));
   SPP_HIP(hipMemset(c->res_dev, 0, c->res_bytes));
@@ -498,8 +500,6 @@ spp_status grouped_ffn(spp_ctx* c, LayerState& ls, LayerState* next, const int32
     rcount[r] = ng - rstart[r];
     maxg = std::max(maxg, rcount[r]);
   }
-  SPP_HIP(hipMemcpyAsync(c->groups_dev, c->groups_host, sizeof(spp::GroupDesc) * ng, hipMemcpyHostToDevice,
-                         c->compute));
   // ranges of 128 units (one 16-unit tile per wave); 64 when the largest
   // round would not give two workgroups per compute unit
   const int upw = static_cast<long>(maxg) * ((d.I + 127) / 128) >= 2L * c->num_cu ? 128 : 64;
