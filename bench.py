@@ -162,6 +162,9 @@ def main():
                     help="offload tier of k distinct expert layers shared round-robin (0: one per layer)")
     ap.add_argument("--sweep", type=lambda v: [int(x) for x in v.split(",") if x != ""], default=[],
                     help="extra modes at these M_max values, e.g. 0,1,2,4,8,16")
+    ap.add_argument("--tier-gbps", type=lambda v: [float(x) for x in v.split(",") if x != ""], default=[],
+                    help="storage emulation: for each offload-tier bandwidth (GB/s, below the link's), "
+                         "time OFF and M_max 1, 2 with every expert copy slowed to it")
     ap.add_argument("--copy-probe", action="store_true",
                     help="only run a 256 MiB device-to-device copy three times (counter calibration)")
     args = ap.parse_args()
@@ -224,6 +227,17 @@ def main():
              f"coverage={modes[f'M{M}']['next_layer_coverage']:.3f} "
              f"exposed={modes[f'M{M}']['exposed_transfer_pct']:.1f}%")
 
+    for gbps in args.tier_gbps:
+        # one expert then takes blob / gbps: a busy wait of the difference before each copy
+        delay = max(0, int(round(cfg.blob_bytes / (gbps * 1e3) - per_expert_us)))
+        spp.spp_set_tier_delay(stack.ctx, min(delay, 100000))
+        for name, M in (("off", -1), ("M1", 1), ("M2", 2)):
+            r = run_mode(stack, dev_h, row_bytes, args.warmup, args.steps, M)
+            r["tier_gbps"], r["tier_delay_us"] = gbps, delay
+            modes[f"tier{gbps:g}_{name}"] = r
+            _log(f"[bench] tier {gbps:g} GB/s (+{delay} us per expert) {name} {r['tokens_per_s']:.1f} tok/s "
+                 f"coverage={r['next_layer_coverage']:.3f}")
+        spp.spp_set_tier_delay(stack.ctx, 0)
     window_us = on["compute_window_us"]
     implied_budget = (spp.select_prefetch_budget(window_us, per_expert_us, cfg.n)
                       if window_us is not None else None)

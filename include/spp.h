@@ -284,13 +284,21 @@ spp_status spp_set_prefetch_source(spp_ctx* ctx, int32_t source);
  * every context in the process. */
 spp_status spp_set_ffn_workgroups(spp_ctx* ctx, int32_t wgs);
 
+/* Storage-speed emulation ("Storage Sensitivity", Figure 5): every expert
+ * copy is preceded, on each copy stream, by a bounded busy kernel of about
+ * delay_us (0..100000), so one expert takes delay_us plus its transfer --
+ * the offload tier behaves like slower storage behind the same link.
+ * Outputs are unchanged.  EINVAL outside the range. */
+spp_status spp_set_tier_delay(spp_ctx* ctx, int32_t delay_us);
+
 /* Test hooks for the copy/compute fences (for tests, not for production runs).
  * Poison: before every expert copy the target slot is filled with 0xFF bytes
  * (NaN in bf16 and fp32) on the copy streams, so a kernel that read a slot
  * before its copy completed would produce NaN.  Copy delay: a bounded busy
  * kernel of about delay_us (0..100000) runs on each copy stream before every
- * copy, so copies are still in flight when the FFN is enqueued and the
- * compute stream must wait on their events.  Outputs are unchanged by both. */
+ * copy (the mechanism of spp_set_tier_delay), so copies are still in flight
+ * when the FFN is enqueued and the compute stream must wait on their events.
+ * Outputs are unchanged by both. */
 spp_status spp_debug_set_poison(spp_ctx* ctx, int32_t enabled);
 spp_status spp_debug_set_copy_delay(spp_ctx* ctx, int32_t delay_us);
 

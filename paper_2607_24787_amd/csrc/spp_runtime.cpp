@@ -1093,6 +1093,8 @@ spp_status spp_debug_set_poison(spp_ctx* c, int32_t enabled) {
   return SPP_OK;
 }
 
+spp_status spp_set_tier_delay(spp_ctx* c, int32_t delay_us) { return spp_debug_set_copy_delay(c, delay_us); }
+
 spp_status spp_debug_set_copy_delay(spp_ctx* c, int32_t delay_us) {
   if (spp_status s = check_ctx(c)) return s;
   if (delay_us < 0 || delay_us > 100000) return fail(SPP_EINVAL, "delay_us must be in [0, 100000]");

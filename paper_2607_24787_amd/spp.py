@@ -81,6 +81,7 @@ _SIGS = {
     "spp_reset_run_stats": (c_int32, [c_void_p]),
     "spp_profile_expert_copy": (c_int32, [c_void_p, c_int32, c_int32, POINTER(c_double)]),
     "spp_set_prefetch_source": (c_int32, [c_void_p, c_int32]),
+    "spp_set_tier_delay": (c_int32, [c_void_p, c_int32]),
     "spp_set_ffn_workgroups": (c_int32, [c_void_p, c_int32]),
     "spp_debug_set_poison": (c_int32, [c_void_p, c_int32]),
     "spp_debug_set_copy_delay": (c_int32, [c_void_p, c_int32]),
@@ -324,6 +325,10 @@ def spp_profile_expert_copy(ctx, l, reps) -> float:
     us = c_double()
     _check(lib().spp_profile_expert_copy(c_void_p(ctx), l, reps, byref(us)))
     return us.value
+
+
+def spp_set_tier_delay(ctx, delay_us: int):
+    _check(lib().spp_set_tier_delay(c_void_p(ctx), int(delay_us)))
 
 
 def spp_set_prefetch_source(ctx, source: int):

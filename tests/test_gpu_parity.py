@@ -260,6 +260,17 @@ def test_error_paths_on_device(torch_cuda):
             spp.moe_layer_forward(st.ctx, 0, st.hbuf[0].data_ptr(), st.hbuf[1].data_ptr(), 2, cfg.K, 1)
         with pytest.raises(spp.SppError):
             spp.spp_set_resident(st.ctx, 0, [0, 0])
+        for bad in (-1, 100001):
+            with pytest.raises(spp.SppError) as e:
+                spp.spp_set_tier_delay(st.ctx, bad)
+            assert e.value.status == spp.SPP_EINVAL
+        with pytest.raises(spp.SppError) as e:
+            spp.spp_set_prefetch_source(st.ctx, 7)
+        assert e.value.status == spp.SPP_EINVAL
+        with pytest.raises(spp.SppError) as e:                 # whole-step call: buffers must be distinct
+            spp.spp_decode_step(st.ctx, cfg.L, st.hbuf[0].data_ptr(), st.hbuf[0].data_ptr(), st.hbuf[1].data_ptr(),
+                                1, cfg.K, 1)
+        assert e.value.status == spp.SPP_EINVAL
         # a slot count below the batch demand is refused at the first layer call
         small = _stack(cfg, S=cfg.K - 1, resident=[])
         try:
