@@ -117,6 +117,47 @@ def run_mode(stack, dev_h, row_bytes, warmup, steps, M_max, naive=False):
     }
 
 
+def distill_adapters(stack, cfg, seqs: int, length: int):
+    """Train every adapter by KL distillation on traces of `seqs` fresh AR(1)
+    sequences of `length` tokens (same weights, other sequence streams), score
+    ExpertRecall on 4 held-out sequences, and return a stack bound to the
+    distilled adapters with the report."""
+    import numpy as np
+    from paper_2607_24787_amd import distill
+    from paper_2607_24787_amd.model import OffloadedMoEStack
+    from workload import gen
+
+    t0 = time.perf_counter()
+    B = cfg.batch
+    pool = gen.hidden_states(cfg.with_(batch=B * (1 + seqs + 4)), tokens=length)   # [T, B*(1+seqs+4), D]
+    def seq_block(first, count):   # sequences first..first+count-1 in groups of B, laid end to end in time
+        blk = pool[:, B * first: B * (first + count)].reshape(length, count, B, cfg.D)
+        return np.ascontiguousarray(blk.transpose(1, 0, 2, 3).reshape(count * length, B, cfg.D))
+    X, Z = distill.collect_traces(stack, seq_block(1, seqs))
+    Xe, Ze = distill.collect_traces(stack, seq_block(1 + seqs, 4))
+
+    def values(a):
+        a = np.asarray(a)
+        return (a.astype(np.uint32) << np.uint32(16)).view(np.float32) if a.dtype == np.uint16 else a.astype(np.float32)
+    adapters, report = {}, []
+    for l in range(cfg.L - 1):
+        A0, B0 = (values(m) for m in gen.adapter_weights(cfg, l))
+        A, Bm, (k0, k1) = distill.distill_adapter(X[l], Z[l + 1], A0, B0, seed=l)
+        adapters[l] = (A, Bm)
+        row = {"layer": l, "kl_start": k0, "kl_end": k1}
+        for M in sorted({max(1, cfg.K // 2), cfg.K, cfg.K + 2}):
+            row[f"recall@{M}_svd"] = distill.expert_recall(A0, B0, Xe[l], Ze[l + 1], cfg.K, M)
+            row[f"recall@{M}_distilled"] = distill.expert_recall(A, Bm, Xe[l], Ze[l + 1], cfg.K, M)
+        report.append(row)
+        _log(f"[bench] distill layer {l}: KL {k0:.4f} -> {k1:.4f}, held-out recall@{cfg.K} "
+             f"{row[f'recall@{cfg.K}_svd']:.3f} -> {row[f'recall@{cfg.K}_distilled']:.3f}")
+    stack.close()
+    new = OffloadedMoEStack(cfg, adapter_values=lambda l: adapters[l])
+    info = {"sequences": seqs, "tokens_per_sequence": length, "held_out_sequences": 4,
+            "train_pairs_per_layer": int(X[0].shape[0]), "seconds": time.perf_counter() - t0, "layers": report}
+    return new, info
+
+
 def cpu_baseline(cfg, tokens: int):
     """The oracle, untuned, on the host cores: decode of the first `tokens` steps
     through all layers (expert weights decoded before the timed region)."""
@@ -162,6 +203,9 @@ def main():
                     help="offload tier of k distinct expert layers shared round-robin (0: one per layer)")
     ap.add_argument("--sweep", type=lambda v: [int(x) for x in v.split(",") if x != ""], default=[],
                     help="extra modes at these M_max values, e.g. 0,1,2,4,8,16")
+    ap.add_argument("--distill", type=int, default=0,
+                    help="train the adapters by KL distillation on traces of this many fresh sequences first")
+    ap.add_argument("--distill-len", type=int, default=64, help="tokens per distillation sequence")
     ap.add_argument("--tier-gbps", type=lambda v: [float(x) for x in v.split(",") if x != ""], default=[],
                     help="storage emulation: for each offload-tier bandwidth (GB/s, below the link's), "
                          "time OFF and M_max 1, 2 with every expert copy slowed to it")
@@ -207,6 +251,12 @@ def main():
     dev_h = torch.from_numpy(np.ascontiguousarray(h_all).reshape(-1).view(np.uint8).copy()).to(stack.device)
     torch.cuda.synchronize()
     _log(f"[bench] setup {time.perf_counter() - t_setup:.1f}s workload={cfg.name}")
+
+    distilled = None
+    if args.distill > 0:
+        stack, distilled = distill_adapters(stack, cfg, args.distill, args.distill_len)
+        if args.ffn_wgs:
+            spp.spp_set_ffn_workgroups(stack.ctx, args.ffn_wgs)
 
     per_expert_us = spp.spp_profile_expert_copy(stack.ctx, 0, 32)
     link_gbs = cfg.blob_bytes / (per_expert_us * 1e3)
@@ -284,6 +334,9 @@ def main():
                    "implied_budget": implied_budget, "configured_budget": cfg.window},
         "modes": modes,
     }
+    if distilled is not None:
+        line["config"]["adapters"] = "KL-distilled on synthetic traces"
+        line["distill"] = distilled
     stack.close()
     if args.cpu_tokens > 0:
         _log(f"[bench] cpu baseline: oracle on {args.cpu_tokens} tokens")

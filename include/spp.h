@@ -260,6 +260,12 @@ spp_status spp_get_last_transfers(spp_ctx* ctx, int32_t* loads_out, int32_t* n_l
 spp_status spp_get_last_priorities(spp_ctx* ctx, float* s_out);
 spp_status spp_get_last_router_input(spp_ctx* ctx, float* x_out, int32_t B);
 
+/* Native router logits z (host fp32 [B,n]) of the last moe_layer_forward
+ * (the distillation targets of section "Training Objective").  ESTATE when
+ * that call ran the adapter at B > 1 (its selection kernel reuses the logit
+ * buffer) or after adapter_predict; B at most the last call's batch. */
+spp_status spp_get_last_logits(spp_ctx* ctx, float* z_out, int32_t B);
+
 /* Event timing of layer calls (adds ~6 event records per call). */
 spp_status spp_set_timing(spp_ctx* ctx, int32_t enabled);
 /* Waits for all enqueued work, folds finished event timings into the totals. */

@@ -112,6 +112,7 @@ struct spp_ctx {
   std::vector<spp::Transfer> last_loads, last_pref;
   std::vector<float> last_s;
   int32_t last_B = 0;
+  bool logits_valid = false;  // zbuf still holds the last call's router logits
   bool last_s_valid = false;
   // timing
   bool timing = false;
@@ -664,6 +665,7 @@ spp_status layer_forward_impl(spp_ctx* c, int32_t l, const void* h_in, void* h_o
   c->last_pref.clear();
   c->last_s_valid = predict;
   c->last_B = B;
+  c->logits_valid = !(adapter_on && B > 1);  // the batched selection overwrites logits with pi_hat
   if (predict) {
     std::memcpy(c->last_s.data(), s, sizeof(float) * d.n);
     if (nx) {
@@ -941,6 +943,7 @@ spp_status adapter_predict(spp_ctx* c, int32_t l, const float* x_dev, int32_t B,
   ra.eps = d.rms_eps;
   ra.x_given = 1;
   ra.router_on = 0;
+  c->logits_valid = false;
   ra.done_host = reinterpret_cast<unsigned*>(c->res_host_dev + c->off_flag);
   ra.seq = next_router_seq(c);
   SPP_HIP(spp::launch_router(ra, d.dtype, c->compute));
@@ -1035,6 +1038,17 @@ spp_status spp_get_last_router_input(spp_ctx* c, float* x_out, int32_t B) {
   if (!x_out || B < 1 || B > c->d.max_batch) return fail(SPP_EINVAL, "bad x_out / B");
   SPP_HIP(hipStreamSynchronize(c->compute));
   SPP_HIP(hipMemcpy(x_out, c->x_dev, sizeof(float) * B * c->d.D, hipMemcpyDeviceToHost));
+  return SPP_OK;
+}
+
+spp_status spp_get_last_logits(spp_ctx* c, float* z_out, int32_t B) {
+  if (spp_status s = check_ctx(c)) return s;
+  if (!z_out || B < 1 || B > c->last_B) return fail(SPP_EINVAL, "bad z_out / B");
+  if (!c->logits_valid) return fail(SPP_ESTATE, "the last call did not leave its router logits");
+  SPP_HIP(hipStreamSynchronize(c->compute));
+  const size_t ldz = static_cast<size_t>(c->d.n) + c->d.r;
+  SPP_HIP(hipMemcpy2D(z_out, sizeof(float) * c->d.n, c->zbuf, sizeof(float) * ldz, sizeof(float) * c->d.n, B,
+                      hipMemcpyDeviceToHost));
   return SPP_OK;
 }
 

@@ -82,6 +82,7 @@ _SIGS = {
     "spp_profile_expert_copy": (c_int32, [c_void_p, c_int32, c_int32, POINTER(c_double)]),
     "spp_set_prefetch_source": (c_int32, [c_void_p, c_int32]),
     "spp_set_tier_delay": (c_int32, [c_void_p, c_int32]),
+    "spp_get_last_logits": (c_int32, [c_void_p, POINTER(c_float), c_int32]),
     "spp_set_ffn_workgroups": (c_int32, [c_void_p, c_int32]),
     "spp_debug_set_poison": (c_int32, [c_void_p, c_int32]),
     "spp_debug_set_copy_delay": (c_int32, [c_void_p, c_int32]),
@@ -305,6 +306,12 @@ def spp_get_last_router_input(ctx, B, D):
     x = np.zeros((B, D), dtype=np.float32)
     _check(lib().spp_get_last_router_input(c_void_p(ctx), x.ctypes.data_as(POINTER(c_float)), B))
     return x
+
+
+def spp_get_last_logits(ctx, B, n):
+    z = np.zeros((B, n), dtype=np.float32)
+    _check(lib().spp_get_last_logits(c_void_p(ctx), z.ctypes.data_as(POINTER(c_float)), B))
+    return z
 
 
 def spp_set_timing(ctx, enabled: bool):

@@ -314,3 +314,28 @@ def test_decode_step_matches_per_layer_calls(torch_cuda):
     finally:
         a.close()
         b.close()
+
+
+def test_last_logits_match_the_oracle(torch_cuda):
+    """spp_get_last_logits (the distillation targets) equals the oracle's fp32
+    router logits, and is refused after a batched call that ran the adapter."""
+    from paper_2607_24787_amd import spp
+    for cfg, M in ((RAGGED, -1), (BATCH_BF16, -1)):
+        W = o.OracleWeights(cfg)
+        h0 = gen.hidden_states(cfg, tokens=2)
+        st = _stack(cfg)
+        try:
+            caches = [o.SlotCache(st.S, cfg.n, list(range(min(st.S, cfg.n)))) for _ in range(cfg.L)]
+            st.upload_hidden(h0[0], 0)
+            ref = o.layer_step(cfg, W, 0, h0[0], caches[0], caches[1], 1, M)
+            spp.spp_set_clock(st.ctx, 0)
+            st.layer(0, 0, 1, M)
+            z = spp.spp_get_last_logits(st.ctx, cfg.batch, cfg.n)
+            np.testing.assert_allclose(z, ref.z, rtol=1e-5, atol=1e-6)
+            if cfg.batch > 1:
+                st.layer(0, 0, 1, 2)
+                with pytest.raises(spp.SppError) as e:
+                    spp.spp_get_last_logits(st.ctx, cfg.batch, cfg.n)
+                assert e.value.status == spp.SPP_ESTATE
+        finally:
+            st.close()
