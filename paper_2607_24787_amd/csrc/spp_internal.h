@@ -27,9 +27,9 @@ struct RouterArgs {
   int32_t* topk_host;   // [B, K] host-mapped mirror (device-visible address) or nullptr
   float* gates_host;    // [B, K] host-mapped mirror or nullptr
   float* s_host;        // [n] host-mapped mirror or nullptr
-  unsigned* counter;    // zero between launches
-  unsigned* done_host;  // host-mapped completion flag (device-visible address) or nullptr
-  unsigned seq;         // value written to *done_host once every host mirror is written
+  unsigned* counter;    // [2] zero between launches (router rows, adapter rows)
+  unsigned* done_host;  // [2] host-mapped completion flags (device-visible address) or nullptr
+  unsigned seq;         // written to done_host[0] once topk/gates mirrors are complete, to done_host[1] for s
   int B, D, n, K, r;
   float eps;
   int x_given;          // u holds x (no normalisation)

@@ -22,7 +22,6 @@ namespace {
 constexpr int kWaves = 4;
 constexpr int kThreads = 64 * kWaves;
 constexpr int kBStage = 8192;  // adapter B elements staged in LDS (n * r)
-constexpr int kZStage = 2048;  // logits + adapter hidden units staged per token chunk
 
 template <typename T>
 struct Vec;
@@ -148,9 +147,10 @@ __device__ __forceinline__ uint4 ld_chunk(const void* row, int c) {
 }
 
 // Raw 16-byte chunks of a row in lane layout (zero past the row end).  FULL:
-// the row is exactly 64*NCH chunks, so no lane needs a bounds check.  Past
-// the end a lane re-reads chunk 0 and keeps zero: the loads carry no branch,
-// so all of them are in flight before the first wait.
+// the row is exactly 64*NCH chunks, so no lane needs a bounds check and the
+// loaded data goes through no select (a select forces a wait for its load).
+// Past the end a lane re-reads chunk 0 and keeps zero; the loads carry no
+// branch.
 template <int NCH, bool FULL = false, bool NT = false>
 __device__ __forceinline__ void load_chunks(const void* row, int lane, int nch, uint4 (&r)[NCH]) {
 #pragma unroll
@@ -166,8 +166,8 @@ __device__ __forceinline__ void load_chunks(const void* row, int lane, int nch, 
   }
 }
 
-// fp32 row (V values per chunk of the storage type T) in lane layout.
-template <typename T, int NCH>
+// fp32 row (V values per chunk of the storage type T) in lane layout; FULL as above.
+template <typename T, int NCH, bool FULL = false>
 __device__ __forceinline__ void load_row_f32(const float* src, int lane, int nch, float (&xv)[NCH][Vec<T>::N]) {
   constexpr int V = Vec<T>::N;
   constexpr int Q = V / 4;  // 16-byte fp32 pieces per storage chunk
@@ -175,11 +175,11 @@ __device__ __forceinline__ void load_row_f32(const float* src, int lane, int nch
 #pragma unroll
   for (int j = 0; j < NCH; ++j) {
     const int c = lane + 64 * j;
-    const bool ok = c < nch;
+    const bool ok = FULL || c < nch;
 #pragma unroll
     for (int q = 0; q < Q; ++q) {
       const uint4 v = ld16(src + (ok ? c : 0) * V + 4 * q);  // no branch: all loads go out together
-      r[j][q] = ok ? v : make_uint4(0, 0, 0, 0);
+      r[j][q] = FULL || ok ? v : make_uint4(0, 0, 0, 0);
     }
   }
 #pragma unroll
@@ -188,10 +188,10 @@ __device__ __forceinline__ void load_row_f32(const float* src, int lane, int nch
     for (int q = 0; q < Q; ++q) unpack<float>(r[j][q], &xv[j][4 * q]);
 }
 
-template <typename T, int NCH>
+template <typename T, int NCH, bool FULL = false>
 __device__ __forceinline__ void load_row_storage(const T* src, int lane, int nch, float (&xv)[NCH][Vec<T>::N]) {
   uint4 r[NCH];
-  load_chunks<NCH>(src, lane, nch, r);
+  load_chunks<NCH, FULL>(src, lane, nch, r);
 #pragma unroll
   for (int j = 0; j < NCH; ++j) unpack<T>(r[j], xv[j]);
 }
@@ -209,49 +209,90 @@ __device__ __forceinline__ float rms_scale(float (&xv)[NCH][Vec<T>::N], int D, f
 
 constexpr int kEQ = kMaxExpertsTopK / kThreads;  // experts per thread in the tails
 
-// Completion signal for the host: every thread's host-mirror writes are made
-// visible system-wide, then one thread stores the launch's sequence number
-// into the host-mapped flag.  Called by every thread of the last workgroup.
-__device__ __forceinline__ void signal_done(const RouterArgs& a, int tid) {
-  if (!a.done_host) return;
-  __builtin_amdgcn_fence(__ATOMIC_RELEASE, "");
-  __syncthreads();
-  if (tid == 0) __hip_atomic_store(a.done_host, a.seq, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_SYSTEM);
+// Host handoff.  The host mirrors are written with system-scope atomic stores,
+// which the GPU's caches do not hold back, and cross-workgroup values with
+// agent-scope atomic stores and loads.  For such stores, waiting until the
+// wave's own outstanding memory operations have completed is the whole of a
+// release: a store issued after the wait (a counter increment, a flag) is seen
+// only after them.  This avoids the L2 write-back that a release fence adds
+// for ordinary stores.
+__device__ __forceinline__ void st_system(float* p, float v) {
+  __hip_atomic_store(p, v, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_SYSTEM);
+}
+__device__ __forceinline__ void st_system(int32_t* p, int32_t v) {
+  __hip_atomic_store(p, v, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_SYSTEM);
+}
+__device__ __forceinline__ void wait_own_stores() { asm volatile("s_waitcnt vmcnt(0)" ::: "memory"); }
+
+// Completion flags, one lane, after wait_own_stores in every wave that wrote
+// host mirrors: word 0 = the launch's routing results (topk, gates of every
+// token), word 1 = its priorities s.
+__device__ __forceinline__ void raise_flag(const RouterArgs& a, int word) {
+  __hip_atomic_store(a.done_host + word, a.seq, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_SYSTEM);
 }
 
-// Top-K of one token's logits zb (LDS, n values) by rank counting -- expert e
-// takes position rank(e) = #{e' beating e}, where e' beats e iff z_e' > z_e, or
-// z_e' == z_e and e' < e -- then its combine weights (softmax over all n
-// renormalised over the K selected = softmax over the selected).  Writes token
-// b's outputs.  Every thread of the workgroup calls it.
-__device__ __forceinline__ void select_token(const RouterArgs& a, const float* zb, int b, int tid, float* s_zsel,
-                                             int* s_isel) {
+// Order-preserving key of (logit z, expert e): key(e') > key(e) exactly when e'
+// beats e under the Top-K rule -- a larger logit, or an equal logit and a lower
+// index.  -0 is folded into +0 first, so the two stay equal as in a float
+// comparison.
+__device__ __forceinline__ uint64_t topk_key(float z, int e) {
+  uint32_t u = __float_as_uint(z);
+  if (u == 0x80000000u) u = 0u;
+  u = (u & 0x80000000u) ? ~u : (u | 0x80000000u);
+  return (static_cast<uint64_t>(u) << 32) | (0xFFFFFFFFu - static_cast<uint32_t>(e));
+}
+__device__ __forceinline__ float key_logit(uint64_t k) {
+  const uint32_t u = static_cast<uint32_t>(k >> 32);
+  return __uint_as_float((u & 0x80000000u) ? (u & 0x7FFFFFFFu) : ~u);
+}
+
+// Top-K of one token by rank counting over its keys (LDS, n values): expert e
+// takes position rank(e) = #{e' : key(e') > key(e)} (the keys are distinct, so
+// the ranks are a permutation).  With n <= 128 two threads share an expert,
+// each counting over half of the candidates.  Wave 0 then forms the combine
+// weights (softmax over all n renormalised over the K selected = softmax over
+// the selected) and writes token b's outputs, the host mirrors included.
+// Every thread of the workgroup calls it.
+__device__ __forceinline__ void select_topk(const RouterArgs& a, const uint64_t* s_key, int b, int tid, int* s_rk,
+                                            float* s_zsel, int* s_isel) {
   const int n = a.n;
-  for (int e = tid; e < n; e += kThreads) {
-    const float v = zb[e];
+  const int P = n <= kThreads / 2 ? 2 : 1;
+  const int E = kThreads / P;
+  const int part = tid / E, el = tid - part * E;
+  const int span = (n + P - 1) / P;
+  const int j0 = part * span, j1 = min(n, j0 + span);
+  for (int e0 = 0; e0 < n; e0 += E) {
+    const int e = e0 + el;
+    const uint64_t ke = s_key[min(e, n - 1)];
     int rank = 0;
 #pragma unroll 8
-    for (int j = 0; j < n; ++j) {
-      const float u = zb[j];
-      rank += (u > v || (u == v && j < e)) ? 1 : 0;
+    for (int j = j0; j < j1; ++j) rank += s_key[j] > ke ? 1 : 0;
+    if (P == 2) {  // one pass: E >= n
+      s_rk[tid] = rank;
+      __syncthreads();
+      if (part == 0) rank += s_rk[tid + E];
     }
-    if (rank < a.K) {
+    if (part == 0 && e < n && rank < a.K) {
       s_isel[rank] = e;
-      s_zsel[rank] = v;
+      s_zsel[rank] = key_logit(ke);
     }
   }
   __syncthreads();
-  if (tid < a.K) {
+  if (tid < 64) {
+    const bool on = tid < a.K;
     const float m = s_zsel[0];
-    float sum = 0.f;
-    for (int k = 0; k < a.K; ++k) sum += expf(s_zsel[k] - m);
-    const int idx = b * a.K + tid;
-    const float gk = expf(s_zsel[tid] - m) / sum;
-    a.topk[idx] = s_isel[tid];
-    a.gates[idx] = gk;
-    if (a.topk_host) {
-      a.topk_host[idx] = s_isel[tid];
-      a.gates_host[idx] = gk;
+    const float v = on ? expf(s_zsel[on ? tid : 0] - m) : 0.f;
+    const float sum = wave_sum(v);
+    if (on) {
+      const int idx = b * a.K + tid;
+      const int e = s_isel[tid];
+      const float gk = v / sum;
+      a.topk[idx] = e;
+      a.gates[idx] = gk;
+      if (a.topk_host) {
+        st_system(a.topk_host + idx, e);
+        st_system(a.gates_host + idx, gk);
+      }
     }
   }
 }
@@ -303,21 +344,28 @@ __device__ __forceinline__ void adapter_token(const RouterArgs& a, const float* 
   for (int q = 0; q < kEQ; ++q) pi[q] /= sum;
 }
 
-// Adapter B, transposed into LDS ([r][n]); the loads are issued by the caller
-// (load_B_chunks) before its first barrier.
+// The token's input row (always a valid address).
+__device__ __forceinline__ const void* input_row(const RouterArgs& a) {
+  return a.u ? static_cast<const void*>(a.u) : a.h;
+}
+
+// Adapter B, transposed into LDS ([r][n]); the loads are issued early by the
+// caller and stored after its first wait.  The loads carry no branch: a chunk
+// past the end (or every chunk, when B is not wanted) re-reads the first 16
+// bytes of B (or of the input row) and is never stored.
 template <typename T>
 struct BStage {
   static constexpr int VB = Vec<T>::N;
   static constexpr int kLoads = kBStage / VB / kThreads;  // 16-byte chunks per thread
   uint4 rb[kLoads];
   int nchunk = 0;
-  __device__ __forceinline__ void load(const RouterArgs& a, int tid, bool staged) {
-    nchunk = staged ? (a.n * a.r) / VB : 0;  // n*r*sizeof(T) is a multiple of 16 (checked at launch)
+  __device__ __forceinline__ void load(const RouterArgs& a, int tid, bool want) {
+    nchunk = want ? (a.n * a.r) / VB : 0;  // n*r*sizeof(T) is a multiple of 16 (checked at launch)
+    const uint8_t* src = static_cast<const uint8_t*>(want ? a.Bm : input_row(a));
 #pragma unroll
     for (int q = 0; q < kLoads; ++q) {
       const int c = tid + q * kThreads;
-      rb[q] = c < nchunk ? ld16(reinterpret_cast<const T*>(a.Bm) + static_cast<size_t>(c) * VB)
-                         : make_uint4(0, 0, 0, 0);
+      rb[q] = ld16(src + static_cast<size_t>(c < nchunk ? c : 0) * 16);  // store() reads only c < nchunk
     }
   }
   __device__ __forceinline__ void store(const RouterArgs& a, int tid, float* s_B) const {
@@ -339,140 +387,133 @@ struct BStage {
 };
 
 // ---------------------------------------------------------------------------
-// Router logits, adapter hidden units, then (last workgroup) Top-K, gates and
-// adapter priorities.  One wave per weight row.
+// Router for one token, one launch.  Workgroups [0, gr) hold the router rows,
+// the rest the adapter-A rows, one wave per weight row.  Each kind hands off
+// in a single pass: the last router workgroup to finish selects the Top-K and
+// gates, the last adapter workgroup forms the adapter distribution -- the two
+// tails run at the same time on different compute units.  Adapter workgroups
+// fetch B together with their rows, so the scoring tail starts with B in
+// registers.
 // ---------------------------------------------------------------------------
-template <typename T, int NCH>
+template <typename T, int NCH, bool FULL>
 __global__ __launch_bounds__(kThreads) void router_adapter_kernel(RouterArgs a) {
   constexpr int V = Vec<T>::N;
   const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
-  const int D = a.D, nch = D / V, n = a.n, r = a.r, ldz = a.n + a.r;
+  const int D = a.D, nch = D / V, n = a.n, r = a.r;
   const int nr = a.router_on ? n : 0;
   const int na = a.A ? r : 0;
-  const int row = blockIdx.x * kWaves + wave;
+  const int gr = (nr + kWaves - 1) / kWaves;
+  const bool adapter_wg = static_cast<int>(blockIdx.x) >= gr;
+  const int row = (adapter_wg ? static_cast<int>(blockIdx.x) - gr : static_cast<int>(blockIdx.x)) * kWaves + wave;
 
   __shared__ int s_last;
   __shared__ float s_zsel[32];
   __shared__ int s_isel[32];
   __shared__ float s_red[kWaves];
+  __shared__ int s_rk[kThreads];
   __shared__ float s_a[256];
+  __shared__ uint64_t s_key[kMaxExpertsTopK];
   __shared__ float s_B[kBStage];  // adapter B transposed ([r][n]) when n*r fits
-  __shared__ float s_zall[kZStage];  // logits | adapter hidden units of a chunk of tokens
 
-  const T* wrow = nullptr;
-  int zcol = 0;
-  if (row < nr) {
-    wrow = reinterpret_cast<const T*>(a.Wr) + static_cast<size_t>(row) * D;
-    zcol = row;
-  } else if (row < nr + na) {
-    wrow = reinterpret_cast<const T*>(a.A) + static_cast<size_t>(row - nr) * D;
-    zcol = n + (row - nr);
-  }
+  // a wave past its kind's last row re-reads that row (a valid address) and drops it
+  const int rows = adapter_wg ? na : nr;
+  const bool has_row = row < rows;
+  const T* wrow = reinterpret_cast<const T*>(adapter_wg ? a.A : a.Wr) + static_cast<size_t>(min(row, rows - 1)) * D;
+  const int zcol = adapter_wg ? n + row : row;
   uint4 w[NCH];
-  load_chunks<NCH>(wrow ? wrow : reinterpret_cast<const T*>(a.Wr), lane, wrow ? nch : 0, w);
+  load_chunks<NCH, FULL>(wrow, lane, has_row ? nch : 0, w);
+  const bool staged = na && n * r <= kBStage;
+  BStage<T> bst;
+  bst.load(a, tid, adapter_wg && staged);
 
-  for (int b = 0; b < a.B; ++b) {
-    float xv[NCH][V];
-    if (a.u) {
-      load_row_f32<T, NCH>(a.u + static_cast<size_t>(b) * D, lane, nch, xv);
-    } else {
-      load_row_storage<T, NCH>(reinterpret_cast<const T*>(a.h) + static_cast<size_t>(b) * D, lane, nch, xv);
-    }
-    if (!a.x_given) {
-      const float inv = rms_scale<T, NCH>(xv, D, a.eps);
+  float xv[NCH][V];
+  if (a.u) {
+    load_row_f32<T, NCH, FULL>(a.u, lane, nch, xv);
+  } else {
+    load_row_storage<T, NCH, FULL>(reinterpret_cast<const T*>(a.h), lane, nch, xv);
+  }
+  if (!a.x_given) {
+    const float inv = rms_scale<T, NCH>(xv, D, a.eps);
 #pragma unroll
-      for (int j = 0; j < NCH; ++j)
+    for (int j = 0; j < NCH; ++j)
 #pragma unroll
-        for (int v = 0; v < V; ++v) xv[j][v] *= inv;
-    }
-    if (blockIdx.x == 0 && wave == 0 && a.x_out) {
+      for (int v = 0; v < V; ++v) xv[j][v] *= inv;
+  }
+  if (blockIdx.x == 0 && wave == 0 && a.x_out) {
 #pragma unroll
-      for (int j = 0; j < NCH; ++j) {
-        const int c = lane + 64 * j;
-        if (c < nch) {
-          float* dst = a.x_out + static_cast<size_t>(b) * D + c * V;
+    for (int j = 0; j < NCH; ++j) {
+      const int c = lane + 64 * j;
+      if (c < nch) {
+        float* dst = a.x_out + c * V;
 #pragma unroll
-          for (int v = 0; v < V; ++v) dst[v] = xv[j][v];
-        }
+        for (int v = 0; v < V; ++v) dst[v] = xv[j][v];
       }
-    }
-    if (wrow) {
-      float acc = 0.f;
-#pragma unroll
-      for (int j = 0; j < NCH; ++j) {
-        float wf[V];
-        unpack<T>(w[j], wf);
-#pragma unroll
-        for (int v = 0; v < V; ++v) acc += wf[v] * xv[j][v];
-      }
-      acc = wave_sum(acc);
-      if (lane == 0) st_agent(a.zbuf + static_cast<size_t>(b) * ldz + zcol, acc);
     }
   }
+  if (has_row) {
+    float acc = 0.f;
+#pragma unroll
+    for (int j = 0; j < NCH; ++j) {
+      float wf[V];
+      unpack<T>(w[j], wf);
+#pragma unroll
+      for (int v = 0; v < V; ++v) acc += wf[v] * xv[j][v];
+    }
+    acc = wave_sum(acc);
+    if (lane == 0) st_agent(a.zbuf + zcol, acc);
+  }
 
-  // single-pass handoff: the last workgroup to finish does the selection
-  __builtin_amdgcn_fence(__ATOMIC_RELEASE, "agent");  // release this workgroup's results
+  wait_own_stores();  // release this wave's value
   __syncthreads();
   if (tid == 0) {
-    const unsigned prev = __hip_atomic_fetch_add(a.counter, 1u, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
-    s_last = (prev == gridDim.x - 1);
+    const int kind = adapter_wg ? 1 : 0;
+    const unsigned total = adapter_wg ? gridDim.x - gr : gr;
+    const unsigned prev = __hip_atomic_fetch_add(a.counter + kind, 1u, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
+    s_last = (prev == total - 1);
   }
   __syncthreads();
   if (!s_last) return;
-  __builtin_amdgcn_fence(__ATOMIC_ACQUIRE, "agent");
 
-  // Every load of the tail is issued before the first barrier: adapter B (staged
-  // transposed in LDS when it fits) and the logits / adapter hidden units of a
-  // chunk of tokens.
-  const bool staged = na && n * r <= kBStage;
-  BStage<T> bst;
-  bst.load(a, tid, staged);
-  float sacc[kEQ];
+  if (!adapter_wg) {
+    // Top-K and gates over the n logits (agent-scope loads: other workgroups wrote them)
+    float z[kEQ];
 #pragma unroll
-  for (int q = 0; q < kEQ; ++q) sacc[q] = 0.f;
-  static_assert(kZStage >= kMaxExpertsTopK + 256, "one token's logits and hidden units fit the stage");
-  const int bchunk = kZStage / ldz;
-  for (int b0 = 0; b0 < a.B; b0 += bchunk) {
-    const int nb = min(bchunk, a.B - b0);
-    const int cnt = nb * ldz;
-    float zr[kZStage / kThreads];
-#pragma unroll
-    for (int q = 0; q < kZStage / kThreads; ++q) {
-      const int idx = tid + q * kThreads;
-      zr[q] = idx < cnt ? ld_agent(a.zbuf + static_cast<size_t>(b0) * ldz + idx) : 0.f;
-    }
-    __syncthreads();  // previous chunk is done with s_zall
-    if (b0 == 0) bst.store(a, tid, s_B);
-#pragma unroll
-    for (int q = 0; q < kZStage / kThreads; ++q) {
-      const int idx = tid + q * kThreads;
-      if (idx < cnt) s_zall[idx] = zr[q];
-    }
-    __syncthreads();
-    for (int bb = 0; bb < nb; ++bb) {
-      const float* zb = s_zall + bb * ldz;
-      if (a.router_on) select_token(a, zb, b0 + bb, tid, s_zsel, s_isel);
-      if (na) {
-        float pi[kEQ];
-        adapter_token<T>(a, zb + n, staged, s_B, tid, lane, wave, s_red, pi);
-#pragma unroll
-        for (int q = 0; q < kEQ; ++q) sacc[q] += pi[q];
-      }
-      __syncthreads();  // s_isel / s_red are reused by the next token
-    }
-  }
-  if (na) {
+    for (int q = 0; q < kEQ; ++q) z[q] = ld_agent(a.zbuf + min(tid + kThreads * q, n - 1));
 #pragma unroll
     for (int q = 0; q < kEQ; ++q) {
       const int e = tid + kThreads * q;
-      if (e < n) {
-        a.s[e] = sacc[q];
-        if (a.s_host) a.s_host[e] = sacc[q];
-      }
+      if (e < n) s_key[e] = topk_key(z[q], e);
+    }
+    __syncthreads();
+    select_topk(a, s_key, 0, tid, s_rk, s_zsel, s_isel);
+    if (tid == 0) __hip_atomic_store(a.counter, 0u, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
+    if (a.done_host && tid < 64) {  // wave 0 wrote the mirrors
+      wait_own_stores();
+      if (tid == 0) raise_flag(a, 0);
+    }
+    return;
+  }
+
+  // adapter distribution pi_hat = softmax(B a) over the r hidden units
+  if (tid < na) s_a[tid] = ld_agent(a.zbuf + n + tid);
+  bst.store(a, tid, s_B);
+  __syncthreads();
+  float pi[kEQ];
+  adapter_token<T>(a, s_a, staged, s_B, tid, lane, wave, s_red, pi);
+#pragma unroll
+  for (int q = 0; q < kEQ; ++q) {
+    const int e = tid + kThreads * q;
+    if (e < n) {
+      a.s[e] = pi[q];
+      if (a.s_host) st_system(a.s_host + e, pi[q]);
     }
   }
-  if (tid == 0) __hip_atomic_store(a.counter, 0u, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
-  signal_done(a, tid);
+  if (tid == 0) __hip_atomic_store(a.counter + 1, 0u, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
+  if (a.done_host) {
+    wait_own_stores();
+    __syncthreads();
+    if (tid == 0) raise_flag(a, 1);
+  }
 }
 
 // ---------------------------------------------------------------------------
@@ -485,7 +526,7 @@ __global__ __launch_bounds__(kThreads) void router_adapter_kernel(RouterArgs a) 
 // ---------------------------------------------------------------------------
 constexpr int kRowTok = 8;
 
-template <typename T, int NCH>
+template <typename T, int NCH, bool FULL>
 __global__ __launch_bounds__(kThreads) void router_rows_kernel(RouterArgs a) {
   constexpr int V = Vec<T>::N;
   const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
@@ -503,14 +544,25 @@ __global__ __launch_bounds__(kThreads) void router_rows_kernel(RouterArgs a) {
     zcol = n + (row - nr);
   }
   uint4 w[NCH];
-  load_chunks<NCH>(wrow ? wrow : reinterpret_cast<const T*>(a.Wr), lane, wrow ? nch : 0, w);
-  const int b1 = min(a.B, static_cast<int>(blockIdx.y + 1) * kRowTok);
-  for (int b = blockIdx.y * kRowTok; b < b1; ++b) {
-    float xv[NCH][V];
-    if (a.u) {
-      load_row_f32<T, NCH>(a.u + static_cast<size_t>(b) * D, lane, nch, xv);
-    } else {
-      load_row_storage<T, NCH>(reinterpret_cast<const T*>(a.h) + static_cast<size_t>(b) * D, lane, nch, xv);
+  // a wave past the last row re-reads the token's input row (a valid address) and drops it
+  load_chunks<NCH, FULL>(wrow ? static_cast<const void*>(wrow) : input_row(a), lane, wrow ? nch : 0, w);
+  const int b0 = blockIdx.y * kRowTok;
+  const int b1 = min(a.B, b0 + kRowTok);
+  // the first token's row goes out with the weight row: the unpacked weights
+  // are hoisted out of the token loop, which waits for them
+  float xv[NCH][V];
+  if (a.u) {
+    load_row_f32<T, NCH, FULL>(a.u + static_cast<size_t>(b0) * D, lane, nch, xv);
+  } else {
+    load_row_storage<T, NCH, FULL>(reinterpret_cast<const T*>(a.h) + static_cast<size_t>(b0) * D, lane, nch, xv);
+  }
+  for (int b = b0; b < b1; ++b) {
+    if (b > b0) {
+      if (a.u) {
+        load_row_f32<T, NCH, FULL>(a.u + static_cast<size_t>(b) * D, lane, nch, xv);
+      } else {
+        load_row_storage<T, NCH, FULL>(reinterpret_cast<const T*>(a.h) + static_cast<size_t>(b) * D, lane, nch, xv);
+      }
     }
     if (!a.x_given) {
       const float inv = rms_scale<T, NCH>(xv, D, a.eps);
@@ -552,24 +604,35 @@ __global__ __launch_bounds__(kThreads) void router_select_kernel(RouterArgs a) {
   const int na = a.A ? r : 0;
   const int b = blockIdx.x;
   __shared__ int s_last;
-  __shared__ float s_row[kMaxExpertsTopK + 256];
   __shared__ float s_zsel[32];
   __shared__ int s_isel[32];
   __shared__ float s_red[kWaves];
+  __shared__ int s_rk[kThreads];
+  __shared__ float s_a[256];
+  __shared__ uint64_t s_key[kMaxExpertsTopK];
   __shared__ float s_B[kBStage];
 
   const bool staged = na && n * r <= kBStage;
   BStage<T> bst;
   bst.load(a, tid, staged);
-  float* zrow = a.zbuf + static_cast<size_t>(b) * ldz;
-  for (int e = tid; e < ldz; e += kThreads) s_row[e] = zrow[e];   // written by the rows launch
+  float* zrow = a.zbuf + static_cast<size_t>(b) * ldz;  // written by the rows launch
+  float z[kEQ];
+#pragma unroll
+  for (int q = 0; q < kEQ; ++q) z[q] = zrow[min(tid + kThreads * q, n - 1)];
+  const float hid = zrow[n + min(tid, max(na - 1, 0))];
+#pragma unroll
+  for (int q = 0; q < kEQ; ++q) {
+    const int e = tid + kThreads * q;
+    if (e < n) s_key[e] = topk_key(z[q], e);
+  }
+  if (tid < na) s_a[tid] = hid;
   bst.store(a, tid, s_B);
   __syncthreads();
-  if (a.router_on) select_token(a, s_row, b, tid, s_zsel, s_isel);
+  if (a.router_on) select_topk(a, s_key, b, tid, s_rk, s_zsel, s_isel);
   if (!na && !a.done_host) return;
   if (na) {
     float pi[kEQ];
-    adapter_token<T>(a, s_row + n, staged, s_B, tid, lane, wave, s_red, pi);
+    adapter_token<T>(a, s_a, staged, s_B, tid, lane, wave, s_red, pi);
     // this token's distribution replaces its logits in zbuf (only this workgroup touches row b)
 #pragma unroll
     for (int q = 0; q < kEQ; ++q) {
@@ -577,11 +640,7 @@ __global__ __launch_bounds__(kThreads) void router_select_kernel(RouterArgs a) {
       if (e < n) st_agent(zrow + e, pi[q]);
     }
   }
-  // release this token's results; system scope when the host reads the mirrors
-  if (a.done_host)
-    __builtin_amdgcn_fence(__ATOMIC_RELEASE, "");
-  else
-    __builtin_amdgcn_fence(__ATOMIC_RELEASE, "agent");
+  wait_own_stores();  // release this token's distribution and host mirrors
   __syncthreads();
   if (tid == 0) {
     const unsigned prev = __hip_atomic_fetch_add(a.counter, 1u, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
@@ -589,17 +648,31 @@ __global__ __launch_bounds__(kThreads) void router_select_kernel(RouterArgs a) {
   }
   __syncthreads();
   if (!s_last) return;
-  __builtin_amdgcn_fence(__ATOMIC_ACQUIRE, "agent");
+  if (a.done_host && a.router_on && tid == 0) raise_flag(a, 0);  // every token's mirrors have completed
   if (na) {
+    // s = sum over the tokens, in token order, of their distributions; the
+    // loads go out 16 tokens at a time
+    constexpr int kTB = 16;
     for (int e = tid; e < n; e += kThreads) {
       float acc = 0.f;
-      for (int bb = 0; bb < a.B; ++bb) acc += ld_agent(a.zbuf + static_cast<size_t>(bb) * ldz + e);
+      for (int b0 = 0; b0 < a.B; b0 += kTB) {
+        float v[kTB];
+#pragma unroll
+        for (int q = 0; q < kTB; ++q) v[q] = ld_agent(a.zbuf + static_cast<size_t>(min(b0 + q, a.B - 1)) * ldz + e);
+#pragma unroll
+        for (int q = 0; q < kTB; ++q)
+          if (b0 + q < a.B) acc += v[q];
+      }
       a.s[e] = acc;
-      if (a.s_host) a.s_host[e] = acc;
+      if (a.s_host) st_system(a.s_host + e, acc);
     }
   }
   if (tid == 0) __hip_atomic_store(a.counter, 0u, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
-  signal_done(a, tid);
+  if (na && a.done_host) {
+    wait_own_stores();
+    __syncthreads();
+    if (tid == 0) raise_flag(a, 1);
+  }
 }
 
 // ---------------------------------------------------------------------------
@@ -638,7 +711,7 @@ __global__ __launch_bounds__(kFfnThreads) void ffn_units_kernel(FfnArgs a) {
   // unit's loads, and the math of the first units overlaps the arrival of
   // the later ones
   float xv[NCH][V];
-  load_row_f32<T, NCH>(a.x, lane, nch, xv);
+  load_row_f32<T, NCH, FULL>(a.x, lane, nch, xv);
   __builtin_amdgcn_sched_barrier(0);
 
   const int total = a.nW * I;
@@ -1202,7 +1275,7 @@ __global__ __launch_bounds__(256) void ffn_combine_batched_kernel(CombineBArgs a
 }
 
 // Stand-in projection prologue: u = h + P rms(h) (fp32 result).  One wave per row of P.
-template <typename T, int NCH>
+template <typename T, int NCH, bool FULL>
 __global__ __launch_bounds__(kThreads) void proj_kernel(ProjArgs a) {
   constexpr int V = Vec<T>::N;
   const int lane = threadIdx.x & 63, wave = threadIdx.x >> 6;
@@ -1211,11 +1284,21 @@ __global__ __launch_bounds__(kThreads) void proj_kernel(ProjArgs a) {
   if (row >= D) return;
   const T* prow = reinterpret_cast<const T*>(a.P) + static_cast<size_t>(row) * D;
   uint4 w[NCH];
-  load_chunks<NCH>(prow, lane, nch, w);
+  load_chunks<NCH, FULL>(prow, lane, nch, w);
+  // the first token's row and residual go out with the weight row: the
+  // unpacked weights are hoisted out of the token loop, which waits for them
+  uint4 hr[NCH];
+  load_chunks<NCH, FULL>(a.h, lane, nch, hr);
+  float res = load_elem<T>(a.h, row);
   for (int b = 0; b < a.B; ++b) {
     const T* hb = reinterpret_cast<const T*>(a.h) + static_cast<size_t>(b) * D;
+    if (b > 0) {
+      load_chunks<NCH, FULL>(hb, lane, nch, hr);
+      res = load_elem<T>(hb, row);
+    }
     float xv[NCH][V];
-    load_row_storage<T, NCH>(hb, lane, nch, xv);
+#pragma unroll
+    for (int j = 0; j < NCH; ++j) unpack<T>(hr[j], xv[j]);
     const float inv = rms_scale<T, NCH>(xv, D, a.eps);
     float acc = 0.f;
 #pragma unroll
@@ -1226,7 +1309,7 @@ __global__ __launch_bounds__(kThreads) void proj_kernel(ProjArgs a) {
       for (int v = 0; v < V; ++v) acc += wf[v] * (xv[j][v] * inv);
     }
     acc = wave_sum(acc);
-    if (lane == 0) a.u[static_cast<size_t>(b) * D + row] = load_elem<T>(hb, row) + acc;
+    if (lane == 0) a.u[static_cast<size_t>(b) * D + row] = res + acc;
   }
 }
 
@@ -1315,24 +1398,38 @@ int nch_for(int D) {
     default: return hipErrorInvalidValue;                    \
   }
 
+// FULL: D fills every lane's chunks (D / elements-per-chunk a multiple of 64)
 template <typename T>
-hipError_t router_t(const RouterArgs& a, hipStream_t st) {
+bool full_rows(int D) {
+  return (D / Vec<T>::N) % 64 == 0;
+}
+
+template <typename T, bool FULL>
+hipError_t router_tf(const RouterArgs& a, hipStream_t st) {
   const int rows = (a.router_on ? a.n : 0) + (a.A ? a.r : 0);
   if (rows <= 0) return hipErrorInvalidValue;
   // the staged adapter path reads B in 16-byte chunks
   if (a.A && (static_cast<size_t>(a.n) * a.r * sizeof(T)) % 16 != 0) return hipErrorInvalidValue;
   const int grid = (rows + kWaves - 1) / kWaves;
   if (a.B == 1) {
-    SPP_DISPATCH_NCH(nch_for<T>(a.D),
-                     hipLaunchKernelGGL((router_adapter_kernel<T, NCH>), dim3(grid), dim3(kThreads), 0, st, a));
+    // router rows and adapter rows in workgroups of their own
+    const int g1 = ((a.router_on ? a.n : 0) + kWaves - 1) / kWaves + ((a.A ? a.r : 0) + kWaves - 1) / kWaves;
+    SPP_DISPATCH_NCH(nch_for<T>(a.D), hipLaunchKernelGGL((router_adapter_kernel<T, NCH, FULL>), dim3(g1),
+                                                         dim3(kThreads), 0, st, a));
     return hipGetLastError();
   }
   const dim3 g2(grid, (a.B + kRowTok - 1) / kRowTok);
-  SPP_DISPATCH_NCH(nch_for<T>(a.D), hipLaunchKernelGGL((router_rows_kernel<T, NCH>), g2, dim3(kThreads), 0, st, a));
+  SPP_DISPATCH_NCH(nch_for<T>(a.D),
+                   hipLaunchKernelGGL((router_rows_kernel<T, NCH, FULL>), g2, dim3(kThreads), 0, st, a));
   hipError_t e = hipGetLastError();
   if (e != hipSuccess) return e;
   hipLaunchKernelGGL((router_select_kernel<T>), dim3(a.B), dim3(kThreads), 0, st, a);
   return hipGetLastError();
+}
+
+template <typename T>
+hipError_t router_t(const RouterArgs& a, hipStream_t st) {
+  return full_rows<T>(a.D) ? router_tf<T, true>(a, st) : router_tf<T, false>(a, st);
 }
 
 template <typename T, bool FULL>
@@ -1350,16 +1447,20 @@ hipError_t ffn_tf(const FfnArgs& a, int grid, hipStream_t st, hipEvent_t start, 
 
 template <typename T>
 hipError_t ffn_t(const FfnArgs& a, int grid, hipStream_t st, hipEvent_t start, hipEvent_t stop) {
-  const int nch = a.D / Vec<T>::N;
-  return nch % 64 == 0 ? ffn_tf<T, true>(a, grid, st, start, stop) : ffn_tf<T, false>(a, grid, st, start, stop);
+  return full_rows<T>(a.D) ? ffn_tf<T, true>(a, grid, st, start, stop) : ffn_tf<T, false>(a, grid, st, start, stop);
+}
+
+template <typename T, bool FULL>
+hipError_t proj_tf(const ProjArgs& a, hipStream_t st) {
+  const int grid = (a.D + kWaves - 1) / kWaves;
+  SPP_DISPATCH_NCH(nch_for<T>(a.D),
+                   hipLaunchKernelGGL((proj_kernel<T, NCH, FULL>), dim3(grid), dim3(kThreads), 0, st, a));
+  return hipGetLastError();
 }
 
 template <typename T>
 hipError_t proj_t(const ProjArgs& a, hipStream_t st) {
-  const int grid = (a.D + kWaves - 1) / kWaves;
-  SPP_DISPATCH_NCH(nch_for<T>(a.D),
-                   hipLaunchKernelGGL((proj_kernel<T, NCH>), dim3(grid), dim3(kThreads), 0, st, a));
-  return hipGetLastError();
+  return full_rows<T>(a.D) ? proj_tf<T, true>(a, st) : proj_tf<T, false>(a, st);
 }
 
 int g_ffn_target_wgs = 512;

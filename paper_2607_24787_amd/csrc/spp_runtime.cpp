@@ -395,12 +395,13 @@ uint32_t next_router_seq(spp_ctx* c) {
   return c->router_seq;
 }
 
-// Wait until the router launch tagged `seq` has written its host mirrors: spin
-// on the host-mapped flag its last workgroup stores after a system-scope
-// release.  After about 20 ms of spinning (queued work ahead of the router)
+// Wait until the router launch tagged `seq` has written a part of its host
+// mirrors: flag word 0 covers the routing results (topk, gates), word 1 the
+// priorities s.  The kernel stores the flag once the mirrors' stores have
+// completed.  After about 20 ms of spinning (queued work ahead of the router)
 // the wait blocks on the stream instead; a flag still not set then is an error.
-spp_status wait_router(spp_ctx* c, uint32_t seq) {
-  const uint32_t* flag = reinterpret_cast<const uint32_t*>(c->res_host + c->off_flag);
+spp_status wait_router(spp_ctx* c, uint32_t seq, int word) {
+  const uint32_t* flag = reinterpret_cast<const uint32_t*>(c->res_host + c->off_flag) + word;
   const auto t0 = std::chrono::steady_clock::now();
   for (uint32_t it = 1;; ++it) {
     if (__atomic_load_n(flag, __ATOMIC_ACQUIRE) == seq) return SPP_OK;
@@ -615,7 +616,7 @@ spp_status layer_forward_impl(spp_ctx* c, int32_t l, const void* h_in, void* h_o
   ra.seq = next_router_seq(c);
   SPP_HIP(spp::launch_router(ra, dt, c->compute));
   if (c->timing) SPP_HIP(hipEventRecord(ts.ev[kEvRouted], c->compute));
-  if (spp_status e = wait_router(c, ra.seq)) return e;
+  if (spp_status e = wait_router(c, ra.seq, 0)) return e;
   if (c->timing && c->pending_sets.size() >= 64) harvest(c, c->pending_sets.size());
 
   const int32_t* T = reinterpret_cast<const int32_t*>(c->res_host);
@@ -660,7 +661,17 @@ spp_status layer_forward_impl(spp_ctx* c, int32_t l, const void* h_in, void* h_o
   if (!ls.policy->on_demand(T, BK, tau, &c->last_loads, &rounds, &why)) return fail(SPP_ESTATE, why);
   st.misses = static_cast<int32_t>(c->last_loads.size());
 
-  // prefetch selection for layer l+1 (the copies are enqueued after this layer's loads)
+  {
+    std::vector<spp::Transfer> first;
+    for (const spp::Transfer& t : c->last_loads)
+      if (t.round == 0) first.push_back(t);
+    if (spp_status e = issue_copies(c, ls, first, ls.last_read_valid ? ls.last_read : nullptr, true)) return e;
+  }
+
+  // prefetch selection for layer l+1 (the copies are enqueued after this
+  // layer's loads); the adapter's priorities have their own flag
+  if (adapter_on)
+    if (spp_status e = wait_router(c, ra.seq, 1)) return e;
   LayerState* nx = predict && M_max > 0 ? &c->layers[l + 1] : nullptr;
   c->last_pref.clear();
   c->last_s_valid = predict;
@@ -674,12 +685,6 @@ spp_status layer_forward_impl(spp_ctx* c, int32_t l, const void* h_in, void* h_o
       for (const spp::Transfer& t : c->last_pref) nx->pending_prefetch.push_back(t.expert);
       st.prefetched = static_cast<int32_t>(c->last_pref.size());
     }
-  }
-  {
-    std::vector<spp::Transfer> first;
-    for (const spp::Transfer& t : c->last_loads)
-      if (t.round == 0) first.push_back(t);
-    if (spp_status e = issue_copies(c, ls, first, ls.last_read_valid ? ls.last_read : nullptr, true)) return e;
   }
   if (rounds.size() == 1 && nx)
     if (spp_status e = issue_copies(c, *nx, c->last_pref, nx->last_read_valid ? nx->last_read : nullptr, false))
@@ -947,7 +952,7 @@ spp_status adapter_predict(spp_ctx* c, int32_t l, const float* x_dev, int32_t B,
   ra.done_host = reinterpret_cast<unsigned*>(c->res_host_dev + c->off_flag);
   ra.seq = next_router_seq(c);
   SPP_HIP(spp::launch_router(ra, d.dtype, c->compute));
-  if (spp_status e = wait_router(c, ra.seq)) return e;
+  if (spp_status e = wait_router(c, ra.seq, 1)) return e;
   std::memcpy(s_out, c->res_host + c->off_s, sizeof(float) * d.n);
   return SPP_OK;
 }
