@@ -209,6 +209,9 @@ def main():
     ap.add_argument("--tier-gbps", type=lambda v: [float(x) for x in v.split(",") if x != ""], default=[],
                     help="storage emulation: for each offload-tier bandwidth (GB/s, below the link's), "
                          "time OFF and M_max 1, 2 with every expert copy slowed to it")
+    ap.add_argument("--copy-engine", choices=("split", "kernel", "sdma"), default="split",
+                    help="expert copies: on-demand by the copy kernel and prefetches by the DMA engines "
+                         "(split, default), all by the copy kernel, or all by the DMA engines")
     ap.add_argument("--copy-probe", action="store_true",
                     help="only run a 256 MiB device-to-device copy three times (counter calibration)")
     args = ap.parse_args()
@@ -258,9 +261,19 @@ def main():
         if args.ffn_wgs:
             spp.spp_set_ffn_workgroups(stack.ctx, args.ffn_wgs)
 
+    engines = {"split": spp.COPY_SPLIT, "kernel": spp.COPY_KERNEL, "sdma": spp.COPY_SDMA}
+    engine = engines[args.copy_engine]
+    # per-expert cost on each engine (the budget uses the one of on-demand loads)
+    engine_us = {}
+    for name in ("kernel", "sdma"):
+        spp.spp_set_copy_engine(stack.ctx, engines[name])
+        engine_us[name] = spp.spp_profile_expert_copy(stack.ctx, 0, 32)
+    spp.spp_set_copy_engine(stack.ctx, engine)
     per_expert_us = spp.spp_profile_expert_copy(stack.ctx, 0, 32)
     link_gbs = cfg.blob_bytes / (per_expert_us * 1e3)
-    _log(f"[bench] pinned H2D per expert {per_expert_us:.1f} us = {link_gbs:.2f} GB/s")
+    _log(f"[bench] pinned H2D per expert: copy kernel {engine_us['kernel']:.1f} us "
+         f"({cfg.blob_bytes / (engine_us['kernel'] * 1e3):.2f} GB/s), DMA {engine_us['sdma']:.1f} us "
+         f"({cfg.blob_bytes / (engine_us['sdma'] * 1e3):.2f} GB/s); engine {args.copy_engine}")
 
     on = run_mode(stack, dev_h, row_bytes, args.warmup, args.steps, cfg.window)
     _log(f"[bench] ON  {on['tokens_per_s']:.1f} tok/s coverage={on['next_layer_coverage']:.3f} "
@@ -271,6 +284,16 @@ def main():
             modes[name] = run_mode(stack, dev_h, row_bytes, args.warmup, args.steps, M, naive)
             _log(f"[bench] {name} {modes[name]['tokens_per_s']:.1f} tok/s "
                  f"coverage={modes[name]['next_layer_coverage']:.3f}")
+        # the same SpecPrefetch run with the other copy engines
+        for ename in engines:
+            if ename == args.copy_engine:
+                continue
+            spp.spp_set_copy_engine(stack.ctx, engines[ename])
+            name = f"on_copy_{ename}"
+            modes[name] = run_mode(stack, dev_h, row_bytes, args.warmup, args.steps, cfg.window)
+            _log(f"[bench] {name} {modes[name]['tokens_per_s']:.1f} tok/s "
+                 f"exposed={modes[name]['exposed_transfer_pct']:.1f}% ffn={modes[name]['ffn_kernel_us']:.2f}us")
+        spp.spp_set_copy_engine(stack.ctx, engine)
     for M in args.sweep:
         modes[f"M{M}"] = run_mode(stack, dev_h, row_bytes, args.warmup, args.steps, M)
         _log(f"[bench] sweep M_max={M} {modes[f'M{M}']['tokens_per_s']:.1f} tok/s "
@@ -326,7 +349,9 @@ def main():
         "roofline": {"kernel": kernel + " (routed-expert SwiGLU FFN)", "bound": "hbm",
                      "achieved": achieved, "peak": HBM_PEAK_GBS, "unit": "GB/s", "frac": achieved / HBM_PEAK_GBS,
                      "traffic": traffic, "bytes_per_launch": ffn_bytes, "avg_launch_us": on["ffn_kernel_us"]},
-        "link": {"bound": "host link (pinned H2D)", "per_expert_us": per_expert_us, "peak_gbs_measured": link_gbs,
+        "link": {"bound": "host link (pinned H2D)", "copy_engine": args.copy_engine,
+                 "per_expert_us": per_expert_us, "peak_gbs_measured": link_gbs,
+                 "per_expert_us_by_engine": engine_us,
                  "achieved_gbs_during_run": on["h2d_gbs_during_run"],
                  "frac": (on["h2d_gbs_during_run"] / link_gbs) if on["h2d_gbs_during_run"] else None},
         "window": {"compute_window_us": window_us, "live_window_us": on["window_us"],

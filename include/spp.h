@@ -78,6 +78,7 @@ enum { SPP_DTYPE_F32 = 0, SPP_DTYPE_BF16 = 1 };
 enum { SPP_LAYOUT_UNITS = 0, SPP_LAYOUT_TILED = 1, SPP_LAYOUT_Q4_UNITS = 2 };
 enum { SPP_CODEC_PLAIN = 0, SPP_CODEC_Q4 = 1 };
 enum { SPP_PREFETCH_ADAPTER = 0, SPP_PREFETCH_PREV_TOKEN = 1 };
+enum { SPP_COPY_KERNEL = 0, SPP_COPY_SDMA = 1, SPP_COPY_SPLIT = 2 };
 
 /* Model shape.  Notation of the paper's problem formulation: L MoE layers,
  * n routed experts per layer, top-K routing, router input size D, adapter
@@ -155,8 +156,9 @@ spp_status spp_destroy(spp_ctx* ctx);
  * adapter_b: dev [n,r] (both NULL for the last layer, which has no adapter);
  * proj_w: dev [D,D] or NULL (required iff has_proj); shared_blobs: dev
  * n_shared blobs at blob stride (NULL iff n_shared == 0); host_store: the
- * offload tier, n blobs at blob stride in pinned host memory (hipHostMalloc
- * or a pinned torch tensor), expert e at host_store + e*stride. */
+ * offload tier, n*stride bytes of pinned host memory (hipHostMalloc or a
+ * pinned torch tensor), 16-byte aligned, expert e at host_store + e*stride.  EINVAL if host_store is not pinned (it has no device-visible
+ * address) or not aligned. */
 spp_status spp_bind_layer(spp_ctx* ctx, int32_t l, const void* router_w, const void* adapter_a,
                           const void* adapter_b, const void* proj_w, const void* shared_blobs,
                           const void* host_store);
@@ -272,8 +274,9 @@ spp_status spp_set_timing(spp_ctx* ctx, int32_t enabled);
 spp_status spp_get_run_stats(spp_ctx* ctx, spp_run_stats* out);
 spp_status spp_reset_run_stats(spp_ctx* ctx);
 
-/* Measured host-to-device cost of one expert blob on the copy stream
- * (average over reps copies from layer l's host store into scratch), in us. */
+/* Measured host-to-device cost of one expert blob on a copy stream with the
+ * prefetch engine (average over reps copies from layer l's host store into
+ * scratch), in us: the per-expert cost c of the prefetch budget. */
 spp_status spp_profile_expert_copy(spp_ctx* ctx, int32_t l, int32_t reps, double* per_expert_us);
 
 /* Where moe_layer_forward takes the priorities for the next layer's prefetch
@@ -289,6 +292,22 @@ spp_status spp_set_prefetch_source(spp_ctx* ctx, int32_t source);
  * (expert, unit) work list of one token (default 512; 1..4096).  Applies to
  * every context in the process. */
 spp_status spp_set_ffn_workgroups(spp_ctx* ctx, int32_t wgs);
+
+/* Engine of the expert copies from the offload tier.  A copy kernel reads
+ * the pinned host store through its device-visible address (shader loads over
+ * the host link); the DMA engines copy with hipMemcpyAsync.
+ *   SPP_COPY_SPLIT (default): a layer's on-demand loads are one copy kernel
+ *     (64 workgroups, all its blobs) on the compute stream ahead of the FFN
+ *     that waits for them anyway; prefetches go to the DMA engines on the two
+ *     copy streams, since they overlap compute kernels, which copy waves on
+ *     the same compute units would slow down.
+ *   SPP_COPY_KERNEL: every copy by a copy kernel (32 workgroups per half blob)
+ *     on the copy streams.
+ *   SPP_COPY_SDMA: every copy by the DMA engines on the copy streams.
+ * On the copy streams each blob goes in two halves, one per stream.
+ * spp_profile_expert_copy times the prefetch engine.  EINVAL for an unknown
+ * engine. */
+spp_status spp_set_copy_engine(spp_ctx* ctx, int32_t engine);
 
 /* Storage-speed emulation ("Storage Sensitivity", Figure 5): every expert
  * copy is preceded, on each copy stream, by a bounded busy kernel of about

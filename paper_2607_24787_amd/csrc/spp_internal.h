@@ -99,6 +99,18 @@ hipError_t launch_proj(const ProjArgs& a, int dtype, hipStream_t st);
 // Grouped (batched) routed-expert FFN, bf16 only; D % 256 == 0.
 hipError_t launch_ffn_grouped(const GroupArgs& a, hipStream_t st, hipEvent_t start, hipEvent_t stop);
 hipError_t launch_combine_batched(const CombineBArgs& a, int dtype, hipStream_t st);
+// Host-to-device copies by a copy kernel: n copies of n16 16-byte chunks each,
+// from pinned host memory (its device-visible, 16-byte aligned address) to
+// 16-byte aligned device memory, one after the other in one launch of `wgs`
+// workgroups.
+constexpr int kMaxCopyList = 32;
+struct CopyList {
+  const void* src[kMaxCopyList];
+  void* dst[kMaxCopyList];
+  int32_t n;
+  uint64_t n16;
+};
+hipError_t launch_h2d_copies(const CopyList& list, int wgs, hipStream_t st);
 hipError_t launch_spin(uint64_t ticks, uint32_t max_iter, hipStream_t st);
 int ffn_grid_for(int nunits, int* upw);
 // 4-bit experts: one pass per wave, kFfnWaves * 3 units per workgroup.

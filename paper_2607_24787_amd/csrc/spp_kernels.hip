@@ -1371,6 +1371,23 @@ __global__ __launch_bounds__(64) void proj_mfma_kernel(ProjArgs a) {
 // Bounded busy wait used only by the copy-delay test hook: returns after
 // `ticks` of the constant-rate wall clock or after `max_iter` sleeps, whichever
 // comes first.
+// Host-to-device copies by shader loads: each source is the device-visible
+// address of pinned host memory, each destination device memory, n16 the
+// count of 16-byte chunks of every copy.  Each lane keeps one 16-byte read
+// across the host link in flight per step of a grid-stride loop (a grid of a
+// few dozen workgroups saturates the link), and the copies of the list follow
+// one another without a gap between launches.  Loads and stores are
+// non-temporal: the data is read once here and next by a later kernel, from HBM.
+__global__ __launch_bounds__(256) void h2d_copy_kernel(CopyList a) {
+  const size_t stride = static_cast<size_t>(gridDim.x) * blockDim.x;
+  const size_t i0 = static_cast<size_t>(blockIdx.x) * blockDim.x + threadIdx.x;
+  for (int t = 0; t < a.n; ++t) {
+    const u32x4* src = static_cast<const u32x4*>(a.src[t]);
+    u32x4* dst = static_cast<u32x4*>(a.dst[t]);
+    for (size_t i = i0; i < a.n16; i += stride) __builtin_nontemporal_store(__builtin_nontemporal_load(src + i), dst + i);
+  }
+}
+
 __global__ void spin_kernel(uint64_t ticks, uint32_t max_iter) {
   const uint64_t t0 = wall_clock64();
   for (uint32_t it = 0; it < max_iter; ++it) {
@@ -1532,6 +1549,16 @@ hipError_t launch_combine_batched(const CombineBArgs& a, int dtype, hipStream_t 
     hipLaunchKernelGGL((ffn_combine_batched_kernel<uint16_t>), grid, dim3(256), 0, st, a);
   else
     hipLaunchKernelGGL((ffn_combine_batched_kernel<float>), grid, dim3(256), 0, st, a);
+  return hipGetLastError();
+}
+
+hipError_t launch_h2d_copies(const CopyList& list, int wgs, hipStream_t st) {
+  if (list.n < 0 || list.n > kMaxCopyList || wgs < 1) return hipErrorInvalidValue;
+  for (int t = 0; t < list.n; ++t)
+    if (reinterpret_cast<uintptr_t>(list.src[t]) % 16 != 0 || reinterpret_cast<uintptr_t>(list.dst[t]) % 16 != 0)
+      return hipErrorInvalidValue;
+  if (list.n == 0 || list.n16 == 0) return hipSuccess;
+  hipLaunchKernelGGL(h2d_copy_kernel, dim3(wgs), dim3(256), 0, st, list);
   return hipGetLastError();
 }
 

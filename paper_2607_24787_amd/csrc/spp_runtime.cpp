@@ -55,12 +55,14 @@ struct LayerState {
   const void* proj = nullptr;
   const void* shared = nullptr;
   const uint8_t* host_store = nullptr;
+  const uint8_t* host_store_dev = nullptr;  // its device-visible address (read by the copy kernel)
   uint8_t* slots = nullptr;
   std::unique_ptr<spp::SlotPolicy> policy;
   std::vector<hipEvent_t> slot_ready;  // recorded on the copy stream after a copy into the slot
   std::vector<hipEvent_t> slot_ready2; // the same on the second copy stream
   std::vector<int32_t> slot_event;     // the slot whose slot_ready covers this slot's last copy
   std::vector<char> slot_pending;      // that event may not have been waited on
+  std::vector<char> slot_inline;       // loaded on the compute stream by this call (in order before its FFN)
   hipEvent_t last_read = nullptr;      // recorded on the compute stream after the layer's FFN
   bool last_read_valid = false;
   std::vector<int32_t> pending_prefetch;  // prefetched for this layer, not yet executed
@@ -90,6 +92,7 @@ struct spp_ctx {
   size_t res_bytes = 0, off_gates = 0, off_s = 0, off_flag = 0;
   uint32_t router_seq = 0;  // last sequence number handed to a router launch
   int32_t prefetch_source = SPP_PREFETCH_ADAPTER;
+  int32_t copy_engine = SPP_COPY_SPLIT;
   unsigned* counter = nullptr;
   float* partial = nullptr;    // [ffn_max_grid, D]
   uint8_t* probe_dev = nullptr;  // one blob, for copy profiling
@@ -222,14 +225,31 @@ void harvest(spp_ctx* c, size_t count) {
   c->pending_sets.erase(c->pending_sets.begin(), c->pending_sets.begin() + count);
 }
 
-// Issue host->device copies for transfers into layer `ls`; the copy stream
-// first waits on `war` (the last kernel that read slots being overwritten).
-// Enqueue host-to-device copies on the copy stream.  grouped: the copies are
-// consumed together (one on-demand round), so one event after the last copy
-// covers all of them (the copy stream is in order); otherwise every copy gets
-// its own event (prefetches are consumed one by one).
+// One contiguous part of an expert blob from the offload tier (host offset
+// `src_off`) into device memory, on a copy stream.  The copy kernel moves
+// whole 16-byte chunks: a part is rounded up to 16 bytes, which stays inside
+// the blob stride on both sides (the stride is a multiple of 4 KiB).
+constexpr int kCopyWgs = 32;        // per half blob on a copy stream
+constexpr int kInlineCopyWgs = 64;  // on-demand loads on the compute stream
+hipError_t copy_part(spp_ctx* c, const LayerState& ls, uint8_t* dst, size_t src_off, size_t bytes, hipStream_t st) {
+  if (c->copy_engine != SPP_COPY_KERNEL)
+    return hipMemcpyAsync(dst, ls.host_store + src_off, bytes, hipMemcpyHostToDevice, st);
+  spp::CopyList one{};
+  one.src[0] = ls.host_store_dev + src_off;
+  one.dst[0] = dst;
+  one.n = 1;
+  one.n16 = round_up(bytes, 16) / 16;
+  return spp::launch_h2d_copies(one, kCopyWgs, st);
+}
+
+// Enqueue the copies `xs` into layer `ls`'s slots on the two copy streams
+// (each blob in two halves, one per stream), after `war` (the last kernel
+// that read this layer's slots).  demand: on-demand loads, which the compute
+// stream waits for as a group, so one event after the last copy covers them
+// (the streams are in order); otherwise prefetches, consumed one by one, each
+// with its own event.
 spp_status issue_copies(spp_ctx* c, LayerState& ls, const std::vector<spp::Transfer>& xs, hipEvent_t war,
-                        bool grouped) {
+                        bool demand) {
   if (xs.empty()) return SPP_OK;
   // WAR on slot reuse, unless the last kernel that read this layer already finished
   if (war && hipEventQuery(war) != hipSuccess) {
@@ -243,7 +263,6 @@ spp_status issue_copies(spp_ctx* c, LayerState& ls, const std::vector<spp::Trans
   hipStream_t streams[2] = {c->copy, c->copy2};
   for (const spp::Transfer& t : xs) {
     uint8_t* dst = ls.slots + static_cast<size_t>(t.slot) * c->stride;
-    const uint8_t* src = ls.host_store + static_cast<size_t>(t.expert) * c->stride;
     for (int h = 0; h < 2; ++h) {
       if (part[h] == 0) continue;
       if (c->copy_delay_us > 0) {
@@ -252,18 +271,68 @@ spp_status issue_copies(spp_ctx* c, LayerState& ls, const std::vector<spp::Trans
       }
       const size_t off = h == 0 ? 0 : part[0];
       if (c->poison) SPP_HIP(hipMemsetAsync(dst + off, 0xFF, part[h], streams[h]));
-      SPP_HIP(hipMemcpyAsync(dst + off, src + off, part[h], hipMemcpyHostToDevice, streams[h]));
+      SPP_HIP(copy_part(c, ls, dst + off, static_cast<size_t>(t.expert) * c->stride + off, part[h], streams[h]));
     }
-    if (!grouped || t.slot == last) {
+    if (!demand || t.slot == last) {
       SPP_HIP(hipEventRecord(ls.slot_ready[t.slot], c->copy));
       SPP_HIP(hipEventRecord(ls.slot_ready2[t.slot], c->copy2));
     }
-    ls.slot_event[t.slot] = grouped ? last : t.slot;
+    ls.slot_event[t.slot] = demand ? last : t.slot;
     ls.slot_pending[t.slot] = 1;
     c->stats.copies += 1;
     c->stats.copy_bytes += static_cast<int64_t>(c->blob_bytes);
   }
   return SPP_OK;
+}
+
+// On-demand loads on the compute stream (SPP_COPY_SPLIT): copy-list kernels
+// ahead of the FFN that reads the slots, which the stream order then fences
+// (RAW) as it fences their overwrite after the previous FFN (WAR).  A slot
+// whose earlier copy on the copy streams may still be in flight is waited for
+// first (WAW).
+spp_status issue_inline(spp_ctx* c, LayerState& ls, const std::vector<spp::Transfer>& xs) {
+  if (xs.empty()) return SPP_OK;
+  std::vector<int32_t> waited;
+  for (const spp::Transfer& t : xs) {
+    if (!ls.slot_pending[t.slot]) continue;
+    const int32_t ev = ls.slot_event[t.slot];
+    if (std::find(waited.begin(), waited.end(), ev) == waited.end()) {
+      SPP_HIP(hipStreamWaitEvent(c->compute, ls.slot_ready[ev], 0));
+      SPP_HIP(hipStreamWaitEvent(c->compute, ls.slot_ready2[ev], 0));
+      waited.push_back(ev);
+    }
+    ls.slot_pending[t.slot] = 0;
+  }
+  spp::CopyList list{};
+  list.n16 = round_up(c->blob_bytes, 16) / 16;
+  for (size_t i = 0; i < xs.size(); ++i) {
+    const spp::Transfer& t = xs[i];
+    uint8_t* dst = ls.slots + static_cast<size_t>(t.slot) * c->stride;
+    if (c->copy_delay_us > 0) {
+      const uint64_t ticks = c->wall_khz * static_cast<uint64_t>(c->copy_delay_us) / 1000;
+      SPP_HIP(spp::launch_spin(ticks, static_cast<uint32_t>(c->copy_delay_us) * 64u + 1024u, c->compute));
+    }
+    if (c->poison) SPP_HIP(hipMemsetAsync(dst, 0xFF, c->blob_bytes, c->compute));
+    list.src[list.n] = ls.host_store_dev + static_cast<size_t>(t.expert) * c->stride;
+    list.dst[list.n] = dst;
+    ++list.n;
+    // a delayed copy goes out alone, right after its delay
+    if (list.n == spp::kMaxCopyList || i + 1 == xs.size() || c->copy_delay_us > 0) {
+      SPP_HIP(spp::launch_h2d_copies(list, kInlineCopyWgs, c->compute));
+      list.n = 0;
+    }
+    ls.slot_inline[t.slot] = 1;
+    c->stats.copies += 1;
+    c->stats.copy_bytes += static_cast<int64_t>(c->blob_bytes);
+  }
+  return SPP_OK;
+}
+
+// The on-demand loads of one round: on the compute stream (SPP_COPY_SPLIT) or
+// on the copy streams after `war`.
+spp_status issue_demand(spp_ctx* c, LayerState& ls, const std::vector<spp::Transfer>& xs, hipEvent_t war) {
+  if (c->copy_engine == SPP_COPY_SPLIT) return issue_inline(c, ls, xs);
+  return issue_copies(c, ls, xs, war, true);
 }
 
 spp_status sync_all(spp_ctx* c) {
@@ -278,6 +347,7 @@ spp_status fill_slots(spp_ctx* c, LayerState& ls, const std::vector<int32_t>& be
   const auto& table = ls.policy->slot_experts();
   for (int32_t j = 0; j < c->d.S; ++j) {
     ls.slot_pending[j] = 0;
+    ls.slot_inline[j] = 0;
     if (table[j] == spp::kEmpty || table[j] == before[j]) continue;
     SPP_HIP(hipMemcpy(ls.slots + static_cast<size_t>(j) * c->stride,
                       ls.host_store + static_cast<size_t>(table[j]) * c->stride, c->blob_bytes,
@@ -346,6 +416,7 @@ spp_status create_impl(const spp_model_desc* desc, void* stream, spp_ctx** out) 
     ls.slot_ready.assign(d.S, nullptr);
     ls.slot_ready2.assign(d.S, nullptr);
     ls.slot_pending.assign(d.S, 0);
+    ls.slot_inline.assign(d.S, 0);
     ls.slot_event.resize(d.S);
     for (int32_t j = 0; j < d.S; ++j) ls.slot_event[j] = j;
     for (hipEvent_t& e : ls.slot_ready) SPP_HIP(hipEventCreateWithFlags(&e, hipEventDisableTiming));
@@ -418,6 +489,10 @@ spp_status wait_round(spp_ctx* c, LayerState& ls, const spp::Round& round, spp_l
   std::vector<int32_t> waited;  // each covering event is waited on once
   for (const auto& es : round) {
     const int32_t slot = es.second;
+    if (ls.slot_inline[slot]) {  // fenced by the stream order; not ready when the FFN was enqueued
+      ls.slot_inline[slot] = 0;
+      continue;
+    }
     if (!ls.slot_pending[slot]) {
       st->ready_on_time += 1;
       continue;
@@ -515,9 +590,9 @@ spp_status grouped_ffn(spp_ctx* c, LayerState& ls, LayerState* next, const int32
       std::vector<spp::Transfer> xs;
       for (const spp::Transfer& t : loads)
         if (t.round == static_cast<int32_t>(r)) xs.push_back(t);
-      if (spp_status e = issue_copies(c, ls, xs, done, true)) return e;
       if (c->timing)
         if (spp_status e = record_extra(c, ts)) return e;
+      if (spp_status e = issue_demand(c, ls, xs, done)) return e;
       if (spp_status e = wait_round(c, ls, rounds[r], st)) return e;
       if (c->timing)
         if (spp_status e = record_extra(c, ts)) return e;
@@ -661,11 +736,14 @@ spp_status layer_forward_impl(spp_ctx* c, int32_t l, const void* h_in, void* h_o
   if (!ls.policy->on_demand(T, BK, tau, &c->last_loads, &rounds, &why)) return fail(SPP_ESTATE, why);
   st.misses = static_cast<int32_t>(c->last_loads.size());
 
+  // the compute stream's wait for expert copies starts here (on-demand loads
+  // enqueued on it, or its waits for the copy streams)
+  if (c->timing) SPP_HIP(hipEventRecord(ts.ev[kEvWaitA], c->compute));
   {
     std::vector<spp::Transfer> first;
     for (const spp::Transfer& t : c->last_loads)
       if (t.round == 0) first.push_back(t);
-    if (spp_status e = issue_copies(c, ls, first, ls.last_read_valid ? ls.last_read : nullptr, true)) return e;
+    if (spp_status e = issue_demand(c, ls, first, ls.last_read_valid ? ls.last_read : nullptr)) return e;
   }
 
   // prefetch selection for layer l+1 (the copies are enqueued after this
@@ -691,7 +769,6 @@ spp_status layer_forward_impl(spp_ctx* c, int32_t l, const void* h_in, void* h_o
       return e;
 
   // RAW: the FFN reads each needed slot only after its copy completed
-  if (c->timing) SPP_HIP(hipEventRecord(ts.ev[kEvWaitA], c->compute));
   if (spp_status e = wait_round(c, ls, rounds[0], &st)) return e;
   if (c->timing) SPP_HIP(hipEventRecord(ts.ev[kEvWaitB], c->compute));
   if (batched) {
@@ -855,7 +932,14 @@ spp_status spp_bind_layer(spp_ctx* c, int32_t l, const void* router_w, const voi
   if (adapter_a && (l == d.L - 1 || d.r == 0)) return fail(SPP_EINVAL, "the last layer (or r == 0) has no adapter");
   if ((proj_w != nullptr) != (d.has_proj == 1)) return fail(SPP_EINVAL, "proj_w must be given iff has_proj");
   if ((shared_blobs != nullptr) != (d.n_shared > 0)) return fail(SPP_EINVAL, "shared_blobs must be given iff n_shared > 0");
+  if (reinterpret_cast<uintptr_t>(host_store) % 16 != 0) return fail(SPP_EINVAL, "host_store must be 16-byte aligned");
+  void* store_dev = nullptr;
+  if (hipHostGetDevicePointer(&store_dev, const_cast<void*>(host_store), 0) != hipSuccess || !store_dev) {
+    (void)hipGetLastError();
+    return fail(SPP_EINVAL, "host_store is not pinned host memory");
+  }
   LayerState& ls = c->layers[l];
+  ls.host_store_dev = static_cast<const uint8_t*>(store_dev);
   ls.router_w = router_w;
   ls.A = adapter_a;
   ls.Bm = adapter_b;
@@ -879,6 +963,14 @@ spp_status spp_set_resident(spp_ctx* c, int32_t l, const int32_t* experts, int32
   ls.prev_T.clear();  // a new decode sequence: no preceding step
   ls.prev_g.clear();
   return fill_slots(c, ls, before);
+}
+
+spp_status spp_set_copy_engine(spp_ctx* c, int32_t engine) {
+  if (spp_status s = check_ctx(c)) return s;
+  if (engine != SPP_COPY_KERNEL && engine != SPP_COPY_SDMA && engine != SPP_COPY_SPLIT)
+    return fail(SPP_EINVAL, "engine must be SPP_COPY_KERNEL, SPP_COPY_SDMA or SPP_COPY_SPLIT");
+  c->copy_engine = engine;
+  return SPP_OK;
 }
 
 spp_status spp_set_prefetch_source(spp_ctx* c, int32_t source) {
@@ -1093,11 +1185,10 @@ spp_status spp_profile_expert_copy(spp_ctx* c, int32_t l, int32_t reps, double* 
   hipEvent_t e0, e1;
   SPP_HIP(hipEventCreate(&e0));
   SPP_HIP(hipEventCreate(&e1));
-  SPP_HIP(hipMemcpyAsync(c->probe_dev, ls.host_store, c->blob_bytes, hipMemcpyHostToDevice, c->copy));
+  SPP_HIP(copy_part(c, ls, c->probe_dev, 0, c->blob_bytes, c->copy));
   SPP_HIP(hipEventRecord(e0, c->copy));
   for (int32_t i = 0; i < reps; ++i)
-    SPP_HIP(hipMemcpyAsync(c->probe_dev, ls.host_store + static_cast<size_t>(i % c->d.n) * c->stride,
-                           c->blob_bytes, hipMemcpyHostToDevice, c->copy));
+    SPP_HIP(copy_part(c, ls, c->probe_dev, static_cast<size_t>(i % c->d.n) * c->stride, c->blob_bytes, c->copy));
   SPP_HIP(hipEventRecord(e1, c->copy));
   SPP_HIP(hipEventSynchronize(e1));
   *per_expert_us = 1e3 * elapsed(e0, e1) / reps;

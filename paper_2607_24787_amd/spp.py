@@ -20,6 +20,7 @@ DTYPE_F32, DTYPE_BF16 = 0, 1
 LAYOUT_UNITS, LAYOUT_TILED, LAYOUT_Q4_UNITS = 0, 1, 2
 CODEC_PLAIN, CODEC_Q4 = 0, 1
 PREFETCH_ADAPTER, PREFETCH_PREV_TOKEN = 0, 1
+COPY_KERNEL, COPY_SDMA, COPY_SPLIT = 0, 1, 2
 
 
 class SppError(RuntimeError):
@@ -81,6 +82,7 @@ _SIGS = {
     "spp_reset_run_stats": (c_int32, [c_void_p]),
     "spp_profile_expert_copy": (c_int32, [c_void_p, c_int32, c_int32, POINTER(c_double)]),
     "spp_set_prefetch_source": (c_int32, [c_void_p, c_int32]),
+    "spp_set_copy_engine": (c_int32, [c_void_p, c_int32]),
     "spp_set_tier_delay": (c_int32, [c_void_p, c_int32]),
     "spp_get_last_logits": (c_int32, [c_void_p, POINTER(c_float), c_int32]),
     "spp_set_ffn_workgroups": (c_int32, [c_void_p, c_int32]),
@@ -340,6 +342,10 @@ def spp_set_tier_delay(ctx, delay_us: int):
 
 def spp_set_prefetch_source(ctx, source: int):
     _check(lib().spp_set_prefetch_source(c_void_p(ctx), source))
+
+
+def spp_set_copy_engine(ctx, engine: int):
+    _check(lib().spp_set_copy_engine(c_void_p(ctx), engine))
 
 
 def spp_set_ffn_workgroups(ctx, wgs: int):

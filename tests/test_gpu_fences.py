@@ -34,12 +34,13 @@ def torch_cuda():
     return torch
 
 
-def _run(cfg, M_max, tokens, poison=False, delay_us=0):
+def _run(cfg, M_max, tokens, poison=False, delay_us=0, engine=2):
     from paper_2607_24787_amd import spp
     from paper_2607_24787_amd.model import OffloadedMoEStack
     h0 = gen.hidden_states(cfg, tokens=tokens)
     st = OffloadedMoEStack(cfg)
     try:
+        spp.spp_set_copy_engine(st.ctx, engine)
         spp.spp_debug_set_poison(st.ctx, poison)
         spp.spp_debug_set_copy_delay(st.ctx, delay_us)
         outs, on_time, needed, misses = [], 0, 0, 0
@@ -66,16 +67,21 @@ Q4_FENCE = w.MoEConfig(name="q4_D256_n12_k3_I96", L=3, D=256, n=12, K=3, I=96, r
                        codec="q4", seed=21)
 
 
-@pytest.mark.parametrize("cfg,M_max,tokens", [(RAGGED, 2, 12), (w.get("c0"), 1, 16), (BATCH_ROUNDS, 2, 6),
-                                              (Q4_FENCE, 2, 12)],
-                         ids=["ragged", "c0", "batched_rounds", "q4"])
-def test_poisoned_delayed_copies_leave_outputs_unchanged(torch_cuda, cfg, M_max, tokens):
-    _log(f"[fences] {cfg.name} M_max={M_max}")
-    ref, ref_on_time, needed, misses = _run(cfg, M_max, tokens)
+# copy engine 2: on-demand loads by the copy kernel, prefetches by DMA (the
+# default); 0: every copy by the copy kernel; 1: every copy by DMA
+@pytest.mark.parametrize("cfg,M_max,tokens,engine", [(RAGGED, 2, 12, 2), (w.get("c0"), 1, 16, 2),
+                                                     (BATCH_ROUNDS, 2, 6, 2), (Q4_FENCE, 2, 12, 2),
+                                                     (RAGGED, 2, 12, 0), (BATCH_ROUNDS, 2, 6, 0),
+                                                     (RAGGED, 2, 12, 1), (BATCH_ROUNDS, 2, 6, 1)],
+                         ids=["ragged", "c0", "batched_rounds", "q4", "ragged_kernel", "batched_rounds_kernel",
+                              "ragged_sdma", "batched_rounds_sdma"])
+def test_poisoned_delayed_copies_leave_outputs_unchanged(torch_cuda, cfg, M_max, tokens, engine):
+    _log(f"[fences] {cfg.name} M_max={M_max} engine={engine}")
+    ref, ref_on_time, needed, misses = _run(cfg, M_max, tokens, engine=engine)
     assert misses > 0, "the case must exercise on-demand loads"
     assert not np.isnan(o.decode(ref, cfg.dtype)).any()
     for poison, delay in [(True, 0), (True, 300), (False, 300)]:
-        out, on_time, needed2, _ = _run(cfg, M_max, tokens, poison, delay)
+        out, on_time, needed2, _ = _run(cfg, M_max, tokens, poison, delay, engine)
         assert needed2 == needed
         dec = o.decode(out, cfg.dtype)
         assert not np.isnan(dec).any(), (poison, delay)
@@ -92,3 +98,6 @@ def test_repeat_runs_are_bitwise_identical(torch_cuda):
     a, _, _, _ = _run(cfg, cfg.window, 6)
     b, _, _, _ = _run(cfg, cfg.window, 6, poison=True)
     assert np.array_equal(a, b)
+    for engine in (0, 1):   # every copy by the copy kernel, every copy by DMA: the same bytes
+        c, _, _, _ = _run(cfg, cfg.window, 6, poison=True, engine=engine)
+        assert np.array_equal(a, c), engine

@@ -201,14 +201,18 @@ def test_router_preservation_on_device(torch_cuda, cfg):
         assert np.array_equal(out, ref), (S, M)
 
 
-def test_adapter_predict_against_oracle(torch_cuda):
+# adapter rank 6: the last adapter workgroup has waves without a row (and
+# adapter_predict passes no router matrix)
+@pytest.mark.parametrize("cfg", [BATCH.with_(dtype="bf16", D=256, batch=4),
+                                 BATCH.with_(dtype="bf16", D=256, batch=4, r=6)], ids=["r8", "r6"])
+def test_adapter_predict_against_oracle(torch_cuda, cfg):
     import torch
     from paper_2607_24787_amd import spp
-    cfg = BATCH.with_(dtype="bf16", D=256, batch=4)
     st = _stack(cfg)
     try:
         rng = np.random.default_rng(1)
         for B in (1, 3, 4):
+            _log(f"[adapter_predict] r={cfg.r} B={B}")
             x = rng.normal(size=(B, cfg.D)).astype(np.float32)
             xd = torch.from_numpy(x).to(st.device)
             s = spp.adapter_predict(st.ctx, 0, xd.data_ptr(), B, cfg.n)
@@ -219,6 +223,35 @@ def test_adapter_predict_against_oracle(torch_cuda):
         with pytest.raises(spp.SppError) as e:
             spp.adapter_predict(st.ctx, cfg.L - 1, xd.data_ptr(), 1, cfg.n)    # last layer: no adapter
         assert e.value.status == spp.SPP_ESTATE
+    finally:
+        st.close()
+
+
+@pytest.mark.parametrize("cfg", [RAGGED, RAGGED.with_(D=512), BATCH_BF16, BATCH],
+                         ids=["b1_bf16_D640", "b1_bf16_D512", "b5_bf16", "b3_f32"])
+def test_topk_ties_break_to_the_lower_index(torch_cuda, cfg):
+    """Router rows repeated three ways (plus zero rows) make every logit tie
+    with others exactly; the selection must equal the stable order of the
+    device's own logits: larger logit first, the lower index among equals."""
+    import torch
+    from paper_2607_24787_amd import spp
+    st = _stack(cfg)
+    try:
+        R = st.router[0]
+        with torch.no_grad():
+            src = torch.arange(cfg.n, device=R.device) % 3
+            R.copy_(R[src])
+            R[6::7] = 0
+        h0 = gen.hidden_states(cfg, tokens=3)
+        for t in range(3):
+            _log(f"[ties] {cfg.name} token {t}")
+            st.upload_hidden(h0[t], 0)
+            topk, _, _ = st.layer(0, 0, 1, -1)
+            z = spp.spp_get_last_logits(st.ctx, cfg.batch, cfg.n)
+            for b in range(cfg.batch):
+                order = np.lexsort((np.arange(cfg.n), -z[b].astype(np.float64)))
+                assert len(np.unique(z[b])) <= 4
+                assert np.array_equal(np.asarray(topk).reshape(cfg.batch, cfg.K)[b], order[:cfg.K]), (t, b)
     finally:
         st.close()
 
@@ -267,6 +300,17 @@ def test_error_paths_on_device(torch_cuda):
         with pytest.raises(spp.SppError) as e:
             spp.spp_set_prefetch_source(st.ctx, 7)
         assert e.value.status == spp.SPP_EINVAL
+        with pytest.raises(spp.SppError) as e:
+            spp.spp_set_copy_engine(st.ctx, 3)
+        assert e.value.status == spp.SPP_EINVAL
+        # the offload tier must be pinned (the copy kernel reads it through its device address) and aligned
+        pageable = np.zeros(cfg.n * st.stride + 64, dtype=np.uint8)
+        pinned = st.host[0].data_ptr()
+        for host_ptr in (pageable.ctypes.data, pinned + 8):
+            with pytest.raises(spp.SppError) as e:
+                spp.spp_bind_layer(st.ctx, 0, st.router[0].data_ptr(), st.adapter[0][0].data_ptr(),
+                                   st.adapter[0][1].data_ptr(), 0, 0, host_ptr)
+            assert e.value.status == spp.SPP_EINVAL
         with pytest.raises(spp.SppError) as e:                 # whole-step call: buffers must be distinct
             spp.spp_decode_step(st.ctx, cfg.L, st.hbuf[0].data_ptr(), st.hbuf[0].data_ptr(), st.hbuf[1].data_ptr(),
                                 1, cfg.K, 1)
