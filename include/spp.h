@@ -318,11 +318,11 @@ spp_status spp_set_tier_delay(spp_ctx* ctx, int32_t delay_us);
 
 /* Test hooks for the copy/compute fences (for tests, not for production runs).
  * Poison: before every expert copy the target slot is filled with 0xFF bytes
- * (NaN in bf16 and fp32) on the copy streams, so a kernel that read a slot
- * before its copy completed would produce NaN.  Copy delay: a bounded busy
- * kernel of about delay_us (0..100000) runs on each copy stream before every
+ * (NaN in bf16 and fp32) on the stream that copies, so a kernel that read a
+ * slot before its copy completed would produce NaN.  Copy delay: a bounded
+ * busy kernel of about delay_us (0..100000) runs on that stream before every
  * copy (the mechanism of spp_set_tier_delay), so copies are still in flight
- * when the FFN is enqueued and the compute stream must wait on their events.
+ * when the FFN is enqueued and the compute stream must wait for them.
  * Outputs are unchanged by both. */
 spp_status spp_debug_set_poison(spp_ctx* ctx, int32_t enabled);
 spp_status spp_debug_set_copy_delay(spp_ctx* ctx, int32_t delay_us);

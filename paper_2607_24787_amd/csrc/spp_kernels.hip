@@ -996,32 +996,32 @@ __global__ __launch_bounds__(kFfnThreads) void ffn_q4_kernel(FfnArgs a) {
 // 1024 threads cover 64 outputs: 16 groups split the partials (8 loads in
 // flight per thread), then the groups are added in order.
 constexpr int kCombGroups = 16;
+constexpr int kCombRows = 32;
 
 template <typename T>
 __global__ __launch_bounds__(64 * kCombGroups) void ffn_combine_kernel(CombineArgs a) {
   __shared__ float s_part[kCombGroups][64];
   const int lane = threadIdx.x & 63, grp = threadIdx.x >> 6;
-  const int col = blockIdx.x * 64 + lane;
-  float s = 0.f;
-  if (col < a.D) {
-    for (int w0 = grp; w0 < a.nparts; w0 += kCombGroups * 8) {
-      float v[8];
+  const int col0 = static_cast<int>(blockIdx.x) * 64 + lane;
+  const int col = min(col0, a.D - 1);  // lanes past D re-read the last column, unused
+  // group g sums partial rows g*kCombRows.. of every pass; a pass's loads all
+  // go out before the first add (one round trip for up to 512 partial rows),
+  // the residual behind the first pass's (group 0 always has a first pass)
+  float s = 0.f, res = 0.f;
+  for (int w0 = grp * kCombRows; w0 < a.nparts; w0 += kCombGroups * kCombRows) {
+    float v[kCombRows];
 #pragma unroll
-      for (int k = 0; k < 8; ++k) {
-        const int w = w0 + kCombGroups * k;
-        v[k] = w < a.nparts ? a.partial[static_cast<size_t>(w) * a.D + col] : 0.f;
-      }
+    for (int k = 0; k < kCombRows; ++k) v[k] = a.partial[static_cast<size_t>(min(w0 + k, a.nparts - 1)) * a.D + col];
+    if (w0 == grp * kCombRows) res = a.res_u ? a.res_u[col] : load_elem<T>(a.res_h, col);
 #pragma unroll
-      for (int k = 0; k < 8; ++k) s += v[k];
-    }
+    for (int k = 0; k < kCombRows; ++k) s += w0 + k < a.nparts ? v[k] : 0.f;
   }
   s_part[grp][lane] = s;
   __syncthreads();
-  if (grp == 0 && col < a.D) {
+  if (grp == 0 && col0 < a.D) {
     float y = s_part[0][lane];
 #pragma unroll
     for (int g = 1; g < kCombGroups; ++g) y += s_part[g][lane];
-    const float res = a.res_u ? a.res_u[col] : load_elem<T>(a.res_h, col);
     store_elem<T>(a.out, col, res + y);
   }
 }

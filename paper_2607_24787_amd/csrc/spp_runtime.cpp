@@ -247,7 +247,8 @@ hipError_t copy_part(spp_ctx* c, const LayerState& ls, uint8_t* dst, size_t src_
 // that read this layer's slots).  demand: on-demand loads, which the compute
 // stream waits for as a group, so one event after the last copy covers them
 // (the streams are in order); otherwise prefetches, consumed one by one, each
-// with its own event.
+// with its own event.  An event wait costs the host ~14 us while the event is
+// pending, ~0.2 us once it completed, so every wait is preceded by a query.
 spp_status issue_copies(spp_ctx* c, LayerState& ls, const std::vector<spp::Transfer>& xs, hipEvent_t war,
                         bool demand) {
   if (xs.empty()) return SPP_OK;
@@ -297,8 +298,9 @@ spp_status issue_inline(spp_ctx* c, LayerState& ls, const std::vector<spp::Trans
     if (!ls.slot_pending[t.slot]) continue;
     const int32_t ev = ls.slot_event[t.slot];
     if (std::find(waited.begin(), waited.end(), ev) == waited.end()) {
-      SPP_HIP(hipStreamWaitEvent(c->compute, ls.slot_ready[ev], 0));
-      SPP_HIP(hipStreamWaitEvent(c->compute, ls.slot_ready2[ev], 0));
+      if (hipEventQuery(ls.slot_ready[ev]) != hipSuccess) SPP_HIP(hipStreamWaitEvent(c->compute, ls.slot_ready[ev], 0));
+      if (hipEventQuery(ls.slot_ready2[ev]) != hipSuccess)
+        SPP_HIP(hipStreamWaitEvent(c->compute, ls.slot_ready2[ev], 0));
       waited.push_back(ev);
     }
     ls.slot_pending[t.slot] = 0;
@@ -341,6 +343,7 @@ spp_status sync_all(spp_ctx* c) {
   SPP_HIP(hipStreamSynchronize(c->compute));
   return SPP_OK;
 }
+
 
 // Synchronous fill of slots from the host store according to the policy table.
 spp_status fill_slots(spp_ctx* c, LayerState& ls, const std::vector<int32_t>& before) {
@@ -504,8 +507,9 @@ spp_status wait_round(spp_ctx* c, LayerState& ls, const spp::Round& round, spp_l
       continue;
     }
     if (std::find(waited.begin(), waited.end(), ev) == waited.end()) {
-      SPP_HIP(hipStreamWaitEvent(c->compute, ls.slot_ready[ev], 0));
-      SPP_HIP(hipStreamWaitEvent(c->compute, ls.slot_ready2[ev], 0));
+      if (hipEventQuery(ls.slot_ready[ev]) != hipSuccess) SPP_HIP(hipStreamWaitEvent(c->compute, ls.slot_ready[ev], 0));
+      if (hipEventQuery(ls.slot_ready2[ev]) != hipSuccess)
+        SPP_HIP(hipStreamWaitEvent(c->compute, ls.slot_ready2[ev], 0));
       waited.push_back(ev);
     }
   }
@@ -536,9 +540,8 @@ spp_status round_event(spp_ctx* c, size_t r, hipEvent_t* out) {
 // ascending token, at most kGroupTokens per group) round by round, with the
 // shared experts in round 0; upload the list once; per round: the round's
 // copies (waiting for the previous round's FFN, whose slots they reuse), the
-// compute stream's waits for them, one grouped FFN launch; then the next
-// layer's prefetch copies; one combine.
-spp_status grouped_ffn(spp_ctx* c, LayerState& ls, LayerState* next, const int32_t* T, int32_t B,
+// compute stream's waits for them, one grouped FFN launch; then one combine.
+spp_status grouped_ffn(spp_ctx* c, LayerState& ls, const int32_t* T, int32_t B,
                        const void* h_in, void* h_out, const std::vector<spp::Round>& rounds,
                        const std::vector<spp::Transfer>& loads, spp_layer_stats* st, TimingSet& ts) {
   const spp_model_desc& d = c->d;
@@ -611,10 +614,6 @@ spp_status grouped_ffn(spp_ctx* c, LayerState& ls, LayerState* next, const int32
     SPP_HIP(spp::launch_ffn_grouped(ga, c->compute, c->timing && first ? ts.ev[kEvFfnBegin] : nullptr,
                                     c->timing && last ? ts.ev[kEvFfnEnd] : nullptr));
   }
-  if (rounds.size() > 1 && next && !c->last_pref.empty())
-    if (spp_status e = issue_copies(c, *next, c->last_pref, next->last_read_valid ? next->last_read : nullptr,
-                                    false))
-      return e;
   spp::CombineBArgs cb{};
   cb.ypart = c->ypart;
   cb.gates = reinterpret_cast<const float*>(c->res_dev + c->off_gates);
@@ -764,15 +763,12 @@ spp_status layer_forward_impl(spp_ctx* c, int32_t l, const void* h_in, void* h_o
       st.prefetched = static_cast<int32_t>(c->last_pref.size());
     }
   }
-  if (rounds.size() == 1 && nx)
-    if (spp_status e = issue_copies(c, *nx, c->last_pref, nx->last_read_valid ? nx->last_read : nullptr, false))
-      return e;
 
   // RAW: the FFN reads each needed slot only after its copy completed
   if (spp_status e = wait_round(c, ls, rounds[0], &st)) return e;
   if (c->timing) SPP_HIP(hipEventRecord(ts.ev[kEvWaitB], c->compute));
   if (batched) {
-    if (spp_status e = grouped_ffn(c, ls, nx, T, B, h_in, h_out, rounds, c->last_loads, &st, ts)) return e;
+    if (spp_status e = grouped_ffn(c, ls, T, B, h_in, h_out, rounds, c->last_loads, &st, ts)) return e;
   }
   for (int32_t b = 0; b < B && !batched; ++b) {
     spp::FfnArgs fa{};
@@ -815,6 +811,11 @@ spp_status layer_forward_impl(spp_ctx* c, int32_t l, const void* h_in, void* h_o
     SPP_HIP(hipEventRecord(ts.ev[kEvEnd], c->compute));
     c->pending_sets.push_back(ts);
   }
+  // prefetches for layer l+1, behind every on-demand load on the copy streams
+  // and after the FFN launch (the host time they take then overlaps the FFN)
+  if (nx && !c->last_pref.empty())
+    if (spp_status e = issue_copies(c, *nx, c->last_pref, nx->last_read_valid ? nx->last_read : nullptr, false))
+      return e;
 
   if (topk_out) std::memcpy(topk_out, T, sizeof(int32_t) * BK);
   if (gate_out) std::memcpy(gate_out, g, sizeof(float) * BK);

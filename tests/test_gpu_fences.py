@@ -101,3 +101,4 @@ def test_repeat_runs_are_bitwise_identical(torch_cuda):
     for engine in (0, 1):   # every copy by the copy kernel, every copy by DMA: the same bytes
         c, _, _, _ = _run(cfg, cfg.window, 6, poison=True, engine=engine)
         assert np.array_equal(a, c), engine
+
