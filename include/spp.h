@@ -84,8 +84,9 @@ enum { SPP_COPY_KERNEL = 0, SPP_COPY_SDMA = 1, SPP_COPY_SPLIT = 2 };
  * n routed experts per layer, top-K routing, router input size D, adapter
  * rank r.  I: SwiGLU intermediate size of an expert; n_shared: always-resident
  * shared experts per layer (weight 1); S: HBM expert slots per layer;
- * max_batch: largest batch B passed to any call; has_proj: 1 if each layer
- * starts with the dense D x D stand-in projection u = h + P rms(h). */
+ * max_batch: largest batch B passed to any call (above 1, D must be a
+ * multiple of 16); has_proj: 1 if each layer starts with the dense D x D
+ * stand-in projection u = h + P rms(h). */
 typedef struct {
   int32_t L, D, n, K, I, r, n_shared, S, max_batch, dtype, has_proj;
   float rms_eps;

@@ -13,6 +13,7 @@
 #include <climits>
 #include <cmath>
 #include <cstdint>
+#include <type_traits>
 
 #include "spp_internal.h"
 
@@ -518,85 +519,11 @@ __global__ __launch_bounds__(kThreads) void router_adapter_kernel(RouterArgs a) 
 
 // ---------------------------------------------------------------------------
 // Router for B > 1 tokens, in two launches.
-//   rows:   one wave per router / adapter-A row over a block of kRowTok tokens
-//           (the row stays in registers, the tokens' rows are read in turn);
+//   rows:   router_rows_mfma_kernel (below, with the MFMA kernels);
 //   select: one workgroup per token -- Top-K, gates and the adapter
 //           distribution; the last workgroup to finish sums the distributions
 //           over the tokens, in token order, into s.
 // ---------------------------------------------------------------------------
-constexpr int kRowTok = 8;
-
-template <typename T, int NCH, bool FULL>
-__global__ __launch_bounds__(kThreads) void router_rows_kernel(RouterArgs a) {
-  constexpr int V = Vec<T>::N;
-  const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
-  const int D = a.D, nch = D / V, n = a.n, ldz = a.n + a.r;
-  const int nr = a.router_on ? n : 0;
-  const int na = a.A ? a.r : 0;
-  const int row = blockIdx.x * kWaves + wave;
-  const T* wrow = nullptr;
-  int zcol = 0;
-  if (row < nr) {
-    wrow = reinterpret_cast<const T*>(a.Wr) + static_cast<size_t>(row) * D;
-    zcol = row;
-  } else if (row < nr + na) {
-    wrow = reinterpret_cast<const T*>(a.A) + static_cast<size_t>(row - nr) * D;
-    zcol = n + (row - nr);
-  }
-  uint4 w[NCH];
-  // a wave past the last row re-reads the token's input row (a valid address) and drops it
-  load_chunks<NCH, FULL>(wrow ? static_cast<const void*>(wrow) : input_row(a), lane, wrow ? nch : 0, w);
-  const int b0 = blockIdx.y * kRowTok;
-  const int b1 = min(a.B, b0 + kRowTok);
-  // the first token's row goes out with the weight row: the unpacked weights
-  // are hoisted out of the token loop, which waits for them
-  float xv[NCH][V];
-  if (a.u) {
-    load_row_f32<T, NCH, FULL>(a.u + static_cast<size_t>(b0) * D, lane, nch, xv);
-  } else {
-    load_row_storage<T, NCH, FULL>(reinterpret_cast<const T*>(a.h) + static_cast<size_t>(b0) * D, lane, nch, xv);
-  }
-  for (int b = b0; b < b1; ++b) {
-    if (b > b0) {
-      if (a.u) {
-        load_row_f32<T, NCH, FULL>(a.u + static_cast<size_t>(b) * D, lane, nch, xv);
-      } else {
-        load_row_storage<T, NCH, FULL>(reinterpret_cast<const T*>(a.h) + static_cast<size_t>(b) * D, lane, nch, xv);
-      }
-    }
-    if (!a.x_given) {
-      const float inv = rms_scale<T, NCH>(xv, D, a.eps);
-#pragma unroll
-      for (int j = 0; j < NCH; ++j)
-#pragma unroll
-        for (int v = 0; v < V; ++v) xv[j][v] *= inv;
-    }
-    if (blockIdx.x == 0 && wave == 0 && a.x_out) {
-#pragma unroll
-      for (int j = 0; j < NCH; ++j) {
-        const int c = lane + 64 * j;
-        if (c < nch) {
-          float* dst = a.x_out + static_cast<size_t>(b) * D + c * V;
-#pragma unroll
-          for (int v = 0; v < V; ++v) dst[v] = xv[j][v];
-        }
-      }
-    }
-    if (wrow) {
-      float acc = 0.f;
-#pragma unroll
-      for (int j = 0; j < NCH; ++j) {
-        float wf[V];
-        unpack<T>(w[j], wf);
-#pragma unroll
-        for (int v = 0; v < V; ++v) acc += wf[v] * xv[j][v];
-      }
-      acc = wave_sum(acc);
-      if (lane == 0) a.zbuf[static_cast<size_t>(b) * ldz + zcol] = acc;
-    }
-  }
-}
-
 template <typename T>
 __global__ __launch_bounds__(kThreads) void router_select_kernel(RouterArgs a) {
   const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
@@ -651,8 +578,8 @@ __global__ __launch_bounds__(kThreads) void router_select_kernel(RouterArgs a) {
   if (a.done_host && a.router_on && tid == 0) raise_flag(a, 0);  // every token's mirrors have completed
   if (na) {
     // s = sum over the tokens, in token order, of their distributions; the
-    // loads go out 16 tokens at a time
-    constexpr int kTB = 16;
+    // loads go out 64 tokens at a time
+    constexpr int kTB = 64;
     for (int e = tid; e < n; e += kThreads) {
       float acc = 0.f;
       for (int b0 = 0; b0 < a.B; b0 += kTB) {
@@ -1216,62 +1143,71 @@ __global__ __launch_bounds__(kGrpThreads) void ffn_grouped_kernel(GroupArgs a) {
 
 // Batched combine: h_out[b] = round(residual[b] + sum_k g_bk sum_r ypart[(b,k), r]
 //                                   + sum_j sum_r ypart[(b, shared j), r]), fixed order.
-// One thread per 4 consecutive columns; the partials of one pair are loaded
-// four ranges at a time.
-__device__ __forceinline__ float4 sum_ranges(const float* p, int nsplit, int D) {
-  float4 v = make_float4(0.f, 0.f, 0.f, 0.f);
-  int r = 0;
-  for (; r + 4 <= nsplit; r += 4) {
-    float4 w[4];
+// Batched combine: y_b = sum_k g_bk * (sum over unit ranges of pair (b,k)'s
+// partial rows) + the same sums of the shared experts (weight 1), plus the
+// residual.  One workgroup per (256 columns, token); wave w sums the ranges of
+// pairs w, w + kCombWaves, ... with every range load of a pair in flight at
+// once (4 columns per lane); wave 0 then folds the pairs in order from LDS.
+constexpr int kCombWaves = 16;
+constexpr int kCombRanges = 16;  // range loads of one pair in flight per pass
+template <typename T>
+__global__ __launch_bounds__(64 * kCombWaves) void ffn_combine_batched_kernel(CombineBArgs a) {
+  __shared__ float4 s_v[kMaxWork][64];
+  const int lane = threadIdx.x & 63, wave = threadIdx.x >> 6, nwaves = blockDim.x >> 6;
+  const int b = blockIdx.y;
+  const int npairs = a.K + a.n_shared;
+  const int col = 4 * (blockIdx.x * 64 + lane);
+  const int c = min(col, a.D - 4);  // lanes past D re-read the last columns, unused
+  for (int p = wave; p < npairs; p += nwaves) {
+    const int pair = p < a.K ? b * a.K + p : a.B * a.K + b * a.n_shared + (p - a.K);
+    const float* base = a.ypart + static_cast<size_t>(pair) * a.nsplit * a.D + c;
+    float4 v = make_float4(0.f, 0.f, 0.f, 0.f);
+    for (int r0 = 0; r0 < a.nsplit; r0 += kCombRanges) {
+      float4 w[kCombRanges];
 #pragma unroll
-    for (int q = 0; q < 4; ++q) w[q] = *SPP_GLOBAL(float4, p + static_cast<size_t>(r + q) * D);
+      for (int q = 0; q < kCombRanges; ++q)
+        w[q] = *SPP_GLOBAL(float4, base + static_cast<size_t>(min(r0 + q, a.nsplit - 1)) * a.D);
 #pragma unroll
-    for (int q = 0; q < 4; ++q) {
-      v.x += w[q].x;
-      v.y += w[q].y;
-      v.z += w[q].z;
-      v.w += w[q].w;
+      for (int q = 0; q < kCombRanges; ++q) {
+        if (r0 + q < a.nsplit) {  // ranges in order
+          v.x += w[q].x;
+          v.y += w[q].y;
+          v.z += w[q].z;
+          v.w += w[q].w;
+        }
+      }
+    }
+    s_v[p][lane] = v;
+  }
+  // the gates and the residual go out while the other waves finish
+  float4 res = make_float4(0.f, 0.f, 0.f, 0.f);
+  if (wave == 0) {
+    const size_t o = static_cast<size_t>(b) * a.D + c;
+    if (a.res_u) {
+      res = *SPP_GLOBAL(float4, a.res_u + o);
+    } else {
+      res.x = load_elem<T>(a.res_h, o);
+      res.y = load_elem<T>(a.res_h, o + 1);
+      res.z = load_elem<T>(a.res_h, o + 2);
+      res.w = load_elem<T>(a.res_h, o + 3);
     }
   }
-  for (; r < nsplit; ++r) {
-    const float4 w = *SPP_GLOBAL(float4, p + static_cast<size_t>(r) * D);
-    v.x += w.x;
-    v.y += w.y;
-    v.z += w.z;
-    v.w += w.w;
-  }
-  return v;
-}
-
-template <typename T>
-__global__ __launch_bounds__(256) void ffn_combine_batched_kernel(CombineBArgs a) {
-  const int b = blockIdx.y;
-  const int d = 4 * (blockIdx.x * 256 + threadIdx.x);
-  if (d >= a.D) return;
+  __syncthreads();
+  if (wave != 0 || col >= a.D) return;
   float y[4] = {0.f, 0.f, 0.f, 0.f};
-  for (int k = 0; k < a.K; ++k) {
-    const size_t row = static_cast<size_t>(b * a.K + k) * a.nsplit;
-    const float4 v = sum_ranges(a.ypart + row * a.D + d, a.nsplit, a.D);
-    const float gk = a.gates[b * a.K + k];
-    y[0] += gk * v.x;
-    y[1] += gk * v.y;
-    y[2] += gk * v.z;
-    y[3] += gk * v.w;
+  for (int p = 0; p < npairs; ++p) {
+    const float4 v = s_v[p][lane];
+    const float g = p < a.K ? a.gates[b * a.K + p] : 1.f;
+    y[0] = p < a.K ? fmaf(g, v.x, y[0]) : y[0] + v.x;
+    y[1] = p < a.K ? fmaf(g, v.y, y[1]) : y[1] + v.y;
+    y[2] = p < a.K ? fmaf(g, v.z, y[2]) : y[2] + v.z;
+    y[3] = p < a.K ? fmaf(g, v.w, y[3]) : y[3] + v.w;
   }
-  for (int j = 0; j < a.n_shared; ++j) {
-    const size_t row = static_cast<size_t>(a.B * a.K + b * a.n_shared + j) * a.nsplit;
-    const float4 v = sum_ranges(a.ypart + row * a.D + d, a.nsplit, a.D);
-    y[0] += v.x;
-    y[1] += v.y;
-    y[2] += v.z;
-    y[3] += v.w;
-  }
-  const size_t o = static_cast<size_t>(b) * a.D + d;
-#pragma unroll
-  for (int c = 0; c < 4; ++c) {
-    const float res = a.res_u ? a.res_u[o + c] : load_elem<T>(a.res_h, o + c);
-    store_elem<T>(a.out, o + c, res + y[c]);
-  }
+  const size_t o = static_cast<size_t>(b) * a.D + col;
+  store_elem<T>(a.out, o, res.x + y[0]);
+  store_elem<T>(a.out, o + 1, res.y + y[1]);
+  store_elem<T>(a.out, o + 2, res.z + y[2]);
+  store_elem<T>(a.out, o + 3, res.w + y[3]);
 }
 
 // Stand-in projection prologue: u = h + P rms(h) (fp32 result).  One wave per row of P.
@@ -1313,50 +1249,223 @@ __global__ __launch_bounds__(kThreads) void proj_kernel(ProjArgs a) {
   }
 }
 
-// Stand-in projection for a batch (bf16, B > 1): one wave per 16 output rows
-// x 16 tokens on MFMA.  h and P are bf16, so their products are exact on the
-// bf16 MFMA; the normalisation moves to the epilogue,
+// Router and adapter-A rows for B > 1 tokens on fp32 MFMA:
+//   z[b][row] = inv_b * sum_k u[b][k] W[row][k],  inv_b = 1 / rms(u_b)
+// (inv_b = 1 when u already is the router input x); the router rows, then the
+// adapter rows, form the row axis, written to zbuf at their columns.  One
+// workgroup per 16 tokens x 16 rows; its waves split D into runs of 16
+// columns.  A lane loads 4 consecutive columns of its token row and of its
+// weight row, and 4 MFMA steps consume them: step q multiplies columns
+// 16c + 4(lane/16) + q (the step's k index is lane/16), so the four steps
+// cover the run exactly once.  Products are exact in fp32 (bf16 weights widen
+// exactly); the waves' partial tiles and partial sums of squares add in wave
+// order through LDS.  The workgroups also write x = inv_b * u_b (x_out), each
+// a slice of D for its tokens.
+constexpr int kRowWaves = 8;
+constexpr int kRowRuns = 16;  // runs of 16 columns per wave and pass, loads in flight together
+
+template <typename T>
+__device__ __forceinline__ void widen4(const uint2 r, float* f) {
+  f[0] = __uint_as_float(r.x << 16);
+  f[1] = __uint_as_float(r.x & 0xffff0000u);
+  f[2] = __uint_as_float(r.y << 16);
+  f[3] = __uint_as_float(r.y & 0xffff0000u);
+}
+
+// 4 consecutive elements of a row as raw bits: 8 bytes (bf16) or 16 bytes (fp32)
+template <typename T>
+struct Raw4;
+template <>
+struct Raw4<uint16_t> {
+  uint2 v;
+  __device__ __forceinline__ void load(const uint16_t* p) { v = *SPP_GLOBAL(uint2, p); }
+  __device__ __forceinline__ void get(float* f) const { widen4<uint16_t>(v, f); }
+};
+template <>
+struct Raw4<float> {
+  uint4 v;
+  __device__ __forceinline__ void load(const float* p) { v = *SPP_GLOBAL(uint4, p); }
+  __device__ __forceinline__ void get(float* f) const { unpack<float>(v, f); }
+};
+
+// UF: the token rows come as fp32 u (else as h in the storage type T)
+template <typename T, bool UF>
+__global__ __launch_bounds__(64 * kRowWaves) void router_rows_mfma_kernel(RouterArgs a) {
+  using TU = typename std::conditional<UF, float, T>::type;
+  __shared__ f32x4 s_acc[kRowWaves][64];
+  __shared__ float s_ss[kRowWaves][16];
+  __shared__ float s_inv[16];
+  const int lane = threadIdx.x & 63, wave = threadIdx.x >> 6;
+  const int D = a.D, n = a.n, ldz = a.n + a.r;
+  const int nr = a.router_on ? n : 0, na = a.A ? a.r : 0, rows = nr + na;
+  const int b0 = blockIdx.y * 16, r0 = blockIdx.x * 16;
+  const int i = lane & 15, g = lane >> 4;
+  const int tok = min(b0 + i, a.B - 1);
+  const int row = min(r0 + i, rows - 1);
+  const T* wrow = row < nr ? reinterpret_cast<const T*>(a.Wr) + static_cast<size_t>(row) * D
+                           : reinterpret_cast<const T*>(a.A) + static_cast<size_t>(row - nr) * D;
+  const TU* urow = (UF ? reinterpret_cast<const TU*>(a.u) : reinterpret_cast<const TU*>(a.h)) +
+                   static_cast<size_t>(tok) * D;
+  const int nruns = D / 16;  // D % 16 == 0 (checked at launch)
+  const int per = (nruns + kRowWaves - 1) / kRowWaves;
+  const int c_begin = min(nruns, wave * per), c_end = min(nruns, c_begin + per);
+  f32x4 acc = f32x4{0.f, 0.f, 0.f, 0.f};
+  float ss = 0.f;
+  for (int c0 = c_begin; c0 < c_end; c0 += kRowRuns) {
+    Raw4<TU> ur[kRowRuns];
+    Raw4<T> wr[kRowRuns];
+#pragma unroll
+    for (int q = 0; q < kRowRuns; ++q) {
+      const int k = 16 * min(c0 + q, c_end - 1) + 4 * g;  // past the range: a valid run, dropped below
+      ur[q].load(urow + k);
+      wr[q].load(wrow + k);
+    }
+    __builtin_amdgcn_sched_barrier(0);
+#pragma unroll
+    for (int q = 0; q < kRowRuns; ++q) {
+      if (c0 + q < c_end) {  // wave-uniform
+        float uf[4], wf[4];
+        ur[q].get(uf);
+        wr[q].get(wf);
+#pragma unroll
+        for (int st = 0; st < 4; ++st) {
+          acc = __builtin_amdgcn_mfma_f32_16x16x4f32(uf[st], wf[st], acc, 0, 0, 0);
+          ss += uf[st] * uf[st];
+        }
+      }
+    }
+  }
+  // lanes i, i+16, i+32, i+48 hold the column groups of token b0 + i
+  ss += __shfl_xor(ss, 16);
+  ss += __shfl_xor(ss, 32);
+  s_acc[wave][lane] = acc;
+  if (lane < 16) s_ss[wave][lane] = ss;
+  __syncthreads();
+  if (wave == 0) {
+    if (lane < 16) {
+      float sst = s_ss[0][lane];
+#pragma unroll
+      for (int w = 1; w < kRowWaves; ++w) sst += s_ss[w][lane];
+      s_inv[lane] = a.x_given ? 1.f : 1.0f / sqrtf(sst / static_cast<float>(D) + a.eps);
+    }
+    f32x4 z = s_acc[0][lane];
+#pragma unroll
+    for (int w = 1; w < kRowWaves; ++w) {
+      const f32x4 v = s_acc[w][lane];
+      z = f32x4{z[0] + v[0], z[1] + v[1], z[2] + v[2], z[3] + v[3]};
+    }
+    // this lane holds tokens b0 + 4*(lane/16) + j of row r0 + lane%16
+    const int zr = r0 + i;
+    if (zr < rows) {
+      const int zcol = zr < nr ? zr : n + (zr - nr);
+#pragma unroll
+      for (int j = 0; j < 4; ++j) {
+        const int t = 4 * g + j;
+        const int b = b0 + t;
+        if (b < a.B) a.zbuf[static_cast<size_t>(b) * ldz + zcol] = z[j] * s_inv[t];
+      }
+    }
+  }
+  if (!a.x_out) return;
+  __syncthreads();
+  // x = inv * u for the workgroup's tokens: the row tiles of a token tile
+  // share its runs of 16 columns, the waves share a row tile's runs
+  if (b0 + i < a.B) {
+    const float inv = s_inv[i];
+    float* xo = a.x_out + static_cast<size_t>(b0 + i) * D;
+    const int nrt = gridDim.x, rt = blockIdx.x;
+    const int x0 = nruns * rt / nrt, x1 = nruns * (rt + 1) / nrt;
+    constexpr int kX = 4;  // runs per wave and pass, loads in flight together
+    for (int c0 = x0 + wave * kX; c0 < x1; c0 += kRowWaves * kX) {
+      Raw4<TU> ur[kX];
+#pragma unroll
+      for (int q = 0; q < kX; ++q) ur[q].load(urow + 16 * min(c0 + q, x1 - 1) + 4 * g);
+#pragma unroll
+      for (int q = 0; q < kX; ++q) {
+        if (c0 + q < x1) {
+          float f[4];
+          ur[q].get(f);
+          *reinterpret_cast<float4*>(xo + 16 * (c0 + q) + 4 * g) =
+              make_float4(f[0] * inv, f[1] * inv, f[2] * inv, f[3] * inv);
+        }
+      }
+    }
+  }
+}
+
+// Stand-in projection for a batch (bf16, B > 1) on MFMA.  h and P are bf16, so
+// their products are exact on the bf16 MFMA; the normalisation moves to the
+// epilogue,
 //   u[b][o] = h[b][o] + (sum_i P[o][i] h[b][i]) / sqrt(mean_i h[b][i]^2 + eps),
-// with sum_i h[b][i]^2 accumulated from the same loads.  Token rows past B
-// read the last token and are not stored.
-__global__ __launch_bounds__(64) void proj_mfma_kernel(ProjArgs a) {
-  const int lane = threadIdx.x;
+// with sum_i h[b][i]^2 accumulated from the same loads.  One workgroup per 16
+// output rows x 16 tokens; its 4 waves split D in 256-column chunks (wave w
+// takes chunks w, w+4, ..., two chunks' loads in flight per pass), each with
+// a 16x16 accumulator and its tokens' partial sums of squares, added in wave
+// order through LDS.  (One workgroup per 16 rows x 64 tokens reads P once but
+// measured slower: fewer workgroups keep fewer loads in flight.)  Token rows
+// past B read the last token and are not stored.
+constexpr int kProjWaves = 4;
+__global__ __launch_bounds__(64 * kProjWaves) void proj_mfma_kernel(ProjArgs a) {
+  __shared__ f32x4 s_acc[kProjWaves][64];
+  __shared__ float s_ss[kProjWaves][16];
+  const int lane = threadIdx.x & 63, wave = threadIdx.x >> 6;
   const int o0 = blockIdx.x * 16, b0 = blockIdx.y * 16;
-  const int D = a.D;
+  const int D = a.D, nck = D / 256;
   const int krow = lane & 15, koff = 8 * (lane >> 4);
   const int tok = min(b0 + krow, a.B - 1);
   const uint16_t* hrow = reinterpret_cast<const uint16_t*>(a.h) + static_cast<size_t>(tok) * D + koff;
   const uint16_t* prow = reinterpret_cast<const uint16_t*>(a.P) + static_cast<size_t>(o0 + krow) * D + koff;
   f32x4 acc = f32x4{0.f, 0.f, 0.f, 0.f};
   float ss = 0.f;
-  for (int k0 = 0; k0 < D; k0 += 256) {
-    u32x4 ha[8], pb[8];
+  for (int c0 = wave; c0 < nck; c0 += 2 * kProjWaves) {
+    // chunks c0 and c0 + kProjWaves (the second clamped to a valid chunk, then dropped)
+    const int c1 = c0 + kProjWaves;
+    const bool has1 = c1 < nck;
+    const int k0 = 256 * c0, k1 = 256 * (has1 ? c1 : c0);
+    u32x4 ha[16], pb[16];
 #pragma unroll
     for (int j = 0; j < 8; ++j) {
       ha[j] = *SPP_GLOBAL(u32x4, hrow + k0 + 32 * j);
       pb[j] = __builtin_nontemporal_load(SPP_GLOBAL(u32x4, prow + k0 + 32 * j));
+      ha[8 + j] = *SPP_GLOBAL(u32x4, hrow + k1 + 32 * j);
+      pb[8 + j] = __builtin_nontemporal_load(SPP_GLOBAL(u32x4, prow + k1 + 32 * j));
     }
     __builtin_amdgcn_sched_barrier(0);
+    const int nj = has1 ? 16 : 8;
 #pragma unroll
-    for (int j = 0; j < 8; ++j) {
-      acc = __builtin_amdgcn_mfma_f32_16x16x32_bf16(__builtin_bit_cast(bf16x8, ha[j]),
-                                                    __builtin_bit_cast(bf16x8, pb[j]), acc, 0, 0, 0);
-      const uint32_t w[4] = {ha[j].x, ha[j].y, ha[j].z, ha[j].w};
+    for (int j = 0; j < 16; ++j) {
+      if (j < nj) {
+        acc = __builtin_amdgcn_mfma_f32_16x16x32_bf16(__builtin_bit_cast(bf16x8, ha[j]),
+                                                      __builtin_bit_cast(bf16x8, pb[j]), acc, 0, 0, 0);
+        const uint32_t w[4] = {ha[j].x, ha[j].y, ha[j].z, ha[j].w};
 #pragma unroll
-      for (int q = 0; q < 4; ++q) {
-        const float lo = __uint_as_float(w[q] << 16), hi = __uint_as_float(w[q] & 0xffff0000u);
-        ss += lo * lo + hi * hi;
+        for (int q = 0; q < 4; ++q) {
+          const float lo = __uint_as_float(w[q] << 16), hi = __uint_as_float(w[q] & 0xffff0000u);
+          ss += lo * lo + hi * hi;
+        }
       }
     }
   }
   // lanes l, l+16, l+32, l+48 hold the k-slices of token b0 + l%16
   ss += __shfl_xor(ss, 16);
   ss += __shfl_xor(ss, 32);
+  s_acc[wave][lane] = acc;
+  if (lane < 16) s_ss[wave][lane] = ss;
+  __syncthreads();
+  if (wave != 0) return;
+  acc = s_acc[0][lane];
+#pragma unroll
+  for (int w = 1; w < kProjWaves; ++w) {
+    const f32x4 v = s_acc[w][lane];
+    acc = f32x4{acc[0] + v[0], acc[1] + v[1], acc[2] + v[2], acc[3] + v[3]};
+  }
   // this lane holds tokens 4*(lane/16)+j of output row o0 + lane%16
 #pragma unroll
   for (int j = 0; j < 4; ++j) {
     const int t = 4 * (lane >> 4) + j;
-    const float sst = __shfl(ss, t);
+    float sst = s_ss[0][t];
+#pragma unroll
+    for (int w = 1; w < kProjWaves; ++w) sst += s_ss[w][t];
     const int b = b0 + t;
     if (b < a.B) {
       const int o = o0 + krow;
@@ -1427,7 +1536,6 @@ hipError_t router_tf(const RouterArgs& a, hipStream_t st) {
   if (rows <= 0) return hipErrorInvalidValue;
   // the staged adapter path reads B in 16-byte chunks
   if (a.A && (static_cast<size_t>(a.n) * a.r * sizeof(T)) % 16 != 0) return hipErrorInvalidValue;
-  const int grid = (rows + kWaves - 1) / kWaves;
   if (a.B == 1) {
     // router rows and adapter rows in workgroups of their own
     const int g1 = ((a.router_on ? a.n : 0) + kWaves - 1) / kWaves + ((a.A ? a.r : 0) + kWaves - 1) / kWaves;
@@ -1435,9 +1543,12 @@ hipError_t router_tf(const RouterArgs& a, hipStream_t st) {
                                                          dim3(kThreads), 0, st, a));
     return hipGetLastError();
   }
-  const dim3 g2(grid, (a.B + kRowTok - 1) / kRowTok);
-  SPP_DISPATCH_NCH(nch_for<T>(a.D),
-                   hipLaunchKernelGGL((router_rows_kernel<T, NCH, FULL>), g2, dim3(kThreads), 0, st, a));
+  if (a.D % 16 != 0) return hipErrorInvalidValue;
+  const dim3 g2((rows + 15) / 16, (a.B + 15) / 16);
+  if (a.u)
+    hipLaunchKernelGGL((router_rows_mfma_kernel<T, true>), g2, dim3(64 * kRowWaves), 0, st, a);
+  else
+    hipLaunchKernelGGL((router_rows_mfma_kernel<T, false>), g2, dim3(64 * kRowWaves), 0, st, a);
   hipError_t e = hipGetLastError();
   if (e != hipSuccess) return e;
   hipLaunchKernelGGL((router_select_kernel<T>), dim3(a.B), dim3(kThreads), 0, st, a);
@@ -1524,7 +1635,7 @@ hipError_t launch_combine(const CombineArgs& a, int dtype, hipStream_t st) {
 
 hipError_t launch_proj(const ProjArgs& a, int dtype, hipStream_t st) {
   if (dtype == 1 && a.B > 1 && a.D % 256 == 0) {
-    hipLaunchKernelGGL(proj_mfma_kernel, dim3(a.D / 16, (a.B + 15) / 16), dim3(64), 0, st, a);
+    hipLaunchKernelGGL(proj_mfma_kernel, dim3(a.D / 16, (a.B + 15) / 16), dim3(64 * kProjWaves), 0, st, a);
     return hipGetLastError();
   }
   return dtype == 1 ? proj_t<uint16_t>(a, st) : proj_t<float>(a, st);
@@ -1543,12 +1654,14 @@ hipError_t launch_ffn_grouped(const GroupArgs& a, hipStream_t st, hipEvent_t sta
 }
 
 hipError_t launch_combine_batched(const CombineBArgs& a, int dtype, hipStream_t st) {
-  if (a.D % 4 != 0) return hipErrorInvalidValue;
-  const dim3 grid((a.D / 4 + 255) / 256, a.B);
+  const int npairs = a.K + a.n_shared;
+  if (a.D % 4 != 0 || npairs < 1 || npairs > kMaxWork || a.nsplit < 1) return hipErrorInvalidValue;
+  const dim3 grid((a.D / 4 + 63) / 64, a.B);
+  const dim3 block(64 * min(npairs, kCombWaves));
   if (dtype == 1)
-    hipLaunchKernelGGL((ffn_combine_batched_kernel<uint16_t>), grid, dim3(256), 0, st, a);
+    hipLaunchKernelGGL((ffn_combine_batched_kernel<uint16_t>), grid, block, 0, st, a);
   else
-    hipLaunchKernelGGL((ffn_combine_batched_kernel<float>), grid, dim3(256), 0, st, a);
+    hipLaunchKernelGGL((ffn_combine_batched_kernel<float>), grid, block, 0, st, a);
   return hipGetLastError();
 }
 

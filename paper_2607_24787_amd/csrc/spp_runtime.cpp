@@ -150,6 +150,7 @@ bool desc_ok(const spp_model_desc* d, std::string* why) {
   if ((static_cast<int64_t>(d->D) * elem) % 16 != 0) return *why = "D * element size must be a multiple of 16 bytes", false;
   const int nch = (d->D * elem / 16 + 63) / 64;
   if (nch > 8) return *why = "D too large (at most 4096 bf16 / 2048 fp32)", false;
+  if (d->max_batch > 1 && d->D % 16 != 0) return *why = "max_batch > 1 needs D a multiple of 16", false;
   if (d->n > spp::kMaxExpertsTopK) return *why = "n must be <= 1024", false;
   if (d->K > d->n || d->K > 32) return *why = "K must be <= min(n, 32)", false;
   if (d->r < 0 || d->r > 256) return *why = "r must be in [0, 256]", false;
