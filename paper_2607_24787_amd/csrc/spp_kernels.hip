@@ -1643,7 +1643,7 @@ hipError_t launch_proj(const ProjArgs& a, int dtype, hipStream_t st) {
 
 hipError_t launch_ffn_grouped(const GroupArgs& a, hipStream_t st, hipEvent_t start, hipEvent_t stop) {
   if (a.ngroups <= 0 || a.nsplit <= 0 || (a.upw != 64 && a.upw != 128 && a.upw != 256) || a.D % kGrpBlk != 0 ||
-      a.I % 16 != 0 || a.nsplit * a.upw < a.I)
+      a.I % 16 != 0 || a.nsplit * a.upw < a.I || !a.groups || !a.x || !a.ypart)
     return hipErrorInvalidValue;
   const dim3 grid(static_cast<unsigned>(a.ngroups * a.nsplit));
   if (start || stop)
