@@ -313,8 +313,11 @@ spp_status spp_set_copy_engine(spp_ctx* ctx, int32_t engine);
 /* Storage-speed emulation ("Storage Sensitivity", Figure 5): every expert
  * copy is preceded, on each copy stream, by a bounded busy kernel of about
  * delay_us (0..100000), so one expert takes delay_us plus its transfer --
- * the offload tier behaves like slower storage behind the same link.
- * Outputs are unchanged.  EINVAL outside the range. */
+ * the offload tier behaves like slower storage behind the same link.  The
+ * storage serves one expert at a time: while the delay is set, on-demand
+ * loads too go through the copy streams (in issue order with the
+ * prefetches) instead of the compute stream.  Outputs are unchanged.  EINVAL
+ * outside the range. */
 spp_status spp_set_tier_delay(spp_ctx* ctx, int32_t delay_us);
 
 /* Test hooks for the copy/compute fences (for tests, not for production runs).

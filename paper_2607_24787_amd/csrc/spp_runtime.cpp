@@ -110,6 +110,7 @@ struct spp_ctx {
   // test hooks
   bool poison = false;
   int32_t copy_delay_us = 0;
+  bool tier_serial = false;  // storage emulation: every expert read through the copy streams' one queue
   uint64_t wall_khz = 0;
   // last call record
   std::vector<spp::Transfer> last_loads, last_pref;
@@ -334,7 +335,7 @@ spp_status issue_inline(spp_ctx* c, LayerState& ls, const std::vector<spp::Trans
 // The on-demand loads of one round: on the compute stream (SPP_COPY_SPLIT) or
 // on the copy streams after `war`.
 spp_status issue_demand(spp_ctx* c, LayerState& ls, const std::vector<spp::Transfer>& xs, hipEvent_t war) {
-  if (c->copy_engine == SPP_COPY_SPLIT) return issue_inline(c, ls, xs);
+  if (c->copy_engine == SPP_COPY_SPLIT && !c->tier_serial) return issue_inline(c, ls, xs);
   return issue_copies(c, ls, xs, war, true);
 }
 
@@ -1205,7 +1206,11 @@ spp_status spp_debug_set_poison(spp_ctx* c, int32_t enabled) {
   return SPP_OK;
 }
 
-spp_status spp_set_tier_delay(spp_ctx* c, int32_t delay_us) { return spp_debug_set_copy_delay(c, delay_us); }
+spp_status spp_set_tier_delay(spp_ctx* c, int32_t delay_us) {
+  if (spp_status s = spp_debug_set_copy_delay(c, delay_us)) return s;
+  c->tier_serial = delay_us > 0;
+  return SPP_OK;
+}
 
 spp_status spp_debug_set_copy_delay(spp_ctx* c, int32_t delay_us) {
   if (spp_status s = check_ctx(c)) return s;

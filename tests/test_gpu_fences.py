@@ -34,13 +34,15 @@ def torch_cuda():
     return torch
 
 
-def _run(cfg, M_max, tokens, poison=False, delay_us=0, engine=2):
+def _run(cfg, M_max, tokens, poison=False, delay_us=0, engine=2, tier_us=0):
     from paper_2607_24787_amd import spp
     from paper_2607_24787_amd.model import OffloadedMoEStack
     h0 = gen.hidden_states(cfg, tokens=tokens)
     st = OffloadedMoEStack(cfg)
     try:
         spp.spp_set_copy_engine(st.ctx, engine)
+        if tier_us:
+            spp.spp_set_tier_delay(st.ctx, tier_us)
         spp.spp_debug_set_poison(st.ctx, poison)
         spp.spp_debug_set_copy_delay(st.ctx, delay_us)
         outs, on_time, needed, misses = [], 0, 0, 0
@@ -102,3 +104,15 @@ def test_repeat_runs_are_bitwise_identical(torch_cuda):
         c, _, _, _ = _run(cfg, cfg.window, 6, poison=True, engine=engine)
         assert np.array_equal(a, c), engine
 
+
+@pytest.mark.parametrize("cfg,M_max,tokens", [(RAGGED, 2, 12), (BATCH_ROUNDS, 2, 6)], ids=["ragged", "batched_rounds"])
+def test_storage_emulation_leaves_outputs_unchanged(torch_cuda, cfg, M_max, tokens):
+    """Under storage emulation every expert read (on-demand loads included)
+    goes through the copy streams' one queue, each behind its delay; outputs
+    stay bitwise those of the default run."""
+    _log(f"[tier] {cfg.name}")
+    ref, _, needed, misses = _run(cfg, M_max, tokens)
+    assert misses > 0
+    out, on_time, needed2, _ = _run(cfg, M_max, tokens, poison=True, tier_us=300)
+    assert needed2 == needed and on_time < needed
+    assert np.array_equal(out, ref)
