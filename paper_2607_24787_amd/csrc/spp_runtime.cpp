@@ -93,6 +93,8 @@ struct spp_ctx {
   uint32_t router_seq = 0;  // last sequence number handed to a router launch
   int32_t prefetch_source = SPP_PREFETCH_ADAPTER;
   int32_t copy_engine = SPP_COPY_SPLIT;
+  hipEvent_t demand_done = nullptr;  // on the compute stream after the latest on-demand copy kernels
+  bool demand_done_valid = false;
   unsigned* counter = nullptr;
   float* partial = nullptr;    // [ffn_max_grid, D]
   uint8_t* probe_dev = nullptr;  // one blob, for copy profiling
@@ -251,14 +253,24 @@ hipError_t copy_part(spp_ctx* c, const LayerState& ls, uint8_t* dst, size_t src_
 // (the streams are in order); otherwise prefetches, consumed one by one, each
 // with its own event.  An event wait costs the host ~14 us while the event is
 // pending, ~0.2 us once it completed, so every wait is preceded by a query.
+spp_status copy_streams_wait(spp_ctx* c, hipEvent_t e) {
+  if (e && hipEventQuery(e) != hipSuccess) {
+    SPP_HIP(hipStreamWaitEvent(c->copy, e, 0));
+    SPP_HIP(hipStreamWaitEvent(c->copy2, e, 0));
+  }
+  return SPP_OK;
+}
+
 spp_status issue_copies(spp_ctx* c, LayerState& ls, const std::vector<spp::Transfer>& xs, hipEvent_t war,
                         bool demand) {
   if (xs.empty()) return SPP_OK;
   // WAR on slot reuse, unless the last kernel that read this layer already finished
-  if (war && hipEventQuery(war) != hipSuccess) {
-    SPP_HIP(hipStreamWaitEvent(c->copy, war, 0));
-    SPP_HIP(hipStreamWaitEvent(c->copy2, war, 0));
-  }
+  if (spp_status e = copy_streams_wait(c, war)) return e;
+  // prefetches start once the on-demand loads on the compute stream are done:
+  // both cross the same host link, and the on-demand loads are the ones the
+  // next kernel waits for
+  if (!demand && c->demand_done_valid)
+    if (spp_status e = copy_streams_wait(c, c->demand_done)) return e;
   const int32_t last = xs.back().slot;
   // each blob in two halves, one per copy stream (the split is 4 KiB aligned)
   const size_t half = (c->blob_bytes / 2 + 4095) / 4096 * 4096;
@@ -329,6 +341,8 @@ spp_status issue_inline(spp_ctx* c, LayerState& ls, const std::vector<spp::Trans
     c->stats.copies += 1;
     c->stats.copy_bytes += static_cast<int64_t>(c->blob_bytes);
   }
+  SPP_HIP(hipEventRecord(c->demand_done, c->compute));
+  c->demand_done_valid = true;
   return SPP_OK;
 }
 
@@ -385,6 +399,7 @@ void free_ctx(spp_ctx* c) {
   if (c->have_prev) destroy_set(c->prev);
   for (hipEvent_t e : c->round_done)
     if (e) (void)hipEventDestroy(e);
+  if (c->demand_done) (void)hipEventDestroy(c->demand_done);
   for (void* p : {static_cast<void*>(c->u_dev), static_cast<void*>(c->x_dev), static_cast<void*>(c->zbuf),
                   static_cast<void*>(c->res_dev), static_cast<void*>(c->counter), static_cast<void*>(c->partial),
                   static_cast<void*>(c->probe_dev)})
@@ -413,6 +428,7 @@ spp_status create_impl(const spp_model_desc* desc, void* stream, spp_ctx** out) 
   c->stride = round_up(c->blob_bytes, 4096);
   SPP_HIP(hipStreamCreateWithFlags(&c->copy, hipStreamNonBlocking));
   SPP_HIP(hipStreamCreateWithFlags(&c->copy2, hipStreamNonBlocking));
+  SPP_HIP(hipEventCreateWithFlags(&c->demand_done, hipEventDisableTiming));
   const spp_model_desc& d = c->d;
   c->layers.resize(d.L);
   for (LayerState& ls : c->layers) {
@@ -813,7 +829,8 @@ spp_status layer_forward_impl(spp_ctx* c, int32_t l, const void* h_in, void* h_o
     SPP_HIP(hipEventRecord(ts.ev[kEvEnd], c->compute));
     c->pending_sets.push_back(ts);
   }
-  // prefetches for layer l+1, behind every on-demand load on the copy streams
+  // prefetches for layer l+1, behind every on-demand load (in copy-stream
+  // order, or after the completion of the copy kernels on the compute stream)
   // and after the FFN launch (the host time they take then overlaps the FFN)
   if (nx && !c->last_pref.empty())
     if (spp_status e = issue_copies(c, *nx, c->last_pref, nx->last_read_valid ? nx->last_read : nullptr, false))
