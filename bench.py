@@ -114,6 +114,15 @@ def run_mode(stack, dev_h, row_bytes, warmup, steps, M_max, naive=False):
         "window_us": rs.window_us / rs.window_samples if rs.window_samples else None,
         "compute_window_us": rs.compute_window_us / rs.window_samples if rs.window_samples else None,
         "combine_us_per_layer": rs.tail_us / max(rs.layer_calls, 1),
+        "exposed_breakdown_pct": {
+            "on_demand_loads": 100.0 * rs.exposed_load_us / rs.span_us if rs.span_us > 0 else None,
+            "copy_stream_waits": 100.0 * rs.exposed_wait_us / rs.span_us if rs.span_us > 0 else None},
+        "expert_recall": ({f"@{M}": rs.recall_hits[j] / (cfg.K * rs.recall_tokens)
+                           for j, M in enumerate((max(cfg.K // 2, 1), cfg.K, cfg.K + 2))}
+                          if rs.recall_tokens else None),
+        "demand_exceeds_budget": ({f"top{M}": rs.demand_exceeds[j] / rs.pred_events
+                                   for j, M in enumerate((max(cfg.K // 2, 1), cfg.K, cfg.K + 2))}
+                                  if rs.pred_events else None),
     }
 
 
@@ -278,6 +287,12 @@ def main():
     on = run_mode(stack, dev_h, row_bytes, args.warmup, args.steps, cfg.window)
     _log(f"[bench] ON  {on['tokens_per_s']:.1f} tok/s coverage={on['next_layer_coverage']:.3f} "
          f"exposed={on['exposed_transfer_pct']:.1f}% ffn={on['ffn_kernel_us']:.2f}us")
+    if on["expert_recall"]:
+        _log("[bench] ON  expert recall " + " ".join(f"{k}={v:.3f}" for k, v in on["expert_recall"].items())
+             + "; predictions with more missing than M_max: "
+             + " ".join(f"{k}={v:.2f}" for k, v in on["demand_exceeds_budget"].items())
+             + "; exposed = on-demand loads {on_demand_loads:.1f}% + copy-stream waits {copy_stream_waits:.1f}%"
+             .format(**on["exposed_breakdown_pct"]))
     modes = {"on": on}
     if args.ablation:
         for name, M, naive in (("pred0", 0, False), ("off", -1, False), ("naive", cfg.window, True)):
@@ -346,6 +361,9 @@ def main():
                    "offload_tier": "pinned host DRAM", "expert_bytes": cfg.blob_bytes},
         "next_layer_coverage": on["next_layer_coverage"],
         "exposed_transfer_pct": on["exposed_transfer_pct"],
+        "exposed_breakdown_pct": on["exposed_breakdown_pct"],
+        "expert_recall": on["expert_recall"],
+        "demand_exceeds_budget": on["demand_exceeds_budget"],
         "roofline": {"kernel": kernel + " (routed-expert SwiGLU FFN)", "bound": "hbm",
                      "achieved": achieved, "peak": HBM_PEAK_GBS, "unit": "GB/s", "frac": achieved / HBM_PEAK_GBS,
                      "traffic": traffic, "bytes_per_launch": ffn_bytes, "avg_launch_us": on["ffn_kernel_us"]},

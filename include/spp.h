@@ -115,6 +115,23 @@ typedef struct {
   double span_us;     /* first layer start to last layer end */
   double window_us;   /* sum over layer pairs of W_l = t_exec(l+1) - t_pred(l) */
   double compute_window_us;  /* the same minus the copy stalls of both layers inside it */
+  /* exposed_us split in two: on-demand copy kernels on the compute stream
+   * (with the later rounds of a multi-round step), and waits for copies on
+   * the copy streams (prefetches in flight; every load when loads go by DMA) */
+  double exposed_load_us;
+  double exposed_wait_us;
+  /* ExpertRecall@M (section "Evaluation Metrics"), counted while timing is on:
+   * over the tokens of every layer that a prediction targeted, the sum of
+   * |T_b cap Top_M(s)| for M = K/2, K, K+2 (Top_M by s descending, lower
+   * index first; M at most n); ExpertRecall@M = recall_hits[j] / (K * recall_tokens) */
+  int64_t recall_tokens;
+  int64_t recall_hits[3];
+  /* Demand against the window (section "Introduction"), counted while timing
+   * is on: adapter predictions made, and of those the ones where more than
+   * M_max of Top_M(s), M = K/2, K, K+2 (at most n), were not available in
+   * layer l+1 when the prediction was made */
+  int64_t pred_events;
+  int64_t demand_exceeds[3];
 } spp_run_stats;
 
 /* ---------------------------------------------------------------- lifecycle */

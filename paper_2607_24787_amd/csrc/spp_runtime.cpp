@@ -34,8 +34,18 @@ spp_status fail(spp_status s, const std::string& m) {
 
 // Per layer call: start, routing result on the host, before/after the copy
 // waits, FFN kernel begin/end (stamped by the kernel dispatch), end.
-constexpr int kEvStart = 0, kEvRouted = 1, kEvWaitA = 2, kEvWaitB = 3, kEvFfnBegin = 4, kEvFfnEnd = 5, kEvEnd = 6;
-constexpr int kNumEv = 7;
+constexpr int kEvStart = 0, kEvRouted = 1, kEvWaitA = 2, kEvWaitB = 3, kEvFfnBegin = 4, kEvFfnEnd = 5, kEvEnd = 6,
+              kEvLoaded = 7;  // after the on-demand loads enqueued on the compute stream, before the copy waits
+constexpr int kNumEv = 8;
+
+// Events recorded on the compute stream by default end with a system-scope
+// release (an L2 writeback) that stalls the stream for 10-20 us after kernels
+// that wrote a lot.  Events that only order copy-stream work after compute
+// work (no data written before them is read by another agent through them)
+// and timing events (read after the streams synchronised) skip it.  The
+// per-slot copy events keep the default: the FFN reads the copied data.
+constexpr unsigned kOrderEventFlags = hipEventDisableTiming | hipEventDisableSystemFence;
+constexpr unsigned kTimingEventFlags = hipEventDisableSystemFence;
 
 struct TimingSet {
   hipEvent_t ev[kNumEv] = {};
@@ -122,6 +132,8 @@ struct spp_ctx {
   bool last_s_valid = false;
   // timing
   bool timing = false;
+  std::vector<int32_t> pred_top;  // Top_{K+2}(s) of the last prediction (timing only), for layer pred_target
+  int32_t pred_target = -1;
   std::vector<TimingSet> pending_sets, free_sets;
   bool have_prev = false;
   TimingSet prev{};
@@ -188,7 +200,7 @@ spp_status take_set(spp_ctx* c, TimingSet* out) {
     return SPP_OK;
   }
   TimingSet s;
-  for (int i = 0; i < kNumEv; ++i) SPP_HIP(hipEventCreate(&s.ev[i]));
+  for (int i = 0; i < kNumEv; ++i) SPP_HIP(hipEventCreateWithFlags(&s.ev[i], kTimingEventFlags));
   *out = s;
   return SPP_OK;
 }
@@ -206,9 +218,12 @@ void harvest(spp_ctx* c, size_t count) {
     spp_run_stats& st = c->stats;
     st.router_us += 1e3 * elapsed(s.ev[kEvStart], s.ev[kEvRouted]);
     const double exposed = 1e3 * elapsed(s.ev[kEvWaitA], s.ev[kEvWaitB]);
+    const double loads = 1e3 * elapsed(s.ev[kEvWaitA], s.ev[kEvLoaded]);
     double extra = 0.0;
     for (int32_t q = 0; q + 1 < s.extra_used; q += 2) extra += 1e3 * elapsed(s.extra[q], s.extra[q + 1]);
     st.exposed_us += exposed + extra;
+    st.exposed_load_us += loads + extra;
+    st.exposed_wait_us += exposed - loads;
     st.ffn_us += 1e3 * elapsed(s.ev[kEvFfnBegin], s.ev[kEvFfnEnd]) - extra;
     st.tail_us += 1e3 * elapsed(s.ev[kEvFfnEnd], s.ev[kEvEnd]);
     if (c->have_prev) {
@@ -428,7 +443,7 @@ spp_status create_impl(const spp_model_desc* desc, void* stream, spp_ctx** out) 
   c->stride = round_up(c->blob_bytes, 4096);
   SPP_HIP(hipStreamCreateWithFlags(&c->copy, hipStreamNonBlocking));
   SPP_HIP(hipStreamCreateWithFlags(&c->copy2, hipStreamNonBlocking));
-  SPP_HIP(hipEventCreateWithFlags(&c->demand_done, hipEventDisableTiming));
+  SPP_HIP(hipEventCreateWithFlags(&c->demand_done, kOrderEventFlags));
   const spp_model_desc& d = c->d;
   c->layers.resize(d.L);
   for (LayerState& ls : c->layers) {
@@ -442,7 +457,7 @@ spp_status create_impl(const spp_model_desc* desc, void* stream, spp_ctx** out) 
     for (int32_t j = 0; j < d.S; ++j) ls.slot_event[j] = j;
     for (hipEvent_t& e : ls.slot_ready) SPP_HIP(hipEventCreateWithFlags(&e, hipEventDisableTiming));
     for (hipEvent_t& e : ls.slot_ready2) SPP_HIP(hipEventCreateWithFlags(&e, hipEventDisableTiming));
-    SPP_HIP(hipEventCreateWithFlags(&ls.last_read, hipEventDisableTiming));
+    SPP_HIP(hipEventCreateWithFlags(&ls.last_read, kOrderEventFlags));
   }
   const size_t BD = static_cast<size_t>(d.max_batch) * d.D;
   if (hipMalloc(&c->u_dev, BD * sizeof(float)) != hipSuccess ||
@@ -534,10 +549,46 @@ spp_status wait_round(spp_ctx* c, LayerState& ls, const spp::Round& round, spp_l
   return SPP_OK;
 }
 
+// Diagnostics of an adapter prediction made at layer l for layer l+1 (timing
+// only): its Top_{K+2}(s) (s descending, lower index first; at most n) is kept
+// for scoring against layer l+1's routing, and the demand count compares the
+// experts of Top_M(s) not available in layer l+1 with the budget.
+void record_prediction(spp_ctx* c, int32_t l, const float* s, int32_t M_max) {
+  const spp_model_desc& d = c->d;
+  const int32_t top = std::min(d.n, d.K + 2);
+  std::vector<int32_t> idx(d.n);
+  for (int32_t e = 0; e < d.n; ++e) idx[e] = e;
+  std::partial_sort(idx.begin(), idx.begin() + top, idx.end(),
+                    [s](int32_t a, int32_t b) { return s[a] > s[b] || (s[a] == s[b] && a < b); });
+  c->pred_top.assign(idx.begin(), idx.begin() + top);
+  c->pred_target = l + 1;
+  const spp::SlotPolicy& nxp = *c->layers[l + 1].policy;
+  const int32_t Ms[3] = {std::max(d.K / 2, 1), d.K, d.K + 2};
+  for (int j = 0; j < 3; ++j) {
+    int32_t missing = 0;
+    for (int32_t i = 0; i < std::min(Ms[j], top); ++i) missing += nxp.slot_of(c->pred_top[i]) < 0;
+    c->stats.demand_exceeds[j] += missing > std::max(M_max, 0);
+  }
+  c->stats.pred_events += 1;
+}
+
+void score_prediction(spp_ctx* c, const int32_t* T, int32_t B) {
+  const spp_model_desc& d = c->d;
+  const int32_t Ms[3] = {std::max(d.K / 2, 1), d.K, d.K + 2};
+  for (int32_t b = 0; b < B; ++b)
+    for (int j = 0; j < 3; ++j) {
+      const int32_t M = std::min<int32_t>(Ms[j], static_cast<int32_t>(c->pred_top.size()));
+      for (int32_t k = 0; k < d.K; ++k)
+        c->stats.recall_hits[j] +=
+            std::find(c->pred_top.begin(), c->pred_top.begin() + M, T[b * d.K + k]) != c->pred_top.begin() + M;
+    }
+  c->stats.recall_tokens += B;
+}
+
 spp_status record_extra(spp_ctx* c, TimingSet& ts) {
   if (ts.extra_used >= static_cast<int32_t>(ts.extra.size())) {
     hipEvent_t e;
-    SPP_HIP(hipEventCreate(&e));
+    SPP_HIP(hipEventCreateWithFlags(&e, kTimingEventFlags));
     ts.extra.push_back(e);
   }
   SPP_HIP(hipEventRecord(ts.extra[ts.extra_used++], c->compute));
@@ -547,7 +598,7 @@ spp_status record_extra(spp_ctx* c, TimingSet& ts) {
 spp_status round_event(spp_ctx* c, size_t r, hipEvent_t* out) {
   while (c->round_done.size() <= r) {
     hipEvent_t e;
-    SPP_HIP(hipEventCreateWithFlags(&e, hipEventDisableTiming));
+    SPP_HIP(hipEventCreateWithFlags(&e, kOrderEventFlags));
     c->round_done.push_back(e);
   }
   *out = c->round_done[r];
@@ -715,6 +766,8 @@ spp_status layer_forward_impl(spp_ctx* c, int32_t l, const void* h_in, void* h_o
   const float* g = reinterpret_cast<const float*>(c->res_host + c->off_gates);
   const float* s = reinterpret_cast<const float*>(c->res_host + c->off_s);
   const int32_t BK = B * d.K;
+  if (c->timing && c->pred_target == l) score_prediction(c, T, B);
+  c->pred_target = -1;
   std::vector<float> s_naive;
   if (naive && predict) {
     // gate mass of each expert of layer l+1 at its preceding step (fp64 in
@@ -762,6 +815,7 @@ spp_status layer_forward_impl(spp_ctx* c, int32_t l, const void* h_in, void* h_o
       if (t.round == 0) first.push_back(t);
     if (spp_status e = issue_demand(c, ls, first, ls.last_read_valid ? ls.last_read : nullptr)) return e;
   }
+  if (c->timing) SPP_HIP(hipEventRecord(ts.ev[kEvLoaded], c->compute));
 
   // prefetch selection for layer l+1 (the copies are enqueued after this
   // layer's loads); the adapter's priorities have their own flag
@@ -772,6 +826,7 @@ spp_status layer_forward_impl(spp_ctx* c, int32_t l, const void* h_in, void* h_o
   c->last_s_valid = predict;
   c->last_B = B;
   c->logits_valid = !(adapter_on && B > 1);  // the batched selection overwrites logits with pi_hat
+  if (adapter_on && c->timing) record_prediction(c, l, s, M_max);
   if (predict) {
     std::memcpy(c->last_s.data(), s, sizeof(float) * d.n);
     if (nx) {
@@ -1194,6 +1249,7 @@ spp_status spp_reset_run_stats(spp_ctx* c) {
     c->have_prev = false;
   }
   c->stats = spp_run_stats{};
+  c->pred_target = -1;
   return SPP_OK;
 }
 

@@ -44,10 +44,17 @@ class RunStats(ctypes.Structure):
                                          "ready_on_time", "copies", "copy_bytes", "ffn_launches",
                                          "window_samples")]
                 + [(f, c_double) for f in ("router_us", "exposed_us", "ffn_us", "tail_us", "span_us",
-                                           "window_us", "compute_window_us")])
+                                           "window_us", "compute_window_us", "exposed_load_us",
+                                           "exposed_wait_us")]
+                + [("recall_tokens", c_int64), ("recall_hits", c_int64 * 3), ("pred_events", c_int64),
+                   ("demand_exceeds", c_int64 * 3)])
 
     def as_dict(self):
-        return {f: getattr(self, f) for f, _ in self._fields_}
+        out = {}
+        for f, _ in self._fields_:
+            v = getattr(self, f)
+            out[f] = list(v) if isinstance(v, ctypes.Array) else v
+        return out
 
 
 _SIGS = {

@@ -383,3 +383,54 @@ def test_last_logits_match_the_oracle(torch_cuda):
                 assert e.value.status == spp.SPP_ESTATE
         finally:
             st.close()
+
+
+@pytest.mark.parametrize("cfg,M_max", [
+    (w.get("c0"), 1),
+    (w.get("c0"), 0),
+    (w.get("c0"), 3),
+    (BATCH.with_(S=9), 2),
+], ids=["c0_M1", "c0_pred0", "c0_M3", "batch3_S9_M2"])
+def test_run_statistics_match_the_oracle(torch_cuda, cfg, M_max):
+    """The timing pass's counters (ExpertRecall@M, predictions whose missing
+    top-M experts exceed the budget, next-layer coverage, loads, prefetches and
+    used prefetches) equal the oracle's on the same free-running decode, whose
+    routing the device reproduces step by step (fp32 configurations)."""
+    from paper_2607_24787_amd import spp
+    W = o.OracleWeights(cfg)
+    h0 = gen.hidden_states(cfg)
+    ref = o.run_decode(cfg, W, h0, M_max, tokens=cfg.tokens)
+    st = _stack(cfg)
+    try:
+        spp.spp_set_timing(st.ctx, 1)
+        spp.spp_reset_run_stats(st.ctx)
+        token_hits_target = 0
+        i = 0
+        for t in range(cfg.tokens):
+            out = st.step(h0[t], M_max)
+            for l in range(cfg.L):
+                T = np.asarray(out[l][0]).reshape(cfg.batch, cfg.K)
+                want = ref.steps[i].T
+                assert all(sorted(T[b].tolist()) == sorted(want[b].tolist()) for b in range(cfg.batch)), \
+                    f"routing differs at token {t}, layer {l}"
+                if l >= 1:
+                    token_hits_target += out[l][2].token_hits
+                i += 1
+        rs = spp.spp_get_run_stats(st.ctx)
+    finally:
+        st.close()
+    Ms = sorted(set(m for m in (max(1, cfg.K // 2), cfg.K, cfg.K + 2) if m <= cfg.n))
+    _log(f"[stats {cfg.name} M_max={M_max}] recall={ref.expert_recall} demand={ref.demand_exceeds} "
+         f"device hits={list(rs.recall_hits)} tokens={rs.recall_tokens} demand={list(rs.demand_exceeds)} "
+         f"events={rs.pred_events}")
+    assert rs.recall_tokens == cfg.batch * cfg.tokens * (cfg.L - 1)
+    assert rs.pred_events == cfg.tokens * (cfg.L - 1)
+    for j, m in enumerate(Ms):
+        assert rs.recall_hits[j] / (cfg.K * rs.recall_tokens) == pytest.approx(ref.expert_recall[m], abs=1e-12)
+        assert rs.demand_exceeds[j] / rs.pred_events == pytest.approx(ref.demand_exceeds[m], abs=1e-12)
+    assert token_hits_target / (cfg.K * cfg.batch * cfg.tokens * (cfg.L - 1)) == \
+        pytest.approx(ref.ready_recall, abs=1e-12)
+    assert (rs.misses, rs.prefetched, rs.prefetch_used) == (ref.loads, ref.prefetched, ref.prefetch_used)
+    # the exposed time splits into its two parts
+    assert rs.exposed_load_us >= 0.0 and rs.exposed_wait_us >= -1.0
+    assert rs.exposed_load_us + rs.exposed_wait_us == pytest.approx(rs.exposed_us, rel=1e-6, abs=1e-3)
