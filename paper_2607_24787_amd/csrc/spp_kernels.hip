@@ -742,7 +742,8 @@ __global__ __launch_bounds__(kFfnThreads) void ffn_units_kernel(FfnArgs a) {
 // (h scale) q per element and subtracts 8 * sum(h scale) per block at the end.
 // Work list, wave order and the workgroup partials as in ffn_units_kernel.
 // ---------------------------------------------------------------------------
-constexpr int kQ4Upp = 3;  // units per wave and pass; the launch gives each workgroup kFfnWaves * kQ4Upp units
+constexpr int kQ4Upp = 3;  // units per wave and pass; the launch gives each workgroup whole passes
+constexpr int kQ4TargetWgs = 256;
 
 __device__ __forceinline__ float q4_scale(uint16_t bits) {
   return static_cast<float>(__builtin_bit_cast(_Float16, bits));
@@ -1684,11 +1685,15 @@ void set_ffn_target_wgs(int wgs) { g_ffn_target_wgs = wgs > 0 ? wgs : 512; }
 
 // Units per workgroup so that about g_ffn_target_wgs workgroups share the work.
 int ffn_grid_q4(int nunits, int* upw) {
-  // whole passes of kQ4Upp units per wave; more passes once the grid would
-  // exceed the partial buffer (ffn_max_grid rows)
+  // whole passes of kQ4Upp units per wave, as many as keep the grid near 256
+  // workgroups: a wave's later passes then load while its earlier ones decode
+  // (one launch over 8 experts of the Qwen shape: 17.4 us at 512 workgroups of
+  // one pass, 13.9 us at 256 of two); at least as many as keep the grid within
+  // the partial buffer (ffn_max_grid rows)
   const int pass = kFfnWaves * kQ4Upp;
-  const int passes = (nunits + pass * 4096 - 1) / (pass * 4096);
-  *upw = pass * (passes > 0 ? passes : 1);
+  int passes = (nunits + pass * kQ4TargetWgs - 1) / (pass * kQ4TargetWgs);
+  passes = std::max(passes, (nunits + pass * 4096 - 1) / (pass * 4096));
+  *upw = pass * std::max(passes, 1);
   return (nunits + *upw - 1) / *upw;
 }
 
