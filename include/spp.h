@@ -132,6 +132,9 @@ typedef struct {
    * layer l+1 when the prediction was made */
   int64_t pred_events;
   int64_t demand_exceeds[3];
+  /* the same predictions by how many of Top_M(s) were not available:
+   * demand_hist[j][c] counts c missing experts (c = 16 counts 16 or more) */
+  int64_t demand_hist[3][17];
 } spp_run_stats;
 
 /* ---------------------------------------------------------------- lifecycle */

@@ -568,6 +568,7 @@ void record_prediction(spp_ctx* c, int32_t l, const float* s, int32_t M_max) {
     int32_t missing = 0;
     for (int32_t i = 0; i < std::min(Ms[j], top); ++i) missing += nxp.slot_of(c->pred_top[i]) < 0;
     c->stats.demand_exceeds[j] += missing > std::max(M_max, 0);
+    c->stats.demand_hist[j][std::min(missing, 16)] += 1;
   }
   c->stats.pred_events += 1;
 }

@@ -47,13 +47,14 @@ class RunStats(ctypes.Structure):
                                            "window_us", "compute_window_us", "exposed_load_us",
                                            "exposed_wait_us")]
                 + [("recall_tokens", c_int64), ("recall_hits", c_int64 * 3), ("pred_events", c_int64),
-                   ("demand_exceeds", c_int64 * 3)])
+                   ("demand_exceeds", c_int64 * 3), ("demand_hist", (c_int64 * 17) * 3)])
 
     def as_dict(self):
         out = {}
         for f, _ in self._fields_:
             v = getattr(self, f)
-            out[f] = list(v) if isinstance(v, ctypes.Array) else v
+            out[f] = ([list(r) if isinstance(r, ctypes.Array) else r for r in v] if isinstance(v, ctypes.Array)
+                      else v)
         return out
 
 

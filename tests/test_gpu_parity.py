@@ -428,6 +428,11 @@ def test_run_statistics_match_the_oracle(torch_cuda, cfg, M_max):
     for j, m in enumerate(Ms):
         assert rs.recall_hits[j] / (cfg.K * rs.recall_tokens) == pytest.approx(ref.expert_recall[m], abs=1e-12)
         assert rs.demand_exceeds[j] / rs.pred_events == pytest.approx(ref.demand_exceeds[m], abs=1e-12)
+        hist = [0] * 17
+        for step in ref.steps:
+            if step.demand is not None:
+                hist[min(step.demand[m], 16)] += 1
+        assert list(rs.demand_hist[j]) == hist
     assert token_hits_target / (cfg.K * cfg.batch * cfg.tokens * (cfg.L - 1)) == \
         pytest.approx(ref.ready_recall, abs=1e-12)
     assert (rs.misses, rs.prefetched, rs.prefetch_used) == (ref.loads, ref.prefetched, ref.prefetch_used)
