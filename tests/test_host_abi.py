@@ -219,3 +219,25 @@ def test_pack_expert_q4_places_codes_and_scales_where_the_header_says():
         args.update(kw)
         with pytest.raises(spp.SppError):
             spp.spp_create(spp.make_desc(**args), 0)
+
+
+@pytest.mark.parametrize("cname,pyname", [("spp_model_desc", "ModelDesc"), ("spp_layer_stats", "LayerStats"),
+                                          ("spp_run_stats", "RunStats")])
+def test_binding_structs_match_the_header_layout(cname, pyname, tmp_path):
+    """The ctypes structures have the size and field offsets a C compiler gives
+    the header's structs (compiled here with gcc as plain C)."""
+    import shutil
+    import subprocess
+    if shutil.which("gcc") is None:
+        pytest.skip("no C compiler")
+    py = getattr(spp, pyname)
+    fields = [f for f, _ in py._fields_]
+    lines = [f'  printf("%zu\\n", offsetof({cname}, {f}));' for f in fields]
+    src = tmp_path / "layout.c"
+    src.write_text("#include <stddef.h>\n#include <stdio.h>\n#include \"spp.h\"\nint main(void) {\n"
+                   f'  printf("%zu\\n", sizeof({cname}));\n' + "\n".join(lines) + "\n  return 0;\n}\n")
+    exe = tmp_path / "layout"
+    subprocess.run(["gcc", "-std=c99", "-I", os.path.join(ROOT, "include"), str(src), "-o", str(exe)], check=True)
+    out = [int(v) for v in subprocess.run([str(exe)], check=True, capture_output=True, text=True).stdout.split()]
+    assert out[0] == ctypes.sizeof(py)
+    assert out[1:] == [getattr(py, f).offset for f in fields]
