@@ -309,9 +309,10 @@ spp_status spp_profile_expert_copy(spp_ctx* ctx, int32_t l, int32_t reps, double
  * call: nothing is prefetched).  EINVAL for an unknown source. */
 spp_status spp_set_prefetch_source(spp_ctx* ctx, int32_t source);
 
-/* Launch shape of the routed-expert FFN: about `wgs` workgroups share the
- * (expert, unit) work list of one token (default 512; 1..4096).  Applies to
- * every context in the process. */
+/* Launch shape of this context's batch-1 routed-expert FFN over bf16/fp32
+ * experts: about `wgs` workgroups share the (expert, unit) work list of one
+ * token (default 512; 1..4096).  The 4-bit and batched FFNs choose their own
+ * grids. */
 spp_status spp_set_ffn_workgroups(spp_ctx* ctx, int32_t wgs);
 
 /* Engine of the expert copies from the offload tier.  A copy kernel reads

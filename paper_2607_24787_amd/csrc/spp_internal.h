@@ -112,10 +112,12 @@ struct CopyList {
 };
 hipError_t launch_h2d_copies(const CopyList& list, int wgs, hipStream_t st);
 hipError_t launch_spin(uint64_t ticks, uint32_t max_iter, hipStream_t st);
-int ffn_grid_for(int nunits, int* upw);
-// 4-bit experts: one pass per wave, kFfnWaves * 3 units per workgroup.
+// Batch-1 FFN launch over `nunits` (expert, unit) pairs: units per workgroup
+// (*upw) so that about `target_wgs` workgroups share the work; returns the grid.
+int ffn_grid_for(int nunits, int target_wgs, int* upw);
+// 4-bit experts: whole passes of kFfnWaves * 3 units per workgroup, as many as
+// keep the grid near 256 workgroups.
 int ffn_grid_q4(int nunits, int* upw);
 size_t ffn_max_grid();
-void set_ffn_target_wgs(int wgs);
 
 }  // namespace spp

@@ -1592,8 +1592,6 @@ hipError_t proj_t(const ProjArgs& a, hipStream_t st) {
   return full_rows<T>(a.D) ? proj_tf<T, true>(a, st) : proj_tf<T, false>(a, st);
 }
 
-int g_ffn_target_wgs = 512;
-
 }  // namespace
 
 hipError_t launch_router(const RouterArgs& a, int dtype, hipStream_t st) {
@@ -1681,9 +1679,6 @@ hipError_t launch_spin(uint64_t ticks, uint32_t max_iter, hipStream_t st) {
   return hipGetLastError();
 }
 
-void set_ffn_target_wgs(int wgs) { g_ffn_target_wgs = wgs > 0 ? wgs : 512; }
-
-// Units per workgroup so that about g_ffn_target_wgs workgroups share the work.
 int ffn_grid_q4(int nunits, int* upw) {
   // whole passes of kQ4Upp units per wave, as many as keep the grid near 256
   // workgroups: a wave's later passes then load while its earlier ones decode
@@ -1697,9 +1692,9 @@ int ffn_grid_q4(int nunits, int* upw) {
   return (nunits + *upw - 1) / *upw;
 }
 
-int ffn_grid_for(int nunits, int* upw) {
+int ffn_grid_for(int nunits, int target_wgs, int* upw) {
   int grid = (nunits + kFfnWaves - 1) / kFfnWaves;
-  if (grid > g_ffn_target_wgs) grid = g_ffn_target_wgs;
+  if (grid > target_wgs) grid = target_wgs;
   if (grid < 1) grid = 1;
   *upw = (nunits + grid - 1) / grid;
   return (nunits + *upw - 1) / *upw;

@@ -118,7 +118,7 @@ struct spp_ctx {
   float* ypart = nullptr;
   std::vector<hipEvent_t> round_done;  // per on-demand round: its FFN launch finished
   int64_t clock = 0;
-  int ffn_wgs = 256;
+  int ffn_wgs = 512;  // about this many workgroups share one batch-1 FFN launch (bf16/fp32 experts)
   // test hooks
   bool poison = false;
   int32_t copy_delay_us = 0;
@@ -865,7 +865,7 @@ spp_status layer_forward_impl(spp_ctx* c, int32_t l, const void* h_in, void* h_o
     fa.gates = gates_dev;
     fa.partial = c->partial;
     const int grid = d.expert_codec == SPP_CODEC_Q4 ? spp::ffn_grid_q4(nW * d.I, &fa.upw)
-                                                    : spp::ffn_grid_for(nW * d.I, &fa.upw);
+                                                    : spp::ffn_grid_for(nW * d.I, c->ffn_wgs, &fa.upw);
     const bool stamp = c->timing && b == B - 1;
     SPP_HIP(spp::launch_ffn(fa, grid, dt, c->compute, stamp ? ts.ev[kEvFfnBegin] : nullptr,
                             stamp ? ts.ev[kEvFfnEnd] : nullptr));
@@ -1302,7 +1302,6 @@ spp_status spp_debug_set_copy_delay(spp_ctx* c, int32_t delay_us) {
 spp_status spp_set_ffn_workgroups(spp_ctx* c, int32_t wgs) {
   if (spp_status s = check_ctx(c)) return s;
   if (wgs < 1 || static_cast<size_t>(wgs) > spp::ffn_max_grid()) return fail(SPP_EINVAL, "wgs out of range");
-  spp::set_ffn_target_wgs(wgs);
   c->ffn_wgs = wgs;
   return SPP_OK;
 }
