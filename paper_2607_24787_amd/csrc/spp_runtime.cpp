@@ -1163,6 +1163,7 @@ spp_status spp_decode_step(spp_ctx* c, const void* h_in_dev, void* h_out_dev, vo
   if (!h_in_dev || !h_out_dev || !h_scratch_dev) return fail(SPP_EINVAL, "h_in / h_out / h_scratch is NULL");
   if (h_in_dev == h_out_dev || h_in_dev == h_scratch_dev || h_out_dev == h_scratch_dev)
     return fail(SPP_EINVAL, "h_in, h_out and h_scratch must be distinct");
+  if (B < 1 || B > c->d.max_batch) return fail(SPP_EINVAL, "B must be in [1, max_batch]");
   const int32_t L = c->d.L, BK = B * c->d.K;
   for (int32_t l = 0; l < L; ++l)
     if (!c->layers[l].bound) return fail(SPP_ESTATE, "every layer must be bound");

@@ -57,6 +57,12 @@ BATCH_BF16_ROUNDS = BATCH_BF16.with_(S=6)
 QWEN_B16_S32 = w.get("c4").with_(L=2, batch=16, S=32, tokens=2)
 QWEN_B64_S32 = w.get("c4").with_(L=2, tokens=2)
 C2_TIED = w.get("c2").with_(tokens=2, expert_layers=2)
+# the largest shapes a context accepts: D 4096 (bf16) / 2048 (fp32), 1024
+# experts, top-32, adapter rank 256
+MAX_BF16 = w.MoEConfig(name="max_bf16_D4096_n1024_k32_r256", L=2, D=4096, n=1024, K=32, I=16, r=256, S=40,
+                       windows=(4,), tokens=2, seed=21)
+MAX_F32 = w.MoEConfig(name="max_f32_D2048_n1024_k32_r256", L=2, D=2048, n=1024, K=32, I=16, r=256, S=40,
+                      windows=(4,), tokens=2, dtype="f32", seed=22)
 
 
 def _assert_report(rep, cfg, name):
@@ -76,7 +82,9 @@ def _assert_report(rep, cfg, name):
     (PROJ, 2, 10),
     (BATCH, 2, 8),
     (C3_SHORT, 2, 6),
-], ids=["c0_M1", "c0_M3", "ragged", "proj", "batch3", "c3_short"])
+    (MAX_BF16, 4, 2),
+    (MAX_F32, 4, 2),
+], ids=["c0_M1", "c0_M3", "ragged", "proj", "batch3", "c3_short", "max_bf16", "max_f32"])
 def test_lockstep_parity(torch_cuda, cfg, M_max, tokens):
     from lockstep import run_lockstep
     _log(f"[lockstep] {cfg.name} M_max={M_max} tokens={tokens}")
@@ -291,6 +299,18 @@ def test_error_paths_on_device(torch_cuda):
             spp.moe_layer_forward(st.ctx, cfg.L, st.hbuf[0].data_ptr(), st.hbuf[1].data_ptr(), 1, cfg.K, 1)
         with pytest.raises(spp.SppError):
             spp.moe_layer_forward(st.ctx, 0, st.hbuf[0].data_ptr(), st.hbuf[1].data_ptr(), 2, cfg.K, 1)
+        # an empty batch, a budget below -1 and NULL buffers are refused before any device work
+        for args in ((0, 1, False), (1, -2, False), (1, 1, True)):
+            B, M, null = args
+            with pytest.raises(spp.SppError) as e:
+                spp.moe_layer_forward(st.ctx, 0, 0 if null else st.hbuf[0].data_ptr(), st.hbuf[1].data_ptr(),
+                                      B, cfg.K, M)
+            assert e.value.status == spp.SPP_EINVAL, args
+        third = st.torch.empty_like(st.hbuf[0])
+        with pytest.raises(spp.SppError) as e:
+            spp.spp_decode_step(st.ctx, cfg.L, st.hbuf[0].data_ptr(), st.hbuf[1].data_ptr(), third.data_ptr(),
+                                0, cfg.K, 1)
+        assert e.value.status == spp.SPP_EINVAL
         with pytest.raises(spp.SppError):
             spp.spp_set_resident(st.ctx, 0, [0, 0])
         for bad in (-1, 100001):
