@@ -117,6 +117,8 @@ struct spp_ctx {
                                           // router, i.e. after the previous FFN, has finished)
   float* ypart = nullptr;
   std::vector<hipEvent_t> round_done;  // per on-demand round: its FFN launch finished
+  std::vector<int32_t> grp_start, grp_fill, grp_order;  // group building scratch (per call)
+  std::vector<int> grp_rstart, grp_rcount;
   int64_t clock = 0;
   int ffn_wgs = 512;  // about this many workgroups share one batch-1 FFN launch (bf16/fp32 experts)
   // test hooks
@@ -615,36 +617,52 @@ spp_status grouped_ffn(spp_ctx* c, LayerState& ls, const int32_t* T, int32_t B,
                        const void* h_in, void* h_out, const std::vector<spp::Round>& rounds,
                        const std::vector<spp::Transfer>& loads, spp_layer_stats* st, TimingSet& ts) {
   const spp_model_desc& d = c->d;
-  std::vector<std::vector<std::pair<int32_t, int32_t>>> by_expert(d.n);  // (token, pair)
-  for (int32_t b = 0; b < B; ++b)
-    for (int32_t k = 0; k < d.K; ++k) by_expert[T[b * d.K + k]].push_back({b, b * d.K + k});
+  const int32_t BK = B * d.K;
+  // the (token, k) pairs of each expert in pair order: a stable counting sort
+  // into context scratch (pair p belongs to token p / K)
+  std::vector<int32_t>& start = c->grp_start;
+  std::vector<int32_t>& order = c->grp_order;
+  start.assign(d.n + 1, 0);
+  for (int32_t p = 0; p < BK; ++p) start[T[p] + 1] += 1;
+  for (int32_t e = 0; e < d.n; ++e) start[e + 1] += start[e];
+  c->grp_fill.assign(start.begin(), start.end() - 1);
+  order.resize(BK);
+  for (int32_t p = 0; p < BK; ++p) order[c->grp_fill[T[p]]++] = p;
   int ng = 0;
-  auto add = [&](const void* blob, const std::vector<std::pair<int32_t, int32_t>>& rows) -> bool {
-    for (size_t r0 = 0; r0 < rows.size(); r0 += spp::kGroupTokens) {
+  // groups of up to kGroupTokens rows; row i of `count` is (tok(i), pair(i))
+  auto add = [&](const void* blob, int32_t count, auto row) -> bool {
+    for (int32_t r0 = 0; r0 < count; r0 += spp::kGroupTokens) {
       if (ng >= c->max_groups) return false;
       spp::GroupDesc& g = c->groups_host[ng++];
-      std::memset(&g, 0, sizeof(g));
       g.blob = blob;
-      g.m = static_cast<int32_t>(std::min<size_t>(spp::kGroupTokens, rows.size() - r0));
-      for (int32_t t = 0; t < g.m; ++t) {
-        g.tok[t] = rows[r0 + t].first;
-        g.pair[t] = rows[r0 + t].second;
+      g.m = std::min(spp::kGroupTokens, count - r0);
+      for (int32_t t = 0; t < spp::kGroupTokens; ++t) {
+        const bool used = t < g.m;
+        const std::pair<int32_t, int32_t> tp = used ? row(r0 + t) : std::pair<int32_t, int32_t>{0, 0};
+        g.tok[t] = tp.first;
+        g.pair[t] = tp.second;
       }
+      g.pad = 0;
     }
     return true;
   };
-  std::vector<int> rstart(rounds.size()), rcount(rounds.size());
+  std::vector<int>& rstart = c->grp_rstart;
+  std::vector<int>& rcount = c->grp_rcount;
+  rstart.assign(rounds.size(), 0);
+  rcount.assign(rounds.size(), 0);
   int maxg = 0;
   for (size_t r = 0; r < rounds.size(); ++r) {
     rstart[r] = ng;
-    for (const auto& es : rounds[r])
-      if (!add(ls.slots + static_cast<size_t>(es.second) * c->stride, by_expert[es.first]))
+    for (const auto& es : rounds[r]) {
+      const int32_t* rows = order.data() + start[es.first];
+      const auto routed = [&](int32_t i) { return std::pair<int32_t, int32_t>{rows[i] / d.K, rows[i]}; };
+      if (!add(ls.slots + static_cast<size_t>(es.second) * c->stride, start[es.first + 1] - start[es.first], routed))
         return fail(SPP_ESTATE, "group list overflow");
+    }
     if (r == 0)
       for (int32_t j = 0; j < d.n_shared; ++j) {
-        std::vector<std::pair<int32_t, int32_t>> rows;
-        for (int32_t b = 0; b < B; ++b) rows.push_back({b, B * d.K + b * d.n_shared + j});
-        if (!add(static_cast<const uint8_t*>(ls.shared) + static_cast<size_t>(j) * c->stride, rows))
+        const auto shared = [&](int32_t b) { return std::pair<int32_t, int32_t>{b, BK + b * d.n_shared + j}; };
+        if (!add(static_cast<const uint8_t*>(ls.shared) + static_cast<size_t>(j) * c->stride, B, shared))
           return fail(SPP_ESTATE, "group list overflow");
       }
     rcount[r] = ng - rstart[r];
