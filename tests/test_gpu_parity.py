@@ -84,7 +84,8 @@ def _assert_report(rep, cfg, name):
     (C3_SHORT, 2, 6),
     (MAX_BF16, 4, 2),
     (MAX_F32, 4, 2),
-], ids=["c0_M1", "c0_M3", "ragged", "proj", "batch3", "c3_short", "max_bf16", "max_f32"])
+    (w.get("c1p"), 2, 4),
+], ids=["c0_M1", "c0_M3", "ragged", "proj", "batch3", "c3_short", "max_bf16", "max_f32", "qwen_calibrated"])
 def test_lockstep_parity(torch_cuda, cfg, M_max, tokens):
     from lockstep import run_lockstep
     _log(f"[lockstep] {cfg.name} M_max={M_max} tokens={tokens}")
@@ -122,8 +123,9 @@ C3Q4_SHORT = w.get("c3q4").with_(L=3, tokens=4)
 C1Q4 = w.get("c1q4")
 
 
-@pytest.mark.parametrize("cfg,M_max,tokens", [(Q4_SMALL, 2, 10), (Q4_WIDE, 1, 6), (C3Q4_SHORT, 2, 4), (C1Q4, 2, 4)],
-                         ids=["q4_small", "q4_wide", "dsv2_q4", "qwen_q4_full"])
+@pytest.mark.parametrize("cfg,M_max,tokens", [(Q4_SMALL, 2, 10), (Q4_WIDE, 1, 6), (C3Q4_SHORT, 2, 4), (C1Q4, 2, 4),
+                                              (w.get("c3pq4").with_(L=3), 2, 4)],
+                         ids=["q4_small", "q4_wide", "dsv2_q4", "qwen_q4_full", "dsv2_q4_calibrated"])
 def test_lockstep_parity_q4_experts(torch_cuda, cfg, M_max, tokens):
     from lockstep import run_lockstep
     _log(f"[lockstep q4] {cfg.name} M_max={M_max} tokens={tokens}")

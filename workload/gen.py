@@ -12,7 +12,10 @@ checkpoints; neither is available, so synthetic stand-ins take their place):
 
 * router, expert (gate, up, down), shared-expert and stand-in projection
   weights: i.i.d. N(0, w_std^2) drawn in fp32, then rounded to bf16
-  (round-to-nearest-even) for bf16 configurations;
+  (round-to-nearest-even) for bf16 configurations; with router_rank k > 0 a
+  router is instead G1 G2 w_std / sqrt(k) (G1 [n,k], G2 [k,D] i.i.d. N(0,1),
+  a rank-k matrix with entries of std w_std), and down projections (routed
+  and shared) are multiplied by update_scale;
 * adapter of layer l (l < L-1): the rank-r truncated SVD of the *next* layer's
   stored router weights, W^{l+1} = U diag(sig) V^T, split symmetrically as
   A = diag(sqrt(sig_1..r)) V_r^T and B = U_r diag(sqrt(sig_1..r)) (zero rows /
@@ -62,15 +65,24 @@ def _storage(cfg: MoEConfig, a32: np.ndarray) -> np.ndarray:
     return f32_to_bf16_bits(a32) if cfg.dtype == "bf16" else np.ascontiguousarray(a32, dtype=np.float32)
 
 
-def _normal_weights(cfg: MoEConfig, kind: int, layer: int, index: int, shape) -> np.ndarray:
+def _normal_weights(cfg: MoEConfig, kind: int, layer: int, index: int, shape, scale: float = 1.0) -> np.ndarray:
     g = _rng(cfg, kind, layer, index)
     a = g.standard_normal(int(np.prod(shape)), dtype=np.float32) * np.float32(cfg.w_std)
+    if scale != 1.0:
+        a = a * np.float32(scale)
     return _storage(cfg, a.reshape(shape))
 
 
 def router_weight(cfg: MoEConfig, layer: int) -> np.ndarray:
     """Native router weights of a layer, [n, D]."""
-    return _normal_weights(cfg, KIND_ROUTER, layer, 0, (cfg.n, cfg.D))
+    if cfg.router_rank <= 0:
+        return _normal_weights(cfg, KIND_ROUTER, layer, 0, (cfg.n, cfg.D))
+    k = cfg.router_rank
+    g = _rng(cfg, KIND_ROUTER, layer, 0)
+    g1 = g.standard_normal((cfg.n, k))
+    g2 = g.standard_normal((k, cfg.D))
+    a = (g1 @ g2) * (cfg.w_std / np.sqrt(k))
+    return _storage(cfg, a.astype(np.float32))
 
 
 def expert_weights(cfg: MoEConfig, layer: int, expert: int):
@@ -78,7 +90,7 @@ def expert_weights(cfg: MoEConfig, layer: int, expert: int):
     src = cfg.expert_layer(layer)
     return (_normal_weights(cfg, KIND_GATE, src, expert, (cfg.I, cfg.D)),
             _normal_weights(cfg, KIND_UP, src, expert, (cfg.I, cfg.D)),
-            _normal_weights(cfg, KIND_DOWN, src, expert, (cfg.D, cfg.I)))
+            _normal_weights(cfg, KIND_DOWN, src, expert, (cfg.D, cfg.I), cfg.update_scale))
 
 
 def _q4_expert(cfg: MoEConfig, kind_codes: int, kind_scales: int, layer: int, index: int):
@@ -86,7 +98,10 @@ def _q4_expert(cfg: MoEConfig, kind_codes: int, kind_scales: int, layer: int, in
     g = _rng(cfg, kind_codes, layer, index)
     codes = np.clip(np.rint(g.standard_normal((3, cfg.I, cfg.D)) * 2.5), -8, 7).astype(np.int16) + 8
     gs = _rng(cfg, kind_scales, layer, index)
-    scales = (cfg.w_std / 2.5 * gs.uniform(0.75, 1.25, size=(3, cfg.I, nb))).astype(np.float16)
+    scales = cfg.w_std / 2.5 * gs.uniform(0.75, 1.25, size=(3, cfg.I, nb))
+    if cfg.update_scale != 1.0:
+        scales[2] *= cfg.update_scale
+    scales = scales.astype(np.float16)
     # gate [I,D], its scales [I,D/32]; up alike; down [D,I] with scales [I,D/32] (blocks along D of column i)
     return (codes[0].astype(np.uint8), scales[0], codes[1].astype(np.uint8), scales[1],
             np.ascontiguousarray(codes[2].T.astype(np.uint8)), scales[2])
@@ -108,7 +123,7 @@ def shared_expert_weights(cfg: MoEConfig, layer: int, j: int):
     """Always-resident shared expert ``j`` of ``layer``: (gate [I,D], up [I,D], down [D,I])."""
     return (_normal_weights(cfg, KIND_SHARED_GATE, layer, j, (cfg.I, cfg.D)),
             _normal_weights(cfg, KIND_SHARED_UP, layer, j, (cfg.I, cfg.D)),
-            _normal_weights(cfg, KIND_SHARED_DOWN, layer, j, (cfg.D, cfg.I)))
+            _normal_weights(cfg, KIND_SHARED_DOWN, layer, j, (cfg.D, cfg.I), cfg.update_scale))
 
 
 def proj_weight(cfg: MoEConfig, layer: int) -> np.ndarray:
