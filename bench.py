@@ -362,7 +362,11 @@ def main():
         "scaling": "weak",
         "vs_baseline": None,
         "dtype": cfg.dtype,
-        "data": "synthetic (seeded AR(1) hidden states, N(0,0.02) weights, SVD-built adapters)",
+        "data": ("synthetic (seeded AR(1) hidden states, N(0,{w:g}) weights{rr}{us}{q4}, SVD-built adapters)"
+                 .format(w=cfg.w_std,
+                         rr=f", rank-{cfg.router_rank} routers" if cfg.router_rank > 0 else "",
+                         us=f", expert updates x{cfg.update_scale:g}" if cfg.update_scale != 1.0 else "",
+                         q4=", 4-bit experts" if cfg.codec == "q4" else "")),
         "config": {"workload": workload,
                    "layers": cfg.L, "hidden": cfg.D, "experts": cfg.n, "top_k": cfg.K,
                    "intermediate": cfg.I, "adapter_rank": cfg.r, "hbm_slots_per_layer": cfg.S,
