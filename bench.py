@@ -318,6 +318,20 @@ def main():
             _log(f"[bench] {name} {modes[name]['tokens_per_s']:.1f} tok/s "
                  f"exposed={modes[name]['exposed_transfer_pct']:.1f}% ffn={modes[name]['ffn_kernel_us']:.2f}us")
         spp.spp_set_copy_engine(stack.ctx, engine)
+        # SpecPrefetch at the budget the window-aware rule derives from the
+        # compute window measured in the run above (section "Window-Aware
+        # Prefetch Budgeting"); 0 is PRED0, and the configured window is "on"
+        if on["compute_window_us"] is not None:
+            rule_M = spp.select_prefetch_budget(on["compute_window_us"], per_expert_us, cfg.n)
+            if rule_M == 0:
+                modes["rule"] = dict(modes["pred0"], rule_budget=0)
+            elif rule_M == cfg.window:
+                modes["rule"] = dict(on, rule_budget=rule_M)
+            else:
+                modes["rule"] = dict(run_mode(stack, dev_h, row_bytes, args.warmup, args.steps, rule_M),
+                                     rule_budget=rule_M)
+            _log(f"[bench] rule (M_max={rule_M} = floor(W/c)) {modes['rule']['tokens_per_s']:.1f} tok/s "
+                 f"coverage={modes['rule']['next_layer_coverage']:.3f}")
     for M in args.sweep:
         modes[f"M{M}"] = run_mode(stack, dev_h, row_bytes, args.warmup, args.steps, M)
         _log(f"[bench] sweep M_max={M} {modes[f'M{M}']['tokens_per_s']:.1f} tok/s "
@@ -389,7 +403,8 @@ def main():
                  "frac": (on["h2d_gbs_during_run"] / link_gbs) if on["h2d_gbs_during_run"] else None},
         "window": {"compute_window_us": window_us, "live_window_us": on["window_us"],
                    "per_expert_transfer_us": per_expert_us,
-                   "implied_budget": implied_budget, "configured_budget": cfg.window},
+                   "implied_budget": implied_budget, "configured_budget": cfg.window,
+                   "tokens_per_s_at_implied_budget": modes["rule"]["tokens_per_s"] if "rule" in modes else None},
         "modes": modes,
     }
     if distilled is not None:
