@@ -135,6 +135,8 @@ typedef struct {
   /* the same predictions by how many of Top_M(s) were not available:
    * demand_hist[j][c] counts c missing experts (c = 16 counts 16 or more) */
   int64_t demand_hist[3][17];
+  /* batch-1 layer calls whose FFN ran split (spp_set_ffn_overlap) */
+  int64_t ffn_split_launches;
 } spp_run_stats;
 
 /* ---------------------------------------------------------------- lifecycle */
@@ -314,6 +316,17 @@ spp_status spp_set_prefetch_source(spp_ctx* ctx, int32_t source);
  * token (default 512; 1..4096).  The 4-bit and batched FFNs choose their own
  * grids. */
 spp_status spp_set_ffn_workgroups(spp_ctx* ctx, int32_t wgs);
+
+/* Batch-1 FFN split (default 0, off).  1: when a layer call has both experts
+ * whose data is complete (resident, or a copy that finished) and late ones
+ * (loaded by this call's on-demand copies, or a prefetch still in flight),
+ * the FFN of the complete ones runs on a second stream of the context beside
+ * the on-demand copies, and the late ones after their copies on the compute
+ * stream; the combine waits for both.  Outputs are bitwise those of the
+ * single launch (each FFN workgroup works on one expert; the split is
+ * skipped where the launch shape cannot guarantee that).  Batched contexts
+ * ignore it.  Waits for the context's streams.  EINVAL unless 0 or 1. */
+spp_status spp_set_ffn_overlap(spp_ctx* ctx, int32_t enabled);
 
 /* Engine of the expert copies from the offload tier.  A copy kernel reads
  * the pinned host store through its device-visible address (shader loads over

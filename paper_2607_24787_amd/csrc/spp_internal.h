@@ -42,6 +42,10 @@ struct FfnArgs {
   int nW;
   int I, D;
   int upw;                     // units per workgroup
+  int upp;                     // 4-bit experts: units per wave and pass (3 or 4)
+  uint32_t skip_mask;          // bit d set: work item d is left to another launch (0: run all).  A
+                               // workgroup whose units belong to a skipped item writes nothing; a
+                               // nonzero mask needs upw to divide I (each workgroup on one item)
   int codec;                   // 0: experts in dtype; 1: 4-bit blocks (dtype bf16)
   const float* x;              // [D] router input of the token
   const float* gates;
@@ -115,9 +119,9 @@ hipError_t launch_spin(uint64_t ticks, uint32_t max_iter, hipStream_t st);
 // Batch-1 FFN launch over `nunits` (expert, unit) pairs: units per workgroup
 // (*upw) so that about `target_wgs` workgroups share the work; returns the grid.
 int ffn_grid_for(int nunits, int target_wgs, int* upw);
-// 4-bit experts: whole passes of kFfnWaves * 3 units per workgroup, as many as
-// keep the grid near 256 workgroups.
-int ffn_grid_q4(int nunits, int* upw);
+// 4-bit experts: whole passes of kFfnWaves * upp units per workgroup (upp 3
+// or 4 units per wave and pass), as many as keep the grid near 256 workgroups.
+int ffn_grid_q4(int nunits, int I, int* upw, int* upp);
 size_t ffn_max_grid();
 
 }  // namespace spp

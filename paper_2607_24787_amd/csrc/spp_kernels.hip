@@ -628,6 +628,7 @@ __global__ __launch_bounds__(kFfnThreads) void ffn_units_kernel(FfnArgs a) {
   const int tid = threadIdx.x, lane = tid & 63;
   const int wave = __builtin_amdgcn_readfirstlane(tid >> 6);
   const int D = a.D, nch = D / V, I = a.I;
+  if ((a.skip_mask >> ((static_cast<int>(blockIdx.x) * a.upw) / I)) & 1u) return;  // another launch's item
 
   float acc[NCH][V];
 #pragma unroll
@@ -742,7 +743,6 @@ __global__ __launch_bounds__(kFfnThreads) void ffn_units_kernel(FfnArgs a) {
 // (h scale) q per element and subtracts 8 * sum(h scale) per block at the end.
 // Work list, wave order and the workgroup partials as in ffn_units_kernel.
 // ---------------------------------------------------------------------------
-constexpr int kQ4Upp = 3;  // units per wave and pass; the launch gives each workgroup whole passes
 constexpr int kQ4TargetWgs = 256;
 
 __device__ __forceinline__ float q4_scale(uint16_t bits) {
@@ -772,7 +772,7 @@ __device__ __forceinline__ void q4_codes(const uint4& c, float (&q)[32]) {
   }
 }
 
-template <int NQ, bool FULLQ>
+template <int NQ, bool FULLQ, int UPP>
 __global__ __launch_bounds__(kFfnThreads) void ffn_q4_kernel(FfnArgs a) {
   extern __shared__ float s_red[];  // [kFfnWaves / 2][D] wave partials
   const int tid = threadIdx.x, lane = tid & 63;
@@ -780,6 +780,7 @@ __global__ __launch_bounds__(kFfnThreads) void ffn_q4_kernel(FfnArgs a) {
   const int D = a.D, I = a.I, nblk = D / 32;
   const size_t cb = static_cast<size_t>(D) / 2, sb = static_cast<size_t>(nblk) * 2;
   const size_t unit_bytes = 3 * cb + 3 * sb;
+  if ((a.skip_mask >> ((static_cast<int>(blockIdx.x) * a.upw) / I)) & 1u) return;  // another launch's item
 
   // lanes past the row's blocks read block 0 and keep zeros: no branch in front of the loads
   float xv[NQ][32], xs[NQ];
@@ -815,15 +816,15 @@ __global__ __launch_bounds__(kFfnThreads) void ffn_q4_kernel(FfnArgs a) {
   const int total = a.nW * I;
   const int u0 = blockIdx.x * a.upw;
   const int u1 = min(u0 + a.upw, total);
-  for (int ub = u0 + wave; ub < u1; ub += kFfnWaves * kQ4Upp) {
-    uint4 cg[kQ4Upp][NQ], cu[kQ4Upp][NQ], cd[kQ4Upp][NQ];
-    uint16_t sg[kQ4Upp][NQ], su[kQ4Upp][NQ], sd[kQ4Upp][NQ];
-    float gate[kQ4Upp];
+  for (int ub = u0 + wave; ub < u1; ub += kFfnWaves * UPP) {
+    uint4 cg[UPP][NQ], cu[UPP][NQ], cd[UPP][NQ];
+    uint16_t sg[UPP][NQ], su[UPP][NQ], sd[UPP][NQ];
+    float gate[UPP];
     // no branch in front of the loads: a unit past the range re-reads the
     // range's last unit, a lane past the row's blocks reads block 0 (its x is
     // zero and its outputs are not stored)
 #pragma unroll
-    for (int p = 0; p < kQ4Upp; ++p) {
+    for (int p = 0; p < UPP; ++p) {
       const int uu = ub + p * kFfnWaves;
       const int uc = uu < u1 ? uu : u1 - 1;  // wave-uniform
       const int d = uc / I;
@@ -847,7 +848,7 @@ __global__ __launch_bounds__(kFfnThreads) void ffn_q4_kernel(FfnArgs a) {
     }
     __builtin_amdgcn_sched_barrier(0);
 #pragma unroll
-    for (int p = 0; p < kQ4Upp; ++p) {
+    for (int p = 0; p < UPP; ++p) {
       if (ub + p * kFfnWaves >= u1) continue;  // wave-uniform: no work past the range (its loads are harmless)
       float gs = 0.f, us = 0.f;
 #pragma unroll
@@ -1599,18 +1600,27 @@ hipError_t launch_router(const RouterArgs& a, int dtype, hipStream_t st) {
   return dtype == 1 ? router_t<uint16_t>(a, st) : router_t<float>(a, st);
 }
 
-template <int NQ, bool FULLQ>
-hipError_t ffn_q4_t(const FfnArgs& a, int grid, hipStream_t st, hipEvent_t start, hipEvent_t stop) {
+template <int NQ, bool FULLQ, int UPP>
+hipError_t ffn_q4_tu(const FfnArgs& a, int grid, hipStream_t st, hipEvent_t start, hipEvent_t stop) {
   const uint32_t lds = sizeof(float) * (kFfnWaves / 2) * a.D;
   if (start || stop)
-    hipExtLaunchKernelGGL((ffn_q4_kernel<NQ, FULLQ>), dim3(grid), dim3(kFfnThreads), lds, st, start, stop, 0u, a);
+    hipExtLaunchKernelGGL((ffn_q4_kernel<NQ, FULLQ, UPP>), dim3(grid), dim3(kFfnThreads), lds, st, start, stop, 0u,
+                          a);
   else
-    hipLaunchKernelGGL((ffn_q4_kernel<NQ, FULLQ>), dim3(grid), dim3(kFfnThreads), lds, st, a);
+    hipLaunchKernelGGL((ffn_q4_kernel<NQ, FULLQ, UPP>), dim3(grid), dim3(kFfnThreads), lds, st, a);
   return hipGetLastError();
 }
 
+template <int NQ, bool FULLQ>
+hipError_t ffn_q4_t(const FfnArgs& a, int grid, hipStream_t st, hipEvent_t start, hipEvent_t stop) {
+  if (a.upp == 4) return ffn_q4_tu<NQ, FULLQ, 4>(a, grid, st, start, stop);
+  if (a.upp == 3) return ffn_q4_tu<NQ, FULLQ, 3>(a, grid, st, start, stop);
+  return hipErrorInvalidValue;
+}
+
 hipError_t launch_ffn(const FfnArgs& a, int grid, int dtype, hipStream_t st, hipEvent_t start, hipEvent_t stop) {
-  if (a.nW <= 0 || a.nW > kMaxWork || grid <= 0 || a.D > 4096) return hipErrorInvalidValue;
+  if (a.nW <= 0 || a.nW > kMaxWork || grid <= 0 || a.D > 4096 || a.upw <= 0) return hipErrorInvalidValue;
+  if (a.skip_mask != 0 && a.I % a.upw != 0) return hipErrorInvalidValue;  // a workgroup would span two items
   if (a.codec == 1) {
     // 4-bit experts: 32 elements per lane and block, 64 blocks per 2048-element chunk
     if (dtype != 1 || a.D % 256 != 0) return hipErrorInvalidValue;
@@ -1679,16 +1689,26 @@ hipError_t launch_spin(uint64_t ticks, uint32_t max_iter, hipStream_t st) {
   return hipGetLastError();
 }
 
-int ffn_grid_q4(int nunits, int* upw) {
-  // whole passes of kQ4Upp units per wave, as many as keep the grid near 256
-  // workgroups: a wave's later passes then load while its earlier ones decode
-  // (one launch over 8 experts of the Qwen shape: 17.4 us at 512 workgroups of
-  // one pass, 13.9 us at 256 of two); at least as many as keep the grid within
-  // the partial buffer (ffn_max_grid rows)
-  const int pass = kFfnWaves * kQ4Upp;
+int ffn_grid_q4(int nunits, int I, int* upw, int* upp) {
+  // units per wave and pass: 3, or 4 where a pass of 3 per wave cannot tile
+  // an expert's I units but one of 4 can (I = 896: 13.4 -> 12.3 us for one
+  // launch over 8 DeepSeek-shaped experts); then whole passes per wave, as
+  // many as keep the grid near 256 workgroups: a wave's later passes load
+  // while its earlier ones decode (8 Qwen-shaped experts: 17.4 us at 512
+  // workgroups of one pass, 13.9 us at 256 of two), at least as many as keep
+  // the grid within the partial buffer (ffn_max_grid rows), and preferably
+  // a count whose units per workgroup divide I, so that every workgroup
+  // works on one expert
+  *upp = (I % (kFfnWaves * 3) != 0 && I % (kFfnWaves * 4) == 0) ? 4 : 3;
+  const int pass = kFfnWaves * *upp;
   int passes = (nunits + pass * kQ4TargetWgs - 1) / (pass * kQ4TargetWgs);
-  passes = std::max(passes, (nunits + pass * 4096 - 1) / (pass * 4096));
-  *upw = pass * std::max(passes, 1);
+  passes = std::max(std::max(passes, (nunits + pass * 4096 - 1) / (pass * 4096)), 1);
+  for (int p = passes; p < passes + 3; ++p)
+    if (I % (pass * p) == 0) {
+      passes = p;
+      break;
+    }
+  *upw = pass * passes;
   return (nunits + *upw - 1) / *upw;
 }
 

@@ -105,6 +105,12 @@ struct spp_ctx {
   int32_t copy_engine = SPP_COPY_SPLIT;
   hipEvent_t demand_done = nullptr;  // on the compute stream after the latest on-demand copy kernels
   bool demand_done_valid = false;
+  // batch-1 FFN split (spp_set_ffn_overlap): the experts already resident run on
+  // compute2 while the on-demand copies run on the compute stream
+  bool ffn_overlap = false;
+  hipStream_t compute2 = nullptr;
+  hipEvent_t route_done = nullptr;  // compute stream, after the router launch
+  hipEvent_t hits_done = nullptr;   // compute2, after the resident experts' FFN launch
   unsigned* counter = nullptr;
   float* partial = nullptr;    // [ffn_max_grid, D]
   uint8_t* probe_dev = nullptr;  // one blob, for copy profiling
@@ -373,6 +379,7 @@ spp_status issue_demand(spp_ctx* c, LayerState& ls, const std::vector<spp::Trans
 spp_status sync_all(spp_ctx* c) {
   SPP_HIP(hipStreamSynchronize(c->copy));
   SPP_HIP(hipStreamSynchronize(c->copy2));
+  SPP_HIP(hipStreamSynchronize(c->compute2));
   SPP_HIP(hipStreamSynchronize(c->compute));
   return SPP_OK;
 }
@@ -396,6 +403,7 @@ void free_ctx(spp_ctx* c) {
   if (!c) return;
   if (c->copy) (void)hipStreamSynchronize(c->copy);
   if (c->copy2) (void)hipStreamSynchronize(c->copy2);
+  if (c->compute2) (void)hipStreamSynchronize(c->compute2);
   (void)hipStreamSynchronize(c->compute);
   for (LayerState& ls : c->layers) {
     if (ls.slots) (void)hipFree(ls.slots);
@@ -417,6 +425,8 @@ void free_ctx(spp_ctx* c) {
   for (hipEvent_t e : c->round_done)
     if (e) (void)hipEventDestroy(e);
   if (c->demand_done) (void)hipEventDestroy(c->demand_done);
+  if (c->route_done) (void)hipEventDestroy(c->route_done);
+  if (c->hits_done) (void)hipEventDestroy(c->hits_done);
   for (void* p : {static_cast<void*>(c->u_dev), static_cast<void*>(c->x_dev), static_cast<void*>(c->zbuf),
                   static_cast<void*>(c->res_dev), static_cast<void*>(c->counter), static_cast<void*>(c->partial),
                   static_cast<void*>(c->probe_dev)})
@@ -426,6 +436,7 @@ void free_ctx(spp_ctx* c) {
   if (c->ypart) (void)hipFree(c->ypart);
   if (c->copy) (void)hipStreamDestroy(c->copy);
   if (c->copy2) (void)hipStreamDestroy(c->copy2);
+  if (c->compute2) (void)hipStreamDestroy(c->compute2);
   delete c;
 }
 
@@ -446,6 +457,9 @@ spp_status create_impl(const spp_model_desc* desc, void* stream, spp_ctx** out) 
   SPP_HIP(hipStreamCreateWithFlags(&c->copy, hipStreamNonBlocking));
   SPP_HIP(hipStreamCreateWithFlags(&c->copy2, hipStreamNonBlocking));
   SPP_HIP(hipEventCreateWithFlags(&c->demand_done, kOrderEventFlags));
+  SPP_HIP(hipStreamCreateWithFlags(&c->compute2, hipStreamNonBlocking));
+  SPP_HIP(hipEventCreateWithFlags(&c->route_done, kOrderEventFlags));
+  SPP_HIP(hipEventCreateWithFlags(&c->hits_done, kOrderEventFlags));
   const spp_model_desc& d = c->d;
   c->layers.resize(d.L);
   for (LayerState& ls : c->layers) {
@@ -778,6 +792,8 @@ spp_status layer_forward_impl(spp_ctx* c, int32_t l, const void* h_in, void* h_o
   ra.seq = next_router_seq(c);
   SPP_HIP(spp::launch_router(ra, dt, c->compute));
   if (c->timing) SPP_HIP(hipEventRecord(ts.ev[kEvRouted], c->compute));
+  const bool split_ok = c->ffn_overlap && !c->grouped && B == 1;
+  if (split_ok) SPP_HIP(hipEventRecord(c->route_done, c->compute));
   if (spp_status e = wait_router(c, ra.seq, 0)) return e;
   if (c->timing && c->pending_sets.size() >= 64) harvest(c, c->pending_sets.size());
 
@@ -856,6 +872,65 @@ spp_status layer_forward_impl(spp_ctx* c, int32_t l, const void* h_in, void* h_o
     }
   }
 
+  // the batch-1 FFN's work list (routed experts in T order, then the shared ones)
+  auto build_ffn = [&](int32_t b, spp::FfnArgs* fa) -> int {
+    *fa = spp::FfnArgs{};
+    int nW = 0;
+    for (int32_t k = 0; k < d.K; ++k) {
+      fa->blob[nW] = ls.slots + static_cast<size_t>(ls.policy->slot_of(T[b * d.K + k])) * c->stride;
+      fa->gate_idx[nW] = b * d.K + k;
+      ++nW;
+    }
+    for (int32_t j = 0; j < d.n_shared; ++j) {
+      fa->blob[nW] = static_cast<const uint8_t*>(ls.shared) + static_cast<size_t>(j) * c->stride;
+      fa->gate_idx[nW] = -1;
+      ++nW;
+    }
+    fa->nW = nW;
+    fa->I = d.I;
+    fa->D = d.D;
+    fa->codec = d.expert_codec;
+    fa->x = c->x_dev + static_cast<size_t>(b) * d.D;
+    fa->gates = gates_dev;
+    fa->partial = c->partial;
+    return d.expert_codec == SPP_CODEC_Q4 ? spp::ffn_grid_q4(nW * d.I, d.I, &fa->upw, &fa->upp)
+                                          : spp::ffn_grid_for(nW * d.I, c->ffn_wgs, &fa->upw);
+  };
+  // FFN split (batch 1, on request): the experts whose data is complete now
+  // (resident, or a finished copy) run on compute2 beside the on-demand
+  // copies; the late ones (copied in this call, or still in flight) run on the
+  // compute stream after their copies.  Each workgroup works on one expert, so
+  // the two launches write the partial rows a single launch would write, and
+  // the combine gives the same bits.
+  spp::FfnArgs fa0{};
+  int grid0 = 0;
+  uint32_t late = 0, all_items = 0;
+  bool split = false;
+  if (split_ok) {
+    grid0 = build_ffn(0, &fa0);
+    all_items = fa0.nW >= 32 ? 0xFFFFFFFFu : ((1u << fa0.nW) - 1u);
+    if (d.I % fa0.upw == 0) {
+      for (int32_t k = 0; k < d.K; ++k) {
+        const int32_t slot = ls.policy->slot_of(T[k]);
+        bool pending = ls.slot_inline[slot] != 0;
+        if (!pending && ls.slot_pending[slot]) {
+          const int32_t ev = ls.slot_event[slot];
+          pending = hipEventQuery(ls.slot_ready[ev]) != hipSuccess || hipEventQuery(ls.slot_ready2[ev]) != hipSuccess;
+        }
+        if (pending) late |= 1u << k;
+      }
+      split = late != 0 && late != all_items;
+    }
+    if (split) {
+      if (hipEventQuery(c->route_done) != hipSuccess) SPP_HIP(hipStreamWaitEvent(c->compute2, c->route_done, 0));
+      spp::FfnArgs hits = fa0;
+      hits.skip_mask = late;
+      SPP_HIP(spp::launch_ffn(hits, grid0, dt, c->compute2, nullptr, nullptr));
+      SPP_HIP(hipEventRecord(c->hits_done, c->compute2));
+      c->stats.ffn_split_launches += 1;
+    }
+  }
+
   // RAW: the FFN reads each needed slot only after its copy completed
   if (spp_status e = wait_round(c, ls, rounds[0], &st)) return e;
   if (c->timing) SPP_HIP(hipEventRecord(ts.ev[kEvWaitB], c->compute));
@@ -864,29 +939,13 @@ spp_status layer_forward_impl(spp_ctx* c, int32_t l, const void* h_in, void* h_o
   }
   for (int32_t b = 0; b < B && !batched; ++b) {
     spp::FfnArgs fa{};
-    int nW = 0;
-    for (int32_t k = 0; k < d.K; ++k) {
-      fa.blob[nW] = ls.slots + static_cast<size_t>(ls.policy->slot_of(T[b * d.K + k])) * c->stride;
-      fa.gate_idx[nW] = b * d.K + k;
-      ++nW;
-    }
-    for (int32_t j = 0; j < d.n_shared; ++j) {
-      fa.blob[nW] = static_cast<const uint8_t*>(ls.shared) + static_cast<size_t>(j) * c->stride;
-      fa.gate_idx[nW] = -1;
-      ++nW;
-    }
-    fa.nW = nW;
-    fa.I = d.I;
-    fa.D = d.D;
-    fa.codec = d.expert_codec;
-    fa.x = c->x_dev + static_cast<size_t>(b) * d.D;
-    fa.gates = gates_dev;
-    fa.partial = c->partial;
-    const int grid = d.expert_codec == SPP_CODEC_Q4 ? spp::ffn_grid_q4(nW * d.I, &fa.upw)
-                                                    : spp::ffn_grid_for(nW * d.I, c->ffn_wgs, &fa.upw);
+    const int grid = split_ok ? grid0 : build_ffn(b, &fa);
+    if (split_ok) fa = fa0;
+    if (split) fa.skip_mask = all_items & ~late;
     const bool stamp = c->timing && b == B - 1;
     SPP_HIP(spp::launch_ffn(fa, grid, dt, c->compute, stamp ? ts.ev[kEvFfnBegin] : nullptr,
                             stamp ? ts.ev[kEvFfnEnd] : nullptr));
+    if (split && hipEventQuery(c->hits_done) != hipSuccess) SPP_HIP(hipStreamWaitEvent(c->compute, c->hits_done, 0));
     spp::CombineArgs ca{};
     ca.partial = c->partial;
     ca.nparts = grid;
@@ -1315,6 +1374,14 @@ spp_status spp_debug_set_copy_delay(spp_ctx* c, int32_t delay_us) {
     c->wall_khz = static_cast<uint64_t>(khz);
   }
   c->copy_delay_us = delay_us;
+  return SPP_OK;
+}
+
+spp_status spp_set_ffn_overlap(spp_ctx* c, int32_t enabled) {
+  if (spp_status s = check_ctx(c)) return s;
+  if (enabled != 0 && enabled != 1) return fail(SPP_EINVAL, "enabled must be 0 or 1");
+  if (spp_status s = sync_all(c)) return s;
+  c->ffn_overlap = enabled != 0;
   return SPP_OK;
 }
 

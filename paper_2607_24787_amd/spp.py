@@ -47,7 +47,8 @@ class RunStats(ctypes.Structure):
                                            "window_us", "compute_window_us", "exposed_load_us",
                                            "exposed_wait_us")]
                 + [("recall_tokens", c_int64), ("recall_hits", c_int64 * 3), ("pred_events", c_int64),
-                   ("demand_exceeds", c_int64 * 3), ("demand_hist", (c_int64 * 17) * 3)])
+                   ("demand_exceeds", c_int64 * 3), ("demand_hist", (c_int64 * 17) * 3),
+                   ("ffn_split_launches", c_int64)])
 
     def as_dict(self):
         out = {}
@@ -94,6 +95,7 @@ _SIGS = {
     "spp_set_tier_delay": (c_int32, [c_void_p, c_int32]),
     "spp_get_last_logits": (c_int32, [c_void_p, POINTER(c_float), c_int32]),
     "spp_set_ffn_workgroups": (c_int32, [c_void_p, c_int32]),
+    "spp_set_ffn_overlap": (c_int32, [c_void_p, c_int32]),
     "spp_debug_set_poison": (c_int32, [c_void_p, c_int32]),
     "spp_debug_set_copy_delay": (c_int32, [c_void_p, c_int32]),
     "spp_policy_create": (c_int32, [c_int32, c_int32, POINTER(c_int32), c_int32, POINTER(c_void_p)]),
@@ -358,6 +360,10 @@ def spp_set_copy_engine(ctx, engine: int):
 
 def spp_set_ffn_workgroups(ctx, wgs: int):
     _check(lib().spp_set_ffn_workgroups(c_void_p(ctx), wgs))
+
+
+def spp_set_ffn_overlap(ctx, enabled: int):
+    _check(lib().spp_set_ffn_overlap(c_void_p(ctx), enabled))
 
 
 def spp_debug_set_poison(ctx, enabled: bool):

@@ -34,13 +34,14 @@ def torch_cuda():
     return torch
 
 
-def _run(cfg, M_max, tokens, poison=False, delay_us=0, engine=2, tier_us=0):
+def _run(cfg, M_max, tokens, poison=False, delay_us=0, engine=2, tier_us=0, overlap=False, splits=None):
     from paper_2607_24787_amd import spp
     from paper_2607_24787_amd.model import OffloadedMoEStack
     h0 = gen.hidden_states(cfg, tokens=tokens)
     st = OffloadedMoEStack(cfg)
     try:
         spp.spp_set_copy_engine(st.ctx, engine)
+        spp.spp_set_ffn_overlap(st.ctx, 1 if overlap else 0)
         if tier_us:
             spp.spp_set_tier_delay(st.ctx, tier_us)
         spp.spp_debug_set_poison(st.ctx, poison)
@@ -53,6 +54,8 @@ def _run(cfg, M_max, tokens, poison=False, delay_us=0, engine=2, tier_us=0):
                 needed += len(set(topk.ravel().tolist()))
                 misses += stats.misses
             outs.append(st.download(st.hbuf[st.last_buf]))
+        if splits is not None:
+            splits.append(spp.spp_get_run_stats(st.ctx).ffn_split_launches)
         return np.stack(outs), on_time, needed, misses
     finally:
         st.close()
@@ -116,3 +119,24 @@ def test_storage_emulation_leaves_outputs_unchanged(torch_cuda, cfg, M_max, toke
     out, on_time, needed2, _ = _run(cfg, M_max, tokens, poison=True, tier_us=300)
     assert needed2 == needed and on_time < needed
     assert np.array_equal(out, ref)
+
+
+@pytest.mark.parametrize("cfg,M_max,tokens,poison,delay_us", [
+    (RAGGED, 2, 12, False, 0),
+    (RAGGED, 2, 12, True, 60),
+    (Q4_FENCE, 2, 12, False, 0),
+    (Q4_FENCE, 2, 12, True, 60),
+    (w.get("c3q4").with_(L=3), 2, 4, False, 0),
+    (w.get("c1"), 2, 4, False, 0),
+], ids=["ragged", "ragged_poison_delay", "q4", "q4_poison_delay", "dsv2_q4", "qwen_full"])
+def test_ffn_split_gives_the_single_launch_bits(torch_cuda, cfg, M_max, tokens, poison, delay_us):
+    """With the FFN split on (resident experts beside the on-demand copies, late
+    ones after them), every output is bitwise the single launch's, also with
+    poisoned and delayed copies; the split does happen."""
+    _log(f"[split] {cfg.name} M_max={M_max} poison={poison} delay={delay_us}")
+    splits = []
+    base, _, _, _ = _run(cfg, M_max, tokens)
+    got, _, _, misses = _run(cfg, M_max, tokens, poison=poison, delay_us=delay_us, overlap=True, splits=splits)
+    assert not np.isnan(o.decode(got, cfg.dtype)).any()
+    assert np.array_equal(base, got)
+    assert misses > 0 and splits[0] > 0, (misses, splits)
