@@ -194,8 +194,14 @@ def cpu_baseline(cfg, tokens: int):
     t0 = time.perf_counter()
     o.run_decode(cfg, W, h0, M_max=cfg.window)
     dt = time.perf_counter() - t0
+    cpu_model = "unknown"
+    try:
+        with open("/proc/cpuinfo") as f:
+            cpu_model = next(l.split(":", 1)[1].strip() for l in f if l.startswith("model name"))
+    except (OSError, StopIteration):
+        pass
     return {"value": tokens * cfg.batch / dt, "unit": "tokens/s", "cores": int(blas[0]) if blas else 1,
-            "kind": "oracle",
+            "kind": "oracle", "blas_threads": int(blas[0]) if blas else None, "cpu_model": cpu_model,
             "sample": f"first {tokens} decode steps of the same workload (batch 1, all {cfg.L} layers, "
                       f"M_max={cfg.window}), fp64 numpy, {dt:.1f} s; host cores available: "
                       f"{len(os.sched_getaffinity(0))}"}
