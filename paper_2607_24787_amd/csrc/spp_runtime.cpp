@@ -295,12 +295,20 @@ spp_status issue_copies(spp_ctx* c, LayerState& ls, const std::vector<spp::Trans
   if (!demand && c->demand_done_valid)
     if (spp_status e = copy_streams_wait(c, c->demand_done)) return e;
   const int32_t last = xs.back().slot;
-  // each blob in two halves, one per copy stream (the split is 4 KiB aligned)
-  const size_t half = (c->blob_bytes / 2 + 4095) / 4096 * 4096;
+  // Copies go out as two halves of every blob, one per copy stream (the split
+  // is 4 KiB aligned), so that one stream's per-copy gap overlaps the other's
+  // transfer -- except prefetches beside copy-kernel loads, which go out whole
+  // and in issue order on the first copy stream.  Serial prefetches finish
+  // the one needed first (this layer's before the next layer's) at the link's
+  // full rate instead of sharing it; that and one DMA fixed cost per expert
+  // instead of two gave +3-4% tokens/s at M_max 1 on the recall-calibrated
+  // 4-bit workloads against halves or whole copies alternating the streams.
+  const bool whole = !demand && c->copy_engine == SPP_COPY_SPLIT && !c->tier_serial;
+  const size_t half = whole ? c->blob_bytes : (c->blob_bytes / 2 + 4095) / 4096 * 4096;
   const size_t part[2] = {std::min(half, c->blob_bytes), c->blob_bytes - std::min(half, c->blob_bytes)};
-  hipStream_t streams[2] = {c->copy, c->copy2};
   for (const spp::Transfer& t : xs) {
     uint8_t* dst = ls.slots + static_cast<size_t>(t.slot) * c->stride;
+    const hipStream_t streams[2] = {c->copy, c->copy2};  // stream h carries part h
     for (int h = 0; h < 2; ++h) {
       if (part[h] == 0) continue;
       if (c->copy_delay_us > 0) {
@@ -312,6 +320,10 @@ spp_status issue_copies(spp_ctx* c, LayerState& ls, const std::vector<spp::Trans
       SPP_HIP(copy_part(c, ls, dst + off, static_cast<size_t>(t.expert) * c->stride + off, part[h], streams[h]));
     }
     if (!demand || t.slot == last) {
+      // After a whole copy slot_ready2 only marks the second stream's earlier
+      // work; it is complete by the time the slot is read, so the compute
+      // stream skips its wait (a wait on a pending event costs ~12 us of host
+      // time).
       SPP_HIP(hipEventRecord(ls.slot_ready[t.slot], c->copy));
       SPP_HIP(hipEventRecord(ls.slot_ready2[t.slot], c->copy2));
     }
