@@ -339,7 +339,10 @@ spp_status spp_set_ffn_overlap(spp_ctx* ctx, int32_t enabled);
  *   SPP_COPY_KERNEL: every copy by a copy kernel (32 workgroups per half blob)
  *     on the copy streams.
  *   SPP_COPY_SDMA: every copy by the DMA engines on the copy streams.
- * On the copy streams each blob goes in two halves, one per stream.
+ * On the copy streams each blob goes in two halves, one per stream, except
+ * SPP_COPY_SPLIT's prefetches: one whole copy each, in issue order on the
+ * first copy stream.  The engine may change between calls; a new copy into a
+ * slot is ordered after any earlier copy into it still in flight.
  * spp_profile_expert_copy times the prefetch engine.  EINVAL for an unknown
  * engine. */
 spp_status spp_set_copy_engine(spp_ctx* ctx, int32_t engine);
@@ -350,8 +353,8 @@ spp_status spp_set_copy_engine(spp_ctx* ctx, int32_t engine);
  * the offload tier behaves like slower storage behind the same link.  The
  * storage serves one expert at a time: while the delay is set, on-demand
  * loads too go through the copy streams (in issue order with the
- * prefetches) instead of the compute stream.  Outputs are unchanged.  EINVAL
- * outside the range. */
+ * prefetches) instead of the compute stream.  May change between calls.
+ * Outputs are unchanged.  EINVAL outside the range. */
 spp_status spp_set_tier_delay(spp_ctx* ctx, int32_t delay_us);
 
 /* Test hooks for the copy/compute fences (for tests, not for production runs).

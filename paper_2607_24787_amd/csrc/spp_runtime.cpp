@@ -309,6 +309,15 @@ spp_status issue_copies(spp_ctx* c, LayerState& ls, const std::vector<spp::Trans
   for (const spp::Transfer& t : xs) {
     uint8_t* dst = ls.slots + static_cast<size_t>(t.slot) * c->stride;
     const hipStream_t streams[2] = {c->copy, c->copy2};  // stream h carries part h
+    if (ls.slot_pending[t.slot]) {
+      // WAW across a run-time switch between whole and split copies (copy
+      // engine, storage emulation): an earlier copy into this slot that was
+      // never waited on may still be in flight on the stream that the new
+      // copy's bytes are not ordered behind
+      const int32_t ev = ls.slot_event[t.slot];
+      const hipEvent_t other = whole ? ls.slot_ready2[ev] : ls.slot_ready[ev];
+      if (hipEventQuery(other) != hipSuccess) SPP_HIP(hipStreamWaitEvent(whole ? c->copy : c->copy2, other, 0));
+    }
     for (int h = 0; h < 2; ++h) {
       if (part[h] == 0) continue;
       if (c->copy_delay_us > 0) {

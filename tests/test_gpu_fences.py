@@ -108,6 +108,40 @@ def test_repeat_runs_are_bitwise_identical(torch_cuda):
         assert np.array_equal(a, c), engine
 
 
+@pytest.mark.parametrize("cfg,M_max,tokens", [(RAGGED, 2, 16), (w.get("c0"), 1, 12)], ids=["ragged", "c0"])
+def test_switching_copy_modes_between_tokens_keeps_the_bits(torch_cuda, cfg, M_max, tokens):
+    """Copy engine and storage emulation changed before every token, with
+    poisoned, delayed copies: split-engine prefetches go out whole on one copy
+    stream, the other modes in halves on both, so a slot's earlier copy that
+    was never waited on may still be in flight on the other stream when a new
+    copy targets it (WAW).  Outputs stay bitwise those of the default run."""
+    from paper_2607_24787_amd import spp
+    from paper_2607_24787_amd.model import OffloadedMoEStack
+    _log(f"[switch] {cfg.name} M_max={M_max}")
+    ref, _, _, _ = _run(cfg, M_max, tokens)
+    # (engine, tier delay in us): whole prefetches, halves through the one
+    # storage queue, halves by DMA, halves by the copy kernel
+    modes = [(2, 0), (2, 300), (2, 0), (1, 0), (2, 0), (0, 0)]
+    h0 = gen.hidden_states(cfg, tokens=tokens)
+    st = OffloadedMoEStack(cfg)
+    try:
+        spp.spp_debug_set_poison(st.ctx, 1)
+        outs = []
+        for t in range(tokens):
+            engine, tier_us = modes[t % len(modes)]
+            spp.spp_set_copy_engine(st.ctx, engine)
+            spp.spp_set_tier_delay(st.ctx, tier_us)
+            if not tier_us:
+                spp.spp_debug_set_copy_delay(st.ctx, 300)
+            st.step(h0[t], M_max)
+            outs.append(st.download(st.hbuf[st.last_buf]))
+        out = np.stack(outs)
+    finally:
+        st.close()
+    assert not np.isnan(o.decode(out, cfg.dtype)).any()
+    assert np.array_equal(out, ref)
+
+
 @pytest.mark.parametrize("cfg,M_max,tokens", [(RAGGED, 2, 12), (BATCH_ROUNDS, 2, 6)], ids=["ragged", "batched_rounds"])
 def test_storage_emulation_leaves_outputs_unchanged(torch_cuda, cfg, M_max, tokens):
     """Under storage emulation every expert read (on-demand loads included)
