@@ -72,6 +72,7 @@ struct LayerState {
   std::vector<hipEvent_t> slot_ready2; // the same on the second copy stream
   std::vector<int32_t> slot_event;     // the slot whose slot_ready covers this slot's last copy
   std::vector<char> slot_pending;      // that event may not have been waited on
+  std::vector<char> slot_whole;        // the slot's last copy-stream copy was one whole copy
   std::vector<char> slot_inline;       // loaded on the compute stream by this call (in order before its FFN)
   hipEvent_t last_read = nullptr;      // recorded on the compute stream after the layer's FFN
   bool last_read_valid = false;
@@ -309,7 +310,7 @@ spp_status issue_copies(spp_ctx* c, LayerState& ls, const std::vector<spp::Trans
   for (const spp::Transfer& t : xs) {
     uint8_t* dst = ls.slots + static_cast<size_t>(t.slot) * c->stride;
     const hipStream_t streams[2] = {c->copy, c->copy2};  // stream h carries part h
-    if (ls.slot_pending[t.slot]) {
+    if (ls.slot_pending[t.slot] && ls.slot_whole[t.slot] != whole) {
       // WAW across a run-time switch between whole and split copies (copy
       // engine, storage emulation): an earlier copy into this slot that was
       // never waited on may still be in flight on the stream that the new
@@ -338,6 +339,7 @@ spp_status issue_copies(spp_ctx* c, LayerState& ls, const std::vector<spp::Trans
     }
     ls.slot_event[t.slot] = demand ? last : t.slot;
     ls.slot_pending[t.slot] = 1;
+    ls.slot_whole[t.slot] = whole;
     c->stats.copies += 1;
     c->stats.copy_bytes += static_cast<int64_t>(c->blob_bytes);
   }
@@ -489,6 +491,7 @@ spp_status create_impl(const spp_model_desc* desc, void* stream, spp_ctx** out) 
     ls.slot_ready.assign(d.S, nullptr);
     ls.slot_ready2.assign(d.S, nullptr);
     ls.slot_pending.assign(d.S, 0);
+    ls.slot_whole.assign(d.S, 0);
     ls.slot_inline.assign(d.S, 0);
     ls.slot_event.resize(d.S);
     for (int32_t j = 0; j < d.S; ++j) ls.slot_event[j] = j;
