@@ -20,8 +20,9 @@
  *    the last non-OK status of the calling thread is spp_last_error().
  *  - Device work is enqueued on the compute stream given to spp_create; the
  *    library's two copy streams run host-to-device expert copies beside it
- *    (each blob in two halves, one per stream, so that one stream's per-copy
- *    start-up overlaps the other's transfer).  Calls
+ *    (loads in two halves, one per stream, so that one stream's per-copy
+ *    start-up overlaps the other's transfer; prefetches of the default copy
+ *    engine whole, in issue order, on the first stream).  Calls
  *    with host outputs return once those outputs are valid.
  *  - Layouts are row-major.  dtype SPP_DTYPE_F32 stores weights and hidden
  *    states as fp32, SPP_DTYPE_BF16 as bf16 (bit patterns, 2 bytes); router
