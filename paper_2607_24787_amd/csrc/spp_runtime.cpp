@@ -90,8 +90,8 @@ struct spp_ctx {
   int device = 0;
   int num_cu = 256;  // compute units of the device
   hipStream_t compute = nullptr;
-  hipStream_t copy = nullptr;   // expert copies: first half of every blob
-  hipStream_t copy2 = nullptr;  // and second half, so that one stream's per-copy gap overlaps the other's transfer
+  hipStream_t copy = nullptr;   // expert copies: first half of a blob, or the whole blob
+  hipStream_t copy2 = nullptr;  // second half, so that one stream's per-copy gap overlaps the other's transfer
   size_t elem = 0, blob_bytes = 0, stride = 0;
   std::vector<LayerState> layers;
   float* u_dev = nullptr;      // [maxB, D] prologue output
@@ -270,9 +270,9 @@ hipError_t copy_part(spp_ctx* c, const LayerState& ls, uint8_t* dst, size_t src_
   return spp::launch_h2d_copies(one, kCopyWgs, st);
 }
 
-// Enqueue the copies `xs` into layer `ls`'s slots on the two copy streams
-// (each blob in two halves, one per stream), after `war` (the last kernel
-// that read this layer's slots).  demand: on-demand loads, which the compute
+// Enqueue the copies `xs` into layer `ls`'s slots on the copy streams (a blob
+// in two halves, one per stream, or whole on the first stream), after `war`
+// (the last kernel that read this layer's slots).  demand: on-demand loads, which the compute
 // stream waits for as a group, so one event after the last copy covers them
 // (the streams are in order); otherwise prefetches, consumed one by one, each
 // with its own event.  An event wait costs the host ~14 us while the event is
