@@ -219,6 +219,8 @@ def main():
     ap.add_argument("--ffn-wgs", type=int, default=0, help="FFN workgroups (0: library default)")
     ap.add_argument("--ffn-overlap", type=int, default=0,
                     help="1: split the batch-1 FFN, resident experts beside the on-demand copies")
+    ap.add_argument("--prefetch-parallel", type=int, default=0,
+                    help="1: a layer's whole prefetch copies alternate the two copy streams")
     ap.add_argument("--batch", type=int, default=0, help="override the workload's batch (0: keep)")
     ap.add_argument("--slots", type=int, default=0, help="override HBM slots per layer (0: keep)")
     ap.add_argument("--layers", type=int, default=0, help="override the layer count (0: keep)")
@@ -275,6 +277,8 @@ def main():
         spp.spp_set_ffn_workgroups(stack.ctx, args.ffn_wgs)
     if args.ffn_overlap:
         spp.spp_set_ffn_overlap(stack.ctx, 1)
+    if args.prefetch_parallel:
+        spp.spp_set_prefetch_parallel(stack.ctx, 1)
     row_bytes = cfg.batch * cfg.D * cfg.elem_bytes
     dev_h = torch.from_numpy(np.ascontiguousarray(h_all).reshape(-1).view(np.uint8).copy()).to(stack.device)
     torch.cuda.synchronize()
@@ -287,6 +291,8 @@ def main():
             spp.spp_set_ffn_workgroups(stack.ctx, args.ffn_wgs)
         if args.ffn_overlap:
             spp.spp_set_ffn_overlap(stack.ctx, 1)
+        if args.prefetch_parallel:
+            spp.spp_set_prefetch_parallel(stack.ctx, 1)
 
     engines = {"split": spp.COPY_SPLIT, "kernel": spp.COPY_KERNEL, "sdma": spp.COPY_SDMA}
     engine = engines[args.copy_engine]
@@ -398,7 +404,7 @@ def main():
                    "intermediate": cfg.I, "adapter_rank": cfg.r, "hbm_slots_per_layer": cfg.S,
                    "window_experts": cfg.window, "batch": cfg.batch, "shared_experts": cfg.n_shared,
                    "offload_tier": "pinned host DRAM", "expert_bytes": cfg.blob_bytes,
-                   "ffn_split": bool(args.ffn_overlap)},
+                   "ffn_split": bool(args.ffn_overlap), "prefetch_parallel": bool(args.prefetch_parallel)},
         "next_layer_coverage": on["next_layer_coverage"],
         "exposed_transfer_pct": on["exposed_transfer_pct"],
         "exposed_breakdown_pct": on["exposed_breakdown_pct"],

@@ -72,7 +72,7 @@ struct LayerState {
   std::vector<hipEvent_t> slot_ready2; // the same on the second copy stream
   std::vector<int32_t> slot_event;     // the slot whose slot_ready covers this slot's last copy
   std::vector<char> slot_pending;      // that event may not have been waited on
-  std::vector<char> slot_whole;        // the slot's last copy-stream copy was one whole copy
+  std::vector<char> slot_whole;        // last copy-stream copy: 0 two halves, 1 + s whole on copy stream s
   std::vector<char> slot_inline;       // loaded on the compute stream by this call (in order before its FFN)
   hipEvent_t last_read = nullptr;      // recorded on the compute stream after the layer's FFN
   bool last_read_valid = false;
@@ -109,6 +109,7 @@ struct spp_ctx {
   // batch-1 FFN split (spp_set_ffn_overlap): the experts already resident run on
   // compute2 while the on-demand copies run on the compute stream
   bool ffn_overlap = false;
+  bool prefetch_parallel = false;  // whole prefetches of one call alternate the copy streams
   hipStream_t compute2 = nullptr;
   hipEvent_t route_done = nullptr;  // compute stream, after the router launch
   hipEvent_t hits_done = nullptr;   // compute2, after the resident experts' FFN launch
@@ -307,17 +308,32 @@ spp_status issue_copies(spp_ctx* c, LayerState& ls, const std::vector<spp::Trans
   const bool whole = !demand && c->copy_engine == SPP_COPY_SPLIT && !c->tier_serial;
   const size_t half = whole ? c->blob_bytes : (c->blob_bytes / 2 + 4095) / 4096 * 4096;
   const size_t part[2] = {std::min(half, c->blob_bytes), c->blob_bytes - std::min(half, c->blob_bytes)};
+  const hipStream_t cs[2] = {c->copy, c->copy2};
+  int k_whole = 0;
   for (const spp::Transfer& t : xs) {
     uint8_t* dst = ls.slots + static_cast<size_t>(t.slot) * c->stride;
-    const hipStream_t streams[2] = {c->copy, c->copy2};  // stream h carries part h
-    if (ls.slot_pending[t.slot] && ls.slot_whole[t.slot] != whole) {
-      // WAW across a run-time switch between whole and split copies (copy
-      // engine, storage emulation): an earlier copy into this slot that was
-      // never waited on may still be in flight on the stream that the new
-      // copy's bytes are not ordered behind
+    // a whole copy goes to stream ws (the second one for every other copy of
+    // this call with spp_set_prefetch_parallel); halves: stream h carries part h
+    const int ws = whole && c->prefetch_parallel ? (k_whole & 1) : 0;
+    const char code = whole ? static_cast<char>(1 + ws) : 0;
+    const hipStream_t streams[2] = {whole ? cs[ws] : c->copy, c->copy2};
+    if (ls.slot_pending[t.slot] && ls.slot_whole[t.slot] != code) {
+      // WAW after a change of stream assignment (copy engine, storage
+      // emulation, parallel prefetches): an earlier copy into this slot that
+      // was never waited on may still be in flight on a stream that the new
+      // copy's streams are not ordered behind.  Each stream of the new copy
+      // waits for the old copy's events recorded on the other stream.
       const int32_t ev = ls.slot_event[t.slot];
-      const hipEvent_t other = whole ? ls.slot_ready2[ev] : ls.slot_ready[ev];
-      if (hipEventQuery(other) != hipSuccess) SPP_HIP(hipStreamWaitEvent(whole ? c->copy : c->copy2, other, 0));
+      const char old = ls.slot_whole[t.slot];
+      for (int os = 0; os < 2; ++os) {
+        const bool old_on = old == 0 || old == 1 + os;
+        if (!old_on) continue;
+        const hipEvent_t e = old == 0 && os == 1 ? ls.slot_ready2[ev] : ls.slot_ready[ev];
+        for (int ns = 0; ns < 2; ++ns) {
+          const bool new_on = code == 0 || code == 1 + ns;
+          if (new_on && ns != os && hipEventQuery(e) != hipSuccess) SPP_HIP(hipStreamWaitEvent(cs[ns], e, 0));
+        }
+      }
     }
     for (int h = 0; h < 2; ++h) {
       if (part[h] == 0) continue;
@@ -330,16 +346,15 @@ spp_status issue_copies(spp_ctx* c, LayerState& ls, const std::vector<spp::Trans
       SPP_HIP(copy_part(c, ls, dst + off, static_cast<size_t>(t.expert) * c->stride + off, part[h], streams[h]));
     }
     if (!demand || t.slot == last) {
-      // After a whole copy slot_ready2 only marks the second stream's earlier
-      // work; it is complete by the time the slot is read, so the compute
-      // stream skips its wait (a wait on a pending event costs ~12 us of host
-      // time).
-      SPP_HIP(hipEventRecord(ls.slot_ready[t.slot], c->copy));
-      SPP_HIP(hipEventRecord(ls.slot_ready2[t.slot], c->copy2));
+      // a whole copy has one event, slot_ready on its stream; readers skip
+      // slot_ready2 (a wait on a pending event costs ~12 us of host time)
+      SPP_HIP(hipEventRecord(ls.slot_ready[t.slot], streams[0]));
+      if (!whole) SPP_HIP(hipEventRecord(ls.slot_ready2[t.slot], c->copy2));
     }
+    if (whole) ++k_whole;
     ls.slot_event[t.slot] = demand ? last : t.slot;
     ls.slot_pending[t.slot] = 1;
-    ls.slot_whole[t.slot] = whole;
+    ls.slot_whole[t.slot] = code;
     c->stats.copies += 1;
     c->stats.copy_bytes += static_cast<int64_t>(c->blob_bytes);
   }
@@ -359,7 +374,7 @@ spp_status issue_inline(spp_ctx* c, LayerState& ls, const std::vector<spp::Trans
     const int32_t ev = ls.slot_event[t.slot];
     if (std::find(waited.begin(), waited.end(), ev) == waited.end()) {
       if (hipEventQuery(ls.slot_ready[ev]) != hipSuccess) SPP_HIP(hipStreamWaitEvent(c->compute, ls.slot_ready[ev], 0));
-      if (hipEventQuery(ls.slot_ready2[ev]) != hipSuccess)
+      if ((!ls.slot_whole[ev] && hipEventQuery(ls.slot_ready2[ev]) != hipSuccess))
         SPP_HIP(hipStreamWaitEvent(c->compute, ls.slot_ready2[ev], 0));
       waited.push_back(ev);
     }
@@ -574,14 +589,14 @@ spp_status wait_round(spp_ctx* c, LayerState& ls, const spp::Round& round, spp_l
       continue;
     }
     const int32_t ev = ls.slot_event[slot];
-    if (hipEventQuery(ls.slot_ready[ev]) == hipSuccess && hipEventQuery(ls.slot_ready2[ev]) == hipSuccess) {
+    if (hipEventQuery(ls.slot_ready[ev]) == hipSuccess && (ls.slot_whole[ev] || hipEventQuery(ls.slot_ready2[ev]) == hipSuccess)) {
       st->ready_on_time += 1;
       ls.slot_pending[slot] = 0;
       continue;
     }
     if (std::find(waited.begin(), waited.end(), ev) == waited.end()) {
       if (hipEventQuery(ls.slot_ready[ev]) != hipSuccess) SPP_HIP(hipStreamWaitEvent(c->compute, ls.slot_ready[ev], 0));
-      if (hipEventQuery(ls.slot_ready2[ev]) != hipSuccess)
+      if ((!ls.slot_whole[ev] && hipEventQuery(ls.slot_ready2[ev]) != hipSuccess))
         SPP_HIP(hipStreamWaitEvent(c->compute, ls.slot_ready2[ev], 0));
       waited.push_back(ev);
     }
@@ -939,7 +954,7 @@ spp_status layer_forward_impl(spp_ctx* c, int32_t l, const void* h_in, void* h_o
         bool pending = ls.slot_inline[slot] != 0;
         if (!pending && ls.slot_pending[slot]) {
           const int32_t ev = ls.slot_event[slot];
-          pending = hipEventQuery(ls.slot_ready[ev]) != hipSuccess || hipEventQuery(ls.slot_ready2[ev]) != hipSuccess;
+          pending = hipEventQuery(ls.slot_ready[ev]) != hipSuccess || (!ls.slot_whole[ev] && hipEventQuery(ls.slot_ready2[ev]) != hipSuccess);
         }
         if (pending) late |= 1u << k;
       }
@@ -1406,6 +1421,13 @@ spp_status spp_set_ffn_overlap(spp_ctx* c, int32_t enabled) {
   if (enabled != 0 && enabled != 1) return fail(SPP_EINVAL, "enabled must be 0 or 1");
   if (spp_status s = sync_all(c)) return s;
   c->ffn_overlap = enabled != 0;
+  return SPP_OK;
+}
+
+spp_status spp_set_prefetch_parallel(spp_ctx* c, int32_t enabled) {
+  if (spp_status s = check_ctx(c)) return s;
+  if (enabled != 0 && enabled != 1) return fail(SPP_EINVAL, "enabled must be 0 or 1");
+  c->prefetch_parallel = enabled != 0;
   return SPP_OK;
 }
 

@@ -96,6 +96,7 @@ _SIGS = {
     "spp_get_last_logits": (c_int32, [c_void_p, POINTER(c_float), c_int32]),
     "spp_set_ffn_workgroups": (c_int32, [c_void_p, c_int32]),
     "spp_set_ffn_overlap": (c_int32, [c_void_p, c_int32]),
+    "spp_set_prefetch_parallel": (c_int32, [c_void_p, c_int32]),
     "spp_debug_set_poison": (c_int32, [c_void_p, c_int32]),
     "spp_debug_set_copy_delay": (c_int32, [c_void_p, c_int32]),
     "spp_policy_create": (c_int32, [c_int32, c_int32, POINTER(c_int32), c_int32, POINTER(c_void_p)]),
@@ -364,6 +365,10 @@ def spp_set_ffn_workgroups(ctx, wgs: int):
 
 def spp_set_ffn_overlap(ctx, enabled: int):
     _check(lib().spp_set_ffn_overlap(c_void_p(ctx), enabled))
+
+
+def spp_set_prefetch_parallel(ctx, enabled: int):
+    _check(lib().spp_set_prefetch_parallel(c_void_p(ctx), enabled))
 
 
 def spp_debug_set_poison(ctx, enabled: bool):

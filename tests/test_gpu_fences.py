@@ -34,7 +34,8 @@ def torch_cuda():
     return torch
 
 
-def _run(cfg, M_max, tokens, poison=False, delay_us=0, engine=2, tier_us=0, overlap=False, splits=None):
+def _run(cfg, M_max, tokens, poison=False, delay_us=0, engine=2, tier_us=0, overlap=False, splits=None,
+         parallel=False):
     from paper_2607_24787_amd import spp
     from paper_2607_24787_amd.model import OffloadedMoEStack
     h0 = gen.hidden_states(cfg, tokens=tokens)
@@ -42,6 +43,7 @@ def _run(cfg, M_max, tokens, poison=False, delay_us=0, engine=2, tier_us=0, over
     try:
         spp.spp_set_copy_engine(st.ctx, engine)
         spp.spp_set_ffn_overlap(st.ctx, 1 if overlap else 0)
+        spp.spp_set_prefetch_parallel(st.ctx, 1 if parallel else 0)
         if tier_us:
             spp.spp_set_tier_delay(st.ctx, tier_us)
         spp.spp_debug_set_poison(st.ctx, poison)
@@ -108,6 +110,19 @@ def test_repeat_runs_are_bitwise_identical(torch_cuda):
         assert np.array_equal(a, c), engine
 
 
+@pytest.mark.parametrize("cfg,M_max,tokens", [(RAGGED, 4, 16), (w.get("c1q4"), 4, 6)], ids=["ragged", "qwen_q4"])
+def test_parallel_prefetches_leave_outputs_unchanged(torch_cuda, cfg, M_max, tokens):
+    """A layer's whole prefetch copies alternating the two copy streams, with
+    poisoned and delayed copies: outputs bitwise those of the default run."""
+    _log(f"[parallel] {cfg.name} M_max={M_max}")
+    ref, _, needed, _ = _run(cfg, M_max, tokens)
+    for poison, delay in [(True, 0), (True, 300)]:
+        out, on_time, needed2, _ = _run(cfg, M_max, tokens, poison, delay, parallel=True)
+        assert needed2 == needed
+        assert not np.isnan(o.decode(out, cfg.dtype)).any(), (poison, delay)
+        assert np.array_equal(out, ref), (poison, delay)
+
+
 @pytest.mark.parametrize("cfg,M_max,tokens", [(RAGGED, 2, 16), (w.get("c0"), 1, 12)], ids=["ragged", "c0"])
 def test_switching_copy_modes_between_tokens_keeps_the_bits(torch_cuda, cfg, M_max, tokens):
     """Copy engine and storage emulation changed before every token, with
@@ -119,17 +134,19 @@ def test_switching_copy_modes_between_tokens_keeps_the_bits(torch_cuda, cfg, M_m
     from paper_2607_24787_amd.model import OffloadedMoEStack
     _log(f"[switch] {cfg.name} M_max={M_max}")
     ref, _, _, _ = _run(cfg, M_max, tokens)
-    # (engine, tier delay in us): whole prefetches, halves through the one
-    # storage queue, halves by DMA, halves by the copy kernel
-    modes = [(2, 0), (2, 300), (2, 0), (1, 0), (2, 0), (0, 0)]
+    # (engine, tier delay in us, parallel): whole prefetches on one stream,
+    # halves through the one storage queue, whole prefetches alternating the
+    # streams, halves by DMA, whole again, halves by the copy kernel
+    modes = [(2, 0, 0), (2, 300, 0), (2, 0, 1), (1, 0, 0), (2, 0, 1), (2, 0, 0), (0, 0, 0)]
     h0 = gen.hidden_states(cfg, tokens=tokens)
     st = OffloadedMoEStack(cfg)
     try:
         spp.spp_debug_set_poison(st.ctx, 1)
         outs = []
         for t in range(tokens):
-            engine, tier_us = modes[t % len(modes)]
+            engine, tier_us, parallel = modes[t % len(modes)]
             spp.spp_set_copy_engine(st.ctx, engine)
+            spp.spp_set_prefetch_parallel(st.ctx, parallel)
             spp.spp_set_tier_delay(st.ctx, tier_us)
             if not tier_us:
                 spp.spp_debug_set_copy_delay(st.ctx, 300)
