@@ -102,6 +102,15 @@ typedef struct {
   int32_t prefetch_used;  /* experts prefetched for this layer that its native router selected */
   int32_t ready_on_time;  /* needed experts whose copy had completed when the FFN was enqueued */
   int32_t token_hits;     /* sum over tokens b of |T_b cap available| before the on-demand loads */
+  int32_t waited;         /* needed experts the FFN waited for (loaded by this call, or a copy still in
+                           * flight); ready_on_time + waited = the distinct routed experts of the batch */
+  /* With spp_set_timing(ctx, 2) only (the call then returns after the layer
+   * finished on the device; -1 otherwise): exposed_us = compute-stream time
+   * spent on expert copies before and between the FFN rounds (on-demand copy
+   * kernels and waits for copies), layer_us = the layer call's span on the
+   * compute stream, from its first enqueued operation to its last. */
+  float exposed_us;
+  float layer_us;
 } spp_layer_stats;
 
 /* Accumulated since the last spp_reset_run_stats.  Times come from HIP events
@@ -116,9 +125,13 @@ typedef struct {
   double span_us;     /* first layer start to last layer end */
   double window_us;   /* sum over layer pairs of W_l = t_exec(l+1) - t_pred(l) */
   double compute_window_us;  /* the same minus the copy stalls of both layers inside it */
-  /* exposed_us split in two: on-demand copy kernels on the compute stream
-   * (with the later rounds of a multi-round step), and waits for copies on
-   * the copy streams (prefetches in flight; every load when loads go by DMA) */
+  /* exposed_us split in three: on-demand copy kernels on the compute stream
+   * (with the later rounds of a multi-round step) that had the host link to
+   * themselves; the same for layer calls whose on-demand copies were
+   * enqueued while a prefetch copy was still in flight on the link (the two
+   * share it, so the load takes longer); and waits for copies on the copy
+   * streams (prefetches in flight; every load when loads go by DMA).
+   * exposed_us = exposed_load_us + exposed_shared_us + exposed_wait_us. */
   double exposed_load_us;
   double exposed_wait_us;
   /* ExpertRecall@M (section "Evaluation Metrics"), counted while timing is on:
@@ -138,6 +151,11 @@ typedef struct {
   int64_t demand_hist[3][17];
   /* batch-1 layer calls whose FFN ran split (spp_set_ffn_overlap) */
   int64_t ffn_split_launches;
+  /* see exposed_load_us; shared_calls counts the layer calls it covers */
+  double exposed_shared_us;
+  int64_t shared_calls;
+  /* needed experts the FFN waited for (the layer calls' `waited`) */
+  int64_t waited;
 } spp_run_stats;
 
 /* ---------------------------------------------------------------- lifecycle */
@@ -171,8 +189,10 @@ spp_status spp_pack_expert_q4(const spp_model_desc* desc, const uint8_t* gate_q,
 /* Create a context on the current device.  hip_stream: the compute stream
  * (hipStream_t, may be NULL for the null stream).  Allocates S slots per layer
  * plus scratch; every slot starts EMPTY.  Errors: EINVAL for inconsistent
- * shapes (S < K*max_batch when the batch demand could exceed S is allowed but
- * such a call later fails), ENOMEM, EHIP. */
+ * shapes, among them S < min(n, K*max_batch) for a context whose expert
+ * layout is not SPP_LAYOUT_TILED (only the tiled batched path runs a step in
+ * on-demand rounds, so elsewhere every distinct routed expert of a call must
+ * fit in the slots at once), ENOMEM, EHIP. */
 spp_status spp_create(const spp_model_desc* desc, void* hip_stream, spp_ctx** out);
 spp_status spp_destroy(spp_ctx* ctx);
 
@@ -243,7 +263,12 @@ spp_status expert_cache_issue_prefetch(spp_ctx* ctx, int32_t target_layer, const
  * topk_out: host int32 [B,K] or NULL; gate_out: host fp32 [B,K] or NULL;
  * stats: host or NULL.  Outputs never depend on M_max, S or the adapter.
  * Advances the step clock by one.  Returns once topk/gates are on the host;
- * h_out is complete when the compute stream reaches that point. */
+ * h_out is complete when the compute stream reaches that point.  Errors:
+ * EINVAL (bad argument) and ESTATE (layer l, or layer l+1 for a budget, not
+ * bound) before any device work; a refusal after the routing (a batch demand
+ * the slots cannot hold, which spp_create's slot check rules out) restores
+ * the step clock and leaves slot tables, prefetch records and statistics as
+ * they were. */
 spp_status moe_layer_forward(spp_ctx* ctx, int32_t l, const void* h_in_dev, void* h_out_dev, int32_t B,
                              int32_t M_max, int32_t* topk_out, float* gate_out, spp_layer_stats* stats);
 
@@ -292,8 +317,23 @@ spp_status spp_get_last_router_input(spp_ctx* ctx, float* x_out, int32_t B);
  * buffer) or after adapter_predict; B at most the last call's batch. */
 spp_status spp_get_last_logits(spp_ctx* ctx, float* z_out, int32_t B);
 
-/* Event timing of layer calls (adds ~6 event records per call). */
+/* Event timing of layer calls (adds ~6 event records per call).  enabled:
+ * 0 off, 1 on (run and per-layer totals, no host waits), 2 on and every layer
+ * call also fills its spp_layer_stats exposed_us / layer_us, for which it
+ * waits until the layer finished on the device (this serialises host and
+ * device: use 1 for throughput runs).  EINVAL outside 0..2. */
 spp_status spp_set_timing(spp_ctx* ctx, int32_t enabled);
+/* Per-layer totals of the timed layer calls since spp_reset_run_stats, for
+ * layers 0..L-1 (host arrays of L entries, any may be NULL; L must equal the
+ * context's layer count): calls_out = timed calls of layer l; exposed_us_out
+ * = their exposed time (as spp_run_stats.exposed_us); latency_us_out = the
+ * time from each call's start on the compute stream to the start of the next
+ * timed layer call (the per-layer latency of the exposed-transfer share; a
+ * run's last call has no successor and contributes only to calls_out and
+ * exposed_us_out, and latency_calls_out counts the calls that did
+ * contribute).  Waits for all enqueued work first. */
+spp_status spp_get_layer_times(spp_ctx* ctx, int32_t L, int64_t* calls_out, double* exposed_us_out,
+                               double* latency_us_out, int64_t* latency_calls_out);
 /* Waits for all enqueued work, folds finished event timings into the totals. */
 spp_status spp_get_run_stats(spp_ctx* ctx, spp_run_stats* out);
 spp_status spp_reset_run_stats(spp_ctx* ctx);

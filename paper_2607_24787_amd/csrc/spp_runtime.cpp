@@ -51,6 +51,7 @@ struct TimingSet {
   hipEvent_t ev[kNumEv] = {};
   int32_t l = -1;
   bool predicted = false;
+  bool shared = false;  // on-demand copies enqueued while a prefetch copy was in flight on the link
   // batched steps with several on-demand rounds: (before, after) the copy
   // waits of rounds 1.. (inside the FFN span)
   std::vector<hipEvent_t> extra;
@@ -142,6 +143,12 @@ struct spp_ctx {
   bool last_s_valid = false;
   // timing
   bool timing = false;
+  int32_t timing_level = 0;
+  hipEvent_t pf_done[2] = {nullptr, nullptr};  // copy streams, after the latest prefetch copies (timing only)
+  bool pf_done_valid = false;
+  // per-layer totals of the timed calls (spp_get_layer_times)
+  std::vector<int64_t> lt_calls, lt_latency_calls;
+  std::vector<double> lt_exposed, lt_latency;
   std::vector<int32_t> pred_top;  // Top_{K+2}(s) of the last prediction (timing only), for layer pred_target
   int32_t pred_target = -1;
   std::vector<TimingSet> pending_sets, free_sets;
@@ -187,6 +194,10 @@ bool desc_ok(const spp_model_desc* d, std::string* why) {
     return *why = "expert_codec must be SPP_CODEC_PLAIN or SPP_CODEC_Q4", false;
   if (d->expert_codec == SPP_CODEC_Q4 && (d->dtype != SPP_DTYPE_BF16 || d->max_batch != 1 || d->D % 256 != 0))
     return *why = "4-bit experts need dtype bf16, max_batch 1 and D a multiple of 256", false;
+  // only the tiled batched path runs a step in rounds; elsewhere every distinct
+  // routed expert of a call must fit in the slots at once
+  if (!tiled_layout(*d) && static_cast<int64_t>(d->S) < std::min<int64_t>(d->n, static_cast<int64_t>(d->K) * d->max_batch))
+    return *why = "S must be >= min(n, K * max_batch) unless the experts use the tiled batched layout", false;
   return true;
 }
 
@@ -232,12 +243,22 @@ void harvest(spp_ctx* c, size_t count) {
     double extra = 0.0;
     for (int32_t q = 0; q + 1 < s.extra_used; q += 2) extra += 1e3 * elapsed(s.extra[q], s.extra[q + 1]);
     st.exposed_us += exposed + extra;
-    st.exposed_load_us += loads + extra;
+    if (s.shared) {
+      st.exposed_shared_us += loads + extra;
+      st.shared_calls += 1;
+    } else {
+      st.exposed_load_us += loads + extra;
+    }
     st.exposed_wait_us += exposed - loads;
+    c->lt_calls[s.l] += 1;
+    c->lt_exposed[s.l] += exposed + extra;
     st.ffn_us += 1e3 * elapsed(s.ev[kEvFfnBegin], s.ev[kEvFfnEnd]) - extra;
     st.tail_us += 1e3 * elapsed(s.ev[kEvFfnEnd], s.ev[kEvEnd]);
     if (c->have_prev) {
-      st.span_us += 1e3 * elapsed(c->prev.ev[kEvStart], s.ev[kEvStart]);
+      const double span = 1e3 * elapsed(c->prev.ev[kEvStart], s.ev[kEvStart]);
+      st.span_us += span;
+      c->lt_latency[c->prev.l] += span;
+      c->lt_latency_calls[c->prev.l] += 1;
       if (c->prev.predicted && s.l == c->prev.l + 1) {
         // W_l = t_exec(l+1) - t_pred(l); the compute window excludes the copy stalls inside it
         const double w = 1e3 * elapsed(c->prev.ev[kEvRouted], s.ev[kEvFfnBegin]);
@@ -465,6 +486,8 @@ void free_ctx(spp_ctx* c) {
   if (c->demand_done) (void)hipEventDestroy(c->demand_done);
   if (c->route_done) (void)hipEventDestroy(c->route_done);
   if (c->hits_done) (void)hipEventDestroy(c->hits_done);
+  for (hipEvent_t e : c->pf_done)
+    if (e) (void)hipEventDestroy(e);
   for (void* p : {static_cast<void*>(c->u_dev), static_cast<void*>(c->x_dev), static_cast<void*>(c->zbuf),
                   static_cast<void*>(c->res_dev), static_cast<void*>(c->counter), static_cast<void*>(c->partial),
                   static_cast<void*>(c->probe_dev)})
@@ -498,8 +521,13 @@ spp_status create_impl(const spp_model_desc* desc, void* stream, spp_ctx** out) 
   SPP_HIP(hipStreamCreateWithFlags(&c->compute2, hipStreamNonBlocking));
   SPP_HIP(hipEventCreateWithFlags(&c->route_done, kOrderEventFlags));
   SPP_HIP(hipEventCreateWithFlags(&c->hits_done, kOrderEventFlags));
+  for (hipEvent_t& e : c->pf_done) SPP_HIP(hipEventCreateWithFlags(&e, kOrderEventFlags));
   const spp_model_desc& d = c->d;
   c->layers.resize(d.L);
+  c->lt_calls.assign(d.L, 0);
+  c->lt_latency_calls.assign(d.L, 0);
+  c->lt_exposed.assign(d.L, 0.0);
+  c->lt_latency.assign(d.L, 0.0);
   for (LayerState& ls : c->layers) {
     ls.policy.reset(new spp::SlotPolicy(d.S, d.n));
     if (hipMalloc(&ls.slots, c->stride * d.S) != hipSuccess) return fail(SPP_ENOMEM, "slot pool allocation failed");
@@ -575,31 +603,50 @@ spp_status wait_router(spp_ctx* c, uint32_t seq, int word) {
   return fail(SPP_EHIP, "router results were not signalled by the router launch");
 }
 
+// Whether a prefetch copy enqueued by an earlier layer call may still be
+// moving data over the host link (timing only: the events exist then).
+bool prefetch_in_flight(spp_ctx* c) {
+  if (!c->pf_done_valid) return false;
+  return hipEventQuery(c->pf_done[0]) != hipSuccess || hipEventQuery(c->pf_done[1]) != hipSuccess;
+}
+
 // RAW: the compute stream waits for the copies into the slots a round reads.
+// Every slot of the round leaves it no longer pending: the compute stream is
+// then ordered behind its copy, by the stream order (loaded on it), by a wait
+// enqueued here, or because the copy had already completed.  A slot left
+// pending after its group's event was waited on would later query that
+// event again after a new copy into the event's own slot re-recorded it, and
+// wait for that unrelated copy.
 spp_status wait_round(spp_ctx* c, LayerState& ls, const spp::Round& round, spp_layer_stats* st) {
   std::vector<int32_t> waited;  // each covering event is waited on once
   for (const auto& es : round) {
     const int32_t slot = es.second;
     if (ls.slot_inline[slot]) {  // fenced by the stream order; not ready when the FFN was enqueued
       ls.slot_inline[slot] = 0;
+      ls.slot_pending[slot] = 0;
+      st->waited += 1;
       continue;
     }
     if (!ls.slot_pending[slot]) {
       st->ready_on_time += 1;
       continue;
     }
+    ls.slot_pending[slot] = 0;
     const int32_t ev = ls.slot_event[slot];
-    if (hipEventQuery(ls.slot_ready[ev]) == hipSuccess && (ls.slot_whole[ev] || hipEventQuery(ls.slot_ready2[ev]) == hipSuccess)) {
-      st->ready_on_time += 1;
-      ls.slot_pending[slot] = 0;
+    if (std::find(waited.begin(), waited.end(), ev) != waited.end()) {
+      st->waited += 1;  // covered by a wait already enqueued for this round
       continue;
     }
-    if (std::find(waited.begin(), waited.end(), ev) == waited.end()) {
-      if (hipEventQuery(ls.slot_ready[ev]) != hipSuccess) SPP_HIP(hipStreamWaitEvent(c->compute, ls.slot_ready[ev], 0));
-      if ((!ls.slot_whole[ev] && hipEventQuery(ls.slot_ready2[ev]) != hipSuccess))
-        SPP_HIP(hipStreamWaitEvent(c->compute, ls.slot_ready2[ev], 0));
-      waited.push_back(ev);
+    const bool done1 = hipEventQuery(ls.slot_ready[ev]) == hipSuccess;
+    const bool done2 = ls.slot_whole[ev] || hipEventQuery(ls.slot_ready2[ev]) == hipSuccess;
+    if (done1 && done2) {
+      st->ready_on_time += 1;
+      continue;
     }
+    if (!done1) SPP_HIP(hipStreamWaitEvent(c->compute, ls.slot_ready[ev], 0));
+    if (!done2) SPP_HIP(hipStreamWaitEvent(c->compute, ls.slot_ready2[ev], 0));
+    waited.push_back(ev);
+    st->waited += 1;
   }
   return SPP_OK;
 }
@@ -833,13 +880,34 @@ spp_status layer_forward_impl(spp_ctx* c, int32_t l, const void* h_in, void* h_o
   if (c->timing) SPP_HIP(hipEventRecord(ts.ev[kEvRouted], c->compute));
   const bool split_ok = c->ffn_overlap && !c->grouped && B == 1;
   if (split_ok) SPP_HIP(hipEventRecord(c->route_done, c->compute));
-  if (spp_status e = wait_router(c, ra.seq, 0)) return e;
-  if (c->timing && c->pending_sets.size() >= 64) harvest(c, c->pending_sets.size());
+  if (spp_status e = wait_router(c, ra.seq, 0)) {
+    c->clock = tau - 1;
+    if (c->timing) c->free_sets.push_back(ts);
+    return e;
+  }
 
   const int32_t* T = reinterpret_cast<const int32_t*>(c->res_host);
   const float* g = reinterpret_cast<const float*>(c->res_host + c->off_gates);
   const float* s = reinterpret_cast<const float*>(c->res_host + c->off_s);
   const int32_t BK = B * d.K;
+  const bool batched = c->grouped;  // the tiled layout is read by the grouped kernel only
+  {
+    // refusals after the routing leave the context as it was before the call
+    // (the step clock included); nothing below this point has changed it yet
+    spp_status bad = SPP_OK;
+    std::string msg;
+    for (int32_t i = 0; i < BK && bad == SPP_OK; ++i)
+      if (T[i] < 0 || T[i] >= d.n) bad = SPP_EHIP, msg = "router produced an out-of-range expert id";
+    if (bad == SPP_OK && !batched && ls.policy->distinct(T, BK) > d.S)
+      bad = SPP_ESTATE, msg = "batch demand exceeds the slot count; more than S distinct experts per step "
+                              "needs the batched bf16 path";
+    if (bad != SPP_OK) {
+      c->clock = tau - 1;
+      if (c->timing) c->free_sets.push_back(ts);
+      return fail(bad, msg);
+    }
+  }
+  if (c->timing && c->pending_sets.size() >= 64) harvest(c, c->pending_sets.size());
   if (c->timing && c->pred_target == l) score_prediction(c, T, B);
   c->pred_target = -1;
   std::vector<float> s_naive;
@@ -858,11 +926,12 @@ spp_status layer_forward_impl(spp_ctx* c, int32_t l, const void* h_in, void* h_o
   }
 
   spp_layer_stats st{};
+  st.exposed_us = -1.f;
+  st.layer_us = -1.f;
   {
     std::vector<char> seen(d.n, 0);
     for (int32_t i = 0; i < BK; ++i) {
       const int32_t e = T[i];
-      if (e < 0 || e >= d.n) return fail(SPP_EHIP, "router produced an out-of-range expert id");
       if (seen[e]) continue;
       seen[e] = 1;
       if (ls.policy->available(e)) st.hits += 1;
@@ -872,10 +941,6 @@ spp_status layer_forward_impl(spp_ctx* c, int32_t l, const void* h_in, void* h_o
   }
   ls.pending_prefetch.clear();
   std::string why;
-  const bool batched = c->grouped;  // the tiled layout is read by the grouped kernel only
-  if (!batched && ls.policy->distinct(T, BK) > d.S)
-    return fail(SPP_ESTATE, "batch demand exceeds the slot count; more than S distinct experts per step "
-                            "needs the batched bf16 path");
   std::vector<spp::Round> rounds;
   if (!ls.policy->on_demand(T, BK, tau, &c->last_loads, &rounds, &why)) return fail(SPP_ESTATE, why);
   st.misses = static_cast<int32_t>(c->last_loads.size());
@@ -887,6 +952,7 @@ spp_status layer_forward_impl(spp_ctx* c, int32_t l, const void* h_in, void* h_o
     std::vector<spp::Transfer> first;
     for (const spp::Transfer& t : c->last_loads)
       if (t.round == 0) first.push_back(t);
+    if (c->timing) ts.shared = !first.empty() && prefetch_in_flight(c);
     if (spp_status e = issue_demand(c, ls, first, ls.last_read_valid ? ls.last_read : nullptr)) return e;
   }
   if (c->timing) SPP_HIP(hipEventRecord(ts.ev[kEvLoaded], c->compute));
@@ -1004,9 +1070,23 @@ spp_status layer_forward_impl(spp_ctx* c, int32_t l, const void* h_in, void* h_o
   // prefetches for layer l+1, behind every on-demand load (in copy-stream
   // order, or after the completion of the copy kernels on the compute stream)
   // and after the FFN launch (the host time they take then overlaps the FFN)
-  if (nx && !c->last_pref.empty())
+  if (nx && !c->last_pref.empty()) {
     if (spp_status e = issue_copies(c, *nx, c->last_pref, nx->last_read_valid ? nx->last_read : nullptr, false))
       return e;
+    if (c->timing) {
+      // marks the end of these copies on both copy streams, for the next
+      // on-demand loads' question whether a prefetch still holds the link
+      for (int k = 0; k < 2; ++k) SPP_HIP(hipEventRecord(c->pf_done[k], k == 0 ? c->copy : c->copy2));
+      c->pf_done_valid = true;
+    }
+  }
+  if (c->timing_level >= 2 && st_out) {
+    SPP_HIP(hipEventSynchronize(ts.ev[kEvEnd]));
+    double exposed = 1e3 * elapsed(ts.ev[kEvWaitA], ts.ev[kEvWaitB]);
+    for (int32_t q = 0; q + 1 < ts.extra_used; q += 2) exposed += 1e3 * elapsed(ts.extra[q], ts.extra[q + 1]);
+    st.exposed_us = static_cast<float>(exposed);
+    st.layer_us = static_cast<float>(1e3 * elapsed(ts.ev[kEvStart], ts.ev[kEvEnd]));
+  }
 
   if (topk_out) std::memcpy(topk_out, T, sizeof(int32_t) * BK);
   if (gate_out) std::memcpy(gate_out, g, sizeof(float) * BK);
@@ -1018,6 +1098,7 @@ spp_status layer_forward_impl(spp_ctx* c, int32_t l, const void* h_in, void* h_o
   c->stats.prefetched += st.prefetched;
   c->stats.prefetch_used += st.prefetch_used;
   c->stats.ready_on_time += st.ready_on_time;
+  c->stats.waited += st.waited;
   if (st_out) *st_out = st;
   return SPP_OK;
 }
@@ -1344,7 +1425,24 @@ spp_status spp_get_last_logits(spp_ctx* c, float* z_out, int32_t B) {
 
 spp_status spp_set_timing(spp_ctx* c, int32_t enabled) {
   if (spp_status s = check_ctx(c)) return s;
+  if (enabled < 0 || enabled > 2) return fail(SPP_EINVAL, "timing level must be 0, 1 or 2");
   c->timing = enabled != 0;
+  c->timing_level = enabled;
+  return SPP_OK;
+}
+
+spp_status spp_get_layer_times(spp_ctx* c, int32_t L, int64_t* calls_out, double* exposed_us_out,
+                               double* latency_us_out, int64_t* latency_calls_out) {
+  if (spp_status s = check_ctx(c)) return s;
+  if (L != c->d.L) return fail(SPP_EINVAL, "L must equal the context's layer count");
+  if (spp_status s = sync_all(c)) return s;
+  harvest(c, c->pending_sets.size());
+  for (int32_t l = 0; l < L; ++l) {
+    if (calls_out) calls_out[l] = c->lt_calls[l];
+    if (exposed_us_out) exposed_us_out[l] = c->lt_exposed[l];
+    if (latency_us_out) latency_us_out[l] = c->lt_latency[l];
+    if (latency_calls_out) latency_calls_out[l] = c->lt_latency_calls[l];
+  }
   return SPP_OK;
 }
 
@@ -1368,6 +1466,10 @@ spp_status spp_reset_run_stats(spp_ctx* c) {
   }
   c->stats = spp_run_stats{};
   c->pred_target = -1;
+  std::fill(c->lt_calls.begin(), c->lt_calls.end(), 0);
+  std::fill(c->lt_latency_calls.begin(), c->lt_latency_calls.end(), 0);
+  std::fill(c->lt_exposed.begin(), c->lt_exposed.end(), 0.0);
+  std::fill(c->lt_latency.begin(), c->lt_latency.end(), 0.0);
   return SPP_OK;
 }
 

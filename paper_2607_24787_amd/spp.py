@@ -35,8 +35,9 @@ class ModelDesc(ctypes.Structure):
 
 
 class LayerStats(ctypes.Structure):
-    _fields_ = [(f, c_int32) for f in ("hits", "misses", "prefetched", "prefetch_used", "ready_on_time",
-                                       "token_hits")]
+    _fields_ = ([(f, c_int32) for f in ("hits", "misses", "prefetched", "prefetch_used", "ready_on_time",
+                                        "token_hits", "waited")]
+                + [("exposed_us", c_float), ("layer_us", c_float)])
 
 
 class RunStats(ctypes.Structure):
@@ -48,7 +49,8 @@ class RunStats(ctypes.Structure):
                                            "exposed_wait_us")]
                 + [("recall_tokens", c_int64), ("recall_hits", c_int64 * 3), ("pred_events", c_int64),
                    ("demand_exceeds", c_int64 * 3), ("demand_hist", (c_int64 * 17) * 3),
-                   ("ffn_split_launches", c_int64)])
+                   ("ffn_split_launches", c_int64), ("exposed_shared_us", c_double), ("shared_calls", c_int64),
+                   ("waited", c_int64)])
 
     def as_dict(self):
         out = {}
@@ -89,6 +91,8 @@ _SIGS = {
     "spp_set_timing": (c_int32, [c_void_p, c_int32]),
     "spp_get_run_stats": (c_int32, [c_void_p, POINTER(RunStats)]),
     "spp_reset_run_stats": (c_int32, [c_void_p]),
+    "spp_get_layer_times": (c_int32, [c_void_p, c_int32, POINTER(c_int64), POINTER(c_double), POINTER(c_double),
+                                      POINTER(c_int64)]),
     "spp_profile_expert_copy": (c_int32, [c_void_p, c_int32, c_int32, POINTER(c_double)]),
     "spp_set_prefetch_source": (c_int32, [c_void_p, c_int32]),
     "spp_set_copy_engine": (c_int32, [c_void_p, c_int32]),
@@ -327,8 +331,23 @@ def spp_get_last_logits(ctx, B, n):
     return z
 
 
-def spp_set_timing(ctx, enabled: bool):
-    _check(lib().spp_set_timing(c_void_p(ctx), int(bool(enabled))))
+def spp_set_timing(ctx, level: int):
+    """0 off, 1 on (totals only), 2 on with per-call layer times (each call waits for its layer)."""
+    _check(lib().spp_set_timing(c_void_p(ctx), int(level)))
+
+
+def spp_get_layer_times(ctx, L: int):
+    """Per-layer totals of the timed calls: dict of numpy arrays calls, exposed_us,
+    latency_us, latency_calls (each [L])."""
+    calls = np.zeros(L, dtype=np.int64)
+    lat_calls = np.zeros(L, dtype=np.int64)
+    exposed = np.zeros(L, dtype=np.float64)
+    latency = np.zeros(L, dtype=np.float64)
+    _check(lib().spp_get_layer_times(c_void_p(ctx), L, calls.ctypes.data_as(POINTER(c_int64)),
+                                     exposed.ctypes.data_as(POINTER(c_double)),
+                                     latency.ctypes.data_as(POINTER(c_double)),
+                                     lat_calls.ctypes.data_as(POINTER(c_int64))))
+    return {"calls": calls, "exposed_us": exposed, "latency_us": latency, "latency_calls": lat_calls}
 
 
 def spp_get_run_stats(ctx) -> RunStats:

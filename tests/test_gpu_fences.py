@@ -53,8 +53,11 @@ def _run(cfg, M_max, tokens, poison=False, delay_us=0, engine=2, tier_us=0, over
             res = st.step(h0[t], M_max)
             for topk, _, stats in res:
                 on_time += stats.ready_on_time
-                needed += len(set(topk.ravel().tolist()))
+                distinct = len(set(topk.ravel().tolist()))
+                needed += distinct
                 misses += stats.misses
+                # every routed expert was either ready when its FFN was enqueued or waited for
+                assert stats.ready_on_time + stats.waited == distinct, (t, stats.ready_on_time, stats.waited)
             outs.append(st.download(st.hbuf[st.last_buf]))
         if splits is not None:
             splits.append(spp.spp_get_run_stats(st.ctx).ffn_split_launches)
@@ -191,3 +194,54 @@ def test_ffn_split_gives_the_single_launch_bits(torch_cuda, cfg, M_max, tokens, 
     assert not np.isnan(o.decode(got, cfg.dtype)).any()
     assert np.array_equal(base, got)
     assert misses > 0 and splits[0] > 0, (misses, splits)
+
+
+def test_reads_wait_only_for_their_own_copies(torch_cuda):
+    """Storage emulation on: every copy goes through the copy streams, each
+    held about 20 ms.  Layer 1 loads its five routed experts as one group
+    whose completion event belongs to slot 0 (the last load lands there); a
+    prefetch then re-uses slot 0 while the group's copies may still be in
+    flight, which re-records that event for the new copy.  The next call with
+    the same routing must count the four experts still in their slots as
+    ready on time (the first call's wait already covered their copies) and
+    wait only for the one expert it reloads; the output bits stay the first
+    call's."""
+    from paper_2607_24787_amd import spp
+    from paper_2607_24787_amd.model import OffloadedMoEStack
+    cfg = RAGGED.with_(S=5)
+    st = OffloadedMoEStack(cfg)
+    try:
+        h0 = gen.hidden_states(cfg, tokens=1)
+        st.upload_hidden(h0[0], 0)
+        st.layer(0, 0, 1, -1)                       # layer 1's input now sits in buffer 1
+        T1, _, _ = st.layer(1, 1, 0, -1)
+        need = sorted(set(T1.ravel().tolist()))
+        assert len(need) == cfg.K
+        others = [e for e in range(cfg.n) if e not in need]
+        # slots hold experts the call does not need, stamps falling with the
+        # slot index: the loads (ascending expert) take slots 4, 3, 2, 1, 0
+        spp.spp_set_slot_table(st.ctx, 1, np.array(others[:5], np.int32), np.array([9, 7, 5, 3, 1], np.int64))
+        spp.spp_set_clock(st.ctx, 20)
+        spp.spp_set_tier_delay(st.ctx, 20000)
+        _log("[own copies] call A: five loads in one group")
+        _, _, sa = st.layer(1, 1, 0, -1)
+        out_a = st.download(st.hbuf[0])
+        loads, _ = spp.spp_get_last_transfers(st.ctx)
+        assert [t[1] for t in loads] == [4, 3, 2, 1, 0]
+        assert (sa.misses, sa.ready_on_time, sa.waited) == (5, 0, 5)
+        # a hand-issued prefetch for layer 1 evicts the least recently stamped
+        # slot, slot 0 (all stamps equal, lowest index), while nothing waits for it
+        _log("[own copies] prefetch into slot 0")
+        s = np.zeros(cfg.n, np.float32)
+        s[others[0]] = 1.0
+        assert spp.expert_cache_issue_prefetch(st.ctx, 1, s, 1) == [others[0]]
+        e1, _ = spp.spp_get_slot_table(st.ctx, 1, cfg.S)
+        assert int(e1[0]) == others[0]
+        _log("[own copies] call B: same routing")
+        _, _, sb = st.layer(1, 1, 0, -1)
+        assert sb.misses == 1
+        assert (sb.ready_on_time, sb.waited) == (4, 1), (sb.ready_on_time, sb.waited)
+        out_b = st.download(st.hbuf[0])
+        assert np.array_equal(out_a, out_b)
+    finally:
+        st.close()

@@ -337,15 +337,20 @@ def test_error_paths_on_device(torch_cuda):
             spp.spp_decode_step(st.ctx, cfg.L, st.hbuf[0].data_ptr(), st.hbuf[0].data_ptr(), st.hbuf[1].data_ptr(),
                                 1, cfg.K, 1)
         assert e.value.status == spp.SPP_EINVAL
-        # a slot count below the batch demand is refused at the first layer call
-        small = _stack(cfg, S=cfg.K - 1, resident=[])
-        try:
-            small.upload_hidden(h0[0], 0)
-            with pytest.raises(spp.SppError) as e:
-                small.layer(0, 0, 1, 1)
-            assert e.value.status == spp.SPP_ESTATE
-        finally:
-            small.close()
+        # a slot count below the batch demand is refused when the context is created
+        with pytest.raises(spp.SppError) as e:
+            _stack(cfg, S=cfg.K - 1, resident=[])
+        assert e.value.status == spp.SPP_EINVAL and "S must be" in spp.spp_last_error()
+        # refused layer calls leave the step clock and slot tables as they were
+        tau0 = spp.spp_get_clock(st.ctx)
+        tab0 = spp.spp_get_slot_table(st.ctx, 0, cfg.S)
+        for args in ((0, 1), (1, -2)):
+            with pytest.raises(spp.SppError):
+                spp.moe_layer_forward(st.ctx, 0, st.hbuf[0].data_ptr(), st.hbuf[1].data_ptr(), args[0], cfg.K,
+                                      args[1])
+        assert spp.spp_get_clock(st.ctx) == tau0
+        tab1 = spp.spp_get_slot_table(st.ctx, 0, cfg.S)
+        assert tab1[0].tolist() == tab0[0].tolist() and tab1[1].tolist() == tab0[1].tolist()
         # the context still works after refused calls
         topk, _, _ = st.layer(0, 0, 1, 1)
         assert topk.shape == (1, cfg.K)

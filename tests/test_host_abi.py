@@ -99,11 +99,39 @@ def test_create_rejects_bad_shapes_without_touching_a_device():
         spp.make_desc(L=2, D=256, n=8, K=2, I=64, r=300, S=4),          # r too large
         spp.make_desc(L=2, D=8192, n=8, K=2, I=64, r=4, S=4),           # D too large
         spp.make_desc(L=2, D=256, n=8, K=2, I=64, r=4, S=4, dtype=7),
+        # fewer slots than one call's distinct routed experts, outside the tiled batched path
+        spp.make_desc(L=2, D=256, n=8, K=2, I=64, r=4, S=1),                       # batch 1, S < K
+        spp.make_desc(L=2, D=96, n=12, K=3, I=40, r=8, S=8, max_batch=3, dtype=spp.DTYPE_F32),  # S < K*B
+        spp.make_desc(L=2, D=512, n=16, K=4, I=64, r=8, S=3, expert_codec=spp.CODEC_Q4),  # 4-bit, S < K
     ]
     for d in bad:
         with pytest.raises(spp.SppError) as e:
             spp.spp_create(d, 0)
         assert e.value.status == spp.SPP_EINVAL
+    assert "S must be" in spp.spp_last_error()
+
+
+def test_slot_count_check_depends_on_the_layout():
+    """The create-time slot check is exactly S >= min(n, K * max_batch) for the
+    contexts that cannot run a step in rounds; the tiled batched layout may
+    hold fewer slots than a call's demand.  Only shapes the check refuses are
+    created here (a shape it passes would reach the device)."""
+    cases = [  # (desc kwargs, refused)
+        (dict(L=2, D=256, n=8, K=2, I=64, r=4, S=1), True),
+        (dict(L=2, D=96, n=12, K=3, I=40, r=8, S=8, max_batch=3, dtype=spp.DTYPE_F32), True),
+        (dict(L=2, D=96, n=6, K=3, I=40, r=8, S=5, max_batch=3, dtype=spp.DTYPE_F32), True),   # min(n, K*B) = 6
+        (dict(L=2, D=512, n=24, K=4, I=160, r=8, S=6, max_batch=5), False),  # tiled bf16: rounds
+        (dict(L=2, D=96, n=12, K=3, I=40, r=8, S=9, max_batch=3, dtype=spp.DTYPE_F32), False),
+        (dict(L=2, D=96, n=6, K=3, I=40, r=8, S=6, max_batch=3, dtype=spp.DTYPE_F32), False),
+    ]
+    for kw, refused in cases:
+        d = spp.make_desc(**kw)
+        tiled = spp.spp_blob_layout(d) == spp.LAYOUT_TILED
+        assert refused == (not tiled and kw["S"] < min(kw["n"], kw["K"] * kw.get("max_batch", 1))), kw
+        if refused:
+            with pytest.raises(spp.SppError) as e:
+                spp.spp_create(d, 0)
+            assert e.value.status == spp.SPP_EINVAL and "S must be" in spp.spp_last_error(), kw
 
 
 def test_blob_stride():
