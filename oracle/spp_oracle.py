@@ -11,6 +11,9 @@ What is computed, and where the paper defines it:
   pi_hat_e -- Section "Expert Prediction Adapter";
 * the candidate set C_M = Top_M(s) and the adapter parameter count
   (L-1) r (D+n) -- same section;
+* the distillation loss L_pred (KL from the next layer's native routing
+  distribution to the adapter's, averaged over tokens and layer pairs) and its
+  gradient -- Section "Training Objective";
 * the window-aware budget M_max and the prefetch set
   P = Top_{M_max}{ s_e : e not available and not in flight }, issued in
   descending priority, |P| <= M_max -- Section "Window-Aware Prefetch
@@ -164,6 +167,56 @@ def candidate_set(s: np.ndarray, M: int) -> np.ndarray:
 def adapter_param_count(L: int, r: int, D: int, n: int) -> int:
     """Trainable adapter parameters over all adjacent layer pairs: (L-1) r (D+n)."""
     return (L - 1) * r * (D + n)
+
+
+# --------------------------------------------------------------------------
+# Section "Training Objective": adapter distillation
+# --------------------------------------------------------------------------
+
+
+def log_softmax(v: np.ndarray) -> np.ndarray:
+    """log softmax along the last axis in fp64 (v minus its log-sum-exp)."""
+    v = np.asarray(v, dtype=np.float64)
+    m = np.max(v, axis=-1, keepdims=True)
+    return v - m - np.log(np.sum(np.exp(v - m), axis=-1, keepdims=True))
+
+
+def distill_pair_loss(A: np.ndarray, Bm: np.ndarray, X: np.ndarray, Z_next: np.ndarray) -> float:
+    """The loss of one adjacent layer pair: the mean over the tokens of
+    KL(pi || pi_hat), where pi = softmax(z^{l+1}) is the frozen native router's
+    distribution at the next layer (the target) and pi_hat = softmax(B A x^l)
+    the adapter's.  KL(p || q) = sum_e p_e (log p_e - log q_e): the target
+    distribution weights the log ratio.  X [N, D], Z_next [N, n], fp64."""
+    X = np.asarray(X, dtype=np.float64)
+    zhat = (X @ np.asarray(A, dtype=np.float64).T) @ np.asarray(Bm, dtype=np.float64).T
+    logp = log_softmax(Z_next)
+    logq = log_softmax(zhat)
+    kl = np.sum(np.exp(logp) * (logp - logq), axis=-1)
+    return float(np.mean(kl))
+
+
+def distill_pair_grad(A: np.ndarray, Bm: np.ndarray, X: np.ndarray, Z_next: np.ndarray):
+    """Closed-form gradient of distill_pair_loss with respect to A and B.
+
+    With a = A x and z_hat = B a, the derivative of -sum_e pi_e log pi_hat_e
+    with respect to z_hat is pi_hat - pi (pi sums to one), so for the mean over
+    N tokens G = (pi_hat - pi) / N [N, n], dL/dB = G^T a [n, r] and
+    dL/dA = (G B)^T X [r, D].  Returns (dA, dB) in fp64."""
+    X = np.asarray(X, dtype=np.float64)
+    A = np.asarray(A, dtype=np.float64)
+    Bm = np.asarray(Bm, dtype=np.float64)
+    a = X @ A.T
+    G = (softmax(a @ Bm.T) - softmax(Z_next)) / X.shape[0]
+    return (G @ Bm).T @ X, G.T @ a
+
+
+def distill_loss(adapters, X_layers, Z_layers) -> float:
+    """L_pred: the pair losses averaged over the L-1 adjacent layer pairs.
+    adapters[l] = (A^l, B^l) for l = 0..L-2; X_layers[l] the router inputs of
+    layer l and Z_layers[l] its native router logits, over the same tokens."""
+    L = len(X_layers)
+    return float(sum(distill_pair_loss(adapters[l][0], adapters[l][1], X_layers[l], Z_layers[l + 1])
+                     for l in range(L - 1)) / (L - 1))
 
 
 # --------------------------------------------------------------------------

@@ -57,13 +57,15 @@ def _prefetch_gap(s: np.ndarray, occupied: np.ndarray, M: int) -> float:
 
 
 def run_lockstep(stack, cfg, tokens: int, M_max: int, check_x: bool = True,
-                 policy: str = "adapter") -> LockstepReport:
+                 policy: str = "adapter", adapter_override=None, progress=None) -> LockstepReport:
     """policy "naive": Naive Prefetch on both sides (the device via
     spp_set_prefetch_source); the oracle gets each layer's routing of the
-    preceding step."""
+    preceding step.  adapter_override(l) -> (A, B): the adapter values the
+    oracle uses (those the stack was bound with, as stored).  progress(t, l):
+    called after each compared layer."""
     from paper_2607_24787_amd import spp
 
-    W = o.OracleWeights(cfg, cache_experts=cfg.host_layers * cfg.n + 8)
+    W = o.OracleWeights(cfg, cache_experts=cfg.host_layers * cfg.n + 8, adapter_override=adapter_override)
     W.warm()
     h0 = gen.hidden_states(cfg, tokens=tokens)
     S = stack.S
@@ -141,5 +143,7 @@ def run_lockstep(stack, cfg, tokens: int, M_max: int, check_x: bool = True,
                 rep.max_ulp_h = max(rep.max_ulp_h, ulp)
                 assert rel <= tol, f"{tag}: layer output rel err {rel:.3g} > {tol}"
             rep.layers += 1
+            if progress is not None:
+                progress(t, l)
             h = ref.h_out
     return rep

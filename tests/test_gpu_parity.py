@@ -340,7 +340,7 @@ def test_error_paths_on_device(torch_cuda):
         # a slot count below the batch demand is refused when the context is created
         with pytest.raises(spp.SppError) as e:
             _stack(cfg, S=cfg.K - 1, resident=[])
-        assert e.value.status == spp.SPP_EINVAL and "S must be" in spp.spp_last_error()
+        assert e.value.status == spp.SPP_EINVAL and "S must be" in str(e.value)
         # refused layer calls leave the step clock and slot tables as they were
         tau0 = spp.spp_get_clock(st.ctx)
         tab0 = spp.spp_get_slot_table(st.ctx, 0, cfg.S)

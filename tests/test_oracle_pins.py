@@ -495,3 +495,98 @@ def test_q4_layer_against_torch_textbook_block():
     tT, tg, tout, tx = _torch_layer(h, W.router(0), cfg.K, experts, shared, cfg.rms_eps, None)
     assert np.array_equal(T, tT)
     np.testing.assert_allclose(out, tout, rtol=1e-11, atol=1e-12)
+
+
+# --------------------------------------------------------------------------
+# Section "Training Objective": the distillation loss and its gradient
+# --------------------------------------------------------------------------
+
+def _hand_pair():
+    """D = r = 1, two experts: x = 1, A = 1, B = (ln 9, 0) give z_hat = (ln 9, 0)
+    and pi_hat = (0.9, 0.1); the target logits (0, 0) give pi = (0.5, 0.5).
+    KL(pi || pi_hat) = 0.5 ln(0.5/0.9) + 0.5 ln(0.5/0.1) = ln(5/3), while the
+    reverse direction KL(pi_hat || pi) = 0.9 ln 1.8 + 0.1 ln 0.2 = 0.368..."""
+    return (np.array([[1.0]]), np.array([[math.log(9.0)], [0.0]]), np.array([[1.0]]), np.array([[0.0, 0.0]]))
+
+
+def _kl_pins_hold(loss_fn) -> bool:
+    """The pins a KL(pi || pi_hat) implementation must meet: the hand pair's
+    closed form, and scipy's relative entropy D(pi || pi_hat) on random rows."""
+    A, B, X, Z = _hand_pair()
+    if abs(loss_fn(A, B, X, Z) - math.log(5.0 / 3.0)) > 1e-14:
+        return False
+    import scipy.stats
+    rng = np.random.default_rng(11)
+    X = rng.normal(size=(9, 6))
+    A, B = rng.normal(size=(3, 6)), rng.normal(size=(5, 3))
+    Z = 2.0 * rng.normal(size=(9, 5))
+    want = np.mean([scipy.stats.entropy(scipy.special.softmax(Z[i]), scipy.special.softmax(B @ (A @ X[i])))
+                    for i in range(9)])
+    return abs(loss_fn(A, B, X, Z) - want) <= 1e-12 * max(1.0, want)
+
+
+def test_distill_loss_direction_hand_case_and_scipy():
+    assert _kl_pins_hold(o.distill_pair_loss)
+    A, B, X, Z = _hand_pair()
+    reverse = 0.9 * math.log(1.8) + 0.1 * math.log(0.2)
+    assert abs(o.distill_pair_loss(A, B, X, Z) - reverse) > 0.1        # the two directions differ here
+
+
+def test_distill_pins_reject_a_reversed_kl():
+    """A planted mistake in the oracle (the KL direction swapped) fails the pins."""
+    def reversed_kl(A, B, X, Z):
+        zhat = (np.asarray(X) @ np.asarray(A).T) @ np.asarray(B).T
+        lp, lq = o.log_softmax(Z), o.log_softmax(zhat)
+        return float(np.mean(np.sum(np.exp(lq) * (lq - lp), axis=-1)))
+    assert not _kl_pins_hold(reversed_kl)
+    assert _kl_pins_hold(o.distill_pair_loss)
+
+
+def test_distill_grad_hand_case():
+    """pi_hat - pi = (0.4, -0.4): dL/dB = (0.4, -0.4)^T a with a = 1, dL/dA = B^T (0.4, -0.4) x = 0.4 ln 9."""
+    A, B, X, Z = _hand_pair()
+    dA, dB = o.distill_pair_grad(A, B, X, Z)
+    assert np.allclose(dB, [[0.4], [-0.4]], rtol=0, atol=1e-15)
+    assert abs(dA[0, 0] - 0.4 * math.log(9.0)) < 1e-15
+
+
+@pytest.mark.parametrize("seed", range(3))
+def test_distill_grad_finite_differences(seed):
+    """Central differences of the loss (fp64) against the closed-form gradient, every entry."""
+    rng = np.random.default_rng(seed)
+    N, D, r, n = 7, 5, 3, 6
+    X = rng.normal(size=(N, D))
+    A, B = 0.7 * rng.normal(size=(r, D)), 0.7 * rng.normal(size=(n, r))
+    Z = 1.5 * rng.normal(size=(N, n))
+    dA, dB = o.distill_pair_grad(A, B, X, Z)
+    h = 1e-6
+    for M, G in ((A, dA), (B, dB)):
+        for idx in itertools.product(*map(range, M.shape)):
+            keep = M[idx]
+            M[idx] = keep + h
+            up = o.distill_pair_loss(A, B, X, Z)
+            M[idx] = keep - h
+            dn = o.distill_pair_loss(A, B, X, Z)
+            M[idx] = keep
+            assert abs((up - dn) / (2 * h) - G[idx]) < 1e-8, idx
+
+
+def test_distill_loss_invariants_and_pair_average():
+    rng = np.random.default_rng(4)
+    N, D, r, n = 20, 8, 3, 6
+    X = rng.normal(size=(N, D))
+    A, B = rng.normal(size=(r, D)), rng.normal(size=(n, r))
+    # an exact adapter (the target logits are B A x plus a per-token shift): loss 0
+    Z = (X @ A.T) @ B.T + rng.normal(size=(N, 1))
+    assert abs(o.distill_pair_loss(A, B, X, Z)) < 1e-12
+    Z2 = rng.normal(size=(N, n))
+    v = o.distill_pair_loss(A, B, X, Z2)
+    assert v > 0                                                        # Gibbs' inequality
+    assert abs(o.distill_pair_loss(A, B, X, Z2 + 3.0) - v) < 1e-12        # logits up to a shift
+    # L_pred averages the L - 1 pair losses (three layers: pairs 0->1 and 1->2)
+    Xs = [X, rng.normal(size=(N, D)), rng.normal(size=(N, D))]
+    Zs = [rng.normal(size=(N, n)) for _ in range(3)]
+    ads = [(A, B), (rng.normal(size=(r, D)), rng.normal(size=(n, r)))]
+    l01 = o.distill_pair_loss(ads[0][0], ads[0][1], Xs[0], Zs[1])
+    l12 = o.distill_pair_loss(ads[1][0], ads[1][1], Xs[1], Zs[2])
+    assert abs(o.distill_loss(ads, Xs, Zs) - (l01 + l12) / 2) < 1e-14
