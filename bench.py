@@ -116,7 +116,10 @@ def run_mode(stack, dev_h, row_bytes, warmup, steps, M_max, naive=False):
         "combine_us_per_layer": rs.tail_us / max(rs.layer_calls, 1),
         "exposed_breakdown_pct": {
             "on_demand_loads": 100.0 * rs.exposed_load_us / rs.span_us if rs.span_us > 0 else None,
+            "on_demand_loads_sharing_link_with_prefetch":
+                100.0 * rs.exposed_shared_us / rs.span_us if rs.span_us > 0 else None,
             "copy_stream_waits": 100.0 * rs.exposed_wait_us / rs.span_us if rs.span_us > 0 else None},
+        "layer_calls_sharing_link": rs.shared_calls,
         "expert_recall": ({f"@{M}": rs.recall_hits[j] / (cfg.K * rs.recall_tokens)
                            for j, M in enumerate((max(cfg.K // 2, 1), cfg.K, cfg.K + 2))}
                           if rs.recall_tokens else None),

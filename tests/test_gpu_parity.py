@@ -463,6 +463,9 @@ def test_run_statistics_match_the_oracle(torch_cuda, cfg, M_max):
     assert token_hits_target / (cfg.K * cfg.batch * cfg.tokens * (cfg.L - 1)) == \
         pytest.approx(ref.ready_recall, abs=1e-12)
     assert (rs.misses, rs.prefetched, rs.prefetch_used) == (ref.loads, ref.prefetched, ref.prefetch_used)
-    # the exposed time splits into its two parts
-    assert rs.exposed_load_us >= 0.0 and rs.exposed_wait_us >= -1.0
-    assert rs.exposed_load_us + rs.exposed_wait_us == pytest.approx(rs.exposed_us, rel=1e-6, abs=1e-3)
+    # the exposed time splits into its three parts
+    assert rs.exposed_load_us >= 0.0 and rs.exposed_shared_us >= 0.0 and rs.exposed_wait_us >= -1.0
+    assert rs.exposed_load_us + rs.exposed_shared_us + rs.exposed_wait_us == \
+        pytest.approx(rs.exposed_us, rel=1e-6, abs=1e-3)
+    assert rs.shared_calls <= rs.layer_calls
+    assert rs.ready_on_time + rs.waited == sum(len(set(np.asarray(s.T).ravel().tolist())) for s in ref.steps)
