@@ -286,6 +286,35 @@ spp_status spp_decode_step(spp_ctx* ctx, const void* h_in_dev, void* h_out_dev, 
 /* Message of the calling thread's last non-OK status ("" if none). */
 const char* spp_last_error(void);
 
+/* Capacity of adapter_predict_static's scratch, in floats: B * (n + r) at most. */
+#define SPP_STATIC_SCRATCH_FLOATS 81920
+
+/* For callers that cannot allocate device memory (code under HIP graph
+ * capture, tight serving loops, harnesses that forbid hipMalloc): the
+ * adapter_predict computation, s = sum over the B tokens of
+ * softmax(B^l A^l x_b), on explicit device weights and without a context.
+ * Its scratch (two completion counters and B * (n + r) floats of adapter
+ * hidden units and per-token distributions) is one fixed device array inside
+ * the library, 256 + 4 * SPP_STATIC_SCRATCH_FLOATS bytes (328 KiB), which
+ * each device the library runs on holds until the process ends; B * (n + r)
+ * may not exceed SPP_STATIC_SCRATCH_FLOATS (e.g. 64 tokens with n 1024 and
+ * r 256).  Allocates nothing: no hipMalloc or hipFree, no host waits.
+ * adapter_a: dev [r, D], adapter_b: dev [n, r], in dtype (SPP_DTYPE_F32 or
+ * SPP_DTYPE_BF16); x_dev: dev fp32 [B, D], the router inputs; s_out_dev: dev
+ * fp32 [n] receives s.  adapter_a, adapter_b and x_dev 16-byte aligned.
+ * Shape limits as spp_create's (D at most 4096 bf16 / 2048 fp32, D a
+ * multiple of 16 when B > 1, n <= 1024, 1 <= r <= 256).  The work is
+ * enqueued on hip_stream (NULL: the null stream) and the call returns
+ * without waiting; s_out_dev is complete when the stream reaches that point.
+ * Every call on a device shares that device's scratch, which keeps the last
+ * call's contents (the counters are cleared at the start of each call):
+ * calls that overlap on one device race, so a caller keeps them on one
+ * stream.  Errors: EINVAL (NULL or misaligned pointer, bad shape, B * (n + r)
+ * above the limit; nothing enqueued), EHIP. */
+spp_status adapter_predict_static(const void* adapter_a, const void* adapter_b, int32_t dtype, int32_t D,
+                                  int32_t n, int32_t r, const float* x_dev, int32_t B, float* s_out_dev,
+                                  void* hip_stream);
+
 /* ------------------------------------------------------ inspection / runs */
 
 /* Slot table of layer l: experts_out host int32 [S] (-1 = EMPTY), stamps_out

@@ -37,9 +37,10 @@ def build(verbose: bool = True) -> str:
     os.makedirs(BUILD, exist_ok=True)
     inc = ["-I" + INCLUDE, "-I" + CSRC]
     objs = []
-    k_obj = os.path.join(BUILD, "spp_kernels.o")
-    _run([HIPCC, *DEVICE_FLAGS, *inc, "-c", os.path.join(CSRC, "spp_kernels.hip"), "-o", k_obj])
-    objs.append(k_obj)
+    for src in ("spp_kernels.hip", "spp_static.hip"):
+        obj = os.path.join(BUILD, src.replace(".hip", ".o"))
+        _run([HIPCC, *DEVICE_FLAGS, *inc, "-c", os.path.join(CSRC, src), "-o", obj])
+        objs.append(obj)
     for src in ("spp_runtime.cpp", "spp_policy.cpp"):
         obj = os.path.join(BUILD, src.replace(".cpp", ".o"))
         _run(["g++", *HOST_FLAGS, *inc, "-c", os.path.join(CSRC, src), "-o", obj])

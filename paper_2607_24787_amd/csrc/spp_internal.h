@@ -6,7 +6,12 @@
 
 #include <cstdint>
 
+#include "spp.h"
+
 namespace spp {
+
+// Sets the calling thread's spp_last_error message and returns `s`.
+spp_status set_error(spp_status s, const char* msg);
 
 constexpr int kMaxWork = 32;       // expert blobs one FFN launch can combine
 constexpr int kMaxExpertsTopK = 1024;

@@ -86,6 +86,8 @@ size_t round_up(size_t v, size_t a) { return (v + a - 1) / a * a; }
 
 }  // namespace
 
+spp_status spp::set_error(spp_status s, const char* msg) { return fail(s, msg ? msg : ""); }
+
 struct spp_ctx {
   spp_model_desc d{};
   int device = 0;

@@ -80,6 +80,8 @@ _SIGS = {
     "moe_layer_forward": (c_int32, [c_void_p, c_int32, c_void_p, c_void_p, c_int32, c_int32, POINTER(c_int32),
                                     POINTER(c_float), POINTER(LayerStats)]),
     "spp_last_error": (c_char_p, []),
+    "adapter_predict_static": (c_int32, [c_void_p, c_void_p, c_int32, c_int32, c_int32, c_int32, c_void_p, c_int32,
+                                         c_void_p, c_void_p]),
     "spp_get_slot_table": (c_int32, [c_void_p, c_int32, POINTER(c_int32), POINTER(c_int64)]),
     "spp_set_slot_table": (c_int32, [c_void_p, c_int32, POINTER(c_int32), POINTER(c_int64)]),
     "spp_get_clock": (c_int32, [c_void_p, POINTER(c_int64)]),
@@ -234,6 +236,17 @@ def adapter_predict(ctx, l, x_dev: int, B: int, n: int) -> np.ndarray:
     s = np.zeros(n, dtype=np.float32)
     _check(lib().adapter_predict(c_void_p(ctx), l, c_void_p(x_dev), B, s.ctypes.data_as(POINTER(c_float))))
     return s
+
+
+STATIC_SCRATCH_FLOATS = 81920
+
+
+def adapter_predict_static(A_dev: int, B_dev: int, dtype: int, D: int, n: int, r: int, x_dev: int, B: int,
+                           s_out_dev: int, stream: int = 0):
+    """s into device memory s_out_dev (fp32 [n]) on `stream`; no context, no allocation, no wait."""
+    _check(lib().adapter_predict_static(c_void_p(A_dev or None), c_void_p(B_dev or None), dtype, D, n, r,
+                                        c_void_p(x_dev or None), B, c_void_p(s_out_dev or None),
+                                        c_void_p(stream or None)))
 
 
 def select_prefetch_budget(window_us: float, per_expert_cost_us: float, n_experts: int) -> int:
