@@ -52,6 +52,8 @@ struct FfnArgs {
                                // workgroup whose units belong to a skipped item writes nothing; a
                                // nonzero mask needs upw to divide I (each workgroup on one item)
   int codec;                   // 0: experts in dtype; 1: 4-bit blocks (dtype bf16)
+  int rounds;                  // 0: workgroup b takes units [b*upw, (b+1)*upw) (ffn_units_kernel);
+                               // 1..3: sweep rounds of ffn_slices_kernel (see ffn_grid_slices); upw unused
   const float* x;              // [D] router input of the token
   const float* gates;
   float* partial;              // [gridDim.x, D]
@@ -124,6 +126,10 @@ hipError_t launch_spin(uint64_t ticks, uint32_t max_iter, hipStream_t st);
 // Batch-1 FFN launch over `nunits` (expert, unit) pairs: units per workgroup
 // (*upw) so that about `target_wgs` workgroups share the work; returns the grid.
 int ffn_grid_for(int nunits, int target_wgs, int* upw);
+// The same work list in sweep rounds (bf16/fp32 experts, no skip mask): the
+// number of rounds (*rounds, 1..3) that puts the grid nearest `target_wgs`
+// workgroups; returns the grid, or 0 when it would exceed ffn_max_grid().
+int ffn_grid_slices(int nunits, int D, int dtype, int target_wgs, int* rounds);
 // 4-bit experts: whole passes of kFfnWaves * upp units per workgroup (upp 3
 // or 4 units per wave and pass), as many as keep the grid near 256 workgroups.
 int ffn_grid_q4(int nunits, int I, int* upw, int* upp);

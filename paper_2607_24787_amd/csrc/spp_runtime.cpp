@@ -1000,8 +1000,14 @@ spp_status layer_forward_impl(spp_ctx* c, int32_t l, const void* h_in, void* h_o
     fa->x = c->x_dev + static_cast<size_t>(b) * d.D;
     fa->gates = gates_dev;
     fa->partial = c->partial;
-    return d.expert_codec == SPP_CODEC_Q4 ? spp::ffn_grid_q4(nW * d.I, d.I, &fa->upw, &fa->upp)
-                                          : spp::ffn_grid_for(nW * d.I, c->ffn_wgs, &fa->upw);
+    if (d.expert_codec == SPP_CODEC_Q4) return spp::ffn_grid_q4(nW * d.I, d.I, &fa->upw, &fa->upp);
+    // the sweep-round kernel, except under the FFN split, whose two launches
+    // need every workgroup on one item (the units kernel's assignment)
+    if (!split_ok) {
+      const int g = spp::ffn_grid_slices(nW * d.I, d.D, d.dtype, c->ffn_wgs, &fa->rounds);
+      if (g > 0) return g;
+    }
+    return spp::ffn_grid_for(nW * d.I, c->ffn_wgs, &fa->upw);
   };
   // FFN split (batch 1, on request): the experts whose data is complete now
   // (resident, or a finished copy) run on compute2 beside the on-demand

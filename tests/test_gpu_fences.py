@@ -185,11 +185,13 @@ def test_storage_emulation_leaves_outputs_unchanged(torch_cuda, cfg, M_max, toke
 ], ids=["ragged", "ragged_poison_delay", "q4", "q4_poison_delay", "dsv2_q4", "qwen_full"])
 def test_ffn_split_gives_the_single_launch_bits(torch_cuda, cfg, M_max, tokens, poison, delay_us):
     """With the FFN split on (resident experts beside the on-demand copies, late
-    ones after them), every output is bitwise the single launch's, also with
-    poisoned and delayed copies; the split does happen."""
+    ones after them), every output is bitwise the same whichever experts are
+    late -- the same as a single launch of the split's kernel, which runs every
+    batch-1 FFN of the context while the split is on -- also with poisoned and
+    delayed copies, which make more experts late; the split does happen."""
     _log(f"[split] {cfg.name} M_max={M_max} poison={poison} delay={delay_us}")
     splits = []
-    base, _, _, _ = _run(cfg, M_max, tokens)
+    base, _, _, _ = _run(cfg, M_max, tokens, overlap=True)
     got, _, _, misses = _run(cfg, M_max, tokens, poison=poison, delay_us=delay_us, overlap=True, splits=splits)
     assert not np.isnan(o.decode(got, cfg.dtype)).any()
     assert np.array_equal(base, got)

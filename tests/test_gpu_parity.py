@@ -97,6 +97,23 @@ def test_lockstep_parity(torch_cuda, cfg, M_max, tokens):
     _assert_report(rep, cfg, cfg.name)
 
 
+@pytest.mark.parametrize("cfg,M_max,tokens", [(RAGGED, 2, 10), (w.get("c1"), 2, 4)], ids=["ragged", "qwen_full"])
+def test_lockstep_parity_with_the_ffn_split(torch_cuda, cfg, M_max, tokens):
+    """The FFN split option (spp_set_ffn_overlap) runs every batch-1 FFN of the
+    context with the item-aligned kernel, split or not: lock-step parity."""
+    from lockstep import run_lockstep
+    from paper_2607_24787_amd import spp
+    _log(f"[lockstep split] {cfg.name} M_max={M_max} tokens={tokens}")
+    st = _stack(cfg)
+    try:
+        spp.spp_set_ffn_overlap(st.ctx, 1)
+        rep = run_lockstep(st, cfg, tokens, M_max)
+        assert spp.spp_get_run_stats(st.ctx).ffn_split_launches > 0
+    finally:
+        st.close()
+    _assert_report(rep, cfg, cfg.name + " split")
+
+
 @pytest.mark.parametrize("cfg,M_max,tokens", [(BATCH_BF16, 2, 6), (QWEN_B16, 4, 3), (DSV2_B4, 2, 3),
                                               (BATCH_BF16_ROUNDS, 2, 6), (QWEN_B16_S32, 4, 2),
                                               (QWEN_B64_S32, 4, 2)],
