@@ -695,15 +695,29 @@ __global__ __launch_bounds__(kFfnThreads) void ffn_units_kernel(FfnArgs a) {
     }
   }
 
-  // sum the waves of this workgroup in a fixed order: (w + w+H) for w < H, then slots 0..H-1
+  // sum the waves of this workgroup in a fixed order: (w + w+H) for w < H,
+  // then slots 0..H-1.  With 8 values per chunk (bf16) a chunk's two 16-byte
+  // halves are swapped in every other group of four chunks (element 8c + 4h + e
+  // at word 8c + 4 (h ^ ((c >> 2) & 1)) + e), so that the 16-byte stores of
+  // eight consecutive lanes and the natural-order reads of the last pass touch
+  // every bank once; fp32 (4 values per chunk) needs no swizzle.  The swizzle
+  // is taken within each wave pair's D-float region.
   constexpr int H = kFfnWaves / 2;
+  auto widx = [](int d) -> int {
+    if (V != 8) return d;
+    const int c = d >> 3, e = d & 7;
+    return 8 * c + 4 * ((e >> 2) ^ ((c >> 2) & 1)) + (e & 3);
+  };
+  float4* s_red4 = reinterpret_cast<float4*>(s_red);
   if (wave >= H) {
 #pragma unroll
     for (int j = 0; j < NCH; ++j) {
       const int c = lane + 64 * j;
       if (c < nch) {
 #pragma unroll
-        for (int v = 0; v < V; ++v) s_red[(wave - H) * D + c * V + v] = acc[j][v];
+        for (int h = 0; h < V / 4; ++h)
+          s_red4[((wave - H) * D + widx(c * V + 4 * h)) / 4] =
+              make_float4(acc[j][4 * h], acc[j][4 * h + 1], acc[j][4 * h + 2], acc[j][4 * h + 3]);
       }
     }
   }
@@ -714,9 +728,11 @@ __global__ __launch_bounds__(kFfnThreads) void ffn_units_kernel(FfnArgs a) {
       const int c = lane + 64 * j;
       if (c < nch) {
 #pragma unroll
-        for (int v = 0; v < V; ++v) {
-          float* slot = &s_red[wave * D + c * V + v];
-          *slot = acc[j][v] + *slot;
+        for (int h = 0; h < V / 4; ++h) {
+          float4* slot = &s_red4[(wave * D + widx(c * V + 4 * h)) / 4];
+          const float4 o = *slot;
+          *slot = make_float4(acc[j][4 * h] + o.x, acc[j][4 * h + 1] + o.y, acc[j][4 * h + 2] + o.z,
+                              acc[j][4 * h + 3] + o.w);
         }
       }
     }
@@ -724,9 +740,10 @@ __global__ __launch_bounds__(kFfnThreads) void ffn_units_kernel(FfnArgs a) {
   __syncthreads();
   float* out = a.partial + static_cast<size_t>(blockIdx.x) * D;
   for (int d = tid; d < D; d += kFfnThreads) {
-    float v = s_red[d];
+    const int w = widx(d);
+    float v = s_red[w];
 #pragma unroll
-    for (int wv = 1; wv < H; ++wv) v += s_red[wv * D + d];
+    for (int wv = 1; wv < H; ++wv) v += s_red[wv * D + w];
     out[d] = v;
   }
 }
@@ -1010,15 +1027,23 @@ __global__ __launch_bounds__(kFfnThreads) void ffn_q4_kernel(FfnArgs a) {
 #pragma unroll
     for (int j = 0; j < 32; ++j) acc[q][j] -= 8.f * corr[q];
 
-  // sum the waves of this workgroup in a fixed order: (w + w+H) for w < H, then slots 0..H-1
+  // sum the waves of this workgroup in a fixed order: (w + w+H) for w < H,
+  // then slots 0..H-1.  LDS layout: element 32 blk + 4k + e (k < 8, e < 4) at
+  // word 32 blk + 4 (k ^ (blk & 7)) + e, so that the 16-byte stores of eight
+  // consecutive lanes (blocks 128 bytes apart) and the natural-order reads of
+  // the last pass both touch every bank once (a plain layout puts all 64
+  // lanes on one bank: 3-8 us per launch).
   constexpr int H = kFfnWaves / 2;
+  float4* s_red4 = reinterpret_cast<float4*>(s_red);
   if (wave >= H) {
 #pragma unroll
     for (int q = 0; q < NQ; ++q) {
       const int blk = lane + 64 * q;
       if (FULLQ || blk < nblk) {
 #pragma unroll
-        for (int j = 0; j < 32; ++j) s_red[(wave - H) * D + 32 * blk + j] = acc[q][j];
+        for (int k = 0; k < 8; ++k)
+          s_red4[((wave - H) * D + 32 * blk) / 4 + (k ^ (blk & 7))] =
+              make_float4(acc[q][4 * k], acc[q][4 * k + 1], acc[q][4 * k + 2], acc[q][4 * k + 3]);
       }
     }
   }
@@ -1029,9 +1054,11 @@ __global__ __launch_bounds__(kFfnThreads) void ffn_q4_kernel(FfnArgs a) {
       const int blk = lane + 64 * q;
       if (FULLQ || blk < nblk) {
 #pragma unroll
-        for (int j = 0; j < 32; ++j) {
-          float* slot = &s_red[wave * D + 32 * blk + j];
-          *slot = acc[q][j] + *slot;
+        for (int k = 0; k < 8; ++k) {
+          float4* slot = &s_red4[(wave * D + 32 * blk) / 4 + (k ^ (blk & 7))];
+          const float4 o = *slot;
+          *slot = make_float4(acc[q][4 * k] + o.x, acc[q][4 * k + 1] + o.y, acc[q][4 * k + 2] + o.z,
+                              acc[q][4 * k + 3] + o.w);
         }
       }
     }
@@ -1039,9 +1066,11 @@ __global__ __launch_bounds__(kFfnThreads) void ffn_q4_kernel(FfnArgs a) {
   __syncthreads();
   float* out = a.partial + static_cast<size_t>(blockIdx.x) * D;
   for (int d = tid; d < D; d += kFfnThreads) {
-    float v = s_red[d];
+    const int blk = d >> 5, j = d & 31;
+    const int w = 32 * blk + 4 * ((j >> 2) ^ (blk & 7)) + (j & 3);
+    float v = s_red[w];
 #pragma unroll
-    for (int wv = 1; wv < H; ++wv) v += s_red[wv * D + d];
+    for (int wv = 1; wv < H; ++wv) v += s_red[wv * D + w];
     out[d] = v;
   }
 }
