@@ -45,6 +45,25 @@ def measured_traffic(profile: str, kernel_source: str):
         return None
 
 
+def step_hbm_bytes(cfg, distinct_per_layer=None) -> int:
+    """Algorithmic HBM bytes of one decode step (all layers, the batch): every
+    layer's router and stand-in projection, the adapters of layers 0..L-2, and
+    each expert the step routes to (K per layer at batch 1; the measured
+    distinct count of a batched step) plus the shared experts, read once."""
+    e = cfg.elem_bytes
+    per_expert = cfg.blob_bytes
+    experts = cfg.K if cfg.batch == 1 or distinct_per_layer is None else distinct_per_layer
+    total = 0.0
+    for l in range(cfg.L):
+        total += cfg.n * cfg.D * e                                   # router
+        if cfg.has_proj:
+            total += cfg.D * cfg.D * e                               # stand-in projection
+        if l < cfg.L - 1 and cfg.r > 0:
+            total += (cfg.r * cfg.D + cfg.n * cfg.r) * e             # adapter A, B
+        total += (experts + cfg.n_shared) * per_expert
+    return int(round(total))
+
+
 def _ffn_stats(rs):
     n = max(rs.ffn_launches, 1)
     return rs.ffn_us / n
@@ -86,6 +105,7 @@ def run_mode(stack, dev_h, row_bytes, warmup, steps, M_max, naive=False):
     torch.cuda.synchronize()
     wall_timed = time.perf_counter() - t1
     rs = spp.spp_get_run_stats(stack.ctx)
+    lt = spp.spp_get_layer_times(stack.ctx, cfg.L)
     spp.spp_set_timing(stack.ctx, 0)
     spp.spp_set_prefetch_source(stack.ctx, spp.PREFETCH_ADAPTER)
     demand = cfg.K * cfg.batch * steps
@@ -120,6 +140,16 @@ def run_mode(stack, dev_h, row_bytes, warmup, steps, M_max, naive=False):
                 100.0 * rs.exposed_shared_us / rs.span_us if rs.span_us > 0 else None,
             "copy_stream_waits": 100.0 * rs.exposed_wait_us / rs.span_us if rs.span_us > 0 else None},
         "layer_calls_sharing_link": rs.shared_calls,
+        # per layer: exposed time / the layer's latency (its start to the next layer's start)
+        "per_layer": [{"layer": l,
+                       "exposed_us_per_call": float(lt["exposed_us"][l] / max(lt["calls"][l], 1)),
+                       "latency_us_per_call": (float(lt["latency_us"][l] / lt["latency_calls"][l])
+                                               if lt["latency_calls"][l] else None),
+                       "exposed_pct": (100.0 * float(lt["exposed_us"][l] / max(lt["calls"][l], 1))
+                                       / float(lt["latency_us"][l] / lt["latency_calls"][l])
+                                       if lt["latency_calls"][l] and lt["latency_us"][l] > 0 else None)}
+                      for l in range(cfg.L)] if cfg.L <= 4 else None,
+        "ready_plus_waited_per_step": (rs.ready_on_time + rs.waited) / steps,
         "expert_recall": ({f"@{M}": rs.recall_hits[j] / (cfg.K * rs.recall_tokens)
                            for j, M in enumerate((max(cfg.K // 2, 1), cfg.K, cfg.K + 2))}
                           if rs.recall_tokens else None),
@@ -193,21 +223,75 @@ def cpu_baseline(cfg, tokens: int):
         if l < cfg.L - 1:
             W.adapter(l)
     h0 = gen.hidden_states(cfg, tokens=tokens)
-    blas = [p.get("num_threads") for p in threadpoolctl.threadpool_info() if p.get("user_api") == "blas"]
-    t0 = time.perf_counter()
-    o.run_decode(cfg, W, h0, M_max=cfg.window)
-    dt = time.perf_counter() - t0
+    avail = len(os.sched_getaffinity(0))
+    with threadpoolctl.threadpool_limits(limits=avail, user_api="blas"):
+        blas = [p.get("num_threads") for p in threadpoolctl.threadpool_info() if p.get("user_api") == "blas"]
+        t0 = time.perf_counter()
+        o.run_decode(cfg, W, h0, M_max=cfg.window)
+        dt = time.perf_counter() - t0
     cpu_model = "unknown"
     try:
         with open("/proc/cpuinfo") as f:
             cpu_model = next(l.split(":", 1)[1].strip() for l in f if l.startswith("model name"))
     except (OSError, StopIteration):
         pass
-    return {"value": tokens * cfg.batch / dt, "unit": "tokens/s", "cores": int(blas[0]) if blas else 1,
-            "kind": "oracle", "blas_threads": int(blas[0]) if blas else None, "cpu_model": cpu_model,
-            "sample": f"first {tokens} decode steps of the same workload (batch 1, all {cfg.L} layers, "
-                      f"M_max={cfg.window}), fp64 numpy, {dt:.1f} s; host cores available: "
-                      f"{len(os.sched_getaffinity(0))}"}
+    used = min(int(blas[0]), avail) if blas else 1
+    return {"value": tokens * cfg.batch / dt, "unit": "tokens/s", "cores": used,
+            "kind": "oracle", "blas_threads": int(blas[0]) if blas else None, "host_cores_available": avail,
+            "cpu_model": cpu_model,
+            "sample": f"first {tokens} decode steps of the same workload (batch {cfg.batch}, all {cfg.L} layers, "
+                      f"M_max={cfg.window}), fp64 numpy with BLAS on {used} threads, expert weights decoded "
+                      f"before the timed region, {dt:.1f} s"}
+
+
+def stack_record(args, key: str, tie: int):
+    """A whole decode stack (the 48-layer Qwen-shaped one by default; stand-in
+    projection per layer, 25% of experts resident, configured window 1): decode
+    tokens/s at the configured window and with prediction off, next-layer
+    coverage, exposure, and the step's algorithmic HBM bytes against the 8 TB/s
+    roofline.  tie > 0: the offload tier holds tie distinct expert layers,
+    shared round-robin by the 48 (bounds pinned host memory and set-up time;
+    routers, adapters, projections and slot pools stay per layer)."""
+    import numpy as np
+    import torch
+
+    import workload
+    from paper_2607_24787_amd.model import OffloadedMoEStack
+    from workload import gen
+
+    cfg = workload.get(key)
+    if tie:
+        cfg = cfg.with_(expert_layers=tie)
+    t0 = time.perf_counter()
+    h_all = gen.hidden_states(cfg, tokens=args.warmup + 2 * args.steps)
+    stack = OffloadedMoEStack(cfg)
+    row_bytes = cfg.batch * cfg.D * cfg.elem_bytes
+    dev_h = torch.from_numpy(np.ascontiguousarray(h_all).reshape(-1).view(np.uint8).copy()).to(stack.device)
+    torch.cuda.synchronize()
+    _log(f"[bench] stack setup {time.perf_counter() - t0:.1f}s workload={cfg.name} (offload tier tied over {tie})")
+    try:
+        on = run_mode(stack, dev_h, row_bytes, args.warmup, args.steps, cfg.window)
+        _log(f"[bench] stack ON  {on['tokens_per_s']:.1f} tok/s coverage={on['next_layer_coverage']:.3f} "
+             f"exposed={on['exposed_transfer_pct']:.1f}%")
+        off = run_mode(stack, dev_h, row_bytes, args.warmup, args.steps, -1)
+        _log(f"[bench] stack OFF {off['tokens_per_s']:.1f} tok/s coverage={off['next_layer_coverage']:.3f}")
+    finally:
+        stack.close()
+    per_token = step_hbm_bytes(cfg) / cfg.batch
+    ceiling = HBM_PEAK_GBS * 1e9 / per_token
+    rec = {"workload": cfg.name + (f"+expert_layers={tie}" if tie else ""), "layers": cfg.L,
+           "window_experts": cfg.window, "hbm_slots_per_layer": cfg.S, "steps": args.steps, "warmup": args.warmup,
+           "tokens_per_s": on["tokens_per_s"], "ms_per_step": on["ms_per_step"],
+           "next_layer_coverage": on["next_layer_coverage"], "exposed_transfer_pct": on["exposed_transfer_pct"],
+           "exposed_breakdown_pct": on["exposed_breakdown_pct"],
+           "hbm_bytes_per_token": int(per_token), "hbm_roofline_tokens_per_s": ceiling,
+           "hbm_roofline_frac": on["tokens_per_s"] / ceiling,
+           "h2d_gbs_during_run": on["h2d_gbs_during_run"],
+           "modes": {"on": on, "off": off}}
+    if args.stack_cpu_tokens > 0:
+        _log(f"[bench] stack cpu baseline: oracle on {args.stack_cpu_tokens} tokens")
+        rec["cpu_baseline"] = cpu_baseline(cfg, args.stack_cpu_tokens)
+    return rec
 
 
 def main():
@@ -240,6 +324,11 @@ def main():
     ap.add_argument("--copy-engine", choices=("split", "kernel", "sdma"), default="split",
                     help="expert copies: on-demand by the copy kernel and prefetches by the DMA engines "
                          "(split, default), all by the copy kernel, or all by the DMA engines")
+    ap.add_argument("--stack", default="c2",
+                    help="workload key of the whole-stack record run after the headline pair ('' disables)")
+    ap.add_argument("--stack-tie", type=int, default=4,
+                    help="distinct expert layers of the stack record's offload tier (0: one per layer)")
+    ap.add_argument("--stack-cpu-tokens", type=int, default=1, help="oracle sample of the stack record (steps)")
     ap.add_argument("--copy-probe", action="store_true",
                     help="only run a 256 MiB device-to-device copy three times (counter calibration)")
     args = ap.parse_args()
@@ -311,6 +400,13 @@ def main():
          f"({cfg.blob_bytes / (engine_us['kernel'] * 1e3):.2f} GB/s), DMA {engine_us['sdma']:.1f} us "
          f"({cfg.blob_bytes / (engine_us['sdma'] * 1e3):.2f} GB/s); engine {args.copy_engine}")
 
+    # what the batch-1 FFN's own access pattern streams without its arithmetic
+    read_probe = None
+    if (spp.spp_blob_layout(stack.desc) == spp.LAYOUT_UNITS and cfg.dtype == "bf16" and cfg.codec == "plain"):
+        probe_us, probe_gbs = spp.spp_probe_read_ceiling(stack.ctx, 40)
+        read_probe = {"us_per_launch": probe_us, "gbs": probe_gbs, "frac_of_peak": probe_gbs / HBM_PEAK_GBS}
+        _log(f"[bench] read probe (FFN loads, no arithmetic): {probe_us:.2f} us per launch, {probe_gbs:.0f} GB/s")
+
     on = run_mode(stack, dev_h, row_bytes, args.warmup, args.steps, cfg.window)
     _log(f"[bench] ON  {on['tokens_per_s']:.1f} tok/s coverage={on['next_layer_coverage']:.3f} "
          f"exposed={on['exposed_transfer_pct']:.1f}% ffn={on['ffn_kernel_us']:.2f}us")
@@ -381,6 +477,8 @@ def main():
     layout = spp.spp_blob_layout(stack.desc)
     kernel = {spp.LAYOUT_TILED: "ffn_grouped_kernel", spp.LAYOUT_Q4_UNITS: "ffn_q4_kernel"}.get(layout,
                                                                                              "ffn_units_kernel")
+    step_bytes = step_hbm_bytes(cfg, on["distinct_experts_per_layer"])
+    hbm_ceiling = HBM_PEAK_GBS * 1e9 * cfg.batch / step_bytes          # tokens/s at 8 TB/s
     workload = cfg.name + ("" if not over else "+" + ",".join(f"{k}={v}" for k, v in over.items()))
     slug = workload.replace("+", "__").replace("=", "").replace(",", "_")
     traffic = measured_traffic(os.path.join(ROOT, "profiles", f"{kernel}__{slug}.md"),
@@ -410,6 +508,12 @@ def main():
                    "ffn_split": bool(args.ffn_overlap), "prefetch_parallel": bool(args.prefetch_parallel)},
         "next_layer_coverage": on["next_layer_coverage"],
         "exposed_transfer_pct": on["exposed_transfer_pct"],
+        # the headline layer of a pair is its prefetch target, layer 1
+        "exposed_transfer_pct_layer1": (on["per_layer"][1]["exposed_pct"]
+                                        if on["per_layer"] and cfg.L >= 2 else None),
+        "hbm_bytes_per_token": int(step_bytes / cfg.batch),
+        "hbm_roofline_tokens_per_s": hbm_ceiling,
+        "hbm_roofline_frac": on["tokens_per_s"] / hbm_ceiling,
         "exposed_breakdown_pct": on["exposed_breakdown_pct"],
         "expert_recall": on["expert_recall"],
         "demand_exceeds_budget": on["demand_exceeds_budget"],
@@ -417,7 +521,9 @@ def main():
         "demand_exceeds_window_pred0": modes["pred0"]["demand_exceeds_window"] if "pred0" in modes else None,
         "roofline": {"kernel": kernel + " (routed-expert SwiGLU FFN)", "bound": "hbm",
                      "achieved": achieved, "peak": HBM_PEAK_GBS, "unit": "GB/s", "frac": achieved / HBM_PEAK_GBS,
-                     "traffic": traffic, "bytes_per_launch": ffn_bytes, "avg_launch_us": on["ffn_kernel_us"]},
+                     "traffic": traffic, "bytes_per_launch": ffn_bytes, "avg_launch_us": on["ffn_kernel_us"],
+                     "read_probe": read_probe,
+                     "frac_of_read_probe": achieved / read_probe["gbs"] if read_probe else None},
         "link": {"bound": "host link (pinned H2D)", "copy_engine": args.copy_engine,
                  "per_expert_us_prefetch_engine": per_expert_us, "peak_gbs_measured": link_gbs,
                  "per_expert_us_by_engine": engine_us,
@@ -436,6 +542,8 @@ def main():
     if args.cpu_tokens > 0:
         _log(f"[bench] cpu baseline: oracle on {args.cpu_tokens} tokens")
         line["cpu_baseline"] = cpu_baseline(cfg, args.cpu_tokens)
+    if args.stack:
+        line["stack48" if args.stack == "c2" else "stack"] = stack_record(args, args.stack, args.stack_tie)
     print(json.dumps(line), flush=True)
 
 

@@ -372,6 +372,17 @@ spp_status spp_reset_run_stats(spp_ctx* ctx);
  * scratch), in us: the per-expert cost c of the prefetch budget. */
 spp_status spp_profile_expert_copy(spp_ctx* ctx, int32_t l, int32_t reps, double* per_expert_us);
 
+/* HBM read ceiling of the batch-1 FFN's access pattern (measurement, not part
+ * of the hot path): the loads of one FFN launch over K expert slots -- the
+ * same grid, unit order and 16-byte non-temporal loads as the sweep-round FFN
+ * kernel of this context -- without its arithmetic, timed by the kernel's own
+ * begin/end stamps and averaged over `reps` launches (after two untimed
+ * ones), each launch on other slots of the context's pools.  us_out: average
+ * time per launch; gbs_out: K expert blobs per launch / that time.  Waits for
+ * all enqueued work first.  ESTATE unless the experts are bf16 in the batch-1
+ * unit layout; EINVAL for reps outside 1..10000. */
+spp_status spp_probe_read_ceiling(spp_ctx* ctx, int32_t reps, double* us_out, double* gbs_out);
+
 /* Where moe_layer_forward takes the priorities for the next layer's prefetch
  * (Table 5).  SPP_PREFETCH_ADAPTER (default): the layer's adapter, as above.
  * SPP_PREFETCH_PREV_TOKEN (Naive Prefetch): the experts layer l+1 activated

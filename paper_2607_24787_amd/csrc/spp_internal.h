@@ -130,6 +130,11 @@ int ffn_grid_for(int nunits, int target_wgs, int* upw);
 // number of rounds (*rounds, 1..3) that puts the grid nearest `target_wgs`
 // workgroups; returns the grid, or 0 when it would exceed ffn_max_grid().
 int ffn_grid_slices(int nunits, int D, int dtype, int target_wgs, int* rounds);
+// The loads of a bf16 ffn_slices_kernel launch with the same arguments and
+// grid, and nothing else (a read-ceiling probe); one checksum word per
+// workgroup into sink [grid]; start/stop stamped with the kernel's own times.
+hipError_t launch_read_probe(const FfnArgs& a, int grid, uint32_t* sink, hipStream_t st, hipEvent_t start,
+                             hipEvent_t stop);
 // 4-bit experts: whole passes of kFfnWaves * upp units per workgroup (upp 3
 // or 4 units per wave and pass), as many as keep the grid near 256 workgroups.
 int ffn_grid_q4(int nunits, int I, int* upw, int* upp);

@@ -874,6 +874,64 @@ __global__ __launch_bounds__(64 * kSlWaves) void ffn_slices_kernel(FfnArgs a) {
 }
 
 // ---------------------------------------------------------------------------
+// Read-ceiling probe (measurement only, never on the hot path): the loads of
+// ffn_slices_kernel -- same grid, rounds, unit order and D-slices, the same
+// non-temporal 16-byte loads -- with no arithmetic beyond folding the loaded
+// words into one checksum per workgroup.  Its time is what the FFN's own
+// access pattern can stream from HBM on this part.
+// ---------------------------------------------------------------------------
+template <int NCH, int R, int DS>
+__global__ __launch_bounds__(64 * kSlWaves) void read_probe_kernel(FfnArgs a, uint32_t* sink) {
+  using T = uint16_t;
+  constexpr int V = Vec<T>::N;
+  constexpr int W = kSlWaves;
+  const int lane = threadIdx.x & 63;
+  const int wave = __builtin_amdgcn_readfirstlane(static_cast<int>(threadIdx.x) >> 6);
+  const int D = a.D, nch = D / V, I = a.I;
+  const int total = a.nW * I;
+  const int band = static_cast<int>(gridDim.x) * W;
+  const int first = static_cast<int>(blockIdx.x) * W;
+  const size_t unit_elems = static_cast<size_t>(3) * D;
+  const int cpw = (nch + W - 1) / W;
+  const int c0 = wave * cpw;
+  uint4 rg[R][NCH], ru[R][NCH], rd[R][W][DS];
+#pragma unroll
+  for (int r = 0; r < R; ++r) {
+    const int ub = r * band + first;
+    const int u = ub + wave;
+    const int uc = u < total ? u : total - 1;
+    const int d = uc / I;
+    const T* base = reinterpret_cast<const T*>(a.blob[d]) + static_cast<size_t>(uc - d * I) * unit_elems;
+    load_chunks<NCH, false, true>(base, lane, nch, rg[r]);
+    load_chunks<NCH, false, true>(base + D, lane, nch, ru[r]);
+#pragma unroll
+    for (int w2 = 0; w2 < W; ++w2) {
+      const int v = ub + w2;
+      const int vc = v < total ? v : total - 1;
+      const int d2 = vc / I;
+      const T* dbase = reinterpret_cast<const T*>(a.blob[d2]) + static_cast<size_t>(vc - d2 * I) * unit_elems + 2 * D;
+#pragma unroll
+      for (int s = 0; s < DS; ++s) {
+        const int c = c0 + lane + 64 * s;
+        rd[r][w2][s] = ld_chunk<true>(dbase, lane + 64 * s < cpw && c < nch ? c : 0);
+      }
+    }
+  }
+  uint32_t z = 0;
+#pragma unroll
+  for (int r = 0; r < R; ++r) {
+#pragma unroll
+    for (int j = 0; j < NCH; ++j) z ^= rg[r][j].x ^ rg[r][j].w ^ ru[r][j].y ^ ru[r][j].z;
+#pragma unroll
+    for (int w2 = 0; w2 < W; ++w2)
+#pragma unroll
+      for (int s = 0; s < DS; ++s) z ^= rd[r][w2][s].x ^ rd[r][w2][s].w;
+  }
+  z = __builtin_amdgcn_readfirstlane(z) ^ __builtin_amdgcn_readlane(z, 63);
+  if (threadIdx.x == 0) sink[blockIdx.x] = z;
+}
+
+// ---------------------------------------------------------------------------
 // Routed-expert SwiGLU FFN over 4-bit experts (batch 1).  Unit i of an expert
 // is one contiguous run: [gate codes | up codes | down codes] (D/2 bytes each,
 // two codes per byte, low nibble first) then [gate | up | down scales] (D/32
@@ -1903,6 +1961,24 @@ int ffn_grid_q4(int nunits, int I, int* upw, int* upp) {
     }
   *upw = pass * passes;
   return (nunits + *upw - 1) / *upw;
+}
+
+hipError_t launch_read_probe(const FfnArgs& a, int grid, uint32_t* sink, hipStream_t st, hipEvent_t start,
+                             hipEvent_t stop) {
+  if (a.nW <= 0 || a.nW > kMaxWork || grid <= 0 || a.rounds < 1 || a.rounds > 3 || !sink) return hipErrorInvalidValue;
+  if (static_cast<long>(grid) * kSlWaves * a.rounds < static_cast<long>(a.nW) * a.I) return hipErrorInvalidValue;
+  const int nchl = nch_for<uint16_t>(a.D);
+  if (a.rounds > 1 && nchl > 4) return hipErrorInvalidValue;
+#define SPP_PROBE(RR)                                                                                       \
+  SPP_DISPATCH_NCH(nchl, hipExtLaunchKernelGGL((read_probe_kernel<NCH, (NCH <= 4 ? RR : 1), slices_ds<NCH>()>), \
+                                                dim3(grid), dim3(64 * kSlWaves), 0, st, start, stop, 0u, a, sink))
+  switch (a.rounds) {
+    case 1: SPP_PROBE(1); break;
+    case 2: SPP_PROBE(2); break;
+    default: SPP_PROBE(3); break;
+  }
+#undef SPP_PROBE
+  return hipGetLastError();
 }
 
 int ffn_grid_slices(int nunits, int D, int dtype, int target_wgs, int* rounds) {

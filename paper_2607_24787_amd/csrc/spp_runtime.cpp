@@ -1501,6 +1501,47 @@ spp_status spp_profile_expert_copy(spp_ctx* c, int32_t l, int32_t reps, double* 
   return SPP_OK;
 }
 
+spp_status spp_probe_read_ceiling(spp_ctx* c, int32_t reps, double* us_out, double* gbs_out) {
+  if (spp_status s = check_ctx(c)) return s;
+  const spp_model_desc& d = c->d;
+  if (reps < 1 || reps > 10000) return fail(SPP_EINVAL, "reps must be in [1, 10000]");
+  if (d.dtype != SPP_DTYPE_BF16 || c->grouped || d.expert_codec != SPP_CODEC_PLAIN)
+    return fail(SPP_ESTATE, "the read probe needs bf16 experts in the batch-1 unit layout");
+  spp::FfnArgs fa{};
+  fa.nW = d.K;
+  fa.I = d.I;
+  fa.D = d.D;
+  const int grid = spp::ffn_grid_slices(d.K * d.I, d.D, d.dtype, c->ffn_wgs, &fa.rounds);
+  if (grid <= 0) return fail(SPP_ESTATE, "the batch-1 FFN of this shape does not use the sweep-round kernel");
+  if (spp_status e = sync_all(c)) return e;
+  hipEvent_t e0, e1;
+  SPP_HIP(hipEventCreate(&e0));
+  SPP_HIP(hipEventCreate(&e1));
+  const int64_t nslots = static_cast<int64_t>(d.L) * d.S;
+  double total_ms = 0.0;
+  hipError_t err = hipSuccess;
+  for (int32_t it = 0; it < reps + 2 && err == hipSuccess; ++it) {
+    // K slots per launch, rotating over every layer's pool so that a launch
+    // rarely finds its bytes in the last-level cache
+    for (int32_t k = 0; k < d.K; ++k) {
+      const int64_t slot = (static_cast<int64_t>(it) * d.K + k) % nslots;
+      fa.blob[k] = c->layers[slot / d.S].slots + static_cast<size_t>(slot % d.S) * c->stride;
+    }
+    err = spp::launch_read_probe(fa, grid, reinterpret_cast<uint32_t*>(c->partial), c->compute, e0, e1);
+    if (err == hipSuccess) err = hipEventSynchronize(e1);
+    float ms = 0.f;
+    if (err == hipSuccess) err = hipEventElapsedTime(&ms, e0, e1);
+    if (it >= 2) total_ms += ms;  // the first two launches warm the code and the TLB
+  }
+  (void)hipEventDestroy(e0);
+  (void)hipEventDestroy(e1);
+  if (err != hipSuccess) return fail(SPP_EHIP, std::string("read probe: ") + hipGetErrorString(err));
+  const double us = 1e3 * total_ms / reps;
+  if (us_out) *us_out = us;
+  if (gbs_out) *gbs_out = static_cast<double>(d.K) * c->blob_bytes / (us * 1e3);
+  return SPP_OK;
+}
+
 spp_status spp_debug_set_poison(spp_ctx* c, int32_t enabled) {
   if (spp_status s = check_ctx(c)) return s;
   c->poison = enabled != 0;
