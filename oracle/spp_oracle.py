@@ -387,10 +387,14 @@ class SlotCache:
 
 
 def expert_ffn(Wg: np.ndarray, Wu: np.ndarray, Wd: np.ndarray, x: np.ndarray) -> np.ndarray:
-    """Wd (silu(Wg x) * (Wu x)) in fp64 for one token."""
+    """Wd (silu(Wg x) * (Wu x)) in fp64 for one token x [D], or row by row for
+    the tokens of x [m, D] (one matrix product per weight; every row is the
+    one-token value)."""
     x = np.asarray(x, dtype=np.float64)
-    return np.asarray(Wd, dtype=np.float64) @ (silu(np.asarray(Wg, dtype=np.float64) @ x)
-                                               * (np.asarray(Wu, dtype=np.float64) @ x))
+    Wg, Wu, Wd = (np.asarray(w, dtype=np.float64) for w in (Wg, Wu, Wd))
+    if x.ndim == 1:
+        return Wd @ (silu(Wg @ x) * (Wu @ x))
+    return (silu(x @ Wg.T) * (x @ Wu.T)) @ Wd.T
 
 
 # --------------------------------------------------------------------------
@@ -411,9 +415,9 @@ def q4_decode_expert(gq, gs, uq, us, dq, ds):
 class OracleWeights:
     """Decoded (fp64-valued) weights of a workload, regenerated from its seeds.
 
-    Expert matrices are kept as decoded fp32 (exact for bf16 and fp32 storage)
-    in a bounded cache.  ``adapter_override(l) -> (A, B)`` replaces the seeded
-    adapters (values, not storage) for special-case tests.
+    Expert matrices are kept decoded as fp64 (exact for bf16, fp32 and 4-bit
+    storage) in a bounded cache.  ``adapter_override(l) -> (A, B)`` replaces
+    the seeded adapters (values, not storage) for special-case tests.
     """
 
     def __init__(self, cfg, cache_experts: int = 48, adapter_override=None):
@@ -429,7 +433,7 @@ class OracleWeights:
         self.adapter_override = adapter_override
 
     def _dec(self, a):
-        return decode(a, self.cfg.dtype).astype(np.float32)
+        return decode(a, self.cfg.dtype)
 
     def router(self, l: int) -> np.ndarray:
         if l not in self._router:
@@ -454,7 +458,7 @@ class OracleWeights:
         if key in self._cache:
             return self._cache[key]
         if self.cfg.codec == "q4":
-            w = tuple(a.astype(np.float32) for a in q4_decode_expert(*self.gen.expert_weights_q4(self.cfg, l, e)))
+            w = q4_decode_expert(*self.gen.expert_weights_q4(self.cfg, l, e))
         else:
             w = tuple(self._dec(a) for a in self.gen.expert_weights(self.cfg, l, e))
         self._cache[key] = w
@@ -475,8 +479,7 @@ class OracleWeights:
         key = (l, j)
         if key not in self._shared:
             if self.cfg.codec == "q4":
-                self._shared[key] = tuple(a.astype(np.float32) for a in
-                                          q4_decode_expert(*self.gen.shared_expert_weights_q4(self.cfg, l, j)))
+                self._shared[key] = q4_decode_expert(*self.gen.shared_expert_weights_q4(self.cfg, l, j))
             else:
                 self._shared[key] = tuple(self._dec(a) for a in self.gen.shared_expert_weights(self.cfg, l, j))
         return self._shared[key]
@@ -521,21 +524,27 @@ def layer_prologue(cfg, W: OracleWeights, l: int, h: np.ndarray):
 
 
 def moe_output(cfg, W: OracleWeights, l: int, cache: SlotCache, u, x, T, g):
-    """h' = u + sum_k g_k FFN_{T_k}(x) (+ shared experts with weight 1), weights
-    looked up through the slot each expert ran from (the round structure of the
-    on-demand step decides which slot held it at its turn)."""
+    """h'_b = u_b + sum_k g_bk FFN_{T_bk}(x_b) (+ shared experts with weight 1),
+    accumulated for each token in k order.  An expert must have run from a slot
+    (the round structure of the on-demand step decides which slot held it at its
+    turn).  FFN_e(x_b) is evaluated for all tokens routed to e at once (one
+    matrix product per weight of e, each row the one-token value)."""
     B = x.shape[0]
+    ffn = {}
+    for e in sorted(set(int(v) for v in np.asarray(T).ravel())):
+        if cache.run_slot.get(e, EMPTY) == EMPTY:
+            raise AssertionError("executed expert was never resident")
+        rows = [b for b in range(B) if e in T[b]]
+        Y = expert_ffn(*W.expert(l, e), x[rows])
+        for i, b in enumerate(rows):
+            ffn[(b, e)] = Y[i]
+    shared = [expert_ffn(*W.shared(l, j), x) for j in range(cfg.n_shared)]
     y = np.zeros((B, cfg.D))
     for b in range(B):
         for k in range(T.shape[1]):
-            e = int(T[b, k])
-            slot = cache.run_slot.get(e, EMPTY)
-            if slot == EMPTY:
-                raise AssertionError("executed expert was never resident")
-            Wg, Wu, Wd = W.expert(l, e)
-            y[b] += g[b, k] * expert_ffn(Wg, Wu, Wd, x[b])
+            y[b] += g[b, k] * ffn[(b, int(T[b, k]))]
         for j in range(cfg.n_shared):
-            y[b] += expert_ffn(*W.shared(l, j), x[b])
+            y[b] += shared[j][b]
     return u + y
 
 

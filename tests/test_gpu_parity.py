@@ -56,7 +56,11 @@ DSV2_B4 = w.get("c3").with_(L=2, batch=4, S=64, tokens=3)
 BATCH_BF16_ROUNDS = BATCH_BF16.with_(S=6)
 QWEN_B16_S32 = w.get("c4").with_(L=2, batch=16, S=32, tokens=2)
 QWEN_B64_S32 = w.get("c4").with_(L=2, tokens=2)
-C2_TIED = w.get("c2").with_(tokens=2, expert_layers=2)
+C2_TIED = w.get("c2").with_(tokens=8, expert_layers=2)
+# the batched 48-layer stack as specified: 64 sequences, 32 slots per layer
+# (about 126 distinct experts per layer: every step runs in on-demand rounds),
+# window 4, stand-in projection; offload tier tied over 2 expert layers
+C4_FULL = w.get("c4").with_(tokens=2, expert_layers=2)
 # the largest shapes a context accepts: D 4096 (bf16) / 2048 (fp32), 1024
 # experts, top-32, adapter rank 256
 MAX_BF16 = w.MoEConfig(name="max_bf16_D4096_n1024_k32_r256", L=2, D=4096, n=1024, K=32, I=16, r=256, S=40,
@@ -172,16 +176,20 @@ def test_lockstep_parity_naive_prefetch(torch_cuda, cfg, M_max, tokens, must_iss
         assert rep.prefetched > 0, "the case must exercise naive prefetches"
 
 
-@pytest.mark.parametrize("cfg,tokens", [(C3_FULL, 4), (C2_TIED, 2)], ids=["c3_stack12", "c2_stack48_tied"])
+@pytest.mark.parametrize("cfg,tokens", [(C3_FULL, 4), (C2_TIED, 8), (C4_FULL, 2)],
+                         ids=["c3_stack12", "c2_stack48_tied", "c4_stack48_b64_s32_tied"])
 def test_lockstep_parity_full_stacks(torch_cuda, cfg, tokens):
     from lockstep import run_lockstep
-    _log(f"[lockstep] {cfg.name} L={cfg.L} tokens={tokens}")
+    _log(f"[lockstep] {cfg.name} L={cfg.L} B={cfg.batch} S={cfg.S} tokens={tokens}")
     st = _stack(cfg)
     try:
-        rep = run_lockstep(st, cfg, tokens, cfg.window)
+        rep = run_lockstep(st, cfg, tokens, cfg.window,
+                           progress=lambda t, l: _log(f"[lockstep] {cfg.name} t={t} l={l}") if l % 16 == 15 else None)
     finally:
         st.close()
     _assert_report(rep, cfg, cfg.name)
+    if cfg.batch > 1:
+        assert rep.prefetched > 0
 
 
 def test_lockstep_parity_qwen_layer_full_size(torch_cuda):
@@ -189,10 +197,10 @@ def test_lockstep_parity_qwen_layer_full_size(torch_cuda):
     configuration the benchmark times (default FFN workgroups)."""
     from lockstep import run_lockstep
     cfg = w.get("c1")
-    _log(f"[lockstep] {cfg.name} full size, 10 tokens")
+    _log(f"[lockstep] {cfg.name} full size, 32 tokens")
     st = _stack(cfg)
     try:
-        rep = run_lockstep(st, cfg, 10, cfg.window)
+        rep = run_lockstep(st, cfg, 32, cfg.window)
     finally:
         st.close()
     _assert_report(rep, cfg, cfg.name)

@@ -150,6 +150,22 @@ def test_expert_ffn_against_torch():
     assert abs(o.expert_ffn(Wg2, Wu, Wd2, x)).max() < 1e-12
 
 
+def test_expert_ffn_rows_are_the_one_token_values():
+    """The row form (tokens routed to one expert at once) against torch's
+    batched F.linear and against the one-token form, row by row."""
+    rng = np.random.default_rng(7)
+    Wg, Wu = rng.normal(size=(30, 20)), rng.normal(size=(30, 20))
+    Wd = rng.normal(size=(20, 30))
+    X = rng.normal(size=(5, 20))
+    got = o.expert_ffn(Wg, Wu, Wd, X)
+    Xt = torch.tensor(X)
+    ref = F.linear(F.silu(F.linear(Xt, torch.tensor(Wg))) * F.linear(Xt, torch.tensor(Wu)), torch.tensor(Wd)).numpy()
+    assert got.shape == (5, 20)
+    np.testing.assert_allclose(got, ref, rtol=1e-12)
+    for i in range(5):
+        np.testing.assert_allclose(got[i], o.expert_ffn(Wg, Wu, Wd, X[i]), rtol=1e-12)
+
+
 def test_route_gates_and_adapter_scores_invariants():
     rng = np.random.default_rng(5)
     B, D, n, r, K = 5, 32, 10, 4, 3
