@@ -33,25 +33,33 @@ def _run(cmd):
     subprocess.run(cmd, check=True)
 
 
-def build(verbose: bool = True) -> str:
-    os.makedirs(BUILD, exist_ok=True)
+def build(verbose: bool = True, sanitize: str = "") -> str:
+    """Build libspp.so in the package.  sanitize "address" or "undefined":
+    instead, build the host runtime (g++ objects only; the HIP kernels are
+    compiled as usual) with that sanitizer into _build/<sanitize>/libspp.so,
+    for CPU test runs that load it through SPP_LIB_PATH (with the sanitizer's
+    runtime preloaded for ASan).  Returns the library's path."""
+    out_dir = BUILD if not sanitize else os.path.join(BUILD, sanitize)
+    os.makedirs(out_dir, exist_ok=True)
     inc = ["-I" + INCLUDE, "-I" + CSRC]
     objs = []
     for src in ("spp_kernels.hip", "spp_static.hip"):
-        obj = os.path.join(BUILD, src.replace(".hip", ".o"))
+        obj = os.path.join(out_dir, src.replace(".hip", ".o"))
         _run([HIPCC, *DEVICE_FLAGS, *inc, "-c", os.path.join(CSRC, src), "-o", obj])
         objs.append(obj)
+    san = ["-fsanitize=" + sanitize, "-fno-omit-frame-pointer", "-fno-sanitize-recover=all", "-g"] if sanitize else []
     for src in ("spp_runtime.cpp", "spp_policy.cpp"):
-        obj = os.path.join(BUILD, src.replace(".cpp", ".o"))
-        _run(["g++", *HOST_FLAGS, *inc, "-c", os.path.join(CSRC, src), "-o", obj])
+        obj = os.path.join(out_dir, src.replace(".cpp", ".o"))
+        _run(["g++", *HOST_FLAGS, *san, *inc, "-c", os.path.join(CSRC, src), "-o", obj])
         objs.append(obj)
-    tmp = LIB + ".tmp"
-    _run(["g++", "-shared", "-o", tmp, *objs, "-L" + os.path.join(ROCM, "lib"), "-lamdhip64",
+    lib = LIB if not sanitize else os.path.join(out_dir, "libspp.so")
+    tmp = lib + ".tmp"
+    _run(["g++", "-shared", *san, "-o", tmp, *objs, "-L" + os.path.join(ROCM, "lib"), "-lamdhip64",
           "-Wl,-rpath," + os.path.join(ROCM, "lib")])
-    shutil.move(tmp, LIB)
-    return LIB
+    shutil.move(tmp, lib)
+    return lib
 
 
 if __name__ == "__main__":
-    build()
+    build(sanitize=sys.argv[1] if len(sys.argv) > 1 else "")
     sys.exit(0)

@@ -13,7 +13,8 @@ from ctypes import POINTER, byref, c_char_p, c_double, c_float, c_int32, c_int64
 
 import numpy as np
 
-LIB_PATH = os.path.join(os.path.dirname(os.path.abspath(__file__)), "libspp.so")
+# SPP_LIB_PATH selects another build of the same library (a sanitized host runtime)
+LIB_PATH = os.environ.get("SPP_LIB_PATH") or os.path.join(os.path.dirname(os.path.abspath(__file__)), "libspp.so")
 
 SPP_OK, SPP_EINVAL, SPP_ENOMEM, SPP_EHIP, SPP_ESTATE = 0, -1, -2, -3, -4
 DTYPE_F32, DTYPE_BF16 = 0, 1
