@@ -29,12 +29,13 @@ struct RouterArgs {
   int32_t* topk;        // [B, K]
   float* gates;         // [B, K]
   float* s;             // [n]
-  int32_t* topk_host;   // [B, K] host-mapped mirror (device-visible address) or nullptr
-  float* gates_host;    // [B, K] host-mapped mirror or nullptr
-  float* s_host;        // [n] host-mapped mirror or nullptr
+  // host records (pinned, host-mapped; device-visible addresses) or nullptr:
+  // 8-byte words (seq << 32) | payload, each written by one store, so the
+  // host knows a record is this launch's when its high half equals seq
+  uint64_t* route_rec;  // [B*K][2]: expert id, gate (fp32 bits)
+  uint64_t* s_rec;      // [n]: priority s_e (fp32 bits)
   unsigned* counter;    // [2] zero between launches (router rows, adapter rows)
-  unsigned* done_host;  // [2] host-mapped completion flags (device-visible address) or nullptr
-  unsigned seq;         // written to done_host[0] once topk/gates mirrors are complete, to done_host[1] for s
+  unsigned seq;         // this launch's sequence number (never 0)
   int B, D, n, K, r;
   float eps;
   int x_given;          // u holds x (no normalisation)

@@ -210,26 +210,33 @@ __device__ __forceinline__ float rms_scale(float (&xv)[NCH][Vec<T>::N], int D, f
 
 constexpr int kEQ = kMaxExpertsTopK / kThreads;  // experts per thread in the tails
 
-// Host handoff.  The host mirrors are written with system-scope atomic stores,
+// Host handoff.  The host records are written with system-scope atomic stores,
 // which the GPU's caches do not hold back, and cross-workgroup values with
 // agent-scope atomic stores and loads.  For such stores, waiting until the
 // wave's own outstanding memory operations have completed is the whole of a
 // release: a store issued after the wait (a counter increment, a flag) is seen
 // only after them.  This avoids the L2 write-back that a release fence adds
 // for ordinary stores.
-__device__ __forceinline__ void st_system(float* p, float v) {
-  __hip_atomic_store(p, v, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_SYSTEM);
-}
-__device__ __forceinline__ void st_system(int32_t* p, int32_t v) {
-  __hip_atomic_store(p, v, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_SYSTEM);
-}
 __device__ __forceinline__ void wait_own_stores() { asm volatile("s_waitcnt vmcnt(0)" ::: "memory"); }
 
-// Completion flags, one lane, after wait_own_stores in every wave that wrote
-// host mirrors: word 0 = the launch's routing results (topk, gates of every
-// token), word 1 = its priorities s.
-__device__ __forceinline__ void raise_flag(const RouterArgs& a, int word) {
-  __hip_atomic_store(a.done_host + word, a.seq, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_SYSTEM);
+// One host record: the launch's sequence number in the high half and the
+// payload in the low half, in one 8-byte system-scope store.  The host takes
+// a record as written by this launch once its high half equals seq, so no
+// store has to complete before another is issued (a completion flag after
+// the results cost the host one more round trip over the host link).
+__device__ __forceinline__ void st_record(uint64_t* p, unsigned seq, uint32_t payload) {
+  __hip_atomic_store(p, (static_cast<uint64_t>(seq) << 32) | payload, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_SYSTEM);
+}
+
+// Token b's host records from wave 0 after select_topk (lane k < K: expert
+// s_isel[k], gate s_zsel[k]).
+__device__ __forceinline__ void route_records(const RouterArgs& a, int b, int tid, const float* s_zsel,
+                                              const int* s_isel) {
+  if (a.route_rec && tid < a.K) {
+    const int idx = b * a.K + tid;
+    st_record(a.route_rec + 2 * idx, a.seq, static_cast<uint32_t>(s_isel[tid]));
+    st_record(a.route_rec + 2 * idx + 1, a.seq, __float_as_uint(s_zsel[tid]));
+  }
 }
 
 // Order-preserving key of (logit z, expert e): key(e') > key(e) exactly when e'
@@ -252,8 +259,8 @@ __device__ __forceinline__ float key_logit(uint64_t k) {
 // the ranks are a permutation).  With n <= 128 two threads share an expert,
 // each counting over half of the candidates.  Wave 0 then forms the combine
 // weights (softmax over all n renormalised over the K selected = softmax over
-// the selected) and writes token b's outputs, the host mirrors included.
-// Every thread of the workgroup calls it.
+// the selected) and writes token b's device outputs; s_zsel[k] then holds
+// gate k (for route_records).  Every thread of the workgroup calls it.
 __device__ __forceinline__ void select_topk(const RouterArgs& a, const uint64_t* s_key, int b, int tid, int* s_rk,
                                             float* s_zsel, int* s_isel) {
   const int n = a.n;
@@ -290,10 +297,7 @@ __device__ __forceinline__ void select_topk(const RouterArgs& a, const uint64_t*
       const float gk = v / sum;
       a.topk[idx] = e;
       a.gates[idx] = gk;
-      if (a.topk_host) {
-        st_system(a.topk_host + idx, e);
-        st_system(a.gates_host + idx, gk);
-      }
+      s_zsel[tid] = gk;  // each lane rewrites only its own entry
     }
   }
 }
@@ -488,10 +492,7 @@ __global__ __launch_bounds__(kThreads) void router_adapter_kernel(RouterArgs a) 
     __syncthreads();
     select_topk(a, s_key, 0, tid, s_rk, s_zsel, s_isel);
     if (tid == 0) __hip_atomic_store(a.counter, 0u, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
-    if (a.done_host && tid < 64) {  // wave 0 wrote the mirrors
-      wait_own_stores();
-      if (tid == 0) raise_flag(a, 0);
-    }
+    route_records(a, 0, tid, s_zsel, s_isel);
     return;
   }
 
@@ -506,15 +507,10 @@ __global__ __launch_bounds__(kThreads) void router_adapter_kernel(RouterArgs a) 
     const int e = tid + kThreads * q;
     if (e < n) {
       a.s[e] = pi[q];
-      if (a.s_host) st_system(a.s_host + e, pi[q]);
+      if (a.s_rec) st_record(a.s_rec + e, a.seq, __float_as_uint(pi[q]));
     }
   }
   if (tid == 0) __hip_atomic_store(a.counter + 1, 0u, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
-  if (a.done_host) {
-    wait_own_stores();
-    __syncthreads();
-    if (tid == 0) raise_flag(a, 1);
-  }
 }
 
 // ---------------------------------------------------------------------------
@@ -556,7 +552,10 @@ __global__ __launch_bounds__(kThreads) void router_select_kernel(RouterArgs a) {
   bst.store(a, tid, s_B);
   __syncthreads();
   if (a.router_on) select_topk(a, s_key, b, tid, s_rk, s_zsel, s_isel);
-  if (!na && !a.done_host) return;
+  if (!na) {
+    if (a.router_on) route_records(a, b, tid, s_zsel, s_isel);
+    return;
+  }
   if (na) {
     float pi[kEQ];
     adapter_token<T>(a, s_a, staged, s_B, tid, lane, wave, s_red, pi);
@@ -567,16 +566,17 @@ __global__ __launch_bounds__(kThreads) void router_select_kernel(RouterArgs a) {
       if (e < n) st_agent(zrow + e, pi[q]);
     }
   }
-  wait_own_stores();  // release this token's distribution and host mirrors
+  wait_own_stores();  // release this token's distribution (device stores only so far)
   __syncthreads();
   if (tid == 0) {
     const unsigned prev = __hip_atomic_fetch_add(a.counter, 1u, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
     s_last = (prev == gridDim.x - 1);
   }
+  // the host records go out after the release: nothing waits for them
+  if (a.router_on) route_records(a, b, tid, s_zsel, s_isel);
   __syncthreads();
   if (!s_last) return;
-  if (a.done_host && a.router_on && tid == 0) raise_flag(a, 0);  // every token's mirrors have completed
-  if (na) {
+  {
     // s = sum over the tokens, in token order, of their distributions; the
     // loads go out 64 tokens at a time
     constexpr int kTB = 64;
@@ -591,15 +591,10 @@ __global__ __launch_bounds__(kThreads) void router_select_kernel(RouterArgs a) {
           if (b0 + q < a.B) acc += v[q];
       }
       a.s[e] = acc;
-      if (a.s_host) st_system(a.s_host + e, acc);
+      if (a.s_rec) st_record(a.s_rec + e, a.seq, __float_as_uint(acc));
     }
   }
   if (tid == 0) __hip_atomic_store(a.counter, 0u, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
-  if (na && a.done_host) {
-    wait_own_stores();
-    __syncthreads();
-    if (tid == 0) raise_flag(a, 1);
-  }
 }
 
 // ---------------------------------------------------------------------------

@@ -101,9 +101,15 @@ struct spp_ctx {
   float* x_dev = nullptr;      // [maxB, D] router input
   float* zbuf = nullptr;       // [maxB, n + r]
   uint8_t* res_dev = nullptr;  // topk [maxB*K] i32 | gates [maxB*K] f32 | s [n] f32
-  uint8_t* res_host = nullptr; // pinned, host-mapped mirror written by the router kernel
-  uint8_t* res_host_dev = nullptr;  // device-visible address of res_host
-  size_t res_bytes = 0, off_gates = 0, off_s = 0, off_flag = 0;
+  size_t res_bytes = 0, off_gates = 0, off_s = 0;
+  // host records written by the router kernels (pinned, host-mapped):
+  // routing [maxB*K][2] then priorities [n], each (seq << 32) | payload
+  uint64_t* rec_host = nullptr;
+  uint64_t* rec_host_dev = nullptr;  // device-visible address of rec_host
+  size_t rec_count = 0;
+  std::vector<int32_t> host_T;  // the last routing read from the records [maxB*K]
+  std::vector<float> host_g;    // its gates
+  std::vector<float> host_s;    // the last priorities [n]
   uint32_t router_seq = 0;  // last sequence number handed to a router launch
   int32_t prefetch_source = SPP_PREFETCH_ADAPTER;
   int32_t copy_engine = SPP_COPY_SPLIT;
@@ -494,7 +500,7 @@ void free_ctx(spp_ctx* c) {
                   static_cast<void*>(c->res_dev), static_cast<void*>(c->counter), static_cast<void*>(c->partial),
                   static_cast<void*>(c->probe_dev)})
     if (p) (void)hipFree(p);
-  if (c->res_host) (void)hipHostFree(c->res_host);
+  if (c->rec_host) (void)hipHostFree(c->rec_host);
   if (c->groups_host) (void)hipHostFree(c->groups_host);
   if (c->ypart) (void)hipFree(c->ypart);
   if (c->copy) (void)hipStreamDestroy(c->copy);
@@ -554,13 +560,17 @@ spp_status create_impl(const spp_model_desc* desc, void* stream, spp_ctx** out) 
   const size_t bk = static_cast<size_t>(d.max_batch) * d.K;
   c->off_gates = round_up(bk * sizeof(int32_t), 64);
   c->off_s = c->off_gates + round_up(bk * sizeof(float), 64);
-  c->off_flag = c->off_s + round_up(static_cast<size_t>(d.n) * sizeof(float), 64);
-  c->res_bytes = c->off_flag + 64;
+  c->res_bytes = c->off_s + round_up(static_cast<size_t>(d.n) * sizeof(float), 64);
   if (hipMalloc(&c->res_dev, c->res_bytes) != hipSuccess) return fail(SPP_ENOMEM, "result buffer allocation failed");
-  if (hipHostMalloc(&c->res_host, c->res_bytes, hipHostMallocMapped | hipHostMallocCoherent) != hipSuccess)
-    return fail(SPP_ENOMEM, "pinned result buffer allocation failed");
-  SPP_HIP(hipHostGetDevicePointer(reinterpret_cast<void**>(&c->res_host_dev), c->res_host, 0));
-  std::memset(c->res_host, 0, c->res_bytes);
+  c->rec_count = 2 * bk + static_cast<size_t>(d.n);
+  if (hipHostMalloc(&c->rec_host, c->rec_count * sizeof(uint64_t), hipHostMallocMapped | hipHostMallocCoherent) !=
+      hipSuccess)
+    return fail(SPP_ENOMEM, "pinned record buffer allocation failed");
+  SPP_HIP(hipHostGetDevicePointer(reinterpret_cast<void**>(&c->rec_host_dev), c->rec_host, 0));
+  std::memset(c->rec_host, 0, c->rec_count * sizeof(uint64_t));  // sequence 0 is never handed out
+  c->host_T.assign(bk, 0);
+  c->host_g.assign(bk, 0.f);
+  c->host_s.assign(d.n, 0.f);
   // batched decode runs the routed experts as grouped MFMA contractions
   c->grouped = tiled_layout(d);
   if (c->grouped) {
@@ -587,22 +597,46 @@ uint32_t next_router_seq(spp_ctx* c) {
   return c->router_seq;
 }
 
-// Wait until the router launch tagged `seq` has written a part of its host
-// mirrors: flag word 0 covers the routing results (topk, gates), word 1 the
-// priorities s.  The kernel stores the flag once the mirrors' stores have
-// completed.  After about 20 ms of spinning (queued work ahead of the router)
-// the wait blocks on the stream instead; a flag still not set then is an error.
-spp_status wait_router(spp_ctx* c, uint32_t seq, int word) {
-  const uint32_t* flag = reinterpret_cast<const uint32_t*>(c->res_host + c->off_flag) + word;
+// Wait until the router launch tagged `seq` has written its host records:
+// kind 0 the routing of B tokens (expert and gate of every (b, k)), kind 1 the
+// priorities s; then copy their payloads into host_T / host_g or host_s.  A
+// record is this launch's once its high half equals seq; records only ever
+// move on to a newer launch's, so the scan resumes where it stopped.  After
+// about 20 ms of spinning (queued work ahead of the router) the wait blocks on
+// the stream instead; records still missing then are an error.
+spp_status wait_router(spp_ctx* c, uint32_t seq, int kind, int32_t B) {
+  const size_t bk2 = 2 * static_cast<size_t>(c->d.max_batch) * c->d.K;
+  const uint64_t* rec = c->rec_host + (kind == 0 ? 0 : bk2);
+  const size_t count = kind == 0 ? 2 * static_cast<size_t>(B) * c->d.K : static_cast<size_t>(c->d.n);
   const auto t0 = std::chrono::steady_clock::now();
-  for (uint32_t it = 1;; ++it) {
-    if (__atomic_load_n(flag, __ATOMIC_ACQUIRE) == seq) return SPP_OK;
+  size_t i = 0;
+  for (uint32_t it = 1; i < count; ++it) {
+    if (static_cast<uint32_t>(__atomic_load_n(rec + i, __ATOMIC_ACQUIRE) >> 32) == seq) {
+      ++i;
+      continue;
+    }
     if ((it & 1023u) == 0 && std::chrono::steady_clock::now() - t0 > std::chrono::milliseconds(20)) break;
     _mm_pause();
   }
-  SPP_HIP(hipStreamSynchronize(c->compute));
-  if (__atomic_load_n(flag, __ATOMIC_ACQUIRE) == seq) return SPP_OK;
-  return fail(SPP_EHIP, "router results were not signalled by the router launch");
+  if (i < count) {
+    SPP_HIP(hipStreamSynchronize(c->compute));
+    for (; i < count; ++i)
+      if (static_cast<uint32_t>(__atomic_load_n(rec + i, __ATOMIC_ACQUIRE) >> 32) != seq)
+        return fail(SPP_EHIP, "router results were not written by the router launch");
+  }
+  if (kind == 0) {
+    for (size_t j = 0; j < count / 2; ++j) {
+      c->host_T[j] = static_cast<int32_t>(static_cast<uint32_t>(rec[2 * j]));
+      const uint32_t gb = static_cast<uint32_t>(rec[2 * j + 1]);
+      std::memcpy(&c->host_g[j], &gb, sizeof(float));
+    }
+  } else {
+    for (size_t j = 0; j < count; ++j) {
+      const uint32_t sb = static_cast<uint32_t>(rec[j]);
+      std::memcpy(&c->host_s[j], &sb, sizeof(float));
+    }
+  }
+  return SPP_OK;
 }
 
 // Whether a prefetch copy enqueued by an earlier layer call may still be
@@ -864,9 +898,8 @@ spp_status layer_forward_impl(spp_ctx* c, int32_t l, const void* h_in, void* h_o
   ra.topk = topk_dev;
   ra.gates = gates_dev;
   ra.s = s_dev;
-  ra.topk_host = reinterpret_cast<int32_t*>(c->res_host_dev);
-  ra.gates_host = reinterpret_cast<float*>(c->res_host_dev + c->off_gates);
-  ra.s_host = adapter_on ? reinterpret_cast<float*>(c->res_host_dev + c->off_s) : nullptr;
+  ra.route_rec = c->rec_host_dev;
+  ra.s_rec = adapter_on ? c->rec_host_dev + 2 * static_cast<size_t>(d.max_batch) * d.K : nullptr;
   ra.counter = c->counter;
   ra.B = B;
   ra.D = d.D;
@@ -876,21 +909,20 @@ spp_status layer_forward_impl(spp_ctx* c, int32_t l, const void* h_in, void* h_o
   ra.eps = d.rms_eps;
   ra.x_given = 0;
   ra.router_on = 1;
-  ra.done_host = reinterpret_cast<unsigned*>(c->res_host_dev + c->off_flag);
   ra.seq = next_router_seq(c);
   SPP_HIP(spp::launch_router(ra, dt, c->compute));
   if (c->timing) SPP_HIP(hipEventRecord(ts.ev[kEvRouted], c->compute));
   const bool split_ok = c->ffn_overlap && !c->grouped && B == 1;
   if (split_ok) SPP_HIP(hipEventRecord(c->route_done, c->compute));
-  if (spp_status e = wait_router(c, ra.seq, 0)) {
+  if (spp_status e = wait_router(c, ra.seq, 0, B)) {
     c->clock = tau - 1;
     if (c->timing) c->free_sets.push_back(ts);
     return e;
   }
 
-  const int32_t* T = reinterpret_cast<const int32_t*>(c->res_host);
-  const float* g = reinterpret_cast<const float*>(c->res_host + c->off_gates);
-  const float* s = reinterpret_cast<const float*>(c->res_host + c->off_s);
+  const int32_t* T = c->host_T.data();
+  const float* g = c->host_g.data();
+  const float* s = c->host_s.data();  // valid after the wait for kind 1
   const int32_t BK = B * d.K;
   const bool batched = c->grouped;  // the tiled layout is read by the grouped kernel only
   {
@@ -962,7 +994,7 @@ spp_status layer_forward_impl(spp_ctx* c, int32_t l, const void* h_in, void* h_o
   // prefetch selection for layer l+1 (the copies are enqueued after this
   // layer's loads); the adapter's priorities have their own flag
   if (adapter_on)
-    if (spp_status e = wait_router(c, ra.seq, 1)) return e;
+    if (spp_status e = wait_router(c, ra.seq, 1, B)) return e;
   LayerState* nx = predict && M_max > 0 ? &c->layers[l + 1] : nullptr;
   c->last_pref.clear();
   c->last_s_valid = predict;
@@ -1307,7 +1339,7 @@ spp_status adapter_predict(spp_ctx* c, int32_t l, const float* x_dev, int32_t B,
   if (!ls.A || d.r == 0) return fail(SPP_ESTATE, "layer has no adapter");
   spp::RouterArgs ra{};
   ra.u = x_dev;
-  ra.s_host = reinterpret_cast<float*>(c->res_host_dev + c->off_s);
+  ra.s_rec = c->rec_host_dev + 2 * static_cast<size_t>(d.max_batch) * d.K;
   ra.A = ls.A;
   ra.Bm = ls.Bm;
   ra.zbuf = c->zbuf;
@@ -1322,11 +1354,10 @@ spp_status adapter_predict(spp_ctx* c, int32_t l, const float* x_dev, int32_t B,
   ra.x_given = 1;
   ra.router_on = 0;
   c->logits_valid = false;
-  ra.done_host = reinterpret_cast<unsigned*>(c->res_host_dev + c->off_flag);
   ra.seq = next_router_seq(c);
   SPP_HIP(spp::launch_router(ra, d.dtype, c->compute));
-  if (spp_status e = wait_router(c, ra.seq, 1)) return e;
-  std::memcpy(s_out, c->res_host + c->off_s, sizeof(float) * d.n);
+  if (spp_status e = wait_router(c, ra.seq, 1, B)) return e;
+  std::memcpy(s_out, c->host_s.data(), sizeof(float) * d.n);
   return SPP_OK;
 }
 
