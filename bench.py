@@ -475,8 +475,8 @@ def main():
     achieved = ffn_bytes / (on["ffn_kernel_us"] * 1e3)                   # GB/s
     # the FFN kernel this context runs: grouped MFMA over the tiled layout, or the unit-stream kernel
     layout = spp.spp_blob_layout(stack.desc)
-    kernel = {spp.LAYOUT_TILED: "ffn_grouped_kernel", spp.LAYOUT_Q4_UNITS: "ffn_q4_kernel"}.get(layout,
-                                                                                             "ffn_units_kernel")
+    kernel = {spp.LAYOUT_TILED: "ffn_grouped_kernel", spp.LAYOUT_Q4_UNITS: "ffn_q4_kernel"}.get(
+        layout, "ffn_units_kernel" if args.ffn_overlap else "ffn_slices_kernel")
     step_bytes = step_hbm_bytes(cfg, on["distinct_experts_per_layer"])
     hbm_ceiling = HBM_PEAK_GBS * 1e9 * cfg.batch / step_bytes          # tokens/s at 8 TB/s
     workload = cfg.name + ("" if not over else "+" + ",".join(f"{k}={v}" for k, v in over.items()))
