@@ -205,9 +205,13 @@ def distill_adapters(stack, cfg, seqs: int, length: int):
     return new, info
 
 
-def cpu_baseline(cfg, tokens: int):
-    """The oracle, untuned, on the host cores: decode of the first `tokens` steps
-    through all layers (expert weights decoded before the timed region)."""
+def cpu_baseline(cfg, tokens: int, target_s: float = 15.0):
+    """The oracle, untuned, on the host cores: decode of the first steps of the
+    workload through all layers (expert weights decoded before the timed
+    region).  A first pass over `tokens` steps sizes the sample: while a pass
+    takes less than a third of `target_s`, the next one decodes as many steps
+    as the last pass's rate puts at about `target_s` seconds (at most 20,000,
+    and at most three more passes); the last pass is the sample."""
     from concurrent.futures import ThreadPoolExecutor
 
     import threadpoolctl
@@ -222,13 +226,23 @@ def cpu_baseline(cfg, tokens: int):
         W.router(l)
         if l < cfg.L - 1:
             W.adapter(l)
-    h0 = gen.hidden_states(cfg, tokens=tokens)
     avail = len(os.sched_getaffinity(0))
-    with threadpoolctl.threadpool_limits(limits=avail, user_api="blas"):
-        blas = [p.get("num_threads") for p in threadpoolctl.threadpool_info() if p.get("user_api") == "blas"]
+
+    def timed(n):
+        h0 = gen.hidden_states(cfg, tokens=n)
         t0 = time.perf_counter()
         o.run_decode(cfg, W, h0, M_max=cfg.window)
-        dt = time.perf_counter() - t0
+        return time.perf_counter() - t0
+
+    with threadpoolctl.threadpool_limits(limits=avail, user_api="blas"):
+        blas = [p.get("num_threads") for p in threadpoolctl.threadpool_info() if p.get("user_api") == "blas"]
+        n = tokens
+        dt = timed(n)
+        for _ in range(3):
+            if dt >= target_s / 3 or n >= 20000:
+                break
+            n = min(20000, max(n + 1, int(n * target_s / max(dt, 1e-3))))
+            dt = timed(n)
     cpu_model = "unknown"
     try:
         with open("/proc/cpuinfo") as f:
@@ -236,10 +250,10 @@ def cpu_baseline(cfg, tokens: int):
     except (OSError, StopIteration):
         pass
     used = min(int(blas[0]), avail) if blas else 1
-    return {"value": tokens * cfg.batch / dt, "unit": "tokens/s", "cores": used,
+    return {"value": n * cfg.batch / dt, "unit": "tokens/s", "cores": used,
             "kind": "oracle", "blas_threads": int(blas[0]) if blas else None, "host_cores_available": avail,
             "cpu_model": cpu_model,
-            "sample": f"first {tokens} decode steps of the same workload (batch {cfg.batch}, all {cfg.L} layers, "
+            "sample": f"first {n} decode steps of the same workload (batch {cfg.batch}, all {cfg.L} layers, "
                       f"M_max={cfg.window}), fp64 numpy with BLAS on {used} threads, expert weights decoded "
                       f"before the timed region, {dt:.1f} s"}
 
@@ -289,7 +303,7 @@ def stack_record(args, key: str, tie: int):
            "h2d_gbs_during_run": on["h2d_gbs_during_run"],
            "modes": {"on": on, "off": off}}
     if args.stack_cpu_tokens > 0:
-        _log(f"[bench] stack cpu baseline: oracle on {args.stack_cpu_tokens} tokens")
+        _log(f"[bench] stack cpu baseline: oracle, probe of {args.stack_cpu_tokens} tokens")
         rec["cpu_baseline"] = cpu_baseline(cfg, args.stack_cpu_tokens)
     return rec
 
@@ -301,7 +315,7 @@ def main():
     ap.add_argument("--warmup", type=int, default=16)
     ap.add_argument("--workload", default="c1", help="configuration key in workload.configs")
     ap.add_argument("--cpu-tokens", type=int, default=192,
-                    help="oracle sample size in decode steps (0 disables); 192 steps take about 15 s on 16 host cores")
+                    help="oracle probe size in decode steps (0 disables); the timed sample grows from it to about 15 s")
     ap.add_argument("--ablation", type=int, default=1, help="also time OFF, PRED0 and Naive Prefetch modes")
     ap.add_argument("--ffn-wgs", type=int, default=0, help="FFN workgroups (0: library default)")
     ap.add_argument("--ffn-overlap", type=int, default=0,
@@ -328,7 +342,7 @@ def main():
                     help="workload key of the whole-stack record run after the headline pair ('' disables)")
     ap.add_argument("--stack-tie", type=int, default=4,
                     help="distinct expert layers of the stack record's offload tier (0: one per layer)")
-    ap.add_argument("--stack-cpu-tokens", type=int, default=1, help="oracle sample of the stack record (steps)")
+    ap.add_argument("--stack-cpu-tokens", type=int, default=1, help="oracle probe of the stack record in steps (0 disables); the sample grows to about 15 s")
     ap.add_argument("--copy-probe", action="store_true",
                     help="only run a 256 MiB device-to-device copy three times (counter calibration)")
     args = ap.parse_args()
@@ -540,7 +554,7 @@ def main():
         line["distill"] = distilled
     stack.close()
     if args.cpu_tokens > 0:
-        _log(f"[bench] cpu baseline: oracle on {args.cpu_tokens} tokens")
+        _log(f"[bench] cpu baseline: oracle, probe of {args.cpu_tokens} tokens")
         line["cpu_baseline"] = cpu_baseline(cfg, args.cpu_tokens)
     if args.stack:
         line["stack48" if args.stack == "c2" else "stack"] = stack_record(args, args.stack, args.stack_tie)

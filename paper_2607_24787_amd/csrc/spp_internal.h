@@ -53,8 +53,10 @@ struct FfnArgs {
                                // workgroup whose units belong to a skipped item writes nothing; a
                                // nonzero mask needs upw to divide I (each workgroup on one item)
   int codec;                   // 0: experts in dtype; 1: 4-bit blocks (dtype bf16)
-  int rounds;                  // 0: workgroup b takes units [b*upw, (b+1)*upw) (ffn_units_kernel);
-                               // 1..3: sweep rounds of ffn_slices_kernel (see ffn_grid_slices); upw unused
+  int rounds;                  // 0: workgroup b takes units [b*upw, (b+1)*upw) (ffn_units_kernel, and
+                               // ffn_q4_kernel by range); 1..3: sweep rounds of ffn_slices_kernel (see
+                               // ffn_grid_slices); 4-bit experts: 1..2 sweep passes of ffn_q4_kernel
+                               // (see ffn_grid_q4_sweep); upw unused in sweep order
   const float* x;              // [D] router input of the token
   const float* gates;
   float* partial;              // [gridDim.x, D]
@@ -131,6 +133,10 @@ int ffn_grid_for(int nunits, int target_wgs, int* upw);
 // number of rounds (*rounds, 1..3) that puts the grid nearest `target_wgs`
 // workgroups; returns the grid, or 0 when it would exceed ffn_max_grid().
 int ffn_grid_slices(int nunits, int D, int dtype, int target_wgs, int* rounds);
+// 4-bit experts in sweep order (no skip mask): passes (*rounds, 1 or 2) of 3
+// units per wave (*upp); returns the grid, or 0 when it would exceed
+// ffn_max_grid().
+int ffn_grid_q4_sweep(int nunits, int* rounds, int* upp);
 // The loads of a bf16 ffn_slices_kernel launch with the same arguments and
 // grid, and nothing else (a read-ceiling probe); one checksum word per
 // workgroup into sink [grid]; start/stop stamped with the kernel's own times.

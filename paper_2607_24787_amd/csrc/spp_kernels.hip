@@ -128,6 +128,24 @@ __device__ __forceinline__ float wave_max(float v) {
   return fmaxf(fmaxf(lane_value(v, 0), lane_value(v, 16)), fmaxf(lane_value(v, 32), lane_value(v, 48)));
 }
 
+// Unsigned maximum over the 64 lanes (the same DPP steps as wave_max); every
+// lane returns the same value.
+template <int CTRL>
+__device__ __forceinline__ uint32_t dpp_u32(uint32_t v) {
+  return static_cast<uint32_t>(__builtin_amdgcn_update_dpp(0, static_cast<int>(v), CTRL, 0xF, 0xF, false));
+}
+__device__ __forceinline__ uint32_t wave_max_u32(uint32_t v) {
+  v = max(v, dpp_u32<0xB1>(v));
+  v = max(v, dpp_u32<0x4E>(v));
+  v = max(v, dpp_u32<0x141>(v));
+  v = max(v, dpp_u32<0x140>(v));
+  const uint32_t a = static_cast<uint32_t>(__builtin_amdgcn_readlane(static_cast<int>(v), 0));
+  const uint32_t b = static_cast<uint32_t>(__builtin_amdgcn_readlane(static_cast<int>(v), 16));
+  const uint32_t c = static_cast<uint32_t>(__builtin_amdgcn_readlane(static_cast<int>(v), 32));
+  const uint32_t d = static_cast<uint32_t>(__builtin_amdgcn_readlane(static_cast<int>(v), 48));
+  return max(max(a, b), max(c, d));
+}
+
 __device__ __forceinline__ void st_agent(float* p, float v) {
   __hip_atomic_store(p, v, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
 }
@@ -243,16 +261,18 @@ __device__ __forceinline__ void route_records(const RouterArgs& a, int b, int ti
 // beats e under the Top-K rule -- a larger logit, or an equal logit and a lower
 // index.  -0 is folded into +0 first, so the two stay equal as in a float
 // comparison.
-__device__ __forceinline__ uint64_t topk_key(float z, int e) {
+__device__ __forceinline__ uint32_t logit_order(float z) {
   uint32_t u = __float_as_uint(z);
   if (u == 0x80000000u) u = 0u;
-  u = (u & 0x80000000u) ? ~u : (u | 0x80000000u);
-  return (static_cast<uint64_t>(u) << 32) | (0xFFFFFFFFu - static_cast<uint32_t>(e));
+  return (u & 0x80000000u) ? ~u : (u | 0x80000000u);
 }
-__device__ __forceinline__ float key_logit(uint64_t k) {
-  const uint32_t u = static_cast<uint32_t>(k >> 32);
+__device__ __forceinline__ float order_logit(uint32_t u) {
   return __uint_as_float((u & 0x80000000u) ? (u & 0x7FFFFFFFu) : ~u);
 }
+__device__ __forceinline__ uint64_t topk_key(float z, int e) {
+  return (static_cast<uint64_t>(logit_order(z)) << 32) | (0xFFFFFFFFu - static_cast<uint32_t>(e));
+}
+__device__ __forceinline__ float key_logit(uint64_t k) { return order_logit(static_cast<uint32_t>(k >> 32)); }
 
 // Top-K of one token by rank counting over its keys (LDS, n values): expert e
 // takes position rank(e) = #{e' : key(e') > key(e)} (the keys are distinct, so
@@ -396,13 +416,25 @@ struct BStage {
 // the rest the adapter-A rows, one wave per weight row.  Each kind hands off
 // in a single pass: the last router workgroup to finish selects the Top-K and
 // gates, the last adapter workgroup forms the adapter distribution -- the two
-// tails run at the same time on different compute units.  Adapter workgroups
-// fetch B together with their rows, so the scoring tail starts with B in
-// registers.
+// tails run at the same time on different compute units.
+//
+// EPL = 0: the general tails (any n up to kMaxExpertsTopK, K <= 32, any r),
+// run by the whole workgroup through LDS; adapter workgroups fetch B together
+// with their rows, so the scoring tail starts with B in registers.
+// EPL = 1 or 2 (bf16, n <= 64 * EPL, K <= 64, r <= 64 and a multiple of 8):
+// the tails run in wave 0 alone, with no barrier -- lane l holds experts
+// l + 64 q (q < EPL).  Top-K: K rounds of a wave maximum over the 32-bit
+// order of the available logits, the lowest index taking a tie (the same
+// order as topk_key).  Adapter: wave 0 of every adapter workgroup holds B's
+// rows of its lanes' experts in registers; the hidden unit a_j is broadcast
+// from lane j.  Both give the bits of the general tails: the same products in
+// the same order, and the distribution's sum as the sum of the per-64-expert
+// wave sums in expert order.
 // ---------------------------------------------------------------------------
-template <typename T, int NCH, bool FULL>
+template <typename T, int NCH, bool FULL, int EPL>
 __global__ __launch_bounds__(kThreads) void router_adapter_kernel(RouterArgs a) {
   constexpr int V = Vec<T>::N;
+  constexpr int kBC = 8;  // 16-byte chunks of one B row in the fast tail (r <= 64 bf16)
   const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
   const int D = a.D, nch = D / V, n = a.n, r = a.r;
   const int nr = a.router_on ? n : 0;
@@ -418,7 +450,7 @@ __global__ __launch_bounds__(kThreads) void router_adapter_kernel(RouterArgs a) 
   __shared__ int s_rk[kThreads];
   __shared__ float s_a[256];
   __shared__ uint64_t s_key[kMaxExpertsTopK];
-  __shared__ float s_B[kBStage];  // adapter B transposed ([r][n]) when n*r fits
+  __shared__ float s_B[EPL ? 1 : kBStage];  // adapter B transposed ([r][n]) when n*r fits
 
   // a wave past its kind's last row re-reads that row (a valid address) and drops it
   const int rows = adapter_wg ? na : nr;
@@ -429,7 +461,24 @@ __global__ __launch_bounds__(kThreads) void router_adapter_kernel(RouterArgs a) 
   load_chunks<NCH, FULL>(wrow, lane, has_row ? nch : 0, w);
   const bool staged = na && n * r <= kBStage;
   BStage<T> bst;
-  bst.load(a, tid, adapter_wg && staged);
+  uint4 rbf[EPL ? EPL : 1][kBC];
+  if (EPL == 0) {
+    bst.load(a, tid, adapter_wg && staged);
+  } else if (adapter_wg && wave == 0) {
+    // B rows of this lane's experts (a chunk past r, or a row past n, re-reads
+    // the first chunk of B and is dropped)
+    const int rc = r / 8;
+#pragma unroll
+    for (int q = 0; q < (EPL ? EPL : 1); ++q) {
+      const int e = lane + 64 * q;
+#pragma unroll
+      for (int c = 0; c < kBC; ++c) {
+        const bool ok = e < n && c < rc;
+        const uint4 v = ld16(static_cast<const uint8_t*>(a.Bm) + (ok ? (static_cast<size_t>(e) * r + 8 * c) * 2 : 0));
+        rbf[q][c] = ok ? v : make_uint4(0, 0, 0, 0);
+      }
+    }
+  }
 
   float xv[NCH][V];
   if (a.u) {
@@ -470,9 +519,102 @@ __global__ __launch_bounds__(kThreads) void router_adapter_kernel(RouterArgs a) 
 
   wait_own_stores();  // release this wave's value
   __syncthreads();
+  const int kind = adapter_wg ? 1 : 0;
+  const unsigned total = adapter_wg ? gridDim.x - gr : gr;
+  if (EPL) {
+    if (wave != 0) return;
+    unsigned prev = 0;
+    if (lane == 0) prev = __hip_atomic_fetch_add(a.counter + kind, 1u, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
+    prev = static_cast<unsigned>(__builtin_amdgcn_readfirstlane(static_cast<int>(prev)));
+    if (prev != total - 1) return;
+    if (!adapter_wg) {
+      constexpr int Q = EPL ? EPL : 1;
+      uint32_t u[Q];
+      bool av[Q];
+#pragma unroll
+      for (int q = 0; q < Q; ++q) {
+        const int e = lane + 64 * q;
+        av[q] = e < n;
+        u[q] = logit_order(ld_agent(a.zbuf + min(e, n - 1)));
+      }
+      float zsel = 0.f;
+      int isel = 0;
+      for (int k = 0; k < a.K; ++k) {
+        uint32_t c = 0;
+#pragma unroll
+        for (int q = 0; q < Q; ++q) c = max(c, av[q] ? u[q] : 0u);
+        const uint32_t m = wave_max_u32(c);
+        int e = -1;
+#pragma unroll
+        for (int q = 0; q < Q; ++q) {
+          const uint64_t hit = __ballot(av[q] && u[q] == m);
+          if (e < 0 && hit) e = 64 * q + __builtin_ctzll(hit);
+        }
+        if (lane == (e & 63)) {
+#pragma unroll
+          for (int q = 0; q < Q; ++q)
+            if (q == (e >> 6)) av[q] = false;
+        }
+        if (lane == k) {
+          zsel = order_logit(m);
+          isel = e;
+        }
+      }
+      const bool on = lane < a.K;
+      const float m0 = lane_value(zsel, 0);
+      const float v = on ? expf(zsel - m0) : 0.f;
+      const float sum = wave_sum(v);
+      if (lane == 0) __hip_atomic_store(a.counter, 0u, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
+      if (on) {
+        const float gk = v / sum;
+        a.topk[lane] = isel;
+        a.gates[lane] = gk;
+        if (a.route_rec) {
+          st_record(a.route_rec + 2 * lane, a.seq, static_cast<uint32_t>(isel));
+          st_record(a.route_rec + 2 * lane + 1, a.seq, __float_as_uint(gk));
+        }
+      }
+      return;
+    }
+    // adapter distribution pi_hat = softmax(B a)
+    constexpr int Q = EPL ? EPL : 1;
+    const float av = lane < na ? ld_agent(a.zbuf + n + lane) : 0.f;
+    float zh[Q];
+    float mx = -INFINITY;
+#pragma unroll
+    for (int q = 0; q < Q; ++q) {
+      float acc = 0.f;
+#pragma unroll
+      for (int c = 0; c < kBC; ++c) {
+        float f[8];
+        unpack<T>(rbf[q][c], f);
+#pragma unroll
+        for (int v = 0; v < 8; ++v) acc += f[v] * lane_value(av, 8 * c + v);
+      }
+      zh[q] = lane + 64 * q < n ? acc : -INFINITY;
+      mx = fmaxf(mx, zh[q]);
+    }
+    mx = wave_max(mx);
+    float pi[Q];
+    float sum = 0.f;
+#pragma unroll
+    for (int q = 0; q < Q; ++q) {
+      pi[q] = lane + 64 * q < n ? expf(zh[q] - mx) : 0.f;
+      sum = q == 0 ? wave_sum(pi[q]) : sum + wave_sum(pi[q]);
+    }
+    if (lane == 0) __hip_atomic_store(a.counter + 1, 0u, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
+#pragma unroll
+    for (int q = 0; q < Q; ++q) {
+      const int e = lane + 64 * q;
+      if (e < n) {
+        const float p = pi[q] / sum;
+        a.s[e] = p;
+        if (a.s_rec) st_record(a.s_rec + e, a.seq, __float_as_uint(p));
+      }
+    }
+    return;
+  }
   if (tid == 0) {
-    const int kind = adapter_wg ? 1 : 0;
-    const unsigned total = adapter_wg ? gridDim.x - gr : gr;
     const unsigned prev = __hip_atomic_fetch_add(a.counter + kind, 1u, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
     s_last = (prev == total - 1);
   }
@@ -936,7 +1078,13 @@ __global__ __launch_bounds__(64 * kSlWaves) void read_probe_kernel(FfnArgs a, ui
 // offset is folded out: a gate/up dot product is scale * (sum q x - 8 sum x)
 // with the block sums of x taken once, and the down accumulation adds
 // (h scale) q per element and subtracts 8 * sum(h scale) per block at the end.
-// Work list, wave order and the workgroup partials as in ffn_units_kernel.
+// Work list and workgroup partials as in ffn_units_kernel.  PASSES = 0: the
+// units kernel's assignment (workgroup b on units [b*upw, (b+1)*upw), which
+// the FFN split needs); PASSES = 1 or 2: sweep order as in ffn_slices_kernel
+// -- global wave g takes units g + NW (pass UPP + p), NW = G W, so the grid
+// streams one band of consecutive units at a time (8 Qwen-shaped experts:
+// 10.0 us at 512 workgroups of one pass against 11.0 us for the best range
+// assignment, 256 workgroups of two passes).
 // ---------------------------------------------------------------------------
 constexpr int kQ4TargetWgs = 256;
 
@@ -967,15 +1115,15 @@ __device__ __forceinline__ void q4_codes(const uint4& c, float (&q)[32]) {
   }
 }
 
-template <int NQ, bool FULLQ, int UPP>
+template <int NQ, bool FULLQ, int UPP, int PASSES>
 __global__ __launch_bounds__(kFfnThreads) void ffn_q4_kernel(FfnArgs a) {
-  extern __shared__ float s_red[];  // [kFfnWaves / 2][D] wave partials
+  extern __shared__ float s_red[];  // [kFfnWaves][D] wave partials
   const int tid = threadIdx.x, lane = tid & 63;
   const int wave = __builtin_amdgcn_readfirstlane(tid >> 6);
   const int D = a.D, I = a.I, nblk = D / 32;
   const size_t cb = static_cast<size_t>(D) / 2, sb = static_cast<size_t>(nblk) * 2;
   const size_t unit_bytes = 3 * cb + 3 * sb;
-  if ((a.skip_mask >> ((static_cast<int>(blockIdx.x) * a.upw) / I)) & 1u) return;  // another launch's item
+  if (PASSES == 0 && ((a.skip_mask >> ((static_cast<int>(blockIdx.x) * a.upw) / I)) & 1u)) return;  // another launch's item
 
   // lanes past the row's blocks read block 0 and keep zeros: no branch in front of the loads
   float xv[NQ][32], xs[NQ];
@@ -1009,9 +1157,17 @@ __global__ __launch_bounds__(kFfnThreads) void ffn_q4_kernel(FfnArgs a) {
   }
 
   const int total = a.nW * I;
-  const int u0 = blockIdx.x * a.upw;
-  const int u1 = min(u0 + a.upw, total);
-  for (int ub = u0 + wave; ub < u1; ub += kFfnWaves * UPP) {
+  // range assignment: units [u0, u1) of this workgroup, wave stride kFfnWaves;
+  // sweep order: the whole grid's units, stride NW
+  const int NW = static_cast<int>(gridDim.x) * kFfnWaves;
+  const int u0 = PASSES ? 0 : static_cast<int>(blockIdx.x) * a.upw;
+  const int u1 = PASSES ? total : min(u0 + a.upw, total);
+  const int ustride = PASSES ? NW : kFfnWaves;
+  const int ub0 = PASSES ? static_cast<int>(blockIdx.x) * kFfnWaves + wave : u0 + wave;
+  const int npass = PASSES ? PASSES : (a.upw + kFfnWaves * UPP - 1) / (kFfnWaves * UPP);
+  for (int pr = 0; pr < npass; ++pr) {
+    const int ub = ub0 + pr * UPP * ustride;
+    if (PASSES == 0 && ub >= u1) break;  // wave-uniform
     uint4 cg[UPP][NQ], cu[UPP][NQ], cd[UPP][NQ];
     uint16_t sg[UPP][NQ], su[UPP][NQ], sd[UPP][NQ];
     float gate[UPP];
@@ -1020,7 +1176,7 @@ __global__ __launch_bounds__(kFfnThreads) void ffn_q4_kernel(FfnArgs a) {
     // zero and its outputs are not stored)
 #pragma unroll
     for (int p = 0; p < UPP; ++p) {
-      const int uu = ub + p * kFfnWaves;
+      const int uu = ub + p * ustride;
       const int uc = uu < u1 ? uu : u1 - 1;  // wave-uniform
       const int d = uc / I;
       const int i = uc - d * I;
@@ -1044,7 +1200,7 @@ __global__ __launch_bounds__(kFfnThreads) void ffn_q4_kernel(FfnArgs a) {
     __builtin_amdgcn_sched_barrier(0);
 #pragma unroll
     for (int p = 0; p < UPP; ++p) {
-      if (ub + p * kFfnWaves >= u1) continue;  // wave-uniform: no work past the range (its loads are harmless)
+      if (ub + p * ustride >= u1) continue;  // wave-uniform: no work past the range (its loads are harmless)
       float gs = 0.f, us = 0.f;
 #pragma unroll
       for (int q = 0; q < NQ; ++q) {
@@ -1080,40 +1236,22 @@ __global__ __launch_bounds__(kFfnThreads) void ffn_q4_kernel(FfnArgs a) {
 #pragma unroll
     for (int j = 0; j < 32; ++j) acc[q][j] -= 8.f * corr[q];
 
-  // sum the waves of this workgroup in a fixed order: (w + w+H) for w < H,
-  // then slots 0..H-1.  LDS layout: element 32 blk + 4k + e (k < 8, e < 4) at
-  // word 32 blk + 4 (k ^ (blk & 7)) + e, so that the 16-byte stores of eight
-  // consecutive lanes (blocks 128 bytes apart) and the natural-order reads of
-  // the last pass both touch every bank once (a plain layout puts all 64
-  // lanes on one bank: 3-8 us per launch).
-  constexpr int H = kFfnWaves / 2;
+  // sum the waves of this workgroup in a fixed order, (w0 + w2) + (w1 + w3),
+  // after one barrier.  LDS layout per wave: element 32 blk + 4k + e (k < 8,
+  // e < 4) at word 32 blk + 4 (k ^ (blk & 7)) + e, so that the 16-byte stores
+  // of eight consecutive lanes (blocks 128 bytes apart) and the natural-order
+  // reads both touch every bank once (a plain layout puts all 64 lanes on one
+  // bank: 3-8 us per launch; a second barrier and pass cost 0.3 us).
+  static_assert(kFfnWaves == 4, "the fold order below is written for four waves");
   float4* s_red4 = reinterpret_cast<float4*>(s_red);
-  if (wave >= H) {
 #pragma unroll
-    for (int q = 0; q < NQ; ++q) {
-      const int blk = lane + 64 * q;
-      if (FULLQ || blk < nblk) {
+  for (int q = 0; q < NQ; ++q) {
+    const int blk = lane + 64 * q;
+    if (FULLQ || blk < nblk) {
 #pragma unroll
-        for (int k = 0; k < 8; ++k)
-          s_red4[((wave - H) * D + 32 * blk) / 4 + (k ^ (blk & 7))] =
-              make_float4(acc[q][4 * k], acc[q][4 * k + 1], acc[q][4 * k + 2], acc[q][4 * k + 3]);
-      }
-    }
-  }
-  __syncthreads();
-  if (wave < H) {
-#pragma unroll
-    for (int q = 0; q < NQ; ++q) {
-      const int blk = lane + 64 * q;
-      if (FULLQ || blk < nblk) {
-#pragma unroll
-        for (int k = 0; k < 8; ++k) {
-          float4* slot = &s_red4[(wave * D + 32 * blk) / 4 + (k ^ (blk & 7))];
-          const float4 o = *slot;
-          *slot = make_float4(acc[q][4 * k] + o.x, acc[q][4 * k + 1] + o.y, acc[q][4 * k + 2] + o.z,
-                              acc[q][4 * k + 3] + o.w);
-        }
-      }
+      for (int k = 0; k < 8; ++k)
+        s_red4[(wave * D + 32 * blk) / 4 + (k ^ (blk & 7))] =
+            make_float4(acc[q][4 * k], acc[q][4 * k + 1], acc[q][4 * k + 2], acc[q][4 * k + 3]);
     }
   }
   __syncthreads();
@@ -1121,10 +1259,7 @@ __global__ __launch_bounds__(kFfnThreads) void ffn_q4_kernel(FfnArgs a) {
   for (int d = tid; d < D; d += kFfnThreads) {
     const int blk = d >> 5, j = d & 31;
     const int w = 32 * blk + 4 * ((j >> 2) ^ (blk & 7)) + (j & 3);
-    float v = s_red[w];
-#pragma unroll
-    for (int wv = 1; wv < H; ++wv) v += s_red[wv * D + w];
-    out[d] = v;
+    out[d] = (s_red[w] + s_red[2 * D + w]) + (s_red[D + w] + s_red[3 * D + w]);
   }
 }
 
@@ -1748,8 +1883,18 @@ hipError_t router_tf(const RouterArgs& a, hipStream_t st) {
   if (a.B == 1) {
     // router rows and adapter rows in workgroups of their own
     const int g1 = ((a.router_on ? a.n : 0) + kWaves - 1) / kWaves + ((a.A ? a.r : 0) + kWaves - 1) / kWaves;
-    SPP_DISPATCH_NCH(nch_for<T>(a.D), hipLaunchKernelGGL((router_adapter_kernel<T, NCH, FULL>), dim3(g1),
-                                                         dim3(kThreads), 0, st, a));
+    // single-wave tails: bf16, n <= 128, K <= 64, r <= 64 and a multiple of 8
+    const bool fast = sizeof(T) == 2 && a.n <= 128 && a.K <= 64 && (!a.A || (a.r <= 64 && a.r % 8 == 0));
+    if (fast && a.n <= 64) {
+      SPP_DISPATCH_NCH(nch_for<T>(a.D), hipLaunchKernelGGL((router_adapter_kernel<T, NCH, FULL, 1>), dim3(g1),
+                                                           dim3(kThreads), 0, st, a));
+    } else if (fast) {
+      SPP_DISPATCH_NCH(nch_for<T>(a.D), hipLaunchKernelGGL((router_adapter_kernel<T, NCH, FULL, 2>), dim3(g1),
+                                                           dim3(kThreads), 0, st, a));
+    } else {
+      SPP_DISPATCH_NCH(nch_for<T>(a.D), hipLaunchKernelGGL((router_adapter_kernel<T, NCH, FULL, 0>), dim3(g1),
+                                                           dim3(kThreads), 0, st, a));
+    }
     return hipGetLastError();
   }
   if (a.D % 16 != 0) return hipErrorInvalidValue;
@@ -1844,27 +1989,35 @@ hipError_t launch_router(const RouterArgs& a, int dtype, hipStream_t st) {
   return dtype == 1 ? router_t<uint16_t>(a, st) : router_t<float>(a, st);
 }
 
-template <int NQ, bool FULLQ, int UPP>
+template <int NQ, bool FULLQ, int UPP, int PASSES>
 hipError_t ffn_q4_tu(const FfnArgs& a, int grid, hipStream_t st, hipEvent_t start, hipEvent_t stop) {
-  const uint32_t lds = sizeof(float) * (kFfnWaves / 2) * a.D;
+  const uint32_t lds = sizeof(float) * kFfnWaves * a.D;  // 64 KiB at D 4096
   if (start || stop)
-    hipExtLaunchKernelGGL((ffn_q4_kernel<NQ, FULLQ, UPP>), dim3(grid), dim3(kFfnThreads), lds, st, start, stop, 0u,
-                          a);
+    hipExtLaunchKernelGGL((ffn_q4_kernel<NQ, FULLQ, UPP, PASSES>), dim3(grid), dim3(kFfnThreads), lds, st, start,
+                          stop, 0u, a);
   else
-    hipLaunchKernelGGL((ffn_q4_kernel<NQ, FULLQ, UPP>), dim3(grid), dim3(kFfnThreads), lds, st, a);
+    hipLaunchKernelGGL((ffn_q4_kernel<NQ, FULLQ, UPP, PASSES>), dim3(grid), dim3(kFfnThreads), lds, st, a);
   return hipGetLastError();
 }
 
 template <int NQ, bool FULLQ>
 hipError_t ffn_q4_t(const FfnArgs& a, int grid, hipStream_t st, hipEvent_t start, hipEvent_t stop) {
-  if (a.upp == 4) return ffn_q4_tu<NQ, FULLQ, 4>(a, grid, st, start, stop);
-  if (a.upp == 3) return ffn_q4_tu<NQ, FULLQ, 3>(a, grid, st, start, stop);
+  if (a.rounds > 0) {
+    // sweep order: 3 units per wave and pass, the grid's waves cover every unit
+    if (a.upp != 3 || a.rounds > 2 ||
+        static_cast<long>(grid) * kFfnWaves * 3 * a.rounds < static_cast<long>(a.nW) * a.I)
+      return hipErrorInvalidValue;
+    return a.rounds == 1 ? ffn_q4_tu<NQ, FULLQ, 3, 1>(a, grid, st, start, stop)
+                         : ffn_q4_tu<NQ, FULLQ, 3, 2>(a, grid, st, start, stop);
+  }
+  if (a.upp == 4) return ffn_q4_tu<NQ, FULLQ, 4, 0>(a, grid, st, start, stop);
+  if (a.upp == 3) return ffn_q4_tu<NQ, FULLQ, 3, 0>(a, grid, st, start, stop);
   return hipErrorInvalidValue;
 }
 
 hipError_t launch_ffn(const FfnArgs& a, int grid, int dtype, hipStream_t st, hipEvent_t start, hipEvent_t stop) {
   if (a.nW <= 0 || a.nW > kMaxWork || grid <= 0 || a.D > 4096) return hipErrorInvalidValue;
-  if (a.rounds > 0 && (a.codec != 0 || a.skip_mask != 0 || a.rounds > 3)) return hipErrorInvalidValue;
+  if (a.rounds > 0 && (a.skip_mask != 0 || a.rounds > (a.codec ? 2 : 3))) return hipErrorInvalidValue;
   if (a.rounds == 0 && a.upw <= 0) return hipErrorInvalidValue;
   if (a.skip_mask != 0 && a.I % a.upw != 0) return hipErrorInvalidValue;  // a workgroup would span two items
   if (a.codec == 1) {
@@ -1956,6 +2109,21 @@ int ffn_grid_q4(int nunits, int I, int* upw, int* upp) {
     }
   *upw = pass * passes;
   return (nunits + *upw - 1) / *upw;
+}
+
+int ffn_grid_q4_sweep(int nunits, int* rounds, int* upp) {
+  // one pass of 3 units per wave where the grid stays within the partial
+  // buffer (ffn_max_grid rows), else two; 0 where two passes do not fit
+  const int per_wg = kFfnWaves * 3;
+  for (int r = 1; r <= 2; ++r) {
+    const long grid = (static_cast<long>(nunits) + per_wg * r - 1) / (per_wg * r);
+    if (grid <= static_cast<long>(ffn_max_grid())) {
+      *rounds = r;
+      *upp = 3;
+      return static_cast<int>(grid);
+    }
+  }
+  return 0;
 }
 
 hipError_t launch_read_probe(const FfnArgs& a, int grid, uint32_t* sink, hipStream_t st, hipEvent_t start,

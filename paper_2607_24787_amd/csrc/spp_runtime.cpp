@@ -1032,9 +1032,15 @@ spp_status layer_forward_impl(spp_ctx* c, int32_t l, const void* h_in, void* h_o
     fa->x = c->x_dev + static_cast<size_t>(b) * d.D;
     fa->gates = gates_dev;
     fa->partial = c->partial;
-    if (d.expert_codec == SPP_CODEC_Q4) return spp::ffn_grid_q4(nW * d.I, d.I, &fa->upw, &fa->upp);
-    // the sweep-round kernel, except under the FFN split, whose two launches
-    // need every workgroup on one item (the units kernel's assignment)
+    // sweep order, except under the FFN split, whose two launches need every
+    // workgroup on one item (the units kernel's assignment)
+    if (d.expert_codec == SPP_CODEC_Q4) {
+      if (!split_ok) {
+        const int g = spp::ffn_grid_q4_sweep(nW * d.I, &fa->rounds, &fa->upp);
+        if (g > 0) return g;
+      }
+      return spp::ffn_grid_q4(nW * d.I, d.I, &fa->upw, &fa->upp);
+    }
     if (!split_ok) {
       const int g = spp::ffn_grid_slices(nW * d.I, d.D, d.dtype, c->ffn_wgs, &fa->rounds);
       if (g > 0) return g;
