@@ -7,6 +7,7 @@ the host-to-device copies of a memory-copy trace.
     python -m paper_2607_24787_amd.profsum traffic FETCH_DIR WRITE_DIR CAL_FETCH_DIR CAL_WRITE_DIR KERNEL \
         [--bytes ALGORITHMIC_BYTES_PER_LAUNCH]
     python -m paper_2607_24787_amd.profsum copies TRACE_DIR --blob BYTES [--overlap-kernel h2d_copy_kernel]
+    python -m paper_2607_24787_amd.profsum overlap TRACE_DIR KERNEL [KERNEL ...]
 
 Each reads the ``run_*.csv`` files rocprofv3 writes with ``-o run`` and prints
 markdown.  Measurement tooling: not part of the decode path.
@@ -127,6 +128,28 @@ def copies(trace_dir: str, blob: int, overlap_kernel: str = "h2d_copy_kernel", a
     return "\n".join(out)
 
 
+def overlap(trace_dir: str, names) -> str:
+    """Durations of the kernels whose names contain each of `names`, split by
+    whether a host-to-device DMA copy of the memory-copy trace ran during
+    them (any overlap) or not."""
+    cps = sorted((int(r["Start_Timestamp"]), int(r["End_Timestamp"]))
+                 for r in _rows(trace_dir, "run_memory_copy_trace.csv") if r["Direction"].endswith("HOST_TO_DEVICE"))
+    ks = [(int(r["Start_Timestamp"]), int(r["End_Timestamp"]), _short(r["Kernel_Name"]))
+          for r in _rows(trace_dir, "run_kernel_trace.csv")]
+
+    def busy(s, e):
+        return any(cs < e and ce > s for cs, ce in cps)
+
+    out = ["| kernel | launches with a DMA copy beside them | median µs | launches without | median µs |",
+           "|---|---|---|---|---|"]
+    for name in names:
+        w = [(e - s) / 1e3 for s, e, n in ks if name in n and busy(s, e)]
+        wo = [(e - s) / 1e3 for s, e, n in ks if name in n and not busy(s, e)]
+        med = lambda v: f"{statistics.median(v):.2f}" if v else "-"
+        out.append(f"| `{name}` | {len(w)} | {med(w)} | {len(wo)} | {med(wo)} |")
+    return "\n".join(out)
+
+
 def main():
     ap = argparse.ArgumentParser(description=__doc__, formatter_class=argparse.RawDescriptionHelpFormatter)
     sub = ap.add_subparsers(dest="cmd", required=True)
@@ -141,13 +164,18 @@ def main():
     c.add_argument("trace_dir")
     c.add_argument("--blob", type=int, required=True)
     c.add_argument("--overlap-kernel", default="h2d_copy_kernel")
+    o = sub.add_parser("overlap")
+    o.add_argument("trace_dir")
+    o.add_argument("kernels", nargs="+")
     a = ap.parse_args()
     if a.cmd == "kernels":
         print(kernels(a.trace_dir))
     elif a.cmd == "traffic":
         print(traffic(a.fetch_dir, a.write_dir, a.cal_fetch_dir, a.cal_write_dir, a.kernel, a.bytes, a.source))
-    else:
+    elif a.cmd == "copies":
         print(copies(a.trace_dir, a.blob, a.overlap_kernel))
+    else:
+        print(overlap(a.trace_dir, a.kernels))
 
 
 if __name__ == "__main__":
