@@ -37,6 +37,11 @@ def _stack(cfg, **kw):
 
 RAGGED = w.MoEConfig(name="ragged_bf16_D640_n40_k5", L=3, D=640, n=40, K=5, I=100, r=12, S=11, windows=(2,),
                      tokens=16, seed=3)
+# batch-1 bf16 shapes whose router tails run in one wave (r a multiple of 8,
+# n <= 64 and n <= 128: one and two experts per lane); RAGGED's r = 12 takes
+# the workgroup-wide tails
+ONE_WAVE_N40 = RAGGED.with_(name="ragged_bf16_D640_n40_k5_r16", r=16)
+ONE_WAVE_N100 = RAGGED.with_(name="ragged_bf16_D640_n100_k6_r16", n=100, K=6, r=16)
 PROJ = w.MoEConfig(name="proj_bf16_D512_n16_k4", L=3, D=512, n=16, K=4, I=128, r=8, S=8, windows=(2,),
                    tokens=10, has_proj=True, seed=5)
 BATCH = w.MoEConfig(name="batch3_f32_D128_n12_k3", L=2, D=128, n=12, K=3, I=64, r=8, S=12, windows=(2,),
@@ -89,7 +94,9 @@ def _assert_report(rep, cfg, name):
     (MAX_BF16, 4, 2),
     (MAX_F32, 4, 2),
     (w.get("c1p"), 2, 4),
-], ids=["c0_M1", "c0_M3", "ragged", "proj", "batch3", "c3_short", "max_bf16", "max_f32", "qwen_calibrated"])
+    (ONE_WAVE_N100, 2, 12),
+], ids=["c0_M1", "c0_M3", "ragged", "proj", "batch3", "c3_short", "max_bf16", "max_f32", "qwen_calibrated",
+        "ragged_one_wave_n100"])
 def test_lockstep_parity(torch_cuda, cfg, M_max, tokens):
     from lockstep import run_lockstep
     _log(f"[lockstep] {cfg.name} M_max={M_max} tokens={tokens}")
@@ -262,8 +269,9 @@ def test_adapter_predict_against_oracle(torch_cuda, cfg):
         st.close()
 
 
-@pytest.mark.parametrize("cfg", [RAGGED, RAGGED.with_(D=512), BATCH_BF16, BATCH],
-                         ids=["b1_bf16_D640", "b1_bf16_D512", "b5_bf16", "b3_f32"])
+@pytest.mark.parametrize("cfg", [RAGGED, RAGGED.with_(D=512), ONE_WAVE_N40, ONE_WAVE_N100, BATCH_BF16, BATCH],
+                         ids=["b1_bf16_D640", "b1_bf16_D512", "b1_bf16_n40_one_wave", "b1_bf16_n100_one_wave",
+                              "b5_bf16", "b3_f32"])
 def test_topk_ties_break_to_the_lower_index(torch_cuda, cfg):
     """Router rows repeated three ways (plus zero rows) make every logit tie
     with others exactly; the selection must equal the stable order of the
