@@ -108,7 +108,8 @@ def test_lockstep_parity(torch_cuda, cfg, M_max, tokens):
     _assert_report(rep, cfg, cfg.name)
 
 
-@pytest.mark.parametrize("cfg,M_max,tokens", [(RAGGED, 2, 10), (w.get("c1"), 2, 4)], ids=["ragged", "qwen_full"])
+@pytest.mark.parametrize("cfg,M_max,tokens", [(RAGGED, 2, 10), (w.get("c1"), 2, 4), (w.get("c3q4").with_(L=3), 2, 4)],
+                         ids=["ragged", "qwen_full", "dsv2_q4"])
 def test_lockstep_parity_with_the_ffn_split(torch_cuda, cfg, M_max, tokens):
     """The FFN split option (spp_set_ffn_overlap) runs every batch-1 FFN of the
     context with the item-aligned kernel, split or not: lock-step parity."""
@@ -374,9 +375,10 @@ def test_error_paths_on_device(torch_cuda):
         with pytest.raises(spp.SppError) as e:
             _stack(cfg, S=cfg.K - 1, resident=[])
         assert e.value.status == spp.SPP_EINVAL and "S must be" in str(e.value)
-        # refused layer calls leave the step clock and slot tables as they were
+        # refused layer calls leave the step clock, slot tables and run statistics as they were
         tau0 = spp.spp_get_clock(st.ctx)
         tab0 = spp.spp_get_slot_table(st.ctx, 0, cfg.S)
+        rs0 = spp.spp_get_run_stats(st.ctx).as_dict()
         for args in ((0, 1), (1, -2)):
             with pytest.raises(spp.SppError):
                 spp.moe_layer_forward(st.ctx, 0, st.hbuf[0].data_ptr(), st.hbuf[1].data_ptr(), args[0], cfg.K,
@@ -384,6 +386,7 @@ def test_error_paths_on_device(torch_cuda):
         assert spp.spp_get_clock(st.ctx) == tau0
         tab1 = spp.spp_get_slot_table(st.ctx, 0, cfg.S)
         assert tab1[0].tolist() == tab0[0].tolist() and tab1[1].tolist() == tab0[1].tolist()
+        assert spp.spp_get_run_stats(st.ctx).as_dict() == rs0
         # the context still works after refused calls
         topk, _, _ = st.layer(0, 0, 1, 1)
         assert topk.shape == (1, cfg.K)
