@@ -32,7 +32,9 @@ struct RouterArgs {
   // host records (pinned, host-mapped; device-visible addresses) or nullptr:
   // 8-byte words (seq << 32) | payload, each written by one store, so the
   // host knows a record is this launch's when its high half equals seq
-  uint64_t* route_rec;  // [B*K][2]: expert id, gate (fp32 bits)
+  uint64_t* route_rec;  // [B*K]: expert id of (b, k)
+  uint64_t* gate_rec;   // [B*K]: gate of (b, k) (fp32 bits); a separate array, so that the K
+                        // records of a token are one contiguous store per wave, not K
   uint64_t* s_rec;      // [n]: priority s_e (fp32 bits)
   unsigned* counter;    // [2] zero between launches (router rows, adapter rows)
   unsigned seq;         // this launch's sequence number (never 0)

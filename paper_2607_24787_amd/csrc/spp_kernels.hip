@@ -154,6 +154,7 @@ __device__ __forceinline__ float ld_agent(const float* p) {
 }
 
 typedef unsigned int u32x4 __attribute__((ext_vector_type(4)));
+typedef unsigned int u32x2 __attribute__((ext_vector_type(2)));
 
 // One 16-byte load; NT marks it non-temporal (streamed once, kept out of the caches' reuse set).
 template <bool NT>
@@ -252,8 +253,8 @@ __device__ __forceinline__ void route_records(const RouterArgs& a, int b, int ti
                                               const int* s_isel) {
   if (a.route_rec && tid < a.K) {
     const int idx = b * a.K + tid;
-    st_record(a.route_rec + 2 * idx, a.seq, static_cast<uint32_t>(s_isel[tid]));
-    st_record(a.route_rec + 2 * idx + 1, a.seq, __float_as_uint(s_zsel[tid]));
+    st_record(a.route_rec + idx, a.seq, static_cast<uint32_t>(s_isel[tid]));
+    st_record(a.gate_rec + idx, a.seq, __float_as_uint(s_zsel[tid]));
   }
 }
 
@@ -570,8 +571,8 @@ __global__ __launch_bounds__(kThreads) void router_adapter_kernel(RouterArgs a) 
         a.topk[lane] = isel;
         a.gates[lane] = gk;
         if (a.route_rec) {
-          st_record(a.route_rec + 2 * lane, a.seq, static_cast<uint32_t>(isel));
-          st_record(a.route_rec + 2 * lane + 1, a.seq, __float_as_uint(gk));
+          st_record(a.route_rec + lane, a.seq, static_cast<uint32_t>(isel));
+          st_record(a.gate_rec + lane, a.seq, __float_as_uint(gk));
         }
       }
       return;
@@ -1452,9 +1453,13 @@ __global__ __launch_bounds__(kGrpThreads) void ffn_grouped_kernel(GroupArgs a) {
       for (int v = 0; v < 4; ++v) acc[t][v] = 0.f;
     const uint16_t* drun = down + (static_cast<size_t>(dc) * I + i0) * kGrpBlk + lane * 4;
     for (int u = 0; u < nu; u += kUB) {
+      // non-temporal, as the phase-A loads: the down runs are read once per launch
       uint2 raw[kUB];
 #pragma unroll
-      for (int uu = 0; uu < kUB; ++uu) raw[uu] = *SPP_GLOBAL(uint2, drun + static_cast<size_t>(u + uu) * kGrpBlk);
+      for (int uu = 0; uu < kUB; ++uu) {
+        const u32x2 t = __builtin_nontemporal_load(SPP_GLOBAL(u32x2, drun + static_cast<size_t>(u + uu) * kGrpBlk));
+        raw[uu] = make_uint2(t.x, t.y);
+      }
 #pragma unroll
       for (int t = 0; t < kGroupTokens; ++t) {
         if (t < m) {  // wave-uniform
@@ -1475,11 +1480,14 @@ __global__ __launch_bounds__(kGrpThreads) void ffn_grouped_kernel(GroupArgs a) {
         }
       }
     }
+    // non-temporal: the partial rows are read once, by the combine.  Over 128
+    // Qwen-shaped experts at B = 64 (24 MiB of partials) the launch takes
+    // 183 us with no stores, 198 us with these and 204 us with plain stores.
 #pragma unroll
     for (int t = 0; t < kGroupTokens; ++t) {
       if (t < m) {
         float* dst = a.ypart + (static_cast<size_t>(s_pair[t]) * a.nsplit + split) * D + d0;
-        *reinterpret_cast<float4*>(dst) = make_float4(acc[t][0], acc[t][1], acc[t][2], acc[t][3]);
+        __builtin_nontemporal_store(f32x4{acc[t][0], acc[t][1], acc[t][2], acc[t][3]}, reinterpret_cast<f32x4*>(dst));
       }
     }
   }

@@ -605,34 +605,40 @@ uint32_t next_router_seq(spp_ctx* c) {
 // about 20 ms of spinning (queued work ahead of the router) the wait blocks on
 // the stream instead; records still missing then are an error.
 spp_status wait_router(spp_ctx* c, uint32_t seq, int kind, int32_t B) {
-  const size_t bk2 = 2 * static_cast<size_t>(c->d.max_batch) * c->d.K;
-  const uint64_t* rec = c->rec_host + (kind == 0 ? 0 : bk2);
-  const size_t count = kind == 0 ? 2 * static_cast<size_t>(B) * c->d.K : static_cast<size_t>(c->d.n);
+  // record arrays: expert ids [max_batch*K], gates [max_batch*K], priorities [n]
+  const size_t bkmax = static_cast<size_t>(c->d.max_batch) * c->d.K;
+  const size_t bk = static_cast<size_t>(B) * c->d.K;
+  const uint64_t* const part[2] = {kind == 0 ? c->rec_host : c->rec_host + 2 * bkmax,
+                                   kind == 0 ? c->rec_host + bkmax : nullptr};
+  const size_t count = kind == 0 ? bk : static_cast<size_t>(c->d.n);
   const auto t0 = std::chrono::steady_clock::now();
-  size_t i = 0;
-  for (uint32_t it = 1; i < count; ++it) {
-    if (static_cast<uint32_t>(__atomic_load_n(rec + i, __ATOMIC_ACQUIRE) >> 32) == seq) {
-      ++i;
-      continue;
+  for (int q = 0; q < 2 && part[q]; ++q) {
+    const uint64_t* rec = part[q];
+    size_t i = 0;
+    for (uint32_t it = 1; i < count; ++it) {
+      if (static_cast<uint32_t>(__atomic_load_n(rec + i, __ATOMIC_ACQUIRE) >> 32) == seq) {
+        ++i;
+        continue;
+      }
+      if ((it & 1023u) == 0 && std::chrono::steady_clock::now() - t0 > std::chrono::milliseconds(20)) break;
+      _mm_pause();
     }
-    if ((it & 1023u) == 0 && std::chrono::steady_clock::now() - t0 > std::chrono::milliseconds(20)) break;
-    _mm_pause();
-  }
-  if (i < count) {
-    SPP_HIP(hipStreamSynchronize(c->compute));
-    for (; i < count; ++i)
-      if (static_cast<uint32_t>(__atomic_load_n(rec + i, __ATOMIC_ACQUIRE) >> 32) != seq)
-        return fail(SPP_EHIP, "router results were not written by the router launch");
+    if (i < count) {
+      SPP_HIP(hipStreamSynchronize(c->compute));
+      for (; i < count; ++i)
+        if (static_cast<uint32_t>(__atomic_load_n(rec + i, __ATOMIC_ACQUIRE) >> 32) != seq)
+          return fail(SPP_EHIP, "router results were not written by the router launch");
+    }
   }
   if (kind == 0) {
-    for (size_t j = 0; j < count / 2; ++j) {
-      c->host_T[j] = static_cast<int32_t>(static_cast<uint32_t>(rec[2 * j]));
-      const uint32_t gb = static_cast<uint32_t>(rec[2 * j + 1]);
+    for (size_t j = 0; j < bk; ++j) {
+      c->host_T[j] = static_cast<int32_t>(static_cast<uint32_t>(part[0][j]));
+      const uint32_t gb = static_cast<uint32_t>(part[1][j]);
       std::memcpy(&c->host_g[j], &gb, sizeof(float));
     }
   } else {
     for (size_t j = 0; j < count; ++j) {
-      const uint32_t sb = static_cast<uint32_t>(rec[j]);
+      const uint32_t sb = static_cast<uint32_t>(part[0][j]);
       std::memcpy(&c->host_s[j], &sb, sizeof(float));
     }
   }
@@ -899,6 +905,7 @@ spp_status layer_forward_impl(spp_ctx* c, int32_t l, const void* h_in, void* h_o
   ra.gates = gates_dev;
   ra.s = s_dev;
   ra.route_rec = c->rec_host_dev;
+  ra.gate_rec = c->rec_host_dev + static_cast<size_t>(d.max_batch) * d.K;
   ra.s_rec = adapter_on ? c->rec_host_dev + 2 * static_cast<size_t>(d.max_batch) * d.K : nullptr;
   ra.counter = c->counter;
   ra.B = B;
