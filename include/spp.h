@@ -374,13 +374,15 @@ spp_status spp_profile_expert_copy(spp_ctx* ctx, int32_t l, int32_t reps, double
 
 /* HBM read ceiling of the batch-1 FFN's access pattern (measurement, not part
  * of the hot path): the loads of one FFN launch over K expert slots -- the
- * same grid, unit order and 16-byte non-temporal loads as the sweep-round FFN
- * kernel of this context -- without its arithmetic, timed by the kernel's own
- * begin/end stamps and averaged over `reps` launches (after two untimed
- * ones), each launch on other slots of the context's pools.  us_out: average
- * time per launch; gbs_out: K expert blobs per launch / that time.  Waits for
- * all enqueued work first.  ESTATE unless the experts are bf16 in the batch-1
- * unit layout; EINVAL for reps outside 1..10000. */
+ * same grid, unit order and loads as this context's sweep-order FFN kernel
+ * (bf16 experts: 16-byte non-temporal row loads; 4-bit experts: the code and
+ * scale loads of each block) -- without its arithmetic, timed by the
+ * kernel's own begin/end stamps and averaged over `reps` launches (after two
+ * untimed ones), each launch on other slots of the context's pools.  us_out:
+ * average time per launch; gbs_out: K expert blobs per launch / that time.
+ * Waits for all enqueued work first.  ESTATE unless the experts are bf16 or
+ * 4-bit (bf16 storage) in the batch-1 unit layout; EINVAL for reps outside
+ * 1..10000. */
 spp_status spp_probe_read_ceiling(spp_ctx* ctx, int32_t reps, double* us_out, double* gbs_out);
 
 /* Where moe_layer_forward takes the priorities for the next layer's prefetch

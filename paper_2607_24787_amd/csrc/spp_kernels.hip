@@ -1264,6 +1264,54 @@ __global__ __launch_bounds__(kFfnThreads) void ffn_q4_kernel(FfnArgs a) {
   }
 }
 
+// Read-ceiling probe of ffn_q4_kernel in sweep order (measurement only): the
+// same grid, passes, unit order and loads -- 16-byte non-temporal code loads
+// and 2-byte scale loads per row and block -- folded into one checksum per
+// workgroup, with no decode, arithmetic or LDS.
+template <int NQ, bool FULLQ, int PASSES>
+__global__ __launch_bounds__(kFfnThreads) void read_probe_q4_kernel(FfnArgs a, uint32_t* sink) {
+  constexpr int UPP = 3;
+  const int lane = threadIdx.x & 63;
+  const int wave = __builtin_amdgcn_readfirstlane(static_cast<int>(threadIdx.x) >> 6);
+  const int D = a.D, I = a.I, nblk = D / 32;
+  const size_t cb = static_cast<size_t>(D) / 2, sb = static_cast<size_t>(nblk) * 2;
+  const size_t unit_bytes = 3 * cb + 3 * sb;
+  const int total = a.nW * I;
+  const int NW = static_cast<int>(gridDim.x) * kFfnWaves;
+  const int ub0 = static_cast<int>(blockIdx.x) * kFfnWaves + wave;
+  uint32_t z = 0;
+#pragma unroll
+  for (int pr = 0; pr < PASSES; ++pr) {
+    const int ub = ub0 + pr * UPP * NW;
+    u32x4 cg[UPP][NQ], cu[UPP][NQ], cd[UPP][NQ];
+    uint16_t sg[UPP][NQ], su[UPP][NQ], sd[UPP][NQ];
+#pragma unroll
+    for (int p = 0; p < UPP; ++p) {
+      const int uu = ub + p * NW;
+      const int uc = uu < total ? uu : total - 1;
+      const int d = uc / I;
+      const uint8_t* base = reinterpret_cast<const uint8_t*>(a.blob[d]) + static_cast<size_t>(uc - d * I) * unit_bytes;
+#pragma unroll
+      for (int q = 0; q < NQ; ++q) {
+        const int blk = (FULLQ || lane + 64 * q < nblk) ? lane + 64 * q : 0;
+        cg[p][q] = __builtin_nontemporal_load(SPP_GLOBAL(u32x4, base + 16 * blk));
+        cu[p][q] = __builtin_nontemporal_load(SPP_GLOBAL(u32x4, base + cb + 16 * blk));
+        cd[p][q] = __builtin_nontemporal_load(SPP_GLOBAL(u32x4, base + 2 * cb + 16 * blk));
+        sg[p][q] = *SPP_GLOBAL(uint16_t, base + 3 * cb + 2 * blk);
+        su[p][q] = *SPP_GLOBAL(uint16_t, base + 3 * cb + sb + 2 * blk);
+        sd[p][q] = *SPP_GLOBAL(uint16_t, base + 3 * cb + 2 * sb + 2 * blk);
+      }
+    }
+#pragma unroll
+    for (int p = 0; p < UPP; ++p)
+#pragma unroll
+      for (int q = 0; q < NQ; ++q)
+        z ^= cg[p][q].x ^ cu[p][q].y ^ cd[p][q].z ^ cg[p][q].w ^ (static_cast<uint32_t>(sg[p][q] ^ su[p][q] ^ sd[p][q]) << 7);
+  }
+  z = __builtin_amdgcn_readfirstlane(z) ^ __builtin_amdgcn_readlane(z, 63);
+  if (threadIdx.x == 0) sink[blockIdx.x] = z;
+}
+
 // y = sum of the workgroup partials (fixed order), h_out = round(residual + y).
 // 1024 threads cover 64 outputs: 16 groups split the partials (8 loads in
 // flight per thread), then the groups are added in order.
@@ -2134,9 +2182,32 @@ int ffn_grid_q4_sweep(int nunits, int* rounds, int* upp) {
   return 0;
 }
 
+template <int NQ, bool FULLQ>
+hipError_t read_probe_q4_t(const FfnArgs& a, int grid, uint32_t* sink, hipStream_t st, hipEvent_t start,
+                           hipEvent_t stop) {
+  if (a.rounds == 1)
+    hipExtLaunchKernelGGL((read_probe_q4_kernel<NQ, FULLQ, 1>), dim3(grid), dim3(kFfnThreads), 0, st, start, stop, 0u,
+                          a, sink);
+  else
+    hipExtLaunchKernelGGL((read_probe_q4_kernel<NQ, FULLQ, 2>), dim3(grid), dim3(kFfnThreads), 0, st, start, stop, 0u,
+                          a, sink);
+  return hipGetLastError();
+}
+
 hipError_t launch_read_probe(const FfnArgs& a, int grid, uint32_t* sink, hipStream_t st, hipEvent_t start,
                              hipEvent_t stop) {
   if (a.nW <= 0 || a.nW > kMaxWork || grid <= 0 || a.rounds < 1 || a.rounds > 3 || !sink) return hipErrorInvalidValue;
+  if (a.codec == 1) {
+    // the sweep-order 4-bit FFN's loads: 3 units per wave and pass, 1 or 2 passes
+    if (a.rounds > 2 || a.upp != 3 || a.D % 256 != 0 || a.D > 4096 ||
+        static_cast<long>(grid) * kFfnWaves * 3 * a.rounds < static_cast<long>(a.nW) * a.I)
+      return hipErrorInvalidValue;
+    const int nblk = a.D / 32;
+    if (nblk == 64) return read_probe_q4_t<1, true>(a, grid, sink, st, start, stop);
+    if (nblk < 64) return read_probe_q4_t<1, false>(a, grid, sink, st, start, stop);
+    if (nblk == 128) return read_probe_q4_t<2, true>(a, grid, sink, st, start, stop);
+    return read_probe_q4_t<2, false>(a, grid, sink, st, start, stop);
+  }
   if (static_cast<long>(grid) * kSlWaves * a.rounds < static_cast<long>(a.nW) * a.I) return hipErrorInvalidValue;
   const int nchl = nch_for<uint16_t>(a.D);
   if (a.rounds > 1 && nchl > 4) return hipErrorInvalidValue;

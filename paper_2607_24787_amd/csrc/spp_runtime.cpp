@@ -1549,14 +1549,16 @@ spp_status spp_probe_read_ceiling(spp_ctx* c, int32_t reps, double* us_out, doub
   if (spp_status s = check_ctx(c)) return s;
   const spp_model_desc& d = c->d;
   if (reps < 1 || reps > 10000) return fail(SPP_EINVAL, "reps must be in [1, 10000]");
-  if (d.dtype != SPP_DTYPE_BF16 || c->grouped || d.expert_codec != SPP_CODEC_PLAIN)
-    return fail(SPP_ESTATE, "the read probe needs bf16 experts in the batch-1 unit layout");
+  if (d.dtype != SPP_DTYPE_BF16 || c->grouped)
+    return fail(SPP_ESTATE, "the read probe needs bf16 or 4-bit experts in the batch-1 unit layout");
   spp::FfnArgs fa{};
   fa.nW = d.K;
   fa.I = d.I;
   fa.D = d.D;
-  const int grid = spp::ffn_grid_slices(d.K * d.I, d.D, d.dtype, c->ffn_wgs, &fa.rounds);
-  if (grid <= 0) return fail(SPP_ESTATE, "the batch-1 FFN of this shape does not use the sweep-round kernel");
+  fa.codec = d.expert_codec == SPP_CODEC_Q4 ? 1 : 0;
+  const int grid = fa.codec ? spp::ffn_grid_q4_sweep(d.K * d.I, &fa.rounds, &fa.upp)
+                            : spp::ffn_grid_slices(d.K * d.I, d.D, d.dtype, c->ffn_wgs, &fa.rounds);
+  if (grid <= 0) return fail(SPP_ESTATE, "the batch-1 FFN of this shape does not run in sweep order");
   if (spp_status e = sync_all(c)) return e;
   hipEvent_t e0, e1;
   SPP_HIP(hipEventCreate(&e0));

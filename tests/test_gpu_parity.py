@@ -505,3 +505,29 @@ def test_run_statistics_match_the_oracle(torch_cuda, cfg, M_max):
         pytest.approx(rs.exposed_us, rel=1e-6, abs=1e-3)
     assert rs.shared_calls <= rs.layer_calls
     assert rs.ready_on_time + rs.waited == sum(len(set(np.asarray(s.T).ravel().tolist())) for s in ref.steps)
+
+
+@pytest.mark.parametrize("cfg", [RAGGED, Q4_SMALL, w.get("c1q4").with_(L=2, tokens=2)],
+                         ids=["bf16_ragged", "q4_small", "q4_qwen"])
+def test_read_ceiling_probe(torch_cuda, cfg):
+    """spp_probe_read_ceiling runs the loads of the context's sweep-order FFN
+    (bf16 rows, or 4-bit codes and scales) and reports a positive time and the
+    K blobs per launch over it; a context with fp32 experts is refused; the
+    context decodes as before afterwards."""
+    from paper_2607_24787_amd import spp
+    st = _stack(cfg)
+    try:
+        us, gbs = spp.spp_probe_read_ceiling(st.ctx, 4)
+        assert np.isfinite(us) and us > 0
+        assert gbs == pytest.approx(cfg.K * cfg.blob_bytes / (us * 1e3), rel=1e-9)
+        topk, _, _ = st.layer(0, 0, 1, 1)
+        assert topk.shape == (1, cfg.K)
+    finally:
+        st.close()
+    st = _stack(w.get("c0"))
+    try:
+        with pytest.raises(spp.SppError) as e:
+            spp.spp_probe_read_ceiling(st.ctx, 4)
+        assert e.value.status == spp.SPP_ESTATE
+    finally:
+        st.close()
