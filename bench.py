@@ -416,7 +416,7 @@ def main():
 
     # what the batch-1 FFN's own access pattern streams without its arithmetic
     read_probe = None
-    if spp.spp_blob_layout(stack.desc) == spp.LAYOUT_UNITS and cfg.dtype == "bf16":
+    if spp.spp_blob_layout(stack.desc) in (spp.LAYOUT_UNITS, spp.LAYOUT_Q4_UNITS) and cfg.dtype == "bf16":
         probe_us, probe_gbs = spp.spp_probe_read_ceiling(stack.ctx, 40)
         read_probe = {"us_per_launch": probe_us, "gbs": probe_gbs, "frac_of_peak": probe_gbs / HBM_PEAK_GBS}
         _log(f"[bench] read probe (FFN loads, no arithmetic): {probe_us:.2f} us per launch, {probe_gbs:.0f} GB/s")
