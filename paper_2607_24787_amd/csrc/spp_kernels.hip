@@ -740,6 +740,148 @@ __global__ __launch_bounds__(kThreads) void router_select_kernel(RouterArgs a) {
   if (tid == 0) __hip_atomic_store(a.counter, 0u, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
 }
 
+// Selection for B > 1 tokens with one wave per token (bf16, n <= 64 EPL,
+// K <= 64, r <= 64 and a multiple of 8): lane l holds experts l + 64 q.  Top-K
+// by K rounds of a wave maximum over the 32-bit logit order (the lowest index
+// taking a tie), the gates, and the adapter distribution from B's rows of the
+// lane's experts in registers -- the products, maxima and sums of
+// router_select_kernel in the same order, so the same bits -- then, as there,
+// the token's distribution replaces its logits in zbuf, and the last token's
+// wave sums the distributions over the tokens in token order.
+template <int EPL>
+__global__ __launch_bounds__(64) void router_select_wave_kernel(RouterArgs a) {
+  using T = uint16_t;
+  constexpr int kBC = 8;
+  const int lane = threadIdx.x;
+  const int n = a.n, r = a.r, ldz = a.n + a.r;
+  const int na = a.A ? r : 0;
+  const int b = blockIdx.x;
+  float* zrow = a.zbuf + static_cast<size_t>(b) * ldz;  // written by the rows launch
+  uint4 rbf[EPL][kBC];
+  if (na) {
+    const int rc = r / 8;
+#pragma unroll
+    for (int q = 0; q < EPL; ++q) {
+      const int e = lane + 64 * q;
+#pragma unroll
+      for (int c = 0; c < kBC; ++c) {
+        const bool ok = e < n && c < rc;
+        const uint4 v = ld16(static_cast<const uint8_t*>(a.Bm) + (ok ? (static_cast<size_t>(e) * r + 8 * c) * 2 : 0));
+        rbf[q][c] = ok ? v : make_uint4(0, 0, 0, 0);
+      }
+    }
+  }
+  uint32_t u[EPL];
+  bool av[EPL];
+#pragma unroll
+  for (int q = 0; q < EPL; ++q) {
+    const int e = lane + 64 * q;
+    av[q] = e < n;
+    u[q] = logit_order(zrow[min(e, n - 1)]);
+  }
+  const float hid = lane < na ? zrow[n + lane] : 0.f;
+  float zsel = 0.f, gk = 0.f;
+  int isel = 0;
+  if (a.router_on) {
+    for (int k = 0; k < a.K; ++k) {
+      uint32_t c = 0;
+#pragma unroll
+      for (int q = 0; q < EPL; ++q) c = max(c, av[q] ? u[q] : 0u);
+      const uint32_t m = wave_max_u32(c);
+      int e = -1;
+#pragma unroll
+      for (int q = 0; q < EPL; ++q) {
+        const uint64_t hit = __ballot(av[q] && u[q] == m);
+        if (e < 0 && hit) e = 64 * q + __builtin_ctzll(hit);
+      }
+      if (lane == (e & 63)) {
+#pragma unroll
+        for (int q = 0; q < EPL; ++q)
+          if (q == (e >> 6)) av[q] = false;
+      }
+      if (lane == k) {
+        zsel = order_logit(m);
+        isel = e;
+      }
+    }
+    const bool on = lane < a.K;
+    const float m0 = lane_value(zsel, 0);
+    const float v = on ? expf(zsel - m0) : 0.f;
+    const float sum = wave_sum(v);
+    if (on) {
+      gk = v / sum;
+      a.topk[b * a.K + lane] = isel;
+      a.gates[b * a.K + lane] = gk;
+    }
+  }
+  auto records = [&]() {
+    if (a.router_on && a.route_rec && lane < a.K) {
+      st_record(a.route_rec + b * a.K + lane, a.seq, static_cast<uint32_t>(isel));
+      st_record(a.gate_rec + b * a.K + lane, a.seq, __float_as_uint(gk));
+    }
+  };
+  if (!na) {
+    records();
+    return;
+  }
+  // adapter distribution pi_hat = softmax(B a) of this token
+  float zh[EPL];
+  float mx = -INFINITY;
+#pragma unroll
+  for (int q = 0; q < EPL; ++q) {
+    float acc = 0.f;
+#pragma unroll
+    for (int c = 0; c < kBC; ++c) {
+      float f[8];
+      unpack<T>(rbf[q][c], f);
+#pragma unroll
+      for (int v = 0; v < 8; ++v) acc += f[v] * lane_value(hid, 8 * c + v);
+    }
+    zh[q] = lane + 64 * q < n ? acc : -INFINITY;
+    mx = fmaxf(mx, zh[q]);
+  }
+  mx = wave_max(mx);
+  float pi[EPL];
+  float sum = 0.f;
+#pragma unroll
+  for (int q = 0; q < EPL; ++q) {
+    pi[q] = lane + 64 * q < n ? expf(zh[q] - mx) : 0.f;
+    sum = q == 0 ? wave_sum(pi[q]) : sum + wave_sum(pi[q]);
+  }
+#pragma unroll
+  for (int q = 0; q < EPL; ++q) {
+    const int e = lane + 64 * q;
+    if (e < n) st_agent(zrow + e, pi[q] / sum);
+  }
+  wait_own_stores();  // release this token's distribution
+  unsigned prev = 0;
+  if (lane == 0) prev = __hip_atomic_fetch_add(a.counter, 1u, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
+  prev = static_cast<unsigned>(__builtin_amdgcn_readfirstlane(static_cast<int>(prev)));
+  records();  // the host records go out after the release: nothing waits for them
+  if (prev != gridDim.x - 1) return;
+  // s = sum over the tokens, in token order, of their distributions
+  constexpr int kTB = 64;
+#pragma unroll
+  for (int q = 0; q < EPL; ++q) {
+    const int e = lane + 64 * q;
+    const int ec = min(e, n - 1);
+    float acc = 0.f;
+    for (int b0 = 0; b0 < a.B; b0 += kTB) {
+      float v[kTB];
+#pragma unroll
+      for (int t = 0; t < kTB; ++t) v[t] = ld_agent(a.zbuf + static_cast<size_t>(min(b0 + t, a.B - 1)) * ldz + ec);
+#pragma unroll
+      for (int t = 0; t < kTB; ++t)
+        if (b0 + t < a.B) acc += v[t];
+    }
+    if (e < n) {
+      a.s[e] = acc;
+      if (a.s_rec) st_record(a.s_rec + e, a.seq, __float_as_uint(acc));
+    }
+  }
+  if (lane == 0) __hip_atomic_store(a.counter, 0u, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
+}
+
 // ---------------------------------------------------------------------------
 // Routed-expert SwiGLU FFN, one pass over the expert blobs.  The work is the
 // flat list of (expert, unit i) pairs; unit i of an expert is the contiguous
@@ -1961,7 +2103,14 @@ hipError_t router_tf(const RouterArgs& a, hipStream_t st) {
     hipLaunchKernelGGL((router_rows_mfma_kernel<T, false>), g2, dim3(64 * kRowWaves), 0, st, a);
   hipError_t e = hipGetLastError();
   if (e != hipSuccess) return e;
-  hipLaunchKernelGGL((router_select_kernel<T>), dim3(a.B), dim3(kThreads), 0, st, a);
+  // one wave per token where the shapes allow it (as the batch-1 one-wave tails)
+  const bool wave1 = sizeof(T) == 2 && a.n <= 128 && a.K <= 64 && (!a.A || (a.r <= 64 && a.r % 8 == 0));
+  if (wave1 && a.n <= 64)
+    hipLaunchKernelGGL((router_select_wave_kernel<1>), dim3(a.B), dim3(64), 0, st, a);
+  else if (wave1)
+    hipLaunchKernelGGL((router_select_wave_kernel<2>), dim3(a.B), dim3(64), 0, st, a);
+  else
+    hipLaunchKernelGGL((router_select_kernel<T>), dim3(a.B), dim3(kThreads), 0, st, a);
   return hipGetLastError();
 }
 
