@@ -26,6 +26,8 @@ struct RouterArgs {
   const void* Bm;       // [n, r]
   float* x_out;         // [B, D] router input written by block 0 (nullptr: skip)
   float* zbuf;          // [B, n + r] logits then adapter hidden units
+  uint64_t* ztag;       // [n + r] the same values tagged (seq << 32) | fp32 bits, for the batch-1
+                        // single-wave tails (polled instead of a completion counter), or nullptr
   int32_t* topk;        // [B, K]
   float* gates;         // [B, K]
   float* s;             // [n]

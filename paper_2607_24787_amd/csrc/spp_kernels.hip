@@ -247,6 +247,39 @@ __device__ __forceinline__ void st_record(uint64_t* p, unsigned seq, uint32_t pa
   __hip_atomic_store(p, (static_cast<uint64_t>(seq) << 32) | payload, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_SYSTEM);
 }
 
+// The same tagging between the workgroups of one launch (device memory,
+// agent scope): a value whose high half is this launch's seq is this launch's,
+// so a reader polls for it instead of waiting on a completion counter, which
+// costs the writer a wait for its own store and then an atomic round trip.
+__device__ __forceinline__ void st_tag(uint64_t* p, unsigned seq, float v) {
+  __hip_atomic_store(p, (static_cast<uint64_t>(seq) << 32) | __float_as_uint(v), __ATOMIC_RELAXED,
+                     __HIP_MEMORY_SCOPE_AGENT);
+}
+
+// Bound on the polls of one wait (each at least one device-memory round trip,
+// so about a second): every workgroup of a launch this small is resident at
+// once, so the bound is only reached if the launch cannot make progress.
+constexpr unsigned kPollMax = 1u << 20;
+
+// Lane l's values p[l + 64 q] (q < Q; indices >= cnt are not waited for) once
+// every one carries seq; false if the bound ran out first.
+template <int Q>
+__device__ __forceinline__ bool poll_tags(const uint64_t* p, int cnt, int lane, unsigned seq, float* v) {
+  for (unsigned it = 0; it < kPollMax; ++it) {
+    bool ok = true;
+#pragma unroll
+    for (int q = 0; q < Q; ++q) {
+      const int i = lane + 64 * q;
+      const uint64_t t = __hip_atomic_load(p + min(i, cnt - 1), __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
+      v[q] = __uint_as_float(static_cast<uint32_t>(t));
+      ok = ok && (i >= cnt || static_cast<uint32_t>(t >> 32) == seq);
+    }
+    if (__all(ok)) return true;
+    __builtin_amdgcn_s_sleep(1);
+  }
+  return false;
+}
+
 // Token b's host records from wave 0 after select_topk (lane k < K: expert
 // s_isel[k], gate s_zsel[k]).
 __device__ __forceinline__ void route_records(const RouterArgs& a, int b, int tid, const float* s_zsel,
@@ -426,11 +459,16 @@ struct BStage {
 // the tails run in wave 0 alone, with no barrier -- lane l holds experts
 // l + 64 q (q < EPL).  Top-K: K rounds of a wave maximum over the 32-bit
 // order of the available logits, the lowest index taking a tie (the same
-// order as topk_key).  Adapter: wave 0 of every adapter workgroup holds B's
-// rows of its lanes' experts in registers; the hidden unit a_j is broadcast
-// from lane j.  Both give the bits of the general tails: the same products in
-// the same order, and the distribution's sum as the sum of the per-64-expert
-// wave sums in expert order.
+// order as topk_key).  Adapter: the tail wave holds B's rows of its lanes'
+// experts in registers; the hidden unit a_j is broadcast from lane j.  Both
+// give the bits of the general tails: the same products in the same order, and
+// the distribution's sum as the sum of the per-64-expert wave sums in expert
+// order.  With a tag buffer (a.ztag) every row's value is also stored tagged
+// with the launch's seq, and wave 0 of the first workgroup of each kind takes
+// that kind's tail as soon as its poll sees every value tagged: the writers
+// neither wait for their stores nor pass a counter (1.0 us less per launch
+// than the last-arriver handoff, same outputs).  Without one (a caller with no
+// sequence numbers), the last workgroup through the counter takes it.
 // ---------------------------------------------------------------------------
 template <typename T, int NCH, bool FULL, int EPL>
 __global__ __launch_bounds__(kThreads) void router_adapter_kernel(RouterArgs a) {
@@ -465,8 +503,8 @@ __global__ __launch_bounds__(kThreads) void router_adapter_kernel(RouterArgs a) 
   uint4 rbf[EPL ? EPL : 1][kBC];
   if (EPL == 0) {
     bst.load(a, tid, adapter_wg && staged);
-  } else if (adapter_wg && wave == 0) {
-    // B rows of this lane's experts (a chunk past r, or a row past n, re-reads
+  } else if (adapter_wg && wave == 0 && (!a.ztag || static_cast<int>(blockIdx.x) == gr)) {
+    // B rows of this lane's experts (in the workgroup that may take the tail) (a chunk past r, or a row past n, re-reads
     // the first chunk of B and is dropped)
     const int rc = r / 8;
 #pragma unroll
@@ -494,7 +532,9 @@ __global__ __launch_bounds__(kThreads) void router_adapter_kernel(RouterArgs a) 
 #pragma unroll
       for (int v = 0; v < V; ++v) xv[j][v] *= inv;
   }
-  if (blockIdx.x == 0 && wave == 0 && a.x_out) {
+  // x goes out from the last wave of the last workgroup: never a tail wave,
+  // whose first wait would otherwise include these stores
+  if (blockIdx.x == gridDim.x - 1 && wave == kWaves - 1 && a.x_out) {
 #pragma unroll
     for (int j = 0; j < NCH; ++j) {
       const int c = lane + 64 * j;
@@ -515,28 +555,48 @@ __global__ __launch_bounds__(kThreads) void router_adapter_kernel(RouterArgs a) 
       for (int v = 0; v < V; ++v) acc += wf[v] * xv[j][v];
     }
     acc = wave_sum(acc);
-    if (lane == 0) st_agent(a.zbuf + zcol, acc);
+    if (lane == 0) {
+      st_agent(a.zbuf + zcol, acc);
+      if (EPL && a.ztag) st_tag(a.ztag + zcol, a.seq, acc);
+    }
   }
 
-  wait_own_stores();  // release this wave's value
-  __syncthreads();
   const int kind = adapter_wg ? 1 : 0;
   const unsigned total = adapter_wg ? gridDim.x - gr : gr;
   if (EPL) {
-    if (wave != 0) return;
-    unsigned prev = 0;
-    if (lane == 0) prev = __hip_atomic_fetch_add(a.counter + kind, 1u, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
-    prev = static_cast<unsigned>(__builtin_amdgcn_readfirstlane(static_cast<int>(prev)));
-    if (prev != total - 1) return;
+    constexpr int Q = EPL ? EPL : 1;
+    // Handoff.  Tagged values: wave 0 of its kind's first workgroup polls
+    // them.  Otherwise the last workgroup to pass the completion counter
+    // takes the tail (after releasing its own values), and resets it.
+    float zv[Q];
+    if (a.ztag) {
+      if (wave != 0 || static_cast<int>(blockIdx.x) != (adapter_wg ? gr : 0)) return;
+      // a poll that runs out leaves this launch's records unwritten: the host reports it
+      if (!(adapter_wg ? poll_tags<1>(a.ztag + n, na, lane, a.seq, zv) : poll_tags<Q>(a.ztag, n, lane, a.seq, zv)))
+        return;
+    } else {
+      wait_own_stores();  // release this wave's value
+      __syncthreads();
+      if (wave != 0) return;
+      unsigned prev = 0;
+      if (lane == 0) prev = __hip_atomic_fetch_add(a.counter + kind, 1u, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
+      prev = static_cast<unsigned>(__builtin_amdgcn_readfirstlane(static_cast<int>(prev)));
+      if (prev != total - 1) return;
+      if (lane == 0) __hip_atomic_store(a.counter + kind, 0u, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
+      if (adapter_wg) {
+        zv[0] = ld_agent(a.zbuf + n + min(lane, na - 1));
+      } else {
+#pragma unroll
+        for (int q = 0; q < Q; ++q) zv[q] = ld_agent(a.zbuf + min(lane + 64 * q, n - 1));
+      }
+    }
     if (!adapter_wg) {
-      constexpr int Q = EPL ? EPL : 1;
       uint32_t u[Q];
       bool av[Q];
 #pragma unroll
       for (int q = 0; q < Q; ++q) {
-        const int e = lane + 64 * q;
-        av[q] = e < n;
-        u[q] = logit_order(ld_agent(a.zbuf + min(e, n - 1)));
+        av[q] = lane + 64 * q < n;
+        u[q] = logit_order(zv[q]);
       }
       float zsel = 0.f;
       int isel = 0;
@@ -565,7 +625,6 @@ __global__ __launch_bounds__(kThreads) void router_adapter_kernel(RouterArgs a) 
       const float m0 = lane_value(zsel, 0);
       const float v = on ? expf(zsel - m0) : 0.f;
       const float sum = wave_sum(v);
-      if (lane == 0) __hip_atomic_store(a.counter, 0u, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
       if (on) {
         const float gk = v / sum;
         a.topk[lane] = isel;
@@ -578,8 +637,7 @@ __global__ __launch_bounds__(kThreads) void router_adapter_kernel(RouterArgs a) 
       return;
     }
     // adapter distribution pi_hat = softmax(B a)
-    constexpr int Q = EPL ? EPL : 1;
-    const float av = lane < na ? ld_agent(a.zbuf + n + lane) : 0.f;
+    const float av = lane < na ? zv[0] : 0.f;
     float zh[Q];
     float mx = -INFINITY;
 #pragma unroll
@@ -603,7 +661,6 @@ __global__ __launch_bounds__(kThreads) void router_adapter_kernel(RouterArgs a) 
       pi[q] = lane + 64 * q < n ? expf(zh[q] - mx) : 0.f;
       sum = q == 0 ? wave_sum(pi[q]) : sum + wave_sum(pi[q]);
     }
-    if (lane == 0) __hip_atomic_store(a.counter + 1, 0u, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
 #pragma unroll
     for (int q = 0; q < Q; ++q) {
       const int e = lane + 64 * q;
@@ -615,6 +672,8 @@ __global__ __launch_bounds__(kThreads) void router_adapter_kernel(RouterArgs a) 
     }
     return;
   }
+  wait_own_stores();  // release this wave's value
+  __syncthreads();
   if (tid == 0) {
     const unsigned prev = __hip_atomic_fetch_add(a.counter + kind, 1u, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
     s_last = (prev == total - 1);

@@ -100,6 +100,7 @@ struct spp_ctx {
   float* u_dev = nullptr;      // [maxB, D] prologue output
   float* x_dev = nullptr;      // [maxB, D] router input
   float* zbuf = nullptr;       // [maxB, n + r]
+  uint64_t* ztag = nullptr;    // [n + r] batch-1 router values tagged with their launch's seq (zero: none yet)
   uint8_t* res_dev = nullptr;  // topk [maxB*K] i32 | gates [maxB*K] f32 | s [n] f32
   size_t res_bytes = 0, off_gates = 0, off_s = 0;
   // host records written by the router kernels (pinned, host-mapped):
@@ -497,8 +498,8 @@ void free_ctx(spp_ctx* c) {
   for (hipEvent_t e : c->pf_done)
     if (e) (void)hipEventDestroy(e);
   for (void* p : {static_cast<void*>(c->u_dev), static_cast<void*>(c->x_dev), static_cast<void*>(c->zbuf),
-                  static_cast<void*>(c->res_dev), static_cast<void*>(c->counter), static_cast<void*>(c->partial),
-                  static_cast<void*>(c->probe_dev)})
+                  static_cast<void*>(c->ztag), static_cast<void*>(c->res_dev), static_cast<void*>(c->counter),
+                  static_cast<void*>(c->partial), static_cast<void*>(c->probe_dev)})
     if (p) (void)hipFree(p);
   if (c->rec_host) (void)hipHostFree(c->rec_host);
   if (c->groups_host) (void)hipHostFree(c->groups_host);
@@ -554,6 +555,7 @@ spp_status create_impl(const spp_model_desc* desc, void* stream, spp_ctx** out) 
   if (hipMalloc(&c->u_dev, BD * sizeof(float)) != hipSuccess ||
       hipMalloc(&c->x_dev, BD * sizeof(float)) != hipSuccess ||
       hipMalloc(&c->zbuf, static_cast<size_t>(d.max_batch) * (d.n + d.r) * sizeof(float)) != hipSuccess ||
+      hipMalloc(&c->ztag, static_cast<size_t>(d.n + d.r) * sizeof(uint64_t)) != hipSuccess ||
       hipMalloc(&c->partial, spp::ffn_max_grid() * d.D * sizeof(float)) != hipSuccess ||
       hipMalloc(&c->counter, 256) != hipSuccess)
     return fail(SPP_ENOMEM, "scratch allocation failed");
@@ -584,6 +586,7 @@ spp_status create_impl(const spp_model_desc* desc, void* stream, spp_ctx** out) 
     SPP_HIP(hipHostGetDevicePointer(reinterpret_cast<void**>(&c->groups_dev), c->groups_host, 0));
   }
   SPP_HIP(hipMemset(c->counter, 0, 256));
+  SPP_HIP(hipMemset(c->ztag, 0, static_cast<size_t>(d.n + d.r) * sizeof(uint64_t)));  // seq 0 is never handed out
   SPP_HIP(hipMemset(c->res_dev, 0, c->res_bytes));
   c->last_s.assign(d.n, 0.f);
   SPP_HIP(hipDeviceSynchronize());
@@ -901,6 +904,7 @@ spp_status layer_forward_impl(spp_ctx* c, int32_t l, const void* h_in, void* h_o
   ra.Bm = ls.Bm;
   ra.x_out = c->x_dev;
   ra.zbuf = c->zbuf;
+  ra.ztag = c->ztag;
   ra.topk = topk_dev;
   ra.gates = gates_dev;
   ra.s = s_dev;
@@ -1356,6 +1360,7 @@ spp_status adapter_predict(spp_ctx* c, int32_t l, const float* x_dev, int32_t B,
   ra.A = ls.A;
   ra.Bm = ls.Bm;
   ra.zbuf = c->zbuf;
+  ra.ztag = c->ztag;
   ra.s = reinterpret_cast<float*>(c->res_dev + c->off_s);
   ra.counter = c->counter;
   ra.B = B;
