@@ -464,7 +464,7 @@ struct BStage {
 // give the bits of the general tails: the same products in the same order, and
 // the distribution's sum as the sum of the per-64-expert wave sums in expert
 // order.  With a tag buffer (a.ztag) every row's value is also stored tagged
-// with the launch's seq, and wave 0 of the first workgroup of each kind takes
+// with the launch's seq, and wave 0 of the last workgroup of each kind takes
 // that kind's tail as soon as its poll sees every value tagged: the writers
 // neither wait for their stores nor pass a counter (1.0 us less per launch
 // than the last-arriver handoff, same outputs).  Without one (a caller with no
@@ -503,7 +503,7 @@ __global__ __launch_bounds__(kThreads) void router_adapter_kernel(RouterArgs a) 
   uint4 rbf[EPL ? EPL : 1][kBC];
   if (EPL == 0) {
     bst.load(a, tid, adapter_wg && staged);
-  } else if (adapter_wg && wave == 0 && (!a.ztag || static_cast<int>(blockIdx.x) == gr)) {
+  } else if (adapter_wg && wave == 0 && (!a.ztag || blockIdx.x == gridDim.x - 1)) {
     // B rows of this lane's experts (in the workgroup that may take the tail) (a chunk past r, or a row past n, re-reads
     // the first chunk of B and is dropped)
     const int rc = r / 8;
@@ -565,12 +565,13 @@ __global__ __launch_bounds__(kThreads) void router_adapter_kernel(RouterArgs a) 
   const unsigned total = adapter_wg ? gridDim.x - gr : gr;
   if (EPL) {
     constexpr int Q = EPL ? EPL : 1;
-    // Handoff.  Tagged values: wave 0 of its kind's first workgroup polls
-    // them.  Otherwise the last workgroup to pass the completion counter
-    // takes the tail (after releasing its own values), and resets it.
+    // Handoff.  Tagged values: wave 0 of its kind's last workgroup polls
+    // them (it waits only for workgroups dispatched before it).  Otherwise
+    // the last workgroup to pass the completion counter takes the tail
+    // (after releasing its own values), and resets it.
     float zv[Q];
     if (a.ztag) {
-      if (wave != 0 || static_cast<int>(blockIdx.x) != (adapter_wg ? gr : 0)) return;
+      if (wave != 0 || static_cast<int>(blockIdx.x) != (adapter_wg ? static_cast<int>(gridDim.x) : gr) - 1) return;
       // a poll that runs out leaves this launch's records unwritten: the host reports it
       if (!(adapter_wg ? poll_tags<1>(a.ztag + n, na, lane, a.seq, zv) : poll_tags<Q>(a.ztag, n, lane, a.seq, zv)))
         return;
@@ -1998,69 +1999,76 @@ __global__ __launch_bounds__(64 * kRowWaves) void router_rows_mfma_kernel(Router
 // their products are exact on the bf16 MFMA; the normalisation moves to the
 // epilogue,
 //   u[b][o] = h[b][o] + (sum_i P[o][i] h[b][i]) / sqrt(mean_i h[b][i]^2 + eps),
-// with sum_i h[b][i]^2 accumulated from the same loads.  One workgroup per 16
-// output rows x 16 tokens; its 4 waves split D in 256-column chunks (wave w
-// takes chunks w, w+4, ..., two chunks' loads in flight per pass), each with
-// a 16x16 accumulator and its tokens' partial sums of squares, added in wave
-// order through LDS.  (One workgroup per 16 rows x 64 tokens reads P once but
-// measured slower: fewer workgroups keep fewer loads in flight.)  Token rows
-// past B read the last token and are not stored.
-constexpr int kProjWaves = 4;
+// with sum_i h[b][i]^2 accumulated from the same loads.  One workgroup per
+// kProjRB x 16 output rows x 16 tokens; its 8 waves split D in 256-column
+// chunks (wave w takes chunks w, w+8, ...), each loading the chunk's h pieces
+// once for its kProjRB 16x16 accumulators, and its tokens' partial sums of
+// squares; the partials are added in wave order through LDS.  The kernel is
+// bound by the operand traffic from L2 (h is re-read by every row block, P by
+// every token block): measured as loads alone at B = 64, D = 2048, 16 rows
+// per workgroup of 4 waves (the earlier design) took 8.3 us by events and 2
+// row blocks per workgroup of 8 waves 6.3 us; 4 token or row blocks per
+// workgroup were slower again (fewer workgroups).  Token rows past B read the
+// last token and are not stored.
+constexpr int kProjWaves = 8;
+constexpr int kProjRB = 2;  // 16-row blocks of P per workgroup (D a multiple of 256)
 __global__ __launch_bounds__(64 * kProjWaves) void proj_mfma_kernel(ProjArgs a) {
-  __shared__ f32x4 s_acc[kProjWaves][64];
+  __shared__ f32x4 s_acc[kProjWaves][kProjRB][64];
   __shared__ float s_ss[kProjWaves][16];
   const int lane = threadIdx.x & 63, wave = threadIdx.x >> 6;
-  const int o0 = blockIdx.x * 16, b0 = blockIdx.y * 16;
+  const int o0 = blockIdx.x * 16 * kProjRB, b0 = blockIdx.y * 16;
   const int D = a.D, nck = D / 256;
   const int krow = lane & 15, koff = 8 * (lane >> 4);
   const int tok = min(b0 + krow, a.B - 1);
   const uint16_t* hrow = reinterpret_cast<const uint16_t*>(a.h) + static_cast<size_t>(tok) * D + koff;
-  const uint16_t* prow = reinterpret_cast<const uint16_t*>(a.P) + static_cast<size_t>(o0 + krow) * D + koff;
-  f32x4 acc = f32x4{0.f, 0.f, 0.f, 0.f};
+  const uint16_t* prow[kProjRB];
+#pragma unroll
+  for (int r = 0; r < kProjRB; ++r)
+    prow[r] = reinterpret_cast<const uint16_t*>(a.P) + static_cast<size_t>(o0 + 16 * r + krow) * D + koff;
+  f32x4 acc[kProjRB];
+#pragma unroll
+  for (int r = 0; r < kProjRB; ++r) acc[r] = f32x4{0.f, 0.f, 0.f, 0.f};
   float ss = 0.f;
-  for (int c0 = wave; c0 < nck; c0 += 2 * kProjWaves) {
-    // chunks c0 and c0 + kProjWaves (the second clamped to a valid chunk, then dropped)
-    const int c1 = c0 + kProjWaves;
-    const bool has1 = c1 < nck;
-    const int k0 = 256 * c0, k1 = 256 * (has1 ? c1 : c0);
-    u32x4 ha[16], pb[16];
+  for (int c = wave; c < nck; c += kProjWaves) {
+    const int k0 = 256 * c;
+    u32x4 ha[8], pb[kProjRB][8];
 #pragma unroll
     for (int j = 0; j < 8; ++j) {
       ha[j] = *SPP_GLOBAL(u32x4, hrow + k0 + 32 * j);
-      pb[j] = __builtin_nontemporal_load(SPP_GLOBAL(u32x4, prow + k0 + 32 * j));
-      ha[8 + j] = *SPP_GLOBAL(u32x4, hrow + k1 + 32 * j);
-      pb[8 + j] = __builtin_nontemporal_load(SPP_GLOBAL(u32x4, prow + k1 + 32 * j));
+#pragma unroll
+      for (int r = 0; r < kProjRB; ++r) pb[r][j] = __builtin_nontemporal_load(SPP_GLOBAL(u32x4, prow[r] + k0 + 32 * j));
     }
     __builtin_amdgcn_sched_barrier(0);
-    const int nj = has1 ? 16 : 8;
 #pragma unroll
-    for (int j = 0; j < 16; ++j) {
-      if (j < nj) {
-        acc = __builtin_amdgcn_mfma_f32_16x16x32_bf16(__builtin_bit_cast(bf16x8, ha[j]),
-                                                      __builtin_bit_cast(bf16x8, pb[j]), acc, 0, 0, 0);
-        const uint32_t w[4] = {ha[j].x, ha[j].y, ha[j].z, ha[j].w};
+    for (int j = 0; j < 8; ++j) {
+      const bf16x8 hv = __builtin_bit_cast(bf16x8, ha[j]);
 #pragma unroll
-        for (int q = 0; q < 4; ++q) {
-          const float lo = __uint_as_float(w[q] << 16), hi = __uint_as_float(w[q] & 0xffff0000u);
-          ss += lo * lo + hi * hi;
-        }
+      for (int r = 0; r < kProjRB; ++r)
+        acc[r] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(hv, __builtin_bit_cast(bf16x8, pb[r][j]), acc[r], 0, 0, 0);
+      const uint32_t w[4] = {ha[j].x, ha[j].y, ha[j].z, ha[j].w};
+#pragma unroll
+      for (int q = 0; q < 4; ++q) {
+        const float lo = __uint_as_float(w[q] << 16), hi = __uint_as_float(w[q] & 0xffff0000u);
+        ss += lo * lo + hi * hi;
       }
     }
   }
   // lanes l, l+16, l+32, l+48 hold the k-slices of token b0 + l%16
   ss += __shfl_xor(ss, 16);
   ss += __shfl_xor(ss, 32);
-  s_acc[wave][lane] = acc;
+#pragma unroll
+  for (int r = 0; r < kProjRB; ++r) s_acc[wave][r][lane] = acc[r];
   if (lane < 16) s_ss[wave][lane] = ss;
   __syncthreads();
-  if (wave != 0) return;
-  acc = s_acc[0][lane];
+  if (wave >= kProjRB) return;
+  // wave r finishes row block r
+  f32x4 y = s_acc[0][wave][lane];
 #pragma unroll
   for (int w = 1; w < kProjWaves; ++w) {
-    const f32x4 v = s_acc[w][lane];
-    acc = f32x4{acc[0] + v[0], acc[1] + v[1], acc[2] + v[2], acc[3] + v[3]};
+    const f32x4 v = s_acc[w][wave][lane];
+    y = f32x4{y[0] + v[0], y[1] + v[1], y[2] + v[2], y[3] + v[3]};
   }
-  // this lane holds tokens 4*(lane/16)+j of output row o0 + lane%16
+  // this lane holds tokens 4*(lane/16)+j of output row o0 + 16*wave + lane%16
 #pragma unroll
   for (int j = 0; j < 4; ++j) {
     const int t = 4 * (lane >> 4) + j;
@@ -2069,11 +2077,11 @@ __global__ __launch_bounds__(64 * kProjWaves) void proj_mfma_kernel(ProjArgs a) 
     for (int w = 1; w < kProjWaves; ++w) sst += s_ss[w][t];
     const int b = b0 + t;
     if (b < a.B) {
-      const int o = o0 + krow;
+      const int o = o0 + 16 * wave + krow;
       const float inv = 1.0f / sqrtf(sst / static_cast<float>(D) + a.eps);
       const size_t idx = static_cast<size_t>(b) * D + o;
       a.u[idx] = __uint_as_float(static_cast<uint32_t>(reinterpret_cast<const uint16_t*>(a.h)[idx]) << 16) +
-                 inv * acc[j];
+                 inv * y[j];
     }
   }
 }
@@ -2307,7 +2315,7 @@ hipError_t launch_combine(const CombineArgs& a, int dtype, hipStream_t st) {
 
 hipError_t launch_proj(const ProjArgs& a, int dtype, hipStream_t st) {
   if (dtype == 1 && a.B > 1 && a.D % 256 == 0) {
-    hipLaunchKernelGGL(proj_mfma_kernel, dim3(a.D / 16, (a.B + 15) / 16), dim3(64 * kProjWaves), 0, st, a);
+    hipLaunchKernelGGL(proj_mfma_kernel, dim3(a.D / (16 * kProjRB), (a.B + 15) / 16), dim3(64 * kProjWaves), 0, st, a);
     return hipGetLastError();
   }
   return dtype == 1 ? proj_t<uint16_t>(a, st) : proj_t<float>(a, st);
