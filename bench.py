@@ -126,6 +126,9 @@ def run_mode(stack, dev_h, row_bytes, warmup, steps, M_max, naive=False):
         "ffn_launches": rs.ffn_launches,
         "misses_per_step": rs.misses / steps,
         "prefetched_per_step": rs.prefetched / steps,
+        # m_l: prefetch copies issued per prediction, as fractions of the predictions
+        "prefetch_count_hist": ({str(m): rs.prefetch_hist[m] / sum(rs.prefetch_hist)
+                                 for m in range(17) if rs.prefetch_hist[m]} if sum(rs.prefetch_hist) else None),
         "prefetch_used_per_step": rs.prefetch_used / steps,
         "ready_on_time_frac": rs.ready_on_time / max(rs.hits + rs.misses, 1),
         "copy_bytes": rs.copy_bytes,

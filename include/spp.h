@@ -156,6 +156,11 @@ typedef struct {
   int64_t shared_calls;
   /* needed experts the FFN waited for (the layer calls' `waited`) */
   int64_t waited;
+  /* prefetch copies issued per prediction (m_l, section "Window-Aware
+   * Prefetch Budgeting"): prefetch_hist[m] counts the predictions (layer
+   * calls that predict layer l+1, M_max >= 0, and expert_cache_issue_prefetch
+   * calls) that issued m copies (m = 16 counts 16 or more) */
+  int64_t prefetch_hist[17];
 } spp_run_stats;
 
 /* ---------------------------------------------------------------- lifecycle */

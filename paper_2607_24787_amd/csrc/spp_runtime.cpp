@@ -1020,6 +1020,7 @@ spp_status layer_forward_impl(spp_ctx* c, int32_t l, const void* h_in, void* h_o
       for (const spp::Transfer& t : c->last_pref) nx->pending_prefetch.push_back(t.expert);
       st.prefetched = static_cast<int32_t>(c->last_pref.size());
     }
+    c->stats.prefetch_hist[std::min(st.prefetched, 16)] += 1;
   }
 
   // the batch-1 FFN's work list (routed experts in T order, then the shared ones)
@@ -1403,6 +1404,7 @@ spp_status expert_cache_issue_prefetch(spp_ctx* c, int32_t target_layer, const f
   }
   *m_out = static_cast<int32_t>(placed.size());
   c->stats.prefetched += *m_out;
+  c->stats.prefetch_hist[std::min(*m_out, 16)] += 1;
   return SPP_OK;
 }
 

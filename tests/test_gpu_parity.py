@@ -499,6 +499,12 @@ def test_run_statistics_match_the_oracle(torch_cuda, cfg, M_max):
     assert token_hits_target / (cfg.K * cfg.batch * cfg.tokens * (cfg.L - 1)) == \
         pytest.approx(ref.ready_recall, abs=1e-12)
     assert (rs.misses, rs.prefetched, rs.prefetch_used) == (ref.loads, ref.prefetched, ref.prefetch_used)
+    # m_l: the prefetches issued by each prediction
+    mhist = [0] * 17
+    for step in ref.steps:
+        if step.l < cfg.L - 1:
+            mhist[min(len(step.P), 16)] += 1
+    assert list(rs.prefetch_hist) == mhist
     # the exposed time splits into its three parts
     assert rs.exposed_load_us >= 0.0 and rs.exposed_shared_us >= 0.0 and rs.exposed_wait_us >= -1.0
     assert rs.exposed_load_us + rs.exposed_shared_us + rs.exposed_wait_us == \
