@@ -423,6 +423,12 @@ def main():
         probe_us, probe_gbs = spp.spp_probe_read_ceiling(stack.ctx, 40)
         read_probe = {"us_per_launch": probe_us, "gbs": probe_gbs, "frac_of_peak": probe_gbs / HBM_PEAK_GBS}
         _log(f"[bench] read probe (FFN loads, no arithmetic): {probe_us:.2f} us per launch, {probe_gbs:.0f} GB/s")
+    # the same byte count read as one contiguous stream: the chip's ceiling for it in one launch
+    stream_probe = None
+    if cfg.S >= cfg.K:
+        s_us, s_gbs = spp.spp_probe_stream_read(stack.ctx, 40)
+        stream_probe = {"us_per_launch": s_us, "gbs": s_gbs, "frac_of_peak": s_gbs / HBM_PEAK_GBS}
+        _log(f"[bench] stream probe (the same bytes, one contiguous read): {s_us:.2f} us per launch, {s_gbs:.0f} GB/s")
 
     on = run_mode(stack, dev_h, row_bytes, args.warmup, args.steps, cfg.window)
     _log(f"[bench] ON  {on['tokens_per_s']:.1f} tok/s coverage={on['next_layer_coverage']:.3f} "
@@ -540,7 +546,9 @@ def main():
                      "achieved": achieved, "peak": HBM_PEAK_GBS, "unit": "GB/s", "frac": achieved / HBM_PEAK_GBS,
                      "traffic": traffic, "bytes_per_launch": ffn_bytes, "avg_launch_us": on["ffn_kernel_us"],
                      "read_probe": read_probe,
-                     "frac_of_read_probe": achieved / read_probe["gbs"] if read_probe else None},
+                     "frac_of_read_probe": achieved / read_probe["gbs"] if read_probe else None,
+                     "stream_probe": stream_probe,
+                     "frac_of_stream_probe": achieved / stream_probe["gbs"] if stream_probe else None},
         "link": {"bound": "host link (pinned H2D)", "copy_engine": args.copy_engine,
                  "per_expert_us_prefetch_engine": per_expert_us, "peak_gbs_measured": link_gbs,
                  "per_expert_us_by_engine": engine_us,

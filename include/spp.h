@@ -390,6 +390,16 @@ spp_status spp_profile_expert_copy(spp_ctx* ctx, int32_t l, int32_t reps, double
  * 1..10000. */
 spp_status spp_probe_read_ceiling(spp_ctx* ctx, int32_t reps, double* us_out, double* gbs_out);
 
+/* Plain streaming read of the same byte count (measurement, not part of the
+ * hot path): K expert blobs' bytes read as one contiguous range of a layer's
+ * slot pool by a grid-stride kernel (2048 workgroups, 16-byte non-temporal
+ * loads, eight per lane in flight), the ranges rotating over every layer's
+ * pool; timed and averaged as spp_probe_read_ceiling.  us_out: average time
+ * per launch; gbs_out: the bytes read / that time.  Waits for all enqueued
+ * work first.  ESTATE if a layer has fewer than K slots; EINVAL for reps
+ * outside 1..10000. */
+spp_status spp_probe_stream_read(spp_ctx* ctx, int32_t reps, double* us_out, double* gbs_out);
+
 /* Where moe_layer_forward takes the priorities for the next layer's prefetch
  * (Table 5).  SPP_PREFETCH_ADAPTER (default): the layer's adapter, as above.
  * SPP_PREFETCH_PREV_TOKEN (Naive Prefetch): the experts layer l+1 activated

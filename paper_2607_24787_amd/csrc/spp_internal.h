@@ -144,6 +144,10 @@ int ffn_grid_q4_sweep(int nunits, int* rounds, int* upp);
 // The loads of a bf16 ffn_slices_kernel launch with the same arguments and
 // grid, and nothing else (a read-ceiling probe); one checksum word per
 // workgroup into sink [grid]; start/stop stamped with the kernel's own times.
+// Plain streaming read of `bytes` (a multiple of 16) from base (16-byte
+// aligned), timed by start/stop; sink takes at least 256 words.
+hipError_t launch_stream_probe(const void* base, size_t bytes, uint32_t* sink, hipStream_t st, hipEvent_t start,
+                               hipEvent_t stop);
 hipError_t launch_read_probe(const FfnArgs& a, int grid, uint32_t* sink, hipStream_t st, hipEvent_t start,
                              hipEvent_t stop);
 // 4-bit experts: whole passes of kFfnWaves * upp units per workgroup (upp 3

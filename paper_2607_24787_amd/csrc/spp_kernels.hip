@@ -1466,6 +1466,31 @@ __global__ __launch_bounds__(kFfnThreads) void ffn_q4_kernel(FfnArgs a) {
   }
 }
 
+// Plain streaming read (measurement only): n16 16-byte chunks from base,
+// contiguous, each wave taking kStreamIn consecutive 1 KiB pieces (64 lanes x
+// 16 bytes) per step of a grid-stride loop, non-temporal; the words are folded
+// and stored only on a magic value.  The ceiling of reading the FFN's bytes
+// with no access pattern of its own.
+constexpr int kStreamIn = 8;
+constexpr int kStreamGrid = 2048;
+__global__ __launch_bounds__(256) void stream_probe_kernel(const u32x4* __restrict__ base, size_t n16, uint32_t* sink) {
+  const size_t lane = threadIdx.x & 63;
+  const size_t wave = (static_cast<size_t>(blockIdx.x) * 256 + threadIdx.x) >> 6;
+  const size_t nwaves = static_cast<size_t>(gridDim.x) * 4;
+  uint32_t z = 0;
+  for (size_t b0 = wave * 64 * kStreamIn; b0 < n16; b0 += nwaves * 64 * kStreamIn) {
+    u32x4 v[kStreamIn];
+#pragma unroll
+    for (int k = 0; k < kStreamIn; ++k) {
+      const size_t i = b0 + 64 * k + lane;
+      v[k] = __builtin_nontemporal_load(base + (i < n16 ? i : n16 - 1));  // past the end: re-read the last chunk
+    }
+#pragma unroll
+    for (int k = 0; k < kStreamIn; ++k) z ^= v[k].x ^ v[k].y ^ v[k].z ^ v[k].w;
+  }
+  if (z == 0x9E3779B9u) sink[threadIdx.x] = z;
+}
+
 // Read-ceiling probe of ffn_q4_kernel in sweep order (measurement only): the
 // same grid, passes, unit order and loads -- 16-byte non-temporal code loads
 // and 2-byte scale loads per row and block -- folded into one checksum per
@@ -2436,6 +2461,15 @@ hipError_t launch_read_probe(const FfnArgs& a, int grid, uint32_t* sink, hipStre
     default: SPP_PROBE(3); break;
   }
 #undef SPP_PROBE
+  return hipGetLastError();
+}
+
+hipError_t launch_stream_probe(const void* base, size_t bytes, uint32_t* sink, hipStream_t st, hipEvent_t start,
+                               hipEvent_t stop) {
+  if (!base || !sink || bytes < 16 || bytes % 16 != 0 || reinterpret_cast<uintptr_t>(base) % 16 != 0)
+    return hipErrorInvalidValue;
+  hipExtLaunchKernelGGL(stream_probe_kernel, dim3(kStreamGrid), dim3(256), 0, st, start, stop, 0u,
+                        static_cast<const u32x4*>(base), bytes / 16, sink);
   return hipGetLastError();
 }
 

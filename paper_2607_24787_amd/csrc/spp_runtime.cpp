@@ -1595,6 +1595,40 @@ spp_status spp_probe_read_ceiling(spp_ctx* c, int32_t reps, double* us_out, doub
   return SPP_OK;
 }
 
+spp_status spp_probe_stream_read(spp_ctx* c, int32_t reps, double* us_out, double* gbs_out) {
+  if (spp_status s = check_ctx(c)) return s;
+  const spp_model_desc& d = c->d;
+  if (reps < 1 || reps > 10000) return fail(SPP_EINVAL, "reps must be in [1, 10000]");
+  if (d.S < d.K) return fail(SPP_ESTATE, "the stream probe needs at least K slots per layer");
+  if (spp_status e = sync_all(c)) return e;
+  // K slots' worth of blob bytes, contiguous inside one layer's pool; the
+  // groups of K slots rotate over every layer's pool, as the read probe's slots do
+  const size_t bytes = static_cast<size_t>(d.K) * c->blob_bytes / 16 * 16;
+  const int32_t per_pool = d.S / d.K;
+  const int32_t groups = d.L * per_pool;
+  hipEvent_t e0, e1;
+  SPP_HIP(hipEventCreate(&e0));
+  SPP_HIP(hipEventCreate(&e1));
+  double total_ms = 0.0;
+  hipError_t err = hipSuccess;
+  for (int32_t it = 0; it < reps + 2 && err == hipSuccess; ++it) {
+    const int32_t g = it % groups;
+    const uint8_t* base = c->layers[g / per_pool].slots + static_cast<size_t>(g % per_pool) * d.K * c->stride;
+    err = spp::launch_stream_probe(base, bytes, reinterpret_cast<uint32_t*>(c->partial), c->compute, e0, e1);
+    if (err == hipSuccess) err = hipEventSynchronize(e1);
+    float ms = 0.f;
+    if (err == hipSuccess) err = hipEventElapsedTime(&ms, e0, e1);
+    if (it >= 2) total_ms += ms;  // the first two launches warm the code and the TLB
+  }
+  (void)hipEventDestroy(e0);
+  (void)hipEventDestroy(e1);
+  if (err != hipSuccess) return fail(SPP_EHIP, std::string("stream probe: ") + hipGetErrorString(err));
+  const double us = 1e3 * total_ms / reps;
+  if (us_out) *us_out = us;
+  if (gbs_out) *gbs_out = static_cast<double>(bytes) / (us * 1e3);
+  return SPP_OK;
+}
+
 spp_status spp_debug_set_poison(spp_ctx* c, int32_t enabled) {
   if (spp_status s = check_ctx(c)) return s;
   c->poison = enabled != 0;

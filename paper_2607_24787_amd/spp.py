@@ -98,6 +98,7 @@ _SIGS = {
                                       POINTER(c_int64)]),
     "spp_profile_expert_copy": (c_int32, [c_void_p, c_int32, c_int32, POINTER(c_double)]),
     "spp_probe_read_ceiling": (c_int32, [c_void_p, c_int32, POINTER(c_double), POINTER(c_double)]),
+    "spp_probe_stream_read": (c_int32, [c_void_p, c_int32, POINTER(c_double), POINTER(c_double)]),
     "spp_set_prefetch_source": (c_int32, [c_void_p, c_int32]),
     "spp_set_copy_engine": (c_int32, [c_void_p, c_int32]),
     "spp_set_tier_delay": (c_int32, [c_void_p, c_int32]),
@@ -379,6 +380,13 @@ def spp_probe_read_ceiling(ctx, reps: int = 40):
     """(average us per launch, GB/s) of the FFN's loads without its arithmetic."""
     us, gbs = c_double(), c_double()
     _check(lib().spp_probe_read_ceiling(c_void_p(ctx), reps, byref(us), byref(gbs)))
+    return us.value, gbs.value
+
+
+def spp_probe_stream_read(ctx, reps: int = 40):
+    """(average us per launch, GB/s) of a plain contiguous read of K expert blobs' bytes."""
+    us, gbs = c_double(), c_double()
+    _check(lib().spp_probe_stream_read(c_void_p(ctx), reps, byref(us), byref(gbs)))
     return us.value, gbs.value
 
 

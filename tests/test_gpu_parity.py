@@ -526,6 +526,10 @@ def test_read_ceiling_probe(torch_cuda, cfg):
         us, gbs = spp.spp_probe_read_ceiling(st.ctx, 4)
         assert np.isfinite(us) and us > 0
         assert gbs == pytest.approx(cfg.K * cfg.blob_bytes / (us * 1e3), rel=1e-9)
+        # the plain contiguous read of the same bytes
+        us, gbs = spp.spp_probe_stream_read(st.ctx, 4)
+        assert np.isfinite(us) and us > 0
+        assert gbs == pytest.approx(cfg.K * cfg.blob_bytes // 16 * 16 / (us * 1e3), rel=1e-9)
         topk, _, _ = st.layer(0, 0, 1, 1)
         assert topk.shape == (1, cfg.K)
     finally:
