@@ -42,6 +42,12 @@ RAGGED = w.MoEConfig(name="ragged_bf16_D640_n40_k5", L=3, D=640, n=40, K=5, I=10
 # the workgroup-wide tails
 ONE_WAVE_N40 = RAGGED.with_(name="ragged_bf16_D640_n40_k5_r16", r=16)
 ONE_WAVE_N100 = RAGGED.with_(name="ragged_bf16_D640_n100_k6_r16", n=100, K=6, r=16)
+# degenerate routing: every expert selected (a full sort, gates over all n),
+# and top-1 (gate 1)
+K_EQ_N = w.MoEConfig(name="k_eq_n_bf16_D256_n8_k8", L=2, D=256, n=8, K=8, I=64, r=8, S=8, windows=(2,), tokens=6,
+                     seed=31)
+TOP1 = w.MoEConfig(name="top1_bf16_D256_n16_k1", L=3, D=256, n=16, K=1, I=64, r=8, S=4, windows=(2,), tokens=12,
+                   seed=33)
 PROJ = w.MoEConfig(name="proj_bf16_D512_n16_k4", L=3, D=512, n=16, K=4, I=128, r=8, S=8, windows=(2,),
                    tokens=10, has_proj=True, seed=5)
 BATCH = w.MoEConfig(name="batch3_f32_D128_n12_k3", L=2, D=128, n=12, K=3, I=64, r=8, S=12, windows=(2,),
@@ -95,8 +101,10 @@ def _assert_report(rep, cfg, name):
     (MAX_F32, 4, 2),
     (w.get("c1p"), 2, 4),
     (ONE_WAVE_N100, 2, 12),
+    (K_EQ_N, 2, 6),
+    (TOP1, 2, 12),
 ], ids=["c0_M1", "c0_M3", "ragged", "proj", "batch3", "c3_short", "max_bf16", "max_f32", "qwen_calibrated",
-        "ragged_one_wave_n100"])
+        "ragged_one_wave_n100", "k_eq_n", "top1"])
 def test_lockstep_parity(torch_cuda, cfg, M_max, tokens):
     from lockstep import run_lockstep
     _log(f"[lockstep] {cfg.name} M_max={M_max} tokens={tokens}")
