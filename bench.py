@@ -361,7 +361,7 @@ def main():
         return
 
     if args.gpus != 1 or int(os.environ.get("WORLD_SIZE", "1")) != 1:
-        print(json.dumps({"error": "this build runs the offloaded-MoE hot path on one GPU only; "
+        print(json.dumps({"error": "the offloaded-MoE hot path runs on one GPU only; "
                                    "run with --gpus 1"}), flush=True)
         sys.exit(2)
 

@@ -2,7 +2,7 @@
 
 TEST INFRASTRUCTURE ONLY.  This package is a plain, slow, fp64 numpy
 restatement of what the method computes, used to check the device path.  Only
-the test suite, the graft smoke check and the benchmark's CPU-baseline leg may
+the test suite, the smoke check and the benchmark's CPU-baseline leg may
 import it; the product path (the HIP library and its Python binding) never
 does, and shares no code with it.  The only module both sides read is
 ``workload`` (seeded inputs, no arithmetic of the method).

@@ -9,7 +9,7 @@
   reaches 0.82M, at rank 64, so these figures do not pin that term; the
   array shapes test pins it.)
 * The 4-bit expert size (section "On Device Evaluation"): the packed blob of
-  the DeepSeek-VL2-Tiny shape under this build's 4-bit reading (4-bit codes,
+  the DeepSeek-VL2-Tiny shape under the codec's reading of the paper (4-bit codes,
   one fp16 scale per 32 elements) occupies the printed 1.94 MB.
 * ExpertRecall@(K/2) never exceeds the printed 50% bound.
 * The workload configurations use the printed K and expert counts.
