@@ -1002,27 +1002,6 @@ spp_status layer_forward_impl(spp_ctx* c, int32_t l, const void* h_in, void* h_o
   }
   if (c->timing) SPP_HIP(hipEventRecord(ts.ev[kEvLoaded], c->compute));
 
-  // prefetch selection for layer l+1 (the copies are enqueued after this
-  // layer's loads); the adapter's priorities have their own flag
-  if (adapter_on)
-    if (spp_status e = wait_router(c, ra.seq, 1, B)) return e;
-  LayerState* nx = predict && M_max > 0 ? &c->layers[l + 1] : nullptr;
-  c->last_pref.clear();
-  c->last_s_valid = predict;
-  c->last_B = B;
-  c->logits_valid = !(adapter_on && B > 1);  // the batched selection overwrites logits with pi_hat
-  if (adapter_on && c->timing) record_prediction(c, l, s, M_max);
-  if (predict) {
-    std::memcpy(c->last_s.data(), s, sizeof(float) * d.n);
-    if (nx) {
-      nx->policy->prefetch(s, M_max, tau, &c->last_pref);
-      nx->pending_prefetch.clear();
-      for (const spp::Transfer& t : c->last_pref) nx->pending_prefetch.push_back(t.expert);
-      st.prefetched = static_cast<int32_t>(c->last_pref.size());
-    }
-    c->stats.prefetch_hist[std::min(st.prefetched, 16)] += 1;
-  }
-
   // the batch-1 FFN's work list (routed experts in T order, then the shared ones)
   auto build_ffn = [&](int32_t b, spp::FfnArgs* fa) -> int {
     *fa = spp::FfnArgs{};
@@ -1125,6 +1104,28 @@ spp_status layer_forward_impl(spp_ctx* c, int32_t l, const void* h_in, void* h_o
     SPP_HIP(hipEventRecord(ts.ev[kEvEnd], c->compute));
     c->pending_sets.push_back(ts);
   }
+  // prefetch selection for layer l+1, after the FFN launch: the adapter's
+  // priorities have records of their own, which the batched selection writes
+  // after every token's routing, so the FFN does not wait for them
+  if (adapter_on)
+    if (spp_status e = wait_router(c, ra.seq, 1, B)) return e;
+  LayerState* nx = predict && M_max > 0 ? &c->layers[l + 1] : nullptr;
+  c->last_pref.clear();
+  c->last_s_valid = predict;
+  c->last_B = B;
+  c->logits_valid = !(adapter_on && B > 1);  // the batched selection overwrites logits with pi_hat
+  if (adapter_on && c->timing) record_prediction(c, l, s, M_max);
+  if (predict) {
+    std::memcpy(c->last_s.data(), s, sizeof(float) * d.n);
+    if (nx) {
+      nx->policy->prefetch(s, M_max, tau, &c->last_pref);
+      nx->pending_prefetch.clear();
+      for (const spp::Transfer& t : c->last_pref) nx->pending_prefetch.push_back(t.expert);
+      st.prefetched = static_cast<int32_t>(c->last_pref.size());
+    }
+    c->stats.prefetch_hist[std::min(st.prefetched, 16)] += 1;
+  }
+
   // prefetches for layer l+1, behind every on-demand load (in copy-stream
   // order, or after the completion of the copy kernels on the compute stream)
   // and after the FFN launch (the host time they take then overlaps the FFN)
