@@ -81,13 +81,15 @@ def run_mode(stack, dev_h, row_bytes, warmup, steps, M_max, naive=False):
     spp.spp_set_timing(stack.ctx, 0)
     for t in range(warmup):
         stack.decode_step_from(base + t * row_bytes, M_max)
-    # pass 1, uninstrumented: the throughput
+    # pass 1, uninstrumented: the throughput (and the host timers, which cost nothing)
     torch.cuda.synchronize()
+    spp.spp_reset_run_stats(stack.ctx)
     t0 = time.perf_counter()
     for t in range(warmup, warmup + steps):
         stack.decode_step_from(base + t * row_bytes, M_max)
     torch.cuda.synchronize()
     wall = time.perf_counter() - t0
+    rs1 = spp.spp_get_run_stats(stack.ctx)
     # pass 2, the next `steps` tokens with HIP events on: coverage, exposed share, windows, kernel times
     spp.spp_reset_run_stats(stack.ctx)
     spp.spp_set_timing(stack.ctx, 1)
@@ -122,6 +124,10 @@ def run_mode(stack, dev_h, row_bytes, warmup, steps, M_max, naive=False):
         "span_us": rs.span_us,
         "exposed_us": rs.exposed_us,
         "router_us_per_layer": rs.router_us / max(rs.layer_calls, 1),
+        # host time per layer call in the uninstrumented pass: router launch ->
+        # routing seen, routing seen -> FFN enqueued
+        "host_route_us_per_layer": rs1.host_route_us / max(rs1.layer_calls, 1),
+        "host_decide_us_per_layer": rs1.host_decide_us / max(rs1.layer_calls, 1),
         "ffn_kernel_us": _ffn_stats(rs),
         "ffn_launches": rs.ffn_launches,
         "misses_per_step": rs.misses / steps,

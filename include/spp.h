@@ -161,6 +161,13 @@ typedef struct {
    * calls that predict layer l+1, M_max >= 0, and expert_cache_issue_prefetch
    * calls) that issued m copies (m = 16 counts 16 or more) */
   int64_t prefetch_hist[17];
+  /* host time of every layer call (timing on or off): from the router
+   * launch's return to the routing records being seen (host_route_us: the
+   * host waits for the device to reach and finish the router), and from
+   * there to the FFN launch's return (host_decide_us: the statistics, slot
+   * decisions, on-demand copies and FFN enqueue on the critical path) */
+  double host_route_us;
+  double host_decide_us;
 } spp_run_stats;
 
 /* ---------------------------------------------------------------- lifecycle */

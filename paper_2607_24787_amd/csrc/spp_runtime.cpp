@@ -124,6 +124,7 @@ struct spp_ctx {
   hipEvent_t route_done = nullptr;  // compute stream, after the router launch
   hipEvent_t hits_done = nullptr;   // compute2, after the resident experts' FFN launch
   unsigned* counter = nullptr;
+  std::chrono::steady_clock::time_point t_grouped_launched{};  // the first grouped FFN launch's return
   float* partial = nullptr;    // [ffn_max_grid, D]
   uint8_t* probe_dev = nullptr;  // one blob, for copy profiling
   // batched decode (B > 1, bf16): expert groups and partial outputs
@@ -846,6 +847,7 @@ spp_status grouped_ffn(spp_ctx* c, LayerState& ls, const int32_t* T, int32_t B,
     const bool first = r == 0, last = r + 1 == rounds.size();
     SPP_HIP(spp::launch_ffn_grouped(ga, c->compute, c->timing && first ? ts.ev[kEvFfnBegin] : nullptr,
                                     c->timing && last ? ts.ev[kEvFfnEnd] : nullptr));
+    if (first) c->t_grouped_launched = std::chrono::steady_clock::now();
   }
   spp::CombineBArgs cb{};
   cb.ypart = c->ypart;
@@ -922,6 +924,7 @@ spp_status layer_forward_impl(spp_ctx* c, int32_t l, const void* h_in, void* h_o
   ra.router_on = 1;
   ra.seq = next_router_seq(c);
   SPP_HIP(spp::launch_router(ra, dt, c->compute));
+  const auto t_router = std::chrono::steady_clock::now();
   if (c->timing) SPP_HIP(hipEventRecord(ts.ev[kEvRouted], c->compute));
   const bool split_ok = c->ffn_overlap && !c->grouped && B == 1;
   if (split_ok) SPP_HIP(hipEventRecord(c->route_done, c->compute));
@@ -930,6 +933,7 @@ spp_status layer_forward_impl(spp_ctx* c, int32_t l, const void* h_in, void* h_o
     if (c->timing) c->free_sets.push_back(ts);
     return e;
   }
+  const auto t_routed = std::chrono::steady_clock::now();
 
   const int32_t* T = c->host_T.data();
   const float* g = c->host_g.data();
@@ -1079,6 +1083,7 @@ spp_status layer_forward_impl(spp_ctx* c, int32_t l, const void* h_in, void* h_o
   if (batched) {
     if (spp_status e = grouped_ffn(c, ls, T, B, h_in, h_out, rounds, c->last_loads, &st, ts)) return e;
   }
+  std::chrono::steady_clock::time_point t_ffn{};
   for (int32_t b = 0; b < B && !batched; ++b) {
     spp::FfnArgs fa{};
     const int grid = split_ok ? grid0 : build_ffn(b, &fa);
@@ -1087,6 +1092,7 @@ spp_status layer_forward_impl(spp_ctx* c, int32_t l, const void* h_in, void* h_o
     const bool stamp = c->timing && b == B - 1;
     SPP_HIP(spp::launch_ffn(fa, grid, dt, c->compute, stamp ? ts.ev[kEvFfnBegin] : nullptr,
                             stamp ? ts.ev[kEvFfnEnd] : nullptr));
+    if (b == 0) t_ffn = std::chrono::steady_clock::now();
     if (split && hipEventQuery(c->hits_done) != hipSuccess) SPP_HIP(hipStreamWaitEvent(c->compute, c->hits_done, 0));
     spp::CombineArgs ca{};
     ca.partial = c->partial;
@@ -1103,6 +1109,14 @@ spp_status layer_forward_impl(spp_ctx* c, int32_t l, const void* h_in, void* h_o
   if (c->timing) {
     SPP_HIP(hipEventRecord(ts.ev[kEvEnd], c->compute));
     c->pending_sets.push_back(ts);
+  }
+  {
+    if (batched) t_ffn = c->t_grouped_launched;
+    const auto us = [](std::chrono::steady_clock::duration dt) {
+      return std::chrono::duration<double, std::micro>(dt).count();
+    };
+    c->stats.host_route_us += us(t_routed - t_router);
+    c->stats.host_decide_us += us(t_ffn - t_routed);
   }
   // prefetch selection for layer l+1, after the FFN launch: the adapter's
   // priorities have records of their own, which the batched selection writes

@@ -51,7 +51,8 @@ class RunStats(ctypes.Structure):
                 + [("recall_tokens", c_int64), ("recall_hits", c_int64 * 3), ("pred_events", c_int64),
                    ("demand_exceeds", c_int64 * 3), ("demand_hist", (c_int64 * 17) * 3),
                    ("ffn_split_launches", c_int64), ("exposed_shared_us", c_double), ("shared_calls", c_int64),
-                   ("waited", c_int64), ("prefetch_hist", c_int64 * 17)])
+                   ("waited", c_int64), ("prefetch_hist", c_int64 * 17),
+                   ("host_route_us", c_double), ("host_decide_us", c_double)])
 
     def as_dict(self):
         out = {}
