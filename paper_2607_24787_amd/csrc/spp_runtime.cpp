@@ -764,6 +764,8 @@ spp_status grouped_ffn(spp_ctx* c, LayerState& ls, const int32_t* T, int32_t B,
                        const std::vector<spp::Transfer>& loads, spp_layer_stats* st, TimingSet& ts) {
   const spp_model_desc& d = c->d;
   const int32_t BK = B * d.K;
+  bool launched = false;  // the first grouped launch stamps c->t_grouped_launched
+  c->t_grouped_launched = std::chrono::steady_clock::now();
   // the (token, k) pairs of each expert in pair order: a stable counting sort
   // into context scratch (pair p belongs to token p / K)
   std::vector<int32_t>& start = c->grp_start;
@@ -847,7 +849,8 @@ spp_status grouped_ffn(spp_ctx* c, LayerState& ls, const int32_t* T, int32_t B,
     const bool first = r == 0, last = r + 1 == rounds.size();
     SPP_HIP(spp::launch_ffn_grouped(ga, c->compute, c->timing && first ? ts.ev[kEvFfnBegin] : nullptr,
                                     c->timing && last ? ts.ev[kEvFfnEnd] : nullptr));
-    if (first) c->t_grouped_launched = std::chrono::steady_clock::now();
+    if (!launched) c->t_grouped_launched = std::chrono::steady_clock::now();
+    launched = true;
   }
   spp::CombineBArgs cb{};
   cb.ypart = c->ypart;
