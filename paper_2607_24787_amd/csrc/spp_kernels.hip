@@ -1582,7 +1582,7 @@ __global__ __launch_bounds__(64 * kCombGroups) void ffn_combine_kernel(CombineAr
 //   down part, after the 2*I*D gate/up elements: run (s*I + i) holds
 //     W_down[256 s + c][i], c < 256 -- consecutive units of a slice are contiguous.
 // Each workgroup takes one group (up to 16 tokens routed to the same expert)
-// and one range of upw units of that expert (upw = 64, 128 or 256).
+// and one range of upw units of that expert (upw = 64, 128, 192 or 256).
 //   phase A: G = X W_gate^T and U = X W_up^T on MFMA (v_mfma_f32_16x16x32_bf16,
 //            tokens padded to the 16 rows of the tile, units as the 16
 //            columns, D as the contraction); wave w owns tiles w, w+8.  x is
@@ -2347,8 +2347,8 @@ hipError_t launch_proj(const ProjArgs& a, int dtype, hipStream_t st) {
 }
 
 hipError_t launch_ffn_grouped(const GroupArgs& a, hipStream_t st, hipEvent_t start, hipEvent_t stop) {
-  if (a.ngroups <= 0 || a.nsplit <= 0 || (a.upw != 64 && a.upw != 128 && a.upw != 256) || a.D % kGrpBlk != 0 ||
-      a.I % 16 != 0 || a.nsplit * a.upw < a.I || !a.groups || !a.x || !a.ypart)
+  if (a.ngroups <= 0 || a.nsplit <= 0 || (a.upw != 64 && a.upw != 128 && a.upw != 192 && a.upw != 256) ||
+      a.D % kGrpBlk != 0 || a.I % 16 != 0 || a.nsplit * a.upw < a.I || !a.groups || !a.x || !a.ypart)
     return hipErrorInvalidValue;
   const dim3 grid(static_cast<unsigned>(a.ngroups * a.nsplit));
   if (start || stop)

@@ -67,6 +67,9 @@ DSV2_B4 = w.get("c3").with_(L=2, batch=4, S=64, tokens=3)
 BATCH_BF16_ROUNDS = BATCH_BF16.with_(S=6)
 QWEN_B16_S32 = w.get("c4").with_(L=2, batch=16, S=32, tokens=2)
 QWEN_B64_S32 = w.get("c4").with_(L=2, tokens=2)
+# every expert resident at B = 64: about 126 groups per step, so the grouped
+# kernel takes its widest unit ranges (192 units, 4 per expert)
+QWEN_B64_S128 = w.get("c4").with_(L=2, S=128, tokens=2)
 C2_TIED = w.get("c2").with_(tokens=8, expert_layers=2)
 # the batched 48-layer stack as specified: 64 sequences, 32 slots per layer
 # (about 126 distinct experts per layer: every step runs in on-demand rounds),
@@ -136,9 +139,9 @@ def test_lockstep_parity_with_the_ffn_split(torch_cuda, cfg, M_max, tokens):
 
 @pytest.mark.parametrize("cfg,M_max,tokens", [(BATCH_BF16, 2, 6), (QWEN_B16, 4, 3), (DSV2_B4, 2, 3),
                                               (BATCH_BF16_ROUNDS, 2, 6), (QWEN_B16_S32, 4, 2),
-                                              (QWEN_B64_S32, 4, 2)],
+                                              (QWEN_B64_S32, 4, 2), (QWEN_B64_S128, 4, 2)],
                          ids=["batch5_bf16", "qwen_b16", "dsv2_b4", "batch5_rounds", "qwen_b16_s32_rounds",
-                              "qwen_b64_s32_rounds"])
+                              "qwen_b64_s32_rounds", "qwen_b64_s128"])
 def test_lockstep_parity_batched_grouped(torch_cuda, cfg, M_max, tokens):
     from lockstep import run_lockstep
     _log(f"[lockstep] {cfg.name} B={cfg.batch} M_max={M_max} tokens={tokens}")
