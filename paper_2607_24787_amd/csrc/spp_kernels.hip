@@ -1276,18 +1276,33 @@ __global__ __launch_bounds__(64 * kSlWaves) void read_probe_kernel(FfnArgs a, ui
 // is one contiguous run: [gate codes | up codes | down codes] (D/2 bytes each,
 // two codes per byte, low nibble first) then [gate | up | down scales] (D/32
 // fp16 each); value = scale * (q - 8) per block of 32 elements along D.
-// Lane l owns blocks l and l + 64 (NQ of them): 32 consecutive elements of x,
-// one 16-byte code load and one 2-byte scale load per row and block.  The -8
-// offset is folded out: a gate/up dot product is scale * (sum q x - 8 sum x)
-// with the block sums of x taken once, and the down accumulation adds
-// (h scale) q per element and subtracts 8 * sum(h scale) per block at the end.
+// Lane l owns blocks l and l + 64 (NQ of them): one 16-byte code load and one
+// 2-byte scale load per row and block.
+//   gate/up: integer dot products.  x of a block is taken in fixed point,
+//     X_k = rint(x_k 2^(18 - e)) with e the frexp exponent of the block's
+//     largest |x_k| (so |X_k| <= 2^18, |x_k - X_k 2^(e-18)| <= 2^-18 of that
+//     largest value), written in five balanced base-16 digits
+//     X_k = sum_j 16^j d_jk, d_jk in [-8, 7].  A code word XOR 0x88888888
+//     holds q - 8 as signed nibbles, so sum_k (q_k - 8) X_k =
+//     sum_j 16^j dot8(q ^ 8, d_j) with v_dot8c_i32_i4 (8 products per
+//     instruction), exact in int32 (|.| <= 2^26); the block adds
+//     scale 2^(e-18) float(that sum).  The workgroup forms the digit words
+//     once: thread t takes word t % 4 (8 elements) of block t / 4, the
+//     block's largest |x| by two quad permutes, X_k + 0x88888 by one float
+//     add (rounding to nearest even), and the digit words by a nibble
+//     transpose of byte and half-word permutes; the words pass through LDS
+//     behind the first pass's weight loads.
+//   down: the accumulation adds (h scale) q per element (q converted by
+//     v_cvt_f32_ubyte*) and subtracts 8 sum(h scale) per block at the end.
 // Work list and workgroup partials as in ffn_units_kernel.  PASSES = 0: the
 // units kernel's assignment (workgroup b on units [b*upw, (b+1)*upw), which
 // the FFN split needs); PASSES = 1 or 2: sweep order as in ffn_slices_kernel
 // -- global wave g takes units g + NW (pass UPP + p), NW = G W, so the grid
 // streams one band of consecutive units at a time (8 Qwen-shaped experts:
 // 10.0 us at 512 workgroups of one pass against 11.0 us for the best range
-// assignment, 256 workgroups of two passes).
+// assignment, 256 workgroups of two passes).  The integer gate/up products
+// took the Qwen-shaped launch from 8.5 to 8.0 us in isolation (9.5 to 9.0 us
+// behind a 512 MB read); fp32 products cost a convert and an FMA per code.
 // ---------------------------------------------------------------------------
 constexpr int kQ4TargetWgs = 256;
 
@@ -1318,45 +1333,96 @@ __device__ __forceinline__ void q4_codes(const uint4& c, float (&q)[32]) {
   }
 }
 
-template <int NQ, bool FULLQ, int UPP, int PASSES>
-__global__ __launch_bounds__(kFfnThreads) void ffn_q4_kernel(FfnArgs a) {
-  extern __shared__ float s_red[];  // [kFfnWaves][D] wave partials
-  const int tid = threadIdx.x, lane = tid & 63;
-  const int wave = __builtin_amdgcn_readfirstlane(tid >> 6);
+// The weight loads of one pass: units ub + p * ustride (p < UPP) of this wave.
+// No branch in front of the loads: a unit past the range re-reads the range's
+// last unit, a lane past the row's blocks reads block 0 (its x digits are
+// zero and its outputs are not stored).
+template <int NQ, bool FULLQ, int UPP>
+__device__ __forceinline__ void q4_pass_loads(const FfnArgs& a, int ub, int ustride, int u1, int lane,
+                                              uint4 (&cg)[UPP][NQ], uint4 (&cu)[UPP][NQ], uint4 (&cd)[UPP][NQ],
+                                              uint16_t (&sg)[UPP][NQ], uint16_t (&su)[UPP][NQ],
+                                              uint16_t (&sd)[UPP][NQ], float (&gate)[UPP]) {
   const int D = a.D, I = a.I, nblk = D / 32;
   const size_t cb = static_cast<size_t>(D) / 2, sb = static_cast<size_t>(nblk) * 2;
   const size_t unit_bytes = 3 * cb + 3 * sb;
+#pragma unroll
+  for (int p = 0; p < UPP; ++p) {
+    const int uu = ub + p * ustride;
+    const int uc = uu < u1 ? uu : u1 - 1;  // wave-uniform
+    const int d = uc / I;
+    const int i = uc - d * I;
+    const uint8_t* base = reinterpret_cast<const uint8_t*>(a.blob[d]) + static_cast<size_t>(i) * unit_bytes;
+#pragma unroll
+    for (int q = 0; q < NQ; ++q) {
+      const int blk = (FULLQ || lane + 64 * q < nblk) ? lane + 64 * q : 0;
+      const u32x4 g4 = __builtin_nontemporal_load(SPP_GLOBAL(u32x4, base + 16 * blk));
+      const u32x4 u4 = __builtin_nontemporal_load(SPP_GLOBAL(u32x4, base + cb + 16 * blk));
+      const u32x4 d4 = __builtin_nontemporal_load(SPP_GLOBAL(u32x4, base + 2 * cb + 16 * blk));
+      cg[p][q] = make_uint4(g4.x, g4.y, g4.z, g4.w);
+      cu[p][q] = make_uint4(u4.x, u4.y, u4.z, u4.w);
+      cd[p][q] = make_uint4(d4.x, d4.y, d4.z, d4.w);
+      sg[p][q] = *SPP_GLOBAL(uint16_t, base + 3 * cb + 2 * blk);
+      su[p][q] = *SPP_GLOBAL(uint16_t, base + 3 * cb + sb + 2 * blk);
+      sd[p][q] = *SPP_GLOBAL(uint16_t, base + 3 * cb + 2 * sb + 2 * blk);
+    }
+    const int gi = a.gate_idx[d];
+    gate[p] = gi >= 0 ? a.gates[gi] : 1.f;
+  }
+}
+
+// Digit words of 8 consecutive elements x_0..x_7 of a block whose largest
+// |x| has frexp exponent e: nibble k of word j is d_jk (two's complement).
+// Y_k = (X_k + 0x88888) ^ 0x88888 holds d_0k..d_4k in its five low nibbles
+// (X_k + 0x88888 = sum_j (d_jk + 8) 16^j with every digit in [0, 15]); the
+// float sum x_k 2^(18-e) + 1.5 * 2^23 rounds X_k to nearest even and leaves
+// X_k + 2^22 in the mantissa.  The transpose: half-words of Y_k and Y_k+4,
+// then bytes of those pairs, then nibbles.
+__device__ __forceinline__ void q4_x_digits(const float (&xe)[8], int e, uint32_t (&w)[5]) {
+  const float sc = ldexpf(1.f, 18 - e);
+  uint32_t Y[8];
+#pragma unroll
+  for (int k = 0; k < 8; ++k)
+    Y[k] = (__float_as_uint(fmaf(xe[k], sc, 12582912.f)) - (0x4B400000u - 0x88888u)) ^ 0x88888u;
+  uint32_t P[4], Q[4];
+#pragma unroll
+  for (int k = 0; k < 4; ++k) {
+    P[k] = __builtin_amdgcn_perm(Y[k + 4], Y[k], 0x05040100u);  // low halves: nibbles 0-3 of Y_k, Y_k+4
+    Q[k] = __builtin_amdgcn_perm(Y[k + 4], Y[k], 0x07060302u);  // high halves: nibble 4 of Y_k, Y_k+4
+  }
+  uint32_t R[2], S[2];
+#pragma unroll
+  for (int k = 0; k < 2; ++k) {
+    R[k] = __builtin_amdgcn_perm(P[k + 2], P[k], 0x06020400u);  // byte 0 of Y_k, Y_k+2, Y_k+4, Y_k+6
+    S[k] = __builtin_amdgcn_perm(P[k + 2], P[k], 0x07030501u);  // byte 1 of the same
+  }
+  w[0] = (R[0] & 0x0F0F0F0Fu) | ((R[1] & 0x0F0F0F0Fu) << 4);
+  w[1] = ((R[0] >> 4) & 0x0F0F0F0Fu) | (R[1] & 0xF0F0F0F0u);
+  w[2] = (S[0] & 0x0F0F0F0Fu) | ((S[1] & 0x0F0F0F0Fu) << 4);
+  w[3] = ((S[0] >> 4) & 0x0F0F0F0Fu) | (S[1] & 0xF0F0F0F0u);
+  w[4] = Q[0] | (Q[1] << 4) | (Q[2] << 8) | (Q[3] << 12);
+}
+
+template <int NQ, bool FULLQ, int UPP, int PASSES>
+__global__ __launch_bounds__(kFfnThreads) void ffn_q4_kernel(FfnArgs a) {
+  static_assert(kFfnThreads == 256, "the digit words take four threads per block, 64 blocks per pass");
+  extern __shared__ float s_red[];  // [kFfnWaves][D] wave partials
+  __shared__ uint4 s_dig[NQ * 64 * 5];  // [block][digit j] words 0..3
+  __shared__ float s_eb[NQ * 64];       // [block] 2^(e - 18)
+  const int tid = threadIdx.x, lane = tid & 63;
+  const int wave = __builtin_amdgcn_readfirstlane(tid >> 6);
+  const int D = a.D, I = a.I, nblk = D / 32;
   if (PASSES == 0 && ((a.skip_mask >> ((static_cast<int>(blockIdx.x) * a.upw) / I)) & 1u)) return;  // another launch's item
 
-  // lanes past the row's blocks read block 0 and keep zeros: no branch in front of the loads
-  float xv[NQ][32], xs[NQ];
+  // this thread's 8 elements of x per q: word tid % 4 of block tid / 4 + 64 q
+  // (a block past the row reads block 0; its words are never used)
+  float xe[NQ][8];
 #pragma unroll
   for (int q = 0; q < NQ; ++q) {
-    const int blk = lane + 64 * q;
-    const bool ok = FULLQ || blk < nblk;
-    float4 v[8];
-#pragma unroll
-    for (int j = 0; j < 8; ++j) {
-      const float4 t = *SPP_GLOBAL(float4, a.x + 32 * (ok ? blk : 0) + 4 * j);
-      v[j] = ok ? t : make_float4(0.f, 0.f, 0.f, 0.f);
-    }
-    xs[q] = 0.f;
-#pragma unroll
-    for (int j = 0; j < 8; ++j) {
-      xv[q][4 * j] = v[j].x;
-      xv[q][4 * j + 1] = v[j].y;
-      xv[q][4 * j + 2] = v[j].z;
-      xv[q][4 * j + 3] = v[j].w;
-      xs[q] += (v[j].x + v[j].y) + (v[j].z + v[j].w);
-    }
-  }
-  __builtin_amdgcn_sched_barrier(0);
-  float acc[NQ][32], corr[NQ];
-#pragma unroll
-  for (int q = 0; q < NQ; ++q) {
-    corr[q] = 0.f;
-#pragma unroll
-    for (int j = 0; j < 32; ++j) acc[q][j] = 0.f;
+    const int bq = (tid >> 2) + 64 * q;
+    const float* xs = a.x + 32 * (FULLQ || bq < nblk ? bq : 0) + 8 * (tid & 3);
+    const float4 v0 = *SPP_GLOBAL(float4, xs), v1 = *SPP_GLOBAL(float4, xs + 4);
+    xe[q][0] = v0.x; xe[q][1] = v0.y; xe[q][2] = v0.z; xe[q][3] = v0.w;
+    xe[q][4] = v1.x; xe[q][5] = v1.y; xe[q][6] = v1.z; xe[q][7] = v1.w;
   }
 
   const int total = a.nW * I;
@@ -1368,38 +1434,60 @@ __global__ __launch_bounds__(kFfnThreads) void ffn_q4_kernel(FfnArgs a) {
   const int ustride = PASSES ? NW : kFfnWaves;
   const int ub0 = PASSES ? static_cast<int>(blockIdx.x) * kFfnWaves + wave : u0 + wave;
   const int npass = PASSES ? PASSES : (a.upw + kFfnWaves * UPP - 1) / (kFfnWaves * UPP);
+  uint4 cg[UPP][NQ], cu[UPP][NQ], cd[UPP][NQ];
+  uint16_t sg[UPP][NQ], su[UPP][NQ], sd[UPP][NQ];
+  float gate[UPP];
+  // the first pass's weight loads go out before the digit words are formed
+  const bool first = !(PASSES == 0 && ub0 >= u1);  // wave-uniform
+  if (first) q4_pass_loads<NQ, FULLQ, UPP>(a, ub0, ustride, u1, lane, cg, cu, cd, sg, su, sd, gate);
+  __builtin_amdgcn_sched_barrier(0);
+
+  // digit words of x, one block per four threads, through LDS
+#pragma unroll
+  for (int q = 0; q < NQ; ++q) {
+    float m = 0.f;
+#pragma unroll
+    for (int k = 0; k < 8; ++k) m = fmaxf(m, fabsf(xe[q][k]));
+    m = fmaxf(m, dpp<0xB1>(m));  // quad_perm [1,0,3,2]: the block's four threads
+    m = fmaxf(m, dpp<0x4E>(m));  // quad_perm [2,3,0,1]
+    const int e = m > 0.f ? __builtin_amdgcn_frexp_expf(m) : 0;
+    uint32_t w[5];
+    q4_x_digits(xe[q], e, w);
+    const int bq = (tid >> 2) + 64 * q;
+    uint32_t* s_dw = reinterpret_cast<uint32_t*>(s_dig);
+#pragma unroll
+    for (int j = 0; j < 5; ++j) s_dw[(bq * 5 + j) * 4 + (tid & 3)] = w[j];
+    if ((tid & 3) == 0) s_eb[bq] = ldexpf(1.f, e - 18);
+  }
+  __syncthreads();
+  uint32_t xd[NQ][5][4];
+  float eb[NQ];
+#pragma unroll
+  for (int q = 0; q < NQ; ++q) {
+    const int blk = lane + 64 * q;
+    const bool ok = FULLQ || blk < nblk;
+#pragma unroll
+    for (int j = 0; j < 5; ++j) {
+      const uint4 t = s_dig[blk * 5 + j];
+      xd[q][j][0] = ok ? t.x : 0u;
+      xd[q][j][1] = ok ? t.y : 0u;
+      xd[q][j][2] = ok ? t.z : 0u;
+      xd[q][j][3] = ok ? t.w : 0u;
+    }
+    eb[q] = ok ? s_eb[blk] : 0.f;
+  }
+
+  float acc[NQ][32], corr[NQ];
+#pragma unroll
+  for (int q = 0; q < NQ; ++q) {
+    corr[q] = 0.f;
+#pragma unroll
+    for (int j = 0; j < 32; ++j) acc[q][j] = 0.f;
+  }
   for (int pr = 0; pr < npass; ++pr) {
     const int ub = ub0 + pr * UPP * ustride;
     if (PASSES == 0 && ub >= u1) break;  // wave-uniform
-    uint4 cg[UPP][NQ], cu[UPP][NQ], cd[UPP][NQ];
-    uint16_t sg[UPP][NQ], su[UPP][NQ], sd[UPP][NQ];
-    float gate[UPP];
-    // no branch in front of the loads: a unit past the range re-reads the
-    // range's last unit, a lane past the row's blocks reads block 0 (its x is
-    // zero and its outputs are not stored)
-#pragma unroll
-    for (int p = 0; p < UPP; ++p) {
-      const int uu = ub + p * ustride;
-      const int uc = uu < u1 ? uu : u1 - 1;  // wave-uniform
-      const int d = uc / I;
-      const int i = uc - d * I;
-      const uint8_t* base = reinterpret_cast<const uint8_t*>(a.blob[d]) + static_cast<size_t>(i) * unit_bytes;
-#pragma unroll
-      for (int q = 0; q < NQ; ++q) {
-        const int blk = (FULLQ || lane + 64 * q < nblk) ? lane + 64 * q : 0;
-        const u32x4 g4 = __builtin_nontemporal_load(SPP_GLOBAL(u32x4, base + 16 * blk));
-        const u32x4 u4 = __builtin_nontemporal_load(SPP_GLOBAL(u32x4, base + cb + 16 * blk));
-        const u32x4 d4 = __builtin_nontemporal_load(SPP_GLOBAL(u32x4, base + 2 * cb + 16 * blk));
-        cg[p][q] = make_uint4(g4.x, g4.y, g4.z, g4.w);
-        cu[p][q] = make_uint4(u4.x, u4.y, u4.z, u4.w);
-        cd[p][q] = make_uint4(d4.x, d4.y, d4.z, d4.w);
-        sg[p][q] = *SPP_GLOBAL(uint16_t, base + 3 * cb + 2 * blk);
-        su[p][q] = *SPP_GLOBAL(uint16_t, base + 3 * cb + sb + 2 * blk);
-        sd[p][q] = *SPP_GLOBAL(uint16_t, base + 3 * cb + 2 * sb + 2 * blk);
-      }
-      const int gi = a.gate_idx[d];
-      gate[p] = gi >= 0 ? a.gates[gi] : 1.f;
-    }
+    if (pr > 0) q4_pass_loads<NQ, FULLQ, UPP>(a, ub, ustride, u1, lane, cg, cu, cd, sg, su, sd, gate);
     __builtin_amdgcn_sched_barrier(0);
 #pragma unroll
     for (int p = 0; p < UPP; ++p) {
@@ -1407,18 +1495,22 @@ __global__ __launch_bounds__(kFfnThreads) void ffn_q4_kernel(FfnArgs a) {
       float gs = 0.f, us = 0.f;
 #pragma unroll
       for (int q = 0; q < NQ; ++q) {
-        float qg[32], qu[32];
-        q4_codes(cg[p][q], qg);
-        q4_codes(cu[p][q], qu);
-        // four independent partial sums per row: short dependence chains
-        float dg[4] = {0.f, 0.f, 0.f, 0.f}, du[4] = {0.f, 0.f, 0.f, 0.f};
+        const uint32_t wg[4] = {cg[p][q].x, cg[p][q].y, cg[p][q].z, cg[p][q].w};
+        const uint32_t wu[4] = {cu[p][q].x, cu[p][q].y, cu[p][q].z, cu[p][q].w};
+        int tg[5] = {0, 0, 0, 0, 0}, tu[5] = {0, 0, 0, 0, 0};
 #pragma unroll
-        for (int j = 0; j < 32; ++j) {
-          dg[j & 3] += qg[j] * xv[q][j];
-          du[j & 3] += qu[j] * xv[q][j];
+        for (int m = 0; m < 4; ++m) {
+          const int qg = static_cast<int>(wg[m] ^ 0x88888888u), qu = static_cast<int>(wu[m] ^ 0x88888888u);
+#pragma unroll
+          for (int j = 0; j < 5; ++j) {
+            tg[j] = __builtin_amdgcn_sdot8(qg, static_cast<int>(xd[q][j][m]), tg[j], false);
+            tu[j] = __builtin_amdgcn_sdot8(qu, static_cast<int>(xd[q][j][m]), tu[j], false);
+          }
         }
-        gs += q4_scale(sg[p][q]) * (((dg[0] + dg[1]) + (dg[2] + dg[3])) - 8.f * xs[q]);
-        us += q4_scale(su[p][q]) * (((du[0] + du[1]) + (du[2] + du[3])) - 8.f * xs[q]);
+        const int Tg = (((tg[4] * 16 + tg[3]) * 16 + tg[2]) * 16 + tg[1]) * 16 + tg[0];
+        const int Tu = (((tu[4] * 16 + tu[3]) * 16 + tu[2]) * 16 + tu[1]) * 16 + tu[0];
+        gs += q4_scale(sg[p][q]) * eb[q] * static_cast<float>(Tg);
+        us += q4_scale(su[p][q]) * eb[q] * static_cast<float>(Tu);
       }
       const float g = wave_sum(gs);
       const float u = wave_sum(us);
