@@ -57,17 +57,19 @@ def _prefetch_gap(s: np.ndarray, occupied: np.ndarray, M: int) -> float:
 
 
 def run_lockstep(stack, cfg, tokens: int, M_max: int, check_x: bool = True,
-                 policy: str = "adapter", adapter_override=None, progress=None) -> LockstepReport:
+                 policy: str = "adapter", adapter_override=None, progress=None, h0=None) -> LockstepReport:
     """policy "naive": Naive Prefetch on both sides (the device via
     spp_set_prefetch_source); the oracle gets each layer's routing of the
     preceding step.  adapter_override(l) -> (A, B): the adapter values the
     oracle uses (those the stack was bound with, as stored).  progress(t, l):
-    called after each compared layer."""
+    called after each compared layer.  h0: layer-0 hidden states [tokens,
+    batch, D] in storage form (default: the workload's AR(1) states)."""
     from paper_2607_24787_amd import spp
 
     W = o.OracleWeights(cfg, cache_experts=cfg.host_layers * cfg.n + 8, adapter_override=adapter_override)
     W.warm()
-    h0 = gen.hidden_states(cfg, tokens=tokens)
+    if h0 is None:
+        h0 = gen.hidden_states(cfg, tokens=tokens)
     S = stack.S
     res = list(range(min(S, cfg.n)))
     caches = [o.SlotCache(S, cfg.n, res) for _ in range(cfg.L)]

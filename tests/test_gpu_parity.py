@@ -177,6 +177,39 @@ def test_lockstep_parity_q4_experts(torch_cuda, cfg, M_max, tokens):
     _assert_report(rep, cfg, cfg.name)
 
 
+def _q4_edge_states(cfg, tokens):
+    """AR(1) layer-0 states reshaped to stress the 4-bit kernel's block fixed
+    point for x (per 32-element block, against the block's largest |x|): every
+    token gets an all-zero block, a block at 2^-20 of its scale, and a block of
+    small values (10^-2) around one spike (10x): quantisation steps there are
+    set by the spike."""
+    h = o.decode(gen.hidden_states(cfg, tokens=tokens), cfg.dtype).astype(np.float32)
+    nblk = cfg.D // 32
+    for t in range(tokens):
+        for b in range(cfg.batch):
+            z, tiny, sp = (t % nblk), (t + 2) % nblk, (t + 5) % nblk
+            h[t, b, 32 * z:32 * z + 32] = 0.0
+            h[t, b, 32 * tiny:32 * tiny + 32] *= np.float32(2.0 ** -20)
+            h[t, b, 32 * sp:32 * sp + 32] *= np.float32(1e-2)
+            h[t, b, 32 * sp + (7 * t) % 32] = np.float32(10.0) * np.float32(np.sign(h[t, b, 32 * sp + (7 * t) % 32]) or 1.0)
+    return gen.f32_to_bf16_bits(h)
+
+
+@pytest.mark.parametrize("cfg,M_max,tokens", [(Q4_SMALL, 2, 8), (Q4_WIDE, 1, 6)], ids=["q4_small", "q4_wide"])
+def test_lockstep_parity_q4_fixed_point_edges(torch_cuda, cfg, M_max, tokens):
+    """The 4-bit gate/up products on hidden states with zero, tiny and spiked
+    blocks: routing bit-exact and outputs within one storage ulp, as on the
+    AR(1) states."""
+    from lockstep import run_lockstep
+    _log(f"[lockstep q4 edges] {cfg.name} M_max={M_max} tokens={tokens}")
+    st = _stack(cfg)
+    try:
+        rep = run_lockstep(st, cfg, tokens, M_max, h0=_q4_edge_states(cfg, tokens))
+    finally:
+        st.close()
+    _assert_report(rep, cfg, cfg.name + " edges")
+
+
 @pytest.mark.parametrize("cfg,M_max,tokens,must_issue", [(BATCH_BF16_ROUNDS, 3, 6, True),
                                                          (w.get("c0"), 2, 12, False)],
                          ids=["batch5_rounds", "c0"])
