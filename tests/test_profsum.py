@@ -67,3 +67,40 @@ def test_the_bench_takes_the_traffic_only_while_the_kernel_source_is_unchanged(t
     src.write_text("// kernel source stand-in, changed\n")
     assert bench.measured_traffic(str(prof), str(src)) is None
     assert bench.measured_traffic(str(tmp_path / "missing.md"), str(src)) is None
+
+
+def _trace(d, kernels, copies):
+    os.makedirs(d, exist_ok=True)
+    with open(os.path.join(d, "run_kernel_trace.csv"), "w", newline="") as f:
+        w = csv.DictWriter(f, fieldnames=["Kernel_Name", "Start_Timestamp", "End_Timestamp"])
+        w.writeheader()
+        for name, s, e in kernels:
+            w.writerow({"Kernel_Name": name, "Start_Timestamp": s, "End_Timestamp": e})
+    with open(os.path.join(d, "run_memory_copy_trace.csv"), "w", newline="") as f:
+        w = csv.DictWriter(f, fieldnames=["Direction", "Start_Timestamp", "End_Timestamp"])
+        w.writeheader()
+        for s, e in copies:
+            w.writerow({"Direction": "MEMORY_COPY_HOST_TO_DEVICE", "Start_Timestamp": s, "End_Timestamp": e})
+
+
+def test_overlap_splits_launches_by_a_concurrent_host_copy(tmp_path):
+    # two FFN launches overlap the copy [1000, 5000] ns, one does not; medians 3.0 / 2.0 us
+    _trace(tmp_path, [(KERNEL, 0, 2000), (KERNEL, 4000, 8000), (KERNEL, 10000, 12000)], [(1000, 5000)])
+    text = profsum.overlap(str(tmp_path), ["ffn_slices_kernel"])
+    assert "| `ffn_slices_kernel` | 2 | 3.00 | 1 | 2.00 |" in text
+
+
+def test_copies_rates_and_link_sharing(tmp_path):
+    blob = 9_437_184
+    # an FFN launch marks the decode's start; two prefetches after it, 170 us alone and
+    # 340 us half of which shares the link with an on-demand copy kernel
+    ks = [(KERNEL, 1_000, 2_000), ("h2d_copy_kernel", 300_000, 470_000)]
+    cps = [(-200_000, -30_000), (3_000, 173_000), (300_000, 640_000)]
+    _trace(tmp_path, ks, cps)
+    text = profsum.copies(str(tmp_path), blob)
+    assert "3 host-to-device (1 before the decode" in text and "2 during the decode" in text
+    assert f"median 170.0 µs per copy -> {blob / 170_000:.2f} GB/s" in text
+    assert f"<5% shared): 1, median {blob / 170_000:.2f} GB/s" in text
+    assert f"at least half their time: 1, median {blob / 340_000:.2f} GB/s" in text
+    assert "mean 0.250" in text  # (0 + 0.5) / 2 of each prefetch's time shared
+    assert "80.1% of the decode span (510 of 637 µs)" in text
