@@ -50,7 +50,10 @@
  *    each code run D/2 bytes (byte j: element 2j in the low nibble, 2j+1 in
  *    the high nibble; the down run holds column i of W_down, element d =
  *    W_down[d][i]), each scale run D/32 fp16 values (scale b covers elements
- *    32b..32b+31 of the run).
+ *    32b..32b+31 of the run).  The device FFN forms the gate/up products of
+ *    these experts exactly in integers, with x of each 32-element block in
+ *    fixed point against the block's largest |x| (19 significant bits: an
+ *    error of at most 2^-18 of that element), and the down products in fp32.
  * Blobs are placed at a stride of spp_blob_stride(desc) bytes (the blob size
  * rounded up to 4096); the padding is zero.
  */
